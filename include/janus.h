@@ -1,0 +1,291 @@
+/*
+ * janus.h - C ABI of the MI355X (gfx950) training-step library.
+ *
+ * The library runs one whole training step (forward and backward) of a
+ * dynamic-control-flow model on the GPU: an LSTM driven by a loop whose trip
+ * count depends on the data (per-sequence lengths), and a binary TreeLSTM
+ * driven by recursion over trees, evaluated level by level.  These are the
+ * loops and recursive calls of the paper's imperative programs (Figure 1;
+ * Section 4.2.1, dynamic control flow), executed as one device program per
+ * call instead of per-operation dispatch.
+ *
+ * Conventions shared by every entry point
+ * ---------------------------------------
+ *  - Tensors are caller-owned DEVICE pointers, dense, row-major, with the
+ *    shapes given below.  "dtype" tensors hold float32 or bf16 (raw 16-bit
+ *    patterns) as selected by the descriptor; float* tensors are always
+ *    float32.  Gradients are float32 and are OVERWRITTEN, never accumulated.
+ *  - Arrays documented as "host" are read during the call only.
+ *  - Each call enqueues its kernels on `stream` (a hipStream_t, 0 = the null
+ *    stream) and returns without synchronising; device faults surface at the
+ *    caller's next synchronisation.  Calls are re-entrant given distinct
+ *    workspaces.
+ *  - Workspaces are caller-allocated device memory of at least the size
+ *    returned by the matching *_workspace_bytes function, 256-byte aligned.
+ *    The forward call stores the values its backward needs there; the
+ *    workspace must not be modified between a forward call and its backward.
+ *    The library allocates no device memory.
+ *  - All validation happens before the first device operation.  When a call
+ *    returns anything other than JANUS_OK before launching, no output buffer
+ *    has been written (all-or-nothing state updates, Section 3.2 and
+ *    Section 4.2.3).  JANUS_ERR_DEVICE means a HIP call failed after work was
+ *    enqueued; outputs are then undefined.
+ */
+#ifndef JANUS_H
+#define JANUS_H
+
+#include <stddef.h>
+#include <stdint.h>
+
+#ifdef __cplusplus
+extern "C" {
+#endif
+
+typedef enum {
+    JANUS_OK = 0,
+    JANUS_ERR_INVALID_ARG = 1,   /* NULL required pointer, non-positive size   */
+    JANUS_ERR_LENGTH = 2,        /* sequence length outside [0, T]             */
+    JANUS_ERR_TREE = 3,          /* malformed tree batch                       */
+    JANUS_ERR_TOKEN = 4,         /* token / word / class id outside [0, V)     */
+    JANUS_ERR_WORKSPACE = 5,     /* workspace missing, too small or misaligned */
+    JANUS_ERR_UNSUPPORTED = 6,   /* dtype or shape combination not built       */
+    JANUS_ERR_DEVICE = 7         /* a HIP call failed                          */
+} janus_status;
+
+typedef enum { JANUS_F32 = 0, JANUS_BF16 = 1 } janus_dtype;
+
+/* ------------------------------------------------------------------------ */
+/* LSTM over variable-length sequences                                      */
+/* ------------------------------------------------------------------------ */
+
+/* L stacked layers, input size I, hidden size H, batch B, T time steps. */
+typedef struct {
+    int32_t L, I, H, B, T;
+    janus_dtype dtype;
+} janus_lstm_desc;
+
+/* Bytes of workspace needed by janus_lstm_seq_fwd / _bwd for this shape. */
+size_t janus_lstm_workspace_bytes(const janus_lstm_desc* d);
+
+/*
+ * Forward pass of the recurrence of Figure 1 (``state = rnn_cell(state,
+ * item)`` for every item), with the standard LSTM cell of the LSTM / LM
+ * models of Section 6.1:
+ *     a = Wx x_t + Wh h_{t-1} + b   (gate blocks i, f, g, o)
+ *     c_t = s(a_f) c_{t-1} + s(a_i) tanh(a_g),   h_t = s(a_o) tanh(c_t)
+ * Sequence b advances while t < lengths[b] (a loop with a data-dependent
+ * trip count, Section 4.2.1); afterwards its state is carried unchanged and
+ * its output is 0.  Layer l+1 reads the output of layer l.
+ *
+ *  x        [T, B, I] dtype, time-major.
+ *  lengths  host int32 [B] with 0 <= len <= T, or NULL for all T.
+ *  Wx[l]    [4H, I_l] dtype (I_0 = I, I_l = H above), Wh[l] [4H, H] dtype,
+ *  b[l]     [4H] dtype: host arrays of L device pointers, the per-layer
+ *           layout of torch.nn.LSTM weight_ih_l{k} / weight_hh_l{k} with one
+ *           bias.
+ *  h0, c0   [L, B, H] float32 or NULL (zeros).
+ *  y        [T, B, H] dtype: top-layer output; 0 where t >= len_b.
+ *  hT, cT   [L, B, H] float32 or NULL: state after len_b steps (= h0, c0 for
+ *           a length-0 sequence).
+ *  ws       workspace (see conventions); the forward keeps activations there.
+ *
+ * Errors: NULL d/x/Wx/Wh/b/y/ws or a non-positive L, I, H, B, or T < 0
+ * -> INVALID_ARG; a length outside [0, T] -> LENGTH; ws_bytes too small ->
+ * WORKSPACE; dtype not F32/BF16 -> UNSUPPORTED.
+ */
+janus_status janus_lstm_seq_fwd(const janus_lstm_desc* d, const void* x,
+                                const int32_t* lengths,
+                                const void* const* Wx, const void* const* Wh,
+                                const void* const* b,
+                                const float* h0, const float* c0,
+                                void* y, float* hT, float* cT,
+                                void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward pass through time of the call above (same d, x, lengths, Wx,
+ * Wh and the workspace it filled).
+ *
+ *  dy       [T, B, H] dtype gradient of y, or NULL (zero).  Entries where
+ *           t >= len_b are ignored (y is the constant 0 there).
+ *  dhT, dcT [L, B, H] float32 or NULL (zero).
+ *  dx       [T, B, I] dtype gradient of x, or NULL to skip it; 0 where
+ *           t >= len_b.
+ *  dh0, dc0 [L, B, H] float32 or NULL.
+ *  dWx[l], dWh[l], db[l]: host arrays of L device float32 pointers with the
+ *           shapes of Wx[l], Wh[l], b[l].
+ * Errors as for the forward call; additionally NULL dWx/dWh/db.
+ */
+janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void* x,
+                                const int32_t* lengths,
+                                const void* const* Wx, const void* const* Wh,
+                                void* ws, size_t ws_bytes,
+                                const void* dy, const float* dhT, const float* dcT,
+                                void* dx, float* dh0, float* dc0,
+                                float* const* dWx, float* const* dWh, float* const* db,
+                                void* stream);
+
+/*
+ * Integer schedule of the sequence loop (host only, no device use):
+ *  perm[B]       batch indices sorted by (-len_b, b)
+ *  active[T]     active[t] = #{b : len_b > t} for t < t_eff, 0 after
+ *  offsets[T+1]  offsets[t] = sum of active[t'] for t' < t
+ *  t_eff         max len (the loop's trip count)
+ * Errors: INVALID_ARG for NULL pointers or B <= 0, T < 0; LENGTH.
+ */
+janus_status janus_lstm_schedule(int32_t B, int32_t T, const int32_t* lengths,
+                                 int32_t* perm, int32_t* active, int32_t* offsets,
+                                 int32_t* t_eff);
+
+/* ------------------------------------------------------------------------ */
+/* Binary TreeLSTM over a batch of trees                                    */
+/* ------------------------------------------------------------------------ */
+
+/* Embedding size E, hidden size H, vocabulary V. */
+typedef struct {
+    int32_t E, H, V;
+    janus_dtype dtype;
+} janus_treelstm_desc;
+
+/*
+ * A batch of binary trees as HOST int32 arrays of num_nodes entries:
+ * left[n], right[n] are child node ids, both -1 for a leaf; word[n] is the
+ * token id of a leaf (in [0, V)) and -1 for an internal node.  root[k]
+ * (num_trees entries) is the root of tree k.  Every node has at most one
+ * parent and is reachable from exactly one root.  Node order is arbitrary.
+ */
+typedef struct {
+    int32_t num_trees, num_nodes;
+    const int32_t* left;
+    const int32_t* right;
+    const int32_t* word;
+    const int32_t* root;
+} janus_tree_batch;
+
+/* Workspace bytes for a batch of at most max_nodes nodes and max_trees trees. */
+size_t janus_treelstm_workspace_bytes(const janus_treelstm_desc* d, int32_t max_nodes,
+                                      int32_t max_trees);
+
+/*
+ * Frontier schedule of the recursion (host only): level(leaf) = 0,
+ * level(n) = 1 + max(level(left), level(right)); level_nodes lists node
+ * ids sorted by (level, id); level_offsets[k] = #{n : level(n) < k}.
+ *  node_level[num_nodes], level_offsets[num_nodes + 1], level_nodes[num_nodes].
+ * Errors: INVALID_ARG (NULL, empty batch), TREE (one child, two parents,
+ * bad id, cycle, unreachable node, internal node with a word), TOKEN (leaf
+ * word outside [0, V)).
+ */
+janus_status janus_tree_schedule_build(const janus_tree_batch* t, int32_t V,
+                                       int32_t* node_level, int32_t* level_offsets,
+                                       int32_t* level_nodes, int32_t* num_levels);
+
+/*
+ * Forward pass of the recursive TreeNN program (Section 6.1, footnote 6;
+ * recursion as graph invocations, Section 4.2.1), evaluated one level of
+ * independent nodes at a time.  Cell of node n (binary TreeLSTM of the SST
+ * model, Table 2):
+ *     a = b + (leaf ? W emb[word[n]] : U [h_L; h_R])
+ *     gate blocks (i, f_L, f_R, o, u); c = s(i) tanh(u) + s(f_L) c_L + s(f_R) c_R
+ *     h = s(o) tanh(c); leaves have zero children.
+ *  emb [V, E], W [5H, E], U [5H, 2H], b [5H]: dtype.
+ *  h_root [num_trees, H] dtype: h of root[k].
+ * Errors: INVALID_ARG, TREE, TOKEN, WORKSPACE, UNSUPPORTED (only F32).
+ */
+janus_status janus_treelstm_fwd(const janus_treelstm_desc* d, const janus_tree_batch* t,
+                                const void* emb, const void* W, const void* U,
+                                const void* b, void* h_root,
+                                void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward of the call above (same d, t, emb, W, U and workspace).
+ *  dh_root [num_trees, H] dtype: gradient of h_root (gradient of the roots'
+ *          c is zero).
+ *  demb [V, E], dW [5H, E], dU [5H, 2H], db [5H]: float32, overwritten
+ *          (rows of demb for words not in the batch are 0).
+ */
+janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const janus_tree_batch* t,
+                                const void* emb, const void* W, const void* U,
+                                void* ws, size_t ws_bytes, const void* dh_root,
+                                float* demb, float* dW, float* dU, float* db,
+                                void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Embedding and softmax cross-entropy                                      */
+/* ------------------------------------------------------------------------ */
+
+typedef enum {
+    JANUS_EMBED_FWD = 0,     /* out[r, :] = table[ids[r], :]                         */
+    JANUS_XENT_FWD_BWD = 1,  /* mean cross-entropy of h table^T + bias, all grads   */
+    JANUS_EMBED_BWD = 2      /* dtable[v, :] = sum of in[r, :] over ids[r] == v     */
+} janus_xent_op;
+
+/* Vocabulary (or class count) V, row width H, number of rows. */
+typedef struct {
+    int32_t V, H, rows;
+    janus_dtype dtype;
+} janus_xent_desc;
+
+size_t janus_xent_workspace_bytes(const janus_xent_desc* d, janus_xent_op op);
+
+/*
+ * One of three operations around the LSTM language model and the tree root
+ * classifier (the loss computed at the end of the Figure 1 program):
+ *  ids_host [rows] host int32 and ids_dev [rows] device int32: the same
+ *           ids (token ids for EMBED_*, target classes for XENT).
+ *  EMBED_FWD:  table = E [V, H] dtype; out = x [rows, H] dtype.
+ *  XENT_FWD_BWD: table = Wout [V, H], bias = bout [V], in = h [rows, H]
+ *           (dtype); loss (device float32 scalar) = mean over rows of
+ *           -log softmax(h Wout^T + bout)[ids[r]]; out = dh [rows, H] dtype;
+ *           dtable = dWout [V, H], dbias = dbout [V] float32.
+ *  EMBED_BWD:  in = dx [rows, H] dtype; dtable = dE [V, H] float32
+ *           (deterministic: each row of dE sums its rows in ascending r).
+ * Errors: INVALID_ARG, TOKEN (an id outside [0, V)), WORKSPACE.
+ */
+janus_status janus_embed_softmax_xent(const janus_xent_desc* d, janus_xent_op op,
+                                      const int32_t* ids_host, const int32_t* ids_dev,
+                                      const void* table, const void* bias,
+                                      const void* in, void* out,
+                                      float* dtable, float* dbias, float* loss,
+                                      void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Regression head and scalar losses                                        */
+/* ------------------------------------------------------------------------ */
+
+typedef struct {
+    int32_t rows, H, P;
+    janus_dtype dtype;
+} janus_mse_desc;
+
+size_t janus_mse_workspace_bytes(const janus_mse_desc* d);
+
+/*
+ * Per-row linear projection and mean-squared error:
+ *   yp = h W^T + b,  loss = mean over rows*P of (yp - target)^2
+ *  h [rows, H], W [P, H], b [P], target [rows, P]: dtype.
+ *  dh [rows, H] dtype; dW [P, H], db [P] float32; loss device float32.
+ */
+janus_status janus_linear_mse(const janus_mse_desc* d, const void* h, const void* W,
+                              const void* b, const void* target, void* dh,
+                              float* dW, float* db, float* loss,
+                              void* ws, size_t ws_bytes, void* stream);
+
+typedef enum {
+    JANUS_LOSS_SUMSQ = 0,    /* loss = sum h^2,   dh = 2 h   */
+    JANUS_LOSS_MEAN = 1      /* loss = mean h,    dh = 1 / n */
+} janus_loss_kind;
+
+/* h [n] float32 device; loss device float32 scalar; dh [n] float32 or NULL. */
+janus_status janus_loss_reduce(janus_loss_kind kind, const float* h, int64_t n,
+                               float* loss, float* dh, void* stream);
+
+/* ------------------------------------------------------------------------ */
+/* Misc                                                                     */
+/* ------------------------------------------------------------------------ */
+const char* janus_status_string(janus_status s);
+const char* janus_version(void);
+
+#ifdef __cplusplus
+}
+#endif
+
+#endif /* JANUS_H */

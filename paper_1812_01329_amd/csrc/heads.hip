@@ -1,0 +1,454 @@
+// Embedding lookup and its gradient, softmax cross-entropy, the projection +
+// mean-squared-error head, and scalar losses: the inputs and the
+// ``compute_loss(outputs)`` of the training programs (Figure 1).
+//
+// Reductions are deterministic: every sum is taken in a fixed order (wave
+// shuffles in a fixed butterfly, then a fixed sequence of partials), so two
+// runs on the same inputs give identical bits.
+#include "device.hpp"
+#include "ops.hpp"
+
+namespace janus {
+
+namespace {
+
+__device__ __forceinline__ float wave_sum(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v += __shfl_xor(v, off, 64);
+    return v;
+}
+__device__ __forceinline__ float wave_max(float v) {
+#pragma unroll
+    for (int off = 32; off > 0; off >>= 1) v = fmaxf(v, __shfl_xor(v, off, 64));
+    return v;
+}
+
+// block-wide sum (blockDim.x a multiple of 64, at most 1024); result in all threads
+__device__ float block_sum(float v, float* red) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    v = wave_sum(v);
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    float s = 0.f;
+    for (int i = 0; i < nw; ++i) s += red[i];
+    return s;
+}
+__device__ float block_max(float v, float* red) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6, nw = blockDim.x >> 6;
+    v = wave_max(v);
+    __syncthreads();
+    if (lane == 0) red[wave] = v;
+    __syncthreads();
+    float m = red[0];
+    for (int i = 1; i < nw; ++i) m = fmaxf(m, red[i]);
+    return m;
+}
+
+// --------------------------------------------------------------- embedding
+template <typename T, bool VEC>
+__global__ void embed_fwd_kernel(const T* E, const int32_t* ids, int V, int H, T* out) {
+    const int r = blockIdx.x;
+    // ids were range-checked on the host; the clamp only keeps a mismatched
+    // device copy from reading outside the table
+    const int64_t id = min(max(ids[r], 0), V - 1);
+    const T* src = E + id * H;
+    T* dst = out + int64_t(r) * H;
+    if (VEC) {
+        constexpr int V = 16 / sizeof(T);
+        for (int j = threadIdx.x; j < H / V; j += blockDim.x)
+            reinterpret_cast<uint4*>(dst)[j] = reinterpret_cast<const uint4*>(src)[j];
+    } else {
+        for (int j = threadIdx.x; j < H; j += blockDim.x) dst[j] = src[j];
+    }
+}
+
+// dE[v] = sum of dx[r] over rows with ids[r] == v, summed in ascending r by
+// the block that owns the first occurrence of v (no atomics).
+template <typename T>
+__global__ void embed_bwd_kernel(const T* dx, const int32_t* ids, int rows, int V, int H, float* dE) {
+    extern __shared__ int32_t match[];
+    __shared__ int nmatch;
+    __shared__ int owner;
+    const int r = blockIdx.x;
+    const int32_t id = min(max(ids[r], 0), V - 1);
+    if (threadIdx.x == 0) owner = 1;
+    __syncthreads();
+    for (int q = threadIdx.x; q < r; q += blockDim.x)
+        if (ids[q] == id) owner = 0;
+    __syncthreads();
+    if (!owner) return;
+    if (threadIdx.x == 0) {
+        int n = 0;
+        for (int q = r; q < rows; ++q)
+            if (min(max(ids[q], 0), V - 1) == id) match[n++] = q;
+        nmatch = n;
+    }
+    __syncthreads();
+    const int n = nmatch;
+    for (int j = threadIdx.x; j < H; j += blockDim.x) {
+        float s = 0.f;
+        for (int k = 0; k < n; ++k) s += to_f(dx[int64_t(match[k]) * H + j]);
+        dE[int64_t(id) * H + j] = s;
+    }
+}
+
+// --------------------------------------------------------------- softmax xent
+// per row: loss_r = logsumexp(z) - z[target]; dz = (softmax(z) - onehot) / rows
+template <typename T>
+__global__ __launch_bounds__(256) void xent_row_kernel(const float* logits, int64_t ld, const int32_t* tgt, int V,
+                                                       int rows, T* dz, int64_t ldz, float* loss_rows) {
+    __shared__ float red[16];
+    const int r = blockIdx.x;
+    const float* z = logits + int64_t(r) * ld;
+    float m = -INFINITY;
+    for (int v = threadIdx.x; v < V; v += blockDim.x) m = fmaxf(m, z[v]);
+    m = block_max(m, red);
+    float s = 0.f;
+    for (int v = threadIdx.x; v < V; v += blockDim.x) s += __expf(z[v] - m);
+    s = block_sum(s, red);
+    const float lse = m + __logf(s);
+    const int t = min(max(tgt[r], 0), V - 1);
+    const float inv = 1.f / float(rows);
+    for (int v = threadIdx.x; v < V; v += blockDim.x) {
+        const float p = __expf(z[v] - m) / s;
+        dz[int64_t(r) * ldz + v] = from_f<T>((p - (v == t ? 1.f : 0.f)) * inv);
+    }
+    if (threadIdx.x == 0) loss_rows[r] = lse - z[t];
+}
+
+// loss = scale * sum of n partials, in index order by one block
+__global__ __launch_bounds__(1024) void finish_sum_kernel(const float* part, int64_t n, float scale, float* loss) {
+    __shared__ float red[16];
+    float s = 0.f;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) s += part[i];
+    s = block_sum(s, red);
+    if (threadIdx.x == 0) *loss = s * scale;
+}
+
+// --------------------------------------------------------------- MSE head
+// yp = h W^T + b for a tile, then d = yp - target; writes dY = 2 d / count
+// (dtype) and one partial sum of d^2 per workgroup.
+template <typename T, class Cfg, bool AL>
+__global__ __launch_bounds__(Cfg::NT) void mse_gemm_kernel(int M, int N, int K, const T* h, const T* W, const T* b,
+                                                           const T* tgt, T* dY, float scale, float* part) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    __shared__ float red[16];
+    T* sA = reinterpret_cast<T*>(smem_raw);
+    T* sB = sA + Cfg::BM * Cfg::LD;
+    const int tid = threadIdx.x;
+    const int n0 = blockIdx.x * Cfg::BN, m0 = blockIdx.y * Cfg::BM;
+    LoaderK<T, Cfg::BM, Cfg::BK, Cfg::NT, AL> la;
+    LoaderK<T, Cfg::BN, Cfg::BK, Cfg::NT, AL> lb;
+    la.init(h + int64_t(m0) * K, K, 0, RowsContig{M - m0}, tid);
+    lb.init(W + int64_t(n0) * K, K, 0, RowsContig{N - n0}, tid);
+    f32x16_t acc[Cfg::FM][Cfg::FN];
+    mma_mainloop<Cfg>(acc, la, lb, K, sA, sB, tid);
+    const int lane = tid & 63, wave = tid >> 6;
+    float sq = 0.f;
+#pragma unroll
+    for (int j = 0; j < Cfg::FN; ++j) {
+        const int col = n0 + Cfg::wave_col0(wave) + j * 32 + acc_col(lane);
+        if (col >= N) continue;
+        const float bv = to_f(b[col]);
+#pragma unroll
+        for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) {
+                const int row = m0 + Cfg::wave_row0(wave) + i * 32 + acc_row(v, lane);
+                if (row >= M) continue;
+                const int64_t o = int64_t(row) * N + col;
+                const float d = acc[i][j][v] + bv - to_f(tgt[o]);
+                sq += d * d;
+                dY[o] = from_f<T>(scale * d);
+            }
+    }
+    sq = block_sum(sq, red);
+    if (tid == 0) part[blockIdx.y * gridDim.x + blockIdx.x] = sq;
+}
+
+// --------------------------------------------------------------- scalar losses
+__global__ __launch_bounds__(1024) void loss_reduce_kernel(int kind, const float* h, int64_t n, float* loss) {
+    __shared__ float red[16];
+    float s = 0.f;
+    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) s += kind == 0 ? h[i] * h[i] : h[i];
+    s = block_sum(s, red);
+    if (threadIdx.x == 0) *loss = kind == 0 ? s : s / float(n);
+}
+
+__global__ void loss_grad_kernel(int kind, const float* h, int64_t n, float* dh) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i < n) dh[i] = kind == 0 ? 2.f * h[i] : 1.f / float(n);
+}
+
+using HeadBF16 = TileCfg<bf16_t, 128, 128, 32, 2, 2>;
+using HeadF32 = TileCfg<float, 64, 64, 32, 2, 2>;
+
+struct XentWs {
+    float* logits = nullptr;
+    void* dz = nullptr;
+    float* loss_rows = nullptr;
+    float* part = nullptr;
+    int64_t ldv = 0;
+};
+
+size_t carve_xent(const janus_xent_desc& d, janus_xent_op op, void* base, XentWs& w) {
+    Carver c(base);
+    if (op == JANUS_XENT_FWD_BWD) {
+        w.ldv = round_up(d.V, 8);
+        w.logits = c.take<float>(int64_t(d.rows) * w.ldv);
+        w.dz = c.take<char>(int64_t(d.rows) * w.ldv * dtype_size(d.dtype));
+        w.loss_rows = c.take<float>(d.rows);
+        w.part = c.take<float>(colsum_partial_floats(d.V));
+    }
+    return c.off + 256;
+}
+
+struct MseWs {
+    void* dY = nullptr;
+    float* part = nullptr;
+    float* cpart = nullptr;
+    int nparts = 0;
+};
+
+template <class Cfg>
+int mse_parts(const janus_mse_desc& d) {
+    return ((d.P + Cfg::BN - 1) / Cfg::BN) * ((d.rows + Cfg::BM - 1) / Cfg::BM);
+}
+
+size_t carve_mse(const janus_mse_desc& d, void* base, MseWs& w) {
+    Carver c(base);
+    w.dY = c.take<char>(int64_t(d.rows) * d.P * dtype_size(d.dtype));
+    w.nparts = d.dtype == JANUS_BF16 ? mse_parts<HeadBF16>(d) : mse_parts<HeadF32>(d);
+    w.part = c.take<float>(w.nparts);
+    w.cpart = c.take<float>(colsum_partial_floats(d.P));
+    return c.off + 256;
+}
+
+template <typename T, class Cfg>
+janus_status mse_impl(const janus_mse_desc& d, const void* h, const void* W, const void* b, const void* tgt,
+                      void* dh, float* dW, float* db, float* loss, const MseWs& w, hipStream_t st) {
+    const float count = float(int64_t(d.rows) * d.P);
+    dim3 grid((d.P + Cfg::BN - 1) / Cfg::BN, (d.rows + Cfg::BM - 1) / Cfg::BM);
+    const bool al = (int64_t(d.H) * int64_t(sizeof(T))) % 16 == 0 && reinterpret_cast<uintptr_t>(h) % 16 == 0 &&
+                    reinterpret_cast<uintptr_t>(W) % 16 == 0;
+    if (al)
+        hipLaunchKernelGGL((mse_gemm_kernel<T, Cfg, true>), grid, dim3(Cfg::NT), Cfg::SMEM_BYTES, st, d.rows, d.P,
+                           d.H, static_cast<const T*>(h), static_cast<const T*>(W), static_cast<const T*>(b),
+                           static_cast<const T*>(tgt), static_cast<T*>(w.dY), 2.f / count, w.part);
+    else
+        hipLaunchKernelGGL((mse_gemm_kernel<T, Cfg, false>), grid, dim3(Cfg::NT), Cfg::SMEM_BYTES, st, d.rows, d.P,
+                           d.H, static_cast<const T*>(h), static_cast<const T*>(W), static_cast<const T*>(b),
+                           static_cast<const T*>(tgt), static_cast<T*>(w.dY), 2.f / count, w.part);
+    JANUS_LAUNCH_CHECK();
+    hipLaunchKernelGGL(finish_sum_kernel, dim3(1), dim3(1024), 0, st, w.part, int64_t(w.nparts), 1.f / count, loss);
+    JANUS_LAUNCH_CHECK();
+    // dh = dY W
+    GemmDesc g;
+    g.dtype = d.dtype;
+    g.M = d.rows;
+    g.N = d.H;
+    g.K = d.P;
+    g.A = w.dY;
+    g.lda = d.P;
+    g.b_t = true;
+    g.B = W;
+    g.ldb = d.H;
+    g.C = dh;
+    g.ldc = d.H;
+    g.c_f32 = false;
+    janus_status e = gemm(g, st);
+    if (e != JANUS_OK) return e;
+    // dW = dY^T h
+    GemmDesc q;
+    q.dtype = d.dtype;
+    q.M = d.P;
+    q.N = d.H;
+    q.K = d.rows;
+    q.a_t = true;
+    q.A = w.dY;
+    q.lda = d.P;
+    q.b_t = true;
+    q.B = h;
+    q.ldb = d.H;
+    q.C = dW;
+    q.ldc = d.H;
+    q.c_f32 = true;
+    e = gemm(q, st);
+    if (e != JANUS_OK) return e;
+    return colsum(d.dtype, w.dY, d.rows, d.P, d.P, db, w.cpart, st);
+}
+
+template <typename T>
+janus_status xent_impl(const janus_xent_desc& d, const int32_t* ids_dev, const void* Wout, const void* bout,
+                       const void* h, void* dh, float* dWout, float* dbout, float* loss, const XentWs& w,
+                       hipStream_t st) {
+    GemmDesc g;
+    g.dtype = d.dtype;
+    g.M = d.rows;
+    g.N = d.V;
+    g.K = d.H;
+    g.A = h;
+    g.lda = d.H;
+    g.B = Wout;
+    g.ldb = d.H;
+    g.C = w.logits;
+    g.ldc = w.ldv;
+    g.c_f32 = true;
+    g.bias = bout;
+    janus_status e = gemm(g, st);
+    if (e != JANUS_OK) return e;
+    hipLaunchKernelGGL(xent_row_kernel<T>, dim3(d.rows), dim3(256), 0, st, w.logits, w.ldv, ids_dev, d.V, d.rows,
+                       static_cast<T*>(w.dz), w.ldv, w.loss_rows);
+    JANUS_LAUNCH_CHECK();
+    hipLaunchKernelGGL(finish_sum_kernel, dim3(1), dim3(1024), 0, st, w.loss_rows, int64_t(d.rows),
+                       1.f / float(d.rows), loss);
+    JANUS_LAUNCH_CHECK();
+    // dh = dz Wout
+    GemmDesc q;
+    q.dtype = d.dtype;
+    q.M = d.rows;
+    q.N = d.H;
+    q.K = d.V;
+    q.A = w.dz;
+    q.lda = w.ldv;
+    q.b_t = true;
+    q.B = Wout;
+    q.ldb = d.H;
+    q.C = dh;
+    q.ldc = d.H;
+    q.c_f32 = false;
+    e = gemm(q, st);
+    if (e != JANUS_OK) return e;
+    // dWout = dz^T h
+    GemmDesc r;
+    r.dtype = d.dtype;
+    r.M = d.V;
+    r.N = d.H;
+    r.K = d.rows;
+    r.a_t = true;
+    r.A = w.dz;
+    r.lda = w.ldv;
+    r.b_t = true;
+    r.B = h;
+    r.ldb = d.H;
+    r.C = dWout;
+    r.ldc = d.H;
+    r.c_f32 = true;
+    e = gemm(r, st);
+    if (e != JANUS_OK) return e;
+    return colsum(d.dtype, w.dz, d.rows, d.V, w.ldv, dbout, w.part, st);
+}
+
+}  // namespace
+
+janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_dev, int rows, int H, float* dE, int V,
+                            hipStream_t st) {
+    if (rows > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
+    janus_status e = zero_fill(dE, size_t(V) * H * sizeof(float), st);
+    if (e != JANUS_OK) return e;
+    if (rows <= 0) return JANUS_OK;
+    const size_t sm = size_t(rows) * sizeof(int32_t);
+    if (dt == JANUS_BF16)
+        hipLaunchKernelGGL(embed_bwd_kernel<bf16_t>, dim3(rows), dim3(256), sm, st, static_cast<const bf16_t*>(dx),
+                           ids_dev, rows, V, H, dE);
+    else
+        hipLaunchKernelGGL(embed_bwd_kernel<float>, dim3(rows), dim3(256), sm, st, static_cast<const float*>(dx),
+                           ids_dev, rows, V, H, dE);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+}  // namespace janus
+
+using namespace janus;
+
+extern "C" size_t janus_xent_workspace_bytes(const janus_xent_desc* d, janus_xent_op op) {
+    if (!d || d->V <= 0 || d->H <= 0 || d->rows <= 0) return 0;
+    XentWs w;
+    return carve_xent(*d, op, nullptr, w);
+}
+
+extern "C" janus_status janus_embed_softmax_xent(const janus_xent_desc* d, janus_xent_op op, const int32_t* ids_host,
+                                                 const int32_t* ids_dev, const void* table, const void* bias,
+                                                 const void* in, void* out, float* dtable, float* dbias, float* loss,
+                                                 void* ws, size_t ws_bytes, void* stream) {
+    if (!d || d->V <= 0 || d->H <= 0 || d->rows <= 0 || !ids_host || !ids_dev) return JANUS_ERR_INVALID_ARG;
+    if (!dtype_ok(d->dtype)) return JANUS_ERR_UNSUPPORTED;
+    if (op != JANUS_EMBED_FWD && op != JANUS_XENT_FWD_BWD && op != JANUS_EMBED_BWD) return JANUS_ERR_INVALID_ARG;
+    if (op == JANUS_EMBED_FWD && (!table || !out)) return JANUS_ERR_INVALID_ARG;
+    if (op == JANUS_XENT_FWD_BWD && (!table || !bias || !in || !out || !dtable || !dbias || !loss))
+        return JANUS_ERR_INVALID_ARG;
+    if (op == JANUS_EMBED_BWD && (!in || !dtable)) return JANUS_ERR_INVALID_ARG;
+    if (op == JANUS_EMBED_BWD && d->rows > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
+    for (int32_t r = 0; r < d->rows; ++r)
+        if (ids_host[r] < 0 || ids_host[r] >= d->V) return JANUS_ERR_TOKEN;
+    XentWs w;
+    const size_t need = carve_xent(*d, op, nullptr, w);
+    if (op == JANUS_XENT_FWD_BWD) {
+        if (!ws || ws_bytes < need || reinterpret_cast<uintptr_t>(ws) % 256 != 0) return JANUS_ERR_WORKSPACE;
+        carve_xent(*d, op, ws, w);
+    }
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const size_t es = dtype_size(d->dtype);
+    if (op == JANUS_EMBED_FWD) {
+        const bool vec = (int64_t(d->H) * int64_t(es)) % 16 == 0 && reinterpret_cast<uintptr_t>(table) % 16 == 0 &&
+                         reinterpret_cast<uintptr_t>(out) % 16 == 0;
+        if (d->dtype == JANUS_BF16) {
+            if (vec)
+                hipLaunchKernelGGL((embed_fwd_kernel<bf16_t, true>), dim3(d->rows), dim3(128), 0, st,
+                                   static_cast<const bf16_t*>(table), ids_dev, d->V, d->H, static_cast<bf16_t*>(out));
+            else
+                hipLaunchKernelGGL((embed_fwd_kernel<bf16_t, false>), dim3(d->rows), dim3(128), 0, st,
+                                   static_cast<const bf16_t*>(table), ids_dev, d->V, d->H, static_cast<bf16_t*>(out));
+        } else {
+            if (vec)
+                hipLaunchKernelGGL((embed_fwd_kernel<float, true>), dim3(d->rows), dim3(128), 0, st,
+                                   static_cast<const float*>(table), ids_dev, d->V, d->H, static_cast<float*>(out));
+            else
+                hipLaunchKernelGGL((embed_fwd_kernel<float, false>), dim3(d->rows), dim3(128), 0, st,
+                                   static_cast<const float*>(table), ids_dev, d->V, d->H, static_cast<float*>(out));
+        }
+        JANUS_LAUNCH_CHECK();
+        return JANUS_OK;
+    }
+    if (op == JANUS_EMBED_BWD) return embed_backward(d->dtype, in, ids_dev, d->rows, d->H, dtable, d->V, st);
+    if (d->dtype == JANUS_BF16)
+        return xent_impl<bf16_t>(*d, ids_dev, table, bias, in, out, dtable, dbias, loss, w, st);
+    return xent_impl<float>(*d, ids_dev, table, bias, in, out, dtable, dbias, loss, w, st);
+}
+
+extern "C" size_t janus_mse_workspace_bytes(const janus_mse_desc* d) {
+    if (!d || d->rows <= 0 || d->H <= 0 || d->P <= 0 || !dtype_ok(d->dtype)) return 0;
+    MseWs w;
+    return carve_mse(*d, nullptr, w);
+}
+
+extern "C" janus_status janus_linear_mse(const janus_mse_desc* d, const void* h, const void* W, const void* b,
+                                         const void* target, void* dh, float* dW, float* db, float* loss, void* ws,
+                                         size_t ws_bytes, void* stream) {
+    if (!d || d->rows <= 0 || d->H <= 0 || d->P <= 0) return JANUS_ERR_INVALID_ARG;
+    if (!dtype_ok(d->dtype)) return JANUS_ERR_UNSUPPORTED;
+    if (!h || !W || !b || !target || !dh || !dW || !db || !loss) return JANUS_ERR_INVALID_ARG;
+    MseWs w;
+    if (!ws || ws_bytes < carve_mse(*d, nullptr, w) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return JANUS_ERR_WORKSPACE;
+    carve_mse(*d, ws, w);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if (d->dtype == JANUS_BF16) return mse_impl<bf16_t, HeadBF16>(*d, h, W, b, target, dh, dW, db, loss, w, st);
+    return mse_impl<float, HeadF32>(*d, h, W, b, target, dh, dW, db, loss, w, st);
+}
+
+extern "C" janus_status janus_loss_reduce(janus_loss_kind kind, const float* h, int64_t n, float* loss, float* dh,
+                                          void* stream) {
+    if (!h || !loss || n <= 0) return JANUS_ERR_INVALID_ARG;
+    if (kind != JANUS_LOSS_SUMSQ && kind != JANUS_LOSS_MEAN) return JANUS_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(1024), 0, st, int(kind), h, n, loss);
+    JANUS_LAUNCH_CHECK();
+    if (dh) {
+        hipLaunchKernelGGL(loss_grad_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, int(kind), h, n, dh);
+        JANUS_LAUNCH_CHECK();
+    }
+    return JANUS_OK;
+}

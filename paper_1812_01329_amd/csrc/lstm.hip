@@ -1,0 +1,597 @@
+// LSTM over variable-length sequences: forward and backward through time.
+//
+// The loop of Figure 1 (``state = rnn_cell(state, item)``) with one trip
+// count per sequence (Section 4.2.1).  The batch is sorted longest first, so
+// the sequences still running at step t are the first active[t] sorted rows
+// and their activations are stored "packed": packed row off[t] + r holds
+// sorted row r at step t.  Work per step is then a dense block of active[t]
+// rows; finished rows cost nothing.
+//
+// Per layer, forward:
+//   1. hoisted input projection for every packed row:  XG = X Wx^T + b
+//      (one contraction over all time steps; no dependence on h)
+//   2. for t < t_eff, one fused step kernel: the recurrent contraction
+//      h_{t-1} Wh^T for a tile of rows x (4 gates of U hidden units), then the
+//      cell pointwise on the same tile (gates, c_t, h_t, outputs).
+// Per layer, backward (reverse t):
+//   one fused step kernel per t: dh_rec = dG_{t+1} Wh for a tile of rows x
+//   hidden units, then the cell backward pointwise for step t on the same
+//   tile, writing dG_t and the carried dc.  After the loop, the weight
+//   gradients are single contractions over all packed rows:
+//   dWx = dG^T X, dWh = dG^T H_prev, db = column sums of dG, dX = dG Wx.
+//
+// Workspace layout (identical for forward and backward; see carve()):
+//   perm [B], xrow [T*B], prevrow [T*B]        int32 (variable lengths only)
+//   per layer: Hs [(B + T*B) x ldh] dtype      rows [0, B): h0 (sorted rows),
+//                                               row B + p: h at packed row p
+//              Cs [(B + T*B) x ldh] float32     same for c
+//              Gs [T*B x ldg] dtype             post-activation gates i, f, g, o
+//   XG [T*B x ldg] dtype                        XG in forward, dG in backward
+//   dY [T*B x ldh] dtype                        gradient of a lower layer's output
+//   dh, dc [B x H] float32                      carried gradients (sorted rows)
+//   colsum scratch
+#include <vector>
+
+#include "device.hpp"
+#include "ops.hpp"
+
+namespace janus {
+
+namespace {
+
+struct LstmWs {
+    int32_t* perm = nullptr;
+    int32_t* xrow = nullptr;
+    int32_t* prevrow = nullptr;
+    std::vector<void*> Hs;
+    std::vector<float*> Cs;
+    std::vector<void*> Gs;
+    void* XG = nullptr;
+    void* dY = nullptr;
+    float* dh = nullptr;
+    float* dc = nullptr;
+    float* part = nullptr;
+    int64_t ldh = 0, ldg = 0;
+};
+
+size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
+    Carver c(base);
+    const size_t es = dtype_size(d.dtype);
+    const int64_t TB = int64_t(d.T) * d.B;
+    w.ldh = round_up(d.H, 8);
+    w.ldg = round_up(int64_t(4) * d.H, 8);
+    w.perm = c.take<int32_t>(d.B);
+    w.xrow = c.take<int32_t>(TB);
+    w.prevrow = c.take<int32_t>(TB);
+    w.Hs.assign(d.L, nullptr);
+    w.Cs.assign(d.L, nullptr);
+    w.Gs.assign(d.L, nullptr);
+    for (int l = 0; l < d.L; ++l) {
+        w.Hs[l] = c.take<char>((d.B + TB) * w.ldh * es);
+        w.Cs[l] = c.take<float>((d.B + TB) * w.ldh);
+        w.Gs[l] = c.take<char>(TB * w.ldg * es);
+    }
+    w.XG = c.take<char>(TB * w.ldg * es);
+    w.dY = c.take<char>(TB * w.ldh * es);
+    w.dh = c.take<float>(int64_t(d.B) * d.H);
+    w.dc = c.take<float>(int64_t(d.B) * d.H);
+    w.part = c.take<float>(colsum_partial_floats(4 * d.H));
+    return c.off + 256;
+}
+
+// ------------------------------------------------------------ init kernels
+template <typename T>
+__global__ void fwd_init_kernel(int B, int H, int64_t ldh, const int32_t* perm, const float* h0, const float* c0,
+                                T* Hs, float* Cs, int active0, float* hT, float* cT) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(B) * H) return;
+    const int r = int(i / H), u = int(i % H);
+    const int b = perm ? perm[r] : r;
+    const float hv = h0 ? h0[int64_t(b) * H + u] : 0.f;
+    const float cv = c0 ? c0[int64_t(b) * H + u] : 0.f;
+    Hs[int64_t(r) * ldh + u] = from_f<T>(hv);
+    Cs[int64_t(r) * ldh + u] = cv;
+    if (r >= active0) {   // a length-0 sequence ends in its initial state
+        if (hT) hT[int64_t(b) * H + u] = hv;
+        if (cT) cT[int64_t(b) * H + u] = cv;
+    }
+}
+
+__global__ void bwd_init_kernel(int B, int H, const int32_t* perm, const float* dhT, const float* dcT, float* dh,
+                                float* dc) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(B) * H) return;
+    const int r = int(i / H), u = int(i % H);
+    const int b = perm ? perm[r] : r;
+    dh[i] = dhT ? dhT[int64_t(b) * H + u] : 0.f;
+    dc[i] = dcT ? dcT[int64_t(b) * H + u] : 0.f;
+}
+
+// ------------------------------------------------------------ forward step
+template <typename T>
+struct FwdStep {
+    int H, B, t, active, active_next, U;
+    int64_t off_t, prev_base, ldh, ldg;
+    T* Hs;
+    float* Cs;
+    const T* Wh;
+    const T* XG;
+    T* Gs;
+    T* y;
+    const int32_t* perm;
+    float* hT;
+    float* cT;
+};
+
+template <typename T, class Cfg, bool AL>
+__global__ __launch_bounds__(Cfg::NT) void fwd_step_kernel(FwdStep<T> a) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    T* sA = reinterpret_cast<T*>(smem_raw);
+    T* sB = sA + Cfg::BM * Cfg::LD;
+    const int tid = threadIdx.x;
+    const int U = a.U;
+    const int u0 = blockIdx.x * U;
+    const int m0 = blockIdx.y * Cfg::BM;
+
+    LoaderK<T, Cfg::BM, Cfg::BK, Cfg::NT, AL> la;
+    LoaderK<T, Cfg::BN, Cfg::BK, Cfg::NT, AL> lb;
+    la.init(a.Hs + (a.prev_base + m0) * a.ldh, a.ldh, 0, RowsContig{a.active - m0}, tid);
+    lb.init(a.Wh, a.H, 0, RowsGateMajor{a.H, u0, U, 4}, tid);
+    f32x16_t acc[Cfg::FM][Cfg::FN];
+    mma_mainloop<Cfg>(acc, la, lb, a.H, sA, sB, tid);
+
+    // stage the tile so that the four gates of a unit meet in one thread
+    __syncthreads();
+    constexpr int SLD = Cfg::BN + 1;
+    float* sT = reinterpret_cast<float*>(smem_raw);
+    const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                sT[(Cfg::wave_row0(wave) + i * 32 + acc_row(v, lane)) * SLD + Cfg::wave_col0(wave) + j * 32 +
+                   acc_col(lane)] = acc[i][j][v];
+    __syncthreads();
+
+    const int H = a.H;
+    for (int idx = tid; idx < Cfg::BM * U; idx += Cfg::NT) {
+        const int r = idx / U, j = idx - (idx / U) * U;
+        const int row = m0 + r, u = u0 + j;
+        if (row >= a.active || u >= H) continue;
+        const int64_t p = a.off_t + row;
+        const T* xg = a.XG + p * a.ldg + u;
+        const float ai = sT[r * SLD + 0 * U + j] + to_f(xg[0]);
+        const float af = sT[r * SLD + 1 * U + j] + to_f(xg[H]);
+        const float ag = sT[r * SLD + 2 * U + j] + to_f(xg[2 * H]);
+        const float ao = sT[r * SLD + 3 * U + j] + to_f(xg[3 * H]);
+        const float gi = sigmoidf_(ai), gf = sigmoidf_(af), gg = tanhf_(ag), go = sigmoidf_(ao);
+        const float cp = a.Cs[(a.prev_base + row) * a.ldh + u];
+        const float c = gf * cp + gi * gg;
+        const float h = go * tanhf_(c);
+        a.Cs[(a.B + p) * a.ldh + u] = c;
+        a.Hs[(a.B + p) * a.ldh + u] = from_f<T>(h);
+        T* gs = a.Gs + p * a.ldg + u;
+        gs[0] = from_f<T>(gi);
+        gs[H] = from_f<T>(gf);
+        gs[2 * H] = from_f<T>(gg);
+        gs[3 * H] = from_f<T>(go);
+        const int b = a.perm ? a.perm[row] : row;
+        if (a.y) a.y[(int64_t(a.t) * a.B + b) * H + u] = from_f<T>(h);
+        if (row >= a.active_next) {   // last step of this sequence
+            if (a.hT) a.hT[int64_t(b) * H + u] = h;
+            if (a.cT) a.cT[int64_t(b) * H + u] = c;
+        }
+    }
+}
+
+// ----------------------------------------------------------- backward step
+template <typename T>
+struct BwdStep {
+    int H, B, active, active_next;      // rows of step t; rows with a recurrent product
+    int final_step;                     // 1: write dh0 / dc0 instead of a cell backward
+    int64_t off_t, off_next, prev_base, ldh, ldg;
+    const T* Wh;
+    T* G;                               // dG store: read rows off_next + r, write rows off_t + r
+    const T* Gs;                        // saved gates
+    const float* Cs;
+    const T* dy;                        // gradient of this layer's output, or NULL
+    int64_t dy_ld;
+    const int32_t* dy_rows;             // packed row -> dy row, NULL = identity
+    float* dh;
+    float* dc;
+    const int32_t* perm;
+    float* dh0;
+    float* dc0;
+};
+
+template <typename T, class Cfg, bool AL>
+__global__ __launch_bounds__(Cfg::NT) void bwd_step_kernel(BwdStep<T> a) {
+    extern __shared__ __align__(16) unsigned char smem_raw[];
+    T* sA = reinterpret_cast<T*>(smem_raw);
+    T* sB = sA + Cfg::BM * Cfg::LD;
+    const int tid = threadIdx.x;
+    const int u0 = blockIdx.x * Cfg::BN;
+    const int m0 = blockIdx.y * Cfg::BM;
+    const int H = a.H;
+
+    // dh_rec[r, u] = sum_k dG_{t+1}[r, k] Wh[k, u]   (k over the 4H gate rows)
+    LoaderK<T, Cfg::BM, Cfg::BK, Cfg::NT, AL> la;
+    LoaderR<T, Cfg::BN, Cfg::BK, Cfg::NT, AL> lb;
+    la.init(a.G + (a.off_next + m0) * a.ldg, a.ldg, 0, RowsContig{a.active_next - m0}, tid);
+    lb.init(a.Wh, H, nullptr, u0, H);
+    f32x16_t acc[Cfg::FM][Cfg::FN];
+    mma_mainloop<Cfg>(acc, la, lb, a.active_next > m0 ? 4 * H : 0, sA, sB, tid);
+
+    __syncthreads();
+    constexpr int SLD = Cfg::BN + 1;
+    float* sT = reinterpret_cast<float*>(smem_raw);
+    const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v)
+                sT[(Cfg::wave_row0(wave) + i * 32 + acc_row(v, lane)) * SLD + Cfg::wave_col0(wave) + j * 32 +
+                   acc_col(lane)] = acc[i][j][v];
+    __syncthreads();
+
+    for (int idx = tid; idx < Cfg::BM * Cfg::BN; idx += Cfg::NT) {
+        const int r = idx / Cfg::BN, j = idx % Cfg::BN;
+        const int row = m0 + r, u = u0 + j;
+        if (row >= a.active || u >= H) continue;
+        const int64_t hu = int64_t(row) * H + u;
+        float dhv = row < a.active_next ? sT[r * SLD + j] : a.dh[hu];
+        if (a.final_step) {
+            const int b = a.perm ? a.perm[row] : row;
+            if (a.dh0) a.dh0[int64_t(b) * H + u] = dhv;
+            if (a.dc0) a.dc0[int64_t(b) * H + u] = a.dc[hu];
+            continue;
+        }
+        const int64_t p = a.off_t + row;
+        if (a.dy) {
+            const int64_t yr = a.dy_rows ? int64_t(a.dy_rows[p]) : p;
+            dhv += to_f(a.dy[yr * a.dy_ld + u]);
+        }
+        const T* gs = a.Gs + p * a.ldg + u;
+        const float gi = to_f(gs[0]), gf = to_f(gs[H]), gg = to_f(gs[2 * H]), go = to_f(gs[3 * H]);
+        const float c = a.Cs[(a.B + p) * a.ldh + u];
+        const float cp = a.Cs[(a.prev_base + row) * a.ldh + u];
+        const float tau = tanhf_(c);
+        const float d_o = dhv * tau;
+        const float dct = a.dc[hu] + dhv * go * (1.f - tau * tau);
+        const float d_i = dct * gg, d_g = dct * gi, d_f = dct * cp;
+        a.dc[hu] = dct * gf;
+        T* dg = a.G + p * a.ldg + u;
+        dg[0] = from_f<T>(d_i * gi * (1.f - gi));
+        dg[H] = from_f<T>(d_f * gf * (1.f - gf));
+        dg[2 * H] = from_f<T>(d_g * (1.f - gg * gg));
+        dg[3 * H] = from_f<T>(d_o * go * (1.f - go));
+    }
+}
+
+// bf16: 128 rows x 32 columns per tile, 4 waves of 32x32
+using StepBF16 = TileCfg<bf16_t, 128, 32, 32, 4, 1>;
+// fp32: 64 rows x 32 columns per tile, 2 waves of 32x32
+using StepF32 = TileCfg<float, 64, 32, 32, 2, 1>;
+
+template <class Cfg>
+constexpr int step_smem() {
+    return Cfg::SMEM_BYTES > Cfg::BM * (Cfg::BN + 1) * 4 ? Cfg::SMEM_BYTES : Cfg::BM * (Cfg::BN + 1) * 4;
+}
+
+template <typename T, class Cfg>
+janus_status launch_fwd_step(const FwdStep<T>& a, bool al, hipStream_t s) {
+    dim3 grid((a.H + a.U - 1) / a.U, (a.active + Cfg::BM - 1) / Cfg::BM);
+    if (al)
+        hipLaunchKernelGGL((fwd_step_kernel<T, Cfg, true>), grid, dim3(Cfg::NT), step_smem<Cfg>(), s, a);
+    else
+        hipLaunchKernelGGL((fwd_step_kernel<T, Cfg, false>), grid, dim3(Cfg::NT), step_smem<Cfg>(), s, a);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+template <typename T, class Cfg>
+janus_status launch_bwd_step(const BwdStep<T>& a, bool al, hipStream_t s) {
+    dim3 grid((a.H + Cfg::BN - 1) / Cfg::BN, (a.active + Cfg::BM - 1) / Cfg::BM);
+    if (grid.y == 0) return JANUS_OK;
+    if (al)
+        hipLaunchKernelGGL((bwd_step_kernel<T, Cfg, true>), grid, dim3(Cfg::NT), step_smem<Cfg>(), s, a);
+    else
+        hipLaunchKernelGGL((bwd_step_kernel<T, Cfg, false>), grid, dim3(Cfg::NT), step_smem<Cfg>(), s, a);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+janus_status check_desc(const janus_lstm_desc* d) {
+    if (!d) return JANUS_ERR_INVALID_ARG;
+    if (d->L <= 0 || d->I <= 0 || d->H <= 0 || d->B <= 0 || d->T < 0) return JANUS_ERR_INVALID_ARG;
+    if (!dtype_ok(d->dtype)) return JANUS_ERR_UNSUPPORTED;
+    return JANUS_OK;
+}
+
+bool all_nonnull(const void* const* p, int n) {
+    if (!p) return false;
+    for (int i = 0; i < n; ++i)
+        if (!p[i]) return false;
+    return true;
+}
+
+bool weight_aligned(const janus_lstm_desc& d) {
+    // vector loads of Wh rows need 16-byte aligned rows
+    return (int64_t(d.H) * int64_t(dtype_size(d.dtype))) % 16 == 0;
+}
+
+template <typename T, class Cfg>
+janus_status lstm_fwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const LstmWs& w, const void* x,
+                           const void* const* Wx, const void* const* Wh, const void* const* b, const float* h0,
+                           const float* c0, void* y, float* hT, float* cT, hipStream_t st) {
+    const int B = d.B, H = d.H;
+    const int64_t TB = int64_t(d.T) * B;
+    const int32_t* perm = s.fixed ? nullptr : w.perm;
+    const int32_t* xrow = s.fixed ? nullptr : w.xrow;
+    if (!s.fixed) {
+        janus_status e = zero_fill(y, size_t(TB) * H * sizeof(T), st);
+        if (e != JANUS_OK) return e;
+    }
+    const bool al = weight_aligned(d);
+    for (int l = 0; l < d.L; ++l) {
+        const int64_t bh = int64_t(B) * H;
+        hipLaunchKernelGGL(fwd_init_kernel<T>, dim3(unsigned((bh + 255) / 256)), dim3(256), 0, st, B, H, w.ldh, perm,
+                           h0 ? h0 + l * bh : nullptr, c0 ? c0 + l * bh : nullptr, static_cast<T*>(w.Hs[l]),
+                           w.Cs[l], s.active[0], hT ? hT + l * bh : nullptr, cT ? cT + l * bh : nullptr);
+        JANUS_LAUNCH_CHECK();
+        if (s.packed == 0) continue;
+        // hoisted input projection of every running (t, b)
+        GemmDesc g;
+        g.dtype = d.dtype;
+        g.M = int(s.packed);
+        g.N = 4 * H;
+        g.K = l == 0 ? d.I : H;
+        if (l == 0) {
+            g.A = x;
+            g.lda = d.I;
+            g.a_idx = xrow;
+        } else {
+            g.A = static_cast<const T*>(w.Hs[l - 1]) + int64_t(B) * w.ldh;
+            g.lda = w.ldh;
+        }
+        g.B = Wx[l];
+        g.ldb = g.K;
+        g.C = w.XG;
+        g.ldc = w.ldg;
+        g.c_f32 = false;
+        g.bias = b[l];
+        janus_status e = gemm(g, st);
+        if (e != JANUS_OK) return e;
+        for (int t = 0; t < s.t_eff; ++t) {
+            FwdStep<T> a;
+            a.H = H;
+            a.B = B;
+            a.t = t;
+            a.active = s.active[t];
+            a.active_next = s.active[t + 1];
+            a.U = Cfg::BN / 4;
+            a.off_t = s.offsets[t];
+            a.prev_base = t == 0 ? 0 : int64_t(B) + s.offsets[t - 1];
+            a.ldh = w.ldh;
+            a.ldg = w.ldg;
+            a.Hs = static_cast<T*>(w.Hs[l]);
+            a.Cs = w.Cs[l];
+            a.Wh = static_cast<const T*>(Wh[l]);
+            a.XG = static_cast<const T*>(w.XG);
+            a.Gs = static_cast<T*>(w.Gs[l]);
+            a.y = l == d.L - 1 ? static_cast<T*>(y) : nullptr;
+            a.perm = perm;
+            a.hT = hT ? hT + l * bh : nullptr;
+            a.cT = cT ? cT + l * bh : nullptr;
+            e = launch_fwd_step<T, Cfg>(a, al, st);
+            if (e != JANUS_OK) return e;
+        }
+    }
+    return JANUS_OK;
+}
+
+template <typename T, class Cfg>
+janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const LstmWs& w, const void* x,
+                           const void* const* Wx, const void* const* Wh, const void* dy, const float* dhT,
+                           const float* dcT, void* dx, float* dh0, float* dc0, float* const* dWx,
+                           float* const* dWh, float* const* db, hipStream_t st) {
+    const int B = d.B, H = d.H;
+    const int64_t TB = int64_t(d.T) * B;
+    const int32_t* perm = s.fixed ? nullptr : w.perm;
+    const int32_t* xrow = s.fixed ? nullptr : w.xrow;
+    const int32_t* prevrow = s.fixed ? nullptr : w.prevrow;
+    const bool al = weight_aligned(d);
+    if (dx && !s.fixed) {
+        janus_status e = zero_fill(dx, size_t(TB) * d.I * sizeof(T), st);
+        if (e != JANUS_OK) return e;
+    }
+    const int64_t bh = int64_t(B) * H;
+    for (int l = d.L - 1; l >= 0; --l) {
+        const bool top = l == d.L - 1;
+        hipLaunchKernelGGL(bwd_init_kernel, dim3(unsigned((bh + 255) / 256)), dim3(256), 0, st, B, H, perm,
+                           dhT ? dhT + l * bh : nullptr, dcT ? dcT + l * bh : nullptr, w.dh, w.dc);
+        JANUS_LAUNCH_CHECK();
+        BwdStep<T> a;
+        a.H = H;
+        a.B = B;
+        a.ldh = w.ldh;
+        a.ldg = w.ldg;
+        a.Wh = static_cast<const T*>(Wh[l]);
+        a.G = static_cast<T*>(w.XG);
+        a.Gs = static_cast<const T*>(w.Gs[l]);
+        a.Cs = w.Cs[l];
+        if (top) {
+            a.dy = static_cast<const T*>(dy);
+            a.dy_ld = H;
+            a.dy_rows = xrow;
+        } else {
+            a.dy = static_cast<const T*>(w.dY);
+            a.dy_ld = w.ldh;
+            a.dy_rows = nullptr;
+        }
+        a.dh = w.dh;
+        a.dc = w.dc;
+        a.perm = perm;
+        a.dh0 = dh0 ? dh0 + l * bh : nullptr;
+        a.dc0 = dc0 ? dc0 + l * bh : nullptr;
+        for (int t = s.t_eff - 1; t >= 0; --t) {
+            a.final_step = 0;
+            a.active = s.active[t];
+            a.active_next = s.active[t + 1];
+            a.off_t = s.offsets[t];
+            a.off_next = s.offsets[t + 1];
+            a.prev_base = t == 0 ? 0 : int64_t(B) + s.offsets[t - 1];
+            janus_status e = launch_bwd_step<T, Cfg>(a, al, st);
+            if (e != JANUS_OK) return e;
+        }
+        if (a.dh0 || a.dc0) {
+            a.final_step = 1;
+            a.active = B;
+            a.active_next = s.active[0];
+            a.off_t = 0;
+            a.off_next = 0;
+            a.prev_base = 0;
+            janus_status e = launch_bwd_step<T, Cfg>(a, al, st);
+            if (e != JANUS_OK) return e;
+        }
+        const int Il = l == 0 ? d.I : H;
+        // dWx = dG^T X
+        GemmDesc g;
+        g.dtype = d.dtype;
+        g.M = 4 * H;
+        g.N = Il;
+        g.K = int(s.packed);
+        g.a_t = true;
+        g.A = w.XG;
+        g.lda = w.ldg;
+        g.b_t = true;
+        if (l == 0) {
+            g.B = x;
+            g.ldb = d.I;
+            g.b_idx = xrow;
+        } else {
+            g.B = static_cast<const T*>(w.Hs[l - 1]) + int64_t(B) * w.ldh;
+            g.ldb = w.ldh;
+        }
+        g.C = dWx[l];
+        g.ldc = Il;
+        g.c_f32 = true;
+        janus_status e = gemm(g, st);
+        if (e != JANUS_OK) return e;
+        // dWh = dG^T H_prev
+        g.N = H;
+        g.B = w.Hs[l];
+        g.ldb = w.ldh;
+        g.b_idx = prevrow;
+        g.C = dWh[l];
+        g.ldc = H;
+        e = gemm(g, st);
+        if (e != JANUS_OK) return e;
+        e = colsum(d.dtype, w.XG, s.packed, 4 * H, w.ldg, db[l], w.part, st);
+        if (e != JANUS_OK) return e;
+        // gradient of this layer's input: dG Wx
+        if (l > 0 || dx) {
+            GemmDesc q;
+            q.dtype = d.dtype;
+            q.M = int(s.packed);
+            q.N = Il;
+            q.K = 4 * H;
+            q.A = w.XG;
+            q.lda = w.ldg;
+            q.b_t = true;
+            q.B = Wx[l];
+            q.ldb = Il;
+            q.c_f32 = false;
+            if (l > 0) {
+                q.C = w.dY;
+                q.ldc = w.ldh;
+            } else {
+                q.C = dx;
+                q.ldc = d.I;
+                q.c_idx = xrow;
+            }
+            e = gemm(q, st);
+            if (e != JANUS_OK) return e;
+        }
+    }
+    return JANUS_OK;
+}
+
+janus_status upload_schedule(const SeqSchedule& s, const LstmWs& w, hipStream_t st) {
+    if (s.fixed) return JANUS_OK;
+    janus_status e = upload(w.perm, s.perm.data(), sizeof(int32_t) * s.B, st);
+    if (e != JANUS_OK) return e;
+    if (s.packed > 0) {
+        e = upload(w.xrow, s.xrow.data(), sizeof(int32_t) * s.packed, st);
+        if (e != JANUS_OK) return e;
+        e = upload(w.prevrow, s.prevrow.data(), sizeof(int32_t) * s.packed, st);
+    }
+    return e;
+}
+
+}  // namespace
+
+}  // namespace janus
+
+using namespace janus;
+
+extern "C" size_t janus_lstm_workspace_bytes(const janus_lstm_desc* d) {
+    if (check_desc(d) != JANUS_OK) return 0;
+    LstmWs w;
+    return carve(*d, nullptr, w);
+}
+
+extern "C" janus_status janus_lstm_seq_fwd(const janus_lstm_desc* d, const void* x, const int32_t* lengths,
+                                           const void* const* Wx, const void* const* Wh, const void* const* b,
+                                           const float* h0, const float* c0, void* y, float* hT, float* cT,
+                                           void* ws, size_t ws_bytes, void* stream) {
+    janus_status e = check_desc(d);
+    if (e != JANUS_OK) return e;
+    if ((!x && d->T > 0) || (!y && d->T > 0) || !all_nonnull(Wx, d->L) || !all_nonnull(Wh, d->L) ||
+        !all_nonnull(b, d->L))
+        return JANUS_ERR_INVALID_ARG;
+    if (!ws) return JANUS_ERR_WORKSPACE;
+    SeqSchedule s;
+    e = build_seq_schedule(d->B, d->T, lengths, s);
+    if (e != JANUS_OK) return e;
+    LstmWs w;
+    if (ws_bytes < carve(*d, nullptr, w) || reinterpret_cast<uintptr_t>(ws) % 256 != 0) return JANUS_ERR_WORKSPACE;
+    carve(*d, ws, w);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    e = upload_schedule(s, w, st);
+    if (e != JANUS_OK) return e;
+    if (d->dtype == JANUS_BF16)
+        return lstm_fwd_impl<bf16_t, StepBF16>(*d, s, w, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
+    return lstm_fwd_impl<float, StepF32>(*d, s, w, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
+}
+
+extern "C" janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void* x, const int32_t* lengths,
+                                           const void* const* Wx, const void* const* Wh, void* ws, size_t ws_bytes,
+                                           const void* dy, const float* dhT, const float* dcT, void* dx, float* dh0,
+                                           float* dc0, float* const* dWx, float* const* dWh, float* const* db,
+                                           void* stream) {
+    janus_status e = check_desc(d);
+    if (e != JANUS_OK) return e;
+    if ((!x && d->T > 0) || !all_nonnull(Wx, d->L) || !all_nonnull(Wh, d->L) ||
+        !all_nonnull(reinterpret_cast<const void* const*>(dWx), d->L) ||
+        !all_nonnull(reinterpret_cast<const void* const*>(dWh), d->L) ||
+        !all_nonnull(reinterpret_cast<const void* const*>(db), d->L))
+        return JANUS_ERR_INVALID_ARG;
+    if (!ws) return JANUS_ERR_WORKSPACE;
+    SeqSchedule s;
+    e = build_seq_schedule(d->B, d->T, lengths, s);
+    if (e != JANUS_OK) return e;
+    LstmWs w;
+    if (ws_bytes < carve(*d, nullptr, w) || reinterpret_cast<uintptr_t>(ws) % 256 != 0) return JANUS_ERR_WORKSPACE;
+    carve(*d, ws, w);
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    e = upload_schedule(s, w, st);
+    if (e != JANUS_OK) return e;
+    if (d->dtype == JANUS_BF16)
+        return lstm_bwd_impl<bf16_t, StepBF16>(*d, s, w, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
+    return lstm_bwd_impl<float, StepF32>(*d, s, w, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
+}

@@ -1,0 +1,53 @@
+// Internal launchers shared between the library's translation units.
+#pragma once
+
+#include "runtime.hpp"
+
+namespace janus {
+
+// C[M, N] = alpha * sum_k A(m, k) B(n, k) + bias[n]
+//  A(m, k) = A[a_row(m) * lda + k]        (a_t = false; a_idx maps m, or NULL)
+//          = A[a_row(k) * lda + m]        (a_t = true;  a_idx maps k, or NULL)
+//  B(n, k) = B[b_row(n) * ldb + k]        (b_t = false; b_idx maps n, or NULL)
+//          = B[b_row(k) * ldb + n]        (b_t = true;  b_idx maps k, or NULL)
+//  C row m is written at C[c_row(m) * ldc + n] (c_idx maps m, or NULL), in
+//  float32 when c_f32, else in the operand dtype.  bias (dtype) may be NULL.
+// Supported layouts: (a_t, b_t) = (0, 0), (0, 1), (1, 1).
+struct GemmDesc {
+    janus_dtype dtype = JANUS_BF16;
+    int M = 0, N = 0, K = 0;
+    bool a_t = false;
+    const void* A = nullptr;
+    int64_t lda = 0;
+    const int32_t* a_idx = nullptr;
+    bool b_t = false;
+    const void* B = nullptr;
+    int64_t ldb = 0;
+    const int32_t* b_idx = nullptr;
+    void* C = nullptr;
+    int64_t ldc = 0;
+    const int32_t* c_idx = nullptr;
+    bool c_f32 = true;
+    const void* bias = nullptr;
+    float alpha = 1.0f;
+};
+
+janus_status gemm(const GemmDesc& g, hipStream_t stream);
+
+// out[c] = sum over rows r < R of in[r * ld + c] (float32 result), for
+// c < C; deterministic two-pass reduction using `partial` scratch of
+// colsum_partial_floats(C) floats.
+size_t colsum_partial_floats(int C);
+janus_status colsum(janus_dtype dt, const void* in, int64_t R, int C, int64_t ld, float* out,
+                    float* partial, hipStream_t stream);
+
+// clear `bytes` bytes of device memory (a kernel, so it may be captured)
+janus_status zero_fill(void* p, size_t bytes, hipStream_t stream);
+
+// dE [V, H] float32 = 0, then dE[ids[r]] = sum of dx[r] over rows with that
+// id, in ascending r (one owner per id, no atomics).  rows <= kMaxEmbedBwdRows.
+constexpr int kMaxEmbedBwdRows = 16384;
+janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_dev, int rows, int H, float* dE, int V,
+                            hipStream_t stream);
+
+}  // namespace janus

@@ -1,0 +1,103 @@
+// Host runtime: pinned staging ring for schedule uploads, status strings.
+#include "runtime.hpp"
+
+#include <cstring>
+#include <deque>
+#include <mutex>
+
+namespace janus {
+
+namespace {
+
+// A ring of pinned host memory.  Each upload copies its bytes into the next
+// free region, enqueues an asynchronous host-to-device copy on the caller's
+// stream and records an event; a region is reused only after its event has
+// completed.  The ring is allocated once per process.
+class PinnedRing {
+  public:
+    static constexpr size_t kCapacity = size_t(64) << 20;
+
+    janus_status put(void* dst, const void* src, size_t bytes, hipStream_t stream) {
+        std::lock_guard<std::mutex> lock(mu_);
+        if (!base_) {
+            if (hipHostMalloc(reinterpret_cast<void**>(&base_), kCapacity, hipHostMallocDefault) != hipSuccess) {
+                base_ = nullptr;
+                return JANUS_ERR_DEVICE;
+            }
+        }
+        const size_t need = (bytes + 255) & ~size_t(255);
+        if (need > kCapacity) return JANUS_ERR_UNSUPPORTED;
+        if (head_ + need > kCapacity) head_ = 0;
+        // wait for every in-flight copy that still reads the target region
+        for (auto it = inflight_.begin(); it != inflight_.end();) {
+            const bool overlap = it->off < head_ + need && head_ < it->off + it->len;
+            if (overlap) {
+                if (hipEventSynchronize(it->ev) != hipSuccess) return JANUS_ERR_DEVICE;
+                free_events_.push_back(it->ev);
+                it = inflight_.erase(it);
+            } else {
+                ++it;
+            }
+        }
+        std::memcpy(base_ + head_, src, bytes);
+        if (hipMemcpyAsync(dst, base_ + head_, bytes, hipMemcpyHostToDevice, stream) != hipSuccess)
+            return JANUS_ERR_DEVICE;
+        hipEvent_t ev;
+        if (!free_events_.empty()) {
+            ev = free_events_.back();
+            free_events_.pop_back();
+        } else if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) {
+            return JANUS_ERR_DEVICE;
+        }
+        if (hipEventRecord(ev, stream) != hipSuccess) return JANUS_ERR_DEVICE;
+        inflight_.push_back({head_, need, ev});
+        // retire completed copies so the list stays short
+        while (!inflight_.empty() && hipEventQuery(inflight_.front().ev) == hipSuccess) {
+            free_events_.push_back(inflight_.front().ev);
+            inflight_.pop_front();
+        }
+        head_ += need;
+        return JANUS_OK;
+    }
+
+  private:
+    struct Use {
+        size_t off, len;
+        hipEvent_t ev;
+    };
+    std::mutex mu_;
+    char* base_ = nullptr;
+    size_t head_ = 0;
+    std::deque<Use> inflight_;
+    std::vector<hipEvent_t> free_events_;
+};
+
+PinnedRing& ring() {
+    static PinnedRing r;
+    return r;
+}
+
+}  // namespace
+
+janus_status upload(void* dst_dev, const void* src_host, size_t bytes, hipStream_t stream) {
+    if (bytes == 0) return JANUS_OK;
+    return ring().put(dst_dev, src_host, bytes, stream);
+}
+
+}  // namespace janus
+
+extern "C" const char* janus_status_string(janus_status s) {
+    switch (s) {
+        case JANUS_OK: return "ok";
+        case JANUS_ERR_INVALID_ARG: return "invalid argument";
+        case JANUS_ERR_LENGTH: return "sequence length outside [0, T]";
+        case JANUS_ERR_TREE: return "malformed tree batch";
+        case JANUS_ERR_TOKEN: return "id outside [0, V)";
+        case JANUS_ERR_WORKSPACE: return "workspace missing, too small or misaligned";
+        case JANUS_ERR_UNSUPPORTED: return "unsupported dtype or shape";
+        case JANUS_ERR_DEVICE: return "HIP call failed";
+    }
+    return "unknown status";
+}
+
+extern "C" const char* janus_version(void) { return "janus-mi355x 0.1.0 (gfx950)"; }

@@ -1,0 +1,70 @@
+// Internal host-side declarations shared by the library's translation units.
+#pragma once
+
+#include <hip/hip_runtime_api.h>
+
+#include <cstddef>
+#include <cstdint>
+#include <vector>
+
+#include "../../include/janus.h"
+
+namespace janus {
+
+// ---------------------------------------------------------------- schedules
+struct SeqSchedule {
+    int32_t B = 0, T = 0, t_eff = 0;
+    int64_t packed = 0;              // sum of lengths = rows of all running steps
+    bool fixed = true;               // every length equals T (identity maps)
+    std::vector<int32_t> perm;       // [B]
+    std::vector<int32_t> active;     // [T + 1], active[t] = 0 for t >= t_eff
+    std::vector<int32_t> offsets;    // [T + 2]
+    std::vector<int32_t> xrow;       // [packed] row of x for each packed row (varlen only)
+    std::vector<int32_t> prevrow;    // [packed] row of h_{t-1} in the h store (varlen only)
+};
+
+struct TreeSchedule {
+    int32_t N = 0, num_trees = 0, num_levels = 0, max_level_size = 0;
+    std::vector<int32_t> level;          // [N]
+    std::vector<int32_t> level_offsets;  // [L + 1]
+    std::vector<int32_t> level_nodes;    // [N] node at each level-ordered position
+    std::vector<int32_t> pos;            // [N] level-ordered position of each node
+};
+
+janus_status build_seq_schedule(int32_t B, int32_t T, const int32_t* lengths, SeqSchedule& s);
+janus_status validate_tree_batch(const janus_tree_batch* t, int32_t V);
+janus_status build_tree_schedule(const janus_tree_batch* t, int32_t V, TreeSchedule& s);
+
+// ---------------------------------------------------------------- workspace
+// Bump allocator used both to size a workspace (base == nullptr) and to
+// carve it; identical call sequences give identical layouts.
+struct Carver {
+    char* base;
+    size_t off = 0;
+    explicit Carver(void* b) : base(static_cast<char*>(b)) {}
+    template <typename T>
+    T* take(size_t count) {
+        off = (off + 255) & ~size_t(255);
+        T* p = base ? reinterpret_cast<T*>(base + off) : nullptr;
+        off += count * sizeof(T);
+        return p;
+    }
+};
+
+inline int64_t round_up(int64_t v, int64_t m) { return (v + m - 1) / m * m; }
+inline size_t dtype_size(janus_dtype d) { return d == JANUS_BF16 ? 2 : 4; }
+inline bool dtype_ok(janus_dtype d) { return d == JANUS_F32 || d == JANUS_BF16; }
+
+// Copies small host arrays (schedules, index maps) into device memory
+// through a pinned staging ring, so that the source may be a temporary and
+// the copy stays asynchronous on the caller's stream.
+janus_status upload(void* dst_dev, const void* src_host, size_t bytes, hipStream_t stream);
+
+#define JANUS_HIP(call)                                        \
+    do {                                                       \
+        if ((call) != hipSuccess) return JANUS_ERR_DEVICE;     \
+    } while (0)
+
+#define JANUS_LAUNCH_CHECK() JANUS_HIP(hipGetLastError())
+
+}  // namespace janus

@@ -1,0 +1,223 @@
+"""Host-side tests of the C ABI (no GPU needed): the library loads and
+exports every declared symbol, the integer schedules match the oracle's bit
+for bit, and invalid calls are rejected before any device work."""
+import ctypes as C
+import os
+import re
+
+import numpy as np
+import pytest
+
+from oracle import schedule as osched
+from paper_1812_01329_amd import janus as J
+from paper_1812_01329_amd import workloads as wl
+
+ROOT = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+
+
+def declared_symbols():
+    src = open(os.path.join(ROOT, "include", "janus.h")).read()
+    return sorted(set(re.findall(r"\b(janus_[a-z_0-9]+)\s*\(", src)))
+
+
+def test_library_exports_every_declared_symbol():
+    lib = J.lib()
+    decl = declared_symbols()
+    assert len(decl) >= 15
+    for name in decl:
+        assert hasattr(lib, name), name
+    assert set(decl) == set(J.EXPORTS)
+    assert "gfx950" in J.version()
+    for s in range(8):
+        assert J.status_string(s)
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_seq_schedule_bit_exact(seed):
+    rng = np.random.default_rng(seed)
+    for _ in range(250):
+        B = int(rng.integers(1, 300)); T = int(rng.integers(0, 260))
+        mode = rng.integers(0, 3)
+        if mode == 0:
+            lengths = rng.integers(0, T + 1, B)
+        elif mode == 1:
+            lengths = np.full(B, T)
+        else:
+            lengths = rng.choice([0, T, T // 2], B)
+        perm, active, offsets, t_eff = J.janus_lstm_schedule(B, T, lengths)
+        operm, oactive, ooffsets, ot_eff = osched.seq_schedule(lengths, T)
+        assert t_eff == ot_eff
+        assert np.array_equal(perm, operm)
+        assert np.array_equal(active[:t_eff], oactive)
+        assert np.all(active[t_eff:] == 0)
+        assert np.array_equal(offsets[:t_eff + 1], ooffsets)
+        assert np.all(offsets[t_eff:] == offsets[t_eff])
+
+
+@pytest.mark.parametrize("seed", range(8))
+def test_tree_schedule_bit_exact(seed):
+    rng = np.random.default_rng(100 + seed)
+    for _ in range(150):
+        t = wl.make_trees(rng, int(rng.integers(1, 30)), 1, int(rng.integers(1, 60)), 500)
+        if rng.random() < 0.5:   # arbitrary node numbering
+            N = t.num_nodes
+            p = rng.permutation(N)
+            inv = np.argsort(p)
+            remap = lambda a: np.where(a >= 0, p[np.maximum(a, 0)], -1).astype(np.int32)
+            t = wl.TreeBatch(remap(t.left)[inv], remap(t.right)[inv], t.word[inv], p[t.root].astype(np.int32))
+        lev, off, nodes, L = J.janus_tree_schedule_build(t.left, t.right, t.word, t.root, 500)
+        olev, ooff, onodes, oL = osched.tree_schedule(t.left, t.right, t.word, t.root, 500)
+        assert L == oL
+        assert np.array_equal(lev, olev)
+        assert np.array_equal(off, ooff)
+        assert np.array_equal(nodes, onodes)
+
+
+def _tree(left, right, word, root):
+    return [np.asarray(a, np.int32) for a in (left, right, word, root)]
+
+
+@pytest.mark.parametrize("case,status", [
+    (_tree([-1, -1, 0], [-1, -1, 1], [1, 2, -1], [2]), J.OK),
+    (_tree([-1, -1, 0], [-1, -1, -1], [1, 2, -1], [2]), J.ERR_TREE),
+    (_tree([-1, -1, 0], [-1, -1, 0], [1, 2, -1], [2]), J.ERR_TREE),
+    (_tree([-1, -1, 0, 0], [-1, -1, 1, 1], [1, 2, -1, -1], [2, 3]), J.ERR_TREE),
+    (_tree([-1, -1, 0], [-1, -1, 1], [1, 9, -1], [2]), J.ERR_TOKEN),
+    (_tree([-1, -1, 0], [-1, -1, 1], [1, 2, 4], [2]), J.ERR_TREE),
+    (_tree([-1, -1, 0], [-1, -1, 1], [1, 2, -1], [1]), J.ERR_TREE),
+    (_tree([-1, 2, 1], [-1, 0, 0], [1, -1, -1], [0]), J.ERR_TREE),
+    (_tree([-1, -1, 0], [-1, -1, 5], [1, 2, -1], [2]), J.ERR_TREE),
+    (_tree([-1, -1, 0], [-1, -1, 1], [1, 2, -1], [2, 2]), J.ERR_TREE),
+])
+def test_tree_validation_status(case, status):
+    kind = {J.OK: None, J.ERR_TREE: "tree", J.ERR_TOKEN: "token"}[status]
+    if status == J.OK:
+        J.janus_tree_schedule_build(*case, 5)
+        osched.tree_schedule(*case, 5)
+    else:
+        with pytest.raises(J.JanusError) as e:
+            J.janus_tree_schedule_build(*case, 5)
+        assert e.value.status == status
+        with pytest.raises(osched.ScheduleError) as oe:
+            osched.tree_schedule(*case, 5)
+        assert oe.value.kind == kind
+
+
+class _HostBuf:
+    """A host buffer standing in for a device tensor in calls that must be
+    rejected before any device access; filled with a sentinel."""
+    def __init__(self, nbytes, fill=0x5A):
+        self.a = np.full(max(nbytes, 1), fill, np.uint8)
+
+    def data_ptr(self):
+        return self.a.ctypes.data
+
+    def numel(self):
+        return self.a.size
+
+    def element_size(self):
+        return 1
+
+    def untouched(self, fill=0x5A):
+        return bool(np.all(self.a == fill))
+
+
+def _lstm_args(L=1, I=4, H=8, B=3, T=5, dtype=J.F32, ws_bytes=None):
+    d = J.LstmDesc(L, I, H, B, T, dtype)
+    need = J.janus_lstm_workspace_bytes(L, I, H, B, T, dtype)
+    es = 2 if dtype == J.BF16 else 4
+    bufs = dict(x=_HostBuf(T * B * I * es), y=_HostBuf(T * B * H * es), hT=_HostBuf(L * B * H * 4),
+                cT=_HostBuf(L * B * H * 4), ws=_HostBuf(need if ws_bytes is None else ws_bytes))
+    W = [_HostBuf(4 * H * I * es) for _ in range(L)]
+    U = [_HostBuf(4 * H * H * es) for _ in range(L)]
+    b = [_HostBuf(4 * H * es) for _ in range(L)]
+    return d, bufs, W, U, b
+
+
+@pytest.mark.parametrize("lengths,status", [
+    ([5, -1, 2], J.ERR_LENGTH),
+    ([6, 1, 2], J.ERR_LENGTH),
+])
+def test_lstm_rejects_bad_lengths_untouched(lengths, status):
+    d, bf, W, U, b = _lstm_args()
+    with pytest.raises(J.JanusError) as e:
+        J.janus_lstm_seq_fwd(d, bf["x"], lengths, W, U, b, None, None, bf["y"], bf["hT"], bf["cT"], bf["ws"],
+                             stream=0)
+    assert e.value.status == status
+    assert all(v.untouched() for v in bf.values())
+
+
+def test_lstm_rejects_small_workspace_and_bad_desc():
+    d, bf, W, U, b = _lstm_args(ws_bytes=1024)
+    with pytest.raises(J.JanusError) as e:
+        J.janus_lstm_seq_fwd(d, bf["x"], None, W, U, b, None, None, bf["y"], bf["hT"], bf["cT"], bf["ws"], stream=0)
+    assert e.value.status == J.ERR_WORKSPACE
+    assert all(v.untouched() for v in bf.values())
+    for bad in (J.LstmDesc(0, 4, 8, 3, 5, J.F32), J.LstmDesc(1, 4, -8, 3, 5, J.F32), J.LstmDesc(1, 4, 8, 3, -1, J.F32)):
+        with pytest.raises(J.JanusError) as e:
+            J.janus_lstm_seq_fwd(bad, bf["x"], None, W, U, b, None, None, bf["y"], bf["hT"], bf["cT"], bf["ws"],
+                                 stream=0)
+        assert e.value.status == J.ERR_INVALID_ARG
+    with pytest.raises(J.JanusError) as e:
+        J.janus_lstm_seq_fwd(J.LstmDesc(1, 4, 8, 3, 5, 7), bf["x"], None, W, U, b, None, None, bf["y"], bf["hT"],
+                             bf["cT"], bf["ws"], stream=0)
+    assert e.value.status == J.ERR_UNSUPPORTED
+    with pytest.raises(J.JanusError) as e:
+        J.janus_lstm_seq_fwd(d, None, None, W, U, b, None, None, bf["y"], bf["hT"], bf["cT"], bf["ws"], stream=0)
+    assert e.value.status == J.ERR_INVALID_ARG
+    assert all(v.untouched() for v in bf.values())
+
+
+def test_lstm_bwd_rejects_bad_lengths_untouched():
+    d, bf, W, U, b = _lstm_args()
+    g = [_HostBuf(4 * 8 * 4 * 4) for _ in range(3)]
+    with pytest.raises(J.JanusError) as e:
+        J.janus_lstm_seq_bwd(d, bf["x"], [1, 2, 9], W, U, bf["ws"], bf["y"], None, None, None, None, None,
+                             [g[0]], [g[1]], [g[2]], stream=0)
+    assert e.value.status == J.ERR_LENGTH
+    assert all(v.untouched() for v in bf.values()) and all(v.untouched() for v in g)
+
+
+def test_tree_calls_reject_malformed_trees_untouched():
+    left, right, word, root = _tree([-1, -1, 0], [-1, -1, -1], [1, 2, -1], [2])
+    t = wl.TreeBatch(left, right, word, root)
+    E, H, V = 4, 3, 5
+    need = J.janus_treelstm_workspace_bytes(E, H, V, J.F32, 3, 1)
+    bufs = [_HostBuf(n) for n in (V * E * 4, 5 * H * E * 4, 5 * H * 2 * H * 4, 5 * H * 4, H * 4, need)]
+    with pytest.raises(J.JanusError) as e:
+        J.janus_treelstm_fwd(J.TreeDesc(E, H, V, J.F32), t, *bufs, stream=0)
+    assert e.value.status == J.ERR_TREE
+    assert all(v.untouched() for v in bufs)
+    t2 = wl.TreeBatch(*_tree([-1, -1, 0], [-1, -1, 1], [1, 7, -1], [2]))
+    with pytest.raises(J.JanusError) as e:
+        J.janus_treelstm_fwd(J.TreeDesc(E, H, V, J.F32), t2, *bufs, stream=0)
+    assert e.value.status == J.ERR_TOKEN
+    with pytest.raises(J.JanusError) as e:
+        J.janus_treelstm_fwd(J.TreeDesc(E, H, V, J.BF16), wl.TreeBatch(*_tree([-1], [-1], [1], [0])), *bufs, stream=0)
+    assert e.value.status == J.ERR_UNSUPPORTED
+    assert all(v.untouched() for v in bufs)
+
+
+def test_xent_rejects_bad_ids_untouched():
+    V, H, R = 10, 4, 6
+    d = J.XentDesc(V, H, R, J.F32)
+    bufs = dict(table=_HostBuf(V * H * 4), bias=_HostBuf(V * 4), inp=_HostBuf(R * H * 4), out=_HostBuf(R * H * 4),
+                dtable=_HostBuf(V * H * 4), dbias=_HostBuf(V * 4), loss=_HostBuf(4),
+                ws=_HostBuf(J.janus_xent_workspace_bytes(V, H, R, J.F32, J.XENT_FWD_BWD)))
+    ids_dev = _HostBuf(R * 4)
+    for op in (J.EMBED_FWD, J.XENT_FWD_BWD, J.EMBED_BWD):
+        with pytest.raises(J.JanusError) as e:
+            J.janus_embed_softmax_xent(d, op, np.array([0, 1, 2, 10, 3, 4]), ids_dev, stream=0, **bufs)
+        assert e.value.status == J.ERR_TOKEN
+        with pytest.raises(J.JanusError) as e:
+            J.janus_embed_softmax_xent(d, op, np.array([0, 1, -2, 1, 3, 4]), ids_dev, stream=0, **bufs)
+        assert e.value.status == J.ERR_TOKEN
+    assert all(v.untouched() for v in bufs.values()) and ids_dev.untouched()
+
+
+def test_workspace_sizes_monotone():
+    a = J.janus_lstm_workspace_bytes(1, 32, 64, 4, 16, J.F32)
+    b = J.janus_lstm_workspace_bytes(1, 32, 64, 4, 32, J.F32)
+    c = J.janus_lstm_workspace_bytes(2, 32, 64, 4, 32, J.F32)
+    assert 0 < a < b < c
+    assert J.janus_lstm_workspace_bytes(0, 32, 64, 4, 16, J.F32) == 0

@@ -1,0 +1,181 @@
+"""GPU parity: the HIP path through the C ABI against the float64 oracle on
+the same seeded inputs, element by element, at the path's tolerances."""
+import sys
+
+import numpy as np
+import pytest
+
+from oracle import steps as oracle_steps
+from paper_1812_01329_amd import workloads as wl
+from tests.parity import TOL, check, compare_lstm
+
+pytestmark = pytest.mark.gpu
+
+
+def _run(w):
+    import torch
+    from paper_1812_01329_amd.train_step import make_step
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    print(f"[parity] {w.name} dtype={w.dtype}", flush=True)
+    step = make_step(w)
+    step.run()
+    return step, step.results()
+
+
+def _lstm(head, dtype, L, I, H, B, T, lengths=None, seed=0, h0=False, V=50, P=24, scale=None):
+    rng = np.random.default_rng(seed)
+    a = scale if scale is not None else 1.0 / np.sqrt(H)
+    rnd = lambda shape, s: wl.bf16_round(rng.uniform(-s, s, shape).astype(np.float32)) if dtype == "bf16" \
+        else rng.uniform(-s, s, shape).astype(np.float32)
+    Wx = [rnd((4 * H, I if l == 0 else H), a) for l in range(L)]
+    Wh = [rnd((4 * H, H), a) for l in range(L)]
+    b = [rnd((4 * H,), a) for l in range(L)]
+    x = rnd((T, B, I), 1.0)
+    w = wl.LSTMWorkload(f"lstm-{head}-{dtype}-L{L}I{I}H{H}B{B}T{T}", dtype, L, I, H, B, T, x,
+                        None if lengths is None else np.asarray(lengths, np.int32), Wx, Wh, b, head)
+    if head == "xent":
+        w.V = V
+        w.tokens = rng.integers(0, V, (B, T + 1)).astype(np.int32)
+        w.E = rnd((V, I), 0.5)
+        w.Wout = rnd((V, H), 0.5)
+        w.bout = rnd((V,), 0.5)
+        w.x = None
+    if head == "mse":
+        w.Wout = rnd((P, H), a)
+        w.bout = rnd((P,), a)
+        w.target = rnd((T, B, P), 1.0)
+    if h0:
+        w.h0 = rng.uniform(-0.5, 0.5, (L, B, H)).astype(np.float32)
+        w.c0 = rng.uniform(-0.5, 0.5, (L, B, H)).astype(np.float32)
+    return w
+
+
+# ---------------------------------------------------------------- the five workloads
+def test_tiny_fixed_length_fp32():
+    w = wl.tiny_lstm()
+    _, g = _run(w)
+    compare_lstm(g, oracle_steps.lstm_step(w), "f32")
+
+
+def test_ptb_language_model_bf16():
+    w = wl.ptb_lstm()
+    _, g = _run(w)
+    r = oracle_steps.lstm_step(w)
+    compare_lstm(g, r, "bf16", with_dx=False)
+
+
+def test_varlen_masked_loop_bf16():
+    w = wl.varlen_lstm()
+    _, g = _run(w)
+    r = oracle_steps.lstm_step(w)
+    compare_lstm(g, r, "bf16")
+    # positions past each sequence's end are exactly zero
+    T = w.T
+    mask = np.arange(T)[:, None] >= w.lengths[None, :]
+    assert np.all(g["y"][mask] == 0.0)
+    assert np.all(g["dx"][mask] == 0.0)
+
+
+def test_treelstm_fp32():
+    w = wl.sst_treelstm()
+    _, g = _run(w)
+    r = oracle_steps.tree_step(w)
+    t = TOL["f32"]
+    check("loss", np.array([g["loss"]]), np.array([r["loss"]]), t["out"])
+    check("h_root", g["h_root"], r["h_root"], t["out"])
+    for k in ("dh_root", "dWs", "dbs", "dW", "dU", "db", "demb"):
+        check(k, g[k], r[k], t["grad"])
+    H = w.H
+    assert np.all(g["dW"][H:3 * H] == 0.0)   # forget rows of W see no gradient
+
+
+def test_lm2048_reduced_shape_bf16():
+    """The regression workload's structure (2 layers, projection + MSE) at a
+    shape the oracle runs in seconds, spanning several tiles with ragged tails."""
+    w = wl.lm2048_lstm(T=12, B=70, H=200, I=136, P=72)
+    _, g = _run(w)
+    compare_lstm(g, oracle_steps.lstm_step(w), "bf16", with_dx=False)
+
+
+# ---------------------------------------------------------------- edge cases
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+@pytest.mark.parametrize("head,lengths", [
+    ("sumsq", None),
+    ("mean_final", [7, 0, 3, 7, 1]),
+    ("mse", [1, 1, 1, 1, 1]),
+    ("sumsq", [0, 0, 0, 0, 0]),
+    ("xent", None),
+])
+def test_ragged_shapes(dtype, head, lengths):
+    w = _lstm(head, dtype, L=2, I=13, H=37, B=5, T=7, lengths=lengths, seed=7, h0=(head != "xent"))
+    _, g = _run(w)
+    compare_lstm(g, oracle_steps.lstm_step(w), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_multi_tile_varlen(dtype):
+    """Rows and hidden units spanning several tiles, with a ragged tail."""
+    rng = np.random.default_rng(3)
+    lengths = rng.integers(0, 20, 150)
+    w = _lstm("mean_final", dtype, L=2, I=72, H=104, B=150, T=19, lengths=lengths, seed=3, h0=True)
+    _, g = _run(w)
+    compare_lstm(g, oracle_steps.lstm_step(w), dtype)
+
+
+def test_one_step_sequences():
+    w = _lstm("sumsq", "f32", L=1, I=8, H=16, B=3, T=1, seed=5, h0=True)
+    _, g = _run(w)
+    compare_lstm(g, oracle_steps.lstm_step(w), "f32")
+
+
+def test_single_leaf_and_chain_trees():
+    left, right, word, roots = [], [], [], []
+    rng = np.random.default_rng(1)
+    # a one-leaf tree, a left chain of 12 leaves and a balanced 16-leaf tree
+    roots.append(wl.random_bracketing(rng, 1, np.array([3]), left, right, word))
+    n0 = len(left)
+    prev = None
+    for k in range(12):
+        left.append(-1); right.append(-1); word.append(int(rng.integers(0, 40)))
+        leaf = len(left) - 1
+        if prev is None:
+            prev = leaf
+        else:
+            left.append(prev); right.append(leaf); word.append(-1)
+            prev = len(left) - 1
+    roots.append(prev)
+    roots.append(wl.random_bracketing(rng, 16, rng.integers(0, 40, 16), left, right, word))
+    trees = wl.TreeBatch(np.asarray(left, np.int32), np.asarray(right, np.int32), np.asarray(word, np.int32),
+                         np.asarray(roots, np.int32))
+    base = wl.sst_treelstm(n_trees=2, E=24, H=20, V=40, seed=9)
+    base.trees = trees
+    base.labels = rng.integers(0, base.C, trees.num_trees).astype(np.int32)
+    _, g = _run(base)
+    r = oracle_steps.tree_step(base)
+    check("h_root", g["h_root"], r["h_root"], 1e-4)
+    for k in ("dW", "dU", "db", "demb"):
+        check(k, g[k], r[k], 1e-3)
+
+
+def test_deterministic_repeat():
+    """Two runs of the same step give identical bits."""
+    w = wl.varlen_lstm(T=30, B=40, I=64, H=96)
+    step, g1 = _run(w)
+    step.run()
+    g2 = step.results()
+    for k in ("y", "hT", "dx", "dh0"):
+        assert np.array_equal(g1[k], g2[k]), k
+    for k in ("dWx", "dWh", "db"):
+        for a, b in zip(g1[k], g2[k]):
+            assert np.array_equal(a, b), k
+
+
+def test_batch_permutation_on_device():
+    w = _lstm("mse", "bf16", L=1, I=32, H=64, B=9, T=6, lengths=[6, 2, 5, 0, 3, 6, 1, 4, 2], seed=2, h0=True)
+    _, g1 = _run(w)
+    p = np.array([3, 8, 0, 2, 7, 1, 5, 6, 4])
+    w.x = w.x[:, p]; w.lengths = w.lengths[p]; w.target = w.target[:, p]; w.h0 = w.h0[:, p]; w.c0 = w.c0[:, p]
+    _, g2 = _run(w)
+    np.testing.assert_allclose(g2["y"], g1["y"][:, p], rtol=0, atol=1e-6)
+    assert abs(g1["loss"] - g2["loss"]) <= 1e-4 * abs(g1["loss"])
+    assert check("dWh-perm", g2["dWh"][0], g1["dWh"][0], 1e-3) <= 1e-3
