@@ -279,6 +279,36 @@ janus_status janus_loss_reduce(janus_loss_kind kind, const float* h, int64_t n,
                                float* loss, float* dh, void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Tracing                                                                  */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * Per-kernel timing of the library's own launches.  Between
+ * janus_trace_begin and janus_trace_end every kernel the library enqueues is
+ * bracketed by two HIP events recorded on the stream it is launched on.
+ * janus_trace_end waits for those events and returns one record per kernel
+ * label, in order of first launch: the launch count, the summed event time
+ * and the summed algorithmic work of the launches (2*M*N*K flops for a
+ * contraction, bytes a kernel must move at minimum for memory-bound ones).
+ * Tracing adds two event records per launch; it is meant for measurement
+ * runs, not for the timed loop.  Not thread-safe against concurrent calls
+ * from other threads.
+ *  out: caller array of max_out records; n_out receives the number of labels
+ *  (records beyond max_out are dropped).
+ * Errors: INVALID_ARG (NULL n_out), DEVICE (an event call failed).
+ */
+typedef struct {
+    char label[48];
+    int64_t launches;
+    double total_ms;
+    double flops;
+    double bytes;
+} janus_trace_stat;
+
+janus_status janus_trace_begin(void);
+janus_status janus_trace_end(janus_trace_stat* out, int32_t max_out, int32_t* n_out);
+
+/* ------------------------------------------------------------------------ */
 /* Misc                                                                     */
 /* ------------------------------------------------------------------------ */
 const char* janus_status_string(janus_status s);

@@ -159,23 +159,24 @@ struct LoaderK {
     }
 };
 
-// Operand whose row index is contiguous in memory (a transposed view):
-// elem(r, k) = p[krow(k) * ld + r0 + r], krow = identity or an index array.
-// Each task reads KB consecutive k rows of VEC contiguous elements and
-// writes them transposed into the k-contiguous tile.
+// Transposed operand read in square VEC x VEC blocks: each task loads VEC
+// consecutive k rows of VEC contiguous elements (16 bytes each) and writes
+// VEC rows of VEC consecutive k values (16 bytes each) into the k-contiguous
+// tile, transposing in registers.  elem(r, k) = p[krow(k) * ld + r0 + r].
 template <typename T, int ROWS, int BK, int NT, bool AL>
-struct LoaderR {
+struct LoaderT {
     static constexpr int VEC = 16 / sizeof(T);
-    static constexpr int KB = 4;
     static constexpr int RCH = ROWS / VEC;
-    static constexpr int TASKS = RCH * (BK / KB);
+    static constexpr int KCH = BK / VEC;
+    static constexpr int TASKS = RCH * KCH;
     static constexpr int PER = (TASKS + NT - 1) / NT;
     static constexpr int LD = BK + Lds<T>::PAD;
+    static_assert(ROWS % VEC == 0 && BK % VEC == 0, "tile must be a multiple of the vector width");
     const T* base;
     int64_t ld;
     const int32_t* kidx;
-    int rbase, nrows;            // global first row of the tile, total rows
-    uint4 r[PER][KB];
+    int rbase, nrows;
+    uint4 r[PER][VEC];
 
     __device__ __forceinline__ void init(const T* b, int64_t l, const int32_t* ki, int r0, int n) {
         base = b; ld = l; kidx = ki; rbase = r0; nrows = n;
@@ -183,16 +184,17 @@ struct LoaderR {
     __device__ __forceinline__ void load(int k0, int K, int tid) {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
-            int c = tid + i * NT;
-            int rc = (c % RCH) * VEC;
-            int kb = (c / RCH) * KB;
+            const int c = tid + i * NT;
+            const int rc = (c % RCH) * VEC;
+            const int kb = (c / RCH) * VEC;
+            const int gr = rbase + rc;
+            const bool task = (TASKS % NT == 0 || c < TASKS);
 #pragma unroll
-            for (int j = 0; j < KB; ++j) {
+            for (int j = 0; j < VEC; ++j) {
                 uint4 v = make_uint4(0, 0, 0, 0);
-                int k = k0 + kb + j;
-                int gr = rbase + rc;
-                if ((TASKS % NT == 0 || c < TASKS) && k < K && gr < nrows) {
-                    int64_t krow = kidx ? int64_t(kidx[k]) : int64_t(k);
+                const int k = k0 + kb + j;
+                if (task && k < K && gr < nrows) {
+                    const int64_t krow = kidx ? int64_t(kidx[k]) : int64_t(k);
                     const T* p = base + krow * ld + gr;
                     if (AL && gr + VEC <= nrows) {
                         v = *reinterpret_cast<const uint4*>(p);
@@ -210,18 +212,27 @@ struct LoaderR {
     __device__ __forceinline__ void store(T* s, int tid) const {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
-            int c = tid + i * NT;
+            const int c = tid + i * NT;
             if (!(TASKS % NT == 0 || c < TASKS)) continue;
-            int rc = (c % RCH) * VEC;
-            int kb = (c / RCH) * KB;
-            const T* src[KB];
+            const int rc = (c % RCH) * VEC;
+            const int kb = (c / RCH) * VEC;
+            const uint32_t* w[VEC];
 #pragma unroll
-            for (int j = 0; j < KB; ++j) src[j] = reinterpret_cast<const T*>(&r[i][j]);
+            for (int j = 0; j < VEC; ++j) w[j] = reinterpret_cast<const uint32_t*>(&r[i][j]);
 #pragma unroll
             for (int e = 0; e < VEC; ++e) {
-                T* d = s + (rc + e) * LD + kb;
+                uint4 o;
+                uint32_t* od = reinterpret_cast<uint32_t*>(&o);
+                if constexpr (sizeof(T) == 2) {
+                    const int sh = 16 * (e & 1);
 #pragma unroll
-                for (int j = 0; j < KB; ++j) d[j] = src[j][e];
+                    for (int d = 0; d < 4; ++d)
+                        od[d] = ((w[2 * d][e >> 1] >> sh) & 0xffffu) | (((w[2 * d + 1][e >> 1] >> sh) & 0xffffu) << 16);
+                } else {
+#pragma unroll
+                    for (int d = 0; d < 4; ++d) od[d] = w[d][e];
+                }
+                *reinterpret_cast<uint4*>(s + (rc + e) * LD + kb) = o;
             }
         }
     }
@@ -281,6 +292,58 @@ __device__ __forceinline__ void mma_mainloop(f32x16_t (&acc)[Cfg::FM][Cfg::FN], 
 #pragma unroll
                 for (int j = 0; j < Cfg::FN; ++j) mfma(acc[i][j], fa[i], fb[j]);
         }
+    }
+}
+
+// Double-buffered variant: two LDS stages, one barrier per k tile.  The
+// next tile's global loads are in flight while the current tile is
+// multiplied; `smem` holds 2 * (BM + BN) * LD elements.
+template <class Cfg, typename T, class LA, class LB>
+__device__ __forceinline__ void mma_mainloop_db(f32x16_t (&acc)[Cfg::FM][Cfg::FN], LA& la, LB& lb, int K, T* smem,
+                                                int tid) {
+    constexpr int STAGE = (Cfg::BM + Cfg::BN) * Cfg::LD;
+    const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+    if (K <= 0) return;
+    const int row_in = lane & 31, kq = (lane >> 5) * 8;
+    const int a_off = (Cfg::wave_row0(wave) + row_in) * Cfg::LD + kq;
+    const int b_off = Cfg::BM * Cfg::LD + (Cfg::wave_col0(wave) + row_in) * Cfg::LD + kq;
+    la.load(0, K, tid);
+    lb.load(0, K, tid);
+    la.store(smem, tid);
+    lb.store(smem + Cfg::BM * Cfg::LD, tid);
+    __syncthreads();
+    const int nk = (K + Cfg::BK - 1) / Cfg::BK;
+    for (int it = 0; it < nk; ++it) {
+        T* cur = smem + (it & 1) * STAGE;
+        T* nxt = smem + ((it + 1) & 1) * STAGE;
+        const bool more = it + 1 < nk;
+        if (more) {
+            la.load((it + 1) * Cfg::BK, K, tid);
+            lb.load((it + 1) * Cfg::BK, K, tid);
+        }
+#pragma unroll
+        for (int ks = 0; ks < Cfg::BK / 16; ++ks) {
+            Frag<T> fa[Cfg::FM], fb[Cfg::FN];
+#pragma unroll
+            for (int i = 0; i < Cfg::FM; ++i) fa[i].load(cur + a_off + i * 32 * Cfg::LD + ks * 16);
+#pragma unroll
+            for (int j = 0; j < Cfg::FN; ++j) fb[j].load(cur + b_off + j * 32 * Cfg::LD + ks * 16);
+#pragma unroll
+            for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < Cfg::FN; ++j) mfma(acc[i][j], fa[i], fb[j]);
+        }
+        if (more) {
+            la.store(nxt, tid);
+            lb.store(nxt + Cfg::BM * Cfg::LD, tid);
+        }
+        __syncthreads();
     }
 }
 

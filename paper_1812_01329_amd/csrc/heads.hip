@@ -230,6 +230,9 @@ janus_status mse_impl(const janus_mse_desc& d, const void* h, const void* W, con
                       void* dh, float* dW, float* db, float* loss, const MseWs& w, hipStream_t st) {
     const float count = float(int64_t(d.rows) * d.P);
     dim3 grid((d.P + Cfg::BN - 1) / Cfg::BN, (d.rows + Cfg::BM - 1) / Cfg::BM);
+    {
+    TraceScope trace("mse_gemm", 2.0 * d.rows * double(d.P) * d.H,
+                     double(sizeof(T)) * (double(d.rows) * d.H + double(d.P) * d.H + 2.0 * d.rows * double(d.P)), st);
     const bool al = (int64_t(d.H) * int64_t(sizeof(T))) % 16 == 0 && reinterpret_cast<uintptr_t>(h) % 16 == 0 &&
                     reinterpret_cast<uintptr_t>(W) % 16 == 0;
     if (al)
@@ -241,7 +244,11 @@ janus_status mse_impl(const janus_mse_desc& d, const void* h, const void* W, con
                            d.H, static_cast<const T*>(h), static_cast<const T*>(W), static_cast<const T*>(b),
                            static_cast<const T*>(tgt), static_cast<T*>(w.dY), 2.f / count, w.part);
     JANUS_LAUNCH_CHECK();
+    }
+    {
+    TraceScope trace("finish_sum", 0.0, 4.0 * w.nparts, st);
     hipLaunchKernelGGL(finish_sum_kernel, dim3(1), dim3(1024), 0, st, w.part, int64_t(w.nparts), 1.f / count, loss);
+    }
     JANUS_LAUNCH_CHECK();
     // dh = dY W
     GemmDesc g;
@@ -298,12 +305,18 @@ janus_status xent_impl(const janus_xent_desc& d, const int32_t* ids_dev, const v
     g.bias = bout;
     janus_status e = gemm(g, st);
     if (e != JANUS_OK) return e;
-    hipLaunchKernelGGL(xent_row_kernel<T>, dim3(d.rows), dim3(256), 0, st, w.logits, w.ldv, ids_dev, d.V, d.rows,
-                       static_cast<T*>(w.dz), w.ldv, w.loss_rows);
-    JANUS_LAUNCH_CHECK();
-    hipLaunchKernelGGL(finish_sum_kernel, dim3(1), dim3(1024), 0, st, w.loss_rows, int64_t(d.rows),
-                       1.f / float(d.rows), loss);
-    JANUS_LAUNCH_CHECK();
+    {
+        TraceScope trace_row("xent_row", 0.0, double(d.rows) * d.V * (4.0 + sizeof(T)), st);
+        hipLaunchKernelGGL(xent_row_kernel<T>, dim3(d.rows), dim3(256), 0, st, w.logits, w.ldv, ids_dev, d.V, d.rows,
+                           static_cast<T*>(w.dz), w.ldv, w.loss_rows);
+        JANUS_LAUNCH_CHECK();
+    }
+    {
+        TraceScope trace_fin("finish_sum", 0.0, 4.0 * d.rows, st);
+        hipLaunchKernelGGL(finish_sum_kernel, dim3(1), dim3(1024), 0, st, w.loss_rows, int64_t(d.rows),
+                           1.f / float(d.rows), loss);
+        JANUS_LAUNCH_CHECK();
+    }
     // dh = dz Wout
     GemmDesc q;
     q.dtype = d.dtype;
@@ -349,6 +362,7 @@ janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_d
     if (e != JANUS_OK) return e;
     if (rows <= 0) return JANUS_OK;
     const size_t sm = size_t(rows) * sizeof(int32_t);
+    TraceScope trace("embed_bwd", 0.0, double(rows) * H * (4.0 + dtype_size(dt)), st);
     if (dt == JANUS_BF16)
         hipLaunchKernelGGL(embed_bwd_kernel<bf16_t>, dim3(rows), dim3(256), sm, st, static_cast<const bf16_t*>(dx),
                            ids_dev, rows, V, H, dE);
@@ -392,6 +406,7 @@ extern "C" janus_status janus_embed_softmax_xent(const janus_xent_desc* d, janus
     hipStream_t st = static_cast<hipStream_t>(stream);
     const size_t es = dtype_size(d->dtype);
     if (op == JANUS_EMBED_FWD) {
+        TraceScope trace("embed_fwd", 0.0, 2.0 * d->rows * double(d->H) * es, st);
         const bool vec = (int64_t(d->H) * int64_t(es)) % 16 == 0 && reinterpret_cast<uintptr_t>(table) % 16 == 0 &&
                          reinterpret_cast<uintptr_t>(out) % 16 == 0;
         if (d->dtype == JANUS_BF16) {
@@ -444,6 +459,7 @@ extern "C" janus_status janus_loss_reduce(janus_loss_kind kind, const float* h, 
     if (!h || !loss || n <= 0) return JANUS_ERR_INVALID_ARG;
     if (kind != JANUS_LOSS_SUMSQ && kind != JANUS_LOSS_MEAN) return JANUS_ERR_INVALID_ARG;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    TraceScope trace("loss_reduce", 0.0, 4.0 * n * (dh ? 2.0 : 1.0), st);
     hipLaunchKernelGGL(loss_reduce_kernel, dim3(1), dim3(1024), 0, st, int(kind), h, n, loss);
     JANUS_LAUNCH_CHECK();
     if (dh) {

@@ -33,6 +33,7 @@
 #include <vector>
 
 #include "device.hpp"
+#include "lstm_persist.hpp"
 #include "ops.hpp"
 
 namespace janus {
@@ -51,6 +52,14 @@ struct LstmWs {
     float* dh = nullptr;
     float* dc = nullptr;
     float* part = nullptr;
+    // persistent path
+    std::vector<void*> Wxi;             // per layer: Wx with gate-interleaved rows
+    std::vector<void*> bi;              // per layer: b, gate-interleaved
+    int32_t* perm4 = nullptr;           // [4H] interleaved row -> gate-major row
+    int32_t* act_dev = nullptr;         // [T + 1]
+    int32_t* off_dev = nullptr;         // [T + 2]
+    float* dpart = nullptr;             // [4 x B x H] partial recurrent gradients
+    persist::Sync* sync = nullptr;
     int64_t ldh = 0, ldg = 0;
 };
 
@@ -76,7 +85,86 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     w.dh = c.take<float>(int64_t(d.B) * d.H);
     w.dc = c.take<float>(int64_t(d.B) * d.H);
     w.part = c.take<float>(colsum_partial_floats(4 * d.H));
+    w.Wxi.assign(d.L, nullptr);
+    w.bi.assign(d.L, nullptr);
+    for (int l = 0; l < d.L; ++l) {
+        const int64_t Il = l == 0 ? d.I : d.H;
+        w.Wxi[l] = c.take<char>(int64_t(4) * d.H * Il * es);
+        w.bi[l] = c.take<char>(int64_t(4) * d.H * es);
+    }
+    w.perm4 = c.take<int32_t>(int64_t(4) * d.H);
+    w.act_dev = c.take<int32_t>(int64_t(d.T) + 1);
+    w.off_dev = c.take<int32_t>(int64_t(d.T) + 2);
+    w.dpart = c.take<float>(int64_t(persist::kSlices) * d.B * d.H);
+    w.sync = c.take<persist::Sync>(16);
     return c.off + 256;
+}
+
+// ------------------------------------------------------- persistent path
+struct DeviceInfo {
+    int cus = 0;
+    int coop = 0;
+    size_t lds = 0;
+};
+
+DeviceInfo device_info() {
+    static DeviceInfo cache[64];
+    static bool have[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DeviceInfo{};
+    if (!have[dev]) {
+        DeviceInfo d;
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) d.cus = v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess) d.coop = v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess) d.lds = size_t(v);
+        cache[dev] = d;
+        have[dev] = true;
+    }
+    return cache[dev];
+}
+
+int persist_kw(int B) { return B <= 32 ? 8 : B <= 64 ? 4 : B <= 128 ? 2 : 1; }
+
+size_t persist_red_bytes(int kw) { return size_t(kw - 1) * (persist::kWaves / kw) * 4096; }
+
+size_t persist_fwd_lds(const janus_lstm_desc& d) {
+    return size_t(32) * (round_up(d.H, 64) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
+}
+size_t persist_bwd_lds(const janus_lstm_desc& d) {
+    return size_t(persist::kUnitsBwd) * (round_up(d.H, 64) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
+}
+int persist_fwd_blocks(const janus_lstm_desc& d) { return (d.H + persist::kUnitsFwd - 1) / persist::kUnitsFwd; }
+int persist_bwd_blocks(const janus_lstm_desc& d) {
+    return persist::kSlices * ((d.H + persist::kUnitsBwd - 1) / persist::kUnitsBwd);
+}
+
+// The persistent path needs bf16, H a multiple of 8, at most 256 rows, one
+// co-resident workgroup per slice and the weight slice in LDS.  It can be
+// switched off with JANUS_PERSIST=0 (the per-step kernels then run).
+bool use_persistent(const janus_lstm_desc& d) {
+    const char* e = getenv("JANUS_PERSIST");
+    const bool env = !(e && e[0] == '0');
+    if (!env || d.dtype != JANUS_BF16 || d.H % 8 != 0 || d.B > persist::kMaxB) return false;
+    const DeviceInfo info = device_info();
+    if (!info.coop || info.cus <= 0) return false;
+    if (persist_fwd_blocks(d) > info.cus || persist_bwd_blocks(d) > info.cus) return false;
+    const size_t lds = info.lds > 0 ? info.lds : 65536;
+    return persist_fwd_lds(d) <= lds && persist_bwd_lds(d) <= lds;
+}
+
+__global__ void perm4_kernel(int H, int32_t* perm4) {
+    const int n = blockIdx.x * blockDim.x + threadIdx.x;
+    if (n < 4 * H) perm4[n] = (n & 3) * H + (n >> 2);
+}
+
+// dst row n (interleaved) = src row (n % 4) * H + n / 4, rows of `cols` elements
+template <typename T>
+__global__ void interleave_rows_kernel(const T* src, T* dst, int H, int cols) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(4) * H * cols) return;
+    const int n = int(i / cols), k = int(i % cols);
+    dst[i] = src[(int64_t(n & 3) * H + (n >> 2)) * cols + k];
 }
 
 // ------------------------------------------------------------ init kernels
@@ -218,7 +306,7 @@ __global__ __launch_bounds__(Cfg::NT) void bwd_step_kernel(BwdStep<T> a) {
 
     // dh_rec[r, u] = sum_k dG_{t+1}[r, k] Wh[k, u]   (k over the 4H gate rows)
     LoaderK<T, Cfg::BM, Cfg::BK, Cfg::NT, AL> la;
-    LoaderR<T, Cfg::BN, Cfg::BK, Cfg::NT, AL> lb;
+    LoaderT<T, Cfg::BN, Cfg::BK, Cfg::NT, AL> lb;
     la.init(a.G + (a.off_next + m0) * a.ldg, a.ldg, 0, RowsContig{a.active_next - m0}, tid);
     lb.init(a.Wh, H, nullptr, u0, H);
     f32x16_t acc[Cfg::FM][Cfg::FN];
@@ -285,6 +373,9 @@ constexpr int step_smem() {
 template <typename T, class Cfg>
 janus_status launch_fwd_step(const FwdStep<T>& a, bool al, hipStream_t s) {
     dim3 grid((a.H + a.U - 1) / a.U, (a.active + Cfg::BM - 1) / Cfg::BM);
+    TraceScope trace(sizeof(T) == 2 ? "lstm_fwd_step_bf16" : "lstm_fwd_step_f32",
+                     2.0 * a.active * 4.0 * a.H * a.H,
+                     double(sizeof(T)) * (double(a.active) * a.H + 4.0 * a.H * a.H), s);
     if (al)
         hipLaunchKernelGGL((fwd_step_kernel<T, Cfg, true>), grid, dim3(Cfg::NT), step_smem<Cfg>(), s, a);
     else
@@ -297,6 +388,9 @@ template <typename T, class Cfg>
 janus_status launch_bwd_step(const BwdStep<T>& a, bool al, hipStream_t s) {
     dim3 grid((a.H + Cfg::BN - 1) / Cfg::BN, (a.active + Cfg::BM - 1) / Cfg::BM);
     if (grid.y == 0) return JANUS_OK;
+    TraceScope trace(sizeof(T) == 2 ? "lstm_bwd_step_bf16" : "lstm_bwd_step_f32",
+                     2.0 * a.active_next * 4.0 * a.H * a.H,
+                     double(sizeof(T)) * (4.0 * a.active_next * a.H + 4.0 * a.H * a.H), s);
     if (al)
         hipLaunchKernelGGL((bwd_step_kernel<T, Cfg, true>), grid, dim3(Cfg::NT), step_smem<Cfg>(), s, a);
     else
@@ -324,6 +418,118 @@ bool weight_aligned(const janus_lstm_desc& d) {
     return (int64_t(d.H) * int64_t(dtype_size(d.dtype))) % 16 == 0;
 }
 
+template <class K>
+janus_status coop_launch(K kernel, int blocks, size_t smem, void* arg, hipStream_t st, bool& attr_done) {
+    if (!attr_done) {
+        if (hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                int(smem)) != hipSuccess)
+            return JANUS_ERR_DEVICE;
+        attr_done = true;
+    }
+    void* args[] = {arg};
+    if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), dim3(blocks), dim3(persist::kThreads), args,
+                                   unsigned(smem), st) != hipSuccess)
+        return JANUS_ERR_DEVICE;
+    return JANUS_OK;
+}
+
+janus_status launch_fwd_persistent(const janus_lstm_desc& d, persist::FwdArgs& a, double flops, hipStream_t st) {
+    static bool attr[4] = {};
+    const int kw = persist_kw(d.B);
+    const size_t smem = persist_fwd_lds(d);
+    const int blocks = persist_fwd_blocks(d);
+    TraceScope trace("lstm_fwd_persistent", flops, 0.0, st);
+    switch (kw) {
+        case 1: return coop_launch(persist::lstm_fwd_persistent<1>, blocks, smem, &a, st, attr[0]);
+        case 2: return coop_launch(persist::lstm_fwd_persistent<2>, blocks, smem, &a, st, attr[1]);
+        case 4: return coop_launch(persist::lstm_fwd_persistent<4>, blocks, smem, &a, st, attr[2]);
+        default: return coop_launch(persist::lstm_fwd_persistent<8>, blocks, smem, &a, st, attr[3]);
+    }
+}
+
+janus_status launch_bwd_persistent(const janus_lstm_desc& d, persist::BwdArgs& a, double flops, hipStream_t st) {
+    static bool attr[4] = {};
+    const int kw = persist_kw(d.B);
+    const size_t smem = persist_bwd_lds(d);
+    const int blocks = persist_bwd_blocks(d);
+    TraceScope trace("lstm_bwd_persistent", flops, 0.0, st);
+    switch (kw) {
+        case 1: return coop_launch(persist::lstm_bwd_persistent<1>, blocks, smem, &a, st, attr[0]);
+        case 2: return coop_launch(persist::lstm_bwd_persistent<2>, blocks, smem, &a, st, attr[1]);
+        case 4: return coop_launch(persist::lstm_bwd_persistent<4>, blocks, smem, &a, st, attr[2]);
+        default: return coop_launch(persist::lstm_bwd_persistent<8>, blocks, smem, &a, st, attr[3]);
+    }
+}
+
+// sum over steps of rows with a recurrent product: forward rows t < t_eff,
+// backward rows of the contractions from dG_{t+1}
+double recurrent_rows(const SeqSchedule& s) {
+    double r = 0;
+    for (int t = 0; t < s.t_eff; ++t) r += s.active[t];
+    return r;
+}
+
+// One layer of the forward pass on the persistent path (bf16 only).
+janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s, const LstmWs& w, int l,
+                                  const void* x, const int32_t* xrow, const void* Wx, const void* Wh, const void* b,
+                                  const int32_t* perm, void* y, float* hT, float* cT, hipStream_t st) {
+    const int H = d.H, B = d.B;
+    const int Il = l == 0 ? d.I : H;
+    const int64_t rows4 = int64_t(4) * H * Il;
+    {
+        TraceScope trace("interleave_weights", 0.0, 4.0 * double(rows4 + 4 * H), st);
+        hipLaunchKernelGGL(interleave_rows_kernel<bf16_t>, dim3(unsigned((rows4 + 255) / 256)), dim3(256), 0, st,
+                           static_cast<const bf16_t*>(Wx), static_cast<bf16_t*>(w.Wxi[l]), H, Il);
+        JANUS_LAUNCH_CHECK();
+        hipLaunchKernelGGL(interleave_rows_kernel<bf16_t>, dim3(unsigned((4 * H + 255) / 256)), dim3(256), 0, st,
+                           static_cast<const bf16_t*>(b), static_cast<bf16_t*>(w.bi[l]), H, 1);
+        JANUS_LAUNCH_CHECK();
+    }
+    GemmDesc g;
+    g.dtype = JANUS_BF16;
+    g.M = int(s.packed);
+    g.N = 4 * H;
+    g.K = Il;
+    if (l == 0) {
+        g.A = x;
+        g.lda = d.I;
+        g.a_idx = xrow;
+    } else {
+        g.A = static_cast<const bf16_t*>(w.Hs[l - 1]) + int64_t(B) * w.ldh;
+        g.lda = w.ldh;
+    }
+    g.B = w.Wxi[l];
+    g.ldb = Il;
+    g.C = w.XG;
+    g.ldc = w.ldg;
+    g.c_f32 = false;
+    g.bias = w.bi[l];
+    janus_status e = gemm(g, st);
+    if (e != JANUS_OK) return e;
+    if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;
+    persist::FwdArgs a;
+    a.H = H;
+    a.B = B;
+    a.t_eff = s.t_eff;
+    a.fixed = s.fixed ? 1 : 0;
+    a.Kp = int(round_up(H, 64));
+    a.active = w.act_dev;
+    a.offsets = w.off_dev;
+    a.perm = perm;
+    a.Wh = static_cast<const bf16_t*>(Wh);
+    a.Hs = static_cast<bf16_t*>(w.Hs[l]);
+    a.Cs = w.Cs[l];
+    a.XG = static_cast<const bf16_t*>(w.XG);
+    a.Gs = static_cast<bf16_t*>(w.Gs[l]);
+    a.y = static_cast<bf16_t*>(y);
+    a.hT = hT;
+    a.cT = cT;
+    a.ldh = w.ldh;
+    a.ldg = w.ldg;
+    a.sync = w.sync;
+    return launch_fwd_persistent(d, a, 2.0 * 4.0 * H * double(H) * recurrent_rows(s), st);
+}
+
 template <typename T, class Cfg>
 janus_status lstm_fwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const LstmWs& w, const void* x,
                            const void* const* Wx, const void* const* Wh, const void* const* b, const float* h0,
@@ -337,13 +543,25 @@ janus_status lstm_fwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         if (e != JANUS_OK) return e;
     }
     const bool al = weight_aligned(d);
+    const bool persistent = use_persistent(d);
     for (int l = 0; l < d.L; ++l) {
         const int64_t bh = int64_t(B) * H;
-        hipLaunchKernelGGL(fwd_init_kernel<T>, dim3(unsigned((bh + 255) / 256)), dim3(256), 0, st, B, H, w.ldh, perm,
-                           h0 ? h0 + l * bh : nullptr, c0 ? c0 + l * bh : nullptr, static_cast<T*>(w.Hs[l]),
-                           w.Cs[l], s.active[0], hT ? hT + l * bh : nullptr, cT ? cT + l * bh : nullptr);
-        JANUS_LAUNCH_CHECK();
+        {
+            TraceScope trace("lstm_fwd_init", 0.0, double(bh) * (8.0 + 4.0 + sizeof(T)), st);
+            hipLaunchKernelGGL(fwd_init_kernel<T>, dim3(unsigned((bh + 255) / 256)), dim3(256), 0, st, B, H, w.ldh,
+                               perm, h0 ? h0 + l * bh : nullptr, c0 ? c0 + l * bh : nullptr,
+                               static_cast<T*>(w.Hs[l]), w.Cs[l], s.active[0], hT ? hT + l * bh : nullptr,
+                               cT ? cT + l * bh : nullptr);
+            JANUS_LAUNCH_CHECK();
+        }
         if (s.packed == 0) continue;
+        if (persistent) {
+            janus_status e = fwd_layer_persistent(d, s, w, l, x, xrow, Wx[l], Wh[l], b[l], perm,
+                                                  l == d.L - 1 ? y : nullptr, hT ? hT + l * bh : nullptr,
+                                                  cT ? cT + l * bh : nullptr, st);
+            if (e != JANUS_OK) return e;
+            continue;
+        }
         // hoisted input projection of every running (t, b)
         GemmDesc g;
         g.dtype = d.dtype;
@@ -410,11 +628,58 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         if (e != JANUS_OK) return e;
     }
     const int64_t bh = int64_t(B) * H;
+    const bool persistent = use_persistent(d);
+    if (persistent) {
+        TraceScope trace("perm4", 0.0, 16.0 * H, st);
+        hipLaunchKernelGGL(perm4_kernel, dim3(unsigned((4 * H + 255) / 256)), dim3(256), 0, st, H, w.perm4);
+        JANUS_LAUNCH_CHECK();
+    }
     for (int l = d.L - 1; l >= 0; --l) {
         const bool top = l == d.L - 1;
+        if (persistent) {
+            janus_status e = zero_fill(w.sync, sizeof(persist::Sync), st);
+            if (e != JANUS_OK) return e;
+            persist::BwdArgs a;
+            a.H = H;
+            a.B = B;
+            a.t_eff = s.t_eff;
+            a.fixed = s.fixed ? 1 : 0;
+            a.Ks = H;
+            a.Ksp = int(round_up(H, 64));
+            a.active = w.act_dev;
+            a.offsets = w.off_dev;
+            a.perm = perm;
+            a.Wh = static_cast<const bf16_t*>(Wh[l]);
+            a.G = static_cast<bf16_t*>(w.XG);
+            a.Gs = static_cast<const bf16_t*>(w.Gs[l]);
+            a.Cs = w.Cs[l];
+            if (top) {
+                a.dy = static_cast<const bf16_t*>(dy);
+                a.dy_ld = H;
+                a.dy_rows = xrow;
+            } else {
+                a.dy = static_cast<const bf16_t*>(w.dY);
+                a.dy_ld = w.ldh;
+                a.dy_rows = nullptr;
+            }
+            a.dhT = dhT ? dhT + l * bh : nullptr;
+            a.dcT = dcT ? dcT + l * bh : nullptr;
+            a.dh0 = dh0 ? dh0 + l * bh : nullptr;
+            a.dc0 = dc0 ? dc0 + l * bh : nullptr;
+            a.part = w.dpart;
+            a.ldh = w.ldh;
+            a.ldg = w.ldg;
+            a.sync = w.sync;
+            double rows = 0;
+            for (int t = 0; t < s.t_eff; ++t) rows += s.active[t];
+            if ((e = launch_bwd_persistent(d, a, 2.0 * 4.0 * H * double(H) * rows, st)) != JANUS_OK) return e;
+        } else {
+        {
+        TraceScope trace("lstm_bwd_init", 0.0, double(bh) * 16.0, st);
         hipLaunchKernelGGL(bwd_init_kernel, dim3(unsigned((bh + 255) / 256)), dim3(256), 0, st, B, H, perm,
                            dhT ? dhT + l * bh : nullptr, dcT ? dcT + l * bh : nullptr, w.dh, w.dc);
         JANUS_LAUNCH_CHECK();
+        }
         BwdStep<T> a;
         a.H = H;
         a.B = B;
@@ -458,6 +723,8 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             janus_status e = launch_bwd_step<T, Cfg>(a, al, st);
             if (e != JANUS_OK) return e;
         }
+        }
+        const int32_t* rowmap = persistent ? w.perm4 : nullptr;   // interleaved gate rows -> torch rows
         const int Il = l == 0 ? d.I : H;
         // dWx = dG^T X
         GemmDesc g;
@@ -479,6 +746,7 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         }
         g.C = dWx[l];
         g.ldc = Il;
+        g.c_idx = rowmap;
         g.c_f32 = true;
         janus_status e = gemm(g, st);
         if (e != JANUS_OK) return e;
@@ -491,7 +759,7 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         g.ldc = H;
         e = gemm(g, st);
         if (e != JANUS_OK) return e;
-        e = colsum(d.dtype, w.XG, s.packed, 4 * H, w.ldg, db[l], w.part, st);
+        e = colsum(d.dtype, w.XG, s.packed, 4 * H, w.ldg, db[l], w.part, st, rowmap);
         if (e != JANUS_OK) return e;
         // gradient of this layer's input: dG Wx
         if (l > 0 || dx) {
@@ -503,7 +771,7 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             q.A = w.XG;
             q.lda = w.ldg;
             q.b_t = true;
-            q.B = Wx[l];
+            q.B = persistent ? w.Wxi[l] : Wx[l];
             q.ldb = Il;
             q.c_f32 = false;
             if (l > 0) {
@@ -529,8 +797,11 @@ janus_status upload_schedule(const SeqSchedule& s, const LstmWs& w, hipStream_t 
         e = upload(w.xrow, s.xrow.data(), sizeof(int32_t) * s.packed, st);
         if (e != JANUS_OK) return e;
         e = upload(w.prevrow, s.prevrow.data(), sizeof(int32_t) * s.packed, st);
+        if (e != JANUS_OK) return e;
     }
-    return e;
+    e = upload(w.act_dev, s.active.data(), sizeof(int32_t) * (s.T + 1), st);
+    if (e != JANUS_OK) return e;
+    return upload(w.off_dev, s.offsets.data(), sizeof(int32_t) * (s.T + 2), st);
 }
 
 }  // namespace

@@ -39,7 +39,7 @@ janus_status gemm(const GemmDesc& g, hipStream_t stream);
 // colsum_partial_floats(C) floats.
 size_t colsum_partial_floats(int C);
 janus_status colsum(janus_dtype dt, const void* in, int64_t R, int C, int64_t ld, float* out,
-                    float* partial, hipStream_t stream);
+                    float* partial, hipStream_t stream, const int32_t* out_idx = nullptr);
 
 // clear `bytes` bytes of device memory (a kernel, so it may be captured)
 janus_status zero_fill(void* p, size_t bytes, hipStream_t stream);

@@ -84,7 +84,116 @@ janus_status upload(void* dst_dev, const void* src_host, size_t bytes, hipStream
     return ring().put(dst_dev, src_host, bytes, stream);
 }
 
+// ------------------------------------------------------------------ tracing
+namespace {
+
+struct TraceRec {
+    const char* label;
+    double flops, bytes;
+    hipEvent_t start, stop;
+};
+
+struct TraceState {
+    std::mutex mu;
+    bool on = false;
+    bool failed = false;
+    std::vector<TraceRec> recs;
+    std::vector<hipEvent_t> pool;
+
+    hipEvent_t get() {
+        if (!pool.empty()) {
+            hipEvent_t e = pool.back();
+            pool.pop_back();
+            return e;
+        }
+        hipEvent_t e = nullptr;
+        if (hipEventCreate(&e) != hipSuccess) {
+            failed = true;
+            return nullptr;
+        }
+        return e;
+    }
+};
+
+TraceState& trace() {
+    static TraceState t;
+    return t;
+}
+
+}  // namespace
+
+TraceScope::TraceScope(const char* label, double flops, double bytes, hipStream_t stream) {
+    TraceState& t = trace();
+    if (!t.on) return;
+    std::lock_guard<std::mutex> lock(t.mu);
+    hipEvent_t a = t.get(), b = t.get();
+    if (!a || !b) return;
+    if (hipEventRecord(a, stream) != hipSuccess) {
+        t.failed = true;
+        return;
+    }
+    t.recs.push_back({label, flops, bytes, a, b});
+    slot_ = int(t.recs.size()) - 1;
+    stream_ = stream;
+}
+
+TraceScope::~TraceScope() {
+    if (slot_ < 0) return;
+    TraceState& t = trace();
+    std::lock_guard<std::mutex> lock(t.mu);
+    if (hipEventRecord(t.recs[slot_].stop, stream_) != hipSuccess) t.failed = true;
+}
+
 }  // namespace janus
+
+extern "C" janus_status janus_trace_begin(void) {
+    janus::TraceState& t = janus::trace();
+    std::lock_guard<std::mutex> lock(t.mu);
+    for (auto& r : t.recs) {
+        t.pool.push_back(r.start);
+        t.pool.push_back(r.stop);
+    }
+    t.recs.clear();
+    t.failed = false;
+    t.on = true;
+    return JANUS_OK;
+}
+
+extern "C" janus_status janus_trace_end(janus_trace_stat* out, int32_t max_out, int32_t* n_out) {
+    if (!n_out) return JANUS_ERR_INVALID_ARG;
+    janus::TraceState& t = janus::trace();
+    std::lock_guard<std::mutex> lock(t.mu);
+    t.on = false;
+    std::vector<janus_trace_stat> agg;
+    janus_status st = t.failed ? JANUS_ERR_DEVICE : JANUS_OK;
+    for (auto& r : t.recs) {
+        float ms = 0.f;
+        if (hipEventSynchronize(r.stop) != hipSuccess || hipEventElapsedTime(&ms, r.start, r.stop) != hipSuccess) {
+            st = JANUS_ERR_DEVICE;
+            continue;
+        }
+        janus_trace_stat* s = nullptr;
+        for (auto& a : agg)
+            if (std::strncmp(a.label, r.label, sizeof(a.label)) == 0) s = &a;
+        if (!s) {
+            agg.push_back(janus_trace_stat{});
+            s = &agg.back();
+            std::strncpy(s->label, r.label, sizeof(s->label) - 1);
+        }
+        s->launches += 1;
+        s->total_ms += ms;
+        s->flops += r.flops;
+        s->bytes += r.bytes;
+    }
+    for (auto& r : t.recs) {
+        t.pool.push_back(r.start);
+        t.pool.push_back(r.stop);
+    }
+    t.recs.clear();
+    *n_out = int32_t(agg.size());
+    for (int32_t i = 0; i < int32_t(agg.size()) && i < max_out && out; ++i) out[i] = agg[i];
+    return st;
+}
 
 extern "C" const char* janus_status_string(janus_status s) {
     switch (s) {

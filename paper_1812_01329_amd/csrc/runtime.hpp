@@ -60,6 +60,20 @@ inline bool dtype_ok(janus_dtype d) { return d == JANUS_F32 || d == JANUS_BF16; 
 // the copy stays asynchronous on the caller's stream.
 janus_status upload(void* dst_dev, const void* src_host, size_t bytes, hipStream_t stream);
 
+// Brackets one kernel launch with trace events while tracing is on (see
+// janus_trace_begin); a no-op otherwise.  flops / bytes: algorithmic work.
+class TraceScope {
+  public:
+    TraceScope(const char* label, double flops, double bytes, hipStream_t stream);
+    ~TraceScope();
+    TraceScope(const TraceScope&) = delete;
+    TraceScope& operator=(const TraceScope&) = delete;
+
+  private:
+    int slot_ = -1;
+    hipStream_t stream_ = nullptr;
+};
+
 #define JANUS_HIP(call)                                        \
     do {                                                       \
         if ((call) != hipSuccess) return JANUS_ERR_DEVICE;     \

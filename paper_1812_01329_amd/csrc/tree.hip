@@ -178,7 +178,7 @@ __global__ __launch_bounds__(Cfg::NT) void tree_dh_kernel(int p0, int rows, int 
     const int n0 = blockIdx.x * Cfg::BN, m0 = blockIdx.y * Cfg::BM;
     const int N = 2 * H;
     LoaderK<float, Cfg::BM, Cfg::BK, Cfg::NT, AL> la;
-    LoaderR<float, Cfg::BN, Cfg::BK, Cfg::NT, AL> lb;
+    LoaderT<float, Cfg::BN, Cfg::BK, Cfg::NT, AL> lb;
     la.init(dA + int64_t(p0 + m0) * ld5, ld5, 0, RowsContig{rows - m0}, tid);
     lb.init(U, N, nullptr, n0, N);
     f32x16_t acc[Cfg::FM][Cfg::FN];
@@ -284,6 +284,7 @@ extern "C" janus_status janus_treelstm_fwd(const janus_treelstm_desc* d, const j
         g.bias = b;
         if ((e = gemm(g, st)) != JANUS_OK) return e;
         const int64_t n = int64_t(rows) * H;
+        TraceScope trace("tree_fwd_point", 0.0, 4.0 * n * 14.0, st);
         hipLaunchKernelGGL(tree_fwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H, M0,
                            w.ld5, w.A, w.G, w.C, w.lchild, w.rchild, w.parent, w.rootk, w.HLR,
                            static_cast<float*>(h_root));
@@ -307,18 +308,26 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
     if ((e = upload_tree(t, s, w, st)) != JANUS_OK) return e;
     const int H = d->H, E = d->E, N = s.N;
     const int64_t kh = int64_t(t->num_trees) * H;
+    {
+    TraceScope trace("tree_bwd_init", 0.0, 12.0 * kh, st);
     hipLaunchKernelGGL(tree_bwd_init_kernel, dim3(unsigned((kh + 255) / 256)), dim3(256), 0, st, t->num_trees, H,
                        w.rootpos, static_cast<const float*>(dh_root), w.dh, w.dc);
     JANUS_LAUNCH_CHECK();
+    }
     const bool al = (int64_t(2) * H * 4) % 16 == 0 && reinterpret_cast<uintptr_t>(U) % 16 == 0;
     for (int k = s.num_levels - 1; k >= 0; --k) {
         const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
         const int64_t n = int64_t(rows) * H;
+        {
+        TraceScope trace("tree_bwd_point", 0.0, 4.0 * n * 17.0, st);
         hipLaunchKernelGGL(tree_bwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H,
                            w.ld5, w.G, w.C, w.dh, w.dc, w.lchild, w.rchild, w.A);
         JANUS_LAUNCH_CHECK();
+        }
         if (k == 0) break;
         dim3 grid((2 * H + TreeCfg::BN - 1) / TreeCfg::BN, (rows + TreeCfg::BM - 1) / TreeCfg::BM);
+        TraceScope trace("tree_dh_gemm", 2.0 * rows * 2.0 * H * 5.0 * H,
+                         4.0 * (double(rows) * 5 * H + 10.0 * H * H + 2.0 * rows * H), st);
         if (al)
             hipLaunchKernelGGL((tree_dh_kernel<TreeCfg, true>), grid, dim3(TreeCfg::NT), TreeCfg::SMEM_BYTES, st, p0,
                                rows, H, w.ld5, w.A, static_cast<const float*>(U), w.lchild, w.rchild, w.dh);

@@ -28,8 +28,8 @@ EXPORTS = [
     "janus_lstm_workspace_bytes", "janus_lstm_seq_fwd", "janus_lstm_seq_bwd", "janus_lstm_schedule",
     "janus_treelstm_workspace_bytes", "janus_tree_schedule_build", "janus_treelstm_fwd",
     "janus_treelstm_bwd", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
-    "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_status_string",
-    "janus_version",
+    "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
+    "janus_trace_end", "janus_status_string", "janus_version",
 ]
 
 
@@ -56,6 +56,11 @@ class TreeBatchC(C.Structure):
 
 class XentDesc(C.Structure):
     _fields_ = [("V", C.c_int32), ("H", C.c_int32), ("rows", C.c_int32), ("dtype", C.c_int)]
+
+
+class TraceStat(C.Structure):
+    _fields_ = [("label", C.c_char * 48), ("launches", C.c_int64), ("total_ms", C.c_double),
+                ("flops", C.c_double), ("bytes", C.c_double)]
 
 
 class MseDesc(C.Structure):
@@ -97,6 +102,8 @@ def lib():
         L.janus_mse_workspace_bytes.argtypes = [C.POINTER(MseDesc)]
         L.janus_linear_mse.argtypes = [C.POINTER(MseDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
         L.janus_loss_reduce.argtypes = [C.c_int, vp, i64, vp, vp, vp]
+        L.janus_trace_begin.argtypes = []
+        L.janus_trace_end.argtypes = [C.POINTER(TraceStat), i32, C.POINTER(C.c_int32)]
         for name in EXPORTS:
             if name not in ("janus_status_string", "janus_version") and "workspace_bytes" not in name:
                 getattr(L, name).restype = C.c_int
@@ -246,3 +253,17 @@ def janus_linear_mse(desc: MseDesc, h, W, b, target, dh, dW, db, loss, ws, strea
 def janus_loss_reduce(kind, h, n, loss, dh, stream=None):
     st = lib().janus_loss_reduce(kind, _p(h), n, _p(loss), _p(dh), _stream(stream))
     _check(st, "janus_loss_reduce")
+
+
+# ---------------------------------------------------------------- tracing
+def janus_trace_begin():
+    _check(lib().janus_trace_begin(), "janus_trace_begin")
+
+
+def janus_trace_end(max_out: int = 128):
+    """Per-label kernel statistics of the launches since janus_trace_begin."""
+    out = (TraceStat * max_out)()
+    n = C.c_int32(0)
+    _check(lib().janus_trace_end(out, max_out, C.byref(n)), "janus_trace_end")
+    return [dict(label=out[i].label.decode(), launches=int(out[i].launches), total_ms=float(out[i].total_ms),
+                 flops=float(out[i].flops), bytes=float(out[i].bytes)) for i in range(min(n.value, max_out))]

@@ -179,3 +179,17 @@ def test_batch_permutation_on_device():
     np.testing.assert_allclose(g2["y"], g1["y"][:, p], rtol=0, atol=1e-6)
     assert abs(g1["loss"] - g2["loss"]) <= 1e-4 * abs(g1["loss"])
     assert check("dWh-perm", g2["dWh"][0], g1["dWh"][0], 1e-3) <= 1e-3
+
+
+@pytest.mark.parametrize("persist", ["0", "1"])
+@pytest.mark.parametrize("lengths", [None, "ragged"])
+def test_both_recurrence_paths(persist, lengths, monkeypatch):
+    """bf16 LSTM through the per-step kernels (JANUS_PERSIST=0) and through the
+    persistent kernels, each against the oracle."""
+    monkeypatch.setenv("JANUS_PERSIST", persist)
+    rng = np.random.default_rng(11)
+    B = 96
+    lens = None if lengths is None else rng.integers(0, 13, B)
+    w = _lstm("mse", "bf16", L=2, I=64, H=128, B=B, T=12, lengths=lens, seed=11, h0=True, P=40)
+    _, g = _run(w)
+    compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
