@@ -104,12 +104,26 @@ struct RowsGateMajor {       // rows g * H + u0 + j of a [4H or 5H, K] gate-majo
 };
 
 // ---------------------------------------------------------- tile loaders
+// Swizzled (unpadded) LDS tile: rows of BK elements split into CPR 16-byte
+// chunks; chunk q of row r lives at chunk q ^ ((r ^ (r >> 3)) & (CPR - 1)).
+// K-contiguous stores (8 lanes per row), transposed block stores (lanes 8
+// rows apart) and MFMA fragment reads (32 consecutive rows) then all spread
+// over distinct banks.
+template <typename T, int BK>
+struct Swz {
+    static constexpr int VEC = 16 / sizeof(T);
+    static constexpr int CPR = BK / VEC;
+    static_assert((CPR & (CPR - 1)) == 0, "chunks per row must be a power of two");
+    __device__ static __forceinline__ int sw(int row) { return (row ^ (row >> 3)) & (CPR - 1); }
+    __device__ static __forceinline__ int off(int row, int chunk) { return row * BK + ((chunk ^ sw(row)) * VEC); }
+};
+
 // Shared-memory tiles are stored [rows][BK + PAD] with k contiguous so that
 // every MFMA fragment is one 16- or 32-byte LDS read.
 template <typename T> struct Lds { static constexpr int PAD = 16 / sizeof(T); };
 
 // Operand whose k index is contiguous in memory: elem(r, k) = p[row(r) * ld + k].
-template <typename T, int ROWS, int BK, int NT, bool AL>
+template <typename T, int ROWS, int BK, int NT, bool AL, bool SWZ = false>
 struct LoaderK {
     static constexpr int VEC = 16 / sizeof(T);
     static constexpr int CPR = BK / VEC;
@@ -153,8 +167,10 @@ struct LoaderK {
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
             int c = tid + i * NT;
-            if (CH % NT == 0 || c < CH)
-                *reinterpret_cast<uint4*>(s + (c / CPR) * LD + (c % CPR) * VEC) = r[i];
+            if (CH % NT == 0 || c < CH) {
+                const int o = SWZ ? Swz<T, BK>::off(c / CPR, c % CPR) : (c / CPR) * LD + (c % CPR) * VEC;
+                *reinterpret_cast<uint4*>(s + o) = r[i];
+            }
         }
     }
 };
@@ -163,7 +179,7 @@ struct LoaderK {
 // consecutive k rows of VEC contiguous elements (16 bytes each) and writes
 // VEC rows of VEC consecutive k values (16 bytes each) into the k-contiguous
 // tile, transposing in registers.  elem(r, k) = p[krow(k) * ld + r0 + r].
-template <typename T, int ROWS, int BK, int NT, bool AL>
+template <typename T, int ROWS, int BK, int NT, bool AL, bool SWZ = false>
 struct LoaderT {
     static constexpr int VEC = 16 / sizeof(T);
     static constexpr int RCH = ROWS / VEC;
@@ -232,7 +248,8 @@ struct LoaderT {
 #pragma unroll
                     for (int d = 0; d < 4; ++d) od[d] = w[d][e];
                 }
-                *reinterpret_cast<uint4*>(s + (rc + e) * LD + kb) = o;
+                const int so = SWZ ? Swz<T, BK>::off(rc + e, kb / VEC) : (rc + e) * LD + kb;
+                *reinterpret_cast<uint4*>(s + so) = o;
             }
         }
     }
@@ -342,6 +359,70 @@ __device__ __forceinline__ void mma_mainloop_db(f32x16_t (&acc)[Cfg::FM][Cfg::FN
         if (more) {
             la.store(nxt, tid);
             lb.store(nxt + Cfg::BM * Cfg::LD, tid);
+        }
+        __syncthreads();
+    }
+}
+
+// Double-buffered main loop over swizzled, unpadded LDS tiles (bf16).
+// `smem` holds 2 * (BM + BN) * BK elements.
+template <class Cfg, class LA, class LB>
+__device__ __forceinline__ void mma_mainloop_swz(f32x16_t (&acc)[Cfg::FM][Cfg::FN], LA& la, LB& lb, int K,
+                                                 bf16_t* smem, int tid) {
+    using S = Swz<bf16_t, Cfg::BK>;
+    constexpr int STAGE = (Cfg::BM + Cfg::BN) * Cfg::BK;
+    const int lane = tid & 63, wave = tid >> 6;
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < Cfg::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+    if (K <= 0) return;
+    int arow[Cfg::FM], asw[Cfg::FM], brow[Cfg::FN], bsw[Cfg::FN];
+#pragma unroll
+    for (int i = 0; i < Cfg::FM; ++i) {
+        const int r = Cfg::wave_row0(wave) + i * 32 + (lane & 31);
+        arow[i] = r * Cfg::BK;
+        asw[i] = S::sw(r);
+    }
+#pragma unroll
+    for (int j = 0; j < Cfg::FN; ++j) {
+        const int r = Cfg::wave_col0(wave) + j * 32 + (lane & 31);
+        brow[j] = Cfg::BM * Cfg::BK + r * Cfg::BK;
+        bsw[j] = S::sw(r);
+    }
+    const int kh = lane >> 5;
+    la.load(0, K, tid);
+    lb.load(0, K, tid);
+    la.store(smem, tid);
+    lb.store(smem + Cfg::BM * Cfg::BK, tid);
+    __syncthreads();
+    const int nk = (K + Cfg::BK - 1) / Cfg::BK;
+    for (int it = 0; it < nk; ++it) {
+        bf16_t* cur = smem + (it & 1) * STAGE;
+        bf16_t* nxt = smem + ((it + 1) & 1) * STAGE;
+        const bool more = it + 1 < nk;
+        if (more) {
+            la.load((it + 1) * Cfg::BK, K, tid);
+            lb.load((it + 1) * Cfg::BK, K, tid);
+        }
+#pragma unroll
+        for (int ks = 0; ks < Cfg::BK / 16; ++ks) {
+            const int q = 2 * ks + kh;
+            Frag<bf16_t> fa[Cfg::FM], fb[Cfg::FN];
+#pragma unroll
+            for (int i = 0; i < Cfg::FM; ++i) fa[i].load(cur + arow[i] + ((q ^ asw[i]) << 3));
+#pragma unroll
+            for (int j = 0; j < Cfg::FN; ++j) fb[j].load(cur + brow[j] + ((q ^ bsw[j]) << 3));
+#pragma unroll
+            for (int i = 0; i < Cfg::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < Cfg::FN; ++j) mfma(acc[i][j], fa[i], fb[j]);
+        }
+        if (more) {
+            la.store(nxt, tid);
+            lb.store(nxt + Cfg::BM * Cfg::BK, tid);
         }
         __syncthreads();
     }

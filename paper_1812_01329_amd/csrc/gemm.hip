@@ -113,10 +113,10 @@ void gemm_big_kernel(GemmDesc g, int mtiles, int ntiles) {
     const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
     const bf16_t* A = static_cast<const bf16_t*>(g.A);
     const bf16_t* B = static_cast<const bf16_t*>(g.B);
-    using LA = typename std::conditional<AT, LoaderT<bf16_t, Cfg::BM, Cfg::BK, Cfg::NT, AL>,
-                                         LoaderK<bf16_t, Cfg::BM, Cfg::BK, Cfg::NT, AL>>::type;
-    using LB = typename std::conditional<BT, LoaderT<bf16_t, Cfg::BN, Cfg::BK, Cfg::NT, AL>,
-                                         LoaderK<bf16_t, Cfg::BN, Cfg::BK, Cfg::NT, AL>>::type;
+    using LA = typename std::conditional<AT, LoaderT<bf16_t, Cfg::BM, Cfg::BK, Cfg::NT, AL, true>,
+                                         LoaderK<bf16_t, Cfg::BM, Cfg::BK, Cfg::NT, AL, true>>::type;
+    using LB = typename std::conditional<BT, LoaderT<bf16_t, Cfg::BN, Cfg::BK, Cfg::NT, AL, true>,
+                                         LoaderK<bf16_t, Cfg::BN, Cfg::BK, Cfg::NT, AL, true>>::type;
     LA la;
     LB lb;
     if constexpr (AT) {
@@ -132,7 +132,7 @@ void gemm_big_kernel(GemmDesc g, int mtiles, int ntiles) {
         else lb.init(B + int64_t(n0) * g.ldb, g.ldb, 0, RowsContig{g.N - n0}, tid);
     }
     f32x16_t acc[Cfg::FM][Cfg::FN];
-    mma_mainloop_db<Cfg>(acc, la, lb, g.K, smem, tid);
+    mma_mainloop_swz<Cfg>(acc, la, lb, g.K, smem, tid);
     store_tile<bf16_t, Cfg>(g, acc, m0, n0, tid);
 }
 
@@ -155,7 +155,7 @@ janus_status launch(const GemmDesc& g, hipStream_t s) {
 
 template <class Cfg, bool AT, bool BT, bool AL>
 janus_status launch_big(const GemmDesc& g, hipStream_t s) {
-    constexpr int smem = 2 * (Cfg::BM + Cfg::BN) * Cfg::LD * int(sizeof(bf16_t));
+    constexpr int smem = 2 * (Cfg::BM + Cfg::BN) * Cfg::BK * int(sizeof(bf16_t));
     static bool attr = false;
     if (!attr) {
         if (hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_big_kernel<Cfg, AT, BT, AL>),

@@ -67,8 +67,9 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     Carver c(base);
     const size_t es = dtype_size(d.dtype);
     const int64_t TB = int64_t(d.T) * d.B;
-    w.ldh = round_up(d.H, 8);
-    w.ldg = round_up(int64_t(4) * d.H, 8);
+    // rows padded to whole 128-byte lines (see the persistent kernels' barrier)
+    w.ldh = round_up(d.H, 64);
+    w.ldg = round_up(int64_t(4) * d.H, 64);
     w.perm = c.take<int32_t>(d.B);
     w.xrow = c.take<int32_t>(TB);
     w.prevrow = c.take<int32_t>(TB);

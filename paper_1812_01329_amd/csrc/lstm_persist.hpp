@@ -39,31 +39,87 @@ constexpr int kMaxB = 256;             // batch rows handled by one pass of 8 wa
 constexpr int kCellsPerThread = 4;     // (kMaxB * 8 units) / kThreads
 constexpr int kSpinLimit = 1 << 22;    // bounded wait at each barrier (~0.1 s)
 
+// Device-wide barrier state (zeroed before every launch).  Counters sit in
+// separate 256-byte lines.
 struct Sync {
-    unsigned count;                    // arrivals, monotonically increasing within a launch
+    unsigned count;                    // global arrivals (census first, then one per XCD per barrier)
     unsigned error;                    // set when a wait exceeds its spin limit
+    unsigned pad0[62];
+    unsigned xcd[16][64];              // per-XCD arrivals
+    unsigned census[16][64];           // workgroups resident on each XCD
 };
 
-// Device-wide barrier for a cooperative launch of `nblocks` workgroups.
-// `phase` counts barriers passed so far; after a timeout every later wait
-// returns at once so that all waves still reach the end of the kernel.
-__device__ __forceinline__ void grid_barrier(Sync* s, unsigned nblocks, unsigned& phase) {
-    ++phase;
+__device__ __forceinline__ unsigned xcc_id() {
+    // hardware register XCC_ID (20), bits [3:0]: the XCD this wave runs on
+    return __builtin_amdgcn_s_getreg(20 | (0 << 6) | (3 << 11)) & 0xfu;
+}
+
+// Per-workgroup barrier bookkeeping, meaningful in thread 0 only.
+struct Barrier {
+    Sync* s;
+    unsigned x, xsize, nx, nb, phase;
+};
+
+__device__ __forceinline__ bool spin_until(Sync* s, const unsigned* p, unsigned target) {
+    int spins = 0;
+    while (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
+        if (__hip_atomic_load(&s->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) return false;
+        if (++spins > kSpinLimit) {
+            __hip_atomic_store(&s->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            return false;
+        }
+    }
+    return true;
+}
+
+// Census of the workgroups on every XCD (their L2 is shared), once per launch.
+__device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
+    b.s = s;
+    b.nb = gridDim.x;
+    b.phase = 0;
+    b.x = 0;
+    b.xsize = 1;
+    b.nx = 1;
+    if (threadIdx.x == 0) {
+        b.x = xcc_id();
+        __hip_atomic_fetch_add(&s->census[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&s->count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        spin_until(s, &s->count, b.nb);
+        b.xsize = __hip_atomic_load(&s->census[b.x][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        b.nx = 0;
+        for (int q = 0; q < 16; ++q)
+            b.nx += __hip_atomic_load(&s->census[q][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+    }
+    __syncthreads();
+}
+
+// Device-wide barrier.  Workgroups on one XCD share its L2, so only the last
+// of them to arrive releases (one L2 write-back per XCD) and signals the
+// global count; every workgroup waits until all XCDs have signalled.
+//
+// There is no per-workgroup acquire (an acquire would invalidate the XCD's
+// shared L2 once per workgroup and throw away the lines the other 31
+// workgroups are reading).  This is safe because of how the kernels address
+// memory within one launch: every location one workgroup reads after a
+// barrier that another workgroup wrote before it is either (a) a row written
+// during this launch for the first time and never read before the barrier
+// (h and dG rows of a step; rows are padded to whole 128-byte lines so that
+// no line is shared between steps), so no cache can hold an old copy, or
+// (b) read with the cache-bypassing policy (the reused partial-sum buffer).
+// Caches are invalidated by the dispatch at kernel start.
+//
+// After a timeout every later wait returns at once, so all waves still
+// reach the end of the kernel (results are then garbage and `error` is set).
+__device__ __forceinline__ void grid_barrier(Barrier& b) {
+    ++b.phase;
     __syncthreads();
     if (threadIdx.x == 0) {
-        __threadfence();
-        __hip_atomic_fetch_add(&s->count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
-        const unsigned target = phase * nblocks;
-        int spins = 0;
-        while (__hip_atomic_load(&s->count, __ATOMIC_ACQUIRE, __HIP_MEMORY_SCOPE_AGENT) < target) {
-            if (__hip_atomic_load(&s->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) break;
-            __builtin_amdgcn_s_sleep(1);
-            if (++spins > kSpinLimit) {
-                __hip_atomic_store(&s->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-                break;
-            }
-        }
-        __threadfence();
+        __builtin_amdgcn_s_waitcnt(0);   // this workgroup's stores have reached the L2
+        const unsigned old =
+            __hip_atomic_fetch_add(&b.s->xcd[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (old == b.phase * b.xsize - 1u)
+            __hip_atomic_fetch_add(&b.s->count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+        spin_until(b.s, &b.s->count, b.nb + b.phase * b.nx);
     }
     __syncthreads();
 }
@@ -97,13 +153,19 @@ __device__ __forceinline__ int64_t off_at(const int32_t* offsets, int fixed, int
     return fixed ? int64_t(t) * B : int64_t(__builtin_amdgcn_readfirstlane(offsets[t]));
 }
 
-// Load rows of a gate-interleaved slice of W into LDS: LDS row i (0..31)
-// holds W row `row_of(i)` (or zeros), k contiguous, padded pitch `wld`.
+// LDS row i = 8a + 4h + b of the forward weight slice holds gate b of unit
+// 4h + a: in the 32x32 accumulator layout lane l then holds all four gates
+// of the four consecutive units 4 (l / 32) + [0, 4) of its batch row, so the
+// cell update reads and writes 16- and 32-byte pieces.
+__device__ __forceinline__ int fwd_row_unit(int i) { return 4 * ((i >> 2) & 1) + (i >> 3); }
+
+// Load the 32 rows of the forward weight slice into LDS (k contiguous,
+// padded pitch `wld`, zeros past H).
 __device__ __forceinline__ void stage_fwd_weights(const FwdArgs& a, bf16_t* Ws, int wld, int u0) {
     const int chunks = a.Kp / 8;
     for (int idx = threadIdx.x; idx < 32 * chunks; idx += kThreads) {
         const int i = idx / chunks, kc = (idx - i * chunks) * 8;
-        const int u = u0 + (i >> 2), g = i & 3;
+        const int u = u0 + fwd_row_unit(i), g = i & 3;
         uint4 v = make_uint4(0, 0, 0, 0);
         if (u < a.H && kc < a.H) {
             const bf16_t* src = a.Wh + (int64_t(g) * a.H + u) * a.H + kc;
@@ -126,15 +188,45 @@ __device__ __forceinline__ void stage_fwd_weights(const FwdArgs& a, bf16_t* Ws, 
 // without a branch; a chunk at or past `kmax` (the valid k, a multiple of 8)
 // is sent out of range the same way.  `roff` is the byte offset of element
 // (row, 32 * (lane / 32)) of this lane's row inside the descriptor.  Rows
-// stream through a ring of kDepth k-blocks kept in flight, so the memory
+// stream through a ring of DEPTH k-blocks kept in flight, so the memory
 // latency is paid once per step and each MFMA waits only for its own block.
-constexpr int kDepth = 8;
+constexpr int kDepthFwd = 8;
+constexpr int kDepthBwd = 4;
 constexpr uint32_t kOutOfRange = 0x80000000u;
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
 
 __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, uint32_t bytes) {
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, int(bytes), 0x00020000);
+}
+
+// Stores of per-step results that no other workgroup reads in this launch
+// use the sc0|sc1 cache policy (written through), so that the release at the
+// next barrier has little dirty data left to write back.
+constexpr int kStoreThrough = 1 | 16;
+constexpr int kLoadBypass = 1 | 16;    // sc0 | sc1: read from the coherence point, not the caches
+
+__device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
+    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off), 0, 0);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
+__device__ __forceinline__ float load4_bypass(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
+    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, int(off), 0, kLoadBypass));
+}
+template <int POLICY>
+__device__ __forceinline__ void store4(__amdgpu_buffer_rsrc_t rs, uint32_t off, float v) {
+    __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rs, int(off), 0, POLICY);
+}
+template <int POLICY>
+__device__ __forceinline__ void store16(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint4 v) {
+    const u32x4_t w = {v.x, v.y, v.z, v.w};
+    __builtin_amdgcn_raw_buffer_store_b128(w, rs, int(off), 0, POLICY);
+}
+template <int POLICY>
+__device__ __forceinline__ void store8(__amdgpu_buffer_rsrc_t rs, uint32_t off, uint2 v) {
+    typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
+    const u32x2_t w = {v.x, v.y};
+    __builtin_amdgcn_raw_buffer_store_b64(w, rs, int(off), 0, POLICY);
 }
 
 __device__ __forceinline__ void load_block(uint4 (&hv)[4], __amdgpu_buffer_rsrc_t rs, uint32_t roff, int kb, int kb1,
@@ -161,22 +253,23 @@ __device__ __forceinline__ void mfma_block(f32x16_t& acc, const bf16_t* wrow, co
     }
 }
 
+template <int DEPTH>
 __device__ __forceinline__ void contract_rows(f32x16_t& acc, const bf16_t* wrow, __amdgpu_buffer_rsrc_t rs,
                                               uint32_t roff, int kb0, int kb1, int kmax, int kofs) {
-    uint4 ring[kDepth][4];
+    uint4 ring[DEPTH][4];
 #pragma unroll
-    for (int i = 0; i < kDepth; ++i) load_block(ring[i], rs, roff, kb0 + i, kb1, kmax, kofs);
+    for (int i = 0; i < DEPTH; ++i) load_block(ring[i], rs, roff, kb0 + i, kb1, kmax, kofs);
     int kb = kb0;
-    for (; kb + kDepth <= kb1; kb += kDepth) {
+    for (; kb + DEPTH <= kb1; kb += DEPTH) {
 #pragma unroll
-        for (int i = 0; i < kDepth; ++i) {
+        for (int i = 0; i < DEPTH; ++i) {
             mfma_block(acc, wrow, ring[i], kb + i, kofs);
-            load_block(ring[i], rs, roff, kb + i + kDepth, kb1, kmax, kofs);
+            load_block(ring[i], rs, roff, kb + i + DEPTH, kb1, kmax, kofs);
         }
     }
-    // remaining blocks (fewer than kDepth) are already in the ring
+    // remaining blocks (fewer than DEPTH) are already in the ring
 #pragma unroll
-    for (int i = 0; i < kDepth; ++i)
+    for (int i = 0; i < DEPTH; ++i)
         if (kb + i < kb1) mfma_block(acc, wrow, ring[i], kb + i, kofs);
 }
 
@@ -218,7 +311,8 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
     const int kofs = (lane >> 5) * 32;
     const bf16_t* wrow = Ws + (lane & 31) * wld;
     const int H = a.H;
-    unsigned phase = 0;
+    Barrier bar;
+    barrier_init(bar, a.sync);
 
     stage_fwd_weights(a, Ws, wld, u0);
     __syncthreads();
@@ -229,59 +323,73 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
         const int64_t off_t = off_at(a.offsets, a.fixed, a.B, t);
         const int64_t prev_base = t == 0 ? 0 : int64_t(a.B) + off_at(a.offsets, a.fixed, a.B, t - 1);
         const int row = bt * 32 + (lane & 31);
-        // operands of the cell update do not depend on h_{t-1}: load them first
+        // operands of the cell update do not depend on h_{t-1}: load them
+        // first (branch-free; lanes without a cell read out of range, i.e. 0)
         const bool cell = kw == 0 && row < act;
+        const int ub = u0 + 4 * (lane >> 5);   // this lane's four consecutive units
         const int64_t p = off_t + row;
-        uint2 xg[4];
-        float cprev[4];
-#pragma unroll
-        for (int q = 0; q < 4; ++q) {
-            const int u = u0 + 2 * q + (lane >> 5);
-            xg[q] = make_uint2(0, 0);
-            cprev[q] = 0.f;
-            if (cell && u < H) {
-                xg[q] = *reinterpret_cast<const uint2*>(a.XG + p * a.ldg + 4 * u);
-                cprev[q] = a.Cs[(prev_base + row) * a.ldh + u];
-            }
-        }
+        const auto rxg = make_rsrc(a.XG + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
+        const auto rcp = make_rsrc(a.Cs + prev_base * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 4u);
+        const uint32_t oxg = cell ? (uint32_t(row) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u : kOutOfRange;
+        const uint32_t ocp = cell ? (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 4u : kOutOfRange;
+        const uint4 xg0 = load16(rxg, oxg), xg1 = load16(rxg, oxg + 16u);
+        const uint4 cpv = load16(rcp, ocp);
         f32x16_t acc;
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[v] = 0.f;
         if (bt * 32 < act) {
             // rows [0, act) of h_{t-1} start at Hs row prev_base
             const auto rs = make_rsrc(a.Hs + prev_base * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 2u);
-            contract_rows(acc, wrow, rs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(kofs)) * 2u, kb0, kb1, H, kofs);
+            contract_rows<kDepthFwd>(acc, wrow, rs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(kofs)) * 2u, kb0, kb1, H,
+                                     kofs);
         }
         reduce_kparts<KW>(acc, red, wave, lane);
         if (cell) {
-            const int b = a.perm ? a.perm[row] : row;
+            const uint32_t xw[8] = {xg0.x, xg0.y, xg0.z, xg0.w, xg1.x, xg1.y, xg1.z, xg1.w};
+            const float cpr[4] = {__uint_as_float(cpv.x), __uint_as_float(cpv.y), __uint_as_float(cpv.z),
+                                  __uint_as_float(cpv.w)};
+            float cn[4], hn[4];
+            uint32_t gw[8];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
-                const int u = u0 + 2 * q + (lane >> 5);
-                if (u >= H) continue;
-                const float ai = acc[4 * q + 0] + bf2f(bf16_t(xg[q].x & 0xffffu));
-                const float af = acc[4 * q + 1] + bf2f(bf16_t(xg[q].x >> 16));
-                const float ag = acc[4 * q + 2] + bf2f(bf16_t(xg[q].y & 0xffffu));
-                const float ao = acc[4 * q + 3] + bf2f(bf16_t(xg[q].y >> 16));
+                const uint32_t w0 = xw[2 * q], w1 = xw[2 * q + 1];
+                const float ai = acc[4 * q + 0] + bf2f(bf16_t(w0 & 0xffffu));
+                const float af = acc[4 * q + 1] + bf2f(bf16_t(w0 >> 16));
+                const float ag = acc[4 * q + 2] + bf2f(bf16_t(w1 & 0xffffu));
+                const float ao = acc[4 * q + 3] + bf2f(bf16_t(w1 >> 16));
                 const float gi = sigmoidf_(ai), gf = sigmoidf_(af), gg = tanhf_(ag), go = sigmoidf_(ao);
-                const float cp = cprev[q];
-                const float c = gf * cp + gi * gg;
-                const float h = go * tanhf_(c);
-                a.Cs[(a.B + p) * a.ldh + u] = c;
-                const bf16_t hb = f2bf(h);
-                a.Hs[(a.B + p) * a.ldh + u] = hb;
-                uint2 gs;
-                gs.x = uint32_t(f2bf(gi)) | (uint32_t(f2bf(gf)) << 16);
-                gs.y = uint32_t(f2bf(gg)) | (uint32_t(f2bf(go)) << 16);
-                *reinterpret_cast<uint2*>(a.Gs + p * a.ldg + 4 * u) = gs;
-                if (a.y) a.y[(int64_t(t) * a.B + b) * H + u] = hb;
-                if (row >= act_next) {
-                    if (a.hT) a.hT[int64_t(b) * H + u] = h;
-                    if (a.cT) a.cT[int64_t(b) * H + u] = c;
+                cn[q] = gf * cpr[q] + gi * gg;
+                hn[q] = go * tanhf_(cn[q]);
+                gw[2 * q] = uint32_t(f2bf(gi)) | (uint32_t(f2bf(gf)) << 16);
+                gw[2 * q + 1] = uint32_t(f2bf(gg)) | (uint32_t(f2bf(go)) << 16);
+            }
+            const uint2 hb = make_uint2(uint32_t(f2bf(hn[0])) | (uint32_t(f2bf(hn[1])) << 16),
+                                        uint32_t(f2bf(hn[2])) | (uint32_t(f2bf(hn[3])) << 16));
+            const int64_t nrow = int64_t(a.B) + off_t;   // first row of step t in Hs / Cs
+            const auto rcs = make_rsrc(a.Cs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 4u);
+            const auto rhs = make_rsrc(a.Hs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 2u);
+            const auto rgs = make_rsrc(a.Gs + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
+            store16<kStoreThrough>(rcs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 4u,
+                    make_uint4(__float_as_uint(cn[0]), __float_as_uint(cn[1]), __float_as_uint(cn[2]),
+                               __float_as_uint(cn[3])));
+            store8<kStoreThrough>(rhs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 2u, hb);
+            const uint32_t og = (uint32_t(row) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
+            store16<kStoreThrough>(rgs, og, make_uint4(gw[0], gw[1], gw[2], gw[3]));
+            store16<kStoreThrough>(rgs, og + 16u, make_uint4(gw[4], gw[5], gw[6], gw[7]));
+            const int b = a.perm ? a.perm[row] : row;
+            if (a.y) {
+                const auto ry = make_rsrc(a.y + int64_t(t) * a.B * H, uint32_t(a.B) * uint32_t(H) * 2u);
+                store8<kStoreThrough>(ry, (uint32_t(b) * uint32_t(H) + uint32_t(ub)) * 2u, hb);
+            }
+            if (row >= act_next) {   // last step of this sequence
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    if (a.hT) a.hT[int64_t(b) * H + ub + q] = hn[q];
+                    if (a.cT) a.cT[int64_t(b) * H + ub + q] = cn[q];
                 }
             }
         }
-        if (t + 1 < a.t_eff) grid_barrier(a.sync, gridDim.x, phase);
+        if (t + 1 < a.t_eff) grid_barrier(bar);
     }
 }
 
@@ -340,15 +448,17 @@ __device__ __forceinline__ void bwd_contract(const BwdArgs& a, const bf16_t* Ws,
     if (bt * 32 < rows) {
         const auto rs = make_rsrc(a.G + off * a.ldg, uint32_t(rows) * uint32_t(a.ldg) * 2u);
         const uint32_t roff = (uint32_t(row) * uint32_t(a.ldg) + uint32_t(s) * uint32_t(a.Ks) + uint32_t(kofs)) * 2u;
-        contract_rows(acc, Ws + (lane & 31) * wld, rs, roff, kb0, kb1, a.Ks, kofs);
+        contract_rows<kDepthBwd>(acc, Ws + (lane & 31) * wld, rs, roff, kb0, kb1, a.Ks, kofs);
     }
     reduce_kparts<KW>(acc, red, wave, lane);
     if (kw == 0 && row < rows) {
-        float* dst = a.part + (int64_t(s) * a.B + row) * a.H;
+        // the partial-sum buffer is rewritten every step: write through
+        const auto rp = make_rsrc(a.part + int64_t(s) * a.B * a.H, uint32_t(a.B) * uint32_t(a.H) * 4u);
 #pragma unroll
         for (int v = 0; v < 16; ++v) {
             const int u = v0 + acc_row(v, lane);
-            if (u < a.H) dst[u] = acc[v];
+            const uint32_t o = u < a.H ? (uint32_t(row) * uint32_t(a.H) + uint32_t(u)) * 4u : kOutOfRange;
+            store4<kStoreThrough>(rp, o, acc[v]);
         }
     }
 }
@@ -363,7 +473,8 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
     const int q = blockIdx.x;
     const int s = q % kSlices, v0 = (q / kSlices) * kUnitsBwd;
     const int H = a.H;
-    unsigned phase = 0;
+    Barrier bar;
+    barrier_init(bar, a.sync);
 
     stage_bwd_weights(a, Ws, wld, s, v0);
 
@@ -389,7 +500,7 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
         // partial sums of dh_t from dG_{t+1}
         if (act_next > 0) {
             bwd_contract<KW>(a, Ws, wld, red, s, v0, off_at(a.offsets, a.fixed, a.B, t + 1), act_next);
-            grid_barrier(a.sync, gridDim.x, phase);
+            grid_barrier(bar);
         }
         const int64_t off_t = t >= 0 ? off_at(a.offsets, a.fixed, a.B, t) : 0;
         const int64_t prev_base = t <= 0 ? 0 : int64_t(a.B) + off_at(a.offsets, a.fixed, a.B, t - 1);
@@ -400,9 +511,12 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             if (r >= act || u >= H) continue;
             float dhv = dhp[k];
             if (r < act_next) {
+                // reused every step: read past the caches, sum in slice order
+                const auto rp = make_rsrc(a.part, uint32_t(kSlices) * uint32_t(a.B) * uint32_t(H) * 4u);
                 dhv = 0.f;
 #pragma unroll
-                for (int j = 0; j < kSlices; ++j) dhv += a.part[(int64_t(j) * a.B + r) * H + u];
+                for (int j = 0; j < kSlices; ++j)
+                    dhv += load4_bypass(rp, ((uint32_t(j) * uint32_t(a.B) + uint32_t(r)) * uint32_t(H) + uint32_t(u)) * 4u);
             }
             if (t < 0) {
                 const int b = a.perm ? a.perm[r] : r;
@@ -427,9 +541,10 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             uint2 dg;
             dg.x = uint32_t(f2bf(dct * gg * gi * (1.f - gi))) | (uint32_t(f2bf(dct * cp * gf * (1.f - gf))) << 16);
             dg.y = uint32_t(f2bf(dct * gi * (1.f - gg * gg))) | (uint32_t(f2bf(d_o * go * (1.f - go))) << 16);
-            *reinterpret_cast<uint2*>(a.G + p * a.ldg + 4 * u) = dg;
+            const auto rg = make_rsrc(a.G + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
+            store8<kStoreThrough>(rg, (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(u)) * 2u, dg);
         }
-        if (t >= 0 && act > 0) grid_barrier(a.sync, gridDim.x, phase);
+        if (t >= 0 && act > 0) grid_barrier(bar);
     }
 }
 
