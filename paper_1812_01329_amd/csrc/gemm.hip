@@ -3,6 +3,8 @@
 // step that has no fused epilogue goes through here: the hoisted input
 // projection of all time steps, the weight gradients (one contraction over
 // all packed time steps), input gradients, and the head contractions.
+#include <algorithm>
+
 #include "device.hpp"
 #include "ops.hpp"
 
@@ -91,49 +93,240 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(GemmDesc g) {
     store_tile<T, Cfg>(g, acc, m0, n0, tid);
 }
 
-// Large bf16 contractions: 256 x 256 tiles, four waves of 128 x 128, two LDS
-// stages.  Tiles are numbered so that each XCD (blocks are dealt to the 8
-// XCDs round robin) works on a contiguous range, grouped 8 M-tiles at a time
-// so that neighbouring workgroups share B tiles in that XCD's L2.
-template <class Cfg, bool AT, bool BT, bool AL>
-__global__ __launch_bounds__(Cfg::NT) __attribute__((amdgpu_waves_per_eu(1, 1)))
-void gemm_big_kernel(GemmDesc g, int mtiles, int ntiles) {
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    bf16_t* smem = reinterpret_cast<bf16_t*>(smem_raw);
-    const int tid = threadIdx.x;
-    const int ntot = mtiles * ntiles;
-    int t = blockIdx.x;
-    if (ntot % 8 == 0) t = (t % 8) * (ntot / 8) + t / 8;
-    constexpr int GM = 8;
-    const int in_group = GM * ntiles;
+// ------------------------------------------------------------ fast NT path
+// C[M, N] = A[M, K] . B[N, K]^T for bf16 operands whose K runs contiguously
+// (rows of A and B), the one layout every large contraction of the step is
+// brought into.  256 x 256 x 64 tiles, 8 waves in a 2 x 4 grid (128 x 64
+// each), two LDS stages filled by buffer loads that write LDS directly (no
+// register staging), 16-byte chunks XOR-swizzled by row so that the MFMA
+// fragment reads are conflict-free.  Rows past M / N and k past K read as
+// zero through the buffer range check, so ragged shapes need no separate
+// path.  Optional K split: each split writes float32 partials that a second
+// kernel sums in split order (deterministic).
+struct NtCfg {
+    static constexpr int BM = 256, BN = 256, BK = 64, NSTAGE = 2, NT = 512;
+    static constexpr int WGM = 2, WGN = 4, WTM = BM / WGM, WTN = BN / WGN;
+    static constexpr int FM = WTM / 32, FN = WTN / 32;
+    static constexpr int CPR = BK / 8;                        // 16-byte chunks per tile row
+    static constexpr int RPI = 64 / CPR;                      // tile rows per wave-wide load
+    static constexpr int LOADS = BM / RPI / (NT / 64 / 2);    // loads per wave per stage
+    static constexpr int STAGE = (BM + BN) * BK;              // bf16 elements per stage
+    __device__ static __forceinline__ int wave_row0(int wave) { return (wave / WGN) * WTM; }
+    __device__ static __forceinline__ int wave_col0(int wave) { return (wave % WGN) * WTN; }
+};
+static_assert(NtCfg::LOADS == 8, "load schedule assumes 8 loads per wave per stage");
+
+struct NtArgs {
+    const bf16_t* A;
+    const bf16_t* B;
+    int64_t lda, ldb;
+    const int32_t* a_idx;       // gathered rows (whole-matrix buffer base), or NULL
+    const int32_t* b_idx;
+    int M, N, K;
+    int mt, nt, splits, ktiles_per_split;
+    float* partial;             // [splits, M, N] when splits > 1
+};
+
+constexpr uint32_t kNtOutOfRange = 0x80000000u;
+
+typedef __attribute__((address_space(3))) void* lds_ptr_t;
+
+template <typename OutT, bool SCATTER, bool PARTIAL>
+__global__ __launch_bounds__(NtCfg::NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
+void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
+    using C_ = NtCfg;
+    // The two stages are separate LDS objects and the main loop is unrolled
+    // by two, so every fragment read names the stage it reads: the compiler
+    // can then tell them apart from the direct-to-LDS loads filling the other
+    // stage and does not wait for those loads before reading.
+    __shared__ __align__(16) bf16_t stage0[C_::STAGE];
+    __shared__ __align__(16) bf16_t stage1[C_::STAGE];
+    // wave index made visibly uniform, so that everything derived from it
+    // (operand choice, buffer descriptor, LDS destinations) stays scalar
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    // block -> (split, tile): consecutive blocks go to the 8 XCDs in turn, so
+    // renumber to give each XCD a contiguous range, then walk the tiles in
+    // groups of 4 M-tiles so neighbours share B tiles in that XCD's L2
+    const int ntot = gridDim.x;
+    int b = blockIdx.x;
+    if (ntot % 8 == 0) b = (b % 8) * (ntot / 8) + b / 8;
+    const int tiles = p.mt * p.nt;
+    const int split = b / tiles;
+    const int t = b % tiles;
+    constexpr int GM = 4;
+    const int in_group = GM * p.nt;
     const int first_m = (t / in_group) * GM;
-    const int gsz = min(mtiles - first_m, GM);
-    const int tm = first_m + (t % in_group) % gsz;
-    const int tn = (t % in_group) / gsz;
-    const int m0 = tm * Cfg::BM, n0 = tn * Cfg::BN;
-    const bf16_t* A = static_cast<const bf16_t*>(g.A);
-    const bf16_t* B = static_cast<const bf16_t*>(g.B);
-    using LA = typename std::conditional<AT, LoaderT<bf16_t, Cfg::BM, Cfg::BK, Cfg::NT, AL, true>,
-                                         LoaderK<bf16_t, Cfg::BM, Cfg::BK, Cfg::NT, AL, true>>::type;
-    using LB = typename std::conditional<BT, LoaderT<bf16_t, Cfg::BN, Cfg::BK, Cfg::NT, AL, true>,
-                                         LoaderK<bf16_t, Cfg::BN, Cfg::BK, Cfg::NT, AL, true>>::type;
-    LA la;
-    LB lb;
-    if constexpr (AT) {
-        la.init(A, g.lda, g.a_idx, m0, g.M);
-    } else {
-        if (g.a_idx) la.init(A, g.lda, 0, RowsIndexed{g.a_idx + m0, g.M - m0}, tid);
-        else la.init(A + int64_t(m0) * g.lda, g.lda, 0, RowsContig{g.M - m0}, tid);
+    const int gsz = min(p.mt - first_m, GM);
+    const int m0 = (first_m + (t % in_group) % gsz) * C_::BM;
+    const int n0 = ((t % in_group) / gsz) * C_::BN;
+    const int kt0 = split * p.ktiles_per_split;
+    const int nk = max(0, min(p.ktiles_per_split, (p.K + C_::BK - 1) / C_::BK - kt0));
+
+    // this lane's loads: waves 0-3 fill the A tile, 4-7 the B tile; load j
+    // of wave w covers tile rows 64 (w % 4) + 8 j + lane / 8, physical chunk
+    // lane % 8, holding logical chunk (lane % 8) ^ (row % 8)
+    const bool isA = wave < 4;
+    const int lw = wave & 3;
+    const int row0 = isA ? m0 : n0;
+    const int rows = isA ? p.M : p.N;
+    const int64_t ld = isA ? p.lda : p.ldb;
+    const int32_t* idx = isA ? p.a_idx : p.b_idx;
+    const bf16_t* src = isA ? p.A : p.B;
+    const int kchunk = ((lane & 7) ^ (lane >> 3)) * 8;
+    uint32_t rowoff[C_::LOADS];
+#pragma unroll
+    for (int j = 0; j < C_::LOADS; ++j) {
+        const int r = lw * 64 + j * 8 + (lane >> 3);
+        const int gr = row0 + r;
+        const int64_t src_row = idx ? int64_t(idx[min(gr, rows - 1)]) : int64_t(r);
+        rowoff[j] = gr < rows ? uint32_t(src_row * ld * 2) : kNtOutOfRange;
     }
-    if constexpr (BT) {
-        lb.init(B, g.ldb, g.b_idx, n0, g.N);
-    } else {
-        if (g.b_idx) lb.init(B, g.ldb, 0, RowsIndexed{g.b_idx + n0, g.N - n0}, tid);
-        else lb.init(B + int64_t(n0) * g.ldb, g.ldb, 0, RowsContig{g.N - n0}, tid);
+    const bf16_t* base = idx ? src : src + int64_t(row0) * ld;
+    const __amdgpu_buffer_rsrc_t rs =
+        __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(base), (short)0, 0x7fffffff, 0x00020000);
+    const int lds_op = (isA ? 0 : C_::BM * C_::BK) + lw * 64 * C_::BK;
+
+    // Offsets with bit 31 set are out of range (the descriptor covers 2^31 - 1
+    // bytes and every in-range offset is below 2^31), so masking is an OR.
+    auto issue = [&](int kt, bf16_t* stage) {
+        const int k = kt * C_::BK + kchunk;
+        const uint32_t kbad = k < p.K ? 0u : kNtOutOfRange;
+        bf16_t* dst = stage + lds_op;
+#pragma unroll
+        for (int j = 0; j < C_::LOADS; ++j) {
+            const uint32_t off = (rowoff[j] + uint32_t(k) * 2u) | kbad;
+            __builtin_amdgcn_raw_ptr_buffer_load_lds(rs, (lds_ptr_t)(dst + j * 8 * C_::BK), 16, off, 0, 0, 0);
+        }
+    };
+
+    const int wr0 = C_::wave_row0(wave), wc0 = C_::wave_col0(wave);
+    f32x16_t acc[C_::FM][C_::FN];
+#pragma unroll
+    for (int i = 0; i < C_::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C_::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+    // fragment rows; the row swizzle is row % 8 = lane % 8 for every fragment
+    const int sw = lane & 7, kh = lane >> 5;
+    int arow[C_::FM], brow[C_::FN];
+#pragma unroll
+    for (int i = 0; i < C_::FM; ++i) arow[i] = (wr0 + i * 32 + (lane & 31)) * C_::BK;
+#pragma unroll
+    for (int j = 0; j < C_::FN; ++j) brow[j] = C_::BM * C_::BK + (wc0 + j * 32 + (lane & 31)) * C_::BK;
+
+    auto compute = [&](const bf16_t* cur) {
+#pragma unroll
+        for (int ks = 0; ks < C_::BK / 16; ++ks) {
+            const int q = 2 * ks + kh;
+            Frag<bf16_t> fa[C_::FM], fb[C_::FN];
+#pragma unroll
+            for (int i = 0; i < C_::FM; ++i) fa[i].load(cur + arow[i] + ((q ^ sw) << 3));
+#pragma unroll
+            for (int j = 0; j < C_::FN; ++j) fb[j].load(cur + brow[j] + ((q ^ sw) << 3));
+#pragma unroll
+            for (int i = 0; i < C_::FM; ++i)
+#pragma unroll
+                for (int j = 0; j < C_::FN; ++j) mfma(acc[i][j], fa[i], fb[j]);
+        }
+    };
+
+    // Each half: wait until this wave's loads of the current stage have
+    // landed and its reads of the other stage have returned, barrier (so the
+    // same holds for every wave), refill the other stage, compute on the
+    // current one.  The scheduling barriers keep the compiler from moving
+    // LDS reads across the barrier or sinking the refill below the compute
+    // (which would leave nothing to overlap); a plain __syncthreads would
+    // instead wait for the refill too.
+    auto sync = [&]() {
+        __builtin_amdgcn_sched_barrier(0);
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_barrier();
+    };
+    if (nk > 0) issue(kt0, stage0);
+    int it = 0;
+    for (; it + 1 < nk; it += 2) {
+        sync();
+        issue(kt0 + it + 1, stage1);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(stage0);
+        sync();
+        if (it + 2 < nk) issue(kt0 + it + 2, stage0);
+        __builtin_amdgcn_sched_barrier(0);
+        compute(stage1);
     }
-    f32x16_t acc[Cfg::FM][Cfg::FN];
-    mma_mainloop_swz<Cfg>(acc, la, lb, g.K, smem, tid);
-    store_tile<bf16_t, Cfg>(g, acc, m0, n0, tid);
+    if (it < nk) {
+        sync();
+        compute(stage0);
+    }
+    if constexpr (PARTIAL) {
+        float* P = p.partial + int64_t(split) * p.M * p.N;
+#pragma unroll
+        for (int j = 0; j < C_::FN; ++j) {
+            const int col = n0 + wc0 + j * 32 + acc_col(lane);
+            if (col >= p.N) continue;
+#pragma unroll
+            for (int i = 0; i < C_::FM; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = m0 + wr0 + i * 32 + acc_row(v, lane);
+                    if (row < p.M) P[int64_t(row) * p.N + col] = acc[i][j][v];
+                }
+        }
+    } else {
+        store_tile_impl<bf16_t, NtCfg, OutT, SCATTER>(g, acc, m0, n0, tid);
+    }
+}
+
+// C = alpha * (sum over splits of the partials, in split order) + bias
+template <typename OutT>
+__global__ __launch_bounds__(256) void splitk_reduce_kernel(const float* partial, int splits, int M, int N,
+                                                            GemmDesc g) {
+    const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= int64_t(M) * N) return;
+    const int row = int(i / N), col = int(i % N);
+    float s = 0.f;
+    for (int k = 0; k < splits; ++k) s += partial[int64_t(k) * M * N + i];
+    const float bv = g.bias ? to_f(static_cast<const bf16_t*>(g.bias)[col]) : 0.f;
+    const int64_t crow = g.c_idx ? int64_t(g.c_idx[row]) : int64_t(row);
+    static_cast<OutT*>(g.C)[crow * g.ldc + col] = from_f<OutT>(g.alpha * s + bv);
+}
+
+// out[c * ld_out + r] = in[row(r) * ld_in + c] for r < R, c < C (row(r) =
+// idx[r] or r), bf16; columns r in [R, R_pad) of out are written as zero.
+// Each thread moves one 8 x 8 block: eight 16-byte row loads, a transpose of
+// 16-bit lanes in registers (byte permutes), eight 16-byte stores.  A wave
+// covers 64 rows x 64 columns; lanes 8q..8q+7 read one 128-byte row piece
+// and write one 128-byte output row piece.  Needs C, ld_in, ld_out, R_pad
+// multiples of 8 and 16-byte aligned pointers.
+__global__ __launch_bounds__(256) void transpose_bf16_kernel(const bf16_t* in, int64_t ld_in, const int32_t* idx,
+                                                             int64_t R, int C, bf16_t* out, int64_t ld_out,
+                                                             int64_t R_pad) {
+    const int lane = threadIdx.x & 63, wave = threadIdx.x >> 6;
+    const int64_t r0 = int64_t(blockIdx.x) * 64 + (lane >> 3) * 8;
+    const int c0 = (blockIdx.y * 4 + wave) * 64 + (lane & 7) * 8;
+    if (c0 >= C || r0 >= R_pad) return;
+    uint4 v[8];
+#pragma unroll
+    for (int j = 0; j < 8; ++j) {
+        const int64_t r = r0 + j;
+        v[j] = make_uint4(0, 0, 0, 0);
+        if (r < R) v[j] = *reinterpret_cast<const uint4*>(in + (idx ? int64_t(idx[r]) : r) * ld_in + c0);
+    }
+    // w[e] dword q = (row 2q, column e) | (row 2q + 1, column e) << 16
+#pragma unroll
+    for (int e = 0; e < 8; ++e) {
+        uint32_t d[4];
+#pragma unroll
+        for (int q = 0; q < 4; ++q) {
+            const uint4& lo = v[2 * q];
+            const uint4& hi = v[2 * q + 1];
+            const uint32_t a = (e >> 1) == 0 ? lo.x : (e >> 1) == 1 ? lo.y : (e >> 1) == 2 ? lo.z : lo.w;
+            const uint32_t b = (e >> 1) == 0 ? hi.x : (e >> 1) == 1 ? hi.y : (e >> 1) == 2 ? hi.z : hi.w;
+            d[q] = __builtin_amdgcn_perm(b, a, (e & 1) ? 0x07060302u : 0x05040100u);
+        }
+        *reinterpret_cast<uint4*>(out + int64_t(c0 + e) * ld_out + r0) = make_uint4(d[0], d[1], d[2], d[3]);
+    }
 }
 
 const char* gemm_label(bool at, bool bt, bool bf16) {
@@ -151,32 +344,6 @@ janus_status launch(const GemmDesc& g, hipStream_t s) {
     hipLaunchKernelGGL((gemm_kernel<T, Cfg, AT, BT, AL>), grid, dim3(Cfg::NT), Cfg::SMEM_BYTES, s, g);
     JANUS_LAUNCH_CHECK();
     return JANUS_OK;
-}
-
-template <class Cfg, bool AT, bool BT, bool AL>
-janus_status launch_big(const GemmDesc& g, hipStream_t s) {
-    constexpr int smem = 2 * (Cfg::BM + Cfg::BN) * Cfg::BK * int(sizeof(bf16_t));
-    static bool attr = false;
-    if (!attr) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(&gemm_big_kernel<Cfg, AT, BT, AL>),
-                                hipFuncAttributeMaxDynamicSharedMemorySize, smem) != hipSuccess)
-            return JANUS_ERR_DEVICE;
-        attr = true;
-    }
-    const int mt = (g.M + Cfg::BM - 1) / Cfg::BM, nt = (g.N + Cfg::BN - 1) / Cfg::BN;
-    TraceScope trace(gemm_label(AT, BT, true), 2.0 * g.M * g.N * double(g.K),
-                     (double(g.M) * g.K + double(g.N) * g.K) * 2.0 + double(g.M) * g.N * (g.c_f32 ? 4.0 : 2.0), s);
-    hipLaunchKernelGGL((gemm_big_kernel<Cfg, AT, BT, AL>), dim3(mt * nt), dim3(Cfg::NT), smem, s, g, mt, nt);
-    JANUS_LAUNCH_CHECK();
-    return JANUS_OK;
-}
-
-template <class Cfg>
-janus_status dispatch_big(const GemmDesc& g, bool aligned, hipStream_t s) {
-    if (!g.a_t && !g.b_t) return aligned ? launch_big<Cfg, false, false, true>(g, s) : launch_big<Cfg, false, false, false>(g, s);
-    if (!g.a_t && g.b_t) return aligned ? launch_big<Cfg, false, true, true>(g, s) : launch_big<Cfg, false, true, false>(g, s);
-    if (g.a_t && g.b_t) return aligned ? launch_big<Cfg, true, true, true>(g, s) : launch_big<Cfg, true, true, false>(g, s);
-    return JANUS_ERR_UNSUPPORTED;
 }
 
 template <typename T, class Cfg>
@@ -230,21 +397,176 @@ __global__ void zero_kernel(unsigned char* p, size_t head, uint4* mid, size_t n1
 // bf16: 128x128 tiles, 4 waves of 64x64; fp32: 64x64 tiles, 4 waves of 32x32
 using CfgBF16 = TileCfg<bf16_t, 128, 128, 32, 2, 2>;
 using CfgF32 = TileCfg<float, 64, 64, 32, 2, 2>;
-using CfgBig = TileCfg<bf16_t, 256, 256, 64, 2, 2>;
+
+namespace {
+
+// How a contraction runs on the fast NT path, and the scratch it needs.
+struct NtPlan {
+    bool fast = false;
+    int64_t ldt = 0;                 // leading dimension of transposed copies (K rounded to 64)
+    int splits = 1, ktiles_per_split = 0;
+    size_t a_off = 0, b_off = 0, p_off = 0, bytes = 0;
+};
+
+bool rows16(const void* p, int64_t ld) { return reinterpret_cast<uintptr_t>(p) % 16 == 0 && ld % 8 == 0; }
+
+NtPlan plan_nt(const GemmDesc& g) {
+    NtPlan p;
+    if (g.dtype != JANUS_BF16 || g.M < 128 || g.N < 128 || g.K < 64) return p;
+    // an operand read in place is read in 16-byte chunks along K; transposed
+    // copies are zero-padded along K to a multiple of 64
+    if (g.K % 8 != 0 && ((!g.a_t && !g.a_zero_pad) || (!g.b_t && !g.b_zero_pad))) return p;
+    constexpr int64_t kMaxOff = int64_t(1) << 31;
+    // an operand read in place: 16-byte chunks along K, byte offsets in 31 bits
+    auto in_place_ok = [&](const void* ptr, int64_t ld, const int32_t* idx, int64_t src_rows) {
+        if (!rows16(ptr, ld)) return false;
+        if (idx) return src_rows > 0 && src_rows * ld * 2 < kMaxOff;
+        return int64_t(NtCfg::BM) * ld * 2 < kMaxOff;
+    };
+    // an operand transposed first: read in 16-byte chunks along its rows
+    auto transpose_ok = [&](const void* ptr, int64_t ld, int cols) { return rows16(ptr, ld) && cols % 8 == 0; };
+    if (g.a_t ? !transpose_ok(g.A, g.lda, g.M) : !in_place_ok(g.A, g.lda, g.a_idx, g.a_src_rows)) return p;
+    if (g.b_t ? !transpose_ok(g.B, g.ldb, g.N) : !in_place_ok(g.B, g.ldb, g.b_idx, g.b_src_rows)) return p;
+    p.ldt = round_up(int64_t(g.K), 64);
+    if (int64_t(NtCfg::BM) * p.ldt * 2 >= kMaxOff) return p;
+    const int tiles = ((g.M + NtCfg::BM - 1) / NtCfg::BM) * ((g.N + NtCfg::BN - 1) / NtCfg::BN);
+    const int ktiles = (g.K + NtCfg::BK - 1) / NtCfg::BK;
+    int splits = 1;
+    if (tiles < 160 && ktiles >= 32) splits = std::max(1, std::min({8, 256 / tiles, ktiles / 16}));
+    p.ktiles_per_split = (ktiles + splits - 1) / splits;
+    p.splits = (ktiles + p.ktiles_per_split - 1) / p.ktiles_per_split;
+    size_t off = 0;
+    auto take = [&](size_t bytes) { const size_t o = off; off += (bytes + 255) / 256 * 256; return o; };
+    if (g.a_t) p.a_off = take(size_t(g.M) * p.ldt * 2);
+    if (g.b_t) p.b_off = take(size_t(g.N) * p.ldt * 2);
+    if (p.splits > 1) p.p_off = take(size_t(p.splits) * g.M * g.N * 4);
+    p.bytes = off;
+    p.fast = true;
+    return p;
+}
+
+const char* nt_label(bool f32out, bool scatter, bool partial) {
+    if (partial) return "gemm_nt_splitk";
+    if (f32out) return scatter ? "gemm_nt_f32out_scatter" : "gemm_nt_f32out";
+    return scatter ? "gemm_nt_bf16out_scatter" : "gemm_nt_bf16out";
+}
+
+template <typename OutT, bool SCATTER, bool PARTIAL>
+janus_status launch_nt(const NtArgs& a, const GemmDesc& g, hipStream_t s) {
+    auto kern = &gemm_nt_fast_kernel<OutT, SCATTER, PARTIAL>;
+    const double out_bytes = PARTIAL ? 4.0 * a.splits : (sizeof(OutT) == 4 ? 4.0 : 2.0);
+    TraceScope trace(nt_label(sizeof(OutT) == 4, SCATTER, PARTIAL), 2.0 * g.M * g.N * double(g.K),
+                     (double(g.M) * g.K + double(g.N) * g.K) * 2.0 + double(g.M) * g.N * out_bytes, s);
+    hipLaunchKernelGGL(kern, dim3(unsigned(a.mt * a.nt * a.splits)), dim3(NtCfg::NT), 0, s, a, g);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+janus_status transpose_launch(const bf16_t* in, int64_t ld_in, const int32_t* idx, int64_t R, int C, bf16_t* out,
+                              int64_t ld_out, int64_t R_pad, hipStream_t s) {
+    if (R_pad <= 0 || C <= 0) return JANUS_OK;
+    TraceScope trace("transpose_bf16", 0.0, 2.0 * (double(R) * C + double(R_pad) * C), s);
+    dim3 grid(unsigned((R_pad + 63) / 64), unsigned((C + 255) / 256));
+    hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, s, in, ld_in, idx, R, C, out, ld_out, R_pad);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+janus_status gemm_fast(const GemmDesc& g, const NtPlan& p, hipStream_t s) {
+    char* scratch = static_cast<char*>(g.scratch);
+    NtArgs a{};
+    a.M = g.M;
+    a.N = g.N;
+    a.K = g.K;
+    janus_status e;
+    if (g.a_t) {
+        // A(m, k) = A[row(k) * lda + m]: transpose to [M, K]
+        bf16_t* t = reinterpret_cast<bf16_t*>(scratch + p.a_off);
+        if ((e = transpose_launch(static_cast<const bf16_t*>(g.A), g.lda, g.a_idx, g.K, g.M, t, p.ldt, p.ldt, s)) !=
+            JANUS_OK)
+            return e;
+        a.A = t;
+        a.lda = p.ldt;
+    } else {
+        a.A = static_cast<const bf16_t*>(g.A);
+        a.lda = g.lda;
+        a.a_idx = g.a_idx;
+    }
+    if (g.b_t) {
+        bf16_t* t = reinterpret_cast<bf16_t*>(scratch + p.b_off);
+        if ((e = transpose_launch(static_cast<const bf16_t*>(g.B), g.ldb, g.b_idx, g.K, g.N, t, p.ldt, p.ldt, s)) !=
+            JANUS_OK)
+            return e;
+        a.B = t;
+        a.ldb = p.ldt;
+    } else {
+        a.B = static_cast<const bf16_t*>(g.B);
+        a.ldb = g.ldb;
+        a.b_idx = g.b_idx;
+    }
+    a.mt = (g.M + NtCfg::BM - 1) / NtCfg::BM;
+    a.nt = (g.N + NtCfg::BN - 1) / NtCfg::BN;
+    a.splits = p.splits;
+    a.ktiles_per_split = p.ktiles_per_split;
+    if (p.splits > 1) {
+        a.partial = reinterpret_cast<float*>(scratch + p.p_off);
+        if ((e = launch_nt<float, false, true>(a, g, s)) != JANUS_OK) return e;
+        const int64_t n = int64_t(g.M) * g.N;
+        TraceScope trace("splitk_reduce", 0.0, 4.0 * n * p.splits + n * (g.c_f32 ? 4.0 : 2.0), s);
+        if (g.c_f32)
+            hipLaunchKernelGGL(splitk_reduce_kernel<float>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s,
+                               a.partial, p.splits, g.M, g.N, g);
+        else
+            hipLaunchKernelGGL(splitk_reduce_kernel<bf16_t>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s,
+                               a.partial, p.splits, g.M, g.N, g);
+        JANUS_LAUNCH_CHECK();
+        return JANUS_OK;
+    }
+    if (g.c_f32) return g.c_idx ? launch_nt<float, true, false>(a, g, s) : launch_nt<float, false, false>(a, g, s);
+    return g.c_idx ? launch_nt<bf16_t, true, false>(a, g, s) : launch_nt<bf16_t, false, false>(a, g, s);
+}
+
+}  // namespace
+
+size_t gemm_scratch_bytes(const GemmDesc& g) {
+    const NtPlan p = plan_nt(g);
+    return p.fast ? p.bytes : 0;
+}
+
+size_t gemm_scratch_bound(const GemmDesc& g) {
+    GemmDesc q = g;
+    q.A = q.B = nullptr;            // aligned stand-ins: alignment only ever removes scratch
+    q.a_src_rows = q.a_idx ? int64_t(1) : 0;
+    q.b_src_rows = q.b_idx ? int64_t(1) : 0;
+    const NtPlan p = plan_nt(q);
+    if (!p.fast) return 0;
+    const int tiles = ((g.M + NtCfg::BM - 1) / NtCfg::BM) * ((g.N + NtCfg::BN - 1) / NtCfg::BN);
+    size_t b = 0;
+    if (g.a_t) b += (size_t(g.M) * p.ldt * 2 + 255) / 256 * 256;
+    if (g.b_t) b += (size_t(g.N) * p.ldt * 2 + 255) / 256 * 256;
+    if (tiles < 160) b += (size_t(8) * g.M * g.N * 4 + 255) / 256 * 256;
+    return b;
+}
 
 janus_status gemm(const GemmDesc& g, hipStream_t stream) {
     if (g.M <= 0 || g.N <= 0) return JANUS_OK;
     const size_t es = dtype_size(g.dtype);
     const bool aligned = aligned16(g.A, g.lda, es) && aligned16(g.B, g.ldb, es);
-    if (g.K <= 0) {
-        // empty contraction: C = bias (or 0); handled by the kernel with K = 0
-    }
     if (g.dtype == JANUS_BF16) {
-        if (g.M >= 256 && g.N >= 256) return dispatch_big<CfgBig>(g, aligned, stream);
+        const NtPlan p = plan_nt(g);
+        if (p.fast && (p.bytes == 0 || (g.scratch && g.scratch_bytes >= p.bytes))) return gemm_fast(g, p, stream);
         return dispatch<bf16_t, CfgBF16>(g, aligned, stream);
     }
     if (g.dtype == JANUS_F32) return dispatch<float, CfgF32>(g, aligned, stream);
     return JANUS_ERR_UNSUPPORTED;
+}
+
+janus_status transpose_bf16(const void* in, int64_t ld_in, const int32_t* idx, int64_t R, int C, void* out,
+                            int64_t ld_out, int64_t R_pad, hipStream_t stream) {
+    if (!rows16(in, ld_in) || !rows16(out, ld_out) || C % 8 != 0 || R_pad % 8 != 0 || R_pad < R)
+        return JANUS_ERR_UNSUPPORTED;
+    return transpose_launch(static_cast<const bf16_t*>(in), ld_in, idx, R, C, static_cast<bf16_t*>(out), ld_out,
+                            R_pad, stream);
 }
 
 size_t colsum_partial_floats(int C) { return size_t(kRowChunks) * size_t(C); }

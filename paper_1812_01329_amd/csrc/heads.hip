@@ -5,6 +5,8 @@
 // Reductions are deterministic: every sum is taken in a fixed order (wave
 // shuffles in a fixed butterfly, then a fixed sequence of partials), so two
 // runs on the same inputs give identical bits.
+#include <algorithm>
+
 #include "device.hpp"
 #include "ops.hpp"
 
@@ -189,8 +191,24 @@ struct XentWs {
     void* dz = nullptr;
     float* loss_rows = nullptr;
     float* part = nullptr;
+    void* gs = nullptr;          // contraction scratch
+    size_t gs_bytes = 0;
     int64_t ldv = 0;
 };
+
+// scratch bound of the head's contractions: logits = h Wout^T, dh = dz Wout,
+// dWout = dz^T h (run one after another, so one buffer serves all)
+size_t head_gemm_scratch(janus_dtype dt, int rows, int H, int V) {
+    if (dt != JANUS_BF16) return 0;
+    GemmDesc g;
+    g.dtype = dt;
+    g.M = rows; g.N = V; g.K = H;
+    size_t m = gemm_scratch_bound(g);
+    g.N = H; g.K = V; g.b_t = true;
+    m = std::max(m, gemm_scratch_bound(g));
+    g.M = V; g.N = H; g.K = rows; g.a_t = true;
+    return std::max(m, gemm_scratch_bound(g));
+}
 
 size_t carve_xent(const janus_xent_desc& d, janus_xent_op op, void* base, XentWs& w) {
     Carver c(base);
@@ -200,6 +218,8 @@ size_t carve_xent(const janus_xent_desc& d, janus_xent_op op, void* base, XentWs
         w.dz = c.take<char>(int64_t(d.rows) * w.ldv * dtype_size(d.dtype));
         w.loss_rows = c.take<float>(d.rows);
         w.part = c.take<float>(colsum_partial_floats(d.V));
+        w.gs_bytes = head_gemm_scratch(d.dtype, d.rows, d.H, d.V);
+        w.gs = c.take<char>(int64_t(w.gs_bytes));
     }
     return c.off + 256;
 }
@@ -208,6 +228,8 @@ struct MseWs {
     void* dY = nullptr;
     float* part = nullptr;
     float* cpart = nullptr;
+    void* gs = nullptr;          // contraction scratch
+    size_t gs_bytes = 0;
     int nparts = 0;
 };
 
@@ -222,6 +244,8 @@ size_t carve_mse(const janus_mse_desc& d, void* base, MseWs& w) {
     w.nparts = d.dtype == JANUS_BF16 ? mse_parts<HeadBF16>(d) : mse_parts<HeadF32>(d);
     w.part = c.take<float>(w.nparts);
     w.cpart = c.take<float>(colsum_partial_floats(d.P));
+    w.gs_bytes = head_gemm_scratch(d.dtype, d.rows, d.H, d.P);
+    w.gs = c.take<char>(int64_t(w.gs_bytes));
     return c.off + 256;
 }
 
@@ -264,6 +288,8 @@ janus_status mse_impl(const janus_mse_desc& d, const void* h, const void* W, con
     g.C = dh;
     g.ldc = d.H;
     g.c_f32 = false;
+    g.scratch = w.gs;
+    g.scratch_bytes = w.gs_bytes;
     janus_status e = gemm(g, st);
     if (e != JANUS_OK) return e;
     // dW = dY^T h
@@ -281,6 +307,8 @@ janus_status mse_impl(const janus_mse_desc& d, const void* h, const void* W, con
     q.C = dW;
     q.ldc = d.H;
     q.c_f32 = true;
+    q.scratch = w.gs;
+    q.scratch_bytes = w.gs_bytes;
     e = gemm(q, st);
     if (e != JANUS_OK) return e;
     return colsum(d.dtype, w.dY, d.rows, d.P, d.P, db, w.cpart, st);
@@ -303,6 +331,8 @@ janus_status xent_impl(const janus_xent_desc& d, const int32_t* ids_dev, const v
     g.ldc = w.ldv;
     g.c_f32 = true;
     g.bias = bout;
+    g.scratch = w.gs;
+    g.scratch_bytes = w.gs_bytes;
     janus_status e = gemm(g, st);
     if (e != JANUS_OK) return e;
     {
@@ -331,6 +361,8 @@ janus_status xent_impl(const janus_xent_desc& d, const int32_t* ids_dev, const v
     q.C = dh;
     q.ldc = d.H;
     q.c_f32 = false;
+    q.scratch = w.gs;
+    q.scratch_bytes = w.gs_bytes;
     e = gemm(q, st);
     if (e != JANUS_OK) return e;
     // dWout = dz^T h
@@ -348,6 +380,8 @@ janus_status xent_impl(const janus_xent_desc& d, const int32_t* ids_dev, const v
     r.C = dWout;
     r.ldc = d.H;
     r.c_f32 = true;
+    r.scratch = w.gs;
+    r.scratch_bytes = w.gs_bytes;
     e = gemm(r, st);
     if (e != JANUS_OK) return e;
     return colsum(d.dtype, w.dz, d.rows, d.V, w.ldv, dbout, w.part, st);

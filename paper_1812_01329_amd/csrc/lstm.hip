@@ -30,6 +30,7 @@
 //   dY [T*B x ldh] dtype                        gradient of a lower layer's output
 //   dh, dc [B x H] float32                      carried gradients (sorted rows)
 //   colsum scratch
+#include <algorithm>
 #include <vector>
 
 #include "device.hpp"
@@ -60,8 +61,41 @@ struct LstmWs {
     int32_t* off_dev = nullptr;         // [T + 2]
     float* dpart = nullptr;             // [4 x B x H] partial recurrent gradients
     persist::Sync* sync = nullptr;
-    int64_t ldh = 0, ldg = 0;
+    void* GT = nullptr;                 // dG^T [4H x ldk] (bf16), K-contiguous operand of the weight gradients
+    void* gs = nullptr;                 // contraction scratch (transposed operands, split-K partials)
+    size_t gs_bytes = 0;
+    int64_t ldh = 0, ldg = 0, ldk = 0;
 };
+
+// Contraction scratch for every contraction of the forward and backward
+// passes (they run one after another on one stream, so one buffer serves all).
+size_t lstm_gemm_scratch(const janus_lstm_desc& d) {
+    const int64_t TB = int64_t(d.T) * d.B;
+    if (d.dtype != JANUS_BF16 || TB > INT32_MAX) return 0;
+    size_t m = 0;
+    for (int l = 0; l < d.L; ++l) {
+        const int Il = l == 0 ? d.I : d.H;
+        GemmDesc g;
+        g.dtype = d.dtype;
+        g.M = int(TB); g.N = 4 * d.H; g.K = Il;            // input projection
+        g.a_idx = reinterpret_cast<const int32_t*>(16);
+        m = std::max(m, gemm_scratch_bound(g));
+        g = GemmDesc();
+        g.dtype = d.dtype;
+        g.M = 4 * d.H; g.N = Il; g.K = int(TB);             // dWx, dWh (dG^T in place, rows transposed)
+        g.a_zero_pad = true;
+        g.b_t = true;
+        m = std::max(m, gemm_scratch_bound(g));
+        g.N = d.H;
+        m = std::max(m, gemm_scratch_bound(g));
+        g = GemmDesc();
+        g.dtype = d.dtype;
+        g.M = int(TB); g.N = Il; g.K = 4 * d.H;             // dX = dG Wx
+        g.b_t = true;
+        m = std::max(m, gemm_scratch_bound(g));
+    }
+    return m;
+}
 
 size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     Carver c(base);
@@ -98,6 +132,12 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     w.off_dev = c.take<int32_t>(int64_t(d.T) + 2);
     w.dpart = c.take<float>(int64_t(persist::kSlices) * d.B * d.H);
     w.sync = c.take<persist::Sync>(16);
+    if (d.dtype == JANUS_BF16) {
+        w.ldk = round_up(TB, 64);
+        w.GT = c.take<char>(int64_t(4) * d.H * w.ldk * es);
+        w.gs_bytes = lstm_gemm_scratch(d);
+        w.gs = c.take<char>(int64_t(w.gs_bytes));
+    }
     return c.off + 256;
 }
 
@@ -499,12 +539,15 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
         g.A = static_cast<const bf16_t*>(w.Hs[l - 1]) + int64_t(B) * w.ldh;
         g.lda = w.ldh;
     }
+    g.a_src_rows = int64_t(d.T) * B;
     g.B = w.Wxi[l];
     g.ldb = Il;
     g.C = w.XG;
     g.ldc = w.ldg;
     g.c_f32 = false;
     g.bias = w.bi[l];
+    g.scratch = w.gs;
+    g.scratch_bytes = w.gs_bytes;
     janus_status e = gemm(g, st);
     if (e != JANUS_OK) return e;
     if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;
@@ -577,12 +620,15 @@ janus_status lstm_fwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             g.A = static_cast<const T*>(w.Hs[l - 1]) + int64_t(B) * w.ldh;
             g.lda = w.ldh;
         }
+        g.a_src_rows = TB;
         g.B = Wx[l];
         g.ldb = g.K;
         g.C = w.XG;
         g.ldc = w.ldg;
         g.c_f32 = false;
         g.bias = b[l];
+        g.scratch = w.gs;
+        g.scratch_bytes = w.gs_bytes;
         janus_status e = gemm(g, st);
         if (e != JANUS_OK) return e;
         for (int t = 0; t < s.t_eff; ++t) {
@@ -727,15 +773,30 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         }
         const int32_t* rowmap = persistent ? w.perm4 : nullptr;   // interleaved gate rows -> torch rows
         const int Il = l == 0 ? d.I : H;
+        // dG^T once for both weight gradients, so that they read it in place
+        const bool gt = w.GT && (4 * H) % 8 == 0;
+        if (gt) {
+            janus_status e = transpose_bf16(w.XG, w.ldg, nullptr, s.packed, 4 * H, w.GT, w.ldk,
+                                            round_up(s.packed, 64), st);
+            if (e != JANUS_OK) return e;
+        }
         // dWx = dG^T X
         GemmDesc g;
         g.dtype = d.dtype;
         g.M = 4 * H;
         g.N = Il;
         g.K = int(s.packed);
-        g.a_t = true;
-        g.A = w.XG;
-        g.lda = w.ldg;
+        if (gt) {
+            g.A = w.GT;
+            g.lda = w.ldk;
+            g.a_zero_pad = true;
+        } else {
+            g.a_t = true;
+            g.A = w.XG;
+            g.lda = w.ldg;
+        }
+        g.scratch = w.gs;
+        g.scratch_bytes = w.gs_bytes;
         g.b_t = true;
         if (l == 0) {
             g.B = x;
@@ -775,6 +836,8 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             q.B = persistent ? w.Wxi[l] : Wx[l];
             q.ldb = Il;
             q.c_f32 = false;
+            q.scratch = w.gs;
+            q.scratch_bytes = w.gs_bytes;
             if (l > 0) {
                 q.C = w.dY;
                 q.ldc = w.ldh;

@@ -30,9 +30,30 @@ struct GemmDesc {
     bool c_f32 = true;
     const void* bias = nullptr;
     float alpha = 1.0f;
+    // rows of A / B behind a_idx / b_idx (bounds the gathered offsets; 0 =
+    // unknown, which keeps a gathered operand off the fast path)
+    int64_t a_src_rows = 0, b_src_rows = 0;
+    // (a_t / b_t false only) rows of A / B hold zeros from K up to the next
+    // multiple of 8, so they may be read in whole 16-byte chunks
+    bool a_zero_pad = false, b_zero_pad = false;
+    // device scratch for transposed operand copies and split-K partials,
+    // gemm_scratch_bytes(g) bytes; with less, a slower path that needs none
+    // is taken
+    void* scratch = nullptr;
+    size_t scratch_bytes = 0;
 };
 
 janus_status gemm(const GemmDesc& g, hipStream_t stream);
+size_t gemm_scratch_bytes(const GemmDesc& g);
+// scratch enough for the contraction with any K up to g.K, any operand
+// alignment and any gathered-row count (for sizing workspaces in advance)
+size_t gemm_scratch_bound(const GemmDesc& g);
+
+// out[c * ld_out + r] = in[row(r) * ld_in + c] (bf16), row(r) = idx[r] or r,
+// for r < R, c < C; columns [R, R_pad) of each output row are zero.  C,
+// ld_in, ld_out, R_pad must be multiples of 8 and pointers 16-byte aligned.
+janus_status transpose_bf16(const void* in, int64_t ld_in, const int32_t* idx, int64_t R, int C, void* out,
+                            int64_t ld_out, int64_t R_pad, hipStream_t stream);
 
 // out[c] = sum over rows r < R of in[r * ld + c] (float32 result), for
 // c < C; deterministic two-pass reduction using `partial` scratch of

@@ -193,3 +193,14 @@ def test_both_recurrence_paths(persist, lengths, monkeypatch):
     w = _lstm("mse", "bf16", L=2, I=64, H=128, B=B, T=12, lengths=lens, seed=11, h0=True, P=40)
     _, g = _run(w)
     compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
+
+
+def test_long_ragged_batch_split_contractions():
+    """Enough packed rows (ragged count) that the weight-gradient
+    contractions split K and the input projection gathers rows."""
+    rng = np.random.default_rng(21)
+    B = 100
+    lengths = rng.integers(0, 49, B)
+    w = _lstm("mse", "bf16", L=1, I=64, H=128, B=B, T=48, lengths=lengths, seed=21, h0=True, P=136)
+    _, g = _run(w)
+    compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
