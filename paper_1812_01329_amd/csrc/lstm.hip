@@ -62,6 +62,8 @@ struct LstmWs {
     float* dpart = nullptr;             // [4 x B x H] partial recurrent gradients
     persist::Sync* sync = nullptr;
     void* GT = nullptr;                 // dG^T [4H x ldk] (bf16), K-contiguous operand of the weight gradients
+    bf16_t* Hf = nullptr;               // [T + 1] slots of h in fragment layout (persistent forward)
+    int64_t hf_slot = 0;                // elements per slot
     void* gs = nullptr;                 // contraction scratch (transposed operands, split-K partials)
     size_t gs_bytes = 0;
     int64_t ldh = 0, ldg = 0, ldk = 0;
@@ -133,6 +135,8 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     w.dpart = c.take<float>(int64_t(persist::kSlices) * d.B * d.H);
     w.sync = c.take<persist::Sync>(16);
     if (d.dtype == JANUS_BF16) {
+        w.hf_slot = round_up(d.B, 32) * round_up(d.H, 64);
+        w.Hf = c.take<bf16_t>((int64_t(d.T) + 1) * w.hf_slot);
         w.ldk = round_up(TB, 64);
         w.GT = c.take<char>(int64_t(4) * d.H * w.ldk * es);
         w.gs_bytes = lstm_gemm_scratch(d);
@@ -209,9 +213,11 @@ __global__ void interleave_rows_kernel(const T* src, T* dst, int H, int cols) {
 }
 
 // ------------------------------------------------------------ init kernels
+// initial state of the sorted rows into Hs / Cs rows [0, B) (and, for the
+// persistent forward, into slot 0 of the fragment-layout copy Hf)
 template <typename T>
 __global__ void fwd_init_kernel(int B, int H, int64_t ldh, const int32_t* perm, const float* h0, const float* c0,
-                                T* Hs, float* Cs, int active0, float* hT, float* cT) {
+                                T* Hs, float* Cs, int active0, float* hT, float* cT, T* Hf, int Kp) {
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i >= int64_t(B) * H) return;
     const int r = int(i / H), u = int(i % H);
@@ -220,6 +226,7 @@ __global__ void fwd_init_kernel(int B, int H, int64_t ldh, const int32_t* perm, 
     const float cv = c0 ? c0[int64_t(b) * H + u] : 0.f;
     Hs[int64_t(r) * ldh + u] = from_f<T>(hv);
     Cs[int64_t(r) * ldh + u] = cv;
+    if (Hf) Hf[persist::frag_index(r, u, Kp)] = from_f<T>(hv);
     if (r >= active0) {   // a length-0 sequence ends in its initial state
         if (hT) hT[int64_t(b) * H + u] = hv;
         if (cT) cT[int64_t(b) * H + u] = cv;
@@ -570,6 +577,8 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     a.cT = cT;
     a.ldh = w.ldh;
     a.ldg = w.ldg;
+    a.Hf = w.Hf;
+    a.hf_slot = w.hf_slot;
     a.sync = w.sync;
     return launch_fwd_persistent(d, a, 2.0 * 4.0 * H * double(H) * recurrent_rows(s), st);
 }
@@ -588,6 +597,12 @@ janus_status lstm_fwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
     }
     const bool al = weight_aligned(d);
     const bool persistent = use_persistent(d);
+    if (persistent && H % 64 != 0) {
+        // columns [H, Kp) of the fragment-layout copy are never written and
+        // take part in the contraction against zero weights: make them 0
+        janus_status e = zero_fill(w.Hf, size_t(d.T + 1) * size_t(w.hf_slot) * 2, st);
+        if (e != JANUS_OK) return e;
+    }
     for (int l = 0; l < d.L; ++l) {
         const int64_t bh = int64_t(B) * H;
         {
@@ -595,7 +610,8 @@ janus_status lstm_fwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             hipLaunchKernelGGL(fwd_init_kernel<T>, dim3(unsigned((bh + 255) / 256)), dim3(256), 0, st, B, H, w.ldh,
                                perm, h0 ? h0 + l * bh : nullptr, c0 ? c0 + l * bh : nullptr,
                                static_cast<T*>(w.Hs[l]), w.Cs[l], s.active[0], hT ? hT + l * bh : nullptr,
-                               cT ? cT + l * bh : nullptr);
+                               cT ? cT + l * bh : nullptr, persistent ? reinterpret_cast<T*>(w.Hf) : nullptr,
+                               int(round_up(H, 64)));
             JANUS_LAUNCH_CHECK();
         }
         if (s.packed == 0) continue;

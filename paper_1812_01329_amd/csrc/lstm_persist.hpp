@@ -140,8 +140,20 @@ struct FwdArgs {
     float* hT;
     float* cT;
     int64_t ldh, ldg;
+    bf16_t* Hf;                        // [T + 1] slots of h in fragment layout (slot t = h_{t-1}; slot 0 = h0)
+    int64_t hf_slot;                   // elements per slot: round_up(B, 32) * Kp
     Sync* sync;
 };
+
+// Fragment layout of a [rows x Kp] bf16 operand (Kp a multiple of 16):
+// element (r, k) sits at
+//   ((r / 32) * (Kp / 16) + k / 16) * 512 + (((k % 16) / 8) * 32 + r % 32) * 8 + k % 8,
+// so the 16 bytes lane l supplies to a 32x32x16 MFMA as the B operand (row
+// l % 32, k = 16 j + 8 (l / 32) + [0, 8)) are contiguous and one wave-wide
+// load reads 1 KB in one piece, instead of 16 bytes from each of 32 rows.
+__host__ __device__ __forceinline__ int64_t frag_index(int64_t r, int k, int Kp) {
+    return ((r >> 5) * (Kp >> 4) + (k >> 4)) * 512 + ((((k & 15) >> 3) << 5) + (r & 31)) * 8 + (k & 7);
+}
 
 // Schedule values are the same for every lane; readfirstlane keeps them in
 // scalar registers so that buffer descriptors built from them stay uniform.
@@ -296,59 +308,102 @@ __device__ __forceinline__ void reduce_kparts(f32x16_t& acc, float* red, int wav
     }
 }
 
+// acc += Wslice . R^T for one 32-row group R of an operand in fragment
+// layout, over n k-groups of 16.  `off` is the byte offset of this lane's
+// 16 bytes of the first k-group (k-groups are 1 KB apart); `wrow` is this
+// lane's LDS weight row at the first k-group (16 elements per k-group).
+// Loads stream through a ring of DEPTH k-groups in flight; two accumulators
+// alternate so consecutive MFMAs do not wait on each other.
+template <int DEPTH>
+__device__ __forceinline__ void contract_frag(f32x16_t& acc, const bf16_t* wrow, __amdgpu_buffer_rsrc_t rs,
+                                              uint32_t off, int n) {
+    uint4 ring[DEPTH];
+    f32x16_t acc1;
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc1[v] = 0.f;
+#pragma unroll
+    for (int i = 0; i < DEPTH; ++i) ring[i] = load16(rs, i < n ? off + uint32_t(i) * 1024u : kOutOfRange);
+    int kg = 0;
+    for (; kg + DEPTH <= n; kg += DEPTH) {
+#pragma unroll
+        for (int i = 0; i < DEPTH; ++i) {
+            Frag<bf16_t> fw, fh;
+            fw.v = *reinterpret_cast<const uint4*>(wrow + (kg + i) * 16);
+            fh.v = ring[i];
+            if (i & 1) mfma(acc1, fw, fh);
+            else mfma(acc, fw, fh);
+            const int nx = kg + i + DEPTH;
+            ring[i] = load16(rs, nx < n ? off + uint32_t(nx) * 1024u : kOutOfRange);
+        }
+    }
+#pragma unroll
+    for (int i = 0; i < DEPTH; ++i) {
+        if (kg + i < n) {
+            Frag<bf16_t> fw, fh;
+            fw.v = *reinterpret_cast<const uint4*>(wrow + (kg + i) * 16);
+            fh.v = ring[i];
+            if (i & 1) mfma(acc1, fw, fh);
+            else mfma(acc, fw, fh);
+        }
+    }
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] += acc1[v];
+}
+
+constexpr int kDepthFrag = 16;
+
 template <int KW>
 __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wld = a.Kp + 8;
     bf16_t* Ws = reinterpret_cast<bf16_t*>(smem_raw);
     float* red = reinterpret_cast<float*>(smem_raw + size_t(32) * wld * sizeof(bf16_t));
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int u0 = blockIdx.x * kUnitsFwd;
     constexpr int NB = kWaves / KW;
     const int bt = wave % NB, kw = wave / NB;
-    const int nkb = a.Kp / 64;
-    const int kb0 = kw * nkb / KW, kb1 = (kw + 1) * nkb / KW;
-    const int kofs = (lane >> 5) * 32;
-    const bf16_t* wrow = Ws + (lane & 31) * wld;
+    const int nkg = a.Kp / 16;
+    const int kg0 = kw * nkg / KW, kg1 = (kw + 1) * nkg / KW;
+    const bf16_t* wrow = Ws + (lane & 31) * wld + 8 * (lane >> 5) + kg0 * 16;
+    const uint32_t hoff = (uint32_t(bt * nkg + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
     const int H = a.H;
+    const int row = bt * 32 + (lane & 31);   // this lane's batch row (sorted order)
+    const int ub = u0 + 4 * (lane >> 5);      // its four consecutive units
+    const bool owner = kw == 0;               // lanes of these waves own cells
     Barrier bar;
     barrier_init(bar, a.sync);
 
     stage_fwd_weights(a, Ws, wld, u0);
+    // the cell state of the owned cells stays in registers for the launch
+    float creg[4] = {0.f, 0.f, 0.f, 0.f};
+    if (owner && row < a.B) {
+        const float4 c0 = *reinterpret_cast<const float4*>(a.Cs + int64_t(row) * a.ldh + ub);
+        creg[0] = c0.x; creg[1] = c0.y; creg[2] = c0.z; creg[3] = c0.w;
+    }
     __syncthreads();
 
     for (int t = 0; t < a.t_eff; ++t) {
         const int act = act_at(a.active, a.fixed, a.B, t, a.t_eff);
         const int act_next = act_at(a.active, a.fixed, a.B, t + 1, a.t_eff);
         const int64_t off_t = off_at(a.offsets, a.fixed, a.B, t);
-        const int64_t prev_base = t == 0 ? 0 : int64_t(a.B) + off_at(a.offsets, a.fixed, a.B, t - 1);
-        const int row = bt * 32 + (lane & 31);
-        // operands of the cell update do not depend on h_{t-1}: load them
+        // operand of the cell update that does not depend on h_{t-1}: load it
         // first (branch-free; lanes without a cell read out of range, i.e. 0)
-        const bool cell = kw == 0 && row < act;
-        const int ub = u0 + 4 * (lane >> 5);   // this lane's four consecutive units
-        const int64_t p = off_t + row;
+        const bool cell = owner && row < act;
         const auto rxg = make_rsrc(a.XG + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
-        const auto rcp = make_rsrc(a.Cs + prev_base * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 4u);
         const uint32_t oxg = cell ? (uint32_t(row) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u : kOutOfRange;
-        const uint32_t ocp = cell ? (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 4u : kOutOfRange;
         const uint4 xg0 = load16(rxg, oxg), xg1 = load16(rxg, oxg + 16u);
-        const uint4 cpv = load16(rcp, ocp);
         f32x16_t acc;
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[v] = 0.f;
         if (bt * 32 < act) {
-            // rows [0, act) of h_{t-1} start at Hs row prev_base
-            const auto rs = make_rsrc(a.Hs + prev_base * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 2u);
-            contract_rows<kDepthFwd>(acc, wrow, rs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(kofs)) * 2u, kb0, kb1, H,
-                                     kofs);
+            // h_{t-1} is slot t of the fragment-layout copy
+            const auto rs = make_rsrc(a.Hf + int64_t(t) * a.hf_slot, uint32_t(a.hf_slot) * 2u);
+            contract_frag<kDepthFrag>(acc, wrow, rs, hoff, kg1 - kg0);
         }
         reduce_kparts<KW>(acc, red, wave, lane);
         if (cell) {
             const uint32_t xw[8] = {xg0.x, xg0.y, xg0.z, xg0.w, xg1.x, xg1.y, xg1.z, xg1.w};
-            const float cpr[4] = {__uint_as_float(cpv.x), __uint_as_float(cpv.y), __uint_as_float(cpv.z),
-                                  __uint_as_float(cpv.w)};
-            float cn[4], hn[4];
+            float hn[4];
             uint32_t gw[8];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
@@ -358,20 +413,25 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
                 const float ag = acc[4 * q + 2] + bf2f(bf16_t(w1 & 0xffffu));
                 const float ao = acc[4 * q + 3] + bf2f(bf16_t(w1 >> 16));
                 const float gi = sigmoidf_(ai), gf = sigmoidf_(af), gg = tanhf_(ag), go = sigmoidf_(ao);
-                cn[q] = gf * cpr[q] + gi * gg;
-                hn[q] = go * tanhf_(cn[q]);
+                creg[q] = gf * creg[q] + gi * gg;
+                hn[q] = go * tanhf_(creg[q]);
                 gw[2 * q] = uint32_t(f2bf(gi)) | (uint32_t(f2bf(gf)) << 16);
                 gw[2 * q + 1] = uint32_t(f2bf(gg)) | (uint32_t(f2bf(go)) << 16);
             }
             const uint2 hb = make_uint2(uint32_t(f2bf(hn[0])) | (uint32_t(f2bf(hn[1])) << 16),
                                         uint32_t(f2bf(hn[2])) | (uint32_t(f2bf(hn[3])) << 16));
+            // h_t for the next step (fragment layout, slot t + 1)
+            if (t + 1 < a.t_eff && row < act_next) {
+                const auto rhf = make_rsrc(a.Hf + int64_t(t + 1) * a.hf_slot, uint32_t(a.hf_slot) * 2u);
+                store8<kStoreThrough>(rhf, uint32_t(frag_index(row, ub, a.Kp)) * 2u, hb);
+            }
             const int64_t nrow = int64_t(a.B) + off_t;   // first row of step t in Hs / Cs
             const auto rcs = make_rsrc(a.Cs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 4u);
             const auto rhs = make_rsrc(a.Hs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 2u);
             const auto rgs = make_rsrc(a.Gs + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
             store16<kStoreThrough>(rcs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 4u,
-                    make_uint4(__float_as_uint(cn[0]), __float_as_uint(cn[1]), __float_as_uint(cn[2]),
-                               __float_as_uint(cn[3])));
+                    make_uint4(__float_as_uint(creg[0]), __float_as_uint(creg[1]), __float_as_uint(creg[2]),
+                               __float_as_uint(creg[3])));
             store8<kStoreThrough>(rhs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 2u, hb);
             const uint32_t og = (uint32_t(row) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
             store16<kStoreThrough>(rgs, og, make_uint4(gw[0], gw[1], gw[2], gw[3]));
@@ -385,7 +445,7 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
 #pragma unroll
                 for (int q = 0; q < 4; ++q) {
                     if (a.hT) a.hT[int64_t(b) * H + ub + q] = hn[q];
-                    if (a.cT) a.cT[int64_t(b) * H + ub + q] = cn[q];
+                    if (a.cT) a.cT[int64_t(b) * H + ub + q] = creg[q];
                 }
             }
         }
