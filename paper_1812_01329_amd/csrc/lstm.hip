@@ -59,7 +59,9 @@ struct LstmWs {
     int32_t* perm4 = nullptr;           // [4H] interleaved row -> gate-major row
     int32_t* act_dev = nullptr;         // [T + 1]
     int32_t* off_dev = nullptr;         // [T + 2]
-    float* dpart = nullptr;             // [4 x B x H] partial recurrent gradients
+    float* dpart = nullptr;             // [T + 1] slots of [4 x B x H] partial recurrent gradients
+    bf16_t* Gf = nullptr;               // [T] slots of dG in fragment layout (persistent backward)
+    int64_t gf_slot = 0;                // elements per slot
     persist::Sync* sync = nullptr;
     void* GT = nullptr;                 // dG^T [4H x ldk] (bf16), K-contiguous operand of the weight gradients
     bf16_t* Hf = nullptr;               // [T + 1] slots of h in fragment layout (persistent forward)
@@ -132,9 +134,11 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     w.perm4 = c.take<int32_t>(int64_t(4) * d.H);
     w.act_dev = c.take<int32_t>(int64_t(d.T) + 1);
     w.off_dev = c.take<int32_t>(int64_t(d.T) + 2);
-    w.dpart = c.take<float>(int64_t(persist::kSlices) * d.B * d.H);
-    w.sync = c.take<persist::Sync>(16);
+    w.sync = c.take<persist::Sync>(1);
     if (d.dtype == JANUS_BF16) {
+        w.dpart = c.take<float>((int64_t(d.T) + 1) * persist::kSlices * d.B * d.H);
+        w.gf_slot = round_up(d.B, 32) * int64_t(4) * d.H;
+        w.Gf = c.take<bf16_t>(int64_t(d.T) * w.gf_slot);
         w.hf_slot = round_up(d.B, 32) * round_up(d.H, 64);
         w.Hf = c.take<bf16_t>((int64_t(d.T) + 1) * w.hf_slot);
         w.ldk = round_up(TB, 64);
@@ -176,8 +180,13 @@ size_t persist_red_bytes(int kw) { return size_t(kw - 1) * (persist::kWaves / kw
 size_t persist_fwd_lds(const janus_lstm_desc& d) {
     return size_t(32) * (round_up(d.H, 64) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
 }
+// backward K slices: k-groups of 16 interleaved gate columns, split in kSlices
+int persist_bwd_nkg(const janus_lstm_desc& d) { return d.H / 4; }
+int persist_bwd_ksp(const janus_lstm_desc& d) {
+    return 16 * ((persist_bwd_nkg(d) + persist::kSlices - 1) / persist::kSlices);
+}
 size_t persist_bwd_lds(const janus_lstm_desc& d) {
-    return size_t(persist::kUnitsBwd) * (round_up(d.H, 64) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
+    return size_t(persist::kUnitsBwd) * (persist_bwd_ksp(d) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
 }
 int persist_fwd_blocks(const janus_lstm_desc& d) { return (d.H + persist::kUnitsFwd - 1) / persist::kUnitsFwd; }
 int persist_bwd_blocks(const janus_lstm_desc& d) {
@@ -194,6 +203,7 @@ bool use_persistent(const janus_lstm_desc& d) {
     const DeviceInfo info = device_info();
     if (!info.coop || info.cus <= 0) return false;
     if (persist_fwd_blocks(d) > info.cus || persist_bwd_blocks(d) > info.cus) return false;
+    if ((d.H + persist::kUnitsBwd - 1) / persist::kUnitsBwd > persist::kMaxGroups) return false;
     const size_t lds = info.lds > 0 ? info.lds : 65536;
     return persist_fwd_lds(d) <= lds && persist_bwd_lds(d) <= lds;
 }
@@ -707,8 +717,11 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.B = B;
             a.t_eff = s.t_eff;
             a.fixed = s.fixed ? 1 : 0;
-            a.Ks = H;
-            a.Ksp = int(round_up(H, 64));
+            a.nkg = persist_bwd_nkg(d);
+            a.ksp = persist_bwd_ksp(d);
+            a.Gf = w.Gf;
+            a.gf_slot = w.gf_slot;
+            a.xcd_groups = (persist_bwd_blocks(d) % (8 * persist::kSlices)) == 0 ? 1 : 0;
             a.active = w.act_dev;
             a.offsets = w.off_dev;
             a.perm = perm;

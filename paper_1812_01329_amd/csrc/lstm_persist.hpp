@@ -36,8 +36,8 @@ constexpr int kUnitsFwd = 8;           // hidden units per forward workgroup (32
 constexpr int kUnitsBwd = 32;          // hidden units per backward workgroup
 constexpr int kSlices = 4;             // K-split of the backward contraction
 constexpr int kMaxB = 256;             // batch rows handled by one pass of 8 waves
-constexpr int kCellsPerThread = 4;     // (kMaxB * 8 units) / kThreads
 constexpr int kSpinLimit = 1 << 22;    // bounded wait at each barrier (~0.1 s)
+constexpr int kMaxGroups = 64;         // backward unit groups (H / 32) a launch may have
 
 // Device-wide barrier state (zeroed before every launch).  Counters sit in
 // separate 256-byte lines.
@@ -47,6 +47,7 @@ struct Sync {
     unsigned pad0[62];
     unsigned xcd[16][64];              // per-XCD arrivals
     unsigned census[16][64];           // workgroups resident on each XCD
+    unsigned group[kMaxGroups][64];    // arrivals of each backward unit group
 };
 
 __device__ __forceinline__ unsigned xcc_id() {
@@ -202,8 +203,6 @@ __device__ __forceinline__ void stage_fwd_weights(const FwdArgs& a, bf16_t* Ws, 
 // (row, 32 * (lane / 32)) of this lane's row inside the descriptor.  Rows
 // stream through a ring of DEPTH k-blocks kept in flight, so the memory
 // latency is paid once per step and each MFMA waits only for its own block.
-constexpr int kDepthFwd = 8;
-constexpr int kDepthBwd = 4;
 constexpr uint32_t kOutOfRange = 0x80000000u;
 
 typedef uint32_t u32x4_t __attribute__((ext_vector_type(4)));
@@ -239,50 +238,6 @@ __device__ __forceinline__ void store8(__amdgpu_buffer_rsrc_t rs, uint32_t off, 
     typedef uint32_t u32x2_t __attribute__((ext_vector_type(2)));
     const u32x2_t w = {v.x, v.y};
     __builtin_amdgcn_raw_buffer_store_b64(w, rs, int(off), 0, POLICY);
-}
-
-__device__ __forceinline__ void load_block(uint4 (&hv)[4], __amdgpu_buffer_rsrc_t rs, uint32_t roff, int kb, int kb1,
-                                           int kmax, int kofs) {
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        const bool ok = kb < kb1 && kb * 64 + kofs + 8 * s < kmax;
-        const uint32_t off = ok ? roff + uint32_t(kb * 64 + 8 * s) * 2u : kOutOfRange;
-        const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off), 0, 0);
-        hv[s] = make_uint4(v.x, v.y, v.z, v.w);
-    }
-}
-
-__device__ __forceinline__ void mfma_block(f32x16_t& acc, const bf16_t* wrow, const uint4 (&hv)[4], int kb,
-                                           int kofs) {
-    Frag<bf16_t> fw[4];
-#pragma unroll
-    for (int s = 0; s < 4; ++s) fw[s].v = *reinterpret_cast<const uint4*>(wrow + kb * 64 + kofs + 8 * s);
-#pragma unroll
-    for (int s = 0; s < 4; ++s) {
-        Frag<bf16_t> fh;
-        fh.v = hv[s];
-        mfma(acc, fw[s], fh);
-    }
-}
-
-template <int DEPTH>
-__device__ __forceinline__ void contract_rows(f32x16_t& acc, const bf16_t* wrow, __amdgpu_buffer_rsrc_t rs,
-                                              uint32_t roff, int kb0, int kb1, int kmax, int kofs) {
-    uint4 ring[DEPTH][4];
-#pragma unroll
-    for (int i = 0; i < DEPTH; ++i) load_block(ring[i], rs, roff, kb0 + i, kb1, kmax, kofs);
-    int kb = kb0;
-    for (; kb + DEPTH <= kb1; kb += DEPTH) {
-#pragma unroll
-        for (int i = 0; i < DEPTH; ++i) {
-            mfma_block(acc, wrow, ring[i], kb + i, kofs);
-            load_block(ring[i], rs, roff, kb + i + DEPTH, kb1, kmax, kofs);
-        }
-    }
-    // remaining blocks (fewer than DEPTH) are already in the ring
-#pragma unroll
-    for (int i = 0; i < DEPTH; ++i)
-        if (kb + i < kb1) mfma_block(acc, wrow, ring[i], kb + i, kofs);
 }
 
 // Sum the K parts of the waves that share a batch tile (KW > 1) through
@@ -456,13 +411,15 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
 // ---------------------------------------------------------------- backward
 struct BwdArgs {
     int H, B, t_eff, fixed;
-    int Ks;                            // interleaved gate columns per K slice (= H)
-    int Ksp;                           // Ks rounded up to 64
+    int nkg;                           // k-groups of 16 interleaved gate columns (4H / 16)
+    int ksp;                           // columns of the widest K slice (multiple of 16)
     const int32_t* active;
     const int32_t* offsets;
     const int32_t* perm;
     const bf16_t* Wh;                  // [4H, H] gate-major
-    bf16_t* G;                         // dG store [T*B x ldg] interleaved
+    bf16_t* G;                         // dG store [T*B x ldg] interleaved (for the contractions after the loop)
+    bf16_t* Gf;                        // [T] slots of dG in fragment layout (slot t = dG_t), K = 4H
+    int64_t gf_slot;                   // elements per slot: round_up(B, 32) * 4H
     const bf16_t* Gs;                  // saved gates, interleaved
     const float* Cs;
     const bf16_t* dy;                  // gradient of this layer's output or NULL
@@ -472,84 +429,87 @@ struct BwdArgs {
     const float* dcT;
     float* dh0;
     float* dc0;
-    float* part;                       // [kSlices x B x H]
+    float* part;                       // [t_eff + 1] slots of [kSlices x B x H] partial sums of dh
+    int xcd_groups;                    // 1: group members are 8 blocks apart (one XCD), 0: adjacent
     int64_t ldh, ldg;
     Sync* sync;
 };
 
-// WT[uu][kk] = (Wh interleaved)[s * Ks + kk][v0 + uu] = Wh[(c % 4) * H + c / 4][v0 + uu], c = s * Ks + kk
+// Slice s of the K = 4H interleaved gate columns: k-groups [s nkg / 4, (s + 1) nkg / 4).
+__device__ __forceinline__ int slice_kg0(int nkg, int s) { return s * nkg / kSlices; }
+
+// WT[uu][kk] = (Wh interleaved)[c][v0 + uu] = Wh[(c % 4) * H + c / 4][v0 + uu],  c = 16 kg0 + kk
 __device__ __forceinline__ void stage_bwd_weights(const BwdArgs& a, bf16_t* Ws, int wld, int s, int v0) {
     const int H = a.H;
+    const int c0 = 16 * slice_kg0(a.nkg, s), c1 = 16 * slice_kg0(a.nkg, s + 1);
 #pragma unroll 8
-    for (int idx = threadIdx.x; idx < kUnitsBwd * a.Ksp; idx += kThreads) {
+    for (int idx = threadIdx.x; idx < kUnitsBwd * a.ksp; idx += kThreads) {
         const int kk = idx / kUnitsBwd, uu = idx - kk * kUnitsBwd;
-        const int c = s * a.Ks + kk;
+        const int c = c0 + kk;
         const int u = v0 + uu;
         bf16_t v = 0;
-        if (kk < a.Ks && c < 4 * H && u < H) v = a.Wh[(int64_t(c & 3) * H + (c >> 2)) * H + u];
+        if (c < c1 && c < 4 * H && u < H) v = a.Wh[(int64_t(c & 3) * H + (c >> 2)) * H + u];
         Ws[uu * wld + kk] = v;
     }
 }
 
-// partial dh for units [v0, v0 + 32) from slice s of dG rows [off, off + rows)
-template <int KW>
-__device__ __forceinline__ void bwd_contract(const BwdArgs& a, const bf16_t* Ws, int wld, float* red, int s, int v0,
-                                             int64_t off, int rows) {
-    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
-    constexpr int NB = kWaves / KW;
-    const int bt = wave % NB, kw = wave / NB;
-    const int nkb = a.Ksp / 64;
-    const int kb0 = kw * nkb / KW, kb1 = (kw + 1) * nkb / KW;
-    const int kofs = (lane >> 5) * 32;
-    const int row = bt * 32 + (lane & 31);
-    f32x16_t acc;
-#pragma unroll
-    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
-    if (bt * 32 < rows) {
-        const auto rs = make_rsrc(a.G + off * a.ldg, uint32_t(rows) * uint32_t(a.ldg) * 2u);
-        const uint32_t roff = (uint32_t(row) * uint32_t(a.ldg) + uint32_t(s) * uint32_t(a.Ks) + uint32_t(kofs)) * 2u;
-        contract_rows<kDepthBwd>(acc, Ws + (lane & 31) * wld, rs, roff, kb0, kb1, a.Ks, kofs);
+// Barrier among the kSlices workgroups of one unit group (they exchange
+// partial sums only among themselves).  Same memory argument as the grid
+// barrier: the partial sums are written through, into addresses fresh for
+// each step.
+__device__ __forceinline__ void group_barrier(Sync* s, unsigned* cnt, unsigned& phase) {
+    ++phase;
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        spin_until(s, cnt, phase * unsigned(kSlices));
     }
-    reduce_kparts<KW>(acc, red, wave, lane);
-    if (kw == 0 && row < rows) {
-        // the partial-sum buffer is rewritten every step: write through
-        const auto rp = make_rsrc(a.part + int64_t(s) * a.B * a.H, uint32_t(a.B) * uint32_t(a.H) * 4u);
-#pragma unroll
-        for (int v = 0; v < 16; ++v) {
-            const int u = v0 + acc_row(v, lane);
-            const uint32_t o = u < a.H ? (uint32_t(row) * uint32_t(a.H) + uint32_t(u)) * 4u : kOutOfRange;
-            store4<kStoreThrough>(rp, o, acc[v]);
-        }
-    }
+    __syncthreads();
 }
 
 template <int KW>
 __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    const int wld = a.Ksp + 8;
+    const int wld = a.ksp + 8;
     bf16_t* Ws = reinterpret_cast<bf16_t*>(smem_raw);
     float* red = reinterpret_cast<float*>(smem_raw + size_t(kUnitsBwd) * wld * sizeof(bf16_t));
-    const int tid = threadIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int q = blockIdx.x;
-    const int s = q % kSlices, v0 = (q / kSlices) * kUnitsBwd;
+    // unit group v (32 units) and K slice s of this workgroup
+    const int s = a.xcd_groups ? (q / 8) % kSlices : q % kSlices;
+    const int v = a.xcd_groups ? (q % 8) + 8 * (q / (8 * kSlices)) : q / kSlices;
+    const int v0 = v * kUnitsBwd;
     const int H = a.H;
     Barrier bar;
     barrier_init(bar, a.sync);
+    unsigned* gcnt = &a.sync->group[v][0];
+    unsigned gphase = 0;
 
     stage_bwd_weights(a, Ws, wld, s, v0);
 
-    // cells owned for the pointwise part: units [8q, 8q + 8) x rows
-    float dhp[kCellsPerThread], dcr[kCellsPerThread];
+    // contraction geometry: wave (bt, kw) takes batch rows [32 bt, 32 bt + 32)
+    // and part kw of this slice's k-groups
+    constexpr int NB = kWaves / KW;
+    const int bt = wave % NB, kw = wave / NB;
+    const int sg0 = slice_kg0(a.nkg, s), sgn = slice_kg0(a.nkg, s + 1) - sg0;
+    const int kg0 = kw * sgn / KW, kg1 = (kw + 1) * sgn / KW;
+    const bf16_t* wrow = Ws + (lane & 31) * wld + 8 * (lane >> 5) + kg0 * 16;
+    const uint32_t goff = (uint32_t(bt * a.nkg + sg0 + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
+    const int crow = bt * 32 + (lane & 31);   // batch row of this lane's accumulator column
+
+    // pointwise ownership: row r, units [ub, ub + 4) (member s of the group
+    // takes units [v0 + 8 s, v0 + 8 s + 8))
+    const int r = tid >> 1;
+    const int ub = v0 + 8 * s + 4 * (tid & 1);
+    const bool mine = r < a.B && ub < H;
+    const int b = mine ? (a.perm ? a.perm[r] : r) : 0;
+    float dhp[4] = {0.f, 0.f, 0.f, 0.f}, dcr[4] = {0.f, 0.f, 0.f, 0.f}, cnx[4] = {0.f, 0.f, 0.f, 0.f};
+    if (mine) {
 #pragma unroll
-    for (int k = 0; k < kCellsPerThread; ++k) {
-        const int idx = tid + k * kThreads;
-        const int r = idx >> 3, u = q * 8 + (idx & 7);
-        dhp[k] = 0.f;
-        dcr[k] = 0.f;
-        if (r < a.B && u < H) {
-            const int b = a.perm ? a.perm[r] : r;
-            if (a.dhT) dhp[k] = a.dhT[int64_t(b) * H + u];
-            if (a.dcT) dcr[k] = a.dcT[int64_t(b) * H + u];
+        for (int k = 0; k < 4; ++k) {
+            if (a.dhT) dhp[k] = a.dhT[int64_t(b) * H + ub + k];
+            if (a.dcT) dcr[k] = a.dcT[int64_t(b) * H + ub + k];
         }
     }
     __syncthreads();
@@ -557,52 +517,111 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
     for (int t = a.t_eff - 1; t >= -1; --t) {
         const int act = t >= 0 ? act_at(a.active, a.fixed, a.B, t, a.t_eff) : a.B;
         const int act_next = act_at(a.active, a.fixed, a.B, t + 1, a.t_eff);
-        // partial sums of dh_t from dG_{t+1}
-        if (act_next > 0) {
-            bwd_contract<KW>(a, Ws, wld, red, s, v0, off_at(a.offsets, a.fixed, a.B, t + 1), act_next);
-            grid_barrier(bar);
-        }
         const int64_t off_t = t >= 0 ? off_at(a.offsets, a.fixed, a.B, t) : 0;
         const int64_t prev_base = t <= 0 ? 0 : int64_t(a.B) + off_at(a.offsets, a.fixed, a.B, t - 1);
+        const bool cell = mine && r < act && t >= 0;
+        // operands of the cell backward that do not depend on dh: load them
+        // before the contraction (lanes without a cell read out of range)
+        const int64_t p = off_t + r;
+        const auto rgs = make_rsrc(a.Gs + off_t * a.ldg, uint32_t(max(act, 0)) * uint32_t(a.ldg) * 2u);
+        const uint32_t ogs = cell ? (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u : kOutOfRange;
+        const uint4 g0 = load16(rgs, ogs), g1 = load16(rgs, ogs + 16u);
+        const auto rcp = make_rsrc(a.Cs + prev_base * a.ldh, uint32_t(a.B) * uint32_t(a.ldh) * 4u);
+        const uint4 cpv = load16(rcp, cell ? (uint32_t(r) * uint32_t(a.ldh) + uint32_t(ub)) * 4u : kOutOfRange);
+        // c_t: carried from the previous (later) step when the row was active there
+        const bool fresh = cell && r >= act_next;
+        const auto rcn = make_rsrc(a.Cs + (int64_t(a.B) + off_t) * a.ldh, uint32_t(a.B) * uint32_t(a.ldh) * 4u);
+        const uint4 cnv = load16(rcn, fresh ? (uint32_t(r) * uint32_t(a.ldh) + uint32_t(ub)) * 4u : kOutOfRange);
+        uint2 dyv = make_uint2(0, 0);
+        if (cell && a.dy) {
+            const int64_t yr = a.dy_rows ? int64_t(a.dy_rows[p]) : p;
+            dyv = *reinterpret_cast<const uint2*>(a.dy + yr * a.dy_ld + ub);
+        }
+
+        // partial sums of dh_t from dG_{t+1} (slot t + 1 of the fragment copy)
+        float* part = a.part + int64_t(t + 1) * kSlices * a.B * H;
+        if (act_next > 0) {
+            f32x16_t acc;
 #pragma unroll
-        for (int k = 0; k < kCellsPerThread; ++k) {
-            const int idx = tid + k * kThreads;
-            const int r = idx >> 3, u = q * 8 + (idx & 7);
-            if (r >= act || u >= H) continue;
-            float dhv = dhp[k];
+            for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+            if (bt * 32 < act_next) {
+                const auto rs = make_rsrc(a.Gf + int64_t(t + 1) * a.gf_slot, uint32_t(a.gf_slot) * 2u);
+                contract_frag<kDepthFrag>(acc, wrow, rs, goff, kg1 - kg0);
+            }
+            reduce_kparts<KW>(acc, red, wave, lane);
+            if (kw == 0 && crow < act_next) {
+                // lane holds units v0 + 8 j + 4 (lane / 32) + [0, 4) of row crow, j = 0..3
+                const auto rp = make_rsrc(part + int64_t(s) * a.B * H, uint32_t(a.B) * uint32_t(H) * 4u);
+#pragma unroll
+                for (int j = 0; j < 4; ++j) {
+                    const int u = v0 + 8 * j + 4 * (lane >> 5);
+                    const uint32_t o = u < H ? (uint32_t(crow) * uint32_t(H) + uint32_t(u)) * 4u : kOutOfRange;
+                    store16<kStoreThrough>(rp, o, make_uint4(__float_as_uint(acc[4 * j]), __float_as_uint(acc[4 * j + 1]),
+                                                             __float_as_uint(acc[4 * j + 2]),
+                                                             __float_as_uint(acc[4 * j + 3])));
+                }
+            }
+            group_barrier(a.sync, gcnt, gphase);
+        }
+
+        if (mine && r < act) {
+            float dh[4] = {dhp[0], dhp[1], dhp[2], dhp[3]};
             if (r < act_next) {
-                // reused every step: read past the caches, sum in slice order
-                const auto rp = make_rsrc(a.part, uint32_t(kSlices) * uint32_t(a.B) * uint32_t(H) * 4u);
-                dhv = 0.f;
+                // sum the slices in order
+                dh[0] = dh[1] = dh[2] = dh[3] = 0.f;
 #pragma unroll
-                for (int j = 0; j < kSlices; ++j)
-                    dhv += load4_bypass(rp, ((uint32_t(j) * uint32_t(a.B) + uint32_t(r)) * uint32_t(H) + uint32_t(u)) * 4u);
+                for (int j = 0; j < kSlices; ++j) {
+                    const float4 pv =
+                        *reinterpret_cast<const float4*>(part + (int64_t(j) * a.B + r) * H + ub);
+                    dh[0] += pv.x; dh[1] += pv.y; dh[2] += pv.z; dh[3] += pv.w;
+                }
             }
             if (t < 0) {
-                const int b = a.perm ? a.perm[r] : r;
-                if (a.dh0) a.dh0[int64_t(b) * H + u] = dhv;
-                if (a.dc0) a.dc0[int64_t(b) * H + u] = dcr[k];
-                continue;
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    if (a.dh0) a.dh0[int64_t(b) * H + ub + k] = dh[k];
+                    if (a.dc0) a.dc0[int64_t(b) * H + ub + k] = dcr[k];
+                }
+            } else {
+                const uint32_t gw[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+                const float cpr[4] = {__uint_as_float(cpv.x), __uint_as_float(cpv.y), __uint_as_float(cpv.z),
+                                      __uint_as_float(cpv.w)};
+                if (fresh) {
+                    cnx[0] = __uint_as_float(cnv.x); cnx[1] = __uint_as_float(cnv.y);
+                    cnx[2] = __uint_as_float(cnv.z); cnx[3] = __uint_as_float(cnv.w);
+                }
+                const float dyf[4] = {bf2f(bf16_t(dyv.x & 0xffffu)), bf2f(bf16_t(dyv.x >> 16)),
+                                      bf2f(bf16_t(dyv.y & 0xffffu)), bf2f(bf16_t(dyv.y >> 16))};
+                uint32_t dgw[8];
+#pragma unroll
+                for (int k = 0; k < 4; ++k) {
+                    const float dhv = dh[k] + dyf[k];
+                    const uint32_t w0 = gw[2 * k], w1 = gw[2 * k + 1];
+                    const float gi = bf2f(bf16_t(w0 & 0xffffu)), gf = bf2f(bf16_t(w0 >> 16));
+                    const float gg = bf2f(bf16_t(w1 & 0xffffu)), go = bf2f(bf16_t(w1 >> 16));
+                    const float tau = tanhf_(cnx[k]);
+                    const float d_o = dhv * tau;
+                    const float dct = dcr[k] + dhv * go * (1.f - tau * tau);
+                    dcr[k] = dct * gf;
+                    dgw[2 * k] = uint32_t(f2bf(dct * gg * gi * (1.f - gi))) |
+                                 (uint32_t(f2bf(dct * cpr[k] * gf * (1.f - gf))) << 16);
+                    dgw[2 * k + 1] = uint32_t(f2bf(dct * gi * (1.f - gg * gg))) |
+                                     (uint32_t(f2bf(d_o * go * (1.f - go))) << 16);
+                    cnx[k] = cpr[k];   // c_{t-1} is the next (earlier) step's c_t
+                }
+                // dG_t row-major (for the contractions after the loop) and in
+                // fragment layout (columns 4 ub .. 4 ub + 15: one k-group)
+                const auto rg = make_rsrc(a.G + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
+                const uint32_t og = (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
+                store16<kStoreThrough>(rg, og, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
+                store16<kStoreThrough>(rg, og + 16u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
+                {
+                    const auto rf = make_rsrc(a.Gf + int64_t(t) * a.gf_slot, uint32_t(a.gf_slot) * 2u);
+                    const uint32_t of = uint32_t(frag_index(r, 4 * ub, 4 * H)) * 2u;
+                    store16<kStoreThrough>(rf, of, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
+                    store16<kStoreThrough>(rf, of + 512u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
+                }
             }
-            const int64_t p = off_t + r;
-            if (a.dy) {
-                const int64_t yr = a.dy_rows ? int64_t(a.dy_rows[p]) : p;
-                dhv += bf2f(a.dy[yr * a.dy_ld + u]);
-            }
-            const uint2 gv = *reinterpret_cast<const uint2*>(a.Gs + p * a.ldg + 4 * u);
-            const float gi = bf2f(bf16_t(gv.x & 0xffffu)), gf = bf2f(bf16_t(gv.x >> 16));
-            const float gg = bf2f(bf16_t(gv.y & 0xffffu)), go = bf2f(bf16_t(gv.y >> 16));
-            const float c = a.Cs[(a.B + p) * a.ldh + u];
-            const float cp = a.Cs[(prev_base + r) * a.ldh + u];
-            const float tau = tanhf_(c);
-            const float d_o = dhv * tau;
-            const float dct = dcr[k] + dhv * go * (1.f - tau * tau);
-            dcr[k] = dct * gf;
-            uint2 dg;
-            dg.x = uint32_t(f2bf(dct * gg * gi * (1.f - gi))) | (uint32_t(f2bf(dct * cp * gf * (1.f - gf))) << 16);
-            dg.y = uint32_t(f2bf(dct * gi * (1.f - gg * gg))) | (uint32_t(f2bf(d_o * go * (1.f - go))) << 16);
-            const auto rg = make_rsrc(a.G + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
-            store8<kStoreThrough>(rg, (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(u)) * 2u, dg);
         }
         if (t >= 0 && act > 0) grid_barrier(bar);
     }
