@@ -94,20 +94,21 @@ __device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
     __syncthreads();
 }
 
-// Device-wide barrier.  Workgroups on one XCD share its L2, so only the last
-// of them to arrive releases (one L2 write-back per XCD) and signals the
-// global count; every workgroup waits until all XCDs have signalled.
-//
-// There is no per-workgroup acquire (an acquire would invalidate the XCD's
-// shared L2 once per workgroup and throw away the lines the other 31
-// workgroups are reading).  This is safe because of how the kernels address
-// memory within one launch: every location one workgroup reads after a
-// barrier that another workgroup wrote before it is either (a) a row written
-// during this launch for the first time and never read before the barrier
-// (h and dG rows of a step; rows are padded to whole 128-byte lines so that
-// no line is shared between steps), so no cache can hold an old copy, or
-// (b) read with the cache-bypassing policy (the reused partial-sum buffer).
-// Caches are invalidated by the dispatch at kernel start.
+// Device-wide barrier: every workgroup arrives on its XCD's counter, the
+// last arrival of each XCD signals the global count, and every workgroup
+// waits until all XCDs have signalled.  Arrivals are relaxed, with no L2
+// write-back and no invalidate.  That is safe because of how the kernels
+// address memory within one launch.  Every value one workgroup reads after a
+// barrier that another workgroup wrote before it is:
+//   * stored with the write-through policy, and acknowledged (each wave
+//     waits for its stores before the workgroup arrives), so it is in memory
+//     before the arrival; and
+//   * at an address written for the first time in this launch and never
+//     read before that barrier (a fresh slot per step; slots and rows are
+//     whole 128-byte lines), so no cache on the reading side holds a copy.
+// Results that only later kernels read are stored write-back; the end of the
+// kernel writes them back.  Caches are invalidated by the dispatch at
+// kernel start.
 //
 // After a timeout every later wait returns at once, so all waves still
 // reach the end of the kernel (results are then garbage and `error` is set).
@@ -115,11 +116,11 @@ __device__ __forceinline__ void grid_barrier(Barrier& b) {
     ++b.phase;
     __syncthreads();
     if (threadIdx.x == 0) {
-        __builtin_amdgcn_s_waitcnt(0);   // this workgroup's stores have reached the L2
+        __builtin_amdgcn_s_waitcnt(0);
         const unsigned old =
             __hip_atomic_fetch_add(&b.s->xcd[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (old == b.phase * b.xsize - 1u)
-            __hip_atomic_fetch_add(&b.s->count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+            __hip_atomic_fetch_add(&b.s->count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         spin_until(b.s, &b.s->count, b.nb + b.phase * b.nx);
     }
     __syncthreads();
@@ -211,18 +212,15 @@ __device__ __forceinline__ __amdgpu_buffer_rsrc_t make_rsrc(const void* base, ui
     return __builtin_amdgcn_make_buffer_rsrc(const_cast<void*>(base), (short)0, int(bytes), 0x00020000);
 }
 
-// Stores of per-step results that no other workgroup reads in this launch
-// use the sc0|sc1 cache policy (written through), so that the release at the
-// next barrier has little dirty data left to write back.
+// Store policies: values other workgroups read later in the same launch are
+// written through (sc0 | sc1) to memory; values only later kernels read are
+// written back through the L2 as usual.
 constexpr int kStoreThrough = 1 | 16;
-constexpr int kLoadBypass = 1 | 16;    // sc0 | sc1: read from the coherence point, not the caches
+constexpr int kStoreBack = 0;
 
 __device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
     const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off), 0, 0);
     return make_uint4(v.x, v.y, v.z, v.w);
-}
-__device__ __forceinline__ float load4_bypass(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
-    return __builtin_bit_cast(float, __builtin_amdgcn_raw_buffer_load_b32(rs, int(off), 0, kLoadBypass));
 }
 template <int POLICY>
 __device__ __forceinline__ void store4(__amdgpu_buffer_rsrc_t rs, uint32_t off, float v) {
@@ -325,6 +323,7 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
     const int row = bt * 32 + (lane & 31);   // this lane's batch row (sorted order)
     const int ub = u0 + 4 * (lane >> 5);      // its four consecutive units
     const bool owner = kw == 0;               // lanes of these waves own cells
+    const int b = (owner && row < a.B && a.perm) ? a.perm[row] : row;   // caller's batch index
     Barrier bar;
     barrier_init(bar, a.sync);
 
@@ -384,17 +383,16 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
             const auto rcs = make_rsrc(a.Cs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 4u);
             const auto rhs = make_rsrc(a.Hs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 2u);
             const auto rgs = make_rsrc(a.Gs + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
-            store16<kStoreThrough>(rcs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 4u,
+            store16<kStoreBack>(rcs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 4u,
                     make_uint4(__float_as_uint(creg[0]), __float_as_uint(creg[1]), __float_as_uint(creg[2]),
                                __float_as_uint(creg[3])));
-            store8<kStoreThrough>(rhs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 2u, hb);
+            store8<kStoreBack>(rhs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 2u, hb);
             const uint32_t og = (uint32_t(row) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
-            store16<kStoreThrough>(rgs, og, make_uint4(gw[0], gw[1], gw[2], gw[3]));
-            store16<kStoreThrough>(rgs, og + 16u, make_uint4(gw[4], gw[5], gw[6], gw[7]));
-            const int b = a.perm ? a.perm[row] : row;
+            store16<kStoreBack>(rgs, og, make_uint4(gw[0], gw[1], gw[2], gw[3]));
+            store16<kStoreBack>(rgs, og + 16u, make_uint4(gw[4], gw[5], gw[6], gw[7]));
             if (a.y) {
                 const auto ry = make_rsrc(a.y + int64_t(t) * a.B * H, uint32_t(a.B) * uint32_t(H) * 2u);
-                store8<kStoreThrough>(ry, (uint32_t(b) * uint32_t(H) + uint32_t(ub)) * 2u, hb);
+                store8<kStoreBack>(ry, (uint32_t(b) * uint32_t(H) + uint32_t(ub)) * 2u, hb);
             }
             if (row >= act_next) {   // last step of this sequence
 #pragma unroll
@@ -613,8 +611,8 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                 // fragment layout (columns 4 ub .. 4 ub + 15: one k-group)
                 const auto rg = make_rsrc(a.G + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
                 const uint32_t og = (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
-                store16<kStoreThrough>(rg, og, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
-                store16<kStoreThrough>(rg, og + 16u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
+                store16<kStoreBack>(rg, og, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
+                store16<kStoreBack>(rg, og + 16u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
                 {
                     const auto rf = make_rsrc(a.Gf + int64_t(t) * a.gf_slot, uint32_t(a.gf_slot) * 2u);
                     const uint32_t of = uint32_t(frag_index(r, 4 * ub, 4 * H)) * 2u;
