@@ -125,13 +125,23 @@ struct NtArgs {
     int M, N, K;
     int mt, nt, splits, ktiles_per_split;
     float* partial;             // [splits, M, N] when splits > 1
+    // MSE epilogue: d = C + bias - tgt; dY = scale d (bf16); per workgroup
+    // sum of d^2 into part_sq[block] and column sums of dY into
+    // part_col[m-tile * N + col]
+    const bf16_t* tgt;
+    bf16_t* dY;
+    float scale;
+    float* part_sq;
+    float* part_col;
 };
+
+enum NtEpilogue { kEpiStore = 0, kEpiPartial = 1, kEpiMse = 2 };
 
 constexpr uint32_t kNtOutOfRange = 0x80000000u;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-template <typename OutT, bool SCATTER, bool PARTIAL>
+template <typename OutT, bool SCATTER, int EPI>
 __global__ __launch_bounds__(NtCfg::NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
     using C_ = NtCfg;
@@ -259,7 +269,57 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
         sync();
         compute(stage0);
     }
-    if constexpr (PARTIAL) {
+    if constexpr (EPI == kEpiMse) {
+        const bf16_t* bias = static_cast<const bf16_t*>(g.bias);
+        float sq = 0.f;
+        float cs[C_::FN];
+#pragma unroll
+        for (int j = 0; j < C_::FN; ++j) {
+            cs[j] = 0.f;
+            const int col = n0 + wc0 + j * 32 + acc_col(lane);
+            if (col >= p.N) continue;
+            const float bv = bias ? bf2f(bias[col]) : 0.f;
+#pragma unroll
+            for (int i = 0; i < C_::FM; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = m0 + wr0 + i * 32 + acc_row(v, lane);
+                    if (row < p.M) {
+                        const int64_t o = int64_t(row) * p.N + col;
+                        const float d = acc[i][j][v] + bv - bf2f(p.tgt[o]);
+                        sq += d * d;
+                        const float dy = p.scale * d;
+                        p.dY[o] = f2bf(dy);
+                        cs[j] += dy;
+                    }
+                }
+        }
+        // lanes l and l ^ 32 hold the same columns; then the two wave rows
+        // meet in LDS (the stages are free now), in a fixed order
+#pragma unroll
+        for (int j = 0; j < C_::FN; ++j) cs[j] += __shfl_xor(cs[j], 32);
+#pragma unroll
+        for (int m = 1; m < 64; m <<= 1) sq += __shfl_xor(sq, m);
+        __syncthreads();
+        float* red = reinterpret_cast<float*>(stage0);   // [WGM][BN] column sums, then [8] squares
+        if (lane < 32) {
+#pragma unroll
+            for (int j = 0; j < C_::FN; ++j) red[(wave / C_::WGN) * C_::BN + wc0 + j * 32 + lane] = cs[j];
+        }
+        if (lane == 0) red[C_::WGM * C_::BN + wave] = sq;
+        __syncthreads();
+        if (tid < C_::BN && n0 + tid < p.N) {
+            float c = 0.f;
+#pragma unroll
+            for (int r = 0; r < C_::WGM; ++r) c += red[r * C_::BN + tid];
+            p.part_col[int64_t(m0 / C_::BM) * p.N + n0 + tid] = c;
+        }
+        if (tid == 0) {
+            float q = 0.f;
+            for (int w = 0; w < C_::NT / 64; ++w) q += red[C_::WGM * C_::BN + w];
+            p.part_sq[blockIdx.x] = q;
+        }
+    } else if constexpr (EPI == kEpiPartial) {
         float* P = p.partial + int64_t(split) * p.M * p.N;
 #pragma unroll
         for (int j = 0; j < C_::FN; ++j) {
@@ -451,11 +511,12 @@ const char* nt_label(bool f32out, bool scatter, bool partial) {
     return scatter ? "gemm_nt_bf16out_scatter" : "gemm_nt_bf16out";
 }
 
-template <typename OutT, bool SCATTER, bool PARTIAL>
+template <typename OutT, bool SCATTER, int EPI>
 janus_status launch_nt(const NtArgs& a, const GemmDesc& g, hipStream_t s) {
-    auto kern = &gemm_nt_fast_kernel<OutT, SCATTER, PARTIAL>;
-    const double out_bytes = PARTIAL ? 4.0 * a.splits : (sizeof(OutT) == 4 ? 4.0 : 2.0);
-    TraceScope trace(nt_label(sizeof(OutT) == 4, SCATTER, PARTIAL), 2.0 * g.M * g.N * double(g.K),
+    auto kern = &gemm_nt_fast_kernel<OutT, SCATTER, EPI>;
+    const double out_bytes = EPI == kEpiPartial ? 4.0 * a.splits : EPI == kEpiMse ? 4.0 : (sizeof(OutT) == 4 ? 4.0 : 2.0);
+    TraceScope trace(EPI == kEpiMse ? "gemm_nt_mse" : nt_label(sizeof(OutT) == 4, SCATTER, EPI == kEpiPartial),
+                     2.0 * g.M * g.N * double(g.K),
                      (double(g.M) * g.K + double(g.N) * g.K) * 2.0 + double(g.M) * g.N * out_bytes, s);
     hipLaunchKernelGGL(kern, dim3(unsigned(a.mt * a.nt * a.splits)), dim3(NtCfg::NT), 0, s, a, g);
     JANUS_LAUNCH_CHECK();
@@ -510,7 +571,7 @@ janus_status gemm_fast(const GemmDesc& g, const NtPlan& p, hipStream_t s) {
     a.ktiles_per_split = p.ktiles_per_split;
     if (p.splits > 1) {
         a.partial = reinterpret_cast<float*>(scratch + p.p_off);
-        if ((e = launch_nt<float, false, true>(a, g, s)) != JANUS_OK) return e;
+        if ((e = launch_nt<float, false, kEpiPartial>(a, g, s)) != JANUS_OK) return e;
         const int64_t n = int64_t(g.M) * g.N;
         TraceScope trace("splitk_reduce", 0.0, 4.0 * n * p.splits + n * (g.c_f32 ? 4.0 : 2.0), s);
         if (g.c_f32)
@@ -522,11 +583,78 @@ janus_status gemm_fast(const GemmDesc& g, const NtPlan& p, hipStream_t s) {
         JANUS_LAUNCH_CHECK();
         return JANUS_OK;
     }
-    if (g.c_f32) return g.c_idx ? launch_nt<float, true, false>(a, g, s) : launch_nt<float, false, false>(a, g, s);
-    return g.c_idx ? launch_nt<bf16_t, true, false>(a, g, s) : launch_nt<bf16_t, false, false>(a, g, s);
+    if (g.c_f32) return g.c_idx ? launch_nt<float, true, kEpiStore>(a, g, s) : launch_nt<float, false, kEpiStore>(a, g, s);
+    return g.c_idx ? launch_nt<bf16_t, true, kEpiStore>(a, g, s) : launch_nt<bf16_t, false, kEpiStore>(a, g, s);
 }
 
 }  // namespace
+
+// out[c] = sum over k < n of part[k * C + c], in order k = 0, 1, ...
+__global__ __launch_bounds__(256) void colpart_reduce_kernel(const float* part, int n, int C, float* out) {
+    const int c = blockIdx.x * 256 + threadIdx.x;
+    if (c >= C) return;
+    float s = 0.f;
+    for (int k = 0; k < n; ++k) s += part[int64_t(k) * C + c];
+    out[c] = s;
+}
+
+size_t gemm_mse_partials(int M, int N) {
+    const size_t mt = (M + NtCfg::BM - 1) / NtCfg::BM, nt = (N + NtCfg::BN - 1) / NtCfg::BN;
+    return mt * nt + mt * size_t(N);
+}
+
+bool gemm_mse_fast(int M, int N, int K, const void* h, const void* W) {
+    GemmDesc g;
+    g.dtype = JANUS_BF16;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.A = h;
+    g.lda = K;
+    g.B = W;
+    g.ldb = K;
+    const NtPlan p = plan_nt(g);
+    return p.fast && p.bytes == 0 && p.splits == 1;
+}
+
+janus_status gemm_mse(int M, int N, int K, const void* h, const void* W, const void* bias, const void* tgt, void* dY,
+                      float scale, float* part, float* db, hipStream_t s) {
+    if (!gemm_mse_fast(M, N, K, h, W)) return JANUS_ERR_UNSUPPORTED;
+    GemmDesc g;
+    g.dtype = JANUS_BF16;
+    g.M = M;
+    g.N = N;
+    g.K = K;
+    g.A = h;
+    g.lda = K;
+    g.B = W;
+    g.ldb = K;
+    g.bias = bias;
+    NtArgs a{};
+    a.A = static_cast<const bf16_t*>(h);
+    a.B = static_cast<const bf16_t*>(W);
+    a.lda = K;
+    a.ldb = K;
+    a.M = M;
+    a.N = N;
+    a.K = K;
+    a.mt = (M + NtCfg::BM - 1) / NtCfg::BM;
+    a.nt = (N + NtCfg::BN - 1) / NtCfg::BN;
+    a.splits = 1;
+    a.ktiles_per_split = (K + NtCfg::BK - 1) / NtCfg::BK;
+    a.tgt = static_cast<const bf16_t*>(tgt);
+    a.dY = static_cast<bf16_t*>(dY);
+    a.scale = scale;
+    a.part_sq = part;
+    a.part_col = part + size_t(a.mt) * a.nt;
+    janus_status e = launch_nt<float, false, kEpiMse>(a, g, s);
+    if (e != JANUS_OK) return e;
+    TraceScope trace("colpart_reduce", 0.0, 4.0 * double(a.mt) * N + 4.0 * N, s);
+    hipLaunchKernelGGL(colpart_reduce_kernel, dim3(unsigned((N + 255) / 256)), dim3(256), 0, s, a.part_col, a.mt, N,
+                       db);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
 
 size_t gemm_scratch_bytes(const GemmDesc& g) {
     const NtPlan p = plan_nt(g);

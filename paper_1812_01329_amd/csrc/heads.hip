@@ -242,7 +242,8 @@ size_t carve_mse(const janus_mse_desc& d, void* base, MseWs& w) {
     Carver c(base);
     w.dY = c.take<char>(int64_t(d.rows) * d.P * dtype_size(d.dtype));
     w.nparts = d.dtype == JANUS_BF16 ? mse_parts<HeadBF16>(d) : mse_parts<HeadF32>(d);
-    w.part = c.take<float>(w.nparts);
+    w.part = c.take<float>(d.dtype == JANUS_BF16 ? std::max<size_t>(size_t(w.nparts), gemm_mse_partials(d.rows, d.P))
+                                                 : size_t(w.nparts));
     w.cpart = c.take<float>(colsum_partial_floats(d.P));
     w.gs_bytes = head_gemm_scratch(d.dtype, d.rows, d.H, d.P);
     w.gs = c.take<char>(int64_t(w.gs_bytes));
@@ -254,26 +255,40 @@ janus_status mse_impl(const janus_mse_desc& d, const void* h, const void* W, con
                       void* dh, float* dW, float* db, float* loss, const MseWs& w, hipStream_t st) {
     const float count = float(int64_t(d.rows) * d.P);
     dim3 grid((d.P + Cfg::BN - 1) / Cfg::BN, (d.rows + Cfg::BM - 1) / Cfg::BM);
-    {
-    TraceScope trace("mse_gemm", 2.0 * d.rows * double(d.P) * d.H,
-                     double(sizeof(T)) * (double(d.rows) * d.H + double(d.P) * d.H + 2.0 * d.rows * double(d.P)), st);
-    const bool al = (int64_t(d.H) * int64_t(sizeof(T))) % 16 == 0 && reinterpret_cast<uintptr_t>(h) % 16 == 0 &&
-                    reinterpret_cast<uintptr_t>(W) % 16 == 0;
-    if (al)
-        hipLaunchKernelGGL((mse_gemm_kernel<T, Cfg, true>), grid, dim3(Cfg::NT), Cfg::SMEM_BYTES, st, d.rows, d.P,
-                           d.H, static_cast<const T*>(h), static_cast<const T*>(W), static_cast<const T*>(b),
-                           static_cast<const T*>(tgt), static_cast<T*>(w.dY), 2.f / count, w.part);
-    else
-        hipLaunchKernelGGL((mse_gemm_kernel<T, Cfg, false>), grid, dim3(Cfg::NT), Cfg::SMEM_BYTES, st, d.rows, d.P,
-                           d.H, static_cast<const T*>(h), static_cast<const T*>(W), static_cast<const T*>(b),
-                           static_cast<const T*>(tgt), static_cast<T*>(w.dY), 2.f / count, w.part);
-    JANUS_LAUNCH_CHECK();
+    // large bf16 shapes: the fast contraction with the loss in its epilogue,
+    // which also forms db
+    const bool fused = d.dtype == JANUS_BF16 && gemm_mse_fast(d.rows, d.P, d.H, h, W);
+    if (fused) {
+        janus_status e = gemm_mse(d.rows, d.P, d.H, h, W, b, tgt, w.dY, 2.f / count, w.part, db, st);
+        if (e != JANUS_OK) return e;
+        const int64_t nparts = int64_t((d.rows + 255) / 256) * ((d.P + 255) / 256);
+        TraceScope trace("finish_sum", 0.0, 4.0 * nparts, st);
+        hipLaunchKernelGGL(finish_sum_kernel, dim3(1), dim3(1024), 0, st, w.part, nparts, 1.f / count, loss);
+        JANUS_LAUNCH_CHECK();
+    } else {
+        {
+            TraceScope trace("mse_gemm", 2.0 * d.rows * double(d.P) * d.H,
+                             double(sizeof(T)) * (double(d.rows) * d.H + double(d.P) * d.H + 2.0 * d.rows * double(d.P)),
+                             st);
+            const bool al = (int64_t(d.H) * int64_t(sizeof(T))) % 16 == 0 &&
+                            reinterpret_cast<uintptr_t>(h) % 16 == 0 && reinterpret_cast<uintptr_t>(W) % 16 == 0;
+            if (al)
+                hipLaunchKernelGGL((mse_gemm_kernel<T, Cfg, true>), grid, dim3(Cfg::NT), Cfg::SMEM_BYTES, st, d.rows,
+                                   d.P, d.H, static_cast<const T*>(h), static_cast<const T*>(W),
+                                   static_cast<const T*>(b), static_cast<const T*>(tgt), static_cast<T*>(w.dY),
+                                   2.f / count, w.part);
+            else
+                hipLaunchKernelGGL((mse_gemm_kernel<T, Cfg, false>), grid, dim3(Cfg::NT), Cfg::SMEM_BYTES, st, d.rows,
+                                   d.P, d.H, static_cast<const T*>(h), static_cast<const T*>(W),
+                                   static_cast<const T*>(b), static_cast<const T*>(tgt), static_cast<T*>(w.dY),
+                                   2.f / count, w.part);
+            JANUS_LAUNCH_CHECK();
+        }
+        TraceScope trace("finish_sum", 0.0, 4.0 * w.nparts, st);
+        hipLaunchKernelGGL(finish_sum_kernel, dim3(1), dim3(1024), 0, st, w.part, int64_t(w.nparts), 1.f / count,
+                           loss);
+        JANUS_LAUNCH_CHECK();
     }
-    {
-    TraceScope trace("finish_sum", 0.0, 4.0 * w.nparts, st);
-    hipLaunchKernelGGL(finish_sum_kernel, dim3(1), dim3(1024), 0, st, w.part, int64_t(w.nparts), 1.f / count, loss);
-    }
-    JANUS_LAUNCH_CHECK();
     // dh = dY W
     GemmDesc g;
     g.dtype = d.dtype;
@@ -311,6 +326,7 @@ janus_status mse_impl(const janus_mse_desc& d, const void* h, const void* W, con
     q.scratch_bytes = w.gs_bytes;
     e = gemm(q, st);
     if (e != JANUS_OK) return e;
+    if (fused) return JANUS_OK;
     return colsum(d.dtype, w.dY, d.rows, d.P, d.P, db, w.cpart, st);
 }
 

@@ -743,6 +743,7 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.dh0 = dh0 ? dh0 + l * bh : nullptr;
             a.dc0 = dc0 ? dc0 + l * bh : nullptr;
             a.part = w.dpart;
+            a.db = db[l];
             a.ldh = w.ldh;
             a.ldg = w.ldg;
             a.sync = w.sync;
@@ -850,8 +851,10 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         g.ldc = H;
         e = gemm(g, st);
         if (e != JANUS_OK) return e;
-        e = colsum(d.dtype, w.XG, s.packed, 4 * H, w.ldg, db[l], w.part, st, rowmap);
-        if (e != JANUS_OK) return e;
+        if (!persistent) {   // the persistent backward forms db itself
+            e = colsum(d.dtype, w.XG, s.packed, 4 * H, w.ldg, db[l], w.part, st, rowmap);
+            if (e != JANUS_OK) return e;
+        }
         // gradient of this layer's input: dG Wx
         if (l > 0 || dx) {
             GemmDesc q;

@@ -303,7 +303,7 @@ __device__ __forceinline__ void contract_frag(f32x16_t& acc, const bf16_t* wrow,
     for (int v = 0; v < 16; ++v) acc[v] += acc1[v];
 }
 
-constexpr int kDepthFrag = 16;
+constexpr int kDepthFrag = 12;
 
 template <int KW>
 __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
@@ -428,6 +428,7 @@ struct BwdArgs {
     float* dh0;
     float* dc0;
     float* part;                       // [t_eff + 1] slots of [kSlices x B x H] partial sums of dh
+    float* db;                         // [4H] gate-major bias gradient (overwritten), or NULL
     int xcd_groups;                    // 1: group members are 8 blocks apart (one XCD), 0: adjacent
     int64_t ldh, ldg;
     Sync* sync;
@@ -503,6 +504,9 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
     const bool mine = r < a.B && ub < H;
     const int b = mine ? (a.perm ? a.perm[r] : r) : 0;
     float dhp[4] = {0.f, 0.f, 0.f, 0.f}, dcr[4] = {0.f, 0.f, 0.f, 0.f}, cnx[4] = {0.f, 0.f, 0.f, 0.f};
+    float dbs[16];   // running sum over steps of this thread's dG (unit k, gate g at 4 k + g)
+#pragma unroll
+    for (int e = 0; e < 16; ++e) dbs[e] = 0.f;
     if (mine) {
 #pragma unroll
         for (int k = 0; k < 4; ++k) {
@@ -601,10 +605,14 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                     const float d_o = dhv * tau;
                     const float dct = dcr[k] + dhv * go * (1.f - tau * tau);
                     dcr[k] = dct * gf;
-                    dgw[2 * k] = uint32_t(f2bf(dct * gg * gi * (1.f - gi))) |
-                                 (uint32_t(f2bf(dct * cpr[k] * gf * (1.f - gf))) << 16);
-                    dgw[2 * k + 1] = uint32_t(f2bf(dct * gi * (1.f - gg * gg))) |
-                                     (uint32_t(f2bf(d_o * go * (1.f - go))) << 16);
+                    const float dai = dct * gg * gi * (1.f - gi), daf = dct * cpr[k] * gf * (1.f - gf);
+                    const float dag = dct * gi * (1.f - gg * gg), dao = d_o * go * (1.f - go);
+                    dbs[4 * k] += dai;
+                    dbs[4 * k + 1] += daf;
+                    dbs[4 * k + 2] += dag;
+                    dbs[4 * k + 3] += dao;
+                    dgw[2 * k] = uint32_t(f2bf(dai)) | (uint32_t(f2bf(daf)) << 16);
+                    dgw[2 * k + 1] = uint32_t(f2bf(dag)) | (uint32_t(f2bf(dao)) << 16);
                     cnx[k] = cpr[k];   // c_{t-1} is the next (earlier) step's c_t
                 }
                 // dG_t row-major (for the contractions after the loop) and in
@@ -622,6 +630,32 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             }
         }
         if (t >= 0 && act > 0) grid_barrier(bar);
+    }
+
+    // bias gradient: sum dbs over the rows of this workgroup's units, in a
+    // fixed order (lanes of a wave by xor steps, then waves in order); the
+    // weight slice in LDS is no longer needed and holds the wave totals
+    if (a.db) {
+        // lanes 2 r' + half of a wave hold rows r' of one half: reduce over r'
+#pragma unroll
+        for (int e = 0; e < 16; ++e) {
+#pragma unroll
+            for (int m = 2; m < 64; m <<= 1) dbs[e] += __shfl_xor(dbs[e], m);
+        }
+        __syncthreads();
+        float* wsum = reinterpret_cast<float*>(smem_raw);   // [8 waves][2 halves][16]
+        if (lane < 2) {
+#pragma unroll
+            for (int e = 0; e < 16; ++e) wsum[(wave * 2 + lane) * 16 + e] = dbs[e];
+        }
+        __syncthreads();
+        if (tid < 32) {
+            const int half = tid >> 4, e = tid & 15;
+            float sum = 0.f;
+            for (int w = 0; w < kWaves; ++w) sum += wsum[(w * 2 + half) * 16 + e];
+            const int u = v0 + 8 * s + 4 * half + (e >> 2), g = e & 3;
+            if (u < H) a.db[int64_t(g) * H + u] = sum;
+        }
     }
 }
 

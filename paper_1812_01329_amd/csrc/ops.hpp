@@ -49,6 +49,16 @@ size_t gemm_scratch_bytes(const GemmDesc& g);
 // alignment and any gathered-row count (for sizing workspaces in advance)
 size_t gemm_scratch_bound(const GemmDesc& g);
 
+// Projection + MSE in one pass (bf16, K-contiguous h [M, K] and W [N, K]):
+// d = h W^T + bias - tgt, dY = scale d (bf16, [M, N]), part[0, mt * nt) =
+// per-workgroup sums of d^2 (mt, nt = tiles of 256 rows / columns), db[N] =
+// column sums of dY (float32, fixed order).  part needs gemm_mse_partials
+// floats.  gemm_mse_fast tells whether the shape and operands qualify.
+bool gemm_mse_fast(int M, int N, int K, const void* h, const void* W);
+size_t gemm_mse_partials(int M, int N);
+janus_status gemm_mse(int M, int N, int K, const void* h, const void* W, const void* bias, const void* tgt, void* dY,
+                      float scale, float* part, float* db, hipStream_t stream);
+
 // out[c * ld_out + r] = in[row(r) * ld_in + c] (bf16), row(r) = idx[r] or r,
 // for r < R, c < C; columns [R, R_pad) of each output row are zero.  C,
 // ld_in, ld_out, R_pad must be multiples of 8 and pointers 16-byte aligned.
