@@ -64,6 +64,8 @@ struct LstmWs {
     int64_t gf_slot = 0;                // elements per slot
     persist::Sync* sync = nullptr;
     void* GT = nullptr;                 // dG^T [4H x ldk] (bf16), K-contiguous operand of the weight gradients
+    std::vector<bf16_t*> HT;            // per layer: h transposed [H x ldht], columns [0, B) = h0 (persistent forward)
+    int64_t ldht = 0;
     bf16_t* Hf = nullptr;               // [T + 1] slots of h in fragment layout (persistent forward)
     int64_t hf_slot = 0;                // elements per slot
     void* gs = nullptr;                 // contraction scratch (transposed operands, split-K partials)
@@ -139,6 +141,9 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
         w.dpart = c.take<float>((int64_t(d.T) + 1) * persist::kSlices * d.B * d.H);
         w.gf_slot = round_up(d.B, 32) * int64_t(4) * d.H;
         w.Gf = c.take<bf16_t>(int64_t(d.T) * w.gf_slot);
+        w.ldht = round_up(int64_t(d.B) + TB, 64);
+        w.HT.assign(d.L, nullptr);
+        for (int l = 0; l < d.L; ++l) w.HT[l] = c.take<bf16_t>(int64_t(d.H) * w.ldht);
         w.hf_slot = round_up(d.B, 32) * round_up(d.H, 64);
         w.Hf = c.take<bf16_t>((int64_t(d.T) + 1) * w.hf_slot);
         w.ldk = round_up(TB, 64);
@@ -227,7 +232,8 @@ __global__ void interleave_rows_kernel(const T* src, T* dst, int H, int cols) {
 // persistent forward, into slot 0 of the fragment-layout copy Hf)
 template <typename T>
 __global__ void fwd_init_kernel(int B, int H, int64_t ldh, const int32_t* perm, const float* h0, const float* c0,
-                                T* Hs, float* Cs, int active0, float* hT, float* cT, T* Hf, int Kp) {
+                                T* Hs, float* Cs, int active0, float* hT, float* cT, T* Hf, int Kp, T* HT,
+                                int64_t ldht) {
     const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
     if (i >= int64_t(B) * H) return;
     const int r = int(i / H), u = int(i % H);
@@ -237,6 +243,7 @@ __global__ void fwd_init_kernel(int B, int H, int64_t ldh, const int32_t* perm, 
     Hs[int64_t(r) * ldh + u] = from_f<T>(hv);
     Cs[int64_t(r) * ldh + u] = cv;
     if (Hf) Hf[persist::frag_index(r, u, Kp)] = from_f<T>(hv);
+    if (HT) HT[int64_t(u) * ldht + r] = from_f<T>(hv);
     if (r >= active0) {   // a length-0 sequence ends in its initial state
         if (hT) hT[int64_t(b) * H + u] = hv;
         if (cT) cT[int64_t(b) * H + u] = cv;
@@ -527,6 +534,18 @@ double recurrent_rows(const SeqSchedule& s) {
     return r;
 }
 
+// With equal lengths the persistent forward also writes h transposed (HT,
+// h0 in the first B columns): HT is then h_{t-1} transposed for every
+// packed row (the dWh operand) and HT + B is the layer output transposed
+// (the next layer's dWx operand), both read in place (K = T B a multiple of 8).
+bool use_ht(const janus_lstm_desc& d, const SeqSchedule& s, bool persistent) {
+    return persistent && s.fixed && (int64_t(d.T) * d.B) % 8 == 0;
+}
+
+// The persistent backward writes dG transposed itself when the padded tail of
+// each row (past the packed count, to a multiple of 8) needs no zeros.
+bool gt_by_kernel(const SeqSchedule& s, bool persistent) { return persistent && s.packed % 8 == 0; }
+
 // One layer of the forward pass on the persistent path (bf16 only).
 janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s, const LstmWs& w, int l,
                                   const void* x, const int32_t* xrow, const void* Wx, const void* Wh, const void* b,
@@ -589,6 +608,8 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     a.ldg = w.ldg;
     a.Hf = w.Hf;
     a.hf_slot = w.hf_slot;
+    a.HT = use_ht(d, s, true) ? w.HT[l] : nullptr;
+    a.ldht = w.ldht;
     a.sync = w.sync;
     return launch_fwd_persistent(d, a, 2.0 * 4.0 * H * double(H) * recurrent_rows(s), st);
 }
@@ -621,7 +642,8 @@ janus_status lstm_fwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
                                perm, h0 ? h0 + l * bh : nullptr, c0 ? c0 + l * bh : nullptr,
                                static_cast<T*>(w.Hs[l]), w.Cs[l], s.active[0], hT ? hT + l * bh : nullptr,
                                cT ? cT + l * bh : nullptr, persistent ? reinterpret_cast<T*>(w.Hf) : nullptr,
-                               int(round_up(H, 64)));
+                               int(round_up(H, 64)), use_ht(d, s, persistent) ? reinterpret_cast<T*>(w.HT[l]) : nullptr,
+                               w.ldht);
             JANUS_LAUNCH_CHECK();
         }
         if (s.packed == 0) continue;
@@ -744,6 +766,8 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.dc0 = dc0 ? dc0 + l * bh : nullptr;
             a.part = w.dpart;
             a.db = db[l];
+            a.GT = gt_by_kernel(s, persistent) ? static_cast<bf16_t*>(w.GT) : nullptr;
+            a.ldk = w.ldk;
             a.ldh = w.ldh;
             a.ldg = w.ldg;
             a.sync = w.sync;
@@ -804,8 +828,9 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         const int32_t* rowmap = persistent ? w.perm4 : nullptr;   // interleaved gate rows -> torch rows
         const int Il = l == 0 ? d.I : H;
         // dG^T once for both weight gradients, so that they read it in place
+        // (written by the persistent backward itself when it can)
         const bool gt = w.GT && (4 * H) % 8 == 0;
-        if (gt) {
+        if (gt && !gt_by_kernel(s, persistent)) {
             janus_status e = transpose_bf16(w.XG, w.ldg, nullptr, s.packed, 4 * H, w.GT, w.ldk,
                                             round_up(s.packed, 64), st);
             if (e != JANUS_OK) return e;
@@ -827,11 +852,16 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         }
         g.scratch = w.gs;
         g.scratch_bytes = w.gs_bytes;
+        const bool ht = use_ht(d, s, persistent);
         g.b_t = true;
         if (l == 0) {
             g.B = x;
             g.ldb = d.I;
             g.b_idx = xrow;
+        } else if (ht) {
+            g.b_t = false;   // the layer below's output, transposed, in place
+            g.B = w.HT[l - 1] + B;
+            g.ldb = w.ldht;
         } else {
             g.B = static_cast<const T*>(w.Hs[l - 1]) + int64_t(B) * w.ldh;
             g.ldb = w.ldh;
@@ -844,9 +874,17 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         if (e != JANUS_OK) return e;
         // dWh = dG^T H_prev
         g.N = H;
-        g.B = w.Hs[l];
-        g.ldb = w.ldh;
-        g.b_idx = prevrow;
+        if (ht) {
+            g.b_t = false;   // h_{t-1} transposed, in place
+            g.B = w.HT[l];
+            g.ldb = w.ldht;
+            g.b_idx = nullptr;
+        } else {
+            g.b_t = true;
+            g.B = w.Hs[l];
+            g.ldb = w.ldh;
+            g.b_idx = prevrow;
+        }
         g.C = dWh[l];
         g.ldc = H;
         e = gemm(g, st);

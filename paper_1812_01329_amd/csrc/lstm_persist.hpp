@@ -144,6 +144,8 @@ struct FwdArgs {
     int64_t ldh, ldg;
     bf16_t* Hf;                        // [T + 1] slots of h in fragment layout (slot t = h_{t-1}; slot 0 = h0)
     int64_t hf_slot;                   // elements per slot: round_up(B, 32) * Kp
+    bf16_t* HT;                        // [H x ldht] h transposed, column B + p = h at packed row p, or NULL
+    int64_t ldht;
     Sync* sync;
 };
 
@@ -387,6 +389,12 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
                     make_uint4(__float_as_uint(creg[0]), __float_as_uint(creg[1]), __float_as_uint(creg[2]),
                                __float_as_uint(creg[3])));
             store8<kStoreBack>(rhs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 2u, hb);
+            if (a.HT) {
+                // transposed copy, the K-contiguous operand of the weight gradients
+                bf16_t* ht = a.HT + int64_t(ub) * a.ldht + a.B + off_t + row;
+#pragma unroll
+                for (int q = 0; q < 4; ++q) ht[q * a.ldht] = f2bf(hn[q]);
+            }
             const uint32_t og = (uint32_t(row) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
             store16<kStoreBack>(rgs, og, make_uint4(gw[0], gw[1], gw[2], gw[3]));
             store16<kStoreBack>(rgs, og + 16u, make_uint4(gw[4], gw[5], gw[6], gw[7]));
@@ -429,6 +437,8 @@ struct BwdArgs {
     float* dc0;
     float* part;                       // [t_eff + 1] slots of [kSlices x B x H] partial sums of dh
     float* db;                         // [4H] gate-major bias gradient (overwritten), or NULL
+    bf16_t* GT;                        // [4H x ldk] dG transposed (interleaved rows), or NULL
+    int64_t ldk;
     int xcd_groups;                    // 1: group members are 8 blocks apart (one XCD), 0: adjacent
     int64_t ldh, ldg;
     Sync* sync;
@@ -621,6 +631,15 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                 const uint32_t og = (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
                 store16<kStoreBack>(rg, og, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
                 store16<kStoreBack>(rg, og + 16u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
+                if (a.GT) {
+                    // transposed copy: the K-contiguous operand of the weight gradients
+                    bf16_t* gt = a.GT + int64_t(4) * ub * a.ldk + p;
+#pragma unroll
+                    for (int e = 0; e < 8; ++e) {
+                        gt[(2 * e) * a.ldk] = bf16_t(dgw[e] & 0xffffu);
+                        gt[(2 * e + 1) * a.ldk] = bf16_t(dgw[e] >> 16);
+                    }
+                }
                 {
                     const auto rf = make_rsrc(a.Gf + int64_t(t) * a.gf_slot, uint32_t(a.gf_slot) * 2u);
                     const uint32_t of = uint32_t(frag_index(r, 4 * ub, 4 * H)) * 2u;
