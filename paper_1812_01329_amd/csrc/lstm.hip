@@ -768,6 +768,7 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.db = db[l];
             a.GT = gt_by_kernel(s, persistent) ? static_cast<bf16_t*>(w.GT) : nullptr;
             a.ldk = w.ldk;
+            a.gt_pairs = (s.fixed && B % 2 == 0) ? 1 : 0;   // packed offsets t B all even
             a.ldh = w.ldh;
             a.ldg = w.ldg;
             a.sync = w.sync;

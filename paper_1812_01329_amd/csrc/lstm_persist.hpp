@@ -439,6 +439,7 @@ struct BwdArgs {
     float* db;                         // [4H] gate-major bias gradient (overwritten), or NULL
     bf16_t* GT;                        // [4H x ldk] dG transposed (interleaved rows), or NULL
     int64_t ldk;
+    int gt_pairs;                      // 1: every step's packed offset is even (row pairs as 4-byte stores)
     int xcd_groups;                    // 1: group members are 8 blocks apart (one XCD), 0: adjacent
     int64_t ldh, ldg;
     Sync* sync;
@@ -576,6 +577,8 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             group_barrier(a.sync, gcnt, gphase);
         }
 
+        uint32_t dgl[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // this step's dG (for the paired transposed copy)
+        const bool mine_cell = mine && r < act && t >= 0;
         if (mine && r < act) {
             float dh[4] = {dhp[0], dhp[1], dhp[2], dhp[3]};
             if (r < act_next) {
@@ -623,6 +626,8 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                     dbs[4 * k + 3] += dao;
                     dgw[2 * k] = uint32_t(f2bf(dai)) | (uint32_t(f2bf(daf)) << 16);
                     dgw[2 * k + 1] = uint32_t(f2bf(dag)) | (uint32_t(f2bf(dao)) << 16);
+                    dgl[2 * k] = dgw[2 * k];
+                    dgl[2 * k + 1] = dgw[2 * k + 1];
                     cnx[k] = cpr[k];   // c_{t-1} is the next (earlier) step's c_t
                 }
                 // dG_t row-major (for the contractions after the loop) and in
@@ -631,7 +636,7 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                 const uint32_t og = (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
                 store16<kStoreBack>(rg, og, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
                 store16<kStoreBack>(rg, og + 16u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
-                if (a.GT) {
+                if (a.GT && !a.gt_pairs) {
                     // transposed copy: the K-contiguous operand of the weight gradients
                     bf16_t* gt = a.GT + int64_t(4) * ub * a.ldk + p;
 #pragma unroll
@@ -645,6 +650,30 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                     const uint32_t of = uint32_t(frag_index(r, 4 * ub, 4 * H)) * 2u;
                     store16<kStoreThrough>(rf, of, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
                     store16<kStoreThrough>(rf, of + 512u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
+                }
+            }
+        }
+        if (a.GT && a.gt_pairs && t >= 0) {
+            // transposed copy with row pairs: lanes l and l ^ 2 hold rows r and
+            // r ^ 1 of the same units; the even row writes columns 4 ub + [0, 8)
+            // and the odd row columns 4 ub + [8, 16), 4 bytes (two rows) each.
+            // Lanes without a cell this step hold zeros and store nothing.
+            const bool odd = r & 1;
+            uint32_t mine[4], other[4];
+#pragma unroll
+            for (int i = 0; i < 4; ++i) {
+                mine[i] = odd ? dgl[4 + i] : dgl[i];
+                other[i] = __shfl_xor(odd ? dgl[i] : dgl[4 + i], 2);
+            }
+            if (mine_cell) {
+                const int64_t p0 = off_t + (r & ~1);
+                bf16_t* gt = a.GT + (int64_t(4) * ub + (odd ? 8 : 0)) * a.ldk + p0;
+#pragma unroll
+                for (int i = 0; i < 4; ++i) {
+                    const uint32_t lo = odd ? other[i] : mine[i];    // even row's dword
+                    const uint32_t hi = odd ? mine[i] : other[i];    // odd row's dword
+                    *reinterpret_cast<uint32_t*>(gt + (2 * i) * a.ldk) = (lo & 0xffffu) | (hi << 16);
+                    *reinterpret_cast<uint32_t*>(gt + (2 * i + 1) * a.ldk) = (lo >> 16) | (hi & 0xffff0000u);
                 }
             }
         }
