@@ -94,36 +94,50 @@ __device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
     __syncthreads();
 }
 
-// Device-wide barrier: every workgroup arrives on its XCD's counter, the
-// last arrival of each XCD signals the global count, and every workgroup
-// waits until all XCDs have signalled.  Arrivals are relaxed, with no L2
-// write-back and no invalidate.  That is safe because of how the kernels
-// address memory within one launch.  Every value one workgroup reads after a
-// barrier that another workgroup wrote before it is:
-//   * stored with the write-through policy, and acknowledged (each wave
-//     waits for its stores before the workgroup arrives), so it is in memory
-//     before the arrival; and
-//   * at an address written for the first time in this launch and never
-//     read before that barrier (a fresh slot per step; slots and rows are
-//     whole 128-byte lines), so no cache on the reading side holds a copy.
-// Results that only later kernels read are stored write-back; the end of the
-// kernel writes them back.  Caches are invalidated by the dispatch at
-// kernel start.
+// Device-wide barrier, in two halves so that work no other workgroup waits
+// for can run while it completes:
+//   barrier_arrive: every wave waits for its own memory operations, then the
+//     workgroup arrives on its XCD's counter; the last arrival of each XCD
+//     signals the global count;
+//   barrier_wait:   wait until all XCDs have signalled.
+// Between the two a workgroup may issue stores that nobody reads in this
+// launch and loads of data it owns.  The halves use the raw s_barrier (no
+// fence), so memory operations issued between them stay in flight across the
+// wait.
 //
-// After a timeout every later wait returns at once, so all waves still
-// reach the end of the kernel (results are then garbage and `error` is set).
-__device__ __forceinline__ void grid_barrier(Barrier& b) {
+// Arrivals are relaxed, with no L2 write-back and no invalidate.  That is
+// safe because of how the kernels address memory within one launch.  Every
+// value one workgroup reads after a barrier that another workgroup wrote
+// before it is:
+//   * stored with the write-through policy and acknowledged before the
+//     writer arrives, so it is in memory by then; and
+//   * at an address written for the first time in this launch and never read
+//     before that barrier (a fresh slot per step; slots and rows are whole
+//     128-byte lines), so no cache on the reading side holds a copy.
+// Results that only later kernels read are stored write-back; the end of the
+// kernel writes them back.  Caches are invalidated by the dispatch at kernel
+// start.
+//
+// After a timeout every later wait returns at once, so all waves still reach
+// the end of the kernel (results are then garbage and `error` is set).
+__device__ __forceinline__ void barrier_arrive(Barrier& b) {
     ++b.phase;
-    __syncthreads();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
     if (threadIdx.x == 0) {
-        __builtin_amdgcn_s_waitcnt(0);
         const unsigned old =
             __hip_atomic_fetch_add(&b.s->xcd[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         if (old == b.phase * b.xsize - 1u)
             __hip_atomic_fetch_add(&b.s->count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        spin_until(b.s, &b.s->count, b.nb + b.phase * b.nx);
     }
-    __syncthreads();
+}
+__device__ __forceinline__ void barrier_wait(Barrier& b) {
+    if (threadIdx.x == 0) spin_until(b.s, &b.s->count, b.nb + b.phase * b.nx);
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_barrier();
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
 // ---------------------------------------------------------------- forward
@@ -338,16 +352,26 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
     }
     __syncthreads();
 
+    // operand of the cell update that does not depend on h_{t-1}, loaded one
+    // step ahead (branch-free; lanes without a cell read out of range, i.e. 0)
+    uint4 xg0, xg1;
+    auto prefetch_xg = [&](int t) {
+        const int act = act_at(a.active, a.fixed, a.B, t, a.t_eff);
+        const int64_t off = off_at(a.offsets, a.fixed, a.B, t);
+        const auto rxg = make_rsrc(a.XG + off * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
+        const uint32_t o = (owner && row < act) ? (uint32_t(row) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u
+                                                : kOutOfRange;
+        xg0 = load16(rxg, o);
+        xg1 = load16(rxg, o + 16u);
+    };
+    prefetch_xg(0);
+
     for (int t = 0; t < a.t_eff; ++t) {
         const int act = act_at(a.active, a.fixed, a.B, t, a.t_eff);
         const int act_next = act_at(a.active, a.fixed, a.B, t + 1, a.t_eff);
         const int64_t off_t = off_at(a.offsets, a.fixed, a.B, t);
-        // operand of the cell update that does not depend on h_{t-1}: load it
-        // first (branch-free; lanes without a cell read out of range, i.e. 0)
         const bool cell = owner && row < act;
-        const auto rxg = make_rsrc(a.XG + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
-        const uint32_t oxg = cell ? (uint32_t(row) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u : kOutOfRange;
-        const uint4 xg0 = load16(rxg, oxg), xg1 = load16(rxg, oxg + 16u);
+        const bool more = t + 1 < a.t_eff;
         f32x16_t acc;
 #pragma unroll
         for (int v = 0; v < 16; ++v) acc[v] = 0.f;
@@ -357,10 +381,11 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
             contract_frag<kDepthFrag>(acc, wrow, rs, hoff, kg1 - kg0);
         }
         reduce_kparts<KW>(acc, red, wave, lane);
+        float hn[4] = {0.f, 0.f, 0.f, 0.f};
+        uint32_t gw[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
+        uint2 hb = make_uint2(0u, 0u);
         if (cell) {
             const uint32_t xw[8] = {xg0.x, xg0.y, xg0.z, xg0.w, xg1.x, xg1.y, xg1.z, xg1.w};
-            float hn[4];
-            uint32_t gw[8];
 #pragma unroll
             for (int q = 0; q < 4; ++q) {
                 const uint32_t w0 = xw[2 * q], w1 = xw[2 * q + 1];
@@ -374,13 +399,19 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
                 gw[2 * q] = uint32_t(f2bf(gi)) | (uint32_t(f2bf(gf)) << 16);
                 gw[2 * q + 1] = uint32_t(f2bf(gg)) | (uint32_t(f2bf(go)) << 16);
             }
-            const uint2 hb = make_uint2(uint32_t(f2bf(hn[0])) | (uint32_t(f2bf(hn[1])) << 16),
-                                        uint32_t(f2bf(hn[2])) | (uint32_t(f2bf(hn[3])) << 16));
-            // h_t for the next step (fragment layout, slot t + 1)
-            if (t + 1 < a.t_eff && row < act_next) {
+            hb = make_uint2(uint32_t(f2bf(hn[0])) | (uint32_t(f2bf(hn[1])) << 16),
+                            uint32_t(f2bf(hn[2])) | (uint32_t(f2bf(hn[3])) << 16));
+            // h_t for the next step (fragment layout, slot t + 1): the only
+            // value other workgroups read in this launch
+            if (more && row < act_next) {
                 const auto rhf = make_rsrc(a.Hf + int64_t(t + 1) * a.hf_slot, uint32_t(a.hf_slot) * 2u);
                 store8<kStoreThrough>(rhf, uint32_t(frag_index(row, ub, a.Kp)) * 2u, hb);
             }
+        }
+        if (more) barrier_arrive(bar);
+        // results for later kernels and the next step's operand, while the
+        // barrier completes
+        if (cell) {
             const int64_t nrow = int64_t(a.B) + off_t;   // first row of step t in Hs / Cs
             const auto rcs = make_rsrc(a.Cs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 4u);
             const auto rhs = make_rsrc(a.Hs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 2u);
@@ -410,7 +441,10 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
                 }
             }
         }
-        if (t + 1 < a.t_eff) grid_barrier(bar);
+        if (more) {
+            prefetch_xg(t + 1);
+            barrier_wait(bar);
+        }
     }
 }
 
@@ -527,29 +561,42 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
     }
     __syncthreads();
 
-    for (int t = a.t_eff - 1; t >= -1; --t) {
+    // operands of the cell backward that do not depend on dh, loaded one step
+    // ahead (lanes without a cell read out of range, i.e. 0)
+    uint4 g0, g1, cpv, cnv;
+    uint2 dyv;
+    auto prefetch = [&](int t) {
         const int act = t >= 0 ? act_at(a.active, a.fixed, a.B, t, a.t_eff) : a.B;
         const int act_next = act_at(a.active, a.fixed, a.B, t + 1, a.t_eff);
         const int64_t off_t = t >= 0 ? off_at(a.offsets, a.fixed, a.B, t) : 0;
         const int64_t prev_base = t <= 0 ? 0 : int64_t(a.B) + off_at(a.offsets, a.fixed, a.B, t - 1);
         const bool cell = mine && r < act && t >= 0;
-        // operands of the cell backward that do not depend on dh: load them
-        // before the contraction (lanes without a cell read out of range)
-        const int64_t p = off_t + r;
-        const auto rgs = make_rsrc(a.Gs + off_t * a.ldg, uint32_t(max(act, 0)) * uint32_t(a.ldg) * 2u);
+        const auto rgs = make_rsrc(a.Gs + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
         const uint32_t ogs = cell ? (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u : kOutOfRange;
-        const uint4 g0 = load16(rgs, ogs), g1 = load16(rgs, ogs + 16u);
+        g0 = load16(rgs, ogs);
+        g1 = load16(rgs, ogs + 16u);
         const auto rcp = make_rsrc(a.Cs + prev_base * a.ldh, uint32_t(a.B) * uint32_t(a.ldh) * 4u);
-        const uint4 cpv = load16(rcp, cell ? (uint32_t(r) * uint32_t(a.ldh) + uint32_t(ub)) * 4u : kOutOfRange);
-        // c_t: carried from the previous (later) step when the row was active there
+        cpv = load16(rcp, cell ? (uint32_t(r) * uint32_t(a.ldh) + uint32_t(ub)) * 4u : kOutOfRange);
+        // c_t is carried from the later step when the row was active there
         const bool fresh = cell && r >= act_next;
         const auto rcn = make_rsrc(a.Cs + (int64_t(a.B) + off_t) * a.ldh, uint32_t(a.B) * uint32_t(a.ldh) * 4u);
-        const uint4 cnv = load16(rcn, fresh ? (uint32_t(r) * uint32_t(a.ldh) + uint32_t(ub)) * 4u : kOutOfRange);
-        uint2 dyv = make_uint2(0, 0);
+        cnv = load16(rcn, fresh ? (uint32_t(r) * uint32_t(a.ldh) + uint32_t(ub)) * 4u : kOutOfRange);
+        dyv = make_uint2(0, 0);
         if (cell && a.dy) {
+            const int64_t p = off_t + r;
             const int64_t yr = a.dy_rows ? int64_t(a.dy_rows[p]) : p;
             dyv = *reinterpret_cast<const uint2*>(a.dy + yr * a.dy_ld + ub);
         }
+    };
+    prefetch(a.t_eff - 1);
+
+    for (int t = a.t_eff - 1; t >= -1; --t) {
+        const int act = t >= 0 ? act_at(a.active, a.fixed, a.B, t, a.t_eff) : a.B;
+        const int act_next = act_at(a.active, a.fixed, a.B, t + 1, a.t_eff);
+        const int64_t off_t = t >= 0 ? off_at(a.offsets, a.fixed, a.B, t) : 0;
+        const bool cell = mine && r < act && t >= 0;
+        const bool fresh = cell && r >= act_next;
+        const bool sync_after = t >= 0 && act > 0;
 
         // partial sums of dh_t from dG_{t+1} (slot t + 1 of the fragment copy)
         float* part = a.part + int64_t(t + 1) * kSlices * a.B * H;
@@ -577,10 +624,9 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             group_barrier(a.sync, gcnt, gphase);
         }
 
-        uint32_t dgl[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // this step's dG (for the paired transposed copy)
-        const bool mine_cell = mine && r < act && t >= 0;
+        uint32_t dgl[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // this step's dG, zero without a cell
+        float dh[4] = {dhp[0], dhp[1], dhp[2], dhp[3]};
         if (mine && r < act) {
-            float dh[4] = {dhp[0], dhp[1], dhp[2], dhp[3]};
             if (r < act_next) {
                 // sum the slices in order
                 dh[0] = dh[1] = dh[2] = dh[3] = 0.f;
@@ -591,65 +637,68 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                     dh[0] += pv.x; dh[1] += pv.y; dh[2] += pv.z; dh[3] += pv.w;
                 }
             }
-            if (t < 0) {
+        }
+        if (cell) {
+            const uint32_t gw[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
+            const float cpr[4] = {__uint_as_float(cpv.x), __uint_as_float(cpv.y), __uint_as_float(cpv.z),
+                                  __uint_as_float(cpv.w)};
+            if (fresh) {
+                cnx[0] = __uint_as_float(cnv.x); cnx[1] = __uint_as_float(cnv.y);
+                cnx[2] = __uint_as_float(cnv.z); cnx[3] = __uint_as_float(cnv.w);
+            }
+            const float dyf[4] = {bf2f(bf16_t(dyv.x & 0xffffu)), bf2f(bf16_t(dyv.x >> 16)),
+                                  bf2f(bf16_t(dyv.y & 0xffffu)), bf2f(bf16_t(dyv.y >> 16))};
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    if (a.dh0) a.dh0[int64_t(b) * H + ub + k] = dh[k];
-                    if (a.dc0) a.dc0[int64_t(b) * H + ub + k] = dcr[k];
-                }
-            } else {
-                const uint32_t gw[8] = {g0.x, g0.y, g0.z, g0.w, g1.x, g1.y, g1.z, g1.w};
-                const float cpr[4] = {__uint_as_float(cpv.x), __uint_as_float(cpv.y), __uint_as_float(cpv.z),
-                                      __uint_as_float(cpv.w)};
-                if (fresh) {
-                    cnx[0] = __uint_as_float(cnv.x); cnx[1] = __uint_as_float(cnv.y);
-                    cnx[2] = __uint_as_float(cnv.z); cnx[3] = __uint_as_float(cnv.w);
-                }
-                const float dyf[4] = {bf2f(bf16_t(dyv.x & 0xffffu)), bf2f(bf16_t(dyv.x >> 16)),
-                                      bf2f(bf16_t(dyv.y & 0xffffu)), bf2f(bf16_t(dyv.y >> 16))};
-                uint32_t dgw[8];
+            for (int k = 0; k < 4; ++k) {
+                const float dhv = dh[k] + dyf[k];
+                const uint32_t w0 = gw[2 * k], w1 = gw[2 * k + 1];
+                const float gi = bf2f(bf16_t(w0 & 0xffffu)), gf = bf2f(bf16_t(w0 >> 16));
+                const float gg = bf2f(bf16_t(w1 & 0xffffu)), go = bf2f(bf16_t(w1 >> 16));
+                const float tau = tanhf_(cnx[k]);
+                const float d_o = dhv * tau;
+                const float dct = dcr[k] + dhv * go * (1.f - tau * tau);
+                dcr[k] = dct * gf;
+                const float dai = dct * gg * gi * (1.f - gi), daf = dct * cpr[k] * gf * (1.f - gf);
+                const float dag = dct * gi * (1.f - gg * gg), dao = d_o * go * (1.f - go);
+                dbs[4 * k] += dai;
+                dbs[4 * k + 1] += daf;
+                dbs[4 * k + 2] += dag;
+                dbs[4 * k + 3] += dao;
+                dgl[2 * k] = uint32_t(f2bf(dai)) | (uint32_t(f2bf(daf)) << 16);
+                dgl[2 * k + 1] = uint32_t(f2bf(dag)) | (uint32_t(f2bf(dao)) << 16);
+                cnx[k] = cpr[k];   // c_{t-1} is the next (earlier) step's c_t
+            }
+            // dG_t in fragment layout (columns 4 ub .. 4 ub + 15: one k-group):
+            // the only value other workgroups read in this launch
+            const auto rf = make_rsrc(a.Gf + int64_t(t) * a.gf_slot, uint32_t(a.gf_slot) * 2u);
+            const uint32_t of = uint32_t(frag_index(r, 4 * ub, 4 * H)) * 2u;
+            store16<kStoreThrough>(rf, of, make_uint4(dgl[0], dgl[1], dgl[2], dgl[3]));
+            store16<kStoreThrough>(rf, of + 512u, make_uint4(dgl[4], dgl[5], dgl[6], dgl[7]));
+        }
+        if (sync_after) barrier_arrive(bar);
+
+        // results for later kernels and the next (earlier) step's operands,
+        // while the barrier completes
+        if (t < 0 && mine) {
 #pragma unroll
-                for (int k = 0; k < 4; ++k) {
-                    const float dhv = dh[k] + dyf[k];
-                    const uint32_t w0 = gw[2 * k], w1 = gw[2 * k + 1];
-                    const float gi = bf2f(bf16_t(w0 & 0xffffu)), gf = bf2f(bf16_t(w0 >> 16));
-                    const float gg = bf2f(bf16_t(w1 & 0xffffu)), go = bf2f(bf16_t(w1 >> 16));
-                    const float tau = tanhf_(cnx[k]);
-                    const float d_o = dhv * tau;
-                    const float dct = dcr[k] + dhv * go * (1.f - tau * tau);
-                    dcr[k] = dct * gf;
-                    const float dai = dct * gg * gi * (1.f - gi), daf = dct * cpr[k] * gf * (1.f - gf);
-                    const float dag = dct * gi * (1.f - gg * gg), dao = d_o * go * (1.f - go);
-                    dbs[4 * k] += dai;
-                    dbs[4 * k + 1] += daf;
-                    dbs[4 * k + 2] += dag;
-                    dbs[4 * k + 3] += dao;
-                    dgw[2 * k] = uint32_t(f2bf(dai)) | (uint32_t(f2bf(daf)) << 16);
-                    dgw[2 * k + 1] = uint32_t(f2bf(dag)) | (uint32_t(f2bf(dao)) << 16);
-                    dgl[2 * k] = dgw[2 * k];
-                    dgl[2 * k + 1] = dgw[2 * k + 1];
-                    cnx[k] = cpr[k];   // c_{t-1} is the next (earlier) step's c_t
-                }
-                // dG_t row-major (for the contractions after the loop) and in
-                // fragment layout (columns 4 ub .. 4 ub + 15: one k-group)
-                const auto rg = make_rsrc(a.G + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
-                const uint32_t og = (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
-                store16<kStoreBack>(rg, og, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
-                store16<kStoreBack>(rg, og + 16u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
-                if (a.GT && !a.gt_pairs) {
-                    // transposed copy: the K-contiguous operand of the weight gradients
-                    bf16_t* gt = a.GT + int64_t(4) * ub * a.ldk + p;
+            for (int k = 0; k < 4; ++k) {
+                if (a.dh0) a.dh0[int64_t(b) * H + ub + k] = dh[k];
+                if (a.dc0) a.dc0[int64_t(b) * H + ub + k] = dcr[k];
+            }
+        }
+        if (cell) {
+            // dG_t row-major (for the contractions after the loop)
+            const auto rg = make_rsrc(a.G + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
+            const uint32_t og = (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
+            store16<kStoreBack>(rg, og, make_uint4(dgl[0], dgl[1], dgl[2], dgl[3]));
+            store16<kStoreBack>(rg, og + 16u, make_uint4(dgl[4], dgl[5], dgl[6], dgl[7]));
+            if (a.GT && !a.gt_pairs) {
+                // transposed copy: the K-contiguous operand of the weight gradients
+                bf16_t* gt = a.GT + int64_t(4) * ub * a.ldk + off_t + r;
 #pragma unroll
-                    for (int e = 0; e < 8; ++e) {
-                        gt[(2 * e) * a.ldk] = bf16_t(dgw[e] & 0xffffu);
-                        gt[(2 * e + 1) * a.ldk] = bf16_t(dgw[e] >> 16);
-                    }
-                }
-                {
-                    const auto rf = make_rsrc(a.Gf + int64_t(t) * a.gf_slot, uint32_t(a.gf_slot) * 2u);
-                    const uint32_t of = uint32_t(frag_index(r, 4 * ub, 4 * H)) * 2u;
-                    store16<kStoreThrough>(rf, of, make_uint4(dgw[0], dgw[1], dgw[2], dgw[3]));
-                    store16<kStoreThrough>(rf, of + 512u, make_uint4(dgw[4], dgw[5], dgw[6], dgw[7]));
+                for (int e = 0; e < 8; ++e) {
+                    gt[(2 * e) * a.ldk] = bf16_t(dgl[e] & 0xffffu);
+                    gt[(2 * e + 1) * a.ldk] = bf16_t(dgl[e] >> 16);
                 }
             }
         }
@@ -657,27 +706,27 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             // transposed copy with row pairs: lanes l and l ^ 2 hold rows r and
             // r ^ 1 of the same units; the even row writes columns 4 ub + [0, 8)
             // and the odd row columns 4 ub + [8, 16), 4 bytes (two rows) each.
-            // Lanes without a cell this step hold zeros and store nothing.
             const bool odd = r & 1;
-            uint32_t mine[4], other[4];
+            uint32_t own[4], other[4];
 #pragma unroll
             for (int i = 0; i < 4; ++i) {
-                mine[i] = odd ? dgl[4 + i] : dgl[i];
+                own[i] = odd ? dgl[4 + i] : dgl[i];
                 other[i] = __shfl_xor(odd ? dgl[i] : dgl[4 + i], 2);
             }
-            if (mine_cell) {
+            if (cell) {
                 const int64_t p0 = off_t + (r & ~1);
                 bf16_t* gt = a.GT + (int64_t(4) * ub + (odd ? 8 : 0)) * a.ldk + p0;
 #pragma unroll
                 for (int i = 0; i < 4; ++i) {
-                    const uint32_t lo = odd ? other[i] : mine[i];    // even row's dword
-                    const uint32_t hi = odd ? mine[i] : other[i];    // odd row's dword
+                    const uint32_t lo = odd ? other[i] : own[i];    // even row's dword
+                    const uint32_t hi = odd ? own[i] : other[i];    // odd row's dword
                     *reinterpret_cast<uint32_t*>(gt + (2 * i) * a.ldk) = (lo & 0xffffu) | (hi << 16);
                     *reinterpret_cast<uint32_t*>(gt + (2 * i + 1) * a.ldk) = (lo >> 16) | (hi & 0xffff0000u);
                 }
             }
         }
-        if (t >= 0 && act > 0) grid_barrier(bar);
+        if (t >= 0) prefetch(t - 1);
+        if (sync_after) barrier_wait(bar);
     }
 
     // bias gradient: sum dbs over the rows of this workgroup's units, in a
