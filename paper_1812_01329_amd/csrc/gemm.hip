@@ -389,6 +389,40 @@ __global__ __launch_bounds__(256) void transpose_bf16_kernel(const bf16_t* in, i
     }
 }
 
+// The same as transpose_bf16_kernel for any alignment and C: a 64 x 64 tile
+// through LDS, one element per access.
+__global__ __launch_bounds__(256) void transpose_any_kernel(const bf16_t* in, int64_t ld_in, const int32_t* idx,
+                                                            int64_t R, int C, bf16_t* out, int64_t ld_out,
+                                                            int64_t R_pad) {
+    __shared__ bf16_t tile[64][65];
+    const int64_t r0 = int64_t(blockIdx.x) * 64;
+    const int c0 = blockIdx.y * 64;
+    const int tx = threadIdx.x & 63, ty = threadIdx.x >> 6;
+    for (int rr = ty; rr < 64; rr += 4) {
+        const int64_t r = r0 + rr;
+        const int c = c0 + tx;
+        bf16_t v = 0;
+        if (r < R && c < C) v = in[(idx ? int64_t(idx[r]) : r) * ld_in + c];
+        tile[rr][tx] = v;
+    }
+    __syncthreads();
+    for (int cc = ty; cc < 64; cc += 4) {
+        const int c = c0 + cc;
+        const int64_t r = r0 + tx;
+        if (c < C && r < R_pad) out[int64_t(c) * ld_out + r] = tile[tx][cc];
+    }
+}
+
+// out[r * ld_out + k] = in[row(r) * ld_in + k] for k < K, 0 for K <= k < K_pad
+__global__ __launch_bounds__(256) void copy_rows_kernel(const bf16_t* in, int64_t ld_in, const int32_t* idx,
+                                                        int64_t R, int K, bf16_t* out, int64_t ld_out, int K_pad) {
+    const int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x;
+    if (i >= R * K_pad) return;
+    const int64_t r = i / K_pad;
+    const int k = int(i % K_pad);
+    out[r * ld_out + k] = k < K ? in[(idx ? int64_t(idx[r]) : r) * ld_in + k] : bf16_t(0);
+}
+
 const char* gemm_label(bool at, bool bt, bool bf16) {
     if (!at && !bt) return bf16 ? "gemm_nt_bf16" : "gemm_nt_f32";
     if (!at && bt) return bf16 ? "gemm_nn_bf16" : "gemm_nn_f32";
@@ -461,9 +495,16 @@ using CfgF32 = TileCfg<float, 64, 64, 32, 2, 2>;
 namespace {
 
 // How a contraction runs on the fast NT path, and the scratch it needs.
+// How an operand reaches the kernel: read in place, or first written to
+// scratch as a K-contiguous copy (transposed when stored K-major, padded with
+// zeros to a 16-byte multiple of K when its rows cannot be read in 16-byte
+// chunks).
+enum OperandMode { kInPlace = 0, kCopyRows = 1, kCopyTransposed = 2 };
+
 struct NtPlan {
     bool fast = false;
-    int64_t ldt = 0;                 // leading dimension of transposed copies (K rounded to 64)
+    int64_t ldt = 0;                 // leading dimension of copies (K rounded to 64)
+    int amode = kInPlace, bmode = kInPlace;
     int splits = 1, ktiles_per_split = 0;
     size_t a_off = 0, b_off = 0, p_off = 0, bytes = 0;
 };
@@ -473,20 +514,18 @@ bool rows16(const void* p, int64_t ld) { return reinterpret_cast<uintptr_t>(p) %
 NtPlan plan_nt(const GemmDesc& g) {
     NtPlan p;
     if (g.dtype != JANUS_BF16 || g.M < 128 || g.N < 128 || g.K < 64) return p;
-    // an operand read in place is read in 16-byte chunks along K; transposed
-    // copies are zero-padded along K to a multiple of 64
-    if (g.K % 8 != 0 && ((!g.a_t && !g.a_zero_pad) || (!g.b_t && !g.b_zero_pad))) return p;
     constexpr int64_t kMaxOff = int64_t(1) << 31;
-    // an operand read in place: 16-byte chunks along K, byte offsets in 31 bits
-    auto in_place_ok = [&](const void* ptr, int64_t ld, const int32_t* idx, int64_t src_rows) {
-        if (!rows16(ptr, ld)) return false;
+    // an operand read in place: 16-byte chunks along K (K a multiple of 8, or
+    // rows zero-padded past K), byte offsets in 31 bits
+    auto in_place_ok = [&](const void* ptr, int64_t ld, const int32_t* idx, int64_t src_rows, bool zero_pad) {
+        if (!rows16(ptr, ld) || (g.K % 8 != 0 && !zero_pad)) return false;
         if (idx) return src_rows > 0 && src_rows * ld * 2 < kMaxOff;
         return int64_t(NtCfg::BM) * ld * 2 < kMaxOff;
     };
-    // an operand transposed first: read in 16-byte chunks along its rows
-    auto transpose_ok = [&](const void* ptr, int64_t ld, int cols) { return rows16(ptr, ld) && cols % 8 == 0; };
-    if (g.a_t ? !transpose_ok(g.A, g.lda, g.M) : !in_place_ok(g.A, g.lda, g.a_idx, g.a_src_rows)) return p;
-    if (g.b_t ? !transpose_ok(g.B, g.ldb, g.N) : !in_place_ok(g.B, g.ldb, g.b_idx, g.b_src_rows)) return p;
+    p.amode = g.a_t ? kCopyTransposed
+                    : in_place_ok(g.A, g.lda, g.a_idx, g.a_src_rows, g.a_zero_pad) ? kInPlace : kCopyRows;
+    p.bmode = g.b_t ? kCopyTransposed
+                    : in_place_ok(g.B, g.ldb, g.b_idx, g.b_src_rows, g.b_zero_pad) ? kInPlace : kCopyRows;
     p.ldt = round_up(int64_t(g.K), 64);
     if (int64_t(NtCfg::BM) * p.ldt * 2 >= kMaxOff) return p;
     const int tiles = ((g.M + NtCfg::BM - 1) / NtCfg::BM) * ((g.N + NtCfg::BN - 1) / NtCfg::BN);
@@ -497,8 +536,8 @@ NtPlan plan_nt(const GemmDesc& g) {
     p.splits = (ktiles + p.ktiles_per_split - 1) / p.ktiles_per_split;
     size_t off = 0;
     auto take = [&](size_t bytes) { const size_t o = off; off += (bytes + 255) / 256 * 256; return o; };
-    if (g.a_t) p.a_off = take(size_t(g.M) * p.ldt * 2);
-    if (g.b_t) p.b_off = take(size_t(g.N) * p.ldt * 2);
+    if (p.amode != kInPlace) p.a_off = take(size_t(g.M) * p.ldt * 2);
+    if (p.bmode != kInPlace) p.b_off = take(size_t(g.N) * p.ldt * 2);
     if (p.splits > 1) p.p_off = take(size_t(p.splits) * g.M * g.N * 4);
     p.bytes = off;
     p.fast = true;
@@ -527,8 +566,24 @@ janus_status transpose_launch(const bf16_t* in, int64_t ld_in, const int32_t* id
                               int64_t ld_out, int64_t R_pad, hipStream_t s) {
     if (R_pad <= 0 || C <= 0) return JANUS_OK;
     TraceScope trace("transpose_bf16", 0.0, 2.0 * (double(R) * C + double(R_pad) * C), s);
-    dim3 grid(unsigned((R_pad + 63) / 64), unsigned((C + 255) / 256));
-    hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, s, in, ld_in, idx, R, C, out, ld_out, R_pad);
+    if (rows16(in, ld_in) && rows16(out, ld_out) && C % 8 == 0 && R_pad % 8 == 0) {
+        dim3 grid(unsigned((R_pad + 63) / 64), unsigned((C + 255) / 256));
+        hipLaunchKernelGGL(transpose_bf16_kernel, grid, dim3(256), 0, s, in, ld_in, idx, R, C, out, ld_out, R_pad);
+    } else {
+        dim3 grid(unsigned((R_pad + 63) / 64), unsigned((C + 63) / 64));
+        hipLaunchKernelGGL(transpose_any_kernel, grid, dim3(256), 0, s, in, ld_in, idx, R, C, out, ld_out, R_pad);
+    }
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+janus_status copy_rows_launch(const bf16_t* in, int64_t ld_in, const int32_t* idx, int64_t R, int K, bf16_t* out,
+                              int64_t ld_out, int K_pad, hipStream_t s) {
+    const int64_t n = R * K_pad;
+    if (n <= 0) return JANUS_OK;
+    TraceScope trace("copy_rows_bf16", 0.0, 2.0 * (double(R) * K + double(n)), s);
+    hipLaunchKernelGGL(copy_rows_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, s, in, ld_in, idx, R, K, out,
+                       ld_out, K_pad);
     JANUS_LAUNCH_CHECK();
     return JANUS_OK;
 }
@@ -540,31 +595,25 @@ janus_status gemm_fast(const GemmDesc& g, const NtPlan& p, hipStream_t s) {
     a.N = g.N;
     a.K = g.K;
     janus_status e;
-    if (g.a_t) {
-        // A(m, k) = A[row(k) * lda + m]: transpose to [M, K]
-        bf16_t* t = reinterpret_cast<bf16_t*>(scratch + p.a_off);
-        if ((e = transpose_launch(static_cast<const bf16_t*>(g.A), g.lda, g.a_idx, g.K, g.M, t, p.ldt, p.ldt, s)) !=
-            JANUS_OK)
-            return e;
-        a.A = t;
-        a.lda = p.ldt;
-    } else {
-        a.A = static_cast<const bf16_t*>(g.A);
-        a.lda = g.lda;
-        a.a_idx = g.a_idx;
-    }
-    if (g.b_t) {
-        bf16_t* t = reinterpret_cast<bf16_t*>(scratch + p.b_off);
-        if ((e = transpose_launch(static_cast<const bf16_t*>(g.B), g.ldb, g.b_idx, g.K, g.N, t, p.ldt, p.ldt, s)) !=
-            JANUS_OK)
-            return e;
-        a.B = t;
-        a.ldb = p.ldt;
-    } else {
-        a.B = static_cast<const bf16_t*>(g.B);
-        a.ldb = g.ldb;
-        a.b_idx = g.b_idx;
-    }
+    // each operand as the kernel reads it: rows of K contiguous elements
+    auto prepare = [&](int mode, const void* src, int64_t ld, const int32_t* idx, int rows, size_t off,
+                       const bf16_t*& op, int64_t& op_ld, const int32_t*& op_idx) -> janus_status {
+        if (mode == kInPlace) {
+            op = static_cast<const bf16_t*>(src);
+            op_ld = ld;
+            op_idx = idx;
+            return JANUS_OK;
+        }
+        bf16_t* t = reinterpret_cast<bf16_t*>(scratch + off);
+        op = t;
+        op_ld = p.ldt;
+        op_idx = nullptr;
+        if (mode == kCopyTransposed)   // element (row, k) at src[idx(k) * ld + row]
+            return transpose_launch(static_cast<const bf16_t*>(src), ld, idx, g.K, rows, t, p.ldt, p.ldt, s);
+        return copy_rows_launch(static_cast<const bf16_t*>(src), ld, idx, rows, g.K, t, p.ldt, int(p.ldt), s);
+    };
+    if ((e = prepare(p.amode, g.A, g.lda, g.a_idx, g.M, p.a_off, a.A, a.lda, a.a_idx)) != JANUS_OK) return e;
+    if ((e = prepare(p.bmode, g.B, g.ldb, g.b_idx, g.N, p.b_off, a.B, a.ldb, a.b_idx)) != JANUS_OK) return e;
     a.mt = (g.M + NtCfg::BM - 1) / NtCfg::BM;
     a.nt = (g.N + NtCfg::BN - 1) / NtCfg::BN;
     a.splits = p.splits;
@@ -663,15 +712,16 @@ size_t gemm_scratch_bytes(const GemmDesc& g) {
 
 size_t gemm_scratch_bound(const GemmDesc& g) {
     GemmDesc q = g;
-    q.A = q.B = nullptr;            // aligned stand-ins: alignment only ever removes scratch
+    q.A = q.B = nullptr;            // 16-byte aligned stand-ins (unaligned caller tensors may need more;
+                                    // gemm() then takes the slower path that needs none)
     q.a_src_rows = q.a_idx ? int64_t(1) : 0;
     q.b_src_rows = q.b_idx ? int64_t(1) : 0;
     const NtPlan p = plan_nt(q);
     if (!p.fast) return 0;
     const int tiles = ((g.M + NtCfg::BM - 1) / NtCfg::BM) * ((g.N + NtCfg::BN - 1) / NtCfg::BN);
     size_t b = 0;
-    if (g.a_t) b += (size_t(g.M) * p.ldt * 2 + 255) / 256 * 256;
-    if (g.b_t) b += (size_t(g.N) * p.ldt * 2 + 255) / 256 * 256;
+    if (p.amode != kInPlace) b += (size_t(g.M) * p.ldt * 2 + 255) / 256 * 256;
+    if (p.bmode != kInPlace) b += (size_t(g.N) * p.ldt * 2 + 255) / 256 * 256;
     if (tiles < 160) b += (size_t(8) * g.M * g.N * 4 + 255) / 256 * 256;
     return b;
 }

@@ -939,6 +939,185 @@ janus_status upload_schedule(const SeqSchedule& s, const LstmWs& w, hipStream_t 
     return upload(w.off_dev, s.offsets.data(), sizeof(int32_t) * (s.T + 2), st);
 }
 
+// ------------------------------------------------------- padded problems
+// A bf16 problem whose hidden size is not a multiple of 16 or whose input
+// size is not a multiple of 8 runs as the same problem with those sizes
+// rounded up (zero weights, inputs and initial state in the added units and
+// input features), so that every row is a whole number of 16-byte chunks and
+// the fast paths apply.  An added unit then stays exactly 0 (its gates are
+// i = f = o = 1/2, g = 0, so c and h stay 0), feeds nothing (its weight
+// columns are 0) and receives zero gradients, so the results on the real
+// units are those of the unpadded problem.  Parameters and inputs are copied
+// in (padded) and results copied out on every call.
+bool needs_padding(const janus_lstm_desc& d) { return d.dtype == JANUS_BF16 && (d.H % 16 != 0 || d.I % 8 != 0); }
+
+janus_lstm_desc padded_desc(const janus_lstm_desc& d) {
+    janus_lstm_desc p = d;
+    p.H = int(round_up(d.H, 16));
+    p.I = int(round_up(d.I, 8));
+    return p;
+}
+
+struct PadWs {
+    std::vector<void*> Wx, Wh, b;      // padded parameters (bf16, gate-major rows of Hp units)
+    std::vector<float*> dWx, dWh, db;  // padded gradients (float32)
+    void* x = nullptr;                 // [T*B x Ip]
+    void* y = nullptr;                 // [T*B x Hp], and dy in the backward
+    void* dx = nullptr;                // [T*B x Ip]
+    float* s0 = nullptr;               // four [L*B x Hp] float32 state buffers
+    float* s1 = nullptr;
+    float* s2 = nullptr;
+    float* s3 = nullptr;
+};
+
+// the padded problem's own workspace comes first, then the copies
+size_t carve_pad(const janus_lstm_desc& d, void* base, PadWs& w) {
+    const janus_lstm_desc p = padded_desc(d);
+    LstmWs inner;
+    Carver c(base);
+    c.take<char>(carve(p, nullptr, inner));
+    const int64_t TB = int64_t(d.T) * d.B, LB = int64_t(d.L) * d.B;
+    w.Wx.assign(d.L, nullptr);
+    w.Wh.assign(d.L, nullptr);
+    w.b.assign(d.L, nullptr);
+    w.dWx.assign(d.L, nullptr);
+    w.dWh.assign(d.L, nullptr);
+    w.db.assign(d.L, nullptr);
+    for (int l = 0; l < d.L; ++l) {
+        const int64_t Il = l == 0 ? p.I : p.H;
+        w.Wx[l] = c.take<bf16_t>(int64_t(4) * p.H * Il);
+        w.Wh[l] = c.take<bf16_t>(int64_t(4) * p.H * p.H);
+        w.b[l] = c.take<bf16_t>(int64_t(4) * p.H);
+        w.dWx[l] = c.take<float>(int64_t(4) * p.H * Il);
+        w.dWh[l] = c.take<float>(int64_t(4) * p.H * p.H);
+        w.db[l] = c.take<float>(int64_t(4) * p.H);
+    }
+    w.x = c.take<bf16_t>(TB * p.I);
+    w.y = c.take<bf16_t>(TB * p.H);
+    w.dx = c.take<bf16_t>(TB * p.I);
+    w.s0 = c.take<float>(LB * p.H);
+    w.s1 = c.take<float>(LB * p.H);
+    w.s2 = c.take<float>(LB * p.H);
+    w.s3 = c.take<float>(LB * p.H);
+    return c.off + 256;
+}
+
+// dst[r, c] (r < rows, c < cols) = src[sr, c] for c < scols, else 0, where
+// the source row sr is r (gate_dH == 0) or, for gate-major parameter rows,
+// gate g = r / gate_dH, unit u = r % gate_dH, sr = g * gate_sH + u (no source
+// row, i.e. 0, when u >= gate_sH).
+template <typename T>
+__global__ void remap_kernel(const T* src, int64_t sld, int scols, T* dst, int64_t dld, int64_t rows, int cols,
+                             int gate_sH, int gate_dH) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= rows * cols) return;
+    const int64_t r = i / cols;
+    const int c = int(i % cols);
+    int64_t sr = r;
+    bool ok = c < scols;
+    if (gate_dH > 0) {
+        const int64_t g = r / gate_dH, u = r % gate_dH;
+        ok = ok && u < gate_sH;
+        sr = g * gate_sH + u;
+    }
+    dst[r * dld + c] = ok ? src[sr * sld + c] : T(0);
+}
+
+template <typename T>
+janus_status remap(const void* src, int64_t sld, int scols, void* dst, int64_t dld, int64_t rows, int cols, int gate_sH,
+                   int gate_dH, hipStream_t st) {
+    const int64_t n = rows * cols;
+    if (n <= 0) return JANUS_OK;
+    TraceScope trace("pad_copy", 0.0, 2.0 * double(n) * sizeof(T), st);
+    hipLaunchKernelGGL(remap_kernel<T>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, static_cast<const T*>(src),
+                       sld, scols, static_cast<T*>(dst), dld, rows, cols, gate_sH, gate_dH);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+// padded copies of the parameters (and x) shared by both passes
+janus_status pad_params(const janus_lstm_desc& d, const janus_lstm_desc& p, const PadWs& w, const void* x,
+                        const void* const* Wx, const void* const* Wh, const void* const* b, hipStream_t st) {
+    janus_status e;
+    for (int l = 0; l < d.L; ++l) {
+        const int Il = l == 0 ? d.I : d.H, Ilp = l == 0 ? p.I : p.H;
+        if ((e = remap<bf16_t>(Wx[l], Il, Il, w.Wx[l], Ilp, int64_t(4) * p.H, Ilp, d.H, p.H, st)) != JANUS_OK) return e;
+        if ((e = remap<bf16_t>(Wh[l], d.H, d.H, w.Wh[l], p.H, int64_t(4) * p.H, p.H, d.H, p.H, st)) != JANUS_OK)
+            return e;
+        if (b && (e = remap<bf16_t>(b[l], 1, 1, w.b[l], 1, int64_t(4) * p.H, 1, d.H, p.H, st)) != JANUS_OK) return e;
+    }
+    if (x && d.T > 0)
+        return remap<bf16_t>(x, d.I, d.I, w.x, p.I, int64_t(d.T) * d.B, p.I, 0, 0, st);
+    return JANUS_OK;
+}
+
+// [L*B x H] float32 state in / out of the padded layout
+janus_status pad_state(const janus_lstm_desc& d, const janus_lstm_desc& p, const float* src, float* dst,
+                       hipStream_t st) {
+    return remap<float>(src, d.H, d.H, dst, p.H, int64_t(d.L) * d.B, p.H, 0, 0, st);
+}
+janus_status unpad_state(const janus_lstm_desc& d, const janus_lstm_desc& p, const float* src, float* dst,
+                         hipStream_t st) {
+    return remap<float>(src, p.H, p.H, dst, d.H, int64_t(d.L) * d.B, d.H, 0, 0, st);
+}
+
+janus_status lstm_fwd_padded(const janus_lstm_desc& d, const SeqSchedule& s, void* ws, const void* x,
+                             const void* const* Wx, const void* const* Wh, const void* const* b, const float* h0,
+                             const float* c0, void* y, float* hT, float* cT, hipStream_t st) {
+    const janus_lstm_desc p = padded_desc(d);
+    PadWs w;
+    carve_pad(d, ws, w);
+    LstmWs inner;
+    carve(p, ws, inner);
+    janus_status e = pad_params(d, p, w, x, Wx, Wh, b, st);
+    if (e != JANUS_OK) return e;
+    if (h0 && (e = pad_state(d, p, h0, w.s0, st)) != JANUS_OK) return e;
+    if (c0 && (e = pad_state(d, p, c0, w.s1, st)) != JANUS_OK) return e;
+    std::vector<const void*> Wxp(w.Wx.begin(), w.Wx.end()), Whp(w.Wh.begin(), w.Wh.end()), bp(w.b.begin(), w.b.end());
+    e = lstm_fwd_impl<bf16_t, StepBF16>(p, s, inner, w.x, Wxp.data(), Whp.data(), bp.data(), h0 ? w.s0 : nullptr,
+                                        c0 ? w.s1 : nullptr, w.y, w.s2, w.s3, st);
+    if (e != JANUS_OK) return e;
+    if (d.T > 0 && (e = remap<bf16_t>(w.y, p.H, p.H, y, d.H, int64_t(d.T) * d.B, d.H, 0, 0, st)) != JANUS_OK)
+        return e;
+    if (hT && (e = unpad_state(d, p, w.s2, hT, st)) != JANUS_OK) return e;
+    if (cT && (e = unpad_state(d, p, w.s3, cT, st)) != JANUS_OK) return e;
+    return JANUS_OK;
+}
+
+janus_status lstm_bwd_padded(const janus_lstm_desc& d, const SeqSchedule& s, void* ws, const void* x,
+                             const void* const* Wx, const void* const* Wh, const void* dy, const float* dhT,
+                             const float* dcT, void* dx, float* dh0, float* dc0, float* const* dWx, float* const* dWh,
+                             float* const* db, hipStream_t st) {
+    const janus_lstm_desc p = padded_desc(d);
+    PadWs w;
+    carve_pad(d, ws, w);
+    LstmWs inner;
+    carve(p, ws, inner);
+    janus_status e = pad_params(d, p, w, x, Wx, Wh, nullptr, st);
+    if (e != JANUS_OK) return e;
+    const int64_t TB = int64_t(d.T) * d.B;
+    if (dy && TB > 0 && (e = remap<bf16_t>(dy, d.H, d.H, w.y, p.H, TB, p.H, 0, 0, st)) != JANUS_OK) return e;
+    if (dhT && (e = pad_state(d, p, dhT, w.s0, st)) != JANUS_OK) return e;
+    if (dcT && (e = pad_state(d, p, dcT, w.s1, st)) != JANUS_OK) return e;
+    std::vector<const void*> Wxp(w.Wx.begin(), w.Wx.end()), Whp(w.Wh.begin(), w.Wh.end());
+    e = lstm_bwd_impl<bf16_t, StepBF16>(p, s, inner, w.x, Wxp.data(), Whp.data(), dy ? w.y : nullptr,
+                                        dhT ? w.s0 : nullptr, dcT ? w.s1 : nullptr, dx ? w.dx : nullptr, w.s2, w.s3,
+                                        w.dWx.data(), w.dWh.data(), w.db.data(), st);
+    if (e != JANUS_OK) return e;
+    if (dx && TB > 0 && (e = remap<bf16_t>(w.dx, p.I, p.I, dx, d.I, TB, d.I, 0, 0, st)) != JANUS_OK) return e;
+    if (dh0 && (e = unpad_state(d, p, w.s2, dh0, st)) != JANUS_OK) return e;
+    if (dc0 && (e = unpad_state(d, p, w.s3, dc0, st)) != JANUS_OK) return e;
+    for (int l = 0; l < d.L; ++l) {
+        const int Il = l == 0 ? d.I : d.H, Ilp = l == 0 ? p.I : p.H;
+        if ((e = remap<float>(w.dWx[l], Ilp, Ilp, dWx[l], Il, int64_t(4) * d.H, Il, p.H, d.H, st)) != JANUS_OK)
+            return e;
+        if ((e = remap<float>(w.dWh[l], p.H, p.H, dWh[l], d.H, int64_t(4) * d.H, d.H, p.H, d.H, st)) != JANUS_OK)
+            return e;
+        if ((e = remap<float>(w.db[l], 1, 1, db[l], 1, int64_t(4) * d.H, 1, p.H, d.H, st)) != JANUS_OK) return e;
+    }
+    return JANUS_OK;
+}
+
 }  // namespace
 
 }  // namespace janus
@@ -947,6 +1126,10 @@ using namespace janus;
 
 extern "C" size_t janus_lstm_workspace_bytes(const janus_lstm_desc* d) {
     if (check_desc(d) != JANUS_OK) return 0;
+    if (needs_padding(*d)) {
+        PadWs w;
+        return carve_pad(*d, nullptr, w);
+    }
     LstmWs w;
     return carve(*d, nullptr, w);
 }
@@ -964,12 +1147,15 @@ extern "C" janus_status janus_lstm_seq_fwd(const janus_lstm_desc* d, const void*
     SeqSchedule s;
     e = build_seq_schedule(d->B, d->T, lengths, s);
     if (e != JANUS_OK) return e;
+    if (ws_bytes < janus_lstm_workspace_bytes(d) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return JANUS_ERR_WORKSPACE;
+    const bool pad = needs_padding(*d);
     LstmWs w;
-    if (ws_bytes < carve(*d, nullptr, w) || reinterpret_cast<uintptr_t>(ws) % 256 != 0) return JANUS_ERR_WORKSPACE;
-    carve(*d, ws, w);
+    carve(pad ? padded_desc(*d) : *d, ws, w);
     hipStream_t st = static_cast<hipStream_t>(stream);
     e = upload_schedule(s, w, st);
     if (e != JANUS_OK) return e;
+    if (pad) return lstm_fwd_padded(*d, s, ws, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
     if (d->dtype == JANUS_BF16)
         return lstm_fwd_impl<bf16_t, StepBF16>(*d, s, w, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
     return lstm_fwd_impl<float, StepF32>(*d, s, w, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
@@ -991,12 +1177,15 @@ extern "C" janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void*
     SeqSchedule s;
     e = build_seq_schedule(d->B, d->T, lengths, s);
     if (e != JANUS_OK) return e;
+    if (ws_bytes < janus_lstm_workspace_bytes(d) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return JANUS_ERR_WORKSPACE;
+    const bool pad = needs_padding(*d);
     LstmWs w;
-    if (ws_bytes < carve(*d, nullptr, w) || reinterpret_cast<uintptr_t>(ws) % 256 != 0) return JANUS_ERR_WORKSPACE;
-    carve(*d, ws, w);
+    carve(pad ? padded_desc(*d) : *d, ws, w);
     hipStream_t st = static_cast<hipStream_t>(stream);
     e = upload_schedule(s, w, st);
     if (e != JANUS_OK) return e;
+    if (pad) return lstm_bwd_padded(*d, s, ws, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
     if (d->dtype == JANUS_BF16)
         return lstm_bwd_impl<bf16_t, StepBF16>(*d, s, w, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
     return lstm_bwd_impl<float, StepF32>(*d, s, w, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
