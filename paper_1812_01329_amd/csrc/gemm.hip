@@ -270,41 +270,80 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
         compute(stage0);
     }
     if constexpr (EPI == kEpiMse) {
+        // Stage each wave's accumulators through LDS (the stages are free now)
+        // so that the target is read and dY written in 16-byte row pieces:
+        // two halves of 64 rows x 64 columns (float32, 16 KB per wave), 8-column
+        // chunks XOR-swizzled by row.  Lane l then takes chunk l % 8 of rows
+        // l / 8 + 8 q.  Requires N % 8 == 0 (checked by the caller).
         const bf16_t* bias = static_cast<const bf16_t*>(g.bias);
-        float sq = 0.f;
-        float cs[C_::FN];
+        __syncthreads();
+        float* tile = reinterpret_cast<float*>(wave < 4 ? stage0 : stage1) + (wave & 3) * 4096;
+        const int c8 = lane & 7, rq = lane >> 3;
+        const int ccol = n0 + wc0 + c8 * 8;   // first global column of this lane's chunk
+        const bool cok = ccol < p.N;
+        float bv[8];
+        {
+            uint4 braw = make_uint4(0, 0, 0, 0);
+            if (bias && cok) braw = *reinterpret_cast<const uint4*>(bias + ccol);
+            const uint32_t bw[4] = {braw.x, braw.y, braw.z, braw.w};
 #pragma unroll
-        for (int j = 0; j < C_::FN; ++j) {
-            cs[j] = 0.f;
-            const int col = n0 + wc0 + j * 32 + acc_col(lane);
-            if (col >= p.N) continue;
-            const float bv = bias ? bf2f(bias[col]) : 0.f;
-#pragma unroll
-            for (int i = 0; i < C_::FM; ++i)
-#pragma unroll
-                for (int v = 0; v < 16; ++v) {
-                    const int row = m0 + wr0 + i * 32 + acc_row(v, lane);
-                    if (row < p.M) {
-                        const int64_t o = int64_t(row) * p.N + col;
-                        const float d = acc[i][j][v] + bv - bf2f(p.tgt[o]);
-                        sq += d * d;
-                        const float dy = p.scale * d;
-                        p.dY[o] = f2bf(dy);
-                        cs[j] += dy;
-                    }
-                }
+            for (int e = 0; e < 4; ++e) {
+                bv[2 * e] = bf2f(bf16_t(bw[e] & 0xffffu));
+                bv[2 * e + 1] = bf2f(bf16_t(bw[e] >> 16));
+            }
         }
-        // lanes l and l ^ 32 hold the same columns; then the two wave rows
-        // meet in LDS (the stages are free now), in a fixed order
+        float sq = 0.f;
+        float cs[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
 #pragma unroll
-        for (int j = 0; j < C_::FN; ++j) cs[j] += __shfl_xor(cs[j], 32);
+        for (int half = 0; half < 2; ++half) {
+#pragma unroll
+            for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+                for (int j = 0; j < C_::FN; ++j)
+#pragma unroll
+                    for (int v = 0; v < 16; ++v) {
+                        const int r = ii * 32 + acc_row(v, lane), c = j * 32 + acc_col(lane);
+                        tile[r * 64 + (c ^ ((r & 7) << 3))] = acc[2 * half + ii][j][v];
+                    }
+#pragma unroll
+            for (int q = 0; q < 8; ++q) {
+                const int r = rq + 8 * q;
+                const int row = m0 + wr0 + half * 64 + r;
+                const float4 v0 = *reinterpret_cast<const float4*>(tile + r * 64 + ((c8 ^ (r & 7)) << 3));
+                const float4 v1 = *reinterpret_cast<const float4*>(tile + r * 64 + ((c8 ^ (r & 7)) << 3) + 4);
+                if (row < p.M && cok) {
+                    const int64_t o = int64_t(row) * p.N + ccol;
+                    const uint4 tr = *reinterpret_cast<const uint4*>(p.tgt + o);
+                    const uint32_t tw[4] = {tr.x, tr.y, tr.z, tr.w};
+                    const float val[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+                    uint32_t ow[4];
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) {
+                        const float d0 = val[2 * e] + bv[2 * e] - bf2f(bf16_t(tw[e] & 0xffffu));
+                        const float d1 = val[2 * e + 1] + bv[2 * e + 1] - bf2f(bf16_t(tw[e] >> 16));
+                        sq += d0 * d0 + d1 * d1;
+                        const float y0 = p.scale * d0, y1 = p.scale * d1;
+                        cs[2 * e] += y0;
+                        cs[2 * e + 1] += y1;
+                        ow[e] = uint32_t(f2bf(y0)) | (uint32_t(f2bf(y1)) << 16);
+                    }
+                    *reinterpret_cast<uint4*>(p.dY + o) = make_uint4(ow[0], ow[1], ow[2], ow[3]);
+                }
+            }
+        }
+        // column sums: lanes with the same chunk (l % 8) in order of xor steps,
+        // then the two wave rows meet in LDS, in a fixed order
+#pragma unroll
+        for (int e = 0; e < 8; ++e)
+#pragma unroll
+            for (int m = 8; m < 64; m <<= 1) cs[e] += __shfl_xor(cs[e], m);
 #pragma unroll
         for (int m = 1; m < 64; m <<= 1) sq += __shfl_xor(sq, m);
         __syncthreads();
         float* red = reinterpret_cast<float*>(stage0);   // [WGM][BN] column sums, then [8] squares
-        if (lane < 32) {
+        if (lane < 8) {
 #pragma unroll
-            for (int j = 0; j < C_::FN; ++j) red[(wave / C_::WGN) * C_::BN + wc0 + j * 32 + lane] = cs[j];
+            for (int e = 0; e < 8; ++e) red[(wave / C_::WGN) * C_::BN + wc0 + lane * 8 + e] = cs[e];
         }
         if (lane == 0) red[C_::WGM * C_::BN + wave] = sq;
         __syncthreads();
@@ -663,7 +702,8 @@ bool gemm_mse_fast(int M, int N, int K, const void* h, const void* W) {
     g.B = W;
     g.ldb = K;
     const NtPlan p = plan_nt(g);
-    return p.fast && p.bytes == 0 && p.splits == 1;
+    // the epilogue reads the target and writes dY in 16-byte row pieces
+    return p.fast && p.bytes == 0 && p.splits == 1 && N % 8 == 0;
 }
 
 janus_status gemm_mse(int M, int N, int K, const void* h, const void* W, const void* bias, const void* tgt, void* dY,

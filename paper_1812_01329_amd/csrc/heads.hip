@@ -257,7 +257,8 @@ janus_status mse_impl(const janus_mse_desc& d, const void* h, const void* W, con
     dim3 grid((d.P + Cfg::BN - 1) / Cfg::BN, (d.rows + Cfg::BM - 1) / Cfg::BM);
     // large bf16 shapes: the fast contraction with the loss in its epilogue,
     // which also forms db
-    const bool fused = d.dtype == JANUS_BF16 && gemm_mse_fast(d.rows, d.P, d.H, h, W);
+    const bool fused = d.dtype == JANUS_BF16 && gemm_mse_fast(d.rows, d.P, d.H, h, W) &&
+                       reinterpret_cast<uintptr_t>(tgt) % 16 == 0 && reinterpret_cast<uintptr_t>(b) % 16 == 0;
     if (fused) {
         janus_status e = gemm_mse(d.rows, d.P, d.H, h, W, b, tgt, w.dY, 2.f / count, w.part, db, st);
         if (e != JANUS_OK) return e;
