@@ -114,6 +114,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=4, help="sequences in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true")
+    ap.add_argument("--copy-calibration", action="store_true",
+                    help="only copy a 1 GiB buffer three times (reference for HBM byte counters) and exit")
     args = ap.parse_args()
 
     world = int(os.environ.get("WORLD_SIZE", "1"))
@@ -130,6 +132,16 @@ def main():
 
     assert torch.cuda.is_available(), "bench.py needs a GPU"
     torch.cuda.set_device(0)
+    if args.copy_calibration:
+        # a plain device copy of known size: the HBM byte counters of one such
+        # copy read 1 GiB fetched and 1 GiB written when they count bytes
+        src = torch.empty(1 << 29, dtype=torch.bfloat16, device="cuda").fill_(1.0)
+        dst = torch.empty_like(src)
+        for _ in range(3):
+            dst.copy_(src)
+        torch.cuda.synchronize()
+        print(json.dumps({"copy_bytes": src.numel() * src.element_size()}))
+        return
     spec = WORKLOADS[args.workload]
     WORKLOADS_UNIT = spec["unit"]
     w = wl.FULL[args.workload]()
