@@ -59,7 +59,7 @@ struct LstmWs {
     int32_t* perm4 = nullptr;           // [4H] interleaved row -> gate-major row
     int32_t* act_dev = nullptr;         // [T + 1]
     int32_t* off_dev = nullptr;         // [T + 2]
-    float* dpart = nullptr;             // [T + 1] slots of [4 x B x H] partial recurrent gradients
+    float* dpart = nullptr;             // [T + 1] slots of partial recurrent gradients, NS x B x (H rounded to 8 NS)
     bf16_t* Gf = nullptr;               // [T] slots of dG in fragment layout (persistent backward)
     int64_t gf_slot = 0;                // elements per slot
     persist::Sync* sync = nullptr;
@@ -138,7 +138,7 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     w.off_dev = c.take<int32_t>(int64_t(d.T) + 2);
     w.sync = c.take<persist::Sync>(1);
     if (d.dtype == JANUS_BF16) {
-        w.dpart = c.take<float>((int64_t(d.T) + 1) * persist::kSlices * d.B * d.H);
+        w.dpart = c.take<float>((int64_t(d.T) + 1) * persist::kMaxSlices * d.B * round_up(d.H, 8 * persist::kMaxSlices));
         w.gf_slot = round_up(d.B, 32) * int64_t(4) * d.H;
         w.Gf = c.take<bf16_t>(int64_t(d.T) * w.gf_slot);
         w.ldht = round_up(int64_t(d.B) + TB, 64);
@@ -185,17 +185,37 @@ size_t persist_red_bytes(int kw) { return size_t(kw - 1) * (persist::kWaves / kw
 size_t persist_fwd_lds(const janus_lstm_desc& d) {
     return size_t(32) * (round_up(d.H, 64) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
 }
-// backward K slices: k-groups of 16 interleaved gate columns, split in kSlices
+// Backward: the k-groups of 16 interleaved gate columns (4H / 16) are split
+// in `ns` slices and the units in groups of 8 ns; one workgroup per (slice,
+// group) holds that part of Wh^T in LDS.
 int persist_bwd_nkg(const janus_lstm_desc& d) { return d.H / 4; }
-int persist_bwd_ksp(const janus_lstm_desc& d) {
-    return 16 * ((persist_bwd_nkg(d) + persist::kSlices - 1) / persist::kSlices);
+int persist_bwd_ksp(const janus_lstm_desc& d, int ns) { return 16 * ((persist_bwd_nkg(d) + ns - 1) / ns); }
+size_t persist_bwd_lds(const janus_lstm_desc& d, int ns) {
+    return size_t(8 * ns) * (persist_bwd_ksp(d, ns) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
 }
-size_t persist_bwd_lds(const janus_lstm_desc& d) {
-    return size_t(persist::kUnitsBwd) * (persist_bwd_ksp(d) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
-}
+int persist_bwd_groups(const janus_lstm_desc& d, int ns) { return (d.H + 8 * ns - 1) / (8 * ns); }
+int persist_bwd_blocks(const janus_lstm_desc& d, int ns) { return ns * persist_bwd_groups(d, ns); }
 int persist_fwd_blocks(const janus_lstm_desc& d) { return (d.H + persist::kUnitsFwd - 1) / persist::kUnitsFwd; }
-int persist_bwd_blocks(const janus_lstm_desc& d) {
-    return persist::kSlices * ((d.H + persist::kUnitsBwd - 1) / persist::kUnitsBwd);
+
+size_t device_lds(const DeviceInfo& info) { return info.lds > 0 ? info.lds : 65536; }
+
+bool persist_bwd_fits(const janus_lstm_desc& d, int ns, const DeviceInfo& info) {
+    return persist_bwd_blocks(d, ns) <= info.cus && persist_bwd_groups(d, ns) <= persist::kMaxGroups &&
+           persist_bwd_lds(d, ns) <= device_lds(info);
+}
+
+// Slices of the persistent backward: 8 where the layout fits (half the
+// operand traffic per CU of 4 slices), else 4; 0 when neither fits.
+// JANUS_BWD_SLICES=4 or 8 asks for one of them only.
+int persist_bwd_slices(const janus_lstm_desc& d) {
+    const DeviceInfo info = device_info();
+    const char* e = getenv("JANUS_BWD_SLICES");
+    const int forced = (e && e[0] == '4') ? 4 : (e && e[0] == '8') ? 8 : 0;
+    for (int ns : {8, 4}) {
+        if (forced && ns != forced) continue;
+        if (persist_bwd_fits(d, ns, info)) return ns;
+    }
+    return 0;
 }
 
 // The persistent path needs bf16, H a multiple of 8, at most 256 rows, one
@@ -207,10 +227,8 @@ bool use_persistent(const janus_lstm_desc& d) {
     if (!env || d.dtype != JANUS_BF16 || d.H % 8 != 0 || d.B > persist::kMaxB) return false;
     const DeviceInfo info = device_info();
     if (!info.coop || info.cus <= 0) return false;
-    if (persist_fwd_blocks(d) > info.cus || persist_bwd_blocks(d) > info.cus) return false;
-    if ((d.H + persist::kUnitsBwd - 1) / persist::kUnitsBwd > persist::kMaxGroups) return false;
-    const size_t lds = info.lds > 0 ? info.lds : 65536;
-    return persist_fwd_lds(d) <= lds && persist_bwd_lds(d) <= lds;
+    if (persist_fwd_blocks(d) > info.cus || persist_fwd_lds(d) > device_lds(info)) return false;
+    return persist_bwd_slices(d) > 0;
 }
 
 __global__ void perm4_kernel(int H, int32_t* perm4) {
@@ -484,12 +502,13 @@ bool weight_aligned(const janus_lstm_desc& d) {
 }
 
 template <class K>
-janus_status coop_launch(K kernel, int blocks, size_t smem, void* arg, hipStream_t st, bool& attr_done) {
-    if (!attr_done) {
+janus_status coop_launch(K kernel, int blocks, size_t smem, void* arg, hipStream_t st, size_t& attr_smem) {
+    // the kernel's dynamic LDS limit, raised whenever a launch needs more
+    if (smem > attr_smem) {
         if (hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
                                 int(smem)) != hipSuccess)
             return JANUS_ERR_DEVICE;
-        attr_done = true;
+        attr_smem = smem;
     }
     void* args[] = {arg};
     if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), dim3(blocks), dim3(persist::kThreads), args,
@@ -499,7 +518,7 @@ janus_status coop_launch(K kernel, int blocks, size_t smem, void* arg, hipStream
 }
 
 janus_status launch_fwd_persistent(const janus_lstm_desc& d, persist::FwdArgs& a, double flops, hipStream_t st) {
-    static bool attr[4] = {};
+    static size_t attr[4] = {};
     const int kw = persist_kw(d.B);
     const size_t smem = persist_fwd_lds(d);
     const int blocks = persist_fwd_blocks(d);
@@ -512,17 +531,26 @@ janus_status launch_fwd_persistent(const janus_lstm_desc& d, persist::FwdArgs& a
     }
 }
 
-janus_status launch_bwd_persistent(const janus_lstm_desc& d, persist::BwdArgs& a, double flops, hipStream_t st) {
-    static bool attr[4] = {};
+janus_status launch_bwd_persistent(const janus_lstm_desc& d, int ns, persist::BwdArgs& a, double flops,
+                                   hipStream_t st) {
+    static size_t attr[8] = {};
     const int kw = persist_kw(d.B);
-    const size_t smem = persist_bwd_lds(d);
-    const int blocks = persist_bwd_blocks(d);
+    const size_t smem = persist_bwd_lds(d, ns);
+    const int blocks = persist_bwd_blocks(d, ns);
     TraceScope trace("lstm_bwd_persistent", flops, 0.0, st);
+    if (ns == 8) {
+        switch (kw) {
+            case 1: return coop_launch(persist::lstm_bwd_persistent<1, 8>, blocks, smem, &a, st, attr[4]);
+            case 2: return coop_launch(persist::lstm_bwd_persistent<2, 8>, blocks, smem, &a, st, attr[5]);
+            case 4: return coop_launch(persist::lstm_bwd_persistent<4, 8>, blocks, smem, &a, st, attr[6]);
+            default: return coop_launch(persist::lstm_bwd_persistent<8, 8>, blocks, smem, &a, st, attr[7]);
+        }
+    }
     switch (kw) {
-        case 1: return coop_launch(persist::lstm_bwd_persistent<1>, blocks, smem, &a, st, attr[0]);
-        case 2: return coop_launch(persist::lstm_bwd_persistent<2>, blocks, smem, &a, st, attr[1]);
-        case 4: return coop_launch(persist::lstm_bwd_persistent<4>, blocks, smem, &a, st, attr[2]);
-        default: return coop_launch(persist::lstm_bwd_persistent<8>, blocks, smem, &a, st, attr[3]);
+        case 1: return coop_launch(persist::lstm_bwd_persistent<1, 4>, blocks, smem, &a, st, attr[0]);
+        case 2: return coop_launch(persist::lstm_bwd_persistent<2, 4>, blocks, smem, &a, st, attr[1]);
+        case 4: return coop_launch(persist::lstm_bwd_persistent<4, 4>, blocks, smem, &a, st, attr[2]);
+        default: return coop_launch(persist::lstm_bwd_persistent<8, 4>, blocks, smem, &a, st, attr[3]);
     }
 }
 
@@ -587,7 +615,7 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     janus_status e = gemm(g, st);
     if (e != JANUS_OK) return e;
     if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;
-    persist::FwdArgs a;
+    persist::FwdArgs a = {};
     a.H = H;
     a.B = B;
     a.t_eff = s.t_eff;
@@ -734,16 +762,17 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         if (persistent) {
             janus_status e = zero_fill(w.sync, sizeof(persist::Sync), st);
             if (e != JANUS_OK) return e;
-            persist::BwdArgs a;
+            persist::BwdArgs a = {};
             a.H = H;
             a.B = B;
             a.t_eff = s.t_eff;
             a.fixed = s.fixed ? 1 : 0;
+            const int ns = persist_bwd_slices(d);
             a.nkg = persist_bwd_nkg(d);
-            a.ksp = persist_bwd_ksp(d);
+            a.ksp = persist_bwd_ksp(d, ns);
             a.Gf = w.Gf;
             a.gf_slot = w.gf_slot;
-            a.xcd_groups = (persist_bwd_blocks(d) % (8 * persist::kSlices)) == 0 ? 1 : 0;
+            a.xcd_groups = (persist_bwd_blocks(d, ns) % (8 * ns)) == 0 ? 1 : 0;
             a.active = w.act_dev;
             a.offsets = w.off_dev;
             a.perm = perm;
@@ -774,7 +803,7 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.sync = w.sync;
             double rows = 0;
             for (int t = 0; t < s.t_eff; ++t) rows += s.active[t];
-            if ((e = launch_bwd_persistent(d, a, 2.0 * 4.0 * H * double(H) * rows, st)) != JANUS_OK) return e;
+            if ((e = launch_bwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * rows, st)) != JANUS_OK) return e;
         } else {
         {
         TraceScope trace("lstm_bwd_init", 0.0, double(bh) * 16.0, st);

@@ -16,11 +16,14 @@
 // cell update runs in registers.
 //
 // Backward (two barriers per step).  dh_{t-1} = dG_t Wh contracts over 4H.
-// Workgroup (s, v) holds Wh^T for 32 units v and the quarter s of the 4H
-// interleaved gate columns, and writes a partial dh for those units; after a
-// barrier, workgroup q sums the four partials (in order s = 0..3) for units
-// [8q, 8q + 8), applies the cell backward for step t-1 and writes dG_{t-1};
-// after a second barrier the next contraction may read it.  The carried dc
+// The 4H interleaved gate columns are split in NS slices (4 or 8) and the
+// units in groups of 8 NS.  Workgroup (s, v) holds Wh^T for the units of
+// group v and the columns of slice s, and writes a partial dh for those
+// units; after a barrier among the NS workgroups of the group, member s sums
+// the NS partials (in order) for its 8 units [8 NS v + 8 s, + 8), applies
+// the cell backward and writes dG; after a grid barrier the next
+// contraction may read it.  Each workgroup streams 1/NS of dG per step, so
+// more slices mean less operand traffic per CU and more partial sums.  The carried dc
 // (and dh of rows whose sequence has not started in reverse) stay in
 // registers of the owning thread for the whole launch.
 #pragma once
@@ -33,11 +36,10 @@ namespace persist {
 constexpr int kThreads = 512;          // 8 waves
 constexpr int kWaves = kThreads / 64;
 constexpr int kUnitsFwd = 8;           // hidden units per forward workgroup (32 gate rows)
-constexpr int kUnitsBwd = 32;          // hidden units per backward workgroup
-constexpr int kSlices = 4;             // K-split of the backward contraction
+constexpr int kMaxSlices = 8;          // largest K-split of the backward contraction
 constexpr int kMaxB = 256;             // batch rows handled by one pass of 8 waves
 constexpr int kSpinLimit = 1 << 22;    // bounded wait at each barrier (~0.1 s)
-constexpr int kMaxGroups = 64;         // backward unit groups (H / 32) a launch may have
+constexpr int kMaxGroups = 64;         // backward unit groups (H / (8 NS)) a launch may have
 
 // Device-wide barrier state (zeroed before every launch).  Counters sit in
 // separate 256-byte lines.
@@ -48,6 +50,7 @@ struct Sync {
     unsigned xcd[16][64];              // per-XCD arrivals
     unsigned census[16][64];           // workgroups resident on each XCD
     unsigned group[kMaxGroups][64];    // arrivals of each backward unit group
+    unsigned gxcd[kMaxGroups][64];     // XCDs (bit mask) that hold the workgroups of each backward unit group
 };
 
 __device__ __forceinline__ unsigned xcc_id() {
@@ -74,7 +77,9 @@ __device__ __forceinline__ bool spin_until(Sync* s, const unsigned* p, unsigned 
 }
 
 // Census of the workgroups on every XCD (their L2 is shared), once per launch.
-__device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
+// With `xmask`, the workgroup also sets the bit of its XCD there; after the
+// call thread 0 sees the bits of every workgroup that passed the same mask.
+__device__ __forceinline__ void barrier_init(Barrier& b, Sync* s, unsigned* xmask = nullptr) {
     b.s = s;
     b.nb = gridDim.x;
     b.phase = 0;
@@ -83,9 +88,11 @@ __device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
     b.nx = 1;
     if (threadIdx.x == 0) {
         b.x = xcc_id();
+        if (xmask) __hip_atomic_fetch_or(xmask, 1u << b.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_fetch_add(&s->census[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_add(&s->count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&s->count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         spin_until(s, &s->count, b.nb);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         b.xsize = __hip_atomic_load(&s->census[b.x][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         b.nx = 0;
         for (int q = 0; q < 16; ++q)
@@ -238,6 +245,11 @@ __device__ __forceinline__ uint4 load16(__amdgpu_buffer_rsrc_t rs, uint32_t off)
     const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off), 0, 0);
     return make_uint4(v.x, v.y, v.z, v.w);
 }
+// device-scope load (sc1): misses in the L1, so it returns what the L2 holds
+__device__ __forceinline__ uint4 load16_l2(__amdgpu_buffer_rsrc_t rs, uint32_t off) {
+    const u32x4_t v = __builtin_amdgcn_raw_buffer_load_b128(rs, int(off), 0, 16);
+    return make_uint4(v.x, v.y, v.z, v.w);
+}
 template <int POLICY>
 __device__ __forceinline__ void store4(__amdgpu_buffer_rsrc_t rs, uint32_t off, float v) {
     __builtin_amdgcn_raw_buffer_store_b32(__builtin_bit_cast(uint32_t, v), rs, int(off), 0, POLICY);
@@ -319,6 +331,63 @@ __device__ __forceinline__ void contract_frag(f32x16_t& acc, const bf16_t* wrow,
     for (int v = 0; v < 16; ++v) acc[v] += acc1[v];
 }
 
+// The same for MT weight tiles of 32 rows (`wtile` elements apart in LDS)
+// that share each operand fragment: one load feeds MT MFMAs, whose
+// accumulators are independent.  The weight fragments of the next k-group
+// are read from LDS while the MFMAs of this one run, and a scheduling
+// barrier after each refill keeps the compiler from sinking the refills to
+// the end of the unrolled block (which empties the ring).
+template <int DEPTH, int MT>
+__device__ __forceinline__ void contract_frag_mt(f32x16_t (&acc)[MT], const bf16_t* wrow, int wtile,
+                                                 __amdgpu_buffer_rsrc_t rs, uint32_t off, int n) {
+    if constexpr (MT == 1) {
+        contract_frag<DEPTH>(acc[0], wrow, rs, off, n);
+    } else {
+        static_assert(DEPTH % 2 == 0, "even ring depth");
+        const int last = n > 0 ? n - 1 : 0;
+        uint4 w[2][MT];
+        auto wload = [&](uint4 (&dst)[MT], int kg) {
+            const int k = kg < last ? kg : last;
+#pragma unroll
+            for (int m = 0; m < MT; ++m) dst[m] = *reinterpret_cast<const uint4*>(wrow + m * wtile + k * 16);
+        };
+        auto step = [&](const uint4 (&wf)[MT], uint4 h) {
+            Frag<bf16_t> fh;
+            fh.v = h;
+#pragma unroll
+            for (int m = 0; m < MT; ++m) {
+                Frag<bf16_t> fw;
+                fw.v = wf[m];
+                mfma(acc[m], fw, fh);
+            }
+        };
+        uint4 ring[DEPTH];
+#pragma unroll
+        for (int i = 0; i < DEPTH; ++i) ring[i] = load16(rs, i < n ? off + uint32_t(i) * 1024u : kOutOfRange);
+        wload(w[0], 0);
+        int kg = 0;
+        for (; kg + DEPTH <= n; kg += DEPTH) {
+#pragma unroll
+            for (int i = 0; i < DEPTH; ++i) {
+                wload(w[(i + 1) & 1], kg + i + 1);
+                step(w[i & 1], ring[i]);
+                const int nx = kg + i + DEPTH;
+                ring[i] = load16(rs, nx < n ? off + uint32_t(nx) * 1024u : kOutOfRange);
+                __builtin_amdgcn_sched_barrier(0);
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < DEPTH; ++i) {
+            if (kg + i < n) {
+                wload(w[(i + 1) & 1], kg + i + 1);
+                step(w[i & 1], ring[i]);
+            }
+        }
+    }
+}
+
+// ring depth with two weight tiles (each fragment feeds two MFMAs)
+constexpr int kDepthFrag2 = 8;
 constexpr int kDepthFrag = 12;
 
 template <int KW>
@@ -469,7 +538,7 @@ struct BwdArgs {
     const float* dcT;
     float* dh0;
     float* dc0;
-    float* part;                       // [t_eff + 1] slots of [kSlices x B x H] partial sums of dh
+    float* part;                       // [t_eff + 1] slots of NS x B x (8 NS groups) partial sums of dh
     float* db;                         // [4H] gate-major bias gradient (overwritten), or NULL
     bf16_t* GT;                        // [4H x ldk] dG transposed (interleaved rows), or NULL
     int64_t ldk;
@@ -479,16 +548,19 @@ struct BwdArgs {
     Sync* sync;
 };
 
-// Slice s of the K = 4H interleaved gate columns: k-groups [s nkg / 4, (s + 1) nkg / 4).
-__device__ __forceinline__ int slice_kg0(int nkg, int s) { return s * nkg / kSlices; }
+// Slice s of the K = 4H interleaved gate columns: k-groups [s nkg / NS, (s + 1) nkg / NS).
+template <int NS>
+__device__ __forceinline__ int slice_kg0(int nkg, int s) { return s * nkg / NS; }
 
 // WT[uu][kk] = (Wh interleaved)[c][v0 + uu] = Wh[(c % 4) * H + c / 4][v0 + uu],  c = 16 kg0 + kk
+template <int NS>
 __device__ __forceinline__ void stage_bwd_weights(const BwdArgs& a, bf16_t* Ws, int wld, int s, int v0) {
+    constexpr int UNITS = 8 * NS;
     const int H = a.H;
-    const int c0 = 16 * slice_kg0(a.nkg, s), c1 = 16 * slice_kg0(a.nkg, s + 1);
+    const int c0 = 16 * slice_kg0<NS>(a.nkg, s), c1 = 16 * slice_kg0<NS>(a.nkg, s + 1);
 #pragma unroll 8
-    for (int idx = threadIdx.x; idx < kUnitsBwd * a.ksp; idx += kThreads) {
-        const int kk = idx / kUnitsBwd, uu = idx - kk * kUnitsBwd;
+    for (int idx = threadIdx.x; idx < UNITS * a.ksp; idx += kThreads) {
+        const int kk = idx / UNITS, uu = idx - kk * UNITS;
         const int c = c0 + kk;
         const int u = v0 + uu;
         bf16_t v = 0;
@@ -497,46 +569,62 @@ __device__ __forceinline__ void stage_bwd_weights(const BwdArgs& a, bf16_t* Ws, 
     }
 }
 
-// Barrier among the kSlices workgroups of one unit group (they exchange
-// partial sums only among themselves).  Same memory argument as the grid
-// barrier: the partial sums are written through, into addresses fresh for
-// each step.
-__device__ __forceinline__ void group_barrier(Sync* s, unsigned* cnt, unsigned& phase) {
+// Barrier among the `members` workgroups of one unit group (they exchange
+// partial sums only among themselves).  When all members run on one XCD they
+// share its L2: the sums are stored write-back (the L2 acknowledges them
+// before the arrival) and read with device-scope loads, which miss in the L1
+// and return the L2's copy, so one slot serves every step (a step's sums are
+// read before the grid barrier after which the next step overwrites them).
+// Otherwise they are written through to memory into a slot fresh for each
+// step, as for the grid barrier.
+__device__ __forceinline__ void group_barrier(Sync* s, unsigned* cnt, unsigned& phase, unsigned members) {
     ++phase;
     __syncthreads();
     if (threadIdx.x == 0) {
         __builtin_amdgcn_s_waitcnt(0);
         __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        spin_until(s, cnt, phase * unsigned(kSlices));
+        spin_until(s, cnt, phase * members);
     }
     __syncthreads();
 }
 
-template <int KW>
+template <int KW, int NS>
 __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
+    static_assert(NS == 4 || NS == 8, "slices of the backward contraction");
+    constexpr int UNITS = 8 * NS;     // units of a group
+    constexpr int MT = UNITS / 32;    // 32-row weight tiles per wave
     extern __shared__ __align__(16) unsigned char smem_raw[];
     const int wld = a.ksp + 8;
     bf16_t* Ws = reinterpret_cast<bf16_t*>(smem_raw);
-    float* red = reinterpret_cast<float*>(smem_raw + size_t(kUnitsBwd) * wld * sizeof(bf16_t));
+    float* red = reinterpret_cast<float*>(smem_raw + size_t(UNITS) * wld * sizeof(bf16_t));
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     const int q = blockIdx.x;
-    // unit group v (32 units) and K slice s of this workgroup
-    const int s = a.xcd_groups ? (q / 8) % kSlices : q % kSlices;
-    const int v = a.xcd_groups ? (q % 8) + 8 * (q / (8 * kSlices)) : q / kSlices;
-    const int v0 = v * kUnitsBwd;
+    // unit group v and K slice s of this workgroup
+    const int s = a.xcd_groups ? (q / 8) % NS : q % NS;
+    const int v = a.xcd_groups ? (q % 8) + 8 * (q / (8 * NS)) : q / NS;
+    const int v0 = v * UNITS;
+    const int ngroups = int(gridDim.x) / NS;
     const int H = a.H;
     Barrier bar;
-    barrier_init(bar, a.sync);
+    barrier_init(bar, a.sync, &a.sync->gxcd[v][0]);
     unsigned* gcnt = &a.sync->group[v][0];
     unsigned gphase = 0;
+    // partial sums stay in the L2 when the whole group shares one
+    __shared__ int group_local;
+    if (threadIdx.x == 0) {
+        const unsigned m = __hip_atomic_load(&a.sync->gxcd[v][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        group_local = (m & (m - 1u)) == 0u ? 1 : 0;
+    }
+    __syncthreads();
+    const bool plocal = group_local != 0;
 
-    stage_bwd_weights(a, Ws, wld, s, v0);
+    stage_bwd_weights<NS>(a, Ws, wld, s, v0);
 
     // contraction geometry: wave (bt, kw) takes batch rows [32 bt, 32 bt + 32)
     // and part kw of this slice's k-groups
     constexpr int NB = kWaves / KW;
     const int bt = wave % NB, kw = wave / NB;
-    const int sg0 = slice_kg0(a.nkg, s), sgn = slice_kg0(a.nkg, s + 1) - sg0;
+    const int sg0 = slice_kg0<NS>(a.nkg, s), sgn = slice_kg0<NS>(a.nkg, s + 1) - sg0;
     const int kg0 = kw * sgn / KW, kg1 = (kw + 1) * sgn / KW;
     const bf16_t* wrow = Ws + (lane & 31) * wld + 8 * (lane >> 5) + kg0 * 16;
     const uint32_t goff = (uint32_t(bt * a.nkg + sg0 + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
@@ -598,30 +686,48 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
         const bool fresh = cell && r >= act_next;
         const bool sync_after = t >= 0 && act > 0;
 
-        // partial sums of dh_t from dG_{t+1} (slot t + 1 of the fragment copy)
-        float* part = a.part + int64_t(t + 1) * kSlices * a.B * H;
+        // partial sums of dh_t from dG_{t+1} (slot t + 1 of the fragment copy).
+        // Slot layout [writer slice][group][reader member][row][8 units]: what
+        // one wave stores, and what one wave of a reader loads, is 1 KB in one
+        // piece (32 rows x 32 bytes).
+        const int64_t pslot = int64_t(NS) * ngroups * NS * a.B * 8;
+        float* part = plocal ? a.part : a.part + int64_t(t + 1) * pslot;
         if (act_next > 0) {
-            f32x16_t acc;
+            f32x16_t acc[MT];
 #pragma unroll
-            for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+            for (int m = 0; m < MT; ++m)
+#pragma unroll
+                for (int e = 0; e < 16; ++e) acc[m][e] = 0.f;
             if (bt * 32 < act_next) {
                 const auto rs = make_rsrc(a.Gf + int64_t(t + 1) * a.gf_slot, uint32_t(a.gf_slot) * 2u);
-                contract_frag<kDepthFrag>(acc, wrow, rs, goff, kg1 - kg0);
+                contract_frag_mt<MT == 1 ? kDepthFrag : kDepthFrag2, MT>(acc, wrow, 32 * wld, rs, goff, kg1 - kg0);
             }
-            reduce_kparts<KW>(acc, red, wave, lane);
-            if (kw == 0 && crow < act_next) {
-                // lane holds units v0 + 8 j + 4 (lane / 32) + [0, 4) of row crow, j = 0..3
-                const auto rp = make_rsrc(part + int64_t(s) * a.B * H, uint32_t(a.B) * uint32_t(H) * 4u);
 #pragma unroll
-                for (int j = 0; j < 4; ++j) {
-                    const int u = v0 + 8 * j + 4 * (lane >> 5);
-                    const uint32_t o = u < H ? (uint32_t(crow) * uint32_t(H) + uint32_t(u)) * 4u : kOutOfRange;
-                    store16<kStoreThrough>(rp, o, make_uint4(__float_as_uint(acc[4 * j]), __float_as_uint(acc[4 * j + 1]),
-                                                             __float_as_uint(acc[4 * j + 2]),
-                                                             __float_as_uint(acc[4 * j + 3])));
-                }
+            for (int m = 0; m < MT; ++m) {
+                if (KW > 1 && m > 0) __syncthreads();   // the previous tile's K parts have been read
+                reduce_kparts<KW>(acc[m], red, wave, lane);
             }
-            group_barrier(a.sync, gcnt, gphase);
+            if (kw == 0 && crow < act_next) {
+                // tile m of a lane holds units v0 + 32 m + 8 j + 4 (lane / 32) + [0, 4) of row crow:
+                // reader member 4 m + j, unit offset 4 (lane / 32) in its octet
+                const auto rp = make_rsrc(part + (int64_t(s) * ngroups + v) * NS * a.B * 8,
+                                          uint32_t(NS) * uint32_t(a.B) * 32u);
+#pragma unroll
+                for (int m = 0; m < MT; ++m)
+#pragma unroll
+                    for (int j = 0; j < 4; ++j) {
+                        const int u = v0 + 32 * m + 8 * j + 4 * (lane >> 5);
+                        const uint32_t o =
+                            u < H ? ((uint32_t(4 * m + j) * uint32_t(a.B) + uint32_t(crow)) * 8u + 4u * uint32_t(lane >> 5)) * 4u
+                                  : kOutOfRange;
+                        const uint4 pv = make_uint4(__float_as_uint(acc[m][4 * j]), __float_as_uint(acc[m][4 * j + 1]),
+                                                    __float_as_uint(acc[m][4 * j + 2]),
+                                                    __float_as_uint(acc[m][4 * j + 3]));
+                        if (plocal) store16<kStoreBack>(rp, o, pv);
+                        else store16<kStoreThrough>(rp, o, pv);
+                    }
+            }
+            group_barrier(a.sync, gcnt, gphase, unsigned(NS));
         }
 
         uint32_t dgl[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // this step's dG, zero without a cell
@@ -631,10 +737,13 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                 // sum the slices in order
                 dh[0] = dh[1] = dh[2] = dh[3] = 0.f;
 #pragma unroll
-                for (int j = 0; j < kSlices; ++j) {
-                    const float4 pv =
-                        *reinterpret_cast<const float4*>(part + (int64_t(j) * a.B + r) * H + ub);
-                    dh[0] += pv.x; dh[1] += pv.y; dh[2] += pv.z; dh[3] += pv.w;
+                for (int j = 0; j < NS; ++j) {
+                    const auto rp = make_rsrc(part + ((int64_t(j) * ngroups + v) * NS + s) * a.B * 8,
+                                              uint32_t(a.B) * 32u);
+                    const uint32_t o = (uint32_t(r) * 8u + 4u * uint32_t(tid & 1)) * 4u;
+                    const uint4 pv = plocal ? load16_l2(rp, o) : load16(rp, o);
+                    dh[0] += __uint_as_float(pv.x); dh[1] += __uint_as_float(pv.y);
+                    dh[2] += __uint_as_float(pv.z); dh[3] += __uint_as_float(pv.w);
                 }
             }
         }

@@ -204,3 +204,22 @@ def test_long_ragged_batch_split_contractions():
     w = _lstm("mse", "bf16", L=1, I=64, H=128, B=B, T=48, lengths=lengths, seed=21, h0=True, P=136)
     _, g = _run(w)
     compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
+
+
+@pytest.mark.parametrize("slices", ["4", "8"])
+@pytest.mark.parametrize("H,B,ragged", [(512, 256, False), (200, 70, True)])
+def test_backward_slices(slices, H, B, ragged, monkeypatch):
+    """The persistent backward with its K = 4H gate columns in 4 and in 8
+    slices (JANUS_BWD_SLICES): unit groups of 32 or 64, one or two weight
+    tiles per wave, groups placed on one XCD (H = 512) or adjacent (H = 200,
+    padded to 208, last group partial), full and split-K waves (B = 256, 70)."""
+    from paper_1812_01329_amd import janus as J
+    monkeypatch.setenv("JANUS_BWD_SLICES", slices)
+    rng = np.random.default_rng(31)
+    lens = rng.integers(0, 11, B) if ragged else None
+    w = _lstm("mse", "bf16", L=2, I=64, H=H, B=B, T=10, lengths=lens, seed=31, h0=True, P=40)
+    J.janus_trace_begin()
+    _, g = _run(w)
+    labels = {r["label"] for r in J.janus_trace_end()}
+    assert "lstm_bwd_persistent" in labels, labels
+    compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
