@@ -125,6 +125,30 @@ janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void* x,
                                 void* stream);
 
 /*
+ * Report of the last janus_lstm_seq_fwd or janus_lstm_seq_bwd call made with
+ * this workspace (same d).  The persistent recurrence kernels separate their
+ * time steps with device-wide barriers whose waits are bounded; when a wait
+ * runs out, the kernels drain and the outputs are undefined.  Those calls
+ * return without synchronising, so this call synchronises `stream` and reads
+ * the report back.
+ *  timed_out         1 if any wait of the call ran out.
+ *  bwd_groups        backward unit groups launched, summed over layers (0
+ *                    when the per-step kernels ran).
+ *  bwd_local_groups  of those, groups whose workgroups all ran on one XCD
+ *                    and kept their partial sums in its L2.
+ * Errors: INVALID_ARG (bad d, NULL out), WORKSPACE (as for the calls above),
+ * DEVICE (a HIP call failed, or timed_out is 1).
+ */
+typedef struct {
+    int32_t timed_out;
+    int32_t bwd_groups;
+    int32_t bwd_local_groups;
+} janus_lstm_report;
+
+janus_status janus_lstm_device_report(const janus_lstm_desc* d, const void* ws, size_t ws_bytes,
+                                      janus_lstm_report* out, void* stream);
+
+/*
  * Integer schedule of the sequence loop (host only, no device use):
  *  perm[B]       batch indices sorted by (-len_b, b)
  *  active[T]     active[t] = #{b : len_b > t} for t < t_eff, 0 after

@@ -614,7 +614,7 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     g.scratch_bytes = w.gs_bytes;
     janus_status e = gemm(g, st);
     if (e != JANUS_OK) return e;
-    if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;
+    if ((e = zero_fill(w.sync, persist::kSyncCounterBytes, st)) != JANUS_OK) return e;
     persist::FwdArgs a = {};
     a.H = H;
     a.B = B;
@@ -760,7 +760,7 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
     for (int l = d.L - 1; l >= 0; --l) {
         const bool top = l == d.L - 1;
         if (persistent) {
-            janus_status e = zero_fill(w.sync, sizeof(persist::Sync), st);
+            janus_status e = zero_fill(w.sync, persist::kSyncCounterBytes, st);
             if (e != JANUS_OK) return e;
             persist::BwdArgs a = {};
             a.H = H;
@@ -772,7 +772,6 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.ksp = persist_bwd_ksp(d, ns);
             a.Gf = w.Gf;
             a.gf_slot = w.gf_slot;
-            a.xcd_groups = (persist_bwd_blocks(d, ns) % (8 * ns)) == 0 ? 1 : 0;
             a.active = w.act_dev;
             a.offsets = w.off_dev;
             a.perm = perm;
@@ -1184,6 +1183,7 @@ extern "C" janus_status janus_lstm_seq_fwd(const janus_lstm_desc* d, const void*
     hipStream_t st = static_cast<hipStream_t>(stream);
     e = upload_schedule(s, w, st);
     if (e != JANUS_OK) return e;
+    if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;   // the call's report
     if (pad) return lstm_fwd_padded(*d, s, ws, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
     if (d->dtype == JANUS_BF16)
         return lstm_fwd_impl<bf16_t, StepBF16>(*d, s, w, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
@@ -1214,8 +1214,28 @@ extern "C" janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void*
     hipStream_t st = static_cast<hipStream_t>(stream);
     e = upload_schedule(s, w, st);
     if (e != JANUS_OK) return e;
+    if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;   // the call's report
     if (pad) return lstm_bwd_padded(*d, s, ws, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
     if (d->dtype == JANUS_BF16)
         return lstm_bwd_impl<bf16_t, StepBF16>(*d, s, w, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
     return lstm_bwd_impl<float, StepF32>(*d, s, w, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
+}
+
+extern "C" janus_status janus_lstm_device_report(const janus_lstm_desc* d, const void* ws, size_t ws_bytes,
+                                                 janus_lstm_report* out, void* stream) {
+    janus_status e = check_desc(d);
+    if (e != JANUS_OK) return e;
+    if (!out) return JANUS_ERR_INVALID_ARG;
+    if (!ws) return JANUS_ERR_WORKSPACE;
+    if (ws_bytes < janus_lstm_workspace_bytes(d) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return JANUS_ERR_WORKSPACE;
+    LstmWs w;
+    carve(needs_padding(*d) ? padded_desc(*d) : *d, const_cast<void*>(ws), w);
+    unsigned rep[3] = {0u, 0u, 0u};
+    if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return JANUS_ERR_DEVICE;
+    if (hipMemcpy(rep, &w.sync->error, sizeof(rep), hipMemcpyDeviceToHost) != hipSuccess) return JANUS_ERR_DEVICE;
+    out->timed_out = rep[0] != 0u ? 1 : 0;
+    out->bwd_groups = int32_t(rep[1]);
+    out->bwd_local_groups = int32_t(rep[2]);
+    return out->timed_out ? JANUS_ERR_DEVICE : JANUS_OK;
 }

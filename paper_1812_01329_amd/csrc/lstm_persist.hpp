@@ -28,6 +28,8 @@
 // registers of the owning thread for the whole launch.
 #pragma once
 
+#include <cstddef>
+
 #include "device.hpp"
 
 namespace janus {
@@ -41,17 +43,21 @@ constexpr int kMaxB = 256;             // batch rows handled by one pass of 8 wa
 constexpr int kSpinLimit = 1 << 22;    // bounded wait at each barrier (~0.1 s)
 constexpr int kMaxGroups = 64;         // backward unit groups (H / (8 NS)) a launch may have
 
-// Device-wide barrier state (zeroed before every launch).  Counters sit in
-// separate 256-byte lines.
+// Device-wide barrier state.  The counters (up to `error`) are zeroed before
+// every launch; the report that follows them is zeroed once per library call
+// and accumulates over its launches.  Counters sit in separate 256-byte lines.
 struct Sync {
     unsigned count;                    // global arrivals (census first, then one per XCD per barrier)
-    unsigned error;                    // set when a wait exceeds its spin limit
-    unsigned pad0[62];
+    unsigned pad0[63];
     unsigned xcd[16][64];              // per-XCD arrivals
     unsigned census[16][64];           // workgroups resident on each XCD
     unsigned group[kMaxGroups][64];    // arrivals of each backward unit group
-    unsigned gxcd[kMaxGroups][64];     // XCDs (bit mask) that hold the workgroups of each backward unit group
+    unsigned error;                    // set when a wait exceeds its spin limit
+    unsigned groups;                   // backward unit groups launched
+    unsigned local_groups;             // of which kept their partial sums in one XCD's L2
+    unsigned pad1[61];
 };
+constexpr size_t kSyncCounterBytes = offsetof(Sync, error);
 
 __device__ __forceinline__ unsigned xcc_id() {
     // hardware register XCC_ID (20), bits [3:0]: the XCD this wave runs on
@@ -62,6 +68,8 @@ __device__ __forceinline__ unsigned xcc_id() {
 struct Barrier {
     Sync* s;
     unsigned x, xsize, nx, nb, phase;
+    unsigned xidx;                     // arrival order of this workgroup among those on its XCD
+    unsigned xfirst;                   // workgroups on the XCDs numbered below this one
 };
 
 __device__ __forceinline__ bool spin_until(Sync* s, const unsigned* p, unsigned target) {
@@ -77,26 +85,31 @@ __device__ __forceinline__ bool spin_until(Sync* s, const unsigned* p, unsigned 
 }
 
 // Census of the workgroups on every XCD (their L2 is shared), once per launch.
-// With `xmask`, the workgroup also sets the bit of its XCD there; after the
-// call thread 0 sees the bits of every workgroup that passed the same mask.
-__device__ __forceinline__ void barrier_init(Barrier& b, Sync* s, unsigned* xmask = nullptr) {
+// Ordering the workgroups by (XCD, arrival order on it) gives each a rank
+// xfirst + xidx in [0, gridDim.x) under which consecutive ranks share an XCD
+// wherever possible, whatever order the hardware placed them in.
+__device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
     b.s = s;
     b.nb = gridDim.x;
     b.phase = 0;
     b.x = 0;
     b.xsize = 1;
     b.nx = 1;
+    b.xidx = 0;
+    b.xfirst = 0;
     if (threadIdx.x == 0) {
         b.x = xcc_id();
-        if (xmask) __hip_atomic_fetch_or(xmask, 1u << b.x, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        __hip_atomic_fetch_add(&s->census[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        b.xidx = __hip_atomic_fetch_add(&s->census[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         __hip_atomic_fetch_add(&s->count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
         spin_until(s, &s->count, b.nb);
         __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
         b.xsize = __hip_atomic_load(&s->census[b.x][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
         b.nx = 0;
-        for (int q = 0; q < 16; ++q)
-            b.nx += __hip_atomic_load(&s->census[q][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u;
+        for (unsigned q = 0; q < 16; ++q) {
+            const unsigned c = __hip_atomic_load(&s->census[q][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            b.nx += c != 0u;
+            if (q < b.x) b.xfirst += c;
+        }
     }
     __syncthreads();
 }
@@ -543,7 +556,6 @@ struct BwdArgs {
     bf16_t* GT;                        // [4H x ldk] dG transposed (interleaved rows), or NULL
     int64_t ldk;
     int gt_pairs;                      // 1: every step's packed offset is even (row pairs as 4-byte stores)
-    int xcd_groups;                    // 1: group members are 8 blocks apart (one XCD), 0: adjacent
     int64_t ldh, ldg;
     Sync* sync;
 };
@@ -598,25 +610,32 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
     bf16_t* Ws = reinterpret_cast<bf16_t*>(smem_raw);
     float* red = reinterpret_cast<float*>(smem_raw + size_t(UNITS) * wld * sizeof(bf16_t));
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int q = blockIdx.x;
-    // unit group v and K slice s of this workgroup
-    const int s = a.xcd_groups ? (q / 8) % NS : q % NS;
-    const int v = a.xcd_groups ? (q % 8) + 8 * (q / (8 * NS)) : q / NS;
+    Barrier bar;
+    barrier_init(bar, a.sync);
+    // Unit group v and K slice s of this workgroup from its census rank p:
+    // the members of a group hold consecutive ranks, so they run on one XCD
+    // unless the group straddles the end of an XCD's workgroups.  The
+    // partial sums of such a local group stay in the L2 its members share.
+    __shared__ int assign[3];
+    if (threadIdx.x == 0) {
+        const unsigned p = bar.xfirst + bar.xidx;
+        const unsigned g0 = p - p % NS;   // rank of the group's first member
+        assign[0] = int(p % NS);
+        assign[1] = int(p / NS);
+        assign[2] = (g0 >= bar.xfirst && g0 + NS <= bar.xfirst + bar.xsize) ? 1 : 0;
+    }
+    __syncthreads();
+    const int s = assign[0], v = assign[1];
+    const bool plocal = assign[2] != 0;
+    if (threadIdx.x == 0 && s == 0) {
+        __hip_atomic_fetch_add(&a.sync->groups, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        if (plocal) __hip_atomic_fetch_add(&a.sync->local_groups, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
     const int v0 = v * UNITS;
     const int ngroups = int(gridDim.x) / NS;
     const int H = a.H;
-    Barrier bar;
-    barrier_init(bar, a.sync, &a.sync->gxcd[v][0]);
     unsigned* gcnt = &a.sync->group[v][0];
     unsigned gphase = 0;
-    // partial sums stay in the L2 when the whole group shares one
-    __shared__ int group_local;
-    if (threadIdx.x == 0) {
-        const unsigned m = __hip_atomic_load(&a.sync->gxcd[v][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        group_local = (m & (m - 1u)) == 0u ? 1 : 0;
-    }
-    __syncthreads();
-    const bool plocal = group_local != 0;
 
     stage_bwd_weights<NS>(a, Ws, wld, s, v0);
 

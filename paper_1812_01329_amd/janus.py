@@ -25,7 +25,8 @@ EMBED_FWD, XENT_FWD_BWD, EMBED_BWD = 0, 1, 2
 LOSS_SUMSQ, LOSS_MEAN = 0, 1
 
 EXPORTS = [
-    "janus_lstm_workspace_bytes", "janus_lstm_seq_fwd", "janus_lstm_seq_bwd", "janus_lstm_schedule",
+    "janus_lstm_workspace_bytes", "janus_lstm_seq_fwd", "janus_lstm_seq_bwd", "janus_lstm_device_report",
+    "janus_lstm_schedule",
     "janus_treelstm_workspace_bytes", "janus_tree_schedule_build", "janus_treelstm_fwd",
     "janus_treelstm_bwd", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
     "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
@@ -63,6 +64,10 @@ class TraceStat(C.Structure):
                 ("flops", C.c_double), ("bytes", C.c_double)]
 
 
+class LstmReport(C.Structure):
+    _fields_ = [("timed_out", C.c_int32), ("bwd_groups", C.c_int32), ("bwd_local_groups", C.c_int32)]
+
+
 class MseDesc(C.Structure):
     _fields_ = [("rows", C.c_int32), ("H", C.c_int32), ("P", C.c_int32), ("dtype", C.c_int)]
 
@@ -88,6 +93,7 @@ def lib():
         L.janus_lstm_seq_bwd.argtypes = [C.POINTER(LstmDesc), vp, pi32, vp, vp, vp, sz, vp, vp, vp, vp, vp, vp,
                                          vp, vp, vp, vp]
         L.janus_lstm_schedule.argtypes = [i32, i32, pi32, pi32, pi32, pi32, pi32]
+        L.janus_lstm_device_report.argtypes = [C.POINTER(LstmDesc), vp, sz, C.POINTER(LstmReport), vp]
         L.janus_treelstm_workspace_bytes.restype = sz
         L.janus_treelstm_workspace_bytes.argtypes = [C.POINTER(TreeDesc), i32, i32]
         L.janus_tree_schedule_build.argtypes = [C.POINTER(TreeBatchC), i32, pi32, pi32, pi32, pi32]
@@ -178,6 +184,17 @@ def janus_lstm_seq_bwd(desc: LstmDesc, x, lengths, Wx, Wh, ws, dy, dhT, dcT, dx,
                                   ws.numel() * ws.element_size(), _p(dy), _p(dhT), _p(dcT), _p(dx), _p(dh0),
                                   _p(dc0), _ptr_array(dWx), _ptr_array(dWh), _ptr_array(db), _stream(stream))
     _check(st, "janus_lstm_seq_bwd")
+
+
+def janus_lstm_device_report(desc: LstmDesc, ws, stream=None) -> dict:
+    """Synchronises the stream and returns the report of the last LSTM call on
+    this workspace; raises JanusError(DEVICE) if a barrier wait ran out."""
+    rep = LstmReport()
+    st = lib().janus_lstm_device_report(C.byref(desc), _p(ws), ws.numel() * ws.element_size(), C.byref(rep),
+                                        _stream(stream))
+    _check(st, "janus_lstm_device_report")
+    return dict(timed_out=int(rep.timed_out), bwd_groups=int(rep.bwd_groups),
+                bwd_local_groups=int(rep.bwd_local_groups))
 
 
 def janus_lstm_schedule(B: int, T: int, lengths):

@@ -168,6 +168,22 @@ def test_lstm_rejects_small_workspace_and_bad_desc():
     assert all(v.untouched() for v in bf.values())
 
 
+def test_lstm_device_report_rejects_bad_arguments():
+    """The report call validates before it touches the device."""
+    import ctypes as C
+    d, bf, W, U, b = _lstm_args(ws_bytes=1024)
+    rep = J.LstmReport()
+    L = J.lib()
+    assert L.janus_lstm_device_report(C.byref(d), None, 0, None, None) == J.ERR_INVALID_ARG
+    assert L.janus_lstm_device_report(C.byref(d), None, 0, C.byref(rep), None) == J.ERR_WORKSPACE
+    with pytest.raises(J.JanusError) as e:
+        J.janus_lstm_device_report(d, bf["ws"], stream=0)
+    assert e.value.status == J.ERR_WORKSPACE
+    with pytest.raises(J.JanusError) as e:
+        J.janus_lstm_device_report(J.LstmDesc(1, 4, 8, 3, 5, 7), bf["ws"], stream=0)
+    assert e.value.status == J.ERR_UNSUPPORTED
+
+
 def test_lstm_bwd_rejects_bad_lengths_untouched():
     d, bf, W, U, b = _lstm_args()
     g = [_HostBuf(4 * 8 * 4 * 4) for _ in range(3)]

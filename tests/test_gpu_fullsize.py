@@ -38,6 +38,9 @@ def full_step():
     step = make_step(w)
     step.run()
     g = step.results()
+    from paper_1812_01329_amd import janus as J
+    rep = J.janus_lstm_device_report(step.desc, step.ws)   # raises if a barrier wait ran out
+    print(f"[fullsize] device report {rep}", flush=True)
     return w, g
 
 

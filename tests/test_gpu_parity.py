@@ -211,15 +211,27 @@ def test_long_ragged_batch_split_contractions():
 def test_backward_slices(slices, H, B, ragged, monkeypatch):
     """The persistent backward with its K = 4H gate columns in 4 and in 8
     slices (JANUS_BWD_SLICES): unit groups of 32 or 64, one or two weight
-    tiles per wave, groups placed on one XCD (H = 512) or adjacent (H = 200,
-    padded to 208, last group partial), full and split-K waves (B = 256, 70)."""
+    tiles per wave, full and split-K waves (B = 256, 70).  With H = 512 every
+    XCD holds whole groups (partial sums kept in the L2); with H = 200
+    (padded to 208, last group partial) the workgroup count is not a multiple
+    of 8 slices per XCD, so some groups straddle two XCDs and write their
+    partial sums through to memory."""
     from paper_1812_01329_amd import janus as J
     monkeypatch.setenv("JANUS_BWD_SLICES", slices)
     rng = np.random.default_rng(31)
     lens = rng.integers(0, 11, B) if ragged else None
     w = _lstm("mse", "bf16", L=2, I=64, H=H, B=B, T=10, lengths=lens, seed=31, h0=True, P=40)
     J.janus_trace_begin()
-    _, g = _run(w)
+    step, g = _run(w)
     labels = {r["label"] for r in J.janus_trace_end()}
     assert "lstm_bwd_persistent" in labels, labels
+    rep = J.janus_lstm_device_report(step.desc, step.ws)
+    print(f"[slices] H={H} B={B} NS={slices} report {rep}", flush=True)
+    units = 8 * int(slices)
+    assert rep["timed_out"] == 0
+    hp = (H + 15) // 16 * 16   # H padded to 16
+    assert rep["bwd_groups"] == 2 * ((hp + units - 1) // units)   # two layers
+    assert 0 <= rep["bwd_local_groups"] <= rep["bwd_groups"]
+    if H == 512:   # 64 workgroups: whole groups fit on the XCDs of an even placement
+        assert rep["bwd_local_groups"] > 0, rep
     compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
