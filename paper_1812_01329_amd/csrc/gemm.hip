@@ -133,6 +133,9 @@ struct NtArgs {
     float scale;
     float* part_sq;
     float* part_col;
+    // plain store epilogue in 16-byte row pieces through LDS (N and ldc
+    // multiples of 8, C and the bias 16-byte aligned)
+    int vec_store;
 };
 
 enum NtEpilogue { kEpiStore = 0, kEpiPartial = 1, kEpiMse = 2 };
@@ -373,7 +376,68 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
                 }
         }
     } else {
-        store_tile_impl<bf16_t, NtCfg, OutT, SCATTER>(g, acc, m0, n0, tid);
+        if (p.vec_store) {
+            // Stage each wave's accumulators through LDS as in the MSE epilogue
+            // (two halves of 64 rows x 64 columns, 8-column chunks swizzled by
+            // row); lane l then writes columns 8 (l % 8) .. + 7 of rows
+            // l / 8 + 8 q: 16 bytes (bf16) or 32 bytes (float32) per store.
+            const bf16_t* bias = static_cast<const bf16_t*>(g.bias);
+            OutT* C = static_cast<OutT*>(g.C);
+            __syncthreads();
+            float* tile = reinterpret_cast<float*>(wave < 4 ? stage0 : stage1) + (wave & 3) * 4096;
+            const int c8 = lane & 7, rq = lane >> 3;
+            const int ccol = n0 + wc0 + c8 * 8;
+            const bool cok = ccol < p.N;
+            float bv[8] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};
+            if (bias && cok) {
+                const uint4 braw = *reinterpret_cast<const uint4*>(bias + ccol);
+                const uint32_t bw[4] = {braw.x, braw.y, braw.z, braw.w};
+#pragma unroll
+                for (int e = 0; e < 4; ++e) {
+                    bv[2 * e] = bf2f(bf16_t(bw[e] & 0xffffu));
+                    bv[2 * e + 1] = bf2f(bf16_t(bw[e] >> 16));
+                }
+            }
+#pragma unroll
+            for (int half = 0; half < 2; ++half) {
+#pragma unroll
+                for (int ii = 0; ii < 2; ++ii)
+#pragma unroll
+                    for (int j = 0; j < C_::FN; ++j)
+#pragma unroll
+                        for (int v = 0; v < 16; ++v) {
+                            const int r = ii * 32 + acc_row(v, lane), c = j * 32 + acc_col(lane);
+                            tile[r * 64 + (c ^ ((r & 7) << 3))] = acc[2 * half + ii][j][v];
+                        }
+#pragma unroll
+                for (int q = 0; q < 8; ++q) {
+                    const int r = rq + 8 * q;
+                    const int row = m0 + wr0 + half * 64 + r;
+                    const float4 v0 = *reinterpret_cast<const float4*>(tile + r * 64 + ((c8 ^ (r & 7)) << 3));
+                    const float4 v1 = *reinterpret_cast<const float4*>(tile + r * 64 + ((c8 ^ (r & 7)) << 3) + 4);
+                    if (row < p.M && cok) {
+                        const int64_t crow = SCATTER ? int64_t(g.c_idx[row]) : int64_t(row);
+                        const float val[8] = {v0.x, v0.y, v0.z, v0.w, v1.x, v1.y, v1.z, v1.w};
+                        float o[8];
+#pragma unroll
+                        for (int e = 0; e < 8; ++e) o[e] = g.alpha * val[e] + bv[e];
+                        OutT* dst = C + crow * g.ldc + ccol;
+                        if constexpr (sizeof(OutT) == 2) {
+                            uint32_t w[4];
+#pragma unroll
+                            for (int e = 0; e < 4; ++e)
+                                w[e] = uint32_t(f2bf(o[2 * e])) | (uint32_t(f2bf(o[2 * e + 1])) << 16);
+                            *reinterpret_cast<uint4*>(dst) = make_uint4(w[0], w[1], w[2], w[3]);
+                        } else {
+                            *reinterpret_cast<float4*>(dst) = make_float4(o[0], o[1], o[2], o[3]);
+                            *reinterpret_cast<float4*>(dst + 4) = make_float4(o[4], o[5], o[6], o[7]);
+                        }
+                    }
+                }
+            }
+        } else {
+            store_tile_impl<bf16_t, NtCfg, OutT, SCATTER>(g, acc, m0, n0, tid);
+        }
     }
 }
 
@@ -590,8 +654,13 @@ const char* nt_label(bool f32out, bool scatter, bool partial) {
 }
 
 template <typename OutT, bool SCATTER, int EPI>
-janus_status launch_nt(const NtArgs& a, const GemmDesc& g, hipStream_t s) {
+janus_status launch_nt(const NtArgs& args, const GemmDesc& g, hipStream_t s) {
     auto kern = &gemm_nt_fast_kernel<OutT, SCATTER, EPI>;
+    NtArgs a = args;
+    a.vec_store = (EPI == kEpiStore && g.N % 8 == 0 && g.ldc % 8 == 0 && reinterpret_cast<uintptr_t>(g.C) % 16 == 0 &&
+                   (!g.bias || reinterpret_cast<uintptr_t>(g.bias) % 16 == 0))
+                      ? 1
+                      : 0;
     const double out_bytes = EPI == kEpiPartial ? 4.0 * a.splits : EPI == kEpiMse ? 4.0 : (sizeof(OutT) == 4 ? 4.0 : 2.0);
     TraceScope trace(EPI == kEpiMse ? "gemm_nt_mse" : nt_label(sizeof(OutT) == 4, SCATTER, EPI == kEpiPartial),
                      2.0 * g.M * g.N * double(g.K),
