@@ -45,6 +45,8 @@ struct TreeWs {
     float* dh = nullptr;         // [N x H]
     float* dc = nullptr;         // [N x H]
     float* dxl = nullptr;        // [N x E]   gradient of leaf inputs
+    float* Wt = nullptr;         // [E x 5H]  W transposed (forward)
+    float* Ut = nullptr;         // [2H x 5H] U transposed (forward)
     float* part = nullptr;
     int64_t ld5 = 0;
 };
@@ -66,6 +68,8 @@ size_t carve(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base, Tre
     w.dh = c.take<float>(int64_t(N) * H);
     w.dc = c.take<float>(int64_t(N) * H);
     w.dxl = c.take<float>(int64_t(N) * d.E);
+    w.Wt = c.take<float>(int64_t(d.E) * 5 * H);
+    w.Ut = c.take<float>(int64_t(2) * H * 5 * H);
     w.part = c.take<float>(colsum_partial_floats(5 * H));
     return c.off + 256;
 }
@@ -166,42 +170,118 @@ __global__ void tree_bwd_point_kernel(int p0, int rows, int H, int64_t ld5, cons
     }
 }
 
-// [dh_L; dh_R] = da U for the nodes of one level, scattered to the children
-template <class Cfg, bool AL>
-__global__ __launch_bounds__(Cfg::NT) void tree_dh_kernel(int p0, int rows, int H, int64_t ld5, const float* dA,
-                                                          const float* U, const int32_t* lchild,
-                                                          const int32_t* rchild, float* dh) {
-    extern __shared__ __align__(16) unsigned char smem_raw[];
-    float* sA = reinterpret_cast<float*>(smem_raw);
-    float* sB = sA + Cfg::BM * Cfg::LD;
-    const int tid = threadIdx.x;
-    const int n0 = blockIdx.x * Cfg::BN, m0 = blockIdx.y * Cfg::BM;
-    const int N = 2 * H;
-    LoaderK<float, Cfg::BM, Cfg::BK, Cfg::NT, AL> la;
-    LoaderT<float, Cfg::BN, Cfg::BK, Cfg::NT, AL> lb;
-    la.init(dA + int64_t(p0 + m0) * ld5, ld5, 0, RowsContig{rows - m0}, tid);
-    lb.init(U, N, nullptr, n0, N);
-    f32x16_t acc[Cfg::FM][Cfg::FN];
-    mma_mainloop<Cfg>(acc, la, lb, 5 * H, sA, sB, tid);
-    const int lane = tid & 63, wave = tid >> 6;
+// The contractions of the tree step are small: per level a few to a few
+// hundred rows against a 750 x 300 weight, and the weight gradients with
+// K = a few hundred nodes.  Tiles that walk K serially leave most of the GPU
+// idle and wait on one load round trip after another.  Instead each block
+// computes 8 rows x 64 columns of C = a . B with K split over its 8 waves:
+//   a(m, k) = A[arow(m) * lda + k]  (arow(m) = a_idx[m] or m), or with AT
+//             A[k * lda + m];
+//   B row k = B + brow(k) * ldb      (brow(k) = b_idx[k] or k), N contiguous.
+// The block's slab of a (8 rows, K in chunks of 1024) is staged in LDS and
+// read as broadcasts; each lane owns one column and streams its B entries
+// from the L2 (every row block reads the same B), 16 loads in flight.  The
+// waves' partial sums are added through LDS in wave order.  Epilogues: rows
+// of C (+ bias), or the backward's [dh_L; dh_R], whose two halves go to the
+// rows of the two children.
+constexpr int kSimtRows = 8, kSimtCols = 64, kSimtWaves = 8, kSimtKc = 1024;
+enum SimtEpi { kSimtStore = 0, kSimtChildren = 1 };
+
+template <bool AT, int EPI>
+__global__ __launch_bounds__(64 * kSimtWaves) void simt_gemm_kernel(int M, int N, int K, const float* A, int64_t lda,
+                                                                    const int32_t* a_idx, const float* B, int64_t ldb,
+                                                                    const int32_t* b_idx, const float* bias, float* C,
+                                                                    int64_t ldc, const int32_t* lchild,
+                                                                    const int32_t* rchild, int H) {
+    __shared__ __align__(16) float sA[kSimtKc][kSimtRows];
+    __shared__ float red[kSimtWaves][kSimtRows][kSimtCols];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int n = blockIdx.x * kSimtCols + lane;
+    const int m0 = blockIdx.y * kSimtRows;
+    float acc[kSimtRows];
 #pragma unroll
-    for (int j = 0; j < Cfg::FN; ++j) {
-        const int col = n0 + Cfg::wave_col0(wave) + j * 32 + acc_col(lane);
-        if (col >= N) continue;
-#pragma unroll
-        for (int i = 0; i < Cfg::FM; ++i)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) {
-                const int row = m0 + Cfg::wave_row0(wave) + i * 32 + acc_row(v, lane);
-                if (row >= rows) continue;
-                const int p = p0 + row;
-                if (col < H) dh[int64_t(lchild[p]) * H + col] = acc[i][j][v];
-                else dh[int64_t(rchild[p]) * H + col - H] = acc[i][j][v];
+    for (int r = 0; r < kSimtRows; ++r) acc[r] = 0.f;
+    for (int k0 = 0; k0 < K; k0 += kSimtKc) {
+        const int kc = min(kSimtKc, K - k0);
+        __syncthreads();
+        for (int i = tid; i < kSimtKc * kSimtRows; i += 64 * kSimtWaves) {
+            // AT: consecutive threads read consecutive m of one k; otherwise
+            // consecutive k of one row
+            const int r = AT ? i % kSimtRows : i / kSimtKc, kk = AT ? i / kSimtRows : i % kSimtKc;
+            const int m = m0 + r;
+            float v = 0.f;
+            if (m < M && kk < kc) {
+                if (AT) v = A[int64_t(k0 + kk) * lda + m];
+                else v = A[(a_idx ? int64_t(a_idx[m]) : int64_t(m)) * lda + k0 + kk];
             }
+            sA[kk][r] = v;
+        }
+        __syncthreads();
+        const int kb = wave * kc / kSimtWaves, ke = (wave + 1) * kc / kSimtWaves;
+        if (n < N) {
+#pragma unroll 16
+            for (int kk = kb; kk < ke; ++kk) {
+                const int k = k0 + kk;
+                const float bv = B[(b_idx ? int64_t(b_idx[k]) : int64_t(k)) * ldb + n];
+                const float4 a0 = *reinterpret_cast<const float4*>(&sA[kk][0]);
+                const float4 a1 = *reinterpret_cast<const float4*>(&sA[kk][4]);
+                acc[0] += a0.x * bv; acc[1] += a0.y * bv; acc[2] += a0.z * bv; acc[3] += a0.w * bv;
+                acc[4] += a1.x * bv; acc[5] += a1.y * bv; acc[6] += a1.z * bv; acc[7] += a1.w * bv;
+            }
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kSimtRows; ++r) red[wave][r][lane] = acc[r];
+    __syncthreads();
+    // thread (row r = wave, column lane) adds the waves' parts in order
+    const int r = wave, m = m0 + r;
+    if (m >= M || n >= N) return;
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kSimtWaves; ++w) sum += red[w][r][lane];
+    if constexpr (EPI == kSimtChildren) {
+        if (n < H) C[int64_t(lchild[m]) * H + n] = sum;
+        else C[int64_t(rchild[m]) * H + n - H] = sum;
+    } else {
+        C[int64_t(m) * ldc + n] = sum + (bias ? bias[n] : 0.f);
     }
 }
 
-using TreeCfg = TileCfg<float, 64, 64, 32, 2, 2>;
+template <bool AT, int EPI>
+janus_status simt_gemm(const char* label, int M, int N, int K, const float* A, int64_t lda, const int32_t* a_idx,
+                       const float* B, int64_t ldb, const int32_t* b_idx, const float* bias, float* C, int64_t ldc,
+                       hipStream_t st, const int32_t* lchild = nullptr, const int32_t* rchild = nullptr, int H = 0) {
+    if (M <= 0 || N <= 0) return JANUS_OK;
+    dim3 grid(unsigned((N + kSimtCols - 1) / kSimtCols), unsigned((M + kSimtRows - 1) / kSimtRows));
+    TraceScope trace(label, 2.0 * M * N * double(K), 4.0 * (double(M) * K + double(K) * N + double(M) * N), st);
+    hipLaunchKernelGGL((simt_gemm_kernel<AT, EPI>), grid, dim3(64 * kSimtWaves), 0, st, M, N, K, A, lda, a_idx, B,
+                       ldb, b_idx, bias, C, ldc, lchild, rchild, H);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+// out[c * R + r] = in[r * C + c], float32
+__global__ void transpose_f32_kernel(const float* in, int R, int C, float* out) {
+    __shared__ float t[32][33];
+    const int c0 = blockIdx.x * 32, r0 = blockIdx.y * 32;
+    for (int i = threadIdx.y; i < 32; i += 8) {
+        const int r = r0 + i, c = c0 + threadIdx.x;
+        if (r < R && c < C) t[i][threadIdx.x] = in[int64_t(r) * C + c];
+    }
+    __syncthreads();
+    for (int i = threadIdx.y; i < 32; i += 8) {
+        const int c = c0 + i, r = r0 + threadIdx.x;
+        if (r < R && c < C) out[int64_t(c) * R + r] = t[threadIdx.x][i];
+    }
+}
+
+janus_status transpose_f32(const float* in, int R, int C, float* out, hipStream_t st) {
+    TraceScope trace("transpose_f32", 0.0, 8.0 * R * double(C), st);
+    hipLaunchKernelGGL(transpose_f32_kernel, dim3(unsigned((C + 31) / 32), unsigned((R + 31) / 32)), dim3(32, 8), 0, st,
+                       in, R, C, out);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
 
 janus_status check(const janus_treelstm_desc* d) {
     if (!d || d->E <= 0 || d->H <= 0 || d->V <= 0) return JANUS_ERR_INVALID_ARG;
@@ -258,31 +338,22 @@ extern "C" janus_status janus_treelstm_fwd(const janus_treelstm_desc* d, const j
     if ((e = upload_tree(t, s, w, st)) != JANUS_OK) return e;
     const int H = d->H, E = d->E;
     const int M0 = s.level_offsets[1];
+    // the level contractions read W and U transposed (N = 5H contiguous)
+    if ((e = transpose_f32(static_cast<const float*>(W), 5 * H, E, w.Wt, st)) != JANUS_OK) return e;
+    if ((e = transpose_f32(static_cast<const float*>(U), 5 * H, 2 * H, w.Ut, st)) != JANUS_OK) return e;
+    const float* bias = static_cast<const float*>(b);
     for (int k = 0; k < s.num_levels; ++k) {
         const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
-        GemmDesc g;
-        g.dtype = JANUS_F32;
-        g.M = rows;
-        g.N = 5 * H;
-        if (k == 0) {
-            g.K = E;
-            g.A = emb;
-            g.lda = E;
-            g.a_idx = w.lword;
-            g.B = W;
-            g.ldb = E;
-        } else {
-            g.K = 2 * H;
-            g.A = w.HLR + int64_t(p0 - M0) * 2 * H;
-            g.lda = 2 * H;
-            g.B = U;
-            g.ldb = 2 * H;
-        }
-        g.C = w.A + int64_t(p0) * w.ld5;
-        g.ldc = w.ld5;
-        g.c_f32 = true;
-        g.bias = b;
-        if ((e = gemm(g, st)) != JANUS_OK) return e;
+        // A_k = a . W^T + b over the rows of level k: leaves gather their
+        // embedding rows, internal nodes read [h_L; h_R]
+        if (k == 0)
+            e = simt_gemm<false, kSimtStore>("tree_level_gemm", rows, 5 * H, E, static_cast<const float*>(emb), E,
+                                             w.lword, w.Wt, 5 * H, nullptr, bias, w.A, w.ld5, st);
+        else
+            e = simt_gemm<false, kSimtStore>("tree_level_gemm", rows, 5 * H, 2 * H,
+                                             w.HLR + int64_t(p0 - M0) * 2 * H, 2 * H, nullptr, w.Ut, 5 * H, nullptr,
+                                             bias, w.A + int64_t(p0) * w.ld5, w.ld5, st);
+        if (e != JANUS_OK) return e;
         const int64_t n = int64_t(rows) * H;
         TraceScope trace("tree_fwd_point", 0.0, 4.0 * n * 14.0, st);
         hipLaunchKernelGGL(tree_fwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H, M0,
@@ -314,7 +385,6 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
                        w.rootpos, static_cast<const float*>(dh_root), w.dh, w.dc);
     JANUS_LAUNCH_CHECK();
     }
-    const bool al = (int64_t(2) * H * 4) % 16 == 0 && reinterpret_cast<uintptr_t>(U) % 16 == 0;
     for (int k = s.num_levels - 1; k >= 0; --k) {
         const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
         const int64_t n = int64_t(rows) * H;
@@ -325,58 +395,24 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
         JANUS_LAUNCH_CHECK();
         }
         if (k == 0) break;
-        dim3 grid((2 * H + TreeCfg::BN - 1) / TreeCfg::BN, (rows + TreeCfg::BM - 1) / TreeCfg::BM);
-        TraceScope trace("tree_dh_gemm", 2.0 * rows * 2.0 * H * 5.0 * H,
-                         4.0 * (double(rows) * 5 * H + 10.0 * H * H + 2.0 * rows * H), st);
-        if (al)
-            hipLaunchKernelGGL((tree_dh_kernel<TreeCfg, true>), grid, dim3(TreeCfg::NT), TreeCfg::SMEM_BYTES, st, p0,
-                               rows, H, w.ld5, w.A, static_cast<const float*>(U), w.lchild, w.rchild, w.dh);
-        else
-            hipLaunchKernelGGL((tree_dh_kernel<TreeCfg, false>), grid, dim3(TreeCfg::NT), TreeCfg::SMEM_BYTES, st, p0,
-                               rows, H, w.ld5, w.A, static_cast<const float*>(U), w.lchild, w.rchild, w.dh);
-        JANUS_LAUNCH_CHECK();
+        // [dh_L; dh_R] = da U for the nodes of the level, to their children
+        e = simt_gemm<false, kSimtChildren>("tree_dh_gemm", rows, 2 * H, 5 * H, w.A + int64_t(p0) * w.ld5, w.ld5,
+                                            nullptr, static_cast<const float*>(U), 2 * H, nullptr, nullptr, w.dh, 0,
+                                            st, w.lchild + p0, w.rchild + p0, H);
+        if (e != JANUS_OK) return e;
     }
     // dU = da_int^T HLR  (K = internal nodes)
-    GemmDesc g;
-    g.dtype = JANUS_F32;
-    g.M = 5 * H;
-    g.N = 2 * H;
-    g.K = N - M0;
-    g.a_t = true;
-    g.A = w.A + int64_t(M0) * w.ld5;
-    g.lda = w.ld5;
-    g.b_t = true;
-    g.B = w.HLR;
-    g.ldb = 2 * H;
-    g.C = dU;
-    g.ldc = 2 * H;
-    g.c_f32 = true;
-    if ((e = gemm(g, st)) != JANUS_OK) return e;
+    e = simt_gemm<true, kSimtStore>("tree_dU_gemm", 5 * H, 2 * H, N - M0, w.A + int64_t(M0) * w.ld5, w.ld5, nullptr,
+                                    w.HLR, 2 * H, nullptr, nullptr, dU, 2 * H, st);
+    if (e != JANUS_OK) return e;
     // dW = da_leaf^T emb[word]  (K = leaves, gathered rows of emb)
-    g.N = E;
-    g.K = M0;
-    g.A = w.A;
-    g.B = emb;
-    g.ldb = E;
-    g.b_idx = w.lword;
-    g.C = dW;
-    g.ldc = E;
-    if ((e = gemm(g, st)) != JANUS_OK) return e;
+    e = simt_gemm<true, kSimtStore>("tree_dW_gemm", 5 * H, E, M0, w.A, w.ld5, nullptr, static_cast<const float*>(emb),
+                                    E, w.lword, nullptr, dW, E, st);
+    if (e != JANUS_OK) return e;
     if ((e = colsum(JANUS_F32, w.A, N, 5 * H, w.ld5, db, w.part, st)) != JANUS_OK) return e;
     // dx_leaf = da_leaf W, then the embedding gradient
-    GemmDesc q;
-    q.dtype = JANUS_F32;
-    q.M = M0;
-    q.N = E;
-    q.K = 5 * H;
-    q.A = w.A;
-    q.lda = w.ld5;
-    q.b_t = true;
-    q.B = W;
-    q.ldb = E;
-    q.C = w.dxl;
-    q.ldc = E;
-    q.c_f32 = true;
-    if ((e = gemm(q, st)) != JANUS_OK) return e;
+    e = simt_gemm<false, kSimtStore>("tree_dx_gemm", M0, E, 5 * H, w.A, w.ld5, nullptr, static_cast<const float*>(W), E,
+                                     nullptr, nullptr, w.dxl, E, st);
+    if (e != JANUS_OK) return e;
     return embed_backward(JANUS_F32, w.dxl, w.lword, M0, E, demb, d->V, st);
 }
