@@ -260,6 +260,81 @@ janus_status simt_gemm(const char* label, int M, int N, int K, const float* A, i
     return JANUS_OK;
 }
 
+// One backward level k >= 1 in one launch: block (x, y) first applies the
+// cell backward to the 8 rows y*8.. of the level (all 5H gate columns; every
+// column block does this, block x = 0 also writes da and the children's dc
+// to memory), straight into the LDS slab, then computes columns x*64.. of
+// [dh_L; dh_R] = da U with K = 5H split over its waves, as simt_gemm_kernel.
+__global__ __launch_bounds__(64 * kSimtWaves) void tree_bwd_level_kernel(int p0, int rows, int H, int64_t ld5,
+                                                                         const float* G, const float* C,
+                                                                         const float* dh_in, float* dc,
+                                                                         const int32_t* lchild, const int32_t* rchild,
+                                                                         float* dA, const float* U, float* dh) {
+    __shared__ __align__(16) float sA[kSimtKc][kSimtRows];
+    __shared__ float red[kSimtWaves][kSimtRows][kSimtCols];
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    const int N = 2 * H, K = 5 * H;
+    const int n = blockIdx.x * kSimtCols + lane;
+    const int m0 = blockIdx.y * kSimtRows;
+    const bool writer = blockIdx.x == 0;
+    for (int i = tid; i < kSimtRows * H; i += 64 * kSimtWaves) {
+        const int r = i / H, j = i - r * H, m = m0 + r;
+        float da[5] = {0.f, 0.f, 0.f, 0.f, 0.f};
+        if (m < rows) {
+            const int p = p0 + m;
+            const float* g = G + int64_t(p) * ld5 + j;
+            const float gi = g[0], gl = g[H], gr = g[2 * H], go = g[3 * H], gu = g[4 * H];
+            const int lc = lchild[p], rc = rchild[p];
+            const float cl = C[int64_t(lc) * H + j], cr = C[int64_t(rc) * H + j];
+            const float c = C[int64_t(p) * H + j];
+            const float dhv = dh_in[int64_t(p) * H + j];
+            const float tau = tanhf_(c);
+            const float d_o = dhv * tau;
+            const float dct = dc[int64_t(p) * H + j] + dhv * go * (1.f - tau * tau);
+            da[0] = dct * gu * gi * (1.f - gi);
+            da[1] = dct * cl * gl * (1.f - gl);
+            da[2] = dct * cr * gr * (1.f - gr);
+            da[3] = d_o * go * (1.f - go);
+            da[4] = dct * gi * (1.f - gu * gu);
+            if (writer) {
+                float* dst = dA + int64_t(p) * ld5 + j;
+#pragma unroll
+                for (int q = 0; q < 5; ++q) dst[q * H] = da[q];
+                dc[int64_t(lc) * H + j] = dct * gl;
+                dc[int64_t(rc) * H + j] = dct * gr;
+            }
+        }
+#pragma unroll
+        for (int q = 0; q < 5; ++q) sA[q * H + j][r] = da[q];
+    }
+    __syncthreads();
+    float acc[kSimtRows];
+#pragma unroll
+    for (int r = 0; r < kSimtRows; ++r) acc[r] = 0.f;
+    const int kb = wave * K / kSimtWaves, ke = (wave + 1) * K / kSimtWaves;
+    if (n < N) {
+#pragma unroll 16
+        for (int k = kb; k < ke; ++k) {
+            const float bv = U[int64_t(k) * N + n];
+            const float4 a0 = *reinterpret_cast<const float4*>(&sA[k][0]);
+            const float4 a1 = *reinterpret_cast<const float4*>(&sA[k][4]);
+            acc[0] += a0.x * bv; acc[1] += a0.y * bv; acc[2] += a0.z * bv; acc[3] += a0.w * bv;
+            acc[4] += a1.x * bv; acc[5] += a1.y * bv; acc[6] += a1.z * bv; acc[7] += a1.w * bv;
+        }
+    }
+#pragma unroll
+    for (int r = 0; r < kSimtRows; ++r) red[wave][r][lane] = acc[r];
+    __syncthreads();
+    const int r = wave, m = m0 + r;
+    if (m >= rows || n >= N) return;
+    float sum = 0.f;
+#pragma unroll
+    for (int w = 0; w < kSimtWaves; ++w) sum += red[w][r][lane];
+    const int p = p0 + m;
+    if (n < H) dh[int64_t(lchild[p]) * H + n] = sum;
+    else dh[int64_t(rchild[p]) * H + n - H] = sum;
+}
+
 // out[c * R + r] = in[r * C + c], float32
 __global__ void transpose_f32_kernel(const float* in, int R, int C, float* out) {
     __shared__ float t[32][33];
@@ -388,18 +463,34 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
     for (int k = s.num_levels - 1; k >= 0; --k) {
         const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
         const int64_t n = int64_t(rows) * H;
-        {
-        TraceScope trace("tree_bwd_point", 0.0, 4.0 * n * 17.0, st);
-        hipLaunchKernelGGL(tree_bwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H,
-                           w.ld5, w.G, w.C, w.dh, w.dc, w.lchild, w.rchild, w.A);
-        JANUS_LAUNCH_CHECK();
+        if (k == 0) {
+            TraceScope trace("tree_bwd_point", 0.0, 4.0 * n * 17.0, st);
+            hipLaunchKernelGGL(tree_bwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H,
+                               w.ld5, w.G, w.C, w.dh, w.dc, w.lchild, w.rchild, w.A);
+            JANUS_LAUNCH_CHECK();
+            break;
         }
-        if (k == 0) break;
-        // [dh_L; dh_R] = da U for the nodes of the level, to their children
-        e = simt_gemm<false, kSimtChildren>("tree_dh_gemm", rows, 2 * H, 5 * H, w.A + int64_t(p0) * w.ld5, w.ld5,
-                                            nullptr, static_cast<const float*>(U), 2 * H, nullptr, nullptr, w.dh, 0,
-                                            st, w.lchild + p0, w.rchild + p0, H);
-        if (e != JANUS_OK) return e;
+        if (5 * H > kSimtKc) {
+            // gate columns do not fit one LDS slab: pointwise, then the contraction
+            {
+                TraceScope trace("tree_bwd_point", 0.0, 4.0 * n * 17.0, st);
+                hipLaunchKernelGGL(tree_bwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows,
+                                   H, w.ld5, w.G, w.C, w.dh, w.dc, w.lchild, w.rchild, w.A);
+                JANUS_LAUNCH_CHECK();
+            }
+            e = simt_gemm<false, kSimtChildren>("tree_dh_gemm", rows, 2 * H, 5 * H, w.A + int64_t(p0) * w.ld5, w.ld5,
+                                                nullptr, static_cast<const float*>(U), 2 * H, nullptr, nullptr, w.dh,
+                                                0, st, w.lchild + p0, w.rchild + p0, H);
+            if (e != JANUS_OK) return e;
+            continue;
+        }
+        // cell backward of the level and [dh_L; dh_R] = da U to the children
+        dim3 grid(unsigned((2 * H + kSimtCols - 1) / kSimtCols), unsigned((rows + kSimtRows - 1) / kSimtRows));
+        TraceScope trace("tree_bwd_level", 2.0 * rows * 2.0 * H * 5.0 * H,
+                         4.0 * (double(rows) * 17.0 * H + 10.0 * H * H + 2.0 * rows * H), st);
+        hipLaunchKernelGGL(tree_bwd_level_kernel, grid, dim3(64 * kSimtWaves), 0, st, p0, rows, H, w.ld5, w.G, w.C,
+                           w.dh, w.dc, w.lchild, w.rchild, w.A, static_cast<const float*>(U), w.dh);
+        JANUS_LAUNCH_CHECK();
     }
     // dU = da_int^T HLR  (K = internal nodes)
     e = simt_gemm<true, kSimtStore>("tree_dU_gemm", 5 * H, 2 * H, N - M0, w.A + int64_t(M0) * w.ld5, w.ld5, nullptr,

@@ -89,6 +89,20 @@ def test_treelstm_fp32():
     assert np.all(g["dW"][H:3 * H] == 0.0)   # forget rows of W see no gradient
 
 
+def test_treelstm_wide_hidden_fp32():
+    """H = 240: the five gate blocks (5H = 1200) exceed one LDS slab of the
+    fused backward level kernel, so the levels take the separate pointwise
+    kernel and contraction, and the contractions walk K in two chunks."""
+    w = wl.sst_treelstm(n_trees=6, E=40, H=240, V=64, seed=13)
+    _, g = _run(w)
+    r = oracle_steps.tree_step(w)
+    t = TOL["f32"]
+    check("loss", np.array([g["loss"]]), np.array([r["loss"]]), t["out"])
+    check("h_root", g["h_root"], r["h_root"], t["out"])
+    for k in ("dh_root", "dW", "dU", "db", "demb"):
+        check(k, g[k], r[k], t["grad"])
+
+
 def test_lm2048_reduced_shape_bf16():
     """The regression workload's structure (2 layers, projection + MSE) at a
     shape the oracle runs in seconds, spanning several tiles with ragged tails."""
