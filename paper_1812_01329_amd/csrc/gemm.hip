@@ -104,7 +104,7 @@ __global__ __launch_bounds__(Cfg::NT) void gemm_kernel(GemmDesc g) {
 // path.  Optional K split: each split writes float32 partials that a second
 // kernel sums in split order (deterministic).
 struct NtCfg {
-    static constexpr int BM = 256, BN = 256, BK = 64, NSTAGE = 2, NT = 512;
+    static constexpr int BM = 256, BN = 256, BK = 64, NT = 512;
     static constexpr int WGM = 2, WGN = 4, WTM = BM / WGM, WTN = BN / WGN;
     static constexpr int FM = WTM / 32, FN = WTN / 32;
     static constexpr int CPR = BK / 8;                        // 16-byte chunks per tile row

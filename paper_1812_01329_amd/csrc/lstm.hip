@@ -1030,63 +1030,102 @@ size_t carve_pad(const janus_lstm_desc& d, void* base, PadWs& w) {
     return c.off + 256;
 }
 
-// dst[r, c] (r < rows, c < cols) = src[sr, c] for c < scols, else 0, where
-// the source row sr is r (gate_dH == 0) or, for gate-major parameter rows,
-// gate g = r / gate_dH, unit u = r % gate_dH, sr = g * gate_sH + u (no source
-// row, i.e. 0, when u >= gate_sH).
+// A batch of padding copies in one launch.  Copy o:
+//   dst[r, c] (r < rows, c < cols) = src[sr, c] for c < scols, else 0,
+// where the source row sr is r (gate_dH == 0) or, for gate-major parameter
+// rows, gate g = r / gate_dH, unit u = r % gate_dH, sr = g * gate_sH + u (no
+// source row, i.e. 0, when u >= gate_sH).  Elements are es = 2 or 4 bytes.
+// blockIdx.y selects the copy; blocks stride over its elements.
+constexpr int kMaxRemaps = 16;
+struct RemapOp {
+    const void* src;
+    void* dst;
+    int64_t sld, dld, rows;
+    int scols, cols, gate_sH, gate_dH, es;
+};
+struct RemapBatch {
+    RemapOp op[kMaxRemaps];
+};
+
 template <typename T>
-__global__ void remap_kernel(const T* src, int64_t sld, int scols, T* dst, int64_t dld, int64_t rows, int cols,
-                             int gate_sH, int gate_dH) {
-    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= rows * cols) return;
-    const int64_t r = i / cols;
-    const int c = int(i % cols);
+__device__ __forceinline__ void remap_one(const RemapOp& o, int64_t i) {
+    const int64_t r = i / o.cols;
+    const int c = int(i % o.cols);
     int64_t sr = r;
-    bool ok = c < scols;
-    if (gate_dH > 0) {
-        const int64_t g = r / gate_dH, u = r % gate_dH;
-        ok = ok && u < gate_sH;
-        sr = g * gate_sH + u;
+    bool ok = c < o.scols;
+    if (o.gate_dH > 0) {
+        const int64_t g = r / o.gate_dH, u = r % o.gate_dH;
+        ok = ok && u < o.gate_sH;
+        sr = g * o.gate_sH + u;
     }
-    dst[r * dld + c] = ok ? src[sr * sld + c] : T(0);
+    static_cast<T*>(o.dst)[r * o.dld + c] = ok ? static_cast<const T*>(o.src)[sr * o.sld + c] : T(0);
 }
 
-template <typename T>
-janus_status remap(const void* src, int64_t sld, int scols, void* dst, int64_t dld, int64_t rows, int cols, int gate_sH,
-                   int gate_dH, hipStream_t st) {
-    const int64_t n = rows * cols;
-    if (n <= 0) return JANUS_OK;
-    TraceScope trace("pad_copy", 0.0, 2.0 * double(n) * sizeof(T), st);
-    hipLaunchKernelGGL(remap_kernel<T>, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, static_cast<const T*>(src),
-                       sld, scols, static_cast<T*>(dst), dld, rows, cols, gate_sH, gate_dH);
-    JANUS_LAUNCH_CHECK();
-    return JANUS_OK;
+__global__ __launch_bounds__(256) void remap_batch_kernel(RemapBatch b) {
+    const RemapOp& o = b.op[blockIdx.y];
+    const int64_t n = o.rows * o.cols;
+    for (int64_t i = int64_t(blockIdx.x) * 256 + threadIdx.x; i < n; i += int64_t(gridDim.x) * 256) {
+        if (o.es == 2) remap_one<uint16_t>(o, i);
+        else remap_one<uint32_t>(o, i);
+    }
 }
 
-// padded copies of the parameters (and x) shared by both passes
+// Collects copies and launches them together (in groups of kMaxRemaps).
+struct RemapList {
+    RemapBatch b{};
+    int n = 0;
+    int64_t most = 0;
+    template <typename T>
+    janus_status add(const void* src, int64_t sld, int scols, void* dst, int64_t dld, int64_t rows, int cols,
+                     int gate_sH, int gate_dH, hipStream_t st) {
+        if (rows * cols <= 0) return JANUS_OK;
+        if (n == kMaxRemaps) {
+            janus_status e = launch(st);
+            if (e != JANUS_OK) return e;
+        }
+        b.op[n++] = RemapOp{src, dst, sld, dld, rows, scols, cols, gate_sH, gate_dH, int(sizeof(T))};
+        most = std::max(most, rows * cols);
+        return JANUS_OK;
+    }
+    janus_status launch(hipStream_t st) {
+        if (n == 0) return JANUS_OK;
+        double bytes = 0;
+        for (int i = 0; i < n; ++i) bytes += 2.0 * double(b.op[i].rows) * b.op[i].cols * b.op[i].es;
+        TraceScope trace("pad_copy", 0.0, bytes, st);
+        const unsigned gx = unsigned(std::min<int64_t>((most + 255) / 256, 1024));
+        hipLaunchKernelGGL(remap_batch_kernel, dim3(gx, unsigned(n)), dim3(256), 0, st, b);
+        JANUS_LAUNCH_CHECK();
+        n = 0;
+        most = 0;
+        return JANUS_OK;
+    }
+};
+
+// padded copies of the parameters and x, made by the forward call and kept in
+// the workspace for its backward
 janus_status pad_params(const janus_lstm_desc& d, const janus_lstm_desc& p, const PadWs& w, const void* x,
-                        const void* const* Wx, const void* const* Wh, const void* const* b, hipStream_t st) {
+                        const void* const* Wx, const void* const* Wh, const void* const* b, RemapList& q,
+                        hipStream_t st) {
     janus_status e;
     for (int l = 0; l < d.L; ++l) {
         const int Il = l == 0 ? d.I : d.H, Ilp = l == 0 ? p.I : p.H;
-        if ((e = remap<bf16_t>(Wx[l], Il, Il, w.Wx[l], Ilp, int64_t(4) * p.H, Ilp, d.H, p.H, st)) != JANUS_OK) return e;
-        if ((e = remap<bf16_t>(Wh[l], d.H, d.H, w.Wh[l], p.H, int64_t(4) * p.H, p.H, d.H, p.H, st)) != JANUS_OK)
+        if ((e = q.add<bf16_t>(Wx[l], Il, Il, w.Wx[l], Ilp, int64_t(4) * p.H, Ilp, d.H, p.H, st)) != JANUS_OK) return e;
+        if ((e = q.add<bf16_t>(Wh[l], d.H, d.H, w.Wh[l], p.H, int64_t(4) * p.H, p.H, d.H, p.H, st)) != JANUS_OK)
             return e;
-        if (b && (e = remap<bf16_t>(b[l], 1, 1, w.b[l], 1, int64_t(4) * p.H, 1, d.H, p.H, st)) != JANUS_OK) return e;
+        if ((e = q.add<bf16_t>(b[l], 1, 1, w.b[l], 1, int64_t(4) * p.H, 1, d.H, p.H, st)) != JANUS_OK) return e;
     }
-    if (x && d.T > 0)
-        return remap<bf16_t>(x, d.I, d.I, w.x, p.I, int64_t(d.T) * d.B, p.I, 0, 0, st);
+    if (x && d.T > 0) return q.add<bf16_t>(x, d.I, d.I, w.x, p.I, int64_t(d.T) * d.B, p.I, 0, 0, st);
     return JANUS_OK;
 }
 
 // [L*B x H] float32 state in / out of the padded layout
 janus_status pad_state(const janus_lstm_desc& d, const janus_lstm_desc& p, const float* src, float* dst,
-                       hipStream_t st) {
-    return remap<float>(src, d.H, d.H, dst, p.H, int64_t(d.L) * d.B, p.H, 0, 0, st);
+                       RemapList& q, hipStream_t st) {
+    return q.add<float>(src, d.H, d.H, dst, p.H, int64_t(d.L) * d.B, p.H, 0, 0, st);
 }
 janus_status unpad_state(const janus_lstm_desc& d, const janus_lstm_desc& p, const float* src, float* dst,
-                         hipStream_t st) {
-    return remap<float>(src, p.H, p.H, dst, d.H, int64_t(d.L) * d.B, d.H, 0, 0, st);
+                         RemapList& q, hipStream_t st) {
+    return q.add<float>(src, p.H, p.H, dst, d.H, int64_t(d.L) * d.B, d.H, 0, 0, st);
 }
 
 janus_status lstm_fwd_padded(const janus_lstm_desc& d, const SeqSchedule& s, void* ws, const void* x,
@@ -1097,19 +1136,21 @@ janus_status lstm_fwd_padded(const janus_lstm_desc& d, const SeqSchedule& s, voi
     carve_pad(d, ws, w);
     LstmWs inner;
     carve(p, ws, inner);
-    janus_status e = pad_params(d, p, w, x, Wx, Wh, b, st);
+    RemapList q;
+    janus_status e = pad_params(d, p, w, x, Wx, Wh, b, q, st);
     if (e != JANUS_OK) return e;
-    if (h0 && (e = pad_state(d, p, h0, w.s0, st)) != JANUS_OK) return e;
-    if (c0 && (e = pad_state(d, p, c0, w.s1, st)) != JANUS_OK) return e;
+    if (h0 && (e = pad_state(d, p, h0, w.s0, q, st)) != JANUS_OK) return e;
+    if (c0 && (e = pad_state(d, p, c0, w.s1, q, st)) != JANUS_OK) return e;
+    if ((e = q.launch(st)) != JANUS_OK) return e;
     std::vector<const void*> Wxp(w.Wx.begin(), w.Wx.end()), Whp(w.Wh.begin(), w.Wh.end()), bp(w.b.begin(), w.b.end());
     e = lstm_fwd_impl<bf16_t, StepBF16>(p, s, inner, w.x, Wxp.data(), Whp.data(), bp.data(), h0 ? w.s0 : nullptr,
                                         c0 ? w.s1 : nullptr, w.y, w.s2, w.s3, st);
     if (e != JANUS_OK) return e;
-    if (d.T > 0 && (e = remap<bf16_t>(w.y, p.H, p.H, y, d.H, int64_t(d.T) * d.B, d.H, 0, 0, st)) != JANUS_OK)
+    if (d.T > 0 && (e = q.add<bf16_t>(w.y, p.H, p.H, y, d.H, int64_t(d.T) * d.B, d.H, 0, 0, st)) != JANUS_OK)
         return e;
-    if (hT && (e = unpad_state(d, p, w.s2, hT, st)) != JANUS_OK) return e;
-    if (cT && (e = unpad_state(d, p, w.s3, cT, st)) != JANUS_OK) return e;
-    return JANUS_OK;
+    if (hT && (e = unpad_state(d, p, w.s2, hT, q, st)) != JANUS_OK) return e;
+    if (cT && (e = unpad_state(d, p, w.s3, cT, q, st)) != JANUS_OK) return e;
+    return q.launch(st);
 }
 
 janus_status lstm_bwd_padded(const janus_lstm_desc& d, const SeqSchedule& s, void* ws, const void* x,
@@ -1121,29 +1162,34 @@ janus_status lstm_bwd_padded(const janus_lstm_desc& d, const SeqSchedule& s, voi
     carve_pad(d, ws, w);
     LstmWs inner;
     carve(p, ws, inner);
-    janus_status e = pad_params(d, p, w, x, Wx, Wh, nullptr, st);
-    if (e != JANUS_OK) return e;
+    // the padded Wx, Wh and x are still in the workspace from the forward call
+    (void)x;
+    (void)Wx;
+    (void)Wh;
+    RemapList q;
+    janus_status e;
     const int64_t TB = int64_t(d.T) * d.B;
-    if (dy && TB > 0 && (e = remap<bf16_t>(dy, d.H, d.H, w.y, p.H, TB, p.H, 0, 0, st)) != JANUS_OK) return e;
-    if (dhT && (e = pad_state(d, p, dhT, w.s0, st)) != JANUS_OK) return e;
-    if (dcT && (e = pad_state(d, p, dcT, w.s1, st)) != JANUS_OK) return e;
+    if (dy && TB > 0 && (e = q.add<bf16_t>(dy, d.H, d.H, w.y, p.H, TB, p.H, 0, 0, st)) != JANUS_OK) return e;
+    if (dhT && (e = pad_state(d, p, dhT, w.s0, q, st)) != JANUS_OK) return e;
+    if (dcT && (e = pad_state(d, p, dcT, w.s1, q, st)) != JANUS_OK) return e;
+    if ((e = q.launch(st)) != JANUS_OK) return e;
     std::vector<const void*> Wxp(w.Wx.begin(), w.Wx.end()), Whp(w.Wh.begin(), w.Wh.end());
     e = lstm_bwd_impl<bf16_t, StepBF16>(p, s, inner, w.x, Wxp.data(), Whp.data(), dy ? w.y : nullptr,
                                         dhT ? w.s0 : nullptr, dcT ? w.s1 : nullptr, dx ? w.dx : nullptr, w.s2, w.s3,
                                         w.dWx.data(), w.dWh.data(), w.db.data(), st);
     if (e != JANUS_OK) return e;
-    if (dx && TB > 0 && (e = remap<bf16_t>(w.dx, p.I, p.I, dx, d.I, TB, d.I, 0, 0, st)) != JANUS_OK) return e;
-    if (dh0 && (e = unpad_state(d, p, w.s2, dh0, st)) != JANUS_OK) return e;
-    if (dc0 && (e = unpad_state(d, p, w.s3, dc0, st)) != JANUS_OK) return e;
+    if (dx && TB > 0 && (e = q.add<bf16_t>(w.dx, p.I, p.I, dx, d.I, TB, d.I, 0, 0, st)) != JANUS_OK) return e;
+    if (dh0 && (e = unpad_state(d, p, w.s2, dh0, q, st)) != JANUS_OK) return e;
+    if (dc0 && (e = unpad_state(d, p, w.s3, dc0, q, st)) != JANUS_OK) return e;
     for (int l = 0; l < d.L; ++l) {
         const int Il = l == 0 ? d.I : d.H, Ilp = l == 0 ? p.I : p.H;
-        if ((e = remap<float>(w.dWx[l], Ilp, Ilp, dWx[l], Il, int64_t(4) * d.H, Il, p.H, d.H, st)) != JANUS_OK)
+        if ((e = q.add<float>(w.dWx[l], Ilp, Ilp, dWx[l], Il, int64_t(4) * d.H, Il, p.H, d.H, st)) != JANUS_OK)
             return e;
-        if ((e = remap<float>(w.dWh[l], p.H, p.H, dWh[l], d.H, int64_t(4) * d.H, d.H, p.H, d.H, st)) != JANUS_OK)
+        if ((e = q.add<float>(w.dWh[l], p.H, p.H, dWh[l], d.H, int64_t(4) * d.H, d.H, p.H, d.H, st)) != JANUS_OK)
             return e;
-        if ((e = remap<float>(w.db[l], 1, 1, db[l], 1, int64_t(4) * d.H, 1, p.H, d.H, st)) != JANUS_OK) return e;
+        if ((e = q.add<float>(w.db[l], 1, 1, db[l], 1, int64_t(4) * d.H, 1, p.H, d.H, st)) != JANUS_OK) return e;
     }
-    return JANUS_OK;
+    return q.launch(st);
 }
 
 }  // namespace
