@@ -136,6 +136,9 @@ janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void* x,
  *                    when the per-step kernels ran).
  *  bwd_local_groups  of those, groups whose workgroups all ran on one XCD
  *                    and kept their partial sums in its L2.
+ *  fwd_groups, fwd_local_groups  the same for the forward recurrence when
+ *                    its contraction is split over the columns of Wh (0
+ *                    otherwise).
  * Errors: INVALID_ARG (bad d, NULL out), WORKSPACE (as for the calls above),
  * DEVICE (a HIP call failed, or timed_out is 1).
  */
@@ -143,6 +146,8 @@ typedef struct {
     int32_t timed_out;
     int32_t bwd_groups;
     int32_t bwd_local_groups;
+    int32_t fwd_groups;
+    int32_t fwd_local_groups;
 } janus_lstm_report;
 
 janus_status janus_lstm_device_report(const janus_lstm_desc* d, const void* ws, size_t ws_bytes,
@@ -337,6 +342,11 @@ janus_status janus_trace_end(janus_trace_stat* out, int32_t max_out, int32_t* n_
 /* ------------------------------------------------------------------------ */
 const char* janus_status_string(janus_status s);
 const char* janus_version(void);
+/* Text naming the HIP call behind the last JANUS_ERR_DEVICE returned on the
+ * calling thread (HIP error name and code, the call, source file and line),
+ * or "" before any.  The string is owned by the library and stays valid until
+ * the next such error on the thread. */
+const char* janus_last_error(void);
 
 #ifdef __cplusplus
 }

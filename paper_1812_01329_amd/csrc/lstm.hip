@@ -73,6 +73,60 @@ struct LstmWs {
     int64_t ldh = 0, ldg = 0, ldk = 0;
 };
 
+// ------------------------------------------------------- persistent path
+struct DeviceInfo {
+    int cus = 0;
+    int coop = 0;
+    size_t lds = 0;
+    int xccs = 0;
+};
+
+DeviceInfo device_info() {
+    static DeviceInfo cache[64];
+    static bool have[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DeviceInfo{};
+    if (!have[dev]) {
+        DeviceInfo d;
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) d.cus = v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess) d.coop = v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess) d.lds = size_t(v);
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeNumberOfXccs, dev) == hipSuccess) d.xccs = v;
+        // a failed query must not surface as the error of a later launch check
+        (void)hipGetLastError();
+        cache[dev] = d;
+        have[dev] = true;
+    }
+    return cache[dev];
+}
+
+// Forward K split (persistent path): the k-groups of 16 columns of h (Kp / 16)
+// are split in `ns` slices and the units in groups of 8 ns; one workgroup per
+// (slice, group) holds the rows of the group's units for its slice.
+int persist_fwd_nkg(const janus_lstm_desc& d) { return int(round_up(d.H, 64) / 16); }
+int persist_fwd_ksp(const janus_lstm_desc& d, int ns) { return 16 * ((persist_fwd_nkg(d) + ns - 1) / ns); }
+int persist_fwd_groups(const janus_lstm_desc& d, int ns) { return (d.H + 8 * ns - 1) / (8 * ns); }
+int persist_fwd_blocks(const janus_lstm_desc& d, int ns) { return ns * persist_fwd_groups(d, ns); }
+
+// Groups whose members may straddle an XCD boundary: at most one fewer than
+// the XCDs (all the census can tell apart when the count is unknown).
+int persist_straddle_slots() {
+    const int x = device_info().xccs;
+    return (x > 0 && x <= persist::kMaxXcds ? x : persist::kMaxXcds) - 1;
+}
+
+// Floats of the forward's partial sums at `ns` slices: one slot reused by
+// groups on one XCD, then per step and straddling group a slot of its own.
+int64_t persist_fwd_part_local(const janus_lstm_desc& d, int ns) {
+    return int64_t(ns) * persist_fwd_groups(d, ns) * ns * ((d.B + 31) / 32) * 1024;
+}
+int64_t persist_fwd_part_floats(const janus_lstm_desc& d, int ns) {
+    if (ns <= 1) return 0;
+    return persist_fwd_part_local(d, ns) +
+           int64_t(d.T) * persist_straddle_slots() * ns * ns * ((d.B + 31) / 32) * 1024;
+}
+
 // Contraction scratch for every contraction of the forward and backward
 // passes (they run one after another on one stream, so one buffer serves all).
 size_t lstm_gemm_scratch(const janus_lstm_desc& d) {
@@ -138,7 +192,10 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     w.off_dev = c.take<int32_t>(int64_t(d.T) + 2);
     w.sync = c.take<persist::Sync>(1);
     if (d.dtype == JANUS_BF16) {
-        w.dpart = c.take<float>((int64_t(d.T) + 1) * persist::kMaxSlices * d.B * round_up(d.H, 8 * persist::kMaxSlices));
+        // partial sums of the persistent backward, and of the forward (the two
+        // never run at the same time)
+        const int64_t bwd_part = (int64_t(d.T) + 1) * persist::kMaxSlices * d.B * round_up(d.H, 8 * persist::kMaxSlices);
+        w.dpart = c.take<float>(std::max({bwd_part, persist_fwd_part_floats(d, 2), persist_fwd_part_floats(d, 4)}));
         w.gf_slot = round_up(d.B, 32) * int64_t(4) * d.H;
         w.Gf = c.take<bf16_t>(int64_t(d.T) * w.gf_slot);
         w.ldht = round_up(int64_t(d.B) + TB, 64);
@@ -154,36 +211,12 @@ size_t carve(const janus_lstm_desc& d, void* base, LstmWs& w) {
     return c.off + 256;
 }
 
-// ------------------------------------------------------- persistent path
-struct DeviceInfo {
-    int cus = 0;
-    int coop = 0;
-    size_t lds = 0;
-};
-
-DeviceInfo device_info() {
-    static DeviceInfo cache[64];
-    static bool have[64] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DeviceInfo{};
-    if (!have[dev]) {
-        DeviceInfo d;
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) d.cus = v;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess) d.coop = v;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess) d.lds = size_t(v);
-        cache[dev] = d;
-        have[dev] = true;
-    }
-    return cache[dev];
-}
-
 int persist_kw(int B) { return B <= 32 ? 8 : B <= 64 ? 4 : B <= 128 ? 2 : 1; }
 
 size_t persist_red_bytes(int kw) { return size_t(kw - 1) * (persist::kWaves / kw) * 4096; }
 
-size_t persist_fwd_lds(const janus_lstm_desc& d) {
-    return size_t(32) * (round_up(d.H, 64) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
+size_t persist_fwd_lds(const janus_lstm_desc& d, int ns) {
+    return size_t(32 * ns) * (persist_fwd_ksp(d, ns) + 8) * 2 + persist_red_bytes(persist_kw(d.B));
 }
 // Backward: the k-groups of 16 interleaved gate columns (4H / 16) are split
 // in `ns` slices and the units in groups of 8 ns; one workgroup per (slice,
@@ -195,13 +228,30 @@ size_t persist_bwd_lds(const janus_lstm_desc& d, int ns) {
 }
 int persist_bwd_groups(const janus_lstm_desc& d, int ns) { return (d.H + 8 * ns - 1) / (8 * ns); }
 int persist_bwd_blocks(const janus_lstm_desc& d, int ns) { return ns * persist_bwd_groups(d, ns); }
-int persist_fwd_blocks(const janus_lstm_desc& d) { return (d.H + persist::kUnitsFwd - 1) / persist::kUnitsFwd; }
 
 size_t device_lds(const DeviceInfo& info) { return info.lds > 0 ? info.lds : 65536; }
 
 bool persist_bwd_fits(const janus_lstm_desc& d, int ns, const DeviceInfo& info) {
     return persist_bwd_blocks(d, ns) <= info.cus && persist_bwd_groups(d, ns) <= persist::kMaxGroups &&
            persist_bwd_lds(d, ns) <= device_lds(info);
+}
+
+bool persist_fwd_fits(const janus_lstm_desc& d, int ns, const DeviceInfo& info) {
+    return persist_fwd_blocks(d, ns) <= info.cus && (ns == 1 || persist_fwd_groups(d, ns) <= persist::kMaxGroups) &&
+           persist_fwd_lds(d, ns) <= device_lds(info);
+}
+
+// Slices of the persistent forward: 1 unless JANUS_FWD_SLICES=2 or 4 asks
+// for a split.  At H = 2048, B = 256 two slices shorten the contraction from
+// about 11 to 8 us per step but add the exchange (about 2.5 us), and in a
+// whole training step, with the chip at its power limit, the split ran
+// slower (8.9 against 8.4 ms for the two layers).  Four slices lose more:
+// their partial sums (3 MB per XCD) no longer stay in the L2.
+int persist_fwd_slices(const janus_lstm_desc& d) {
+    const DeviceInfo info = device_info();
+    const char* e = getenv("JANUS_FWD_SLICES");
+    const int forced = (e && (e[0] == '1' || e[0] == '2' || e[0] == '4')) ? e[0] - '0' : 1;
+    return persist_fwd_fits(d, forced, info) ? forced : 0;
 }
 
 // Slices of the persistent backward: 8 where the layout fits (half the
@@ -227,8 +277,7 @@ bool use_persistent(const janus_lstm_desc& d) {
     if (!env || d.dtype != JANUS_BF16 || d.H % 8 != 0 || d.B > persist::kMaxB) return false;
     const DeviceInfo info = device_info();
     if (!info.coop || info.cus <= 0) return false;
-    if (persist_fwd_blocks(d) > info.cus || persist_fwd_lds(d) > device_lds(info)) return false;
-    return persist_bwd_slices(d) > 0;
+    return persist_fwd_slices(d) > 0 && persist_bwd_slices(d) > 0;
 }
 
 __global__ void perm4_kernel(int H, int32_t* perm4) {
@@ -505,30 +554,34 @@ template <class K>
 janus_status coop_launch(K kernel, int blocks, size_t smem, void* arg, hipStream_t st, size_t& attr_smem) {
     // the kernel's dynamic LDS limit, raised whenever a launch needs more
     if (smem > attr_smem) {
-        if (hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                int(smem)) != hipSuccess)
-            return JANUS_ERR_DEVICE;
+        JANUS_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      int(smem)));
         attr_smem = smem;
     }
     void* args[] = {arg};
-    if (hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), dim3(blocks), dim3(persist::kThreads), args,
-                                   unsigned(smem), st) != hipSuccess)
-        return JANUS_ERR_DEVICE;
+    JANUS_HIP(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), dim3(blocks), dim3(persist::kThreads),
+                                         args, unsigned(smem), st));
     return JANUS_OK;
 }
 
-janus_status launch_fwd_persistent(const janus_lstm_desc& d, persist::FwdArgs& a, double flops, hipStream_t st) {
-    static size_t attr[4] = {};
+janus_status launch_fwd_persistent(const janus_lstm_desc& d, int ns, persist::FwdArgs& a, double flops,
+                                   hipStream_t st) {
+    static size_t attr[3][4] = {};
     const int kw = persist_kw(d.B);
-    const size_t smem = persist_fwd_lds(d);
-    const int blocks = persist_fwd_blocks(d);
+    const size_t smem = persist_fwd_lds(d, ns);
+    const int blocks = persist_fwd_blocks(d, ns);
     TraceScope trace("lstm_fwd_persistent", flops, 0.0, st);
-    switch (kw) {
-        case 1: return coop_launch(persist::lstm_fwd_persistent<1>, blocks, smem, &a, st, attr[0]);
-        case 2: return coop_launch(persist::lstm_fwd_persistent<2>, blocks, smem, &a, st, attr[1]);
-        case 4: return coop_launch(persist::lstm_fwd_persistent<4>, blocks, smem, &a, st, attr[2]);
-        default: return coop_launch(persist::lstm_fwd_persistent<8>, blocks, smem, &a, st, attr[3]);
+#define JANUS_FWD_CASES(NS, I)                                                                               \
+    switch (kw) {                                                                                            \
+        case 1: return coop_launch(persist::lstm_fwd_persistent<1, NS>, blocks, smem, &a, st, attr[I][0]); \
+        case 2: return coop_launch(persist::lstm_fwd_persistent<2, NS>, blocks, smem, &a, st, attr[I][1]); \
+        case 4: return coop_launch(persist::lstm_fwd_persistent<4, NS>, blocks, smem, &a, st, attr[I][2]); \
+        default: return coop_launch(persist::lstm_fwd_persistent<8, NS>, blocks, smem, &a, st, attr[I][3]); \
     }
+    if (ns == 4) JANUS_FWD_CASES(4, 2)
+    if (ns == 2) JANUS_FWD_CASES(2, 1)
+    JANUS_FWD_CASES(1, 0)
+#undef JANUS_FWD_CASES
 }
 
 janus_status launch_bwd_persistent(const janus_lstm_desc& d, int ns, persist::BwdArgs& a, double flops,
@@ -621,6 +674,12 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     a.t_eff = s.t_eff;
     a.fixed = s.fixed ? 1 : 0;
     a.Kp = int(round_up(H, 64));
+    const int ns = persist_fwd_slices(d);
+    a.nkg = persist_fwd_nkg(d);
+    a.ksp = persist_fwd_ksp(d, ns);
+    a.part = w.dpart;
+    a.part_local = persist_fwd_part_local(d, ns);
+    a.nstraddle = persist_straddle_slots();
     a.active = w.act_dev;
     a.offsets = w.off_dev;
     a.perm = perm;
@@ -639,7 +698,7 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     a.HT = use_ht(d, s, true) ? w.HT[l] : nullptr;
     a.ldht = w.ldht;
     a.sync = w.sync;
-    return launch_fwd_persistent(d, a, 2.0 * 4.0 * H * double(H) * recurrent_rows(s), st);
+    return launch_fwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * recurrent_rows(s), st);
 }
 
 template <typename T, class Cfg>
@@ -1277,11 +1336,13 @@ extern "C" janus_status janus_lstm_device_report(const janus_lstm_desc* d, const
         return JANUS_ERR_WORKSPACE;
     LstmWs w;
     carve(needs_padding(*d) ? padded_desc(*d) : *d, const_cast<void*>(ws), w);
-    unsigned rep[3] = {0u, 0u, 0u};
-    if (hipStreamSynchronize(static_cast<hipStream_t>(stream)) != hipSuccess) return JANUS_ERR_DEVICE;
-    if (hipMemcpy(rep, &w.sync->error, sizeof(rep), hipMemcpyDeviceToHost) != hipSuccess) return JANUS_ERR_DEVICE;
+    unsigned rep[5] = {0u, 0u, 0u, 0u, 0u};
+    JANUS_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+    JANUS_HIP(hipMemcpy(rep, &w.sync->error, sizeof(rep), hipMemcpyDeviceToHost));
     out->timed_out = rep[0] != 0u ? 1 : 0;
     out->bwd_groups = int32_t(rep[1]);
     out->bwd_local_groups = int32_t(rep[2]);
+    out->fwd_groups = int32_t(rep[3]);
+    out->fwd_local_groups = int32_t(rep[4]);
     return out->timed_out ? JANUS_ERR_DEVICE : JANUS_OK;
 }

@@ -37,11 +37,11 @@ namespace persist {
 
 constexpr int kThreads = 512;          // 8 waves
 constexpr int kWaves = kThreads / 64;
-constexpr int kUnitsFwd = 8;           // hidden units per forward workgroup (32 gate rows)
 constexpr int kMaxSlices = 8;          // largest K-split of the backward contraction
 constexpr int kMaxB = 256;             // batch rows handled by one pass of 8 waves
 constexpr int kSpinLimit = 1 << 22;    // bounded wait at each barrier (~0.1 s)
-constexpr int kMaxGroups = 64;         // backward unit groups (H / (8 NS)) a launch may have
+constexpr int kMaxGroups = 128;        // unit groups (H / (8 NS)) a launch may have
+constexpr int kMaxXcds = 16;           // XCDs the census can tell apart (XCC_ID is 4 bits)
 
 // Device-wide barrier state.  The counters (up to `error`) are zeroed before
 // every launch; the report that follows them is zeroed once per library call
@@ -51,11 +51,13 @@ struct Sync {
     unsigned pad0[63];
     unsigned xcd[16][64];              // per-XCD arrivals
     unsigned census[16][64];           // workgroups resident on each XCD
-    unsigned group[kMaxGroups][64];    // arrivals of each backward unit group
+    unsigned group[kMaxGroups][64];    // arrivals of each unit group
     unsigned error;                    // set when a wait exceeds its spin limit
     unsigned groups;                   // backward unit groups launched
     unsigned local_groups;             // of which kept their partial sums in one XCD's L2
-    unsigned pad1[61];
+    unsigned fwd_groups;               // the same for the forward
+    unsigned fwd_local_groups;
+    unsigned pad1[59];
 };
 constexpr size_t kSyncCounterBytes = offsetof(Sync, error);
 
@@ -160,10 +162,74 @@ __device__ __forceinline__ void barrier_wait(Barrier& b) {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
 }
 
+// Barrier among the `members` workgroups of one unit group (they exchange
+// partial sums only among themselves).  When all members run on one XCD they
+// share its L2: the sums are stored write-back (the L2 acknowledges them
+// before the arrival) and read with device-scope loads, which miss in the L1
+// and return the L2's copy, so one slot serves every step (a step's sums are
+// read before the grid barrier after which the next step overwrites them).
+// Otherwise they are written through to memory into a slot fresh for each
+// step, as for the grid barrier.
+//
+// Every wave waits for its own stores before the workgroup barrier: the
+// workgroup-scope fence of __syncthreads does not wait for global stores
+// (the waves share the CU's L1), so without it the arrival could overtake
+// another wave's partial sums.
+__device__ __forceinline__ void group_barrier(Sync* s, unsigned* cnt, unsigned& phase, unsigned members) {
+    ++phase;
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x == 0) {
+        __builtin_amdgcn_s_waitcnt(0);
+        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        spin_until(s, cnt, phase * members);
+    }
+    __syncthreads();
+}
+
+// Place of a workgroup in the unit groups of NS members, from its census
+// rank p = xfirst + xidx: member s = p mod NS of group v = p / NS.  The
+// members hold consecutive ranks, so they run on one XCD (`local`) unless
+// the group contains an XCD boundary (a rank at which the next nonempty
+// XCD's workgroups begin).  Such a group is numbered by the boundaries at or
+// before its first rank (`straddle`, below the number of XCDs minus one),
+// which indexes the slots it needs per step.  All members compute the same
+// values from the census, which is complete after barrier_init.
+struct GroupPlace {
+    int s, v, local, straddle;
+};
+template <int NS>
+__device__ __forceinline__ GroupPlace group_place(const Barrier& bar, Sync* sync) {
+    __shared__ int place[4];
+    if (threadIdx.x == 0) {
+        const unsigned p = bar.xfirst + bar.xidx;
+        const unsigned g0 = p - p % NS;
+        unsigned end = 0, before = 0;
+        bool cross = false;
+        for (unsigned q = 0; q < unsigned(kMaxXcds); ++q) {
+            const unsigned c = __hip_atomic_load(&sync->census[q][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (c == 0u) continue;
+            end += c;
+            if (end >= bar.nb) break;   // the end of the last XCD is no boundary
+            if (end <= g0) ++before;
+            else if (end < g0 + NS) cross = true;
+        }
+        place[0] = int(p % NS);
+        place[1] = int(p / NS);
+        place[2] = cross ? 0 : 1;
+        place[3] = int(before);
+    }
+    __syncthreads();
+    return GroupPlace{place[0], place[1], place[2], place[3]};
+}
+
 // ---------------------------------------------------------------- forward
 struct FwdArgs {
     int H, B, t_eff, fixed;
     int Kp;                            // H rounded up to 64
+    int nkg;                           // k-groups of 16 columns of h (Kp / 16)
+    int ksp;                           // columns of the widest K slice (multiple of 16)
     const int32_t* active;             // [T + 1] (ignored when fixed)
     const int32_t* offsets;            // [T + 2] (ignored when fixed)
     const int32_t* perm;               // [B] or NULL
@@ -180,6 +246,13 @@ struct FwdArgs {
     int64_t hf_slot;                   // elements per slot: round_up(B, 32) * Kp
     bf16_t* HT;                        // [H x ldht] h transposed, column B + p = h at packed row p, or NULL
     int64_t ldht;
+    // K-split (NS > 1): partial gate pre-activations exchanged in each unit
+    // group.  `part` holds one slot [writer][group][reader][batch tile][1024]
+    // reused every step by groups on one XCD (part_local floats), then, per
+    // step and straddling group, [t][straddle][writer][reader][batch tile][1024].
+    float* part;
+    int64_t part_local;
+    int nstraddle;                     // straddling groups the slots are sized for
     Sync* sync;
 };
 
@@ -209,15 +282,19 @@ __device__ __forceinline__ int64_t off_at(const int32_t* offsets, int fixed, int
 // cell update reads and writes 16- and 32-byte pieces.
 __device__ __forceinline__ int fwd_row_unit(int i) { return 4 * ((i >> 2) & 1) + (i >> 3); }
 
-// Load the 32 rows of the forward weight slice into LDS (k contiguous,
-// padded pitch `wld`, zeros past H).
-__device__ __forceinline__ void stage_fwd_weights(const FwdArgs& a, bf16_t* Ws, int wld, int u0) {
-    const int chunks = a.Kp / 8;
-    for (int idx = threadIdx.x; idx < 32 * chunks; idx += kThreads) {
-        const int i = idx / chunks, kc = (idx - i * chunks) * 8;
-        const int u = u0 + fwd_row_unit(i), g = i & 3;
+// Load the forward weights of a workgroup into LDS: for each member m of its
+// unit group (units v0 + 8 m + [0, 8)), 32 rows in the order above, columns
+// [c0, c1) of Wh (its K slice) at LDS columns [0, c1 - c0); k contiguous,
+// pitch `wld`, zeros past H.  Tile m starts at row 32 m.
+template <int NS>
+__device__ __forceinline__ void stage_fwd_weights(const FwdArgs& a, bf16_t* Ws, int wld, int v0, int c0, int c1) {
+    const int chunks = a.ksp / 8;
+    for (int idx = threadIdx.x; idx < 32 * NS * chunks; idx += kThreads) {
+        const int i = idx / chunks, kl = (idx - i * chunks) * 8, kc = c0 + kl;
+        const int m = i >> 5, ii = i & 31;
+        const int u = v0 + 8 * m + fwd_row_unit(ii), g = ii & 3;
         uint4 v = make_uint4(0, 0, 0, 0);
-        if (u < a.H && kc < a.H) {
+        if (u < a.H && kc < a.H && kc < c1) {
             const bf16_t* src = a.Wh + (int64_t(g) * a.H + u) * a.H + kc;
             if (kc + 8 <= a.H && (a.H % 8) == 0) {
                 v = *reinterpret_cast<const uint4*>(src);
@@ -227,7 +304,7 @@ __device__ __forceinline__ void stage_fwd_weights(const FwdArgs& a, bf16_t* Ws, 
                 __builtin_memcpy(&v, tmp, 16);
             }
         }
-        *reinterpret_cast<uint4*>(Ws + i * wld + kc) = v;
+        *reinterpret_cast<uint4*>(Ws + i * wld + kl) = v;
     }
 }
 
@@ -403,29 +480,73 @@ __device__ __forceinline__ void contract_frag_mt(f32x16_t (&acc)[MT], const bf16
 constexpr int kDepthFrag2 = 8;
 constexpr int kDepthFrag = 12;
 
-template <int KW>
+// One layer's forward recurrence.  NS == 1: workgroup q owns units
+// [8 q, 8 q + 8) and contracts all of h_{t-1} against their 32 rows of Wh.
+// NS > 1 (K split): the units are split in groups of 8 NS and the columns of
+// Wh in NS slices; member s of group v holds the rows of all 8 NS units for
+// slice s, contracts slice s of h_{t-1} (1 / NS of the stream) into partial
+// pre-activations of the whole group, and owns the cells of units
+// v0 + 8 s + [0, 8).  The members exchange partial sums as the backward does.
+template <int KW, int NS>
 __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
+    static_assert(NS == 1 || NS == 2 || NS == 4, "slices of the forward contraction");
+    constexpr int MT = NS;            // 32-row weight tiles per wave: one per member of the group
     extern __shared__ __align__(16) unsigned char smem_raw[];
-    const int wld = a.Kp + 8;
+    const int wld = a.ksp + 8;
     bf16_t* Ws = reinterpret_cast<bf16_t*>(smem_raw);
-    float* red = reinterpret_cast<float*>(smem_raw + size_t(32) * wld * sizeof(bf16_t));
+    float* red = reinterpret_cast<float*>(smem_raw + size_t(32 * NS) * wld * sizeof(bf16_t));
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
-    const int u0 = blockIdx.x * kUnitsFwd;
+    Barrier bar;
+    barrier_init(bar, a.sync);
+    int s = 0, v = int(blockIdx.x), straddle = 0;
+    bool plocal = true;
+    if constexpr (NS > 1) {
+        const GroupPlace gp = group_place<NS>(bar, a.sync);
+        s = gp.s;
+        v = gp.v;
+        plocal = gp.local != 0;
+        straddle = gp.straddle;
+        if (threadIdx.x == 0 && s == 0) {
+            __hip_atomic_fetch_add(&a.sync->fwd_groups, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            if (plocal)
+                __hip_atomic_fetch_add(&a.sync->fwd_local_groups, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+            // slots were sized for fewer straddling groups than the census found:
+            // report it, and the partial sums below go nowhere
+            if (!plocal && straddle >= a.nstraddle)
+                __hip_atomic_store(&a.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        }
+    }
+    const int ngroups = int(gridDim.x) / NS;
+    const int v0 = v * 8 * NS;                // first unit of the group
+    const int u0 = v0 + 8 * s;                // first unit whose cells this workgroup owns
     constexpr int NB = kWaves / KW;
     const int bt = wave % NB, kw = wave / NB;
-    const int nkg = a.Kp / 16;
-    const int kg0 = kw * nkg / KW, kg1 = (kw + 1) * nkg / KW;
+    const int sg0 = s * a.nkg / NS, sgn = (s + 1) * a.nkg / NS - sg0;   // k-groups of slice s
+    const int kg0 = kw * sgn / KW, kg1 = (kw + 1) * sgn / KW;
     const bf16_t* wrow = Ws + (lane & 31) * wld + 8 * (lane >> 5) + kg0 * 16;
-    const uint32_t hoff = (uint32_t(bt * nkg + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
+    const uint32_t hoff = (uint32_t(bt * a.nkg + sg0 + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
     const int H = a.H;
     const int row = bt * 32 + (lane & 31);   // this lane's batch row (sorted order)
     const int ub = u0 + 4 * (lane >> 5);      // its four consecutive units
-    const bool owner = kw == 0;               // lanes of these waves own cells
+    // lanes of the kw == 0 waves own cells; with NS > 1 the last group may
+    // extend past H, and its units there have none
+    const bool owner = kw == 0 && ub < H;
     const int b = (owner && row < a.B && a.perm) ? a.perm[row] : row;   // caller's batch index
-    Barrier bar;
-    barrier_init(bar, a.sync);
+    unsigned* gcnt = NS > 1 ? &a.sync->group[v][0] : nullptr;
+    unsigned gphase = 0;
+    const int nbt = (a.B + 31) / 32;          // batch tiles of 32 rows
+    const uint32_t tile_bytes = uint32_t(nbt) * 4096u;
+    // tile (writer j, reader m) of this group's partial sums at step t
+    auto part_tile = [&](int j, int m, int t) -> __amdgpu_buffer_rsrc_t {
+        if (plocal)
+            return make_rsrc(a.part + ((int64_t(j) * ngroups + v) * NS + m) * nbt * 1024, tile_bytes);
+        const bool room = straddle < a.nstraddle;
+        return make_rsrc(a.part + a.part_local +
+                             ((((int64_t(t) * a.nstraddle + (room ? straddle : 0)) * NS + j) * NS + m) * nbt) * 1024,
+                         room ? tile_bytes : 0u);
+    };
 
-    stage_fwd_weights(a, Ws, wld, u0);
+    stage_fwd_weights<NS>(a, Ws, wld, v0, 16 * sg0, 16 * (sg0 + sgn));
     // the cell state of the owned cells stays in registers for the launch
     float creg[4] = {0.f, 0.f, 0.f, 0.f};
     if (owner && row < a.B) {
@@ -454,15 +575,71 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
         const int64_t off_t = off_at(a.offsets, a.fixed, a.B, t);
         const bool cell = owner && row < act;
         const bool more = t + 1 < a.t_eff;
-        f32x16_t acc;
+        f32x16_t accs[MT];
 #pragma unroll
-        for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+        for (int m = 0; m < MT; ++m)
+#pragma unroll
+            for (int e = 0; e < 16; ++e) accs[m][e] = 0.f;
         if (bt * 32 < act) {
             // h_{t-1} is slot t of the fragment-layout copy
             const auto rs = make_rsrc(a.Hf + int64_t(t) * a.hf_slot, uint32_t(a.hf_slot) * 2u);
-            contract_frag<kDepthFrag>(acc, wrow, rs, hoff, kg1 - kg0);
+            contract_frag_mt<MT == 1 ? kDepthFrag : kDepthFrag2, MT>(accs, wrow, 32 * wld, rs, hoff, kg1 - kg0);
         }
-        reduce_kparts<KW>(acc, red, wave, lane);
+#pragma unroll
+        for (int m = 0; m < MT; ++m) {
+            if (KW > 1 && m > 0) __syncthreads();   // the previous tile's K parts have been read
+            reduce_kparts<KW>(accs[m], red, wave, lane);
+        }
+        f32x16_t acc = accs[0];
+        if constexpr (NS > 1) {
+            // tile m of a wave holds the pre-activations of member m's units for
+            // its 32 batch rows; lane l's 16 values are stored as four 16-byte
+            // pieces q, so each store of a wave is 1 KB in one piece
+            const uint32_t po = uint32_t((bt * 4) * 64 + lane) * 16u;
+            if (kw == 0 && bt * 32 < act) {
+#pragma unroll
+                for (int m = 0; m < MT; ++m) {
+                    if (m == s) continue;
+                    const auto rp = part_tile(s, m, t);
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const uint4 pv = make_uint4(__float_as_uint(accs[m][4 * q]), __float_as_uint(accs[m][4 * q + 1]),
+                                                    __float_as_uint(accs[m][4 * q + 2]),
+                                                    __float_as_uint(accs[m][4 * q + 3]));
+                        if (plocal) store16<kStoreBack>(rp, po + uint32_t(q) * 1024u, pv);
+                        else store16<kStoreThrough>(rp, po + uint32_t(q) * 1024u, pv);
+                    }
+                }
+            }
+            group_barrier(a.sync, gcnt, gphase, unsigned(NS));
+            // this workgroup's own tile, then the members' sums in member order
+            f32x16_t own = accs[0];
+#pragma unroll
+            for (int m = 1; m < MT; ++m)
+                if (m == s) own = accs[m];
+            uint4 pin[NS][4];
+#pragma unroll
+            for (int j = 0; j < NS; ++j) {
+                const auto rp = part_tile(j, s, t);
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const uint32_t o = (owner && row < act && j != s) ? po + uint32_t(q) * 1024u : kOutOfRange;
+                    pin[j][q] = plocal ? load16_l2(rp, o) : load16(rp, o);
+                }
+            }
+#pragma unroll
+            for (int e = 0; e < 16; ++e) acc[e] = 0.f;
+#pragma unroll
+            for (int j = 0; j < NS; ++j) {
+#pragma unroll
+                for (int q = 0; q < 4; ++q) {
+                    const float pj[4] = {__uint_as_float(pin[j][q].x), __uint_as_float(pin[j][q].y),
+                                         __uint_as_float(pin[j][q].z), __uint_as_float(pin[j][q].w)};
+#pragma unroll
+                    for (int e = 0; e < 4; ++e) acc[4 * q + e] += j == s ? own[4 * q + e] : pj[e];
+                }
+            }
+        }
         float hn[4] = {0.f, 0.f, 0.f, 0.f};
         uint32_t gw[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};
         uint2 hb = make_uint2(0u, 0u);
@@ -579,25 +756,6 @@ __device__ __forceinline__ void stage_bwd_weights(const BwdArgs& a, bf16_t* Ws, 
         if (c < c1 && c < 4 * H && u < H) v = a.Wh[(int64_t(c & 3) * H + (c >> 2)) * H + u];
         Ws[uu * wld + kk] = v;
     }
-}
-
-// Barrier among the `members` workgroups of one unit group (they exchange
-// partial sums only among themselves).  When all members run on one XCD they
-// share its L2: the sums are stored write-back (the L2 acknowledges them
-// before the arrival) and read with device-scope loads, which miss in the L1
-// and return the L2's copy, so one slot serves every step (a step's sums are
-// read before the grid barrier after which the next step overwrites them).
-// Otherwise they are written through to memory into a slot fresh for each
-// step, as for the grid barrier.
-__device__ __forceinline__ void group_barrier(Sync* s, unsigned* cnt, unsigned& phase, unsigned members) {
-    ++phase;
-    __syncthreads();
-    if (threadIdx.x == 0) {
-        __builtin_amdgcn_s_waitcnt(0);
-        __hip_atomic_fetch_add(cnt, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        spin_until(s, cnt, phase * members);
-    }
-    __syncthreads();
 }
 
 template <int KW, int NS>

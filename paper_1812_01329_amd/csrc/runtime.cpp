@@ -1,11 +1,23 @@
 // Host runtime: pinned staging ring for schedule uploads, status strings.
 #include "runtime.hpp"
 
+#include <cstdio>
 #include <cstring>
 #include <deque>
 #include <mutex>
 
 namespace janus {
+
+namespace {
+thread_local char g_last_error[512] = "";
+}
+
+janus_status device_error(hipError_t e, const char* what, const char* file, int line) {
+    const char* base = std::strrchr(file, '/');
+    std::snprintf(g_last_error, sizeof(g_last_error), "%s (%d) from %s at %s:%d", hipGetErrorName(e), int(e), what,
+                  base ? base + 1 : file, line);
+    return JANUS_ERR_DEVICE;
+}
 
 namespace {
 
@@ -20,9 +32,10 @@ class PinnedRing {
     janus_status put(void* dst, const void* src, size_t bytes, hipStream_t stream) {
         std::lock_guard<std::mutex> lock(mu_);
         if (!base_) {
-            if (hipHostMalloc(reinterpret_cast<void**>(&base_), kCapacity, hipHostMallocDefault) != hipSuccess) {
+            const hipError_t e = hipHostMalloc(reinterpret_cast<void**>(&base_), kCapacity, hipHostMallocDefault);
+            if (e != hipSuccess) {
                 base_ = nullptr;
-                return JANUS_ERR_DEVICE;
+                return device_error(e, "hipHostMalloc", __FILE__, __LINE__);
             }
         }
         const size_t need = (bytes + 255) & ~size_t(255);
@@ -32,7 +45,7 @@ class PinnedRing {
         for (auto it = inflight_.begin(); it != inflight_.end();) {
             const bool overlap = it->off < head_ + need && head_ < it->off + it->len;
             if (overlap) {
-                if (hipEventSynchronize(it->ev) != hipSuccess) return JANUS_ERR_DEVICE;
+                JANUS_HIP(hipEventSynchronize(it->ev));
                 free_events_.push_back(it->ev);
                 it = inflight_.erase(it);
             } else {
@@ -40,16 +53,15 @@ class PinnedRing {
             }
         }
         std::memcpy(base_ + head_, src, bytes);
-        if (hipMemcpyAsync(dst, base_ + head_, bytes, hipMemcpyHostToDevice, stream) != hipSuccess)
-            return JANUS_ERR_DEVICE;
+        JANUS_HIP(hipMemcpyAsync(dst, base_ + head_, bytes, hipMemcpyHostToDevice, stream));
         hipEvent_t ev;
         if (!free_events_.empty()) {
             ev = free_events_.back();
             free_events_.pop_back();
-        } else if (hipEventCreateWithFlags(&ev, hipEventDisableTiming) != hipSuccess) {
-            return JANUS_ERR_DEVICE;
+        } else {
+            JANUS_HIP(hipEventCreateWithFlags(&ev, hipEventDisableTiming));
         }
-        if (hipEventRecord(ev, stream) != hipSuccess) return JANUS_ERR_DEVICE;
+        JANUS_HIP(hipEventRecord(ev, stream));
         inflight_.push_back({head_, need, ev});
         // retire completed copies so the list stays short
         while (!inflight_.empty() && hipEventQuery(inflight_.front().ev) == hipSuccess) {
@@ -208,5 +220,7 @@ extern "C" const char* janus_status_string(janus_status s) {
     }
     return "unknown status";
 }
+
+extern "C" const char* janus_last_error(void) { return janus::g_last_error; }
 
 extern "C" const char* janus_version(void) { return "janus-mi355x 0.1.0 (gfx950)"; }

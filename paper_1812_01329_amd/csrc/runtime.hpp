@@ -74,9 +74,14 @@ class TraceScope {
     hipStream_t stream_ = nullptr;
 };
 
-#define JANUS_HIP(call)                                        \
-    do {                                                       \
-        if ((call) != hipSuccess) return JANUS_ERR_DEVICE;     \
+// Records which HIP call failed, with its error, for janus_last_error on
+// this thread, and returns JANUS_ERR_DEVICE.
+janus_status device_error(hipError_t e, const char* what, const char* file, int line);
+
+#define JANUS_HIP(call)                                                                 \
+    do {                                                                                \
+        const hipError_t janus_e_ = (call);                                             \
+        if (janus_e_ != hipSuccess) return ::janus::device_error(janus_e_, #call, __FILE__, __LINE__); \
     } while (0)
 
 #define JANUS_LAUNCH_CHECK() JANUS_HIP(hipGetLastError())

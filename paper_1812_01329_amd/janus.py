@@ -30,14 +30,15 @@ EXPORTS = [
     "janus_treelstm_workspace_bytes", "janus_tree_schedule_build", "janus_treelstm_fwd",
     "janus_treelstm_bwd", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
     "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
-    "janus_trace_end", "janus_status_string", "janus_version",
+    "janus_trace_end", "janus_status_string", "janus_version", "janus_last_error",
 ]
 
 
 class JanusError(RuntimeError):
-    def __init__(self, status: int, where: str):
+    def __init__(self, status: int, where: str, detail: str = ""):
         self.status = status
-        super().__init__(f"{where}: {status_string(status)} (status {status})")
+        self.detail = detail
+        super().__init__(f"{where}: {status_string(status)} (status {status})" + (f": {detail}" if detail else ""))
 
 
 class LstmDesc(C.Structure):
@@ -65,7 +66,8 @@ class TraceStat(C.Structure):
 
 
 class LstmReport(C.Structure):
-    _fields_ = [("timed_out", C.c_int32), ("bwd_groups", C.c_int32), ("bwd_local_groups", C.c_int32)]
+    _fields_ = [("timed_out", C.c_int32), ("bwd_groups", C.c_int32), ("bwd_local_groups", C.c_int32),
+                ("fwd_groups", C.c_int32), ("fwd_local_groups", C.c_int32)]
 
 
 class MseDesc(C.Structure):
@@ -81,12 +83,18 @@ def lib():
     if _lib is None:
         if not os.path.exists(LIB_PATH):
             raise RuntimeError(f"{LIB_PATH} is missing: build it with `python -m paper_1812_01329_amd.build`")
+        # torch brings its own HIP runtime.  Loaded first, it is the one the
+        # library binds to; loaded after the library, a second runtime would
+        # come up beside the system one, and the library's launches would fail
+        # (hipErrorNoDevice) on buffers torch allocated.
+        import torch  # noqa: F401
         L = C.CDLL(LIB_PATH)
         vp, i32, i64, sz = C.c_void_p, C.c_int32, C.c_int64, C.c_size_t
         pi32 = C.POINTER(C.c_int32)
         L.janus_status_string.restype = C.c_char_p
         L.janus_status_string.argtypes = [C.c_int]
         L.janus_version.restype = C.c_char_p
+        L.janus_last_error.restype = C.c_char_p
         L.janus_lstm_workspace_bytes.restype = sz
         L.janus_lstm_workspace_bytes.argtypes = [C.POINTER(LstmDesc)]
         L.janus_lstm_seq_fwd.argtypes = [C.POINTER(LstmDesc), vp, pi32, vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -111,7 +119,7 @@ def lib():
         L.janus_trace_begin.argtypes = []
         L.janus_trace_end.argtypes = [C.POINTER(TraceStat), i32, C.POINTER(C.c_int32)]
         for name in EXPORTS:
-            if name not in ("janus_status_string", "janus_version") and "workspace_bytes" not in name:
+            if name not in ("janus_status_string", "janus_version", "janus_last_error") and "workspace_bytes" not in name:
                 getattr(L, name).restype = C.c_int
         _lib = L
     return _lib
@@ -153,9 +161,14 @@ def _i32p(a: Optional[np.ndarray]):
     return None if a is None else a.ctypes.data_as(C.POINTER(C.c_int32))
 
 
+def last_error() -> str:
+    """Which HIP call failed behind the last DEVICE status on this thread."""
+    return lib().janus_last_error().decode()
+
+
 def _check(st: int, where: str):
     if st != OK:
-        raise JanusError(st, where)
+        raise JanusError(st, where, last_error() if st == ERR_DEVICE else "")
 
 
 def _tree_c(left, right, word, root):
@@ -194,7 +207,8 @@ def janus_lstm_device_report(desc: LstmDesc, ws, stream=None) -> dict:
                                         _stream(stream))
     _check(st, "janus_lstm_device_report")
     return dict(timed_out=int(rep.timed_out), bwd_groups=int(rep.bwd_groups),
-                bwd_local_groups=int(rep.bwd_local_groups))
+                bwd_local_groups=int(rep.bwd_local_groups), fwd_groups=int(rep.fwd_groups),
+                fwd_local_groups=int(rep.fwd_local_groups))
 
 
 def janus_lstm_schedule(B: int, T: int, lengths):

@@ -237,3 +237,29 @@ def test_workspace_sizes_monotone():
     c = J.janus_lstm_workspace_bytes(2, 32, 64, 4, 32, J.F32)
     assert 0 < a < b < c
     assert J.janus_lstm_workspace_bytes(0, 32, 64, 4, 16, J.F32) == 0
+
+
+def test_one_hip_runtime_whatever_the_import_order():
+    """torch ships its own HIP runtime.  Using the binding before torch is
+    imported must still leave one runtime in the process (the library binds
+    to torch's); two runtimes made the library's launches fail with
+    hipErrorNoDevice on tensors torch allocated."""
+    import subprocess
+    import sys
+    code = (
+        "from paper_1812_01329_amd import janus as J\n"
+        "J.janus_trace_begin()\n"
+        "import torch\n"
+        "maps = [l.split()[-1] for l in open('/proc/self/maps') if 'amdhip64' in l and 'r-xp' in l]\n"
+        "print(len(set(maps)))\n"
+    )
+    root = os.path.dirname(os.path.dirname(os.path.abspath(__file__)))
+    out = subprocess.run([sys.executable, "-c", code], cwd=root, capture_output=True, text=True, timeout=600)
+    assert out.returncode == 0, out.stderr[-2000:]
+    assert out.stdout.strip().splitlines()[-1] == "1", out.stdout
+
+
+def test_last_error_text_is_readable():
+    """janus_last_error names the failing HIP call after a DEVICE status; it
+    is a plain (possibly empty) string otherwise."""
+    assert isinstance(J.last_error(), str)

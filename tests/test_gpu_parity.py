@@ -249,3 +249,42 @@ def test_backward_slices(slices, H, B, ragged, monkeypatch):
     if H == 512:   # 64 workgroups: whole groups fit on the XCDs of an even placement
         assert rep["bwd_local_groups"] > 0, rep
     compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
+
+
+@pytest.mark.parametrize("slices", ["1", "2", "4"])
+@pytest.mark.parametrize("H,B,ragged", [(512, 256, False), (200, 70, True), (256, 24, True)])
+def test_forward_slices(slices, H, B, ragged, monkeypatch):
+    """The persistent forward with the columns of Wh in 1, 2 and 4 slices
+    (JANUS_FWD_SLICES): unit groups of 16 or 32 exchange partial
+    pre-activations.  H = 512 places whole groups on the XCDs (partial sums
+    kept in the L2); H = 200 (padded to 208) has 26 or 28 workgroups, so some
+    groups straddle two XCDs and use per-step slots; B = 24 splits each
+    slice's k-groups over 8 waves, some of which get none."""
+    import torch
+    from paper_1812_01329_amd import janus as J
+    from paper_1812_01329_amd.train_step import make_step
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    monkeypatch.setenv("JANUS_FWD_SLICES", slices)
+    rng = np.random.default_rng(37)
+    lens = rng.integers(0, 11, B) if ragged else None
+    w = _lstm("mse", "bf16", L=2, I=64, H=H, B=B, T=10, lengths=lens, seed=37, h0=True, P=40)
+    print(f"[fwd-slices] H={H} B={B} NS={slices}", flush=True)
+    step = make_step(w)
+    J.janus_trace_begin()
+    J.janus_lstm_seq_fwd(step.desc, step.x, step.lengths, step.Wx, step.Wh, step.b, step.h0, step.c0,
+                         step.y, step.hT, step.cT, step.ws)
+    labels = {r["label"] for r in J.janus_trace_end()}
+    assert "lstm_fwd_persistent" in labels, labels
+    rep = J.janus_lstm_device_report(step.desc, step.ws)
+    print(f"[fwd-slices] report {rep}", flush=True)
+    ns = int(slices)
+    assert rep["timed_out"] == 0
+    hp = (H + 15) // 16 * 16   # H padded to 16
+    assert rep["fwd_groups"] == (0 if ns == 1 else 2 * ((hp + 8 * ns - 1) // (8 * ns)))   # two layers
+    assert 0 <= rep["fwd_local_groups"] <= rep["fwd_groups"]
+    if H == 512 and ns > 1:   # 64 workgroups: whole groups fit on the XCDs of an even placement
+        assert rep["fwd_local_groups"] > 0, rep
+    step.run()
+    g = step.results()
+    assert J.janus_lstm_device_report(step.desc, step.ws)["timed_out"] == 0
+    compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
