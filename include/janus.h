@@ -338,6 +338,51 @@ janus_status janus_trace_begin(void);
 janus_status janus_trace_end(janus_trace_stat* out, int32_t max_out, int32_t* n_out);
 
 /* ------------------------------------------------------------------------ */
+/* Parameter update                                                         */
+/* ------------------------------------------------------------------------ */
+/*
+ * SGD with the step scaled down by the global L2 norm of the gradients.  The
+ * paper inserts the parameter update into the generated graph after the
+ * gradients (Section 3.1) and names no optimizer; the rule here is
+ *   norm = sqrt(sum over all tensors and entries of g^2),
+ *   s    = min(1, max_norm / (norm + 1e-6)), or 1 when max_norm <= 0 or +inf,
+ *   p   <- p - lr * s * g            (computed in float32, stored as dtype).
+ * State changes are all-or-nothing (Section 4.2.3): when the norm is not
+ * finite (a NaN or infinite gradient) no parameter is written.  The norm is
+ * summed in float64 in a fixed order, so repeated calls give the same result.
+ */
+typedef struct {
+    int32_t n;            /* parameter tensors, >= 1 */
+    janus_dtype dtype;    /* of the parameters, F32 or BF16 (gradients are float32) */
+    float lr;             /* learning rate, finite */
+    float max_norm;       /* clipping threshold; <= 0 or +inf turns clipping off; not NaN */
+} janus_sgd_desc;
+
+/* Workspace bytes for janus_sgd_clip_update with this descriptor (0 for a
+ * bad descriptor). */
+size_t janus_sgd_workspace_bytes(const janus_sgd_desc* d);
+
+/*
+ *  params[i] host array of n device pointers to the parameters (dtype),
+ *            updated in place; grads[i] host array of n device pointers to
+ *            their float32 gradients; sizes[i] host array of n element
+ *            counts (>= 0; a tensor of 0 elements may have NULL pointers).
+ *            Tensors are flat and contiguous; parameters and gradients must
+ *            not overlap.
+ *  stats     device float32[2] or NULL: [0] the norm before clipping, [1]
+ *            the scale s applied (0 when the update was skipped).
+ *  ws        workspace (see conventions), at least
+ *            janus_sgd_workspace_bytes(d) bytes.
+ * Errors: NULL d/params/grads/sizes, n < 1, non-finite lr, NaN max_norm, a
+ * negative size, a NULL pointer of a non-empty tensor, or a pointer not
+ * aligned to its element -> INVALID_ARG; dtype not F32/BF16 -> UNSUPPORTED;
+ * ws missing, too small or misaligned -> WORKSPACE.
+ */
+janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* const* params,
+                                   const float* const* grads, const int64_t* sizes,
+                                   float* stats, void* ws, size_t ws_bytes, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Misc                                                                     */
 /* ------------------------------------------------------------------------ */
 const char* janus_status_string(janus_status s);

@@ -31,6 +31,7 @@ EXPORTS = [
     "janus_treelstm_bwd", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
     "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
     "janus_trace_end", "janus_status_string", "janus_version", "janus_last_error",
+    "janus_sgd_workspace_bytes", "janus_sgd_clip_update",
 ]
 
 
@@ -74,6 +75,10 @@ class MseDesc(C.Structure):
     _fields_ = [("rows", C.c_int32), ("H", C.c_int32), ("P", C.c_int32), ("dtype", C.c_int)]
 
 
+class SgdDesc(C.Structure):
+    _fields_ = [("n", C.c_int32), ("dtype", C.c_int), ("lr", C.c_float), ("max_norm", C.c_float)]
+
+
 _lib = None
 
 
@@ -112,6 +117,10 @@ def lib():
         L.janus_xent_workspace_bytes.argtypes = [C.POINTER(XentDesc), C.c_int]
         L.janus_embed_softmax_xent.argtypes = [C.POINTER(XentDesc), C.c_int, pi32, vp, vp, vp, vp, vp, vp, vp, vp,
                                                vp, sz, vp]
+        L.janus_sgd_workspace_bytes.restype = sz
+        L.janus_sgd_workspace_bytes.argtypes = [C.POINTER(SgdDesc)]
+        L.janus_sgd_clip_update.argtypes = [C.POINTER(SgdDesc), C.POINTER(vp), C.POINTER(vp),
+                                            C.POINTER(C.c_int64), vp, vp, sz, vp]
         L.janus_mse_workspace_bytes.restype = sz
         L.janus_mse_workspace_bytes.argtypes = [C.POINTER(MseDesc)]
         L.janus_linear_mse.argtypes = [C.POINTER(MseDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -284,6 +293,22 @@ def janus_linear_mse(desc: MseDesc, h, W, b, target, dh, dW, db, loss, ws, strea
 def janus_loss_reduce(kind, h, n, loss, dh, stream=None):
     st = lib().janus_loss_reduce(kind, _p(h), n, _p(loss), _p(dh), _stream(stream))
     _check(st, "janus_loss_reduce")
+
+
+# ---------------------------------------------------------------- update
+def sgd_workspace_bytes(desc: SgdDesc) -> int:
+    return int(lib().janus_sgd_workspace_bytes(C.byref(desc)))
+
+
+def janus_sgd_clip_update(desc: SgdDesc, params, grads, stats=None, ws=None, stream=None):
+    """SGD step with global-norm clipping on lists of flat device tensors
+    (parameters updated in place; float32 gradients)."""
+    n = len(params)
+    S = (C.c_int64 * n)(*[int(t.numel()) for t in params])
+    wsb = 0 if ws is None else ws.numel() * ws.element_size()
+    st = lib().janus_sgd_clip_update(C.byref(desc), _ptr_array(params), _ptr_array(grads), S, _p(stats), _p(ws),
+                                     wsb, _stream(stream))
+    _check(st, "janus_sgd_clip_update")
 
 
 # ---------------------------------------------------------------- tracing

@@ -263,3 +263,64 @@ def test_last_error_text_is_readable():
     """janus_last_error names the failing HIP call after a DEVICE status; it
     is a plain (possibly empty) string otherwise."""
     assert isinstance(J.last_error(), str)
+
+
+def _sgd_call(desc, params, grads, sizes, ws, ws_bytes):
+    L = J.lib()
+    n = len(sizes)
+    P = (C.c_void_p * max(n, 1))(*params)
+    G = (C.c_void_p * max(n, 1))(*grads)
+    S = (C.c_int64 * max(n, 1))(*sizes)
+    return L.janus_sgd_clip_update(None if desc is None else C.byref(desc), P, G, S, None, ws, ws_bytes, None)
+
+
+def test_sgd_workspace_bytes():
+    d = J.SgdDesc(1, J.F32, 0.1, 1.0)
+    one = J.sgd_workspace_bytes(d)
+    assert one > 0 and one % 256 == 0
+    d.n = 65   # a second table of tensors needs its own block sums
+    assert J.sgd_workspace_bytes(d) > one
+    d.n = 0
+    assert J.sgd_workspace_bytes(d) == 0
+
+
+@pytest.mark.parametrize("case,status", [
+    ("null_desc", J.ERR_INVALID_ARG), ("n0", J.ERR_INVALID_ARG), ("dtype", J.ERR_UNSUPPORTED),
+    ("lr_nan", J.ERR_INVALID_ARG), ("lr_inf", J.ERR_INVALID_ARG), ("max_norm_nan", J.ERR_INVALID_ARG),
+    ("neg_size", J.ERR_INVALID_ARG), ("null_ptr", J.ERR_INVALID_ARG), ("grad_unaligned", J.ERR_INVALID_ARG),
+    ("param_unaligned", J.ERR_INVALID_ARG), ("ws_null", J.ERR_WORKSPACE), ("ws_small", J.ERR_WORKSPACE),
+    ("ws_unaligned", J.ERR_WORKSPACE)])
+def test_sgd_rejects_bad_arguments(case, status):
+    """Every error is found before the first device operation (fake device
+    pointers, never dereferenced)."""
+    d = J.SgdDesc(2, J.BF16, 0.1, 1.0)
+    params, grads, sizes = [0x100000, 0x200000], [0x300000, 0x400000], [10, 0]
+    ws = 0x500000
+    wsb = J.sgd_workspace_bytes(d)
+    if case == "null_desc":
+        d = None
+    elif case == "n0":
+        d.n = 0
+    elif case == "dtype":
+        d.dtype = 7
+    elif case == "lr_nan":
+        d.lr = float("nan")
+    elif case == "lr_inf":
+        d.lr = float("inf")
+    elif case == "max_norm_nan":
+        d.max_norm = float("nan")
+    elif case == "neg_size":
+        sizes[1] = -1
+    elif case == "null_ptr":
+        grads[0] = 0
+    elif case == "grad_unaligned":
+        grads[0] += 2
+    elif case == "param_unaligned":
+        params[0] += 1
+    elif case == "ws_null":
+        ws = 0
+    elif case == "ws_small":
+        wsb -= 256
+    elif case == "ws_unaligned":
+        ws += 64
+    assert _sgd_call(d, params, grads, sizes, ws, wsb) == status
