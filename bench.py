@@ -114,6 +114,8 @@ def main():
     ap.add_argument("--cpu-rows", type=int, default=4, help="sequences in the oracle sample")
     ap.add_argument("--no-cpu-baseline", action="store_true")
     ap.add_argument("--no-trace", action="store_true")
+    ap.add_argument("--with-update", action="store_true",
+                    help="end every step with the SGD update with global-norm clipping (lr 0.1, max norm 5)")
     ap.add_argument("--copy-calibration", action="store_true",
                     help="only copy a 1 GiB buffer three times (reference for HBM byte counters) and exit")
     args = ap.parse_args()
@@ -146,7 +148,7 @@ def main():
     WORKLOADS_UNIT = spec["unit"]
     w = wl.FULL[args.workload]()
     print(f"[bench] workload {args.workload}: {spec['desc']}", file=sys.stderr, flush=True)
-    step = make_step(w)
+    step = make_step(w, update=(0.1, 5.0) if args.with_update else None)
     units = w.trees.num_trees if hasattr(w, "trees") else w.B
 
     for _ in range(args.warmup):
@@ -183,7 +185,7 @@ def main():
                                 "avg_us": round(1e3 * s["total_ms"] / s["launches"], 3),
                                 "tflops": round(s["flops"] / (s["total_ms"] * 1e-3) / 1e12, 2) if s["flops"] else None,
                                 "gbs": round(s["bytes"] / (s["total_ms"] * 1e-3) / 1e9, 1)}
-                   for s in stats[:8]}
+                   for s in stats if s in stats[:8] or s["label"].startswith("sgd_")}
         top = stats[0]
         avg_s = top["total_ms"] / top["launches"] * 1e-3
         bf16 = top["label"].endswith("bf16") or w.dtype == wl.BF16
@@ -236,7 +238,8 @@ def main():
         "vs_baseline": None,
         "dtype": "bf16" if getattr(w, "dtype", "f32") == wl.BF16 else "f32",
         "data": "synthetic",
-        "config": {"workload": f"{args.workload}: {spec['desc']}", "units_per_step": units},
+        "config": {"workload": f"{args.workload}: {spec['desc']}", "units_per_step": units,
+                   "update": "sgd, global-norm clip 5.0" if args.with_update else None},
         "roofline": roofline,
         "cpu_baseline": cpu,
     }

@@ -8,7 +8,7 @@ reverse).  All arithmetic happens inside libjanus.so.
 """
 from __future__ import annotations
 
-from typing import Dict, Optional
+from typing import Dict, Optional, Sequence, Tuple
 
 import numpy as np
 import torch
@@ -34,13 +34,34 @@ def _f64(t: torch.Tensor) -> np.ndarray:
     return t.detach().float().cpu().numpy().astype(np.float64)
 
 
+class SgdUpdate:
+    """The parameter update that ends a training step (janus_sgd_clip_update):
+    every parameter tensor with its float32 gradient, one call."""
+
+    def __init__(self, params: Sequence[torch.Tensor], grads: Sequence[torch.Tensor], lr: float, max_norm: float):
+        dts = {p.dtype for p in params}
+        assert len(dts) == 1, "one parameter dtype per update"
+        self.params = [p.view(-1) for p in params]
+        self.grads = [g.view(-1) for g in grads]
+        dt = J.BF16 if params[0].dtype == torch.bfloat16 else J.F32
+        self.desc = J.SgdDesc(len(self.params), dt, lr, max_norm)
+        dev = params[0].device
+        self.ws = torch.empty(J.sgd_workspace_bytes(self.desc), dtype=torch.uint8, device=dev)
+        self.stats = torch.zeros(2, dtype=torch.float32, device=dev)   # [norm before clipping, scale]
+
+    def apply(self):
+        J.janus_sgd_clip_update(self.desc, self.params, self.grads, stats=self.stats, ws=self.ws)
+
+
 class LSTMStep:
     """Device state and call sequence of an LSTM training step.
 
     ``skip_dx``: do not form the gradient of the (non-embedding) input x,
-    as in the regression workload where x is data."""
+    as in the regression workload where x is data.  ``update`` = (lr,
+    max_norm) appends the parameter update to the step."""
 
-    def __init__(self, w: wl.LSTMWorkload, device="cuda", skip_dx: Optional[bool] = None):
+    def __init__(self, w: wl.LSTMWorkload, device="cuda", skip_dx: Optional[bool] = None,
+                 update: Optional[Tuple[float, float]] = None):
         self.w = w
         self.device = device
         tdt = _tdt(w.dtype)
@@ -101,6 +122,25 @@ class LSTMStep:
         if w.head in ("sumsq", "mean_final"):
             self.dhT = zeros(L, B, H)
             self.dy = None
+        self.update = None
+        if update is not None:
+            P, G = self.parameters()
+            self.update = SgdUpdate(P, G, *update)
+
+    def parameters(self):
+        """(parameters, their gradients) in a fixed order: per layer Wx, Wh,
+        b, then the head's table and bias, then the embedding."""
+        P, G = [], []
+        for l in range(self.w.L):
+            P += [self.Wx[l], self.Wh[l], self.b[l]]
+            G += [self.dWx[l], self.dWh[l], self.db[l]]
+        if self.w.head in ("xent", "mse"):
+            P += [self.Wout, self.bout]
+            G += [self.dWout, self.dbout]
+        if self.w.head == "xent":
+            P.append(self.E)
+            G.append(self.dE)
+        return P, G
 
     def run(self):
         w = self.w
@@ -127,6 +167,8 @@ class LSTMStep:
         if w.head == "xent":
             J.janus_embed_softmax_xent(self.edesc, J.EMBED_BWD, self.ids_host, self.ids, inp=self.dx,
                                        dtable=self.dE)
+        if self.update is not None:
+            self.update.apply()
 
     def results(self) -> Dict[str, object]:
         torch.cuda.synchronize()
@@ -146,7 +188,7 @@ class LSTMStep:
 class TreeStep:
     """Device state and call sequence of a TreeLSTM training step."""
 
-    def __init__(self, w: wl.TreeWorkload, device="cuda"):
+    def __init__(self, w: wl.TreeWorkload, device="cuda", update: Optional[Tuple[float, float]] = None):
         self.w = w
         self.device = device
         f = torch.float32
@@ -174,6 +216,10 @@ class TreeStep:
         self.xdesc = J.XentDesc(w.C, w.H, K, J.F32)
         self.xws = torch.empty(J.janus_xent_workspace_bytes(w.C, w.H, K, J.F32, J.XENT_FWD_BWD),
                                dtype=torch.uint8, device=device)
+        self.update = None
+        if update is not None:
+            self.update = SgdUpdate([self.emb, self.W, self.U, self.b, self.Ws, self.bs],
+                                    [self.demb, self.dW, self.dU, self.db, self.dWs, self.dbs], *update)
 
     def run(self):
         w = self.w
@@ -183,6 +229,8 @@ class TreeStep:
                                    dbias=self.dbs, loss=self.loss, ws=self.xws)
         J.janus_treelstm_bwd(self.desc, w.trees, self.emb, self.W, self.U, self.ws, self.dh_root, self.demb,
                              self.dW, self.dU, self.db)
+        if self.update is not None:
+            self.update.apply()
 
     def results(self) -> Dict[str, object]:
         torch.cuda.synchronize()
@@ -191,5 +239,9 @@ class TreeStep:
                     dWs=_f64(self.dWs), dbs=_f64(self.dbs))
 
 
-def make_step(w, device="cuda"):
-    return TreeStep(w, device) if isinstance(w, wl.TreeWorkload) else LSTMStep(w, device)
+def make_step(w, device="cuda", update: Optional[Tuple[float, float]] = None):
+    """The training step of a workload; ``update`` = (lr, max_norm) appends
+    the SGD update with global-norm clipping."""
+    if isinstance(w, wl.TreeWorkload):
+        return TreeStep(w, device, update=update)
+    return LSTMStep(w, device, update=update)

@@ -145,3 +145,39 @@ def test_full_size_parameter_set():
     assert s < 1.0   # the clipping is active at this scale
     assert stats[0] == pytest.approx(norm, rel=2e-7)
     _check(new, ref, P, G, "bf16", lr, s)
+
+
+@pytest.mark.parametrize("max_norm", [1e-3, 0.0])
+def test_training_step_with_update(max_norm):
+    """One float32 LSTM language-model step (embedding, 2 layers, softmax
+    cross-entropy) followed by the update, against the oracle's gradients and
+    the oracle's update of the same initial parameters.  The device step's
+    gradients match the oracle's to the step tolerance, so the parameter
+    change is compared relative to its own size."""
+    import torch
+    from oracle import steps as osteps
+    from paper_1812_01329_amd.train_step import make_step
+    from tests.test_gpu_parity import _lstm
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    w = _lstm("xent", "f32", L=2, I=16, H=32, B=8, T=6, seed=48, V=50)
+    lr = 0.5
+    print(f"[sgd-step] {w.name} max_norm={max_norm}", flush=True)
+    step = make_step(w, update=(lr, max_norm))
+    P0 = [_host(p) for p in step.parameters()[0]]
+    step.run()
+    torch.cuda.synchronize()
+    P1 = [_host(p) for p in step.parameters()[0]]
+    r = osteps.lstm_step(w)
+    G = []
+    for l in range(w.L):
+        G += [r["dWx"][l], r["dWh"][l], r["db"][l]]
+    G += [r["dWout"], r["dbout"], r["dE"]]
+    ref, norm, s, applied = osgd.sgd_clip_update(P0, G, lr, max_norm)
+    stats = _host(step.update.stats)
+    assert applied
+    assert stats[0] == pytest.approx(norm, rel=1e-3)
+    if max_norm > 0:
+        assert s < 1.0
+    d_gpu = np.concatenate([(b - a).ravel() for a, b in zip(P0, P1)])
+    d_ref = np.concatenate([(b - a).ravel() for a, b in zip(P0, ref)])
+    assert np.linalg.norm(d_gpu - d_ref) <= 1e-3 * np.linalg.norm(d_ref)
