@@ -155,3 +155,23 @@ def stack_backward(caches, ys, Wx, Wh, dy=None, dhT=None, dcT=None):
         dh0[layer], dc0[layer] = dh, dc
         g = dx
     return g, np.stack(dh0), np.stack(dc0), dWx, dWh, db
+
+
+def carry_state(hT, cT, B_next):
+    """Initial state of the next batch from the final state of the previous
+    one: the program keeps the recurrent state in ``self.state`` between
+    calls (Figure 1).  Rows both batches have continue; rows only the next
+    batch has start from 0; rows past the next batch end (a smaller last
+    batch, the shape the paper relaxes when its specialized value changes).
+    ``hT`` is None for the first batch (all zeros)."""
+    if hT is None:
+        return None, None
+    hT = np.asarray(hT, dtype=np.float64)
+    cT = np.asarray(cT, dtype=np.float64)
+    L, B_prev, H = hT.shape
+    h0 = np.zeros((L, B_next, H))
+    c0 = np.zeros((L, B_next, H))
+    n = min(B_prev, B_next)
+    h0[:, :n] = hT[:, :n]
+    c0[:, :n] = cT[:, :n]
+    return h0, c0
