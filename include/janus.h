@@ -125,6 +125,27 @@ janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void* x,
                                 void* stream);
 
 /*
+ * Carries the recurrent state of one batch into the next: the program of
+ * Figure 1 keeps the state in self.state between calls, and the stored
+ * state changes only after a whole step has run (deferred state update,
+ * Section 4.2.3), so this call belongs after the step's backward call.
+ *  d        descriptor of the NEXT batch (L, H, B = B_next; I, T unused but
+ *           validated as for the other calls).
+ *  B_prev   rows of the previous batch, >= 0 (0: no previous batch).
+ *  hT, cT   [L, B_prev, H] float32: final state of the previous batch (may be
+ *           NULL when B_prev is 0).
+ *  h0, c0   [L, B_next, H] float32, written: row r of layer l continues
+ *           (= hT, cT) for r < B_prev, starts from 0 otherwise; rows
+ *           r >= B_next of the previous batch end (a smaller last batch).
+ * Errors: bad d -> as janus_lstm_seq_fwd; B_prev < 0, NULL h0/c0, NULL
+ * hT/cT with B_prev > 0, or any of the four buffers overlapping another ->
+ * INVALID_ARG.
+ */
+janus_status janus_lstm_state_carry(const janus_lstm_desc* d, int32_t B_prev,
+                                    const float* hT, const float* cT,
+                                    float* h0, float* c0, void* stream);
+
+/*
  * Report of the last janus_lstm_seq_fwd or janus_lstm_seq_bwd call made with
  * this workspace (same d).  The persistent recurrence kernels separate their
  * time steps with device-wide barriers whose waits are bounded; when a wait

@@ -1326,6 +1326,49 @@ extern "C" janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void*
     return lstm_bwd_impl<float, StepF32>(*d, s, w, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
 }
 
+namespace janus {
+namespace {
+// h0[l, r, :] = hT[l, r, :] for r < Bp, else 0 (the same for c); i runs over
+// the h half, then the c half
+__global__ void state_carry_kernel(int L, int Bp, int Bn, int H, const float* hT, const float* cT, float* h0,
+                                   float* c0) {
+    const int64_t n = int64_t(L) * Bn * H;
+    for (int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x; i < 2 * n; i += int64_t(gridDim.x) * blockDim.x) {
+        const bool cpart = i >= n;
+        const int64_t j = cpart ? i - n : i;
+        const int64_t u = j % H, r = (j / H) % Bn, l = j / (int64_t(H) * Bn);
+        const float* src = cpart ? cT : hT;
+        float* dst = cpart ? c0 : h0;
+        dst[j] = r < Bp ? src[(l * Bp + r) * H + u] : 0.f;
+    }
+}
+
+bool overlaps(const void* a, size_t na, const void* b, size_t nb) {
+    const uintptr_t x = reinterpret_cast<uintptr_t>(a), y = reinterpret_cast<uintptr_t>(b);
+    return na > 0 && nb > 0 && x < y + nb && y < x + na;
+}
+}  // namespace
+}  // namespace janus
+
+extern "C" janus_status janus_lstm_state_carry(const janus_lstm_desc* d, int32_t B_prev, const float* hT,
+                                               const float* cT, float* h0, float* c0, void* stream) {
+    janus_status e = check_desc(d);
+    if (e != JANUS_OK) return e;
+    if (B_prev < 0 || !h0 || !c0 || (B_prev > 0 && (!hT || !cT))) return JANUS_ERR_INVALID_ARG;
+    const size_t nn = size_t(d->L) * d->B * d->H * sizeof(float), np = size_t(d->L) * B_prev * d->H * sizeof(float);
+    if (overlaps(h0, nn, c0, nn) || overlaps(h0, nn, hT, np) || overlaps(h0, nn, cT, np) || overlaps(c0, nn, hT, np) ||
+        overlaps(c0, nn, cT, np))
+        return JANUS_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    const int64_t n = 2 * int64_t(d->L) * d->B * d->H;
+    TraceScope trace("state_carry", 0.0, 4.0 * double(n) * 2.0, st);
+    const unsigned blocks = unsigned(std::min<int64_t>((n + 255) / 256, 4096));
+    hipLaunchKernelGGL(state_carry_kernel, dim3(blocks), dim3(256), 0, st, d->L, int(B_prev), d->B, d->H, hT, cT, h0,
+                       c0);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
 extern "C" janus_status janus_lstm_device_report(const janus_lstm_desc* d, const void* ws, size_t ws_bytes,
                                                  janus_lstm_report* out, void* stream) {
     janus_status e = check_desc(d);

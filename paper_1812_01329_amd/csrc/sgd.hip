@@ -82,6 +82,7 @@ __global__ __launch_bounds__(kSgdThreads) void sgd_sumsq_kernel(SgdTable t, doub
         }
         const int64_t n4 = (len - head) / 4;
         const float4* g4 = reinterpret_cast<const float4*>(g + head);
+#pragma unroll 4
         for (int64_t k = tid; k < n4; k += kSgdThreads) {
             const float4 v = g4[k];
             acc += double(v.x) * v.x + double(v.y) * v.y + double(v.z) * v.z + double(v.w) * v.w;
@@ -139,6 +140,7 @@ __global__ __launch_bounds__(kSgdThreads) void sgd_update_kernel(SgdTable t, con
         if (!vec) head = 0;
         if (tid < head) p[tid] = from_f<T>(to_f<T>(p[tid]) - ls * g[tid]);
         const float4* g4 = reinterpret_cast<const float4*>(g + head);
+#pragma unroll 4
         for (int64_t k = tid; k < n4; k += kSgdThreads) {
             const float4 v = g4[k];
             T* q = p + head + 4 * k;

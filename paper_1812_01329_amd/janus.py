@@ -31,7 +31,7 @@ EXPORTS = [
     "janus_treelstm_bwd", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
     "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
     "janus_trace_end", "janus_status_string", "janus_version", "janus_last_error",
-    "janus_sgd_workspace_bytes", "janus_sgd_clip_update",
+    "janus_sgd_workspace_bytes", "janus_sgd_clip_update", "janus_lstm_state_carry",
 ]
 
 
@@ -117,6 +117,7 @@ def lib():
         L.janus_xent_workspace_bytes.argtypes = [C.POINTER(XentDesc), C.c_int]
         L.janus_embed_softmax_xent.argtypes = [C.POINTER(XentDesc), C.c_int, pi32, vp, vp, vp, vp, vp, vp, vp, vp,
                                                vp, sz, vp]
+        L.janus_lstm_state_carry.argtypes = [C.POINTER(LstmDesc), i32, vp, vp, vp, vp, vp]
         L.janus_sgd_workspace_bytes.restype = sz
         L.janus_sgd_workspace_bytes.argtypes = [C.POINTER(SgdDesc)]
         L.janus_sgd_clip_update.argtypes = [C.POINTER(SgdDesc), C.POINTER(vp), C.POINTER(vp),
@@ -293,6 +294,13 @@ def janus_linear_mse(desc: MseDesc, h, W, b, target, dh, dW, db, loss, ws, strea
 def janus_loss_reduce(kind, h, n, loss, dh, stream=None):
     st = lib().janus_loss_reduce(kind, _p(h), n, _p(loss), _p(dh), _stream(stream))
     _check(st, "janus_loss_reduce")
+
+
+def janus_lstm_state_carry(desc: LstmDesc, B_prev: int, hT, cT, h0, c0, stream=None):
+    """Initial state of the next batch (desc.B rows) from the final state of
+    the previous one (B_prev rows)."""
+    st = lib().janus_lstm_state_carry(C.byref(desc), int(B_prev), _p(hT), _p(cT), _p(h0), _p(c0), _stream(stream))
+    _check(st, "janus_lstm_state_carry")
 
 
 # ---------------------------------------------------------------- update

@@ -127,6 +127,15 @@ class LSTMStep:
             P, G = self.parameters()
             self.update = SgdUpdate(P, G, *update)
 
+    def carry_from(self, prev: "LSTMStep"):
+        """Seeds this step's initial state with the final state of the step
+        that ran before it (run after that step's backward call)."""
+        L, B, H = self.w.L, self.w.B, self.w.H
+        if self.h0 is None:
+            self.h0 = torch.zeros(L, B, H, dtype=torch.float32, device=self.device)
+            self.c0 = torch.zeros(L, B, H, dtype=torch.float32, device=self.device)
+        J.janus_lstm_state_carry(self.desc, prev.w.B, prev.hT, prev.cT, self.h0, self.c0)
+
     def parameters(self):
         """(parameters, their gradients) in a fixed order: per layer Wx, Wh,
         b, then the head's table and bias, then the embedding."""

@@ -324,3 +324,22 @@ def test_sgd_rejects_bad_arguments(case, status):
     elif case == "ws_unaligned":
         ws += 64
     assert _sgd_call(d, params, grads, sizes, ws, wsb) == status
+
+
+@pytest.mark.parametrize("case", ["neg", "null_h0", "null_hT", "overlap"])
+def test_state_carry_rejects_bad_arguments(case):
+    """Checked before any device operation (fake pointers, never used)."""
+    L = J.lib()
+    d = J.LstmDesc(2, 8, 16, 4, 3, J.F32)
+    n = 2 * 4 * 16 * 4
+    Bp, hT, cT, h0, c0 = 4, 0x100000, 0x200000, 0x300000, 0x400000
+    if case == "neg":
+        Bp = -1
+    elif case == "null_h0":
+        h0 = 0
+    elif case == "null_hT":
+        hT = 0
+    elif case == "overlap":
+        c0 = h0 + n // 2
+    st = L.janus_lstm_state_carry(C.byref(d), Bp, hT, cT, h0, c0, None)
+    assert st == J.ERR_INVALID_ARG
