@@ -291,6 +291,43 @@ def sst_treelstm(n_trees=25, E=300, H=150, V=20000, C=5, min_leaves=5, max_leave
     return TreeWorkload("treelstm", E, H, V, C, trees, labels, emb, W, U, b, Ws, bs)
 
 
+@dataclasses.dataclass
+class TreeRNNWorkload:
+    """Inputs of one binary TreeRNN training step (fp32): leaves take their
+    word vector as h (embedding width = H), internal nodes
+    h = tanh(W [h_L; h_R] + b)."""
+    name: str
+    H: int
+    V: int
+    C: int
+    trees: TreeBatch
+    labels: np.ndarray     # [num_trees] int32 in [0, C)
+    emb: np.ndarray        # [V, H]
+    W: np.ndarray          # [H, 2H]
+    b: np.ndarray          # [H]
+    Ws: np.ndarray         # [C, H]
+    bs: np.ndarray         # [C]
+    dtype: str = F32
+
+
+def sst_treernn(n_trees=25, H=300, V=20000, C=5, min_leaves=5, max_leaves=50, seed=None,
+                sizes=None) -> TreeRNNWorkload:
+    """Binary TreeRNN with 300-wide word vectors and hidden state, batch 25
+    random full binary trees over sentences of 5-50 leaves with Zipf(1.1)
+    leaf ids over a 20000 vocabulary (the trees of the TreeLSTM workload),
+    5-class softmax at the root with uniform labels, fp32, all parameters
+    U(-0.1, 0.1)."""
+    rp, _, rtree, rl = _streams(4, seed)
+    emb = uniform(rp, 0.1, (V, H))
+    W = uniform(rp, 0.1, (H, 2 * H))
+    b = uniform(rp, 0.1, (H,))
+    Ws = uniform(rp, 0.1, (C, H))
+    bs = uniform(rp, 0.1, (C,))
+    trees = make_trees(rtree, n_trees, min_leaves, max_leaves, V, sizes=sizes)
+    labels = rl.integers(0, C, size=trees.num_trees).astype(np.int32)
+    return TreeRNNWorkload("treernn", H, V, C, trees, labels, emb, W, b, Ws, bs)
+
+
 # Named full-size workloads, in the order of the five configurations.
 FULL: Dict[str, callable] = {
     "tiny": tiny_lstm,
@@ -298,4 +335,5 @@ FULL: Dict[str, callable] = {
     "varlen": varlen_lstm,
     "treelstm": sst_treelstm,
     "lm2048": lm2048_lstm,
+    "treernn": sst_treernn,
 }
