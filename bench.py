@@ -45,6 +45,8 @@ WORKLOADS = {
                           "5-class softmax at roots", unit="trees/s"),
     "tiny": dict(desc="1-layer LSTM, input 32, hidden 64, batch 4, length 16, fp32, sum of squares of final h",
                  unit="sequences/s"),
+    "treernn": dict(desc="binary TreeRNN, word vectors and hidden 300, 25 trees of 5-50 leaves, fp32, "
+                         "5-class softmax at roots", unit="trees/s"),
 }
 
 
@@ -76,6 +78,7 @@ def cpu_baseline(w, n_rows: int):
     """Time the oracle on the first n_rows sequences of the workload."""
     import numpy as np
     from oracle import steps as oracle_steps
+    from paper_1812_01329_amd import workloads as wl
     try:
         from threadpoolctl import threadpool_info
         info = threadpool_info()
@@ -85,7 +88,10 @@ def cpu_baseline(w, n_rows: int):
         cores, blas = len(os.sched_getaffinity(0)), "?"
     if hasattr(w, "trees"):
         t0 = time.perf_counter()
-        oracle_steps.tree_step(w)
+        if isinstance(w, wl.TreeRNNWorkload):
+            oracle_steps.treernn_step(w)
+        else:
+            oracle_steps.tree_step(w)
         dt = time.perf_counter() - t0
         n = w.trees.num_trees
         sample = f"all {n} trees of the batch, float64 numpy oracle, fwd+bwd"

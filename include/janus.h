@@ -259,6 +259,47 @@ janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const janus_tree_b
                                 void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Binary TreeRNN over a batch of trees                                     */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The paper's other TreeNN (TreeRNN on SST, Table 2), on the same frontier
+ * schedule and tree batches as the TreeLSTM.  Cell of node n:
+ *     h = emb[word[n]]                      (leaf: its word vector)
+ *     h = tanh(W [h_L; h_R] + b)            (internal node)
+ * The descriptor is the TreeLSTM's with E = H (the leaf h is the embedding).
+ */
+typedef janus_treelstm_desc janus_treernn_desc;
+
+/* Workspace bytes for a batch of at most max_nodes nodes and max_trees
+ * trees (0 for a bad descriptor, including E != H). */
+size_t janus_treernn_workspace_bytes(const janus_treernn_desc* d, int32_t max_nodes,
+                                     int32_t max_trees);
+
+/*
+ *  emb [V, H], W [H, 2H], b [H]: float32.
+ *  h_root [num_trees, H] float32: h of root[k].
+ * Errors: INVALID_ARG (as for the TreeLSTM, or E != H), TREE, TOKEN,
+ * WORKSPACE, UNSUPPORTED (only F32).
+ */
+janus_status janus_treernn_fwd(const janus_treernn_desc* d, const janus_tree_batch* t,
+                               const void* emb, const void* W, const void* b,
+                               void* h_root, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward of the call above (same d, t, W and workspace).
+ *  dh_root [num_trees, H] float32: gradient of h_root.
+ *  demb [V, H], dW [H, 2H], db [H]: float32, overwritten (rows of demb for
+ *          words not in the batch are 0; a leaf's gradient is its dh).
+ * Errors: as the forward; UNSUPPORTED when the batch has more than 16384
+ * leaves.
+ */
+janus_status janus_treernn_bwd(const janus_treernn_desc* d, const janus_tree_batch* t,
+                               const void* W, void* ws, size_t ws_bytes,
+                               const void* dh_root, float* demb, float* dW, float* db,
+                               void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Embedding and softmax cross-entropy                                      */
 /* ------------------------------------------------------------------------ */
 

@@ -388,6 +388,100 @@ janus_status prepare(const janus_treelstm_desc* d, const janus_tree_batch* t, vo
     return JANUS_OK;
 }
 
+
+// ------------------------------------------------------------------ TreeRNN
+// Binary TreeRNN on the same frontier schedule: a leaf's h is its word
+// vector (embedding width = H), an internal node h = tanh(W [h_L; h_R] + b).
+// Forward: the leaves copy their embedding rows into their parents' [h_L;
+// h_R] rows; each internal level is one contraction with W^T (bias in its
+// epilogue) and a pointwise tanh that saves h and sends it to the parent.
+// Backward, levels from the top down: da = dh (1 - h^2), then
+// [dh_L; dh_R] = da W to the two children; after the loop dW = da^T HLR and
+// db = column sums of da over the internal nodes, and the leaves' dh is the
+// gradient of their word vectors.
+struct TreeRnnWs {
+    TreeWs s;                    // schedule arrays (lword .. rootpos) only
+    float* A = nullptr;          // [N x H] pre-activations (forward), da (backward)
+    float* Hn = nullptr;         // [N x H] h of every node
+    float* HLR = nullptr;        // [N - M0 x 2H] children's h of internal nodes
+    float* dh = nullptr;         // [N x H]
+    float* Wt = nullptr;         // [2H x H] W transposed
+    float* part = nullptr;
+};
+
+size_t carve_rnn(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base, TreeRnnWs& w) {
+    Carver c(base);
+    const int H = d.H;
+    w.s.lword = c.take<int32_t>(N);
+    w.s.lchild = c.take<int32_t>(N);
+    w.s.rchild = c.take<int32_t>(N);
+    w.s.parent = c.take<int32_t>(N);
+    w.s.rootk = c.take<int32_t>(N);
+    w.s.rootpos = c.take<int32_t>(K);
+    w.A = c.take<float>(int64_t(N) * H);
+    w.Hn = c.take<float>(int64_t(N) * H);
+    w.HLR = c.take<float>(int64_t(N) * 2 * H);
+    w.dh = c.take<float>(int64_t(N) * H);
+    w.Wt = c.take<float>(int64_t(2) * H * H);
+    w.part = c.take<float>(colsum_partial_floats(H));
+    return c.off + 256;
+}
+
+// h of node p (level-ordered) to its parent's [h_L; h_R] row or to h_root
+__device__ __forceinline__ void rnn_send(int p, int j, int H, int M0, float h, const int32_t* parent,
+                                         const int32_t* rootk, float* HLR, float* h_root) {
+    const int par = parent[p];
+    if (par >= 0) HLR[int64_t((par >> 1) - M0) * 2 * H + (par & 1) * H + j] = h;
+    else h_root[int64_t(rootk[p]) * H + j] = h;
+}
+
+__global__ void treernn_leaf_kernel(int rows, int H, int M0, const int32_t* lword, const float* emb,
+                                    const int32_t* parent, const int32_t* rootk, float* Hn, float* HLR,
+                                    float* h_root) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(rows) * H) return;
+    const int p = int(i / H), j = int(i % H);
+    const float h = emb[int64_t(lword[p]) * H + j];
+    Hn[i] = h;
+    rnn_send(p, j, H, M0, h, parent, rootk, HLR, h_root);
+}
+
+__global__ void treernn_fwd_point_kernel(int p0, int rows, int H, int M0, const float* A, const int32_t* parent,
+                                         const int32_t* rootk, float* Hn, float* HLR, float* h_root) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(rows) * H) return;
+    const int p = p0 + int(i / H), j = int(i % H);
+    const float h = tanhf_(A[int64_t(p) * H + j]);
+    Hn[int64_t(p) * H + j] = h;
+    rnn_send(p, j, H, M0, h, parent, rootk, HLR, h_root);
+}
+
+// da = dh (1 - h^2) over the rows of one level
+__global__ void treernn_bwd_point_kernel(int p0, int rows, int H, const float* Hn, const float* dh, float* dA) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(rows) * H) return;
+    const int64_t o = int64_t(p0) * H + i;
+    const float h = Hn[o];
+    dA[o] = dh[o] * (1.f - h * h);
+}
+
+janus_status check_rnn(const janus_treelstm_desc* d) {
+    janus_status e = check(d);
+    if (e != JANUS_OK) return e;
+    return d->E == d->H ? JANUS_OK : JANUS_ERR_INVALID_ARG;
+}
+
+janus_status prepare_rnn(const janus_treelstm_desc* d, const janus_tree_batch* t, void* ws, size_t ws_bytes,
+                         TreeSchedule& s, TreeRnnWs& w) {
+    janus_status e = check_rnn(d);
+    if (e != JANUS_OK) return e;
+    if ((e = build_tree_schedule(t, d->V, s)) != JANUS_OK) return e;
+    if (!ws || ws_bytes < carve_rnn(*d, s.N, t->num_trees, nullptr, w) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return JANUS_ERR_WORKSPACE;
+    carve_rnn(*d, s.N, t->num_trees, ws, w);
+    return JANUS_OK;
+}
+
 }  // namespace
 
 }  // namespace janus
@@ -506,4 +600,96 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
                                      nullptr, nullptr, w.dxl, E, st);
     if (e != JANUS_OK) return e;
     return embed_backward(JANUS_F32, w.dxl, w.lword, M0, E, demb, d->V, st);
+}
+
+extern "C" size_t janus_treernn_workspace_bytes(const janus_treernn_desc* d, int32_t max_nodes, int32_t max_trees) {
+    if (check_rnn(d) != JANUS_OK || max_nodes <= 0 || max_trees <= 0) return 0;
+    TreeRnnWs w;
+    return carve_rnn(*d, max_nodes, max_trees, nullptr, w);
+}
+
+extern "C" janus_status janus_treernn_fwd(const janus_treernn_desc* d, const janus_tree_batch* t, const void* emb,
+                                          const void* W, const void* b, void* h_root, void* ws, size_t ws_bytes,
+                                          void* stream) {
+    if (!emb || !W || !b || !h_root) return JANUS_ERR_INVALID_ARG;
+    TreeSchedule s;
+    TreeRnnWs w;
+    janus_status e = prepare_rnn(d, t, ws, ws_bytes, s, w);
+    if (e != JANUS_OK) return e;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if ((e = upload_tree(t, s, w.s, st)) != JANUS_OK) return e;
+    const int H = d->H;
+    const int M0 = s.level_offsets[1];
+    float* hr = static_cast<float*>(h_root);
+    // the level contractions read W transposed (N = H contiguous)
+    if ((e = transpose_f32(static_cast<const float*>(W), H, 2 * H, w.Wt, st)) != JANUS_OK) return e;
+    {
+        const int64_t n = int64_t(M0) * H;
+        TraceScope trace("treernn_leaf", 0.0, 12.0 * n, st);
+        hipLaunchKernelGGL(treernn_leaf_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, M0, H, M0,
+                           w.s.lword, static_cast<const float*>(emb), w.s.parent, w.s.rootk, w.Hn, w.HLR, hr);
+        JANUS_LAUNCH_CHECK();
+    }
+    for (int k = 1; k < s.num_levels; ++k) {
+        const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
+        e = simt_gemm<false, kSimtStore>("treernn_level_gemm", rows, H, 2 * H, w.HLR + int64_t(p0 - M0) * 2 * H,
+                                         2 * H, nullptr, w.Wt, H, nullptr, static_cast<const float*>(b),
+                                         w.A + int64_t(p0) * H, H, st);
+        if (e != JANUS_OK) return e;
+        const int64_t n = int64_t(rows) * H;
+        TraceScope trace("treernn_fwd_point", 0.0, 12.0 * n, st);
+        hipLaunchKernelGGL(treernn_fwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H,
+                           M0, w.A, w.s.parent, w.s.rootk, w.Hn, w.HLR, hr);
+        JANUS_LAUNCH_CHECK();
+    }
+    return JANUS_OK;
+}
+
+extern "C" janus_status janus_treernn_bwd(const janus_treernn_desc* d, const janus_tree_batch* t, const void* W,
+                                          void* ws, size_t ws_bytes, const void* dh_root, float* demb, float* dW,
+                                          float* db, void* stream) {
+    if (!W || !dh_root || !demb || !dW || !db) return JANUS_ERR_INVALID_ARG;
+    TreeSchedule s;
+    TreeRnnWs w;
+    janus_status e = prepare_rnn(d, t, ws, ws_bytes, s, w);
+    if (e != JANUS_OK) return e;
+    const int M0 = s.level_offsets[1];
+    if (M0 > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    if ((e = upload_tree(t, s, w.s, st)) != JANUS_OK) return e;
+    const int H = d->H, N = s.N;
+    const int64_t kh = int64_t(t->num_trees) * H;
+    {
+        // dh of the roots (the dc half of this kernel's output is unused here)
+        TraceScope trace("tree_bwd_init", 0.0, 12.0 * kh, st);
+        hipLaunchKernelGGL(tree_bwd_init_kernel, dim3(unsigned((kh + 255) / 256)), dim3(256), 0, st, t->num_trees, H,
+                           w.s.rootpos, static_cast<const float*>(dh_root), w.dh, w.A);
+        JANUS_LAUNCH_CHECK();
+    }
+    for (int k = s.num_levels - 1; k >= 1; --k) {
+        const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
+        const int64_t n = int64_t(rows) * H;
+        {
+            TraceScope trace("treernn_bwd_point", 0.0, 12.0 * n, st);
+            hipLaunchKernelGGL(treernn_bwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows,
+                               H, w.Hn, w.dh, w.A);
+            JANUS_LAUNCH_CHECK();
+        }
+        // [dh_L; dh_R] = da W to the children (W rows are N = 2H contiguous)
+        e = simt_gemm<false, kSimtChildren>("treernn_dh_gemm", rows, 2 * H, H, w.A + int64_t(p0) * H, H, nullptr,
+                                            static_cast<const float*>(W), 2 * H, nullptr, nullptr, w.dh, 0, st,
+                                            w.s.lchild + p0, w.s.rchild + p0, H);
+        if (e != JANUS_OK) return e;
+    }
+    // dW = da_int^T HLR  (K = internal nodes), db = column sums of da_int
+    e = simt_gemm<true, kSimtStore>("treernn_dW_gemm", H, 2 * H, N - M0, w.A + int64_t(M0) * H, H, nullptr, w.HLR,
+                                    2 * H, nullptr, nullptr, dW, 2 * H, st);
+    if (e != JANUS_OK) return e;
+    if (N > M0) {
+        if ((e = colsum(JANUS_F32, w.A + int64_t(M0) * H, N - M0, H, H, db, w.part, st)) != JANUS_OK) return e;
+    } else if ((e = zero_fill(db, sizeof(float) * H, st)) != JANUS_OK) {
+        return e;
+    }
+    // the leaves' dh is the gradient of their word vectors
+    return embed_backward(JANUS_F32, w.dh, w.s.lword, M0, H, demb, d->V, st);
 }

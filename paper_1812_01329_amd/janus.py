@@ -32,6 +32,7 @@ EXPORTS = [
     "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
     "janus_trace_end", "janus_status_string", "janus_version", "janus_last_error",
     "janus_sgd_workspace_bytes", "janus_sgd_clip_update", "janus_lstm_state_carry",
+    "janus_treernn_workspace_bytes", "janus_treernn_fwd", "janus_treernn_bwd",
 ]
 
 
@@ -113,6 +114,10 @@ def lib():
         L.janus_treelstm_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, vp, vp, vp, vp, sz, vp]
         L.janus_treelstm_bwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, vp, vp, sz, vp, vp, vp,
                                          vp, vp, vp]
+        L.janus_treernn_workspace_bytes.restype = sz
+        L.janus_treernn_workspace_bytes.argtypes = [C.POINTER(TreeDesc), i32, i32]
+        L.janus_treernn_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, vp, vp, vp, sz, vp]
+        L.janus_treernn_bwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, sz, vp, vp, vp, vp, vp]
         L.janus_xent_workspace_bytes.restype = sz
         L.janus_xent_workspace_bytes.argtypes = [C.POINTER(XentDesc), C.c_int]
         L.janus_embed_softmax_xent.argtypes = [C.POINTER(XentDesc), C.c_int, pi32, vp, vp, vp, vp, vp, vp, vp, vp,
@@ -265,6 +270,24 @@ def janus_treelstm_bwd(desc: TreeDesc, trees, emb, W, U, ws, dh_root, demb, dW, 
                                   ws.numel() * ws.element_size(), _p(dh_root), _p(demb), _p(dW), _p(dU), _p(db),
                                   _stream(stream))
     _check(st, "janus_treelstm_bwd")
+
+
+def janus_treernn_workspace_bytes(H, V, max_nodes, max_trees) -> int:
+    return int(lib().janus_treernn_workspace_bytes(C.byref(TreeDesc(H, H, V, F32)), max_nodes, max_trees))
+
+
+def janus_treernn_fwd(desc: TreeDesc, trees, emb, W, b, h_root, ws, stream=None):
+    tb, keep = _tree_c(trees.left, trees.right, trees.word, trees.root)
+    st = lib().janus_treernn_fwd(C.byref(desc), C.byref(tb), _p(emb), _p(W), _p(b), _p(h_root), _p(ws),
+                                 ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "janus_treernn_fwd")
+
+
+def janus_treernn_bwd(desc: TreeDesc, trees, W, ws, dh_root, demb, dW, db, stream=None):
+    tb, keep = _tree_c(trees.left, trees.right, trees.word, trees.root)
+    st = lib().janus_treernn_bwd(C.byref(desc), C.byref(tb), _p(W), _p(ws), ws.numel() * ws.element_size(),
+                                 _p(dh_root), _p(demb), _p(dW), _p(db), _stream(stream))
+    _check(st, "janus_treernn_bwd")
 
 
 # ---------------------------------------------------------------- heads

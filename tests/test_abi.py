@@ -343,3 +343,21 @@ def test_state_carry_rejects_bad_arguments(case):
         c0 = h0 + n // 2
     st = L.janus_lstm_state_carry(C.byref(d), Bp, hT, cT, h0, c0, None)
     assert st == J.ERR_INVALID_ARG
+
+
+def test_treernn_needs_equal_embedding_and_hidden_width():
+    L = J.lib()
+    d = J.TreeDesc(300, 150, 100, J.F32)
+    assert L.janus_treernn_workspace_bytes(C.byref(d), 10, 2) == 0
+    d.E = 150
+    assert L.janus_treernn_workspace_bytes(C.byref(d), 10, 2) > 0
+    left, right, word, root = (np.array(v, np.int32) for v in ([-1, -1, 0], [-1, -1, 1], [3, 4, -1], [2]))
+    tb, keep = J._tree_c(left, right, word, root)
+    d.E = 300
+    st = L.janus_treernn_fwd(C.byref(d), C.byref(tb), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 1 << 20, None)
+    assert st == J.ERR_INVALID_ARG
+    d.E = 150
+    bad = J._tree_c(np.array([-1, 0, 1], np.int32), np.array([-1, -1, 0], np.int32),
+                    np.array([3, -1, -1], np.int32), np.array([2], np.int32))[0]   # a node with one child
+    st = L.janus_treernn_fwd(C.byref(d), C.byref(bad), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 1 << 20, None)
+    assert st == J.ERR_TREE
