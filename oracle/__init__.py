@@ -18,4 +18,4 @@ The paper does not define the cell equations; it names the models it trains
 (Section 6.1, Table 2: LSTM [51], LM [21], TreeLSTM [40]).  The equations
 used here are the standard ones of those models, stated in each module.
 """
-from . import heads, lstm, schedule, sgd, steps, treelstm, treernn  # noqa: F401
+from . import childsum, heads, lstm, schedule, sgd, steps, treelstm, treernn  # noqa: F401

@@ -13,7 +13,7 @@ from __future__ import annotations
 
 import numpy as np
 
-from . import heads, lstm, treelstm, treernn
+from . import childsum, heads, lstm, treelstm, treernn
 
 
 def _f64(a):
@@ -100,3 +100,15 @@ def treernn_step(w):
     demb, dW, db = treernn.backward_recursive(w.trees, h, w.emb.shape, W, dh_root)
     return dict(loss=loss, h_root=h_root, logits=logits, dh_root=dh_root, dWs=dWs, dbs=dbs,
                 demb=demb, dW=dW, db=db, h=h)
+
+
+def childsum_step(w):
+    """Training step of the Child-Sum TreeLSTM workload: recursion from every
+    root, 5-class softmax cross-entropy at the roots (mean over trees),
+    backward."""
+    W, U, b = _f64(w.W), _f64(w.U), _f64(w.b)
+    h_root, st = childsum.forward_recursive(w.trees, _f64(w.emb), W, U, b)
+    loss, dh_root, dWs, dbs, logits = heads.softmax_xent(h_root, w.Ws, _f64(w.bs), w.labels)
+    demb, dW, dU, db = childsum.backward_recursive(w.trees, st, w.emb.shape, W, U, dh_root)
+    return dict(loss=loss, h_root=h_root, logits=logits, dh_root=dh_root, dWs=dWs, dbs=dbs,
+                demb=demb, dW=dW, dU=dU, db=db, h=st["h"], c=st["c"])

@@ -328,6 +328,91 @@ def sst_treernn(n_trees=25, H=300, V=20000, C=5, min_leaves=5, max_leaves=50, se
     return TreeRNNWorkload("treernn", H, V, C, trees, labels, emb, W, b, Ws, bs)
 
 
+@dataclasses.dataclass
+class NaryTreeBatch:
+    """A batch of trees of any arity as flat int32 arrays: the children of
+    node n are ``children[child_offsets[n]:child_offsets[n + 1]]`` (none for
+    a leaf); every node has a token id ``word[n]`` (dependency-tree style);
+    ``root[k]`` is the root of tree k.  Trees are concatenated, each
+    numbered from its root."""
+    child_offsets: np.ndarray
+    children: np.ndarray
+    word: np.ndarray
+    root: np.ndarray
+
+    @property
+    def num_nodes(self) -> int:
+        return int(self.word.shape[0])
+
+    @property
+    def num_trees(self) -> int:
+        return int(self.root.shape[0])
+
+
+def make_nary_trees(rng: np.random.Generator, n_trees: int, min_nodes: int, max_nodes: int, V: int,
+                    zipf_s: float = 1.1, sizes: Optional[List[int]] = None,
+                    chain: bool = False) -> NaryTreeBatch:
+    """Random recursive trees: node i > 0 of a tree hangs under a uniformly
+    drawn earlier node (under node i - 1 when ``chain``), so arities vary and
+    depth grows like log n.  Words Zipf(s) over [0, V)."""
+    if sizes is None:
+        sizes = [int(s) for s in rng.integers(min_nodes, max_nodes + 1, size=n_trees)]
+    kids: list = []
+    roots = []
+    base = 0
+    for n in sizes:
+        par = [-1] + [(i - 1 if chain else int(rng.integers(0, i))) for i in range(1, n)]
+        lists = [[] for _ in range(n)]
+        for i in range(1, n):
+            lists[par[i]].append(base + i)
+        kids += lists
+        roots.append(base)
+        base += n
+    off = np.zeros(base + 1, np.int32)
+    off[1:] = np.cumsum([len(c) for c in kids])
+    children = np.asarray([c for cl in kids for c in cl], np.int32)
+    words = zipf_truncated(rng, zipf_s, V, base).astype(np.int32)
+    return NaryTreeBatch(off, children, words, np.asarray(roots, np.int32))
+
+
+@dataclasses.dataclass
+class ChildSumWorkload:
+    """Inputs of one Child-Sum TreeLSTM training step (fp32).  Gate blocks of
+    W [4H, E], U [4H, H] and b [4H] are (i, o, u, f)."""
+    name: str
+    E_dim: int
+    H: int
+    V: int
+    C: int
+    trees: NaryTreeBatch
+    labels: np.ndarray
+    emb: np.ndarray
+    W: np.ndarray
+    U: np.ndarray
+    b: np.ndarray
+    Ws: np.ndarray
+    bs: np.ndarray
+    dtype: str = F32
+
+
+def sst_childsum(n_trees=25, E=300, H=150, V=20000, C=5, min_nodes=5, max_nodes=50, seed=None, sizes=None,
+                 chain=False) -> ChildSumWorkload:
+    """Child-Sum TreeLSTM, embedding 300, hidden 150, batch 25 random
+    recursive trees (dependency-tree stand-ins) of 5-50 nodes, a Zipf(1.1)
+    word at every node over a 20000 vocabulary, 5-class softmax at the root
+    with uniform labels, fp32, all parameters U(-0.1, 0.1)."""
+    rp, _, rtree, rl = _streams(6, seed)
+    emb = uniform(rp, 0.1, (V, E))
+    W = uniform(rp, 0.1, (4 * H, E))
+    U = uniform(rp, 0.1, (4 * H, H))
+    b = uniform(rp, 0.1, (4 * H,))
+    Ws = uniform(rp, 0.1, (C, H))
+    bs = uniform(rp, 0.1, (C,))
+    trees = make_nary_trees(rtree, n_trees, min_nodes, max_nodes, V, sizes=sizes, chain=chain)
+    labels = rl.integers(0, C, size=trees.num_trees).astype(np.int32)
+    return ChildSumWorkload("childsum", E, H, V, C, trees, labels, emb, W, U, b, Ws, bs)
+
+
 # Named full-size workloads, in the order of the five configurations.
 FULL: Dict[str, callable] = {
     "tiny": tiny_lstm,
@@ -336,4 +421,5 @@ FULL: Dict[str, callable] = {
     "treelstm": sst_treelstm,
     "lm2048": lm2048_lstm,
     "treernn": sst_treernn,
+    "childsum": sst_childsum,
 }
