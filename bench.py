@@ -47,6 +47,8 @@ WORKLOADS = {
                  unit="sequences/s"),
     "treernn": dict(desc="binary TreeRNN, word vectors and hidden 300, 25 trees of 5-50 leaves, fp32, "
                          "5-class softmax at roots", unit="trees/s"),
+    "childsum": dict(desc="Child-Sum TreeLSTM, embed 300, hidden 150, 25 random trees of 5-50 nodes, a word at "
+                          "every node, fp32, 5-class softmax at roots", unit="trees/s"),
 }
 
 
@@ -90,6 +92,8 @@ def cpu_baseline(w, n_rows: int):
         t0 = time.perf_counter()
         if isinstance(w, wl.TreeRNNWorkload):
             oracle_steps.treernn_step(w)
+        elif isinstance(w, wl.ChildSumWorkload):
+            oracle_steps.childsum_step(w)
         else:
             oracle_steps.tree_step(w)
         dt = time.perf_counter() - t0

@@ -300,6 +300,66 @@ janus_status janus_treernn_bwd(const janus_treernn_desc* d, const janus_tree_bat
                                void* stream);
 
 /* ------------------------------------------------------------------------ */
+/* Child-Sum TreeLSTM over trees of any arity                               */
+/* ------------------------------------------------------------------------ */
+
+/*
+ * The other variant of the TreeLSTM the paper trains ([40]): nodes may have
+ * any number of children and every node reads its word vector x.  With h~
+ * the sum of the children's h:
+ *     i = s(W_i x + U_i h~ + b_i),  o = s(W_o x + U_o h~ + b_o),
+ *     u = tanh(W_u x + U_u h~ + b_u),  f_k = s(W_f x + U_f h_k + b_f) per child,
+ *     c = i u + sum_k f_k c_k,  h = o tanh(c).
+ * Gate blocks of W [4H, E], U [4H, H], b [4H] are (i, o, u, f).  Evaluated
+ * one level of independent nodes at a time, as the binary TreeNNs.
+ */
+typedef janus_treelstm_desc janus_childsum_desc;
+
+/*
+ * A batch of trees as HOST int32 arrays: the children of node n are
+ * children[child_offsets[n] .. child_offsets[n + 1]) (none: a leaf);
+ * child_offsets has num_nodes + 1 entries starting at 0; word[n] in [0, V)
+ * for every node; root[k] (num_trees entries) is the root of tree k.  Every
+ * node has at most one parent and is reachable from exactly one root.
+ */
+typedef struct {
+    int32_t num_trees, num_nodes;
+    const int32_t* child_offsets;
+    const int32_t* children;
+    const int32_t* word;
+    const int32_t* root;
+} janus_nary_tree_batch;
+
+/* Workspace bytes for a batch of at most max_nodes nodes. */
+size_t janus_childsum_workspace_bytes(const janus_childsum_desc* d, int32_t max_nodes);
+
+/*
+ *  emb [V, E], W [4H, E], U [4H, H], b [4H]: float32.
+ *  h_root [num_trees, H] float32: h of root[k].
+ * Errors: INVALID_ARG (NULL pointers or arrays, empty batch, a non-positive
+ * size), TREE (offsets not starting at 0 or decreasing, a child id out of
+ * range, a node with two parents, a root with a parent, a cycle, a node no
+ * root reaches), TOKEN (a word outside [0, V)), WORKSPACE, UNSUPPORTED (only
+ * F32).
+ */
+janus_status janus_childsum_fwd(const janus_childsum_desc* d, const janus_nary_tree_batch* t,
+                                const void* emb, const void* W, const void* U, const void* b,
+                                void* h_root, void* ws, size_t ws_bytes, void* stream);
+
+/*
+ * Backward of the call above (same d, t, emb, W, U and workspace).
+ *  dh_root [num_trees, H] float32: gradient of h_root (the roots' c gets 0).
+ *  demb [V, E], dW [4H, E], dU [4H, H], db [4H]: float32, overwritten (rows
+ *          of demb for words not in the batch are 0).
+ * Errors: as the forward; UNSUPPORTED when the batch has more than 16384
+ * nodes.
+ */
+janus_status janus_childsum_bwd(const janus_childsum_desc* d, const janus_nary_tree_batch* t,
+                                const void* emb, const void* W, const void* U,
+                                void* ws, size_t ws_bytes, const void* dh_root,
+                                float* demb, float* dW, float* dU, float* db, void* stream);
+
+/* ------------------------------------------------------------------------ */
 /* Embedding and softmax cross-entropy                                      */
 /* ------------------------------------------------------------------------ */
 

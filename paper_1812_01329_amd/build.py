@@ -19,7 +19,7 @@ CSRC = os.path.join(PKG, "csrc")
 OUT = os.path.join(PKG, "libjanus.so")
 BUILD_DIR = os.path.join(ROOT, "_build")
 
-SOURCES = ["schedule.cpp", "runtime.cpp", "gemm.hip", "lstm.hip", "heads.hip", "tree.hip", "sgd.hip"]
+SOURCES = ["schedule.cpp", "runtime.cpp", "gemm.hip", "lstm.hip", "heads.hip", "tree.hip", "sgd.hip", "childsum.hip"]
 
 HIPCC = os.environ.get("HIPCC", "/opt/rocm/bin/hipcc")
 ARCH = "gfx950"

@@ -1,0 +1,343 @@
+// Child-Sum TreeLSTM over a batch of trees of any arity, evaluated as
+// level-wise frontiers.
+//
+// The cited TreeLSTM paper defines this variant next to the binary one: every
+// node reads its word vector x, h~ is the sum of its children's h, and each
+// child k has its own forget gate,
+//     i, o = s(W x + U h~ + b),  u = tanh(W x + U h~ + b)   (blocks i, o, u)
+//     f_k  = s(W_f x + U_f h_k + b_f)
+//     c = i u + sum_k f_k c_k,   h = o tanh(c).
+// Levels group nodes by height (a node after all of its children), the same
+// frontiers as the binary TreeNNs (Section 6.3.1, "+PARL").
+//
+// Forward.  x does not depend on the recursion, so XW = X W^T + b is one
+// contraction over all nodes first.  After a level is computed, one
+// contraction G = h U^T (all four blocks) serves its parents: by linearity
+// U_iou h~ of a parent is the sum of its children's G_iou rows, and child k's
+// forget gate reads G_f of row k.  A level is thus one cell kernel (which
+// gathers its children's G and c) and one contraction.
+//
+// Backward, levels from the top down.  A node's cell backward writes, into
+// the row of each child k, dG(k) = [da_iou(parent); da_f(parent, k)] and the
+// child's dc; into its own row dXW = [da_iou; sum_k da_f].  When a level is
+// reached all its rows of dG are complete, so its dh = dG U is one
+// contraction over the level's contiguous rows (roots have dG = 0 and add
+// the head's gradient).  Then dW = dXW^T X, dU = dG^T H, db = sum of dXW,
+// and dX = dXW W for the embedding gradient.
+#include <algorithm>
+#include <vector>
+
+#include "device.hpp"
+#include "ops.hpp"
+#include "simt.hpp"
+
+namespace janus {
+
+namespace {
+
+// Host schedule: nodes ordered by (level, id); children lists by position.
+struct NarySchedule {
+    int32_t N = 0;
+    std::vector<int32_t> level_offsets;   // [num_levels + 1]
+    std::vector<int32_t> pword, pcoff, pkids, rootk, rootpos;
+};
+
+janus_status build_nary_schedule(const janus_nary_tree_batch* t, int32_t V, NarySchedule& s) {
+    if (!t || t->num_trees <= 0 || t->num_nodes <= 0 || !t->child_offsets || !t->word || !t->root)
+        return JANUS_ERR_INVALID_ARG;
+    const int32_t N = t->num_nodes, K = t->num_trees;
+    const int32_t* off = t->child_offsets;
+    if (off[0] != 0) return JANUS_ERR_TREE;
+    for (int32_t n = 0; n < N; ++n)
+        if (off[n + 1] < off[n]) return JANUS_ERR_TREE;
+    const int32_t E = off[N];
+    if (E > 0 && !t->children) return JANUS_ERR_INVALID_ARG;
+    std::vector<int32_t> parent(N, -1);
+    for (int32_t e = 0; e < E; ++e) {
+        const int32_t c = t->children[e];
+        if (c < 0 || c >= N || parent[c] >= 0) return JANUS_ERR_TREE;
+        parent[c] = 1;
+    }
+    for (int32_t n = 0; n < N; ++n)
+        if (t->word[n] < 0 || t->word[n] >= V) return JANUS_ERR_TOKEN;
+    // levels by an explicit post-order walk from every root; a node seen twice
+    // or never is malformed (a cycle, a shared child, an unreachable node)
+    std::vector<int32_t> level(N, -1), state(N, 0), rootk(N, -1);
+    std::vector<std::pair<int32_t, int32_t>> stack;
+    int32_t seen = 0;
+    for (int32_t k = 0; k < K; ++k) {
+        const int32_t r = t->root[k];
+        if (r < 0 || r >= N || parent[r] >= 0 || state[r] != 0) return JANUS_ERR_TREE;
+        rootk[r] = k;
+        stack.push_back({r, off[r]});
+        state[r] = 1;
+        while (!stack.empty()) {
+            auto& [n, next] = stack.back();
+            if (next < off[n + 1]) {
+                const int32_t c = t->children[next++];
+                if (state[c] != 0) return JANUS_ERR_TREE;
+                state[c] = 1;
+                stack.push_back({c, off[c]});
+            } else {
+                int32_t lv = 0;
+                for (int32_t e = off[n]; e < off[n + 1]; ++e) lv = std::max(lv, level[t->children[e]] + 1);
+                level[n] = lv;
+                state[n] = 2;
+                ++seen;
+                stack.pop_back();
+            }
+        }
+    }
+    if (seen != N) return JANUS_ERR_TREE;
+    int32_t L = 0;
+    for (int32_t n = 0; n < N; ++n) L = std::max(L, level[n] + 1);
+    s.N = N;
+    s.level_offsets.assign(L + 1, 0);
+    for (int32_t n = 0; n < N; ++n) ++s.level_offsets[level[n] + 1];
+    for (int32_t k = 0; k < L; ++k) s.level_offsets[k + 1] += s.level_offsets[k];
+    std::vector<int32_t> pos(N), fill(s.level_offsets.begin(), s.level_offsets.end() - 1);
+    for (int32_t n = 0; n < N; ++n) pos[n] = fill[level[n]]++;   // ascending id within a level
+    s.pword.assign(N, 0);
+    s.rootk.assign(N, -1);
+    s.rootpos.assign(K, 0);
+    s.pcoff.assign(N + 1, 0);
+    std::vector<int32_t> node_at(N);
+    for (int32_t n = 0; n < N; ++n) node_at[pos[n]] = n;
+    for (int32_t p = 0; p < N; ++p) {
+        const int32_t n = node_at[p];
+        s.pword[p] = t->word[n];
+        s.rootk[p] = rootk[n];
+        s.pcoff[p + 1] = s.pcoff[p] + (off[n + 1] - off[n]);
+    }
+    s.pkids.assign(std::max(E, 1), 0);
+    for (int32_t p = 0; p < N; ++p) {
+        const int32_t n = node_at[p];
+        for (int32_t e = off[n], q = s.pcoff[p]; e < off[n + 1]; ++e, ++q) s.pkids[q] = pos[t->children[e]];
+    }
+    for (int32_t k = 0; k < K; ++k) s.rootpos[k] = pos[t->root[k]];
+    return JANUS_OK;
+}
+
+struct CsWs {
+    int32_t* pword = nullptr;    // [N] word of the node at each position
+    int32_t* pcoff = nullptr;    // [N + 1] children of position p: pkids[pcoff[p] .. pcoff[p + 1])
+    int32_t* pkids = nullptr;    // [N] child positions
+    int32_t* rootk = nullptr;    // [N] tree index of a root, -1 otherwise
+    float* XW = nullptr;         // [N x 4H] X W^T + b
+    float* G = nullptr;          // [N x 4H] h U^T (forward), dG (backward)
+    float* Gt = nullptr;         // [N x 3H] gates i, o, u
+    float* F = nullptr;          // [N x H]  forget gate of each node towards its parent
+    float* C = nullptr;          // [N x H]
+    float* Hn = nullptr;         // [N x H]
+    float* dXW = nullptr;        // [N x 4H]
+    float* dh = nullptr;         // [N x H]
+    float* dc = nullptr;         // [N x H]
+    float* dx = nullptr;         // [N x E]
+    float* Wt = nullptr;         // [E x 4H]
+    float* Ut = nullptr;         // [H x 4H]
+    float* part = nullptr;
+};
+
+size_t carve_cs(const janus_treelstm_desc& d, int32_t N, void* base, CsWs& w) {
+    Carver c(base);
+    const int H = d.H, E = d.E;
+    w.pword = c.take<int32_t>(N);
+    w.pcoff = c.take<int32_t>(int64_t(N) + 1);
+    w.pkids = c.take<int32_t>(N);
+    w.rootk = c.take<int32_t>(N);
+    w.XW = c.take<float>(int64_t(N) * 4 * H);
+    w.G = c.take<float>(int64_t(N) * 4 * H);
+    w.Gt = c.take<float>(int64_t(N) * 3 * H);
+    w.F = c.take<float>(int64_t(N) * H);
+    w.C = c.take<float>(int64_t(N) * H);
+    w.Hn = c.take<float>(int64_t(N) * H);
+    w.dXW = c.take<float>(int64_t(N) * 4 * H);
+    w.dh = c.take<float>(int64_t(N) * H);
+    w.dc = c.take<float>(int64_t(N) * H);
+    w.dx = c.take<float>(int64_t(N) * E);
+    w.Wt = c.take<float>(int64_t(E) * 4 * H);
+    w.Ut = c.take<float>(int64_t(H) * 4 * H);
+    w.part = c.take<float>(colsum_partial_floats(4 * H));
+    return c.off + 256;
+}
+
+__global__ void cs_fwd_cell_kernel(int p0, int rows, int H, const float* XW, const float* G, const int32_t* pcoff,
+                                   const int32_t* pkids, const int32_t* rootk, float* Gt, float* F, float* C,
+                                   float* Hn, float* h_root) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(rows) * H) return;
+    const int p = p0 + int(i / H), j = int(i % H);
+    const float* xw = XW + int64_t(p) * 4 * H;
+    float ai = xw[j], ao = xw[H + j], au = xw[2 * H + j];
+    const float af = xw[3 * H + j];
+    float csum = 0.f;
+    for (int e = pcoff[p]; e < pcoff[p + 1]; ++e) {
+        const int k = pkids[e];
+        const float* g = G + int64_t(k) * 4 * H;
+        ai += g[j];
+        ao += g[H + j];
+        au += g[2 * H + j];
+        const float f = sigmoidf_(af + g[3 * H + j]);
+        F[int64_t(k) * H + j] = f;
+        csum += f * C[int64_t(k) * H + j];
+    }
+    const float gi = sigmoidf_(ai), go = sigmoidf_(ao), gu = tanhf_(au);
+    const float c = gi * gu + csum;
+    const float h = go * tanhf_(c);
+    C[int64_t(p) * H + j] = c;
+    Hn[int64_t(p) * H + j] = h;
+    float* gt = Gt + int64_t(p) * 3 * H;
+    gt[j] = gi;
+    gt[H + j] = go;
+    gt[2 * H + j] = gu;
+    if (rootk[p] >= 0) h_root[int64_t(rootk[p]) * H + j] = h;
+}
+
+__global__ void cs_bwd_cell_kernel(int p0, int rows, int H, const float* dh, const float* dh_root,
+                                   const int32_t* rootk, const float* Gt, const float* F, const float* C,
+                                   const int32_t* pcoff, const int32_t* pkids, float* dc, float* dG, float* dXW) {
+    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
+    if (i >= int64_t(rows) * H) return;
+    const int p = p0 + int(i / H), j = int(i % H);
+    const int rk = rootk[p];
+    const float dhv = dh[int64_t(p) * H + j] + (rk >= 0 ? dh_root[int64_t(rk) * H + j] : 0.f);
+    const float* gt = Gt + int64_t(p) * 3 * H;
+    const float gi = gt[j], go = gt[H + j], gu = gt[2 * H + j];
+    const float tau = tanhf_(C[int64_t(p) * H + j]);
+    const float dct = dc[int64_t(p) * H + j] + dhv * go * (1.f - tau * tau);
+    const float dai = dct * gu * gi * (1.f - gi);
+    const float dao = dhv * tau * go * (1.f - go);
+    const float dau = dct * gi * (1.f - gu * gu);
+    float dafs = 0.f;
+    for (int e = pcoff[p]; e < pcoff[p + 1]; ++e) {
+        const int k = pkids[e];
+        const float f = F[int64_t(k) * H + j];
+        const float daf = dct * C[int64_t(k) * H + j] * f * (1.f - f);
+        dafs += daf;
+        float* g = dG + int64_t(k) * 4 * H;
+        g[j] = dai;
+        g[H + j] = dao;
+        g[2 * H + j] = dau;
+        g[3 * H + j] = daf;
+        dc[int64_t(k) * H + j] = dct * f;
+    }
+    float* x = dXW + int64_t(p) * 4 * H;
+    x[j] = dai;
+    x[H + j] = dao;
+    x[2 * H + j] = dau;
+    x[3 * H + j] = dafs;
+}
+
+janus_status check_cs(const janus_treelstm_desc* d) {
+    if (!d || d->E <= 0 || d->H <= 0 || d->V <= 0) return JANUS_ERR_INVALID_ARG;
+    if (d->dtype != JANUS_F32) return JANUS_ERR_UNSUPPORTED;
+    return JANUS_OK;
+}
+
+janus_status prepare_cs(const janus_treelstm_desc* d, const janus_nary_tree_batch* t, void* ws, size_t ws_bytes,
+                        NarySchedule& s, CsWs& w, hipStream_t st) {
+    janus_status e = check_cs(d);
+    if (e != JANUS_OK) return e;
+    if ((e = build_nary_schedule(t, d->V, s)) != JANUS_OK) return e;
+    if (!ws || ws_bytes < carve_cs(*d, s.N, nullptr, w) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return JANUS_ERR_WORKSPACE;
+    carve_cs(*d, s.N, ws, w);
+    const size_t nb = sizeof(int32_t) * s.N;
+    if ((e = upload(w.pword, s.pword.data(), nb, st)) != JANUS_OK) return e;
+    if ((e = upload(w.pcoff, s.pcoff.data(), nb + sizeof(int32_t), st)) != JANUS_OK) return e;
+    if ((e = upload(w.pkids, s.pkids.data(), sizeof(int32_t) * s.pkids.size(), st)) != JANUS_OK) return e;
+    return upload(w.rootk, s.rootk.data(), nb, st);
+}
+
+}  // namespace
+
+}  // namespace janus
+
+using namespace janus;
+
+extern "C" size_t janus_childsum_workspace_bytes(const janus_childsum_desc* d, int32_t max_nodes) {
+    if (check_cs(d) != JANUS_OK || max_nodes <= 0) return 0;
+    CsWs w;
+    return carve_cs(*d, max_nodes, nullptr, w);
+}
+
+extern "C" janus_status janus_childsum_fwd(const janus_childsum_desc* d, const janus_nary_tree_batch* t,
+                                           const void* emb, const void* W, const void* U, const void* b, void* h_root,
+                                           void* ws, size_t ws_bytes, void* stream) {
+    if (!emb || !W || !U || !b || !h_root) return JANUS_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    NarySchedule s;
+    CsWs w;
+    janus_status e = prepare_cs(d, t, ws, ws_bytes, s, w, st);
+    if (e != JANUS_OK) return e;
+    const int H = d->H, E = d->E, N = s.N;
+    const int L = int(s.level_offsets.size()) - 1;
+    if ((e = transpose_f32(static_cast<const float*>(W), 4 * H, E, w.Wt, st)) != JANUS_OK) return e;
+    if ((e = transpose_f32(static_cast<const float*>(U), 4 * H, H, w.Ut, st)) != JANUS_OK) return e;
+    // the input part of every node's gates at once
+    e = simt_gemm<false, kSimtStore>("childsum_x_gemm", N, 4 * H, E, static_cast<const float*>(emb), E, w.pword, w.Wt,
+                                     4 * H, nullptr, static_cast<const float*>(b), w.XW, 4 * H, st);
+    if (e != JANUS_OK) return e;
+    for (int k = 0; k < L; ++k) {
+        const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
+        const int64_t n = int64_t(rows) * H;
+        {
+            TraceScope trace("childsum_fwd_cell", 0.0, 4.0 * n * 16.0, st);
+            hipLaunchKernelGGL(cs_fwd_cell_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H,
+                               w.XW, w.G, w.pcoff, w.pkids, w.rootk, w.Gt, w.F, w.C, w.Hn,
+                               static_cast<float*>(h_root));
+            JANUS_LAUNCH_CHECK();
+        }
+        if (k + 1 < L) {   // the top level has no parents
+            e = simt_gemm<false, kSimtStore>("childsum_level_gemm", rows, 4 * H, H, w.Hn + int64_t(p0) * H, H, nullptr,
+                                             w.Ut, 4 * H, nullptr, nullptr, w.G + int64_t(p0) * 4 * H, 4 * H, st);
+            if (e != JANUS_OK) return e;
+        }
+    }
+    return JANUS_OK;
+}
+
+extern "C" janus_status janus_childsum_bwd(const janus_childsum_desc* d, const janus_nary_tree_batch* t,
+                                           const void* emb, const void* W, const void* U, void* ws, size_t ws_bytes,
+                                           const void* dh_root, float* demb, float* dW, float* dU, float* db,
+                                           void* stream) {
+    if (!emb || !W || !U || !dh_root || !demb || !dW || !dU || !db) return JANUS_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    NarySchedule s;
+    CsWs w;
+    janus_status e = prepare_cs(d, t, ws, ws_bytes, s, w, st);
+    if (e != JANUS_OK) return e;
+    const int H = d->H, E = d->E, N = s.N;
+    if (N > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
+    const int L = int(s.level_offsets.size()) - 1;
+    // roots have no parent: their dG rows and dc stay 0
+    if ((e = zero_fill(w.G, sizeof(float) * size_t(N) * 4 * H, st)) != JANUS_OK) return e;
+    if ((e = zero_fill(w.dc, sizeof(float) * size_t(N) * H, st)) != JANUS_OK) return e;
+    for (int k = L - 1; k >= 0; --k) {
+        const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
+        // dh of the level from the dG rows its parents wrote
+        e = simt_gemm<false, kSimtStore>("childsum_dh_gemm", rows, H, 4 * H, w.G + int64_t(p0) * 4 * H, 4 * H, nullptr,
+                                         static_cast<const float*>(U), H, nullptr, nullptr, w.dh + int64_t(p0) * H, H,
+                                         st);
+        if (e != JANUS_OK) return e;
+        const int64_t n = int64_t(rows) * H;
+        TraceScope trace("childsum_bwd_cell", 0.0, 4.0 * n * 20.0, st);
+        hipLaunchKernelGGL(cs_bwd_cell_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H, w.dh,
+                           static_cast<const float*>(dh_root), w.rootk, w.Gt, w.F, w.C, w.pcoff, w.pkids, w.dc, w.G,
+                           w.dXW);
+        JANUS_LAUNCH_CHECK();
+    }
+    // dW = dXW^T X (rows of emb gathered by word), dU = dG^T H, db = sum dXW
+    e = simt_gemm<true, kSimtStore>("childsum_dW_gemm", 4 * H, E, N, w.dXW, 4 * H, nullptr,
+                                    static_cast<const float*>(emb), E, w.pword, nullptr, dW, E, st);
+    if (e != JANUS_OK) return e;
+    e = simt_gemm<true, kSimtStore>("childsum_dU_gemm", 4 * H, H, N, w.G, 4 * H, nullptr, w.Hn, H, nullptr, nullptr,
+                                    dU, H, st);
+    if (e != JANUS_OK) return e;
+    if ((e = colsum(JANUS_F32, w.dXW, N, 4 * H, 4 * H, db, w.part, st)) != JANUS_OK) return e;
+    // dX = dXW W, then the embedding gradient
+    e = simt_gemm<false, kSimtStore>("childsum_dx_gemm", N, E, 4 * H, w.dXW, 4 * H, nullptr,
+                                     static_cast<const float*>(W), E, nullptr, nullptr, w.dx, E, st);
+    if (e != JANUS_OK) return e;
+    return embed_backward(JANUS_F32, w.dx, w.pword, N, E, demb, d->V, st);
+}

@@ -33,6 +33,7 @@ EXPORTS = [
     "janus_trace_end", "janus_status_string", "janus_version", "janus_last_error",
     "janus_sgd_workspace_bytes", "janus_sgd_clip_update", "janus_lstm_state_carry",
     "janus_treernn_workspace_bytes", "janus_treernn_fwd", "janus_treernn_bwd",
+    "janus_childsum_workspace_bytes", "janus_childsum_fwd", "janus_childsum_bwd",
 ]
 
 
@@ -55,6 +56,12 @@ class TreeDesc(C.Structure):
 class TreeBatchC(C.Structure):
     _fields_ = [("num_trees", C.c_int32), ("num_nodes", C.c_int32),
                 ("left", C.POINTER(C.c_int32)), ("right", C.POINTER(C.c_int32)),
+                ("word", C.POINTER(C.c_int32)), ("root", C.POINTER(C.c_int32))]
+
+
+class NaryBatchC(C.Structure):
+    _fields_ = [("num_trees", C.c_int32), ("num_nodes", C.c_int32),
+                ("child_offsets", C.POINTER(C.c_int32)), ("children", C.POINTER(C.c_int32)),
                 ("word", C.POINTER(C.c_int32)), ("root", C.POINTER(C.c_int32))]
 
 
@@ -118,6 +125,11 @@ def lib():
         L.janus_treernn_workspace_bytes.argtypes = [C.POINTER(TreeDesc), i32, i32]
         L.janus_treernn_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, vp, vp, vp, sz, vp]
         L.janus_treernn_bwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, sz, vp, vp, vp, vp, vp]
+        L.janus_childsum_workspace_bytes.restype = sz
+        L.janus_childsum_workspace_bytes.argtypes = [C.POINTER(TreeDesc), i32]
+        L.janus_childsum_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(NaryBatchC), vp, vp, vp, vp, vp, vp, sz, vp]
+        L.janus_childsum_bwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(NaryBatchC), vp, vp, vp, vp, sz, vp, vp, vp,
+                                         vp, vp, vp]
         L.janus_xent_workspace_bytes.restype = sz
         L.janus_xent_workspace_bytes.argtypes = [C.POINTER(XentDesc), C.c_int]
         L.janus_embed_softmax_xent.argtypes = [C.POINTER(XentDesc), C.c_int, pi32, vp, vp, vp, vp, vp, vp, vp, vp,
@@ -288,6 +300,32 @@ def janus_treernn_bwd(desc: TreeDesc, trees, W, ws, dh_root, demb, dW, db, strea
     st = lib().janus_treernn_bwd(C.byref(desc), C.byref(tb), _p(W), _p(ws), ws.numel() * ws.element_size(),
                                  _p(dh_root), _p(demb), _p(dW), _p(db), _stream(stream))
     _check(st, "janus_treernn_bwd")
+
+
+def _nary_c(trees):
+    arrs = [np.ascontiguousarray(a, dtype=np.int32) for a in
+            (trees.child_offsets, trees.children, trees.word, trees.root)]
+    tb = NaryBatchC(len(arrs[3]), len(arrs[2]), *[_i32p(a) for a in arrs])
+    return tb, arrs   # keep the arrays alive with the struct
+
+
+def janus_childsum_workspace_bytes(E, H, V, max_nodes) -> int:
+    return int(lib().janus_childsum_workspace_bytes(C.byref(TreeDesc(E, H, V, F32)), max_nodes))
+
+
+def janus_childsum_fwd(desc: TreeDesc, trees, emb, W, U, b, h_root, ws, stream=None):
+    tb, keep = _nary_c(trees)
+    st = lib().janus_childsum_fwd(C.byref(desc), C.byref(tb), _p(emb), _p(W), _p(U), _p(b), _p(h_root), _p(ws),
+                                  ws.numel() * ws.element_size(), _stream(stream))
+    _check(st, "janus_childsum_fwd")
+
+
+def janus_childsum_bwd(desc: TreeDesc, trees, emb, W, U, ws, dh_root, demb, dW, dU, db, stream=None):
+    tb, keep = _nary_c(trees)
+    st = lib().janus_childsum_bwd(C.byref(desc), C.byref(tb), _p(emb), _p(W), _p(U), _p(ws),
+                                  ws.numel() * ws.element_size(), _p(dh_root), _p(demb), _p(dW), _p(dU), _p(db),
+                                  _stream(stream))
+    _check(st, "janus_childsum_bwd")
 
 
 # ---------------------------------------------------------------- heads

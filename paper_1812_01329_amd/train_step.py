@@ -299,11 +299,67 @@ class TreeRNNStep:
                     dbs=_f64(self.dbs))
 
 
+class ChildSumStep:
+    """Device state and call sequence of a Child-Sum TreeLSTM training step."""
+
+    def __init__(self, w: wl.ChildSumWorkload, device="cuda", update: Optional[Tuple[float, float]] = None):
+        self.w = w
+        self.device = device
+        f = torch.float32
+        self.desc = J.TreeDesc(w.E_dim, w.H, w.V, J.F32)
+        self.emb = _dev(w.emb, f, device)
+        self.W = _dev(w.W, f, device)
+        self.U = _dev(w.U, f, device)
+        self.b = _dev(w.b, f, device)
+        self.Ws = _dev(w.Ws, f, device)
+        self.bs = _dev(w.bs, f, device)
+        K = w.trees.num_trees
+        self.labels_host = np.ascontiguousarray(w.labels, np.int32)
+        self.labels = torch.from_numpy(self.labels_host).to(device)
+        self.h_root = torch.zeros(K, w.H, dtype=f, device=device)
+        self.dh_root = torch.zeros(K, w.H, dtype=f, device=device)
+        self.demb = torch.zeros(w.V, w.E_dim, dtype=f, device=device)
+        self.dW = torch.empty_like(self.W)
+        self.dU = torch.empty_like(self.U)
+        self.db = torch.empty_like(self.b)
+        self.dWs = torch.empty_like(self.Ws)
+        self.dbs = torch.empty_like(self.bs)
+        self.loss = torch.zeros(1, dtype=f, device=device)
+        ws = J.janus_childsum_workspace_bytes(w.E_dim, w.H, w.V, w.trees.num_nodes)
+        self.ws = torch.empty(ws, dtype=torch.uint8, device=device)
+        self.xdesc = J.XentDesc(w.C, w.H, K, J.F32)
+        self.xws = torch.empty(J.janus_xent_workspace_bytes(w.C, w.H, K, J.F32, J.XENT_FWD_BWD),
+                               dtype=torch.uint8, device=device)
+        self.update = None
+        if update is not None:
+            self.update = SgdUpdate([self.emb, self.W, self.U, self.b, self.Ws, self.bs],
+                                    [self.demb, self.dW, self.dU, self.db, self.dWs, self.dbs], *update)
+
+    def run(self):
+        w = self.w
+        J.janus_childsum_fwd(self.desc, w.trees, self.emb, self.W, self.U, self.b, self.h_root, self.ws)
+        J.janus_embed_softmax_xent(self.xdesc, J.XENT_FWD_BWD, self.labels_host, self.labels, table=self.Ws,
+                                   bias=self.bs, inp=self.h_root, out=self.dh_root, dtable=self.dWs,
+                                   dbias=self.dbs, loss=self.loss, ws=self.xws)
+        J.janus_childsum_bwd(self.desc, w.trees, self.emb, self.W, self.U, self.ws, self.dh_root, self.demb,
+                             self.dW, self.dU, self.db)
+        if self.update is not None:
+            self.update.apply()
+
+    def results(self) -> Dict[str, object]:
+        torch.cuda.synchronize()
+        return dict(loss=float(self.loss.item()), h_root=_f64(self.h_root), dh_root=_f64(self.dh_root),
+                    demb=_f64(self.demb), dW=_f64(self.dW), dU=_f64(self.dU), db=_f64(self.db),
+                    dWs=_f64(self.dWs), dbs=_f64(self.dbs))
+
+
 def make_step(w, device="cuda", update: Optional[Tuple[float, float]] = None):
     """The training step of a workload; ``update`` = (lr, max_norm) appends
     the SGD update with global-norm clipping."""
     if isinstance(w, wl.TreeRNNWorkload):
         return TreeRNNStep(w, device, update=update)
+    if isinstance(w, wl.ChildSumWorkload):
+        return ChildSumStep(w, device, update=update)
     if isinstance(w, wl.TreeWorkload):
         return TreeStep(w, device, update=update)
     return LSTMStep(w, device, update=update)

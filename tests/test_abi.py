@@ -361,3 +361,46 @@ def test_treernn_needs_equal_embedding_and_hidden_width():
                     np.array([3, -1, -1], np.int32), np.array([2], np.int32))[0]   # a node with one child
     st = L.janus_treernn_fwd(C.byref(d), C.byref(bad), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, 1 << 20, None)
     assert st == J.ERR_TREE
+
+
+@pytest.mark.parametrize("case,status", [
+    ("ok_but_no_ws", J.ERR_WORKSPACE), ("offset0", J.ERR_TREE), ("decreasing", J.ERR_TREE),
+    ("child_range", J.ERR_TREE), ("two_parents", J.ERR_TREE), ("root_has_parent", J.ERR_TREE),
+    ("cycle", J.ERR_TREE), ("unreachable", J.ERR_TREE), ("word", J.ERR_TOKEN), ("empty", J.ERR_INVALID_ARG)])
+def test_childsum_rejects_malformed_batches(case, status):
+    """Validation of the child-list trees happens before any device work."""
+    L = J.lib()
+    d = J.TreeDesc(8, 4, 10, J.F32)
+    # tree 0: 0 -> (1, 2), 2 -> (3);  tree 1: 4 (a single node)
+    off, kids, word, root = [0, 2, 2, 3, 3, 3], [1, 2, 3], [1, 2, 3, 4, 5], [0, 4]
+    if case == "offset0":
+        off = [1, 2, 2, 3, 3, 4]
+    elif case == "decreasing":
+        off = [0, 2, 1, 3, 3, 3]
+    elif case == "child_range":
+        kids = [1, 9, 3]
+    elif case == "two_parents":
+        kids = [1, 2, 1]
+    elif case == "root_has_parent":
+        kids = [1, 2, 4]
+    elif case == "cycle":
+        off, kids, word, root = [0, 1, 2, 3], [1, 2, 1], [1, 2, 3], [0]   # 1 -> 2 -> 1 hangs off the root
+    elif case == "unreachable":
+        root = [0]
+    elif case == "word":
+        word = [1, 2, 3, 10, 5]
+    elif case == "empty":
+        off, kids, word, root = [0], [], [], []
+    arrs = [np.ascontiguousarray(a, dtype=np.int32) for a in (off, kids or [0], word or [0], root or [0])]
+    tb = J.NaryBatchC(len(root), len(word), *[a.ctypes.data_as(C.POINTER(C.c_int32)) for a in arrs])
+    st = L.janus_childsum_fwd(C.byref(d), C.byref(tb), 0x1000, 0x2000, 0x3000, 0x4000, 0x5000, None, 0, None)
+    assert st == status
+
+
+def test_childsum_workspace_bytes():
+    L = J.lib()
+    d = J.TreeDesc(300, 150, 20000, J.F32)
+    a = L.janus_childsum_workspace_bytes(C.byref(d), 100)
+    assert a > 0 and L.janus_childsum_workspace_bytes(C.byref(d), 200) > a
+    d.dtype = J.BF16
+    assert L.janus_childsum_workspace_bytes(C.byref(d), 100) == 0

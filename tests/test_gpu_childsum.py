@@ -1,0 +1,65 @@
+"""GPU parity of the Child-Sum TreeLSTM step (janus_childsum_fwd/bwd plus the
+5-class softmax cross-entropy at the roots) against the float64 oracle
+(oracle/childsum.py), element by element, at the float32 tolerances."""
+import numpy as np
+import pytest
+
+from oracle import steps as oracle_steps
+from paper_1812_01329_amd import workloads as wl
+from tests.parity import TOL, check
+
+pytestmark = pytest.mark.gpu
+
+
+def _run_and_check(w):
+    import torch
+    from paper_1812_01329_amd.train_step import make_step
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    t = w.trees
+    print(f"[childsum] trees={t.num_trees} nodes={t.num_nodes} E={w.E_dim} H={w.H}", flush=True)
+    step = make_step(w)
+    step.run()
+    g = step.results()
+    r = oracle_steps.childsum_step(w)
+    tol = TOL["f32"]
+    check("loss", np.array([g["loss"]]), np.array([r["loss"]]), tol["out"])
+    check("h_root", g["h_root"], r["h_root"], tol["out"])
+    for k in ("dh_root", "dWs", "dbs", "dW", "dU", "db", "demb"):
+        check(k, g[k], r[k], tol["grad"])
+    return g, r
+
+
+def test_childsum_sst_fp32():
+    """25 random trees of 5-50 nodes, a word at every node, E 300, H 150:
+    the dh contraction's K = 4H = 600, the weight contractions' K = the node
+    count."""
+    _run_and_check(wl.sst_childsum())
+
+
+def test_childsum_chains_stars_and_single_nodes():
+    """Chains (one child per node, 40 levels), a star (one root over 40
+    leaves: one level of 40 children), and single-node trees in one batch."""
+    ch = wl.sst_childsum(n_trees=2, E=24, H=32, V=50, seed=81, sizes=[40, 3], chain=True).trees
+    rt = wl.sst_childsum(n_trees=3, E=24, H=32, V=50, seed=82, sizes=[41, 1, 1]).trees
+    # make the first tree of rt a star: every node under the root
+    n = 41
+    kids = list(range(1, n))
+    off = [0, n - 1] + [n - 1] * (n - 1) + [n - 1 + 0, n - 1 + 0]
+    star = wl.NaryTreeBatch(np.asarray(off, np.int32), np.asarray(kids, np.int32), rt.word, rt.root)
+    # concatenate the chain batch after the star batch
+    base = star.num_nodes
+    off2 = np.concatenate([star.child_offsets[:-1], ch.child_offsets + star.child_offsets[-1]]).astype(np.int32)
+    trees = wl.NaryTreeBatch(off2, np.concatenate([star.children, ch.children + base]).astype(np.int32),
+                             np.concatenate([star.word, ch.word]).astype(np.int32),
+                             np.concatenate([star.root, ch.root + base]).astype(np.int32))
+    w = wl.sst_childsum(n_trees=5, E=24, H=32, V=50, seed=83, sizes=[1, 1, 1, 1, 1])
+    labels = np.arange(trees.num_trees, dtype=np.int32) % w.C
+    w = wl.ChildSumWorkload("childsum-edges", w.E_dim, w.H, w.V, w.C, trees, labels, w.emb, w.W, w.U, w.b,
+                            w.Ws, w.bs)
+    _run_and_check(w)
+
+
+def test_childsum_wide_hidden():
+    """H = 320: the level contraction's N = 4H = 1280 columns in 20 blocks,
+    the dh contraction's K = 1280 in two LDS chunks."""
+    _run_and_check(wl.sst_childsum(n_trees=5, E=40, H=320, V=64, seed=84))
