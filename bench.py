@@ -52,11 +52,16 @@ WORKLOADS = {
 }
 
 
+# The sources that define and launch the persistent recurrence kernels, whose
+# HBM counters profiles/ records: a change to any of them voids the record.
+TRAFFIC_SOURCES = ("device.hpp", "lstm.hip", "lstm_persist.hpp")
+
+
 def source_digest() -> str:
     h = hashlib.sha256()
-    for p in sorted(glob.glob(os.path.join(ROOT, "paper_1812_01329_amd", "csrc", "*"))):
-        with open(p, "rb") as f:
-            h.update(os.path.basename(p).encode())
+    for name in TRAFFIC_SOURCES:
+        with open(os.path.join(ROOT, "paper_1812_01329_amd", "csrc", name), "rb") as f:
+            h.update(name.encode())
             h.update(f.read())
     return h.hexdigest()[:16]
 
