@@ -69,28 +69,40 @@ __global__ void embed_fwd_kernel(const T* E, const int32_t* ids, int V, int H, T
 // the block that owns the first occurrence of v (no atomics).
 template <typename T>
 __global__ void embed_bwd_kernel(const T* dx, const int32_t* ids, int rows, int V, int H, float* dE) {
-    extern __shared__ int32_t match[];
+    extern __shared__ int32_t sid[];   // ids[r ..), then in place the rows that match
     __shared__ int nmatch;
     __shared__ int owner;
     const int r = blockIdx.x;
+    const int tid = threadIdx.x, lane = tid & 63;
     const int32_t id = min(max(ids[r], 0), V - 1);
-    if (threadIdx.x == 0) owner = 1;
+    if (tid == 0) owner = 1;
     __syncthreads();
-    for (int q = threadIdx.x; q < r; q += blockDim.x)
-        if (ids[q] == id) owner = 0;
+    for (int q = tid; q < r; q += blockDim.x)
+        if (min(max(ids[q], 0), V - 1) == id) owner = 0;
     __syncthreads();
     if (!owner) return;
-    if (threadIdx.x == 0) {
+    const int n_rest = rows - r;
+    for (int q = tid; q < n_rest; q += blockDim.x) sid[q] = min(max(ids[r + q], 0), V - 1);
+    __syncthreads();
+    if (tid < 64) {
+        // wave 0 compacts the matching rows in ascending order; a chunk is
+        // read before any of its slots is written, and the matches so far
+        // never outnumber the entries read
         int n = 0;
-        for (int q = r; q < rows; ++q)
-            if (min(max(ids[q], 0), V - 1) == id) match[n++] = q;
-        nmatch = n;
+        for (int q0 = 0; q0 < n_rest; q0 += 64) {
+            const int q = q0 + lane;
+            const bool m = q < n_rest && sid[q] == id;
+            const unsigned long long bal = __ballot(m);
+            if (m) sid[n + __popcll(bal & ((1ull << lane) - 1ull))] = r + q;
+            n += __popcll(bal);
+        }
+        if (lane == 0) nmatch = n;
     }
     __syncthreads();
     const int n = nmatch;
-    for (int j = threadIdx.x; j < H; j += blockDim.x) {
+    for (int j = tid; j < H; j += blockDim.x) {
         float s = 0.f;
-        for (int k = 0; k < n; ++k) s += to_f(dx[int64_t(match[k]) * H + j]);
+        for (int k = 0; k < n; ++k) s += to_f(dx[int64_t(sid[k]) * H + j]);
         dE[int64_t(id) * H + j] = s;
     }
 }
