@@ -94,7 +94,7 @@ def test_closed_form_constant_gates():
         c = i * g * (1 - f ** t) / (1 - f)
         np.testing.assert_allclose(y[t - 1], np.full((B, H), o * np.tanh(c)), rtol=0, atol=1e-14)
     np.testing.assert_allclose(cT, i * g * (1 - f ** T) / (1 - f), atol=1e-14)
-    # the special case of the survey: only b_g nonzero -> c_t = tanh(b)(1 - 2^-t)
+    # closed form: only b_g nonzero -> c_t = tanh(b)(1 - 2^-t)
     b2 = np.zeros(4 * H); b2[2 * H:3 * H] = 0.9
     _, _, c2, _ = lstm.layer_forward(x, None, np.zeros((4 * H, I)), np.zeros((4 * H, H)), b2)
     np.testing.assert_allclose(c2, np.tanh(0.9) * (1 - 2.0 ** -T), atol=1e-14)
