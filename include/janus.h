@@ -89,7 +89,7 @@ size_t janus_lstm_workspace_bytes(const janus_lstm_desc* d);
  *           a length-0 sequence).
  *  ws       workspace (see conventions); the forward keeps activations there.
  *
- * Errors: NULL d/x/Wx/Wh/b/y/ws or a non-positive L, I, H, B, or T < 0
+ * Errors: NULL d/Wx/Wh/b/ws, NULL x or y with T > 0, a non-positive L, I, H, B, or T < 0
  * -> INVALID_ARG; a length outside [0, T] -> LENGTH; ws_bytes too small ->
  * WORKSPACE; dtype not F32/BF16 -> UNSUPPORTED.
  */

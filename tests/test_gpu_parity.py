@@ -136,10 +136,39 @@ def test_multi_tile_varlen(dtype):
     compare_lstm(g, oracle_steps.lstm_step(w), dtype)
 
 
-def test_one_step_sequences():
-    w = _lstm("sumsq", "f32", L=1, I=8, H=16, B=3, T=1, seed=5, h0=True)
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_one_step_sequences(dtype):
+    w = _lstm("sumsq", dtype, L=1, I=8, H=16, B=3, T=1, seed=5, h0=True)
     _, g = _run(w)
-    compare_lstm(g, oracle_steps.lstm_step(w), "f32")
+    compare_lstm(g, oracle_steps.lstm_step(w), dtype)
+
+
+@pytest.mark.parametrize("dtype", ["f32", "bf16"])
+def test_zero_steps(dtype):
+    """T = 0: no step runs, hT = h0 and cT = c0; the loss gradient passes
+    straight back to dh0, dc0 is 0 and every weight gradient is 0."""
+    w = _lstm("sumsq", dtype, L=2, I=8, H=32, B=4, T=0, seed=6, h0=True)
+    _, g = _run(w)
+    r = oracle_steps.lstm_step(w)
+    compare_lstm(g, r, dtype, with_dx=False)
+    assert np.array_equal(g["hT"], w.h0.astype(np.float64)) and np.array_equal(g["cT"], w.c0.astype(np.float64))
+    for k in ("dWx", "dWh", "db"):
+        for t in g[k]:
+            assert not t.any()
+
+
+def test_large_batch_bf16():
+    """B = 300 rows exceed one 256-row pass of the persistent kernels, so
+    the bf16 recurrence takes the per-step kernels."""
+    from paper_1812_01329_amd import janus as J
+    rng = np.random.default_rng(8)
+    w = _lstm("mean_final", "bf16", L=2, I=40, H=64, B=300, T=6, lengths=rng.integers(0, 7, 300), seed=8,
+              h0=True)
+    J.janus_trace_begin()
+    _, g = _run(w)
+    labels = {r["label"] for r in J.janus_trace_end()}
+    assert "lstm_fwd_persistent" not in labels, labels
+    compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
 
 
 def test_single_leaf_and_chain_trees():
