@@ -21,17 +21,30 @@ namespace {
 // read as broadcasts; each lane owns one column and streams its B entries
 // from the L2 (every row block reads the same B), 16 loads in flight.  The
 // waves' partial sums are added through LDS in wave order.  Epilogues: rows
-// of C (+ bias), or the backward's [dh_L; dh_R], whose two halves go to the
-// rows of the two children.
+// of C (+ bias); the backward's [dh_L; dh_R], whose two halves go to the
+// rows of the two children; or (TreeRNN forward) h = tanh(. + bias), saved
+// in C and sent to the parent's [h_L; h_R] row or to h_root.  With
+// kSimtTanhGrad the a slab is da = a (1 - s^2) for a second operand s of
+// a's layout (TreeRNN backward: dh and h), and column block 0 also stores da.
 constexpr int kSimtRows = 8, kSimtCols = 64, kSimtWaves = 8, kSimtKc = 1024;
-enum SimtEpi { kSimtStore = 0, kSimtChildren = 1 };
+enum SimtEpi { kSimtStore = 0, kSimtChildren = 1, kSimtTanhSend = 2 };
+enum SimtAMode { kSimtPlain = 0, kSimtTanhGrad = 1 };
 
-template <bool AT, int EPI>
+// operands of the TreeRNN epilogue and a-transform
+struct SimtExtra {
+    float* HLR = nullptr;        // kSimtTanhSend: [h_L; h_R] rows of internal nodes
+    float* root = nullptr;       //                h_root
+    int M0 = 0;                  //                first internal position
+    const float* S = nullptr;    // kSimtTanhGrad: h, same layout as a
+    float* D = nullptr;          //                da out, same layout as a
+};
+
+template <bool AT, int EPI, int AMODE = kSimtPlain>
 __global__ __launch_bounds__(64 * kSimtWaves) void simt_gemm_kernel(int M, int N, int K, const float* A, int64_t lda,
                                                                     const int32_t* a_idx, const float* B, int64_t ldb,
                                                                     const int32_t* b_idx, const float* bias, float* C,
                                                                     int64_t ldc, const int32_t* lchild,
-                                                                    const int32_t* rchild, int H) {
+                                                                    const int32_t* rchild, int H, SimtExtra x) {
     __shared__ __align__(16) float sA[kSimtKc][kSimtRows];
     __shared__ float red[kSimtWaves][kSimtRows][kSimtCols];
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -50,8 +63,16 @@ __global__ __launch_bounds__(64 * kSimtWaves) void simt_gemm_kernel(int M, int N
             const int m = m0 + r;
             float v = 0.f;
             if (m < M && kk < kc) {
-                if (AT) v = A[int64_t(k0 + kk) * lda + m];
-                else v = A[(a_idx ? int64_t(a_idx[m]) : int64_t(m)) * lda + k0 + kk];
+                if constexpr (AMODE == kSimtTanhGrad) {
+                    const int64_t o = int64_t(m) * lda + k0 + kk;
+                    const float h = x.S[o];
+                    v = A[o] * (1.f - h * h);
+                    if (blockIdx.x == 0) x.D[o] = v;
+                } else if (AT) {
+                    v = A[int64_t(k0 + kk) * lda + m];
+                } else {
+                    v = A[(a_idx ? int64_t(a_idx[m]) : int64_t(m)) * lda + k0 + kk];
+                }
             }
             sA[kk][r] = v;
         }
@@ -78,7 +99,14 @@ __global__ __launch_bounds__(64 * kSimtWaves) void simt_gemm_kernel(int M, int N
     float sum = 0.f;
 #pragma unroll
     for (int w = 0; w < kSimtWaves; ++w) sum += red[w][r][lane];
-    if constexpr (EPI == kSimtChildren) {
+    if constexpr (EPI == kSimtTanhSend) {
+        // lchild / rchild carry the parent slot and the tree index of each row
+        const float h = tanhf_(sum + bias[n]);
+        C[int64_t(m) * ldc + n] = h;
+        const int par = lchild[m];
+        if (par >= 0) x.HLR[int64_t((par >> 1) - x.M0) * 2 * N + (par & 1) * N + n] = h;
+        else x.root[int64_t(rchild[m]) * N + n] = h;
+    } else if constexpr (EPI == kSimtChildren) {
         if (n < H) C[int64_t(lchild[m]) * H + n] = sum;
         else C[int64_t(rchild[m]) * H + n - H] = sum;
     } else {
@@ -86,15 +114,16 @@ __global__ __launch_bounds__(64 * kSimtWaves) void simt_gemm_kernel(int M, int N
     }
 }
 
-template <bool AT, int EPI>
+template <bool AT, int EPI, int AMODE = kSimtPlain>
 janus_status simt_gemm(const char* label, int M, int N, int K, const float* A, int64_t lda, const int32_t* a_idx,
                        const float* B, int64_t ldb, const int32_t* b_idx, const float* bias, float* C, int64_t ldc,
-                       hipStream_t st, const int32_t* lchild = nullptr, const int32_t* rchild = nullptr, int H = 0) {
+                       hipStream_t st, const int32_t* lchild = nullptr, const int32_t* rchild = nullptr, int H = 0,
+                       SimtExtra x = SimtExtra()) {
     if (M <= 0 || N <= 0) return JANUS_OK;
     dim3 grid(unsigned((N + kSimtCols - 1) / kSimtCols), unsigned((M + kSimtRows - 1) / kSimtRows));
     TraceScope trace(label, 2.0 * M * N * double(K), 4.0 * (double(M) * K + double(K) * N + double(M) * N), st);
-    hipLaunchKernelGGL((simt_gemm_kernel<AT, EPI>), grid, dim3(64 * kSimtWaves), 0, st, M, N, K, A, lda, a_idx, B,
-                       ldb, b_idx, bias, C, ldc, lchild, rchild, H);
+    hipLaunchKernelGGL((simt_gemm_kernel<AT, EPI, AMODE>), grid, dim3(64 * kSimtWaves), 0, st, M, N, K, A, lda, a_idx,
+                       B, ldb, b_idx, bias, C, ldc, lchild, rchild, H, x);
     JANUS_LAUNCH_CHECK();
     return JANUS_OK;
 }

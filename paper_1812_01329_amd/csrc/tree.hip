@@ -281,9 +281,10 @@ janus_status prepare(const janus_treelstm_desc* d, const janus_tree_batch* t, vo
 // Binary TreeRNN on the same frontier schedule: a leaf's h is its word
 // vector (embedding width = H), an internal node h = tanh(W [h_L; h_R] + b).
 // Forward: the leaves copy their embedding rows into their parents' [h_L;
-// h_R] rows; each internal level is one contraction with W^T (bias in its
-// epilogue) and a pointwise tanh that saves h and sends it to the parent.
-// Backward, levels from the top down: da = dh (1 - h^2), then
+// h_R] rows; each internal level is one contraction with W^T whose epilogue
+// adds the bias, applies tanh, saves h and sends it to the parent.
+// Backward, levels from the top down, one contraction per level: its a slab
+// is da = dh (1 - h^2) (column block 0 also stores da) and its epilogue sends
 // [dh_L; dh_R] = da W to the two children; after the loop dW = da^T HLR and
 // db = column sums of da over the internal nodes, and the leaves' dh is the
 // gradient of their word vectors.
@@ -332,25 +333,6 @@ __global__ void treernn_leaf_kernel(int rows, int H, int M0, const int32_t* lwor
     const float h = emb[int64_t(lword[p]) * H + j];
     Hn[i] = h;
     rnn_send(p, j, H, M0, h, parent, rootk, HLR, h_root);
-}
-
-__global__ void treernn_fwd_point_kernel(int p0, int rows, int H, int M0, const float* A, const int32_t* parent,
-                                         const int32_t* rootk, float* Hn, float* HLR, float* h_root) {
-    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= int64_t(rows) * H) return;
-    const int p = p0 + int(i / H), j = int(i % H);
-    const float h = tanhf_(A[int64_t(p) * H + j]);
-    Hn[int64_t(p) * H + j] = h;
-    rnn_send(p, j, H, M0, h, parent, rootk, HLR, h_root);
-}
-
-// da = dh (1 - h^2) over the rows of one level
-__global__ void treernn_bwd_point_kernel(int p0, int rows, int H, const float* Hn, const float* dh, float* dA) {
-    const int64_t i = int64_t(blockIdx.x) * blockDim.x + threadIdx.x;
-    if (i >= int64_t(rows) * H) return;
-    const int64_t o = int64_t(p0) * H + i;
-    const float h = Hn[o];
-    dA[o] = dh[o] * (1.f - h * h);
 }
 
 janus_status check_rnn(const janus_treelstm_desc* d) {
@@ -518,17 +500,18 @@ extern "C" janus_status janus_treernn_fwd(const janus_treernn_desc* d, const jan
                            w.s.lword, static_cast<const float*>(emb), w.s.parent, w.s.rootk, w.Hn, w.HLR, hr);
         JANUS_LAUNCH_CHECK();
     }
+    SimtExtra send;
+    send.HLR = w.HLR;
+    send.root = hr;
+    send.M0 = M0;
     for (int k = 1; k < s.num_levels; ++k) {
         const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
-        e = simt_gemm<false, kSimtStore>("treernn_level_gemm", rows, H, 2 * H, w.HLR + int64_t(p0 - M0) * 2 * H,
-                                         2 * H, nullptr, w.Wt, H, nullptr, static_cast<const float*>(b),
-                                         w.A + int64_t(p0) * H, H, st);
+        // h = tanh([h_L; h_R] W^T + b), saved and sent on (parent slot and tree
+        // index of each row through the epilogue's index arguments)
+        e = simt_gemm<false, kSimtTanhSend>("treernn_level", rows, H, 2 * H, w.HLR + int64_t(p0 - M0) * 2 * H, 2 * H,
+                                            nullptr, w.Wt, H, nullptr, static_cast<const float*>(b),
+                                            w.Hn + int64_t(p0) * H, H, st, w.s.parent + p0, w.s.rootk + p0, H, send);
         if (e != JANUS_OK) return e;
-        const int64_t n = int64_t(rows) * H;
-        TraceScope trace("treernn_fwd_point", 0.0, 12.0 * n, st);
-        hipLaunchKernelGGL(treernn_fwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows, H,
-                           M0, w.A, w.s.parent, w.s.rootk, w.Hn, w.HLR, hr);
-        JANUS_LAUNCH_CHECK();
     }
     return JANUS_OK;
 }
@@ -556,17 +539,15 @@ extern "C" janus_status janus_treernn_bwd(const janus_treernn_desc* d, const jan
     }
     for (int k = s.num_levels - 1; k >= 1; --k) {
         const int p0 = s.level_offsets[k], rows = s.level_offsets[k + 1] - p0;
-        const int64_t n = int64_t(rows) * H;
-        {
-            TraceScope trace("treernn_bwd_point", 0.0, 12.0 * n, st);
-            hipLaunchKernelGGL(treernn_bwd_point_kernel, dim3(unsigned((n + 255) / 256)), dim3(256), 0, st, p0, rows,
-                               H, w.Hn, w.dh, w.A);
-            JANUS_LAUNCH_CHECK();
-        }
+        // da = dh (1 - h^2) as the a slab (stored by column block 0), and
         // [dh_L; dh_R] = da W to the children (W rows are N = 2H contiguous)
-        e = simt_gemm<false, kSimtChildren>("treernn_dh_gemm", rows, 2 * H, H, w.A + int64_t(p0) * H, H, nullptr,
-                                            static_cast<const float*>(W), 2 * H, nullptr, nullptr, w.dh, 0, st,
-                                            w.s.lchild + p0, w.s.rchild + p0, H);
+        SimtExtra tg;
+        tg.S = w.Hn + int64_t(p0) * H;
+        tg.D = w.A + int64_t(p0) * H;
+        e = simt_gemm<false, kSimtChildren, kSimtTanhGrad>("treernn_level_bwd", rows, 2 * H, H, w.dh + int64_t(p0) * H,
+                                                           H, nullptr, static_cast<const float*>(W), 2 * H, nullptr,
+                                                           nullptr, w.dh, 0, st, w.s.lchild + p0, w.s.rchild + p0, H,
+                                                           tg);
         if (e != JANUS_OK) return e;
     }
     // dW = da_int^T HLR  (K = internal nodes), db = column sums of da_int
