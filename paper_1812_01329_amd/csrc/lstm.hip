@@ -254,14 +254,20 @@ int persist_fwd_slices(const janus_lstm_desc& d) {
     return persist_fwd_fits(d, forced, info) ? forced : 0;
 }
 
-// Slices of the persistent backward: 8 where the layout fits (half the
-// operand traffic per CU of 4 slices), else 4; 0 when neither fits.
-// JANUS_BWD_SLICES=4 or 8 asks for one of them only.
+// Slices of the persistent backward.  8 slices halve each workgroup's
+// share of the dG stream but double the partial sums it exchanges; they pay
+// where the per-step dG slot (B x 4H bf16) is large, 2 MB and up (0.5 ms of
+// a 35 ms step at H = 2048, B = 256), and 4 slices are faster below (PTB,
+// B 20: 0.55 against 0.66 ms of backward per step; B 128, H 1024: 1.48
+// against 1.55 ms).  The other count is taken when the preferred one does
+// not fit; 0 when neither does.  JANUS_BWD_SLICES=4 or 8 asks for one of
+// them only.
 int persist_bwd_slices(const janus_lstm_desc& d) {
     const DeviceInfo info = device_info();
     const char* e = getenv("JANUS_BWD_SLICES");
     const int forced = (e && e[0] == '4') ? 4 : (e && e[0] == '8') ? 8 : 0;
-    for (int ns : {8, 4}) {
+    const bool big = int64_t(d.B) * 4 * d.H * 2 >= (int64_t(2) << 20);
+    for (int ns : {big ? 8 : 4, big ? 4 : 8}) {
         if (forced && ns != forced) continue;
         if (persist_bwd_fits(d, ns, info)) return ns;
     }
