@@ -498,6 +498,254 @@ __global__ __launch_bounds__(Cfg::NT) void bwd_step_kernel(BwdStep<T> a) {
     }
 }
 
+// ------------------------------------------------- one-workgroup recurrence
+// A problem whose recurrent weights fit one CU's LDS (as float32) runs the
+// whole time loop of a layer in one workgroup: Wh, h and c (forward) or
+// dG_{t+1}, dh and dc (backward) stay in LDS, and steps are separated by
+// workgroup barriers instead of kernel launches.  The state of step t and
+// t + 1 sits in two LDS buffers used in turn, so a step needs one barrier
+// and no cell holds its result in registers across it.  Work item j of a
+// step takes cell (row, unit) j / S and the terms k = j % S (mod S) of its
+// contraction; the S adjacent lanes of a cell add their parts with shuffles
+// in a fixed order, so a cell's four gates meet in one lane and the cell
+// update needs no exchange.  Weight rows are S floats longer than their
+// length, which puts the S parts of the 64 / S cells of a wave in distinct
+// LDS banks.  The operands of a step that do not depend on the recurrence
+// (the input projection; the saved gates, cell states and dy) are loaded
+// one step ahead, across the barrier.  The values the step kernels pass
+// between steps through memory in T (h, dG) are rounded to T here too, and
+// every buffer the step kernels write is written.
+constexpr int kSmallThreads = 1024;
+constexpr int kSmallCells = 8;   // cells per thread at most: B H <= 8192
+
+template <int S>
+__device__ __forceinline__ float small_group_sum(float v) {
+#pragma unroll
+    for (int m = 1; m < S; m <<= 1) v += __shfl_xor(v, m);
+    return v;
+}
+
+template <typename T>
+struct FwdSmall {
+    int H, B, t_eff, fixed;
+    const int32_t* active;
+    const int32_t* offsets;
+    int64_t ldh, ldg;
+    const T* Wh;
+    const T* XG;
+    T* Hs;
+    float* Cs;
+    T* Gs;
+    T* y;
+    const int32_t* perm;
+    float* hT;
+    float* cT;
+};
+
+template <typename T, int S>
+__global__ __launch_bounds__(kSmallThreads) void fwd_small_kernel(FwdSmall<T> a) {
+    extern __shared__ float smem_f[];
+    const int H = a.H, B = a.B, ldw = H + S, BH = B * H;
+    float* Wl = smem_f;              // [4H][H + S]: row k = gate-major row k of Wh
+    float* hl = Wl + 4 * H * ldw;    // [2][B][H]: h of steps t - 1 and t, in turn
+    float* cl = hl + 2 * BH;         // [2][B][H]
+    const int tid = threadIdx.x, part = tid % S;
+    for (int i = tid; i < 4 * H * H; i += kSmallThreads) Wl[(i / H) * ldw + i % H] = to_f(a.Wh[i]);
+    for (int i = tid; i < BH; i += kSmallThreads) {
+        const int r = i / H, u = i % H;
+        hl[i] = to_f(a.Hs[int64_t(r) * a.ldh + u]);
+        cl[i] = a.Cs[int64_t(r) * a.ldh + u];
+    }
+    // input projection of cell i of step t (lane part 0 only)
+    auto load_x = [&](int64_t off, int i, float* x) {
+        const T* xg = a.XG + (off + i / H) * a.ldg + i % H;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) x[g] = to_f(xg[g * H]);
+    };
+    float xpre[4] = {0.f, 0.f, 0.f, 0.f};   // of the first cell of this thread, one step ahead
+    if (part == 0 && tid / S < persist::act_at(a.active, a.fixed, B, 0, a.t_eff) * H)
+        load_x(persist::off_at(a.offsets, a.fixed, B, 0), tid / S, xpre);
+    __syncthreads();
+    for (int t = 0; t < a.t_eff; ++t) {
+        const int act = persist::act_at(a.active, a.fixed, B, t, a.t_eff);
+        const int act_next = persist::act_at(a.active, a.fixed, B, t + 1, a.t_eff);
+        const int64_t off = persist::off_at(a.offsets, a.fixed, B, t);
+        const float* hp = hl + (t & 1) * BH;
+        const float* cp = cl + (t & 1) * BH;
+        float* hn = hl + ((t + 1) & 1) * BH;
+        float* cn = cl + ((t + 1) & 1) * BH;
+        // rows past act stop here for good, so their slots are never read again
+        for (int j = tid; j / S < act * H; j += kSmallThreads) {   // uniform over a cell's S lanes
+            const int i = j / S, r = i / H, u = i % H;
+            const int64_t p = off + r;
+            float x[4] = {xpre[0], xpre[1], xpre[2], xpre[3]};
+            if (part == 0 && j != tid) load_x(off, i, x);
+            const float* hr = hp + r * H;
+            const float *wi = Wl + u * ldw, *wf = Wl + (H + u) * ldw;
+            const float *wg = Wl + (2 * H + u) * ldw, *wo = Wl + (3 * H + u) * ldw;
+            float ai = 0.f, af = 0.f, ag = 0.f, ao = 0.f;
+#pragma unroll 4
+            for (int k = part; k < H; k += S) {
+                const float hk = hr[k];
+                ai += hk * wi[k];
+                af += hk * wf[k];
+                ag += hk * wg[k];
+                ao += hk * wo[k];
+            }
+            ai = small_group_sum<S>(ai);
+            af = small_group_sum<S>(af);
+            ag = small_group_sum<S>(ag);
+            ao = small_group_sum<S>(ao);
+            if (part == 0) {
+                const float gi = sigmoidf_(ai + x[0]), gf = sigmoidf_(af + x[1]);
+                const float gg = tanhf_(ag + x[2]), go = sigmoidf_(ao + x[3]);
+                const float c = gf * cp[i] + gi * gg;
+                const float h = go * tanhf_(c);
+                const T hq = from_f<T>(h);
+                hn[i] = to_f(hq);
+                cn[i] = c;
+                a.Cs[(a.B + p) * a.ldh + u] = c;
+                a.Hs[(a.B + p) * a.ldh + u] = hq;
+                T* gs = a.Gs + p * a.ldg + u;
+                gs[0] = from_f<T>(gi);
+                gs[H] = from_f<T>(gf);
+                gs[2 * H] = from_f<T>(gg);
+                gs[3 * H] = from_f<T>(go);
+                const int b = a.perm ? a.perm[r] : r;
+                if (a.y) a.y[(int64_t(t) * B + b) * H + u] = hq;
+                if (r >= act_next) {   // last step of this sequence
+                    if (a.hT) a.hT[int64_t(b) * H + u] = h;
+                    if (a.cT) a.cT[int64_t(b) * H + u] = c;
+                }
+            }
+        }
+        if (part == 0 && tid / S < act_next * H) load_x(persist::off_at(a.offsets, a.fixed, B, t + 1), tid / S, xpre);
+        __syncthreads();   // step t + 1 reads what step t wrote
+    }
+}
+
+template <typename T>
+struct BwdSmall {
+    int H, B, t_eff, fixed;
+    const int32_t* active;
+    const int32_t* offsets;
+    int64_t ldh, ldg;
+    const T* Wh;
+    T* G;                     // dG rows of every step (for the contractions after the loop)
+    const T* Gs;
+    const float* Cs;
+    const T* dy;
+    int64_t dy_ld;
+    const int32_t* dy_rows;
+    const float* dh;          // initial dh, dc of the sorted rows (from dhT, dcT)
+    const float* dc;
+    const int32_t* perm;
+    float* dh0;
+    float* dc0;
+};
+
+template <typename T, int S>
+__global__ __launch_bounds__(kSmallThreads) void bwd_small_kernel(BwdSmall<T> a) {
+    extern __shared__ float smem_f[];
+    const int H = a.H, B = a.B, G4 = 4 * H, ldk = G4 + S, BH = B * H;
+    float* Wt = smem_f;              // [H][4H + S]: Wt[u][k] = Wh[k][u]
+    float* gl = Wt + H * ldk;        // [2][B][4H]: dG of steps t + 1 and t, in turn
+    float* dcl = gl + 2 * B * G4;    // [2][B][H]
+    float* dhl = dcl + 2 * BH;       // [B][H]: dh of rows not yet started
+    const int tid = threadIdx.x, part = tid % S;
+    for (int i = tid; i < G4 * H; i += kSmallThreads) Wt[(i % H) * ldk + i / H] = to_f(a.Wh[i]);
+    // a row's dc enters from either buffer at the step its sequence ends
+    for (int i = tid; i < BH; i += kSmallThreads) {
+        dhl[i] = a.dh[i];
+        dcl[i] = dcl[BH + i] = a.dc[i];
+    }
+    // saved gates, c_t, c_{t-1} and dy of cell i of step t (lane part 0 only)
+    auto load_ops = [&](int t, int i, float* v) {
+        const int r = i / H, u = i % H;
+        const int64_t p = persist::off_at(a.offsets, a.fixed, B, t) + r;
+        const int64_t prev_base = t == 0 ? 0 : int64_t(B) + persist::off_at(a.offsets, a.fixed, B, t - 1);
+        const T* gs = a.Gs + p * a.ldg + u;
+#pragma unroll
+        for (int g = 0; g < 4; ++g) v[g] = to_f(gs[g * H]);
+        v[4] = a.Cs[(a.B + p) * a.ldh + u];
+        v[5] = a.Cs[(prev_base + r) * a.ldh + u];
+        v[6] = a.dy ? to_f(a.dy[(a.dy_rows ? int64_t(a.dy_rows[p]) : p) * a.dy_ld + u]) : 0.f;
+    };
+    float pre[7] = {0.f, 0.f, 0.f, 0.f, 0.f, 0.f, 0.f};   // of the first cell of this thread, one step ahead
+    if (part == 0 && a.t_eff > 0 && tid / S < persist::act_at(a.active, a.fixed, B, a.t_eff - 1, a.t_eff) * H)
+        load_ops(a.t_eff - 1, tid / S, pre);
+    __syncthreads();
+    // dh of cell i = (r, u): sum_k dG_{t+1}[r, k] Wh[k, u] over the S parts
+    // for a row that ran at t + 1, else the carried dh (all lanes of a cell
+    // take the same branch)
+    auto dh_of = [&](const float* gnext, int i, int act_next) -> float {
+        const int r = i / H, u = i % H;
+        if (r >= act_next) return dhl[i];
+        const float* gr = gnext + r * G4;
+        const float* wr = Wt + u * ldk;
+        float s0 = 0.f, s1 = 0.f;
+        int k = part;
+#pragma unroll 2
+        for (; k + S < G4; k += 2 * S) {
+            s0 += gr[k] * wr[k];
+            s1 += gr[k + S] * wr[k + S];
+        }
+        if (k < G4) s0 += gr[k] * wr[k];
+        return small_group_sum<S>(s0 + s1);
+    };
+    int cur = 0;   // buffer that holds dG_{t+1} and dc_{t+1}
+    for (int t = a.t_eff - 1; t >= 0; --t, cur ^= 1) {
+        const int act = persist::act_at(a.active, a.fixed, B, t, a.t_eff);
+        const int act_next = persist::act_at(a.active, a.fixed, B, t + 1, a.t_eff);
+        const int64_t off = persist::off_at(a.offsets, a.fixed, B, t);
+        const float* gc = gl + cur * B * G4;
+        const float* dcc = dcl + cur * BH;
+        float* gn = gl + (cur ^ 1) * B * G4;
+        float* dcn = dcl + (cur ^ 1) * BH;
+        for (int j = tid; j / S < act * H; j += kSmallThreads) {
+            const int i = j / S, r = i / H, u = i % H;
+            const int64_t p = off + r;
+            float v[7];
+#pragma unroll
+            for (int e = 0; e < 7; ++e) v[e] = pre[e];
+            if (part == 0 && j != tid) load_ops(t, i, v);
+            const float dhv = dh_of(gc, i, act_next) + v[6];
+            if (part == 0) {
+                const float gi = v[0], gf = v[1], gg = v[2], go = v[3], c = v[4], cprev = v[5];
+                const float tau = tanhf_(c);
+                const float d_o = dhv * tau;
+                const float dct = dcc[i] + dhv * go * (1.f - tau * tau);
+                dcn[i] = dct * gf;
+                const float dg[4] = {dct * gg * gi * (1.f - gi), dct * cprev * gf * (1.f - gf),
+                                     dct * gi * (1.f - gg * gg), d_o * go * (1.f - go)};
+                T* gp = a.G + p * a.ldg + u;
+#pragma unroll
+                for (int g = 0; g < 4; ++g) {
+                    const T q = from_f<T>(dg[g]);
+                    gp[g * H] = q;
+                    gn[r * G4 + g * H + u] = to_f(q);
+                }
+            }
+        }
+        if (part == 0 && t > 0 && tid / S < persist::act_at(a.active, a.fixed, B, t - 1, a.t_eff) * H)
+            load_ops(t - 1, tid / S, pre);
+        __syncthreads();   // step t - 1 reads what step t wrote
+    }
+    // gradient of the initial state
+    const int act0 = persist::act_at(a.active, a.fixed, B, 0, a.t_eff);
+    const float* gc = gl + cur * B * G4;
+    const float* dcc = dcl + cur * BH;
+    for (int j = tid; j / S < BH; j += kSmallThreads) {
+        const int i = j / S, r = i / H, u = i % H;
+        const float dhv = dh_of(gc, i, act0);
+        if (part == 0) {
+            const int b = a.perm ? a.perm[r] : r;
+            if (a.dh0) a.dh0[int64_t(b) * H + u] = dhv;
+            if (a.dc0) a.dc0[int64_t(b) * H + u] = dcc[i];
+        }
+    }
+}
+
 // bf16: 128 rows x 32 columns per tile, 4 waves of 32x32
 using StepBF16 = TileCfg<bf16_t, 128, 32, 32, 4, 1>;
 // fp32: 64 rows x 32 columns per tile, 2 waves of 32x32
@@ -535,6 +783,73 @@ janus_status launch_bwd_step(const BwdStep<T>& a, bool al, hipStream_t s) {
         hipLaunchKernelGGL((bwd_step_kernel<T, Cfg, false>), grid, dim3(Cfg::NT), step_smem<Cfg>(), s, a);
     JANUS_LAUNCH_CHECK();
     return JANUS_OK;
+}
+
+// lanes per cell of a one-workgroup kernel whose contraction has K terms:
+// a power of two, as many as the threads allow while each lane keeps at
+// least 32 terms (fewer leave the lanes waiting on LDS latency more than
+// the split saves), at most 8
+int small_split(const janus_lstm_desc& d, int K) {
+    int S = 1;
+    while (S < 8 && int64_t(d.B) * d.H * (2 * S) <= kSmallThreads && K >= 64 * S) S *= 2;
+    return S;
+}
+int small_fwd_split(const janus_lstm_desc& d) { return small_split(d, d.H); }
+int small_bwd_split(const janus_lstm_desc& d) { return small_split(d, 4 * d.H); }
+
+size_t small_fwd_lds(const janus_lstm_desc& d) {
+    return sizeof(float) * (size_t(4) * d.H * (d.H + small_fwd_split(d)) + size_t(4) * d.B * d.H);
+}
+size_t small_bwd_lds(const janus_lstm_desc& d) {
+    return sizeof(float) * (size_t(d.H) * (4 * d.H + small_bwd_split(d)) + size_t(11) * d.B * d.H);
+}
+
+// The one-workgroup recurrence replaces the per-step kernels (it is never
+// taken where the persistent path applies) when every cell has a thread
+// slot and Wh (float32), the state and dG fit one workgroup's LDS.
+// JANUS_SMALL=0 switches it off.
+bool use_small(const janus_lstm_desc& d) {
+    const char* e = getenv("JANUS_SMALL");
+    if (e && e[0] == '0') return false;
+    if (int64_t(d.B) * d.H > int64_t(kSmallThreads) * kSmallCells) return false;
+    const size_t cap = device_lds(device_info());
+    return small_fwd_lds(d) <= cap && small_bwd_lds(d) <= cap;
+}
+
+template <class K, class A>
+janus_status small_launch(K kernel, size_t smem, const A& args, hipStream_t st, size_t& attr_smem) {
+    if (smem > attr_smem) {
+        JANUS_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
+                                      int(smem)));
+        attr_smem = smem;
+    }
+    hipLaunchKernelGGL(kernel, dim3(1), dim3(kSmallThreads), smem, st, args);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+template <typename T>
+janus_status launch_fwd_small(const janus_lstm_desc& d, const FwdSmall<T>& a, hipStream_t st) {
+    static size_t attr[4] = {};
+    const size_t smem = small_fwd_lds(d);
+    switch (small_fwd_split(d)) {
+        case 1: return small_launch(fwd_small_kernel<T, 1>, smem, a, st, attr[0]);
+        case 2: return small_launch(fwd_small_kernel<T, 2>, smem, a, st, attr[1]);
+        case 4: return small_launch(fwd_small_kernel<T, 4>, smem, a, st, attr[2]);
+        default: return small_launch(fwd_small_kernel<T, 8>, smem, a, st, attr[3]);
+    }
+}
+
+template <typename T>
+janus_status launch_bwd_small(const janus_lstm_desc& d, const BwdSmall<T>& a, hipStream_t st) {
+    static size_t attr[4] = {};
+    const size_t smem = small_bwd_lds(d);
+    switch (small_bwd_split(d)) {
+        case 1: return small_launch(bwd_small_kernel<T, 1>, smem, a, st, attr[0]);
+        case 2: return small_launch(bwd_small_kernel<T, 2>, smem, a, st, attr[1]);
+        case 4: return small_launch(bwd_small_kernel<T, 4>, smem, a, st, attr[2]);
+        default: return small_launch(bwd_small_kernel<T, 8>, smem, a, st, attr[3]);
+    }
 }
 
 janus_status check_desc(const janus_lstm_desc* d) {
@@ -772,6 +1087,29 @@ janus_status lstm_fwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         g.scratch_bytes = w.gs_bytes;
         janus_status e = gemm(g, st);
         if (e != JANUS_OK) return e;
+        if (use_small(d)) {
+            FwdSmall<T> a = {};
+            a.H = H;
+            a.B = B;
+            a.t_eff = s.t_eff;
+            a.fixed = s.fixed ? 1 : 0;
+            a.active = w.act_dev;
+            a.offsets = w.off_dev;
+            a.ldh = w.ldh;
+            a.ldg = w.ldg;
+            a.Wh = static_cast<const T*>(Wh[l]);
+            a.XG = static_cast<const T*>(w.XG);
+            a.Hs = static_cast<T*>(w.Hs[l]);
+            a.Cs = w.Cs[l];
+            a.Gs = static_cast<T*>(w.Gs[l]);
+            a.y = l == d.L - 1 ? static_cast<T*>(y) : nullptr;
+            a.perm = perm;
+            a.hT = hT ? hT + l * bh : nullptr;
+            a.cT = cT ? cT + l * bh : nullptr;
+            TraceScope trace("lstm_fwd_small", 2.0 * 4.0 * H * double(H) * double(s.packed), 0.0, st);
+            if ((e = launch_fwd_small(d, a, st)) != JANUS_OK) return e;
+            continue;
+        }
         for (int t = 0; t < s.t_eff; ++t) {
             FwdStep<T> a;
             a.H = H;
@@ -898,6 +1236,34 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
         a.perm = perm;
         a.dh0 = dh0 ? dh0 + l * bh : nullptr;
         a.dc0 = dc0 ? dc0 + l * bh : nullptr;
+        if (use_small(d)) {
+            if (s.t_eff > 0 || a.dh0 || a.dc0) {
+                BwdSmall<T> q = {};
+                q.H = H;
+                q.B = B;
+                q.t_eff = s.t_eff;
+                q.fixed = s.fixed ? 1 : 0;
+                q.active = w.act_dev;
+                q.offsets = w.off_dev;
+                q.ldh = w.ldh;
+                q.ldg = w.ldg;
+                q.Wh = a.Wh;
+                q.G = a.G;
+                q.Gs = a.Gs;
+                q.Cs = a.Cs;
+                q.dy = a.dy;
+                q.dy_ld = a.dy_ld;
+                q.dy_rows = a.dy_rows;
+                q.dh = w.dh;
+                q.dc = w.dc;
+                q.perm = perm;
+                q.dh0 = a.dh0;
+                q.dc0 = a.dc0;
+                TraceScope trace("lstm_bwd_small", 2.0 * 4.0 * H * double(H) * double(recurrent_rows(s)), 0.0, st);
+                janus_status e = launch_bwd_small(d, q, st);
+                if (e != JANUS_OK) return e;
+            }
+        } else {
         for (int t = s.t_eff - 1; t >= 0; --t) {
             a.final_step = 0;
             a.active = s.active[t];
@@ -917,6 +1283,7 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.prev_base = 0;
             janus_status e = launch_bwd_step<T, Cfg>(a, al, st);
             if (e != JANUS_OK) return e;
+        }
         }
         }
         const int32_t* rowmap = persistent ? w.perm4 : nullptr;   // interleaved gate rows -> torch rows

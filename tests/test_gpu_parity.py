@@ -317,3 +317,33 @@ def test_forward_slices(slices, H, B, ragged, monkeypatch):
     g = step.results()
     assert J.janus_lstm_device_report(step.desc, step.ws)["timed_out"] == 0
     compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
+
+
+@pytest.mark.parametrize("small", ["1", "0"])
+@pytest.mark.parametrize("dtype,ragged", [("f32", False), ("f32", True), ("bf16", True)])
+@pytest.mark.parametrize("B,H", [(6, 48), (1, 65), (40, 48)])
+def test_one_workgroup_recurrence(small, dtype, ragged, B, H, monkeypatch):
+    """Small problems run each layer's time loop in one workgroup (weights,
+    state and dG in LDS, steps separated by workgroup barriers); with
+    JANUS_SMALL=0 the per-step kernels run instead.  Both against the
+    oracle, with fixed and ragged lengths (zero-length rows included), the
+    loss on y so dy enters every step, and h0, c0 given.  Lanes per cell
+    (forward, backward): (1, 2); (2, 8), both splitting K unevenly (65 and
+    260 terms); (1, 1) with two cells per thread."""
+    from paper_1812_01329_amd import janus as J
+    monkeypatch.setenv("JANUS_SMALL", small)
+    monkeypatch.setenv("JANUS_PERSIST", "0")
+    lengths = None
+    if ragged:
+        lengths = [int(v) for v in np.random.default_rng(B * 100 + H).integers(0, 10, B)]
+        lengths[-1] = 0
+        lengths[0] = 9
+    print(f"[small] S={small} {dtype} B={B} H={H} lengths={lengths}", flush=True)
+    w = _lstm("mse", dtype, L=2, I=24, H=H, B=B, T=9, lengths=lengths, seed=12, h0=True, P=20)
+    J.janus_trace_begin()
+    _, g = _run(w)
+    labels = {r["label"] for r in J.janus_trace_end()}
+    want = ("lstm_fwd_small", "lstm_bwd_small") if small == "1" else ("lstm_fwd_step", "lstm_bwd_step")
+    for lab in want:
+        assert any(x.startswith(lab) for x in labels), labels
+    compare_lstm(g, oracle_steps.lstm_step(w), dtype)
