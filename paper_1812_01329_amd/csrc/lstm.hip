@@ -241,17 +241,25 @@ bool persist_fwd_fits(const janus_lstm_desc& d, int ns, const DeviceInfo& info) 
            persist_fwd_lds(d, ns) <= device_lds(info);
 }
 
-// Slices of the persistent forward: 1 unless JANUS_FWD_SLICES=2 or 4 asks
-// for a split.  At H = 2048, B = 256 two slices shorten the contraction from
-// about 11 to 8 us per step but add the exchange (about 2.5 us), and in a
-// whole training step, with the chip at its power limit, the split ran
-// slower (8.9 against 8.4 ms for the two layers).  Four slices lose more:
-// their partial sums (3 MB per XCD) no longer stay in the L2.
+// Slices of the persistent forward.  Two slices halve each workgroup's
+// share of the h stream but add the exchange of partial pre-activations
+// (about 2.5 us per step); they pay where the h slot (B x H bf16) is 1 MB
+// and up: at H = 2048, B = 256 the two forward layers of a training step
+// take 8.0 against 8.3 ms.  Below, the stream is short and one slice is
+// faster (B 128, H 1024: 1.26 against 1.48 ms; PTB, B 20: 0.40 against
+// 0.56 ms).  Four slices lose everywhere: at H = 2048 their partial sums
+// (3 MB per XCD) no longer stay in the L2.  One slice is taken when two do
+// not fit; JANUS_FWD_SLICES=1, 2 or 4 asks for a count.
 int persist_fwd_slices(const janus_lstm_desc& d) {
     const DeviceInfo info = device_info();
     const char* e = getenv("JANUS_FWD_SLICES");
-    const int forced = (e && (e[0] == '1' || e[0] == '2' || e[0] == '4')) ? e[0] - '0' : 1;
-    return persist_fwd_fits(d, forced, info) ? forced : 0;
+    if (e && (e[0] == '1' || e[0] == '2' || e[0] == '4')) {
+        const int forced = e[0] - '0';
+        return persist_fwd_fits(d, forced, info) ? forced : 0;
+    }
+    const bool big = int64_t(d.B) * d.H * 2 >= (int64_t(1) << 20);
+    if (big && persist_fwd_fits(d, 2, info)) return 2;
+    return persist_fwd_fits(d, 1, info) ? 1 : 0;
 }
 
 // Slices of the persistent backward.  8 slices halve each workgroup's
