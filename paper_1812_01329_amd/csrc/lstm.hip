@@ -1206,6 +1206,9 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.part = w.dpart;
             a.db = db[l];
             a.GT = gt_by_kernel(s, persistent) ? static_cast<bf16_t*>(w.GT) : nullptr;
+            // row-major dG only where something reads it: dX (the layer below,
+            // or dx asked for), or the weight gradients when dG^T is not here
+            if (l == 0 && !dx && a.GT) a.G = nullptr;
             a.ldk = w.ldk;
             a.gt_pairs = (s.fixed && B % 2 == 0) ? 1 : 0;   // packed offsets t B all even
             a.ldh = w.ldh;

@@ -716,7 +716,7 @@ struct BwdArgs {
     const int32_t* offsets;
     const int32_t* perm;
     const bf16_t* Wh;                  // [4H, H] gate-major
-    bf16_t* G;                         // dG store [T*B x ldg] interleaved (for the contractions after the loop)
+    bf16_t* G;                         // dG store [T*B x ldg] interleaved (for dX after the loop), or NULL
     bf16_t* Gf;                        // [T] slots of dG in fragment layout (slot t = dG_t), K = 4H
     int64_t gf_slot;                   // elements per slot: round_up(B, 32) * 4H
     const bf16_t* Gs;                  // saved gates, interleaved
@@ -973,11 +973,13 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             }
         }
         if (cell) {
-            // dG_t row-major (for the contractions after the loop)
-            const auto rg = make_rsrc(a.G + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
-            const uint32_t og = (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
-            store16<kStoreBack>(rg, og, make_uint4(dgl[0], dgl[1], dgl[2], dgl[3]));
-            store16<kStoreBack>(rg, og + 16u, make_uint4(dgl[4], dgl[5], dgl[6], dgl[7]));
+            if (a.G) {
+                // dG_t row-major (for the contractions after the loop)
+                const auto rg = make_rsrc(a.G + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
+                const uint32_t og = (uint32_t(r) * uint32_t(a.ldg) + 4u * uint32_t(ub)) * 2u;
+                store16<kStoreBack>(rg, og, make_uint4(dgl[0], dgl[1], dgl[2], dgl[3]));
+                store16<kStoreBack>(rg, og + 16u, make_uint4(dgl[4], dgl[5], dgl[6], dgl[7]));
+            }
             if (a.GT && !a.gt_pairs) {
                 // transposed copy: the K-contiguous operand of the weight gradients
                 bf16_t* gt = a.GT + int64_t(4) * ub * a.ldk + off_t + r;
