@@ -1025,6 +1025,9 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     a.Hf = w.Hf;
     a.hf_slot = w.hf_slot;
     a.HT = use_ht(d, s, true) ? w.HT[l] : nullptr;
+    // the top layer's row-major h is read only by its weight gradients, and
+    // only when they cannot take the transposed copy
+    if (l == d.L - 1 && a.HT) a.Hs = nullptr;
     a.ldht = w.ldht;
     a.sync = w.sync;
     return launch_fwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * recurrent_rows(s), st);

@@ -234,7 +234,7 @@ struct FwdArgs {
     const int32_t* offsets;            // [T + 2] (ignored when fixed)
     const int32_t* perm;               // [B] or NULL
     const bf16_t* Wh;                  // [4H, H] gate-major
-    bf16_t* Hs;                        // [(B + T*B) x ldh]
+    bf16_t* Hs;                        // [(B + T*B) x ldh], or NULL (not stored)
     float* Cs;                         // [(B + T*B) x ldh]
     const bf16_t* XG;                  // [T*B x ldg] interleaved, bias included
     bf16_t* Gs;                        // [T*B x ldg] interleaved gates
@@ -673,12 +673,14 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
         if (cell) {
             const int64_t nrow = int64_t(a.B) + off_t;   // first row of step t in Hs / Cs
             const auto rcs = make_rsrc(a.Cs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 4u);
-            const auto rhs = make_rsrc(a.Hs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 2u);
             const auto rgs = make_rsrc(a.Gs + off_t * a.ldg, uint32_t(act) * uint32_t(a.ldg) * 2u);
             store16<kStoreBack>(rcs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 4u,
                     make_uint4(__float_as_uint(creg[0]), __float_as_uint(creg[1]), __float_as_uint(creg[2]),
                                __float_as_uint(creg[3])));
-            store8<kStoreBack>(rhs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 2u, hb);
+            if (a.Hs) {
+                const auto rhs = make_rsrc(a.Hs + nrow * a.ldh, uint32_t(act) * uint32_t(a.ldh) * 2u);
+                store8<kStoreBack>(rhs, (uint32_t(row) * uint32_t(a.ldh) + uint32_t(ub)) * 2u, hb);
+            }
             if (a.HT) {
                 // transposed copy, the K-contiguous operand of the weight gradients
                 bf16_t* ht = a.HT + int64_t(ub) * a.ldht + a.B + off_t + row;
