@@ -182,10 +182,32 @@ __global__ __launch_bounds__(Cfg::NT) void mse_gemm_kernel(int M, int N, int K, 
 }
 
 // --------------------------------------------------------------- scalar losses
+// One workgroup: 16-byte loads, eight in flight per thread (the loop is
+// unrolled), four running sums per thread added in a fixed order, then the
+// fixed-order workgroup sum.  The result does not depend on timing.
 __global__ __launch_bounds__(1024) void loss_reduce_kernel(int kind, const float* h, int64_t n, float* loss) {
     __shared__ float red[16];
-    float s = 0.f;
-    for (int64_t i = threadIdx.x; i < n; i += blockDim.x) s += kind == 0 ? h[i] * h[i] : h[i];
+    const bool vec = (reinterpret_cast<uintptr_t>(h) & 15u) == 0;
+    const int64_t n4 = vec ? n / 4 : 0;
+    const float4* h4 = reinterpret_cast<const float4*>(h);
+    float s0 = 0.f, s1 = 0.f, s2 = 0.f, s3 = 0.f;
+#pragma unroll 8
+    for (int64_t i = threadIdx.x; i < n4; i += 1024) {
+        const float4 v = h4[i];
+        if (kind == 0) {
+            s0 += v.x * v.x;
+            s1 += v.y * v.y;
+            s2 += v.z * v.z;
+            s3 += v.w * v.w;
+        } else {
+            s0 += v.x;
+            s1 += v.y;
+            s2 += v.z;
+            s3 += v.w;
+        }
+    }
+    for (int64_t i = 4 * n4 + threadIdx.x; i < n; i += 1024) s0 += kind == 0 ? h[i] * h[i] : h[i];
+    float s = (s0 + s1) + (s2 + s3);
     s = block_sum(s, red);
     if (threadIdx.x == 0) *loss = kind == 0 ? s : s / float(n);
 }
