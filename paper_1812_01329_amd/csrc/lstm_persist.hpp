@@ -52,6 +52,7 @@ struct Sync {
     unsigned xcd[16][64];              // per-XCD arrivals
     unsigned census[16][64];           // workgroups resident on each XCD
     unsigned group[kMaxGroups][64];    // arrivals of each unit group
+    unsigned ready[kMaxGroups][64];    // backward: members of each unit group whose dG_t is stored
     unsigned error;                    // set when a wait exceeds its spin limit
     unsigned groups;                   // backward unit groups launched
     unsigned local_groups;             // of which kept their partial sums in one XCD's L2
@@ -166,8 +167,10 @@ __device__ __forceinline__ void barrier_wait(Barrier& b) {
 // partial sums only among themselves).  When all members run on one XCD they
 // share its L2: the sums are stored write-back (the L2 acknowledges them
 // before the arrival) and read with device-scope loads, which miss in the L1
-// and return the L2's copy, so one slot serves every step (a step's sums are
-// read before the grid barrier after which the next step overwrites them).
+// and return the L2's copy, so one slot serves every step in the forward (a
+// step's sums are read before the grid barrier after which the next step
+// overwrites them) and two slots, used in turn, in the backward (which has
+// no grid barrier).
 // Otherwise they are written through to memory into a slot fresh for each
 // step, as for the grid barrier.
 //
@@ -805,6 +808,35 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
     const int bt = wave % NB, kw = wave / NB;
     const int sg0 = slice_kg0<NS>(a.nkg, s), sgn = slice_kg0<NS>(a.nkg, s + 1) - sg0;
     const int kg0 = kw * sgn / KW, kg1 = (kw + 1) * sgn / KW;
+
+    // Step-to-step dependency.  The contraction of step t reads slice s of
+    // dG_{t+1}: k-groups [sg0, sg0 + sgn), i.e. units [4 sg0, 4 (sg0 + sgn)),
+    // whose cells belong to unit groups [vr0, vr1].  Instead of a grid
+    // barrier, each workgroup counts itself into its group's `ready` once its
+    // dG_t is stored (written through and acknowledged, as for the grid
+    // barrier), and waits only for the groups its slice reads: NS arrivals
+    // per step each.
+    const int vr0 = (4 * sg0) / UNITS;
+    const int vr1 = min(ngroups - 1, (4 * (sg0 + sgn) - 1) / UNITS);
+    unsigned rphase = 0;
+    auto ready_arrive = [&]() {
+        ++rphase;
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_waitcnt(0);
+        __builtin_amdgcn_s_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        if (threadIdx.x == 0)
+            __hip_atomic_fetch_add(&a.sync->ready[v][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    };
+    auto ready_wait = [&]() {
+        if (threadIdx.x == 0) {
+            for (int q = vr0; q <= vr1; ++q)
+                if (!spin_until(a.sync, &a.sync->ready[q][0], rphase * unsigned(NS))) break;
+        }
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+        __builtin_amdgcn_s_barrier();
+        __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    };
     const bf16_t* wrow = Ws + (lane & 31) * wld + 8 * (lane >> 5) + kg0 * 16;
     const uint32_t goff = (uint32_t(bt * a.nkg + sg0 + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
     const int crow = bt * 32 + (lane & 31);   // batch row of this lane's accumulator column
@@ -869,8 +901,12 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
         // Slot layout [writer slice][group][reader member][row][8 units]: what
         // one wave stores, and what one wave of a reader loads, is 1 KB in one
         // piece (32 rows x 32 bytes).
+        // A local group alternates between slots 0 and 1: without a grid
+        // barrier a member may store step t's sums while another still reads
+        // those of step t + 1, but not those of step t + 2 (its sums of step
+        // t + 1 entered the group barrier first).
         const int64_t pslot = int64_t(NS) * ngroups * NS * a.B * 8;
-        float* part = plocal ? a.part : a.part + int64_t(t + 1) * pslot;
+        float* part = plocal ? a.part + int64_t((t + 1) & 1) * pslot : a.part + int64_t(t + 1) * pslot;
         if (act_next > 0) {
             f32x16_t acc[MT];
 #pragma unroll
@@ -963,10 +999,10 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             store16<kStoreThrough>(rf, of, make_uint4(dgl[0], dgl[1], dgl[2], dgl[3]));
             store16<kStoreThrough>(rf, of + 512u, make_uint4(dgl[4], dgl[5], dgl[6], dgl[7]));
         }
-        if (sync_after) barrier_arrive(bar);
+        if (sync_after) ready_arrive();
 
         // results for later kernels and the next (earlier) step's operands,
-        // while the barrier completes
+        // while the producers of this slice finish the step
         if (t < 0 && mine) {
 #pragma unroll
             for (int k = 0; k < 4; ++k) {
@@ -1016,7 +1052,7 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             }
         }
         if (t >= 0) prefetch(t - 1);
-        if (sync_after) barrier_wait(bar);
+        if (sync_after) ready_wait();
     }
 
     // bias gradient: sum dbs over the rows of this workgroup's units, in a
