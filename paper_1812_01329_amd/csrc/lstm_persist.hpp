@@ -828,10 +828,25 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
         if (threadIdx.x == 0)
             __hip_atomic_fetch_add(&a.sync->ready[v][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
     };
+    // lane q of wave 0 polls group vr0 + q, so the counters are read in
+    // parallel (one round trip per poll, not one per group).  A slice spans
+    // at most ngroups / NS + 1 groups, within one wave for NS >= 4.
+    static_assert(kMaxGroups / 4 + 1 <= 64, "the groups of a slice fit one wave");
     auto ready_wait = [&]() {
-        if (threadIdx.x == 0) {
-            for (int q = vr0; q <= vr1; ++q)
-                if (!spin_until(a.sync, &a.sync->ready[q][0], rphase * unsigned(NS))) break;
+        if (wave == 0) {
+            const int q = vr0 + lane;
+            const unsigned target = rphase * unsigned(NS);
+            bool done = q > vr1;
+            int spins = 0;
+            while (true) {
+                if (!done) done = __hip_atomic_load(&a.sync->ready[q][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target;
+                if (__all(done)) break;
+                if (__hip_atomic_load(&a.sync->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) break;
+                if (++spins > kSpinLimit) {
+                    if (lane == 0) __hip_atomic_store(&a.sync->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                    break;
+                }
+            }
         }
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
         __builtin_amdgcn_s_barrier();
