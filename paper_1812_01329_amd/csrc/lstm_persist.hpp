@@ -67,12 +67,14 @@ __device__ __forceinline__ unsigned xcc_id() {
     return __builtin_amdgcn_s_getreg(20 | (0 << 6) | (3 << 11)) & 0xfu;
 }
 
-// Per-workgroup barrier bookkeeping, meaningful in thread 0 only.
+// Per-workgroup barrier bookkeeping, meaningful in thread 0 only (xcount:
+// in the first 16 lanes of wave 0).
 struct Barrier {
     Sync* s;
     unsigned x, xsize, nx, nb, phase;
     unsigned xidx;                     // arrival order of this workgroup among those on its XCD
     unsigned xfirst;                   // workgroups on the XCDs numbered below this one
+    unsigned xcount;                   // lane q < 16 of wave 0: workgroups on XCD q
 };
 
 __device__ __forceinline__ bool spin_until(Sync* s, const unsigned* p, unsigned target) {
@@ -115,14 +117,18 @@ __device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
         }
     }
     __syncthreads();
+    b.xcount = 0;
+    if (threadIdx.x < 16)
+        b.xcount = __hip_atomic_load(&s->census[threadIdx.x][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 
 // Device-wide barrier, in two halves so that work no other workgroup waits
 // for can run while it completes:
 //   barrier_arrive: every wave waits for its own memory operations, then the
-//     workgroup arrives on its XCD's counter; the last arrival of each XCD
-//     signals the global count;
-//   barrier_wait:   wait until all XCDs have signalled.
+//     workgroup arrives on its XCD's counter;
+//   barrier_wait:   lane q of wave 0 polls XCD q's counter until all of that
+//     XCD's workgroups have arrived, all XCDs at once (one round trip per
+//     poll, and no second hop through a global count).
 // Between the two a workgroup may issue stores that nobody reads in this
 // launch and loads of data it owns.  The halves use the raw s_barrier (no
 // fence), so memory operations issued between them stay in flight across the
@@ -149,15 +155,24 @@ __device__ __forceinline__ void barrier_arrive(Barrier& b) {
     __builtin_amdgcn_s_waitcnt(0);
     __builtin_amdgcn_s_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
-    if (threadIdx.x == 0) {
-        const unsigned old =
-            __hip_atomic_fetch_add(&b.s->xcd[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-        if (old == b.phase * b.xsize - 1u)
-            __hip_atomic_fetch_add(&b.s->count, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
-    }
+    if (threadIdx.x == 0) __hip_atomic_fetch_add(&b.s->xcd[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
 __device__ __forceinline__ void barrier_wait(Barrier& b) {
-    if (threadIdx.x == 0) spin_until(b.s, &b.s->count, b.nb + b.phase * b.nx);
+    if (threadIdx.x < 64) {
+        const unsigned q = threadIdx.x & 15u;
+        const unsigned target = b.phase * b.xcount;   // 0 past lane 15 and for empty XCDs
+        bool done = threadIdx.x >= 16 || b.xcount == 0u;
+        int spins = 0;
+        while (true) {
+            if (!done) done = __hip_atomic_load(&b.s->xcd[q][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) >= target;
+            if (__all(done)) break;
+            if (__hip_atomic_load(&b.s->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) break;
+            if (++spins > kSpinLimit) {
+                if (threadIdx.x == 0) __hip_atomic_store(&b.s->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+        }
+    }
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_barrier();
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
