@@ -31,6 +31,7 @@
 //   dh, dc [B x H] float32                      carried gradients (sorted rows)
 //   colsum scratch
 #include <algorithm>
+#include <mutex>
 #include <vector>
 
 #include "device.hpp"
@@ -81,11 +82,15 @@ struct DeviceInfo {
     int xccs = 0;
 };
 
+// Properties of the current device, queried once per device (under a lock,
+// so concurrent first calls from several host threads do not race).
 DeviceInfo device_info() {
+    static std::mutex m;
     static DeviceInfo cache[64];
     static bool have[64] = {};
     int dev = 0;
     if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return DeviceInfo{};
+    std::lock_guard<std::mutex> lock(m);
     if (!have[dev]) {
         DeviceInfo d;
         int v = 0;
@@ -824,13 +829,25 @@ bool use_small(const janus_lstm_desc& d) {
     return small_fwd_lds(d) <= cap && small_bwd_lds(d) <= cap;
 }
 
-template <class K, class A>
-janus_status small_launch(K kernel, size_t smem, const A& args, hipStream_t st, size_t& attr_smem) {
+// Raise a kernel's dynamic LDS limit when a launch needs more than the
+// largest size set so far (cached per kernel in `attr_smem`).  The cache and
+// the attribute change together under one lock, so calls from several host
+// threads neither race on the cache nor lower the limit under each other.
+template <class K>
+janus_status raise_lds_limit(K kernel, size_t smem, size_t& attr_smem) {
+    static std::mutex m;
+    std::lock_guard<std::mutex> lock(m);
     if (smem > attr_smem) {
         JANUS_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
                                       int(smem)));
         attr_smem = smem;
     }
+    return JANUS_OK;
+}
+
+template <class K, class A>
+janus_status small_launch(K kernel, size_t smem, const A& args, hipStream_t st, size_t& attr_smem) {
+    if (janus_status e = raise_lds_limit(kernel, smem, attr_smem); e != JANUS_OK) return e;
     hipLaunchKernelGGL(kernel, dim3(1), dim3(kSmallThreads), smem, st, args);
     JANUS_LAUNCH_CHECK();
     return JANUS_OK;
@@ -881,12 +898,7 @@ bool weight_aligned(const janus_lstm_desc& d) {
 
 template <class K>
 janus_status coop_launch(K kernel, int blocks, size_t smem, void* arg, hipStream_t st, size_t& attr_smem) {
-    // the kernel's dynamic LDS limit, raised whenever a launch needs more
-    if (smem > attr_smem) {
-        JANUS_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel), hipFuncAttributeMaxDynamicSharedMemorySize,
-                                      int(smem)));
-        attr_smem = smem;
-    }
+    if (janus_status e = raise_lds_limit(kernel, smem, attr_smem); e != JANUS_OK) return e;
     void* args[] = {arg};
     JANUS_HIP(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), dim3(blocks), dim3(persist::kThreads),
                                          args, unsigned(smem), st));
