@@ -213,6 +213,36 @@ def test_deterministic_repeat():
             assert np.array_equal(a, b), k
 
 
+@pytest.mark.parametrize("H,B,ragged", [(1024, 256, False), (2048, 256, True)])
+def test_deterministic_repeat_persistent(H, B, ragged):
+    """The persistent kernels in the configurations of the large workloads:
+    the backward in 8 slices with its readiness counters (dG slot of 2 MB
+    and more) and, at H = 2048 (h slot of 1 MB), the forward in 2 slices.  Without a grid
+    barrier a workgroup may run a step ahead of others; four runs of the
+    same step must still give identical bits (a race on a partial-sum slot
+    or on a dG slot would show here), and the first matches the oracle."""
+    from paper_1812_01329_amd import janus as J
+    lens = None
+    if ragged:
+        lens = [int(v) for v in np.random.default_rng(H + B).integers(1, 7, B)]
+        lens[0] = 6
+    w = _lstm("mse", "bf16", L=2, I=64, H=H, B=B, T=6, lengths=lens, seed=41, h0=True, P=32)
+    step, g1 = _run(w)
+    rep = J.janus_lstm_device_report(step.desc, step.ws)
+    print(f"[repeat] H={H} B={B} report {rep}", flush=True)
+    assert rep["timed_out"] == 0
+    assert rep["bwd_groups"] == 2 * (H // 64)   # 8 slices: groups of 64 units, two layers
+    compare_lstm(g1, oracle_steps.lstm_step(w), "bf16")
+    for _ in range(3):
+        step.run()
+        g2 = step.results()
+        for k in ("y", "hT", "cT", "dh0", "dc0"):
+            assert np.array_equal(g1[k], g2[k]), k
+        for k in ("dWx", "dWh", "db"):
+            for a, b in zip(g1[k], g2[k]):
+                assert np.array_equal(a, b), k
+
+
 def test_batch_permutation_on_device():
     w = _lstm("mse", "bf16", L=1, I=32, H=64, B=9, T=6, lengths=[6, 2, 5, 0, 3, 6, 1, 4, 2], seed=2, h0=True)
     _, g1 = _run(w)
