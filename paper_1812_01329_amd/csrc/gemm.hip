@@ -4,6 +4,7 @@
 // projection of all time steps, the weight gradients (one contraction over
 // all packed time steps), input gradients, and the head contractions.
 #include <algorithm>
+#include <cstdlib>
 
 #include "device.hpp"
 #include "ops.hpp"
@@ -136,6 +137,9 @@ struct NtArgs {
     // plain store epilogue in 16-byte row pieces through LDS (N and ldc
     // multiples of 8, C and the bias 16-byte aligned)
     int vec_store;
+    // persistent launch: the number of tiles; the grid (a multiple of 8)
+    // walks them
+    int ntiles;
 };
 
 enum NtEpilogue { kEpiStore = 0, kEpiPartial = 1, kEpiMse = 2 };
@@ -144,9 +148,14 @@ constexpr uint32_t kNtOutOfRange = 0x80000000u;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
 
-template <typename OutT, bool SCATTER, int EPI>
+// PERSIST (plain store epilogue through LDS only): a grid of one workgroup
+// per CU walks the tiles, and each workgroup issues the first K block of its
+// next tile before the epilogue of the current one, so the load latency of a
+// tile's start hides behind the previous tile's stores.
+template <typename OutT, bool SCATTER, int EPI, bool PERSIST = false>
 __global__ __launch_bounds__(NtCfg::NT) __attribute__((amdgpu_waves_per_eu(2, 2)))
 void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
+    static_assert(!PERSIST || EPI == kEpiStore, "persistent tiles: plain store epilogue only");
     using C_ = NtCfg;
     // The two stages are separate LDS objects and the main loop is unrolled
     // by two, so every fragment read names the stage it reads: the compiler
@@ -159,44 +168,60 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     // block -> (split, tile): consecutive blocks go to the 8 XCDs in turn, so
     // renumber to give each XCD a contiguous range, then walk the tiles in
-    // groups of 4 M-tiles so neighbours share B tiles in that XCD's L2
-    const int ntot = gridDim.x;
-    int b = blockIdx.x;
-    if (ntot % 8 == 0) b = (b % 8) * (ntot / 8) + b / 8;
+    // groups of 4 M-tiles so neighbours share B tiles in that XCD's L2.  A
+    // persistent workgroup w (on XCD w mod 8) takes blocks w / 8 + i G / 8 of
+    // its XCD's range (grid G), in the same order.
+    const int ntot = PERSIST ? p.ntiles : int(gridDim.x);
+    const int per_xcd = ntot / 8, xstep = int(gridDim.x) / 8;
+    int vb;
+    if constexpr (PERSIST) {
+        vb = int(blockIdx.x / 8);   // index within the XCD's range
+    } else {
+        vb = blockIdx.x;
+        if (ntot % 8 == 0) vb = (vb % 8) * (ntot / 8) + vb / 8;
+    }
     const int tiles = p.mt * p.nt;
-    const int split = b / tiles;
-    const int t = b % tiles;
     constexpr int GM = 4;
     const int in_group = GM * p.nt;
-    const int first_m = (t / in_group) * GM;
-    const int gsz = min(p.mt - first_m, GM);
-    const int m0 = (first_m + (t % in_group) % gsz) * C_::BM;
-    const int n0 = ((t % in_group) / gsz) * C_::BN;
-    const int kt0 = split * p.ktiles_per_split;
-    const int nk = max(0, min(p.ktiles_per_split, (p.K + C_::BK - 1) / C_::BK - kt0));
+    int split = 0, m0 = 0, n0 = 0, kt0 = 0, nk = 0;
+    auto map_tile = [&](int b, int& sp, int& tm0, int& tn0, int& tk0, int& tnk) {
+        sp = b / tiles;
+        const int t = b % tiles;
+        const int first_m = (t / in_group) * GM;
+        const int gsz = min(p.mt - first_m, GM);
+        tm0 = (first_m + (t % in_group) % gsz) * C_::BM;
+        tn0 = ((t % in_group) / gsz) * C_::BN;
+        tk0 = sp * p.ktiles_per_split;
+        tnk = max(0, min(p.ktiles_per_split, (p.K + C_::BK - 1) / C_::BK - tk0));
+    };
+    auto block_of = [&](int i) { return PERSIST ? int(blockIdx.x % 8) * per_xcd + i : i; };
+    map_tile(block_of(vb), split, m0, n0, kt0, nk);
 
     // this lane's loads: waves 0-3 fill the A tile, 4-7 the B tile; load j
     // of wave w covers tile rows 64 (w % 4) + 8 j + lane / 8, physical chunk
     // lane % 8, holding logical chunk (lane % 8) ^ (row % 8)
     const bool isA = wave < 4;
     const int lw = wave & 3;
-    const int row0 = isA ? m0 : n0;
     const int rows = isA ? p.M : p.N;
     const int64_t ld = isA ? p.lda : p.ldb;
     const int32_t* idx = isA ? p.a_idx : p.b_idx;
     const bf16_t* src = isA ? p.A : p.B;
     const int kchunk = ((lane & 7) ^ (lane >> 3)) * 8;
     uint32_t rowoff[C_::LOADS];
+    __amdgpu_buffer_rsrc_t rs;
+    auto setup_loads = [&](int tm0, int tn0) {
+        const int row0 = isA ? tm0 : tn0;
 #pragma unroll
-    for (int j = 0; j < C_::LOADS; ++j) {
-        const int r = lw * 64 + j * 8 + (lane >> 3);
-        const int gr = row0 + r;
-        const int64_t src_row = idx ? int64_t(idx[min(gr, rows - 1)]) : int64_t(r);
-        rowoff[j] = gr < rows ? uint32_t(src_row * ld * 2) : kNtOutOfRange;
-    }
-    const bf16_t* base = idx ? src : src + int64_t(row0) * ld;
-    const __amdgpu_buffer_rsrc_t rs =
-        __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(base), (short)0, 0x7fffffff, 0x00020000);
+        for (int j = 0; j < C_::LOADS; ++j) {
+            const int r = lw * 64 + j * 8 + (lane >> 3);
+            const int gr = row0 + r;
+            const int64_t src_row = idx ? int64_t(idx[min(gr, rows - 1)]) : int64_t(r);
+            rowoff[j] = gr < rows ? uint32_t(src_row * ld * 2) : kNtOutOfRange;
+        }
+        const bf16_t* base = idx ? src : src + int64_t(row0) * ld;
+        rs = __builtin_amdgcn_make_buffer_rsrc(const_cast<bf16_t*>(base), (short)0, 0x7fffffff, 0x00020000);
+    };
+    setup_loads(m0, n0);
     const int lds_op = (isA ? 0 : C_::BM * C_::BK) + lw * 64 * C_::BK;
 
     // Offsets with bit 31 set are out of range (the descriptor covers 2^31 - 1
@@ -214,12 +239,6 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
 
     const int wr0 = C_::wave_row0(wave), wc0 = C_::wave_col0(wave);
     f32x16_t acc[C_::FM][C_::FN];
-#pragma unroll
-    for (int i = 0; i < C_::FM; ++i)
-#pragma unroll
-        for (int j = 0; j < C_::FN; ++j)
-#pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
     // fragment rows; the row swizzle is row % 8 = lane % 8 for every fragment
     const int sw = lane & 7, kh = lane >> 5;
     int arow[C_::FM], brow[C_::FN];
@@ -257,6 +276,13 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
         __builtin_amdgcn_s_barrier();
     };
     if (nk > 0) issue(kt0, stage0);
+    while (true) {
+#pragma unroll
+    for (int i = 0; i < C_::FM; ++i)
+#pragma unroll
+        for (int j = 0; j < C_::FN; ++j)
+#pragma unroll
+            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
     int it = 0;
     for (; it + 1 < nk; it += 2) {
         sync();
@@ -271,6 +297,20 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
     if (it < nk) {
         sync();
         compute(stage0);
+    }
+    // persistent: the next tile's first K block goes to stage 0 before this
+    // tile's epilogue (which then stages through stage 1 only)
+    bool more = false;
+    int nsplit = 0, nm0 = 0, nn0 = 0, nkt0 = 0, nnk = 0;
+    if constexpr (PERSIST) {
+        vb += xstep;
+        more = vb < per_xcd;
+        sync();   // every wave is done reading both stages
+        if (more) {
+            map_tile(block_of(vb), nsplit, nm0, nn0, nkt0, nnk);
+            setup_loads(nm0, nn0);
+            if (nnk > 0) issue(nkt0, stage0);
+        }
     }
     if constexpr (EPI == kEpiMse) {
         // Stage each wave's accumulators through LDS (the stages are free now)
@@ -378,13 +418,17 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
     } else {
         if (p.vec_store) {
             // Stage each wave's accumulators through LDS as in the MSE epilogue
-            // (two halves of 64 rows x 64 columns, 8-column chunks swizzled by
+            // (passes of 64 rows x 64 columns, 8-column chunks swizzled by
             // row); lane l then writes columns 8 (l % 8) .. + 7 of rows
             // l / 8 + 8 q: 16 bytes (bf16) or 32 bytes (float32) per store.
+            // Persistent: stage 0 is filling with the next tile, so every wave
+            // stages 32 rows at a time in its 8 KB of stage 1.
+            constexpr int RP = PERSIST ? 32 : 64;   // rows per pass
             const bf16_t* bias = static_cast<const bf16_t*>(g.bias);
             OutT* C = static_cast<OutT*>(g.C);
-            __syncthreads();
-            float* tile = reinterpret_cast<float*>(wave < 4 ? stage0 : stage1) + (wave & 3) * 4096;
+            if constexpr (!PERSIST) __syncthreads();
+            float* tile = PERSIST ? reinterpret_cast<float*>(stage1) + wave * 2048
+                                  : reinterpret_cast<float*>(wave < 4 ? stage0 : stage1) + (wave & 3) * 4096;
             const int c8 = lane & 7, rq = lane >> 3;
             const int ccol = n0 + wc0 + c8 * 8;
             const bool cok = ccol < p.N;
@@ -399,20 +443,20 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
                 }
             }
 #pragma unroll
-            for (int half = 0; half < 2; ++half) {
+            for (int pass = 0; pass < C_::WTM / RP; ++pass) {
 #pragma unroll
-                for (int ii = 0; ii < 2; ++ii)
+                for (int ii = 0; ii < RP / 32; ++ii)
 #pragma unroll
                     for (int j = 0; j < C_::FN; ++j)
 #pragma unroll
                         for (int v = 0; v < 16; ++v) {
                             const int r = ii * 32 + acc_row(v, lane), c = j * 32 + acc_col(lane);
-                            tile[r * 64 + (c ^ ((r & 7) << 3))] = acc[2 * half + ii][j][v];
+                            tile[r * 64 + (c ^ ((r & 7) << 3))] = acc[pass * (RP / 32) + ii][j][v];
                         }
 #pragma unroll
-                for (int q = 0; q < 8; ++q) {
+                for (int q = 0; q < RP / 8; ++q) {
                     const int r = rq + 8 * q;
-                    const int row = m0 + wr0 + half * 64 + r;
+                    const int row = m0 + wr0 + pass * RP + r;
                     const float4 v0 = *reinterpret_cast<const float4*>(tile + r * 64 + ((c8 ^ (r & 7)) << 3));
                     const float4 v1 = *reinterpret_cast<const float4*>(tile + r * 64 + ((c8 ^ (r & 7)) << 3) + 4);
                     if (row < p.M && cok) {
@@ -438,6 +482,13 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
         } else {
             store_tile_impl<bf16_t, NtCfg, OutT, SCATTER>(g, acc, m0, n0, tid);
         }
+    }
+    if (!more) break;
+    split = nsplit;
+    m0 = nm0;
+    n0 = nn0;
+    kt0 = nkt0;
+    nk = nnk;
     }
 }
 
@@ -653,6 +704,22 @@ const char* nt_label(bool f32out, bool scatter, bool partial) {
     return scatter ? "gemm_nt_bf16out_scatter" : "gemm_nt_bf16out";
 }
 
+// JANUS_GEMM_PERSIST=0 switches the persistent tile loop off
+bool getenv_off(const char* name) {
+    const char* e = getenv(name);
+    return e && e[0] == '0';
+}
+
+// compute units of the current device (0 if the query fails)
+int device_cus() {
+    int dev = 0, v = 0;
+    if (hipGetDevice(&dev) != hipSuccess || hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) != hipSuccess) {
+        (void)hipGetLastError();
+        return 0;
+    }
+    return v;
+}
+
 template <typename OutT, bool SCATTER, int EPI>
 janus_status launch_nt(const NtArgs& args, const GemmDesc& g, hipStream_t s) {
     auto kern = &gemm_nt_fast_kernel<OutT, SCATTER, EPI>;
@@ -661,11 +728,28 @@ janus_status launch_nt(const NtArgs& args, const GemmDesc& g, hipStream_t s) {
                    (!g.bias || reinterpret_cast<uintptr_t>(g.bias) % 16 == 0))
                       ? 1
                       : 0;
+    const int ntot = a.mt * a.nt * a.splits;
+    // persistent tiles where every workgroup gets two or more: one per CU
+    // (a multiple of 8, so each XCD holds the same number)
+    int grid = 0;
+    if constexpr (EPI == kEpiStore) {
+        const int cus = device_cus() / 8 * 8;
+        if (a.vec_store && cus >= 8 && ntot % 8 == 0 && ntot >= 2 * cus && !getenv_off("JANUS_GEMM_PERSIST")) grid = cus;
+    }
     const double out_bytes = EPI == kEpiPartial ? 4.0 * a.splits : EPI == kEpiMse ? 4.0 : (sizeof(OutT) == 4 ? 4.0 : 2.0);
     TraceScope trace(EPI == kEpiMse ? "gemm_nt_mse" : nt_label(sizeof(OutT) == 4, SCATTER, EPI == kEpiPartial),
                      2.0 * g.M * g.N * double(g.K),
                      (double(g.M) * g.K + double(g.N) * g.K) * 2.0 + double(g.M) * g.N * out_bytes, s);
-    hipLaunchKernelGGL(kern, dim3(unsigned(a.mt * a.nt * a.splits)), dim3(NtCfg::NT), 0, s, a, g);
+    bool launched = false;
+    if constexpr (EPI == kEpiStore) {
+        if (grid > 0) {
+            a.ntiles = ntot;
+            hipLaunchKernelGGL((gemm_nt_fast_kernel<OutT, SCATTER, EPI, true>), dim3(unsigned(grid)),
+                               dim3(NtCfg::NT), 0, s, a, g);
+            launched = true;
+        }
+    }
+    if (!launched) hipLaunchKernelGGL(kern, dim3(unsigned(ntot)), dim3(NtCfg::NT), 0, s, a, g);
     JANUS_LAUNCH_CHECK();
     return JANUS_OK;
 }

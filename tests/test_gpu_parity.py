@@ -243,6 +243,27 @@ def test_deterministic_repeat_persistent(H, B, ragged):
                 assert np.array_equal(a, b), k
 
 
+def test_persistent_contraction_tiles(monkeypatch):
+    """Contractions of 512 tiles and more run as a persistent grid (one
+    workgroup per CU walking the tiles, the next tile's first K block loaded
+    during the current tile's epilogue).  The input projection here has
+    8192 x 4096 outputs, 512 tiles of 256 x 256: with the persistent grid and
+    without (JANUS_GEMM_PERSIST=0) the step gives identical bits, and matches
+    the oracle."""
+    from paper_1812_01329_amd import janus as J
+    w = _lstm("mse", "bf16", L=1, I=1024, H=1024, B=256, T=32, seed=43, h0=True, P=64)
+    res = {}
+    for mode in ("1", "0"):
+        monkeypatch.setenv("JANUS_GEMM_PERSIST", mode)
+        _, res[mode] = _run(w)
+    for k in ("y", "hT", "cT", "dh0", "dc0"):
+        assert np.array_equal(res["1"][k], res["0"][k]), k
+    for k in ("dWx", "dWh", "db"):
+        for a, b in zip(res["1"][k], res["0"][k]):
+            assert np.array_equal(a, b), k
+    compare_lstm(res["1"], oracle_steps.lstm_step(w), "bf16")
+
+
 def test_batch_permutation_on_device():
     w = _lstm("mse", "bf16", L=1, I=32, H=64, B=9, T=6, lengths=[6, 2, 5, 0, 3, 6, 1, 4, 2], seed=2, h0=True)
     _, g1 = _run(w)
