@@ -243,15 +243,22 @@ def test_deterministic_repeat_persistent(H, B, ragged):
                 assert np.array_equal(a, b), k
 
 
-def test_persistent_contraction_tiles(monkeypatch):
+@pytest.mark.parametrize("ragged", [False, True])
+def test_persistent_contraction_tiles(ragged, monkeypatch):
     """Contractions of 512 tiles and more run as a persistent grid (one
     workgroup per CU walking the tiles, the next tile's first K block loaded
     during the current tile's epilogue).  The input projection here has
-    8192 x 4096 outputs, 512 tiles of 256 x 256: with the persistent grid and
-    without (JANUS_GEMM_PERSIST=0) the step gives identical bits, and matches
-    the oracle."""
-    from paper_1812_01329_amd import janus as J
-    w = _lstm("mse", "bf16", L=1, I=1024, H=1024, B=256, T=32, seed=43, h0=True, P=64)
+    8192 x 4096 outputs (512 tiles of 256 x 256), or, with ragged lengths,
+    about 8300 packed rows (528 tiles, the last M tile partial): with the
+    persistent grid and without (JANUS_GEMM_PERSIST=0) the step gives
+    identical bits, and matches the oracle."""
+    T, lens = 32, None
+    if ragged:
+        T = 64
+        lens = [int(v) for v in np.random.default_rng(44).integers(1, T + 1, 256)]
+        lens[0] = T
+    w = _lstm("mse", "bf16", L=1, I=1024 if not ragged else 256, H=1024, B=256, T=T, lengths=lens, seed=43,
+              h0=True, P=64)
     res = {}
     for mode in ("1", "0"):
         monkeypatch.setenv("JANUS_GEMM_PERSIST", mode)
