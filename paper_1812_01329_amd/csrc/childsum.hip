@@ -243,10 +243,12 @@ janus_status prepare_cs(const janus_treelstm_desc* d, const janus_nary_tree_batc
         return JANUS_ERR_WORKSPACE;
     carve_cs(*d, s.N, ws, w);
     const size_t nb = sizeof(int32_t) * s.N;
-    if ((e = upload(w.pword, s.pword.data(), nb, st)) != JANUS_OK) return e;
-    if ((e = upload(w.pcoff, s.pcoff.data(), nb + sizeof(int32_t), st)) != JANUS_OK) return e;
-    if ((e = upload(w.pkids, s.pkids.data(), sizeof(int32_t) * s.pkids.size(), st)) != JANUS_OK) return e;
-    return upload(w.rootk, s.rootk.data(), nb, st);
+    // carved one after another (nothing else between them): one copy
+    const UploadPiece pieces[] = {{w.pword, s.pword.data(), nb},
+                                  {w.pcoff, s.pcoff.data(), nb + sizeof(int32_t)},
+                                  {w.pkids, s.pkids.data(), sizeof(int32_t) * s.pkids.size()},
+                                  {w.rootk, s.rootk.data(), nb}};
+    return upload_pieces(pieces, 4, st);
 }
 
 }  // namespace

@@ -4,6 +4,7 @@
 #include <cstdio>
 #include <cstring>
 #include <deque>
+#include <vector>
 #include <mutex>
 
 namespace janus {
@@ -94,6 +95,30 @@ PinnedRing& ring() {
 janus_status upload(void* dst_dev, const void* src_host, size_t bytes, hipStream_t stream) {
     if (bytes == 0) return JANUS_OK;
     return ring().put(dst_dev, src_host, bytes, stream);
+}
+
+janus_status upload_pieces(const UploadPiece* pieces, int n, hipStream_t stream) {
+    if (n <= 0) return JANUS_OK;
+    char* const base = static_cast<char*>(pieces[0].dst);
+    size_t span = 0;
+    bool ordered = true;
+    for (int i = 0; i < n; ++i) {
+        char* d = static_cast<char*>(pieces[i].dst);
+        if (d < base + span) ordered = false;   // overlaps or precedes the previous piece
+        if (ordered) span = size_t(d - base) + pieces[i].bytes;
+    }
+    if (!ordered || span > (size_t(16) << 20)) {
+        for (int i = 0; i < n; ++i) {
+            const janus_status e = upload(pieces[i].dst, pieces[i].src, pieces[i].bytes, stream);
+            if (e != JANUS_OK) return e;
+        }
+        return JANUS_OK;
+    }
+    std::vector<char> image(span, 0);
+    for (int i = 0; i < n; ++i)
+        if (pieces[i].bytes) std::memcpy(image.data() + (static_cast<char*>(pieces[i].dst) - base), pieces[i].src,
+                                         pieces[i].bytes);
+    return upload(base, image.data(), span, stream);
 }
 
 // ------------------------------------------------------------------ tracing

@@ -60,6 +60,17 @@ inline bool dtype_ok(janus_dtype d) { return d == JANUS_F32 || d == JANUS_BF16; 
 // the copy stays asynchronous on the caller's stream.
 janus_status upload(void* dst_dev, const void* src_host, size_t bytes, hipStream_t stream);
 
+// Several host arrays for device buffers that lie one after another in one
+// region (carved in order, with padding between them): one copy of a host
+// image of the whole span instead of one copy per array.  Pieces out of
+// order, or a span past the staging capacity, are copied one by one.
+struct UploadPiece {
+    void* dst;
+    const void* src;
+    size_t bytes;
+};
+janus_status upload_pieces(const UploadPiece* pieces, int n, hipStream_t stream);
+
 // Brackets one kernel launch with trace events while tracing is on (see
 // janus_trace_begin); a no-op otherwise.  flops / bytes: algorithmic work.
 class TraceScope {

@@ -256,13 +256,12 @@ janus_status upload_tree(const janus_tree_batch* t, const TreeSchedule& s, const
     TreeHost h;
     build_host(t, s, h);
     const size_t nb = sizeof(int32_t) * s.N;
-    janus_status e;
-    if ((e = upload(w.lword, h.lword.data(), nb, st)) != JANUS_OK) return e;
-    if ((e = upload(w.lchild, h.lchild.data(), nb, st)) != JANUS_OK) return e;
-    if ((e = upload(w.rchild, h.rchild.data(), nb, st)) != JANUS_OK) return e;
-    if ((e = upload(w.parent, h.parent.data(), nb, st)) != JANUS_OK) return e;
-    if ((e = upload(w.rootk, h.rootk.data(), nb, st)) != JANUS_OK) return e;
-    return upload(w.rootpos, h.rootpos.data(), sizeof(int32_t) * t->num_trees, st);
+    // carved one after another (nothing else between them): one copy
+    const UploadPiece pieces[] = {{w.lword, h.lword.data(), nb},   {w.lchild, h.lchild.data(), nb},
+                                  {w.rchild, h.rchild.data(), nb}, {w.parent, h.parent.data(), nb},
+                                  {w.rootk, h.rootk.data(), nb},
+                                  {w.rootpos, h.rootpos.data(), sizeof(int32_t) * t->num_trees}};
+    return upload_pieces(pieces, 6, st);
 }
 
 janus_status prepare(const janus_treelstm_desc* d, const janus_tree_batch* t, void* ws, size_t ws_bytes,
