@@ -100,9 +100,19 @@ __global__ void embed_bwd_kernel(const T* dx, const int32_t* ids, int rows, int 
     }
     __syncthreads();
     const int n = nmatch;
+    // the rows of a frequent id (tens of them) are loaded eight at a time and
+    // added in ascending order, so the loads overlap and the sum stays fixed
     for (int j = tid; j < H; j += blockDim.x) {
         float s = 0.f;
-        for (int k = 0; k < n; ++k) s += to_f(dx[int64_t(sid[k]) * H + j]);
+        int k = 0;
+        for (; k + 8 <= n; k += 8) {
+            float v[8];
+#pragma unroll
+            for (int e = 0; e < 8; ++e) v[e] = to_f(dx[int64_t(sid[k + e]) * H + j]);
+#pragma unroll
+            for (int e = 0; e < 8; ++e) s += v[e];
+        }
+        for (; k < n; ++k) s += to_f(dx[int64_t(sid[k]) * H + j]);
         dE[int64_t(id) * H + j] = s;
     }
 }
