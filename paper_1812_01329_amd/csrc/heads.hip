@@ -119,23 +119,41 @@ __global__ void embed_bwd_kernel(const T* dx, const int32_t* ids, int rows, int 
 
 // --------------------------------------------------------------- softmax xent
 // per row: loss_r = logsumexp(z) - z[target]; dz = (softmax(z) - onehot) / rows
+constexpr int kXentLdsMax = 12288;   // vocabulary whose row a block keeps in LDS (48 KB)
+
 template <typename T>
 __global__ __launch_bounds__(256) void xent_row_kernel(const float* logits, int64_t ld, const int32_t* tgt, int V,
                                                        int rows, T* dz, int64_t ldz, float* loss_rows) {
+    // With dynamic LDS for the row (V floats), the row is read from memory
+    // once: the first pass keeps it, the second replaces it by exp(z - max),
+    // the third writes dz from it.  Every thread touches only its own
+    // entries (v = tid mod 256), so the passes need no barrier between them
+    // beyond the reductions.  Without LDS (a row past 48 KB) each pass reads
+    // the row again.  Both give the same values.
+    extern __shared__ float zs[];
+    const bool keep = (V <= kXentLdsMax);
     __shared__ float red[16];
     const int r = blockIdx.x;
     const float* z = logits + int64_t(r) * ld;
     float m = -INFINITY;
-    for (int v = threadIdx.x; v < V; v += blockDim.x) m = fmaxf(m, z[v]);
+    for (int v = threadIdx.x; v < V; v += blockDim.x) {
+        const float x = z[v];
+        if (keep) zs[v] = x;
+        m = fmaxf(m, x);
+    }
     m = block_max(m, red);
     float s = 0.f;
-    for (int v = threadIdx.x; v < V; v += blockDim.x) s += __expf(z[v] - m);
+    for (int v = threadIdx.x; v < V; v += blockDim.x) {
+        const float e = __expf((keep ? zs[v] : z[v]) - m);
+        if (keep) zs[v] = e;
+        s += e;
+    }
     s = block_sum(s, red);
     const float lse = m + __logf(s);
     const int t = min(max(tgt[r], 0), V - 1);
     const float inv = 1.f / float(rows);
     for (int v = threadIdx.x; v < V; v += blockDim.x) {
-        const float p = __expf(z[v] - m) / s;
+        const float p = (keep ? zs[v] : __expf(z[v] - m)) / s;
         dz[int64_t(r) * ldz + v] = from_f<T>((p - (v == t ? 1.f : 0.f)) * inv);
     }
     if (threadIdx.x == 0) loss_rows[r] = lse - z[t];
@@ -398,7 +416,8 @@ janus_status xent_impl(const janus_xent_desc& d, const int32_t* ids_dev, const v
     if (e != JANUS_OK) return e;
     {
         TraceScope trace_row("xent_row", 0.0, double(d.rows) * d.V * (4.0 + sizeof(T)), st);
-        hipLaunchKernelGGL(xent_row_kernel<T>, dim3(d.rows), dim3(256), 0, st, w.logits, w.ldv, ids_dev, d.V, d.rows,
+        const size_t zsm = d.V <= kXentLdsMax ? sizeof(float) * size_t(d.V) : 0;
+        hipLaunchKernelGGL(xent_row_kernel<T>, dim3(d.rows), dim3(256), zsm, st, w.logits, w.ldv, ids_dev, d.V, d.rows,
                            static_cast<T*>(w.dz), w.ldv, w.loss_rows);
         JANUS_LAUNCH_CHECK();
     }

@@ -76,11 +76,13 @@ def test_embedding_gather_and_scatter(dtype, V, Hd, rows, kind):
 
 
 @pytest.mark.parametrize("dtype,V,Hd,rows", [("f32", 5, 150, 25), ("f32", 1001, 36, 77), ("bf16", 1001, 64, 300),
-                                             ("bf16", 5, 64, 33)])
+                                             ("bf16", 5, 64, 33), ("f32", 13001, 36, 9)])
 @pytest.mark.parametrize("kind", ["same", "ends", "random"])
 def test_softmax_cross_entropy(dtype, V, Hd, rows, kind):
     """XENT_FWD_BWD: mean loss, dh, dWout and dbout of one call, with the
-    targets all on one class, on the two end classes, or random."""
+    targets all on one class, on the two end classes, or random.  A row of
+    up to 12288 logits stays in LDS across the softmax passes; the 13001
+    class case takes the path that reads the row again."""
     import torch
     from paper_1812_01329_amd import janus as J
     rng = np.random.default_rng(3 * V + rows)
