@@ -146,15 +146,19 @@ janus_status janus_lstm_state_carry(const janus_lstm_desc* d, int32_t B_prev,
                                     float* h0, float* c0, void* stream);
 
 /*
- * Report of the last janus_lstm_seq_fwd or janus_lstm_seq_bwd call made with
- * this workspace (same d).  The persistent recurrence kernels separate their
- * time steps with device-wide barriers whose waits are bounded; when a wait
- * runs out, the kernels drain and the outputs are undefined.  Those calls
- * return without synchronising, so this call synchronises `stream` and reads
- * the report back.
- *  timed_out         1 if any wait of the call ran out.
- *  bwd_groups        backward unit groups launched, summed over layers (0
- *                    when the per-step kernels ran).
+ * Report of the current step made with this workspace (same d): the last
+ * janus_lstm_seq_fwd call and the janus_lstm_seq_bwd calls after it.  The
+ * persistent recurrence kernels separate their time steps with device-wide
+ * barriers whose waits are bounded; when a wait runs out, the kernels drain
+ * and the outputs are undefined.  Those calls return without synchronising,
+ * so this call synchronises `stream` and reads the report back.  Reading does
+ * not clear it; the next forward call does.
+ *  timed_out         1 if any wait of the step ran out (forward or
+ *                    backward: the backward keeps the forward's flag, and
+ *                    its kernels then drain at once).
+ *  bwd_groups        backward unit groups launched by the last backward
+ *                    call, summed over layers (0 when the per-step kernels
+ *                    ran, or before a backward).
  *  bwd_local_groups  of those, groups whose workgroups all ran on one XCD
  *                    and kept their partial sums in its L2.
  *  fwd_groups, fwd_local_groups  the same for the forward recurrence when
@@ -173,6 +177,20 @@ typedef struct {
 
 janus_status janus_lstm_device_report(const janus_lstm_desc* d, const void* ws, size_t ws_bytes,
                                       janus_lstm_report* out, void* stream);
+
+/*
+ * Device address of the timeout flag inside an LSTM workspace (no device
+ * work, no synchronisation).  The word is a uint32 that janus_lstm_seq_fwd
+ * clears when it starts and that the persistent kernels set when a bounded
+ * wait runs out; janus_lstm_seq_bwd leaves it as it is, so after a step it is
+ * non-zero if any wait of the step's forward or backward ran out.  Hand it to
+ * janus_sgd_clip_update as `hold` to keep a failed step from updating the
+ * parameters (state changes are all-or-nothing, Section 4.2.3).  The address
+ * stays valid as long as the workspace does.
+ * Errors: INVALID_ARG (bad d, NULL out), WORKSPACE (as for the calls above).
+ */
+janus_status janus_lstm_fault_flag(const janus_lstm_desc* d, const void* ws, size_t ws_bytes,
+                                   const uint32_t** out);
 
 /*
  * Integer schedule of the sequence loop (host only, no device use):
@@ -493,6 +511,11 @@ size_t janus_sgd_workspace_bytes(const janus_sgd_desc* d);
  *            not overlap.
  *  stats     device float32[2] or NULL: [0] the norm before clipping, [1]
  *            the scale s applied (0 when the update was skipped).
+ *  hold      device uint32 or NULL.  Read when the update runs (stream
+ *            order): if it is non-zero, no parameter is written, as for a
+ *            non-finite norm.  Pass janus_lstm_fault_flag's word so that a
+ *            training step whose recurrence timed out leaves the parameters
+ *            unchanged (all-or-nothing, Section 4.2.3).
  *  ws        workspace (see conventions), at least
  *            janus_sgd_workspace_bytes(d) bytes.
  * Errors: NULL d/params/grads/sizes, n < 1, non-finite lr, NaN max_norm, a
@@ -502,7 +525,8 @@ size_t janus_sgd_workspace_bytes(const janus_sgd_desc* d);
  */
 janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* const* params,
                                    const float* const* grads, const int64_t* sizes,
-                                   float* stats, void* ws, size_t ws_bytes, void* stream);
+                                   float* stats, const uint32_t* hold, void* ws, size_t ws_bytes,
+                                   void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Misc                                                                     */

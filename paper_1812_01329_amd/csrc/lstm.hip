@@ -1687,7 +1687,9 @@ extern "C" janus_status janus_lstm_seq_fwd(const janus_lstm_desc* d, const void*
     hipStream_t st = static_cast<hipStream_t>(stream);
     e = upload_schedule(s, w, st);
     if (e != JANUS_OK) return e;
-    if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;   // the call's report
+    // a step starts: the report, timeout flag included, covers this call and
+    // the backward calls after it
+    if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;
     if (pad) return lstm_fwd_padded(*d, s, ws, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
     if (d->dtype == JANUS_BF16)
         return lstm_fwd_impl<bf16_t, StepBF16>(*d, s, w, x, Wx, Wh, b, h0, c0, y, hT, cT, st);
@@ -1718,7 +1720,12 @@ extern "C" janus_status janus_lstm_seq_bwd(const janus_lstm_desc* d, const void*
     hipStream_t st = static_cast<hipStream_t>(stream);
     e = upload_schedule(s, w, st);
     if (e != JANUS_OK) return e;
-    if ((e = zero_fill(w.sync, sizeof(persist::Sync), st)) != JANUS_OK) return e;   // the call's report
+    // The backward's own report fields start at zero; the timeout flag and
+    // the forward's fields stay as the forward left them, so a wait that ran
+    // out in the forward is still reported after the backward (and the
+    // backward's kernels drain at once instead of computing on its garbage).
+    if ((e = zero_fill(w.sync, persist::kSyncCounterBytes, st)) != JANUS_OK) return e;
+    if ((e = zero_fill(&w.sync->groups, 2 * sizeof(unsigned), st)) != JANUS_OK) return e;
     if (pad) return lstm_bwd_padded(*d, s, ws, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
     if (d->dtype == JANUS_BF16)
         return lstm_bwd_impl<bf16_t, StepBF16>(*d, s, w, x, Wx, Wh, dy, dhT, dcT, dx, dh0, dc0, dWx, dWh, db, st);
@@ -1787,4 +1794,19 @@ extern "C" janus_status janus_lstm_device_report(const janus_lstm_desc* d, const
     out->fwd_groups = int32_t(rep[3]);
     out->fwd_local_groups = int32_t(rep[4]);
     return out->timed_out ? JANUS_ERR_DEVICE : JANUS_OK;
+}
+
+extern "C" janus_status janus_lstm_fault_flag(const janus_lstm_desc* d, const void* ws, size_t ws_bytes,
+                                              const uint32_t** out) {
+    janus_status e = check_desc(d);
+    if (e != JANUS_OK) return e;
+    if (!out) return JANUS_ERR_INVALID_ARG;
+    if (!ws) return JANUS_ERR_WORKSPACE;
+    if (ws_bytes < janus_lstm_workspace_bytes(d) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return JANUS_ERR_WORKSPACE;
+    LstmWs w;
+    carve(needs_padding(*d) ? padded_desc(*d) : *d, const_cast<void*>(ws), w);
+    static_assert(sizeof(w.sync->error) == sizeof(uint32_t), "one 32-bit word");
+    *out = reinterpret_cast<const uint32_t*>(&w.sync->error);
+    return JANUS_OK;
 }

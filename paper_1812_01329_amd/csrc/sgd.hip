@@ -98,7 +98,8 @@ __global__ __launch_bounds__(kSgdThreads) void sgd_sumsq_kernel(SgdTable t, doub
 }
 
 __global__ __launch_bounds__(kSgdThreads) void sgd_scale_kernel(const double* partial, int n, float lr,
-                                                                float max_norm, SgdCtrl* ctrl, float* stats) {
+                                                                float max_norm, const uint32_t* hold, SgdCtrl* ctrl,
+                                                                float* stats) {
     __shared__ double red[kSgdThreads / 64];
     double acc = 0.0;
     for (int k = threadIdx.x; k < n; k += kSgdThreads) acc += partial[k];
@@ -106,11 +107,14 @@ __global__ __launch_bounds__(kSgdThreads) void sgd_scale_kernel(const double* pa
     if (threadIdx.x == 0) {
         const double norm = sqrt(total);
         const bool finite = isfinite(norm);
+        // a held update (the step that produced the gradients failed) writes
+        // nothing, as for a non-finite norm
+        const bool held = hold != nullptr && *hold != 0u;
         double s = 1.0;
-        if (!finite) s = 0.0;
+        if (!finite || held) s = 0.0;
         else if (max_norm > 0.f && isfinite(max_norm)) s = fmin(1.0, double(max_norm) / (norm + 1e-6));
         ctrl->ls = float(double(lr) * s);
-        ctrl->skip = finite ? 0 : 1;
+        ctrl->skip = (finite && !held) ? 0 : 1;
         if (stats) {
             stats[0] = float(norm);
             stats[1] = float(s);
@@ -191,8 +195,8 @@ extern "C" size_t janus_sgd_workspace_bytes(const janus_sgd_desc* d) {
 }
 
 extern "C" janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* const* params, const float* const* grads,
-                                              const int64_t* sizes, float* stats, void* ws, size_t ws_bytes,
-                                              void* stream) {
+                                              const int64_t* sizes, float* stats, const uint32_t* hold, void* ws,
+                                              size_t ws_bytes, void* stream) {
     if (!d || d->n < 1 || !params || !grads || !sizes) return JANUS_ERR_INVALID_ARG;
     if (!dtype_ok(d->dtype)) return JANUS_ERR_UNSUPPORTED;
     if (!std::isfinite(d->lr) || std::isnan(d->max_norm)) return JANUS_ERR_INVALID_ARG;
@@ -219,7 +223,7 @@ extern "C" janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* con
     {
         TraceScope trace("sgd_scale", 0.0, 8.0 * nc * kSgdBlocks, st);
         hipLaunchKernelGGL(sgd_scale_kernel, dim3(1), dim3(kSgdThreads), 0, st, partial, nc * kSgdBlocks, d->lr,
-                           d->max_norm, ctrl, stats);
+                           d->max_norm, hold, ctrl, stats);
         JANUS_LAUNCH_CHECK();
     }
     const size_t es = dtype_size(d->dtype);

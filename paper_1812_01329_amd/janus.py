@@ -26,7 +26,7 @@ LOSS_SUMSQ, LOSS_MEAN = 0, 1
 
 EXPORTS = [
     "janus_lstm_workspace_bytes", "janus_lstm_seq_fwd", "janus_lstm_seq_bwd", "janus_lstm_device_report",
-    "janus_lstm_schedule",
+    "janus_lstm_fault_flag", "janus_lstm_schedule",
     "janus_treelstm_workspace_bytes", "janus_tree_schedule_build", "janus_treelstm_fwd",
     "janus_treelstm_bwd", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
     "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
@@ -115,6 +115,7 @@ def lib():
                                          vp, vp, vp, vp]
         L.janus_lstm_schedule.argtypes = [i32, i32, pi32, pi32, pi32, pi32, pi32]
         L.janus_lstm_device_report.argtypes = [C.POINTER(LstmDesc), vp, sz, C.POINTER(LstmReport), vp]
+        L.janus_lstm_fault_flag.argtypes = [C.POINTER(LstmDesc), vp, sz, C.POINTER(vp)]
         L.janus_treelstm_workspace_bytes.restype = sz
         L.janus_treelstm_workspace_bytes.argtypes = [C.POINTER(TreeDesc), i32, i32]
         L.janus_tree_schedule_build.argtypes = [C.POINTER(TreeBatchC), i32, pi32, pi32, pi32, pi32]
@@ -138,7 +139,7 @@ def lib():
         L.janus_sgd_workspace_bytes.restype = sz
         L.janus_sgd_workspace_bytes.argtypes = [C.POINTER(SgdDesc)]
         L.janus_sgd_clip_update.argtypes = [C.POINTER(SgdDesc), C.POINTER(vp), C.POINTER(vp),
-                                            C.POINTER(C.c_int64), vp, vp, sz, vp]
+                                            C.POINTER(C.c_int64), vp, vp, vp, sz, vp]
         L.janus_mse_workspace_bytes.restype = sz
         L.janus_mse_workspace_bytes.argtypes = [C.POINTER(MseDesc)]
         L.janus_linear_mse.argtypes = [C.POINTER(MseDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -227,8 +228,9 @@ def janus_lstm_seq_bwd(desc: LstmDesc, x, lengths, Wx, Wh, ws, dy, dhT, dcT, dx,
 
 
 def janus_lstm_device_report(desc: LstmDesc, ws, stream=None) -> dict:
-    """Synchronises the stream and returns the report of the last LSTM call on
-    this workspace; raises JanusError(DEVICE) if a barrier wait ran out."""
+    """Synchronises the stream and returns the report of the current step on
+    this workspace (the last forward and the backward after it); raises
+    JanusError(DEVICE) if a barrier wait ran out."""
     rep = LstmReport()
     st = lib().janus_lstm_device_report(C.byref(desc), _p(ws), ws.numel() * ws.element_size(), C.byref(rep),
                                         _stream(stream))
@@ -236,6 +238,14 @@ def janus_lstm_device_report(desc: LstmDesc, ws, stream=None) -> dict:
     return dict(timed_out=int(rep.timed_out), bwd_groups=int(rep.bwd_groups),
                 bwd_local_groups=int(rep.bwd_local_groups), fwd_groups=int(rep.fwd_groups),
                 fwd_local_groups=int(rep.fwd_local_groups))
+
+
+def janus_lstm_fault_flag(desc: LstmDesc, ws) -> int:
+    """Device address of the workspace's timeout word (see janus.h)."""
+    out = C.c_void_p(0)
+    st = lib().janus_lstm_fault_flag(C.byref(desc), _p(ws), ws.numel() * ws.element_size(), C.byref(out))
+    _check(st, "janus_lstm_fault_flag")
+    return int(out.value)
 
 
 def janus_lstm_schedule(B: int, T: int, lengths):
@@ -369,14 +379,16 @@ def sgd_workspace_bytes(desc: SgdDesc) -> int:
     return int(lib().janus_sgd_workspace_bytes(C.byref(desc)))
 
 
-def janus_sgd_clip_update(desc: SgdDesc, params, grads, stats=None, ws=None, stream=None):
+def janus_sgd_clip_update(desc: SgdDesc, params, grads, stats=None, ws=None, stream=None, hold=None):
     """SGD step with global-norm clipping on lists of flat device tensors
-    (parameters updated in place; float32 gradients)."""
+    (parameters updated in place; float32 gradients).  ``hold``: a device
+    address (int) of a uint32 that, when non-zero, keeps the update from
+    writing anything (janus_lstm_fault_flag's word)."""
     n = len(params)
     S = (C.c_int64 * n)(*[int(t.numel()) for t in params])
     wsb = 0 if ws is None else ws.numel() * ws.element_size()
-    st = lib().janus_sgd_clip_update(C.byref(desc), _ptr_array(params), _ptr_array(grads), S, _p(stats), _p(ws),
-                                     wsb, _stream(stream))
+    st = lib().janus_sgd_clip_update(C.byref(desc), _ptr_array(params), _ptr_array(grads), S, _p(stats),
+                                     None if hold is None else C.c_void_p(int(hold)), _p(ws), wsb, _stream(stream))
     _check(st, "janus_sgd_clip_update")
 
 

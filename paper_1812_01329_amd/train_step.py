@@ -49,8 +49,10 @@ class SgdUpdate:
         self.ws = torch.empty(J.sgd_workspace_bytes(self.desc), dtype=torch.uint8, device=dev)
         self.stats = torch.zeros(2, dtype=torch.float32, device=dev)   # [norm before clipping, scale]
 
-    def apply(self):
-        J.janus_sgd_clip_update(self.desc, self.params, self.grads, stats=self.stats, ws=self.ws)
+    def apply(self, hold: Optional[int] = None):
+        """``hold``: device address of a uint32 that, when non-zero at run
+        time, leaves every parameter unchanged (a failed step)."""
+        J.janus_sgd_clip_update(self.desc, self.params, self.grads, stats=self.stats, ws=self.ws, hold=hold)
 
 
 class LSTMStep:
@@ -126,6 +128,9 @@ class LSTMStep:
         if update is not None:
             P, G = self.parameters()
             self.update = SgdUpdate(P, G, *update)
+        # the timeout word of the step's recurrences: a step whose forward or
+        # backward wait ran out leaves the parameters unchanged
+        self.fault = J.janus_lstm_fault_flag(self.desc, self.ws)
 
     def carry_from(self, prev: "LSTMStep"):
         """Seeds this step's initial state with the final state of the step
@@ -177,7 +182,7 @@ class LSTMStep:
             J.janus_embed_softmax_xent(self.edesc, J.EMBED_BWD, self.ids_host, self.ids, inp=self.dx,
                                        dtable=self.dE)
         if self.update is not None:
-            self.update.apply()
+            self.update.apply(hold=self.fault)
 
     def results(self) -> Dict[str, object]:
         torch.cuda.synchronize()

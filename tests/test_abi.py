@@ -184,6 +184,29 @@ def test_lstm_device_report_rejects_bad_arguments():
     assert e.value.status == J.ERR_UNSUPPORTED
 
 
+def test_lstm_fault_flag_address():
+    """The timeout word is a 4-byte-aligned word inside the workspace; the
+    call validates like the report and reads or writes no memory (a host
+    buffer stands in for the workspace)."""
+    import ctypes as C
+    L = J.lib()
+    for (nl, I, H, B, T, dt) in [(2, 64, 256, 32, 8, J.BF16), (1, 4, 8, 3, 5, J.F32), (2, 650, 650, 20, 35, J.BF16)]:
+        d = J.LstmDesc(nl, I, H, B, T, dt)
+        need = J.janus_lstm_workspace_bytes(nl, I, H, B, T, dt)
+        raw = np.full(need + 512, 0x5A, np.uint8)
+        base = raw.ctypes.data + (-raw.ctypes.data) % 256
+        out = C.c_void_p(0)
+        assert L.janus_lstm_fault_flag(C.byref(d), C.c_void_p(base), need, C.byref(out)) == J.OK
+        assert base <= out.value <= base + need - 4 and out.value % 4 == 0
+        assert np.all(raw == 0x5A)
+        assert L.janus_lstm_fault_flag(C.byref(d), C.c_void_p(base), need, None) == J.ERR_INVALID_ARG
+        assert L.janus_lstm_fault_flag(C.byref(d), None, need, C.byref(out)) == J.ERR_WORKSPACE
+        assert L.janus_lstm_fault_flag(C.byref(d), C.c_void_p(base), need - 1, C.byref(out)) == J.ERR_WORKSPACE
+        assert L.janus_lstm_fault_flag(C.byref(d), C.c_void_p(base + 16), need, C.byref(out)) == J.ERR_WORKSPACE
+    bad = J.LstmDesc(1, 4, 8, 3, 5, 7)
+    assert L.janus_lstm_fault_flag(C.byref(bad), C.c_void_p(base), need, C.byref(out)) == J.ERR_UNSUPPORTED
+
+
 def test_lstm_bwd_rejects_bad_lengths_untouched():
     d, bf, W, U, b = _lstm_args()
     g = [_HostBuf(4 * 8 * 4 * 4) for _ in range(3)]
@@ -271,7 +294,7 @@ def _sgd_call(desc, params, grads, sizes, ws, ws_bytes):
     P = (C.c_void_p * max(n, 1))(*params)
     G = (C.c_void_p * max(n, 1))(*grads)
     S = (C.c_int64 * max(n, 1))(*sizes)
-    return L.janus_sgd_clip_update(None if desc is None else C.byref(desc), P, G, S, None, ws, ws_bytes, None)
+    return L.janus_sgd_clip_update(None if desc is None else C.byref(desc), P, G, S, None, None, ws, ws_bytes, None)
 
 
 def test_sgd_workspace_bytes():

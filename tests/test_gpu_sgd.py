@@ -181,3 +181,89 @@ def test_training_step_with_update(max_norm):
     d_gpu = np.concatenate([(b - a).ravel() for a, b in zip(P0, P1)])
     d_ref = np.concatenate([(b - a).ravel() for a, b in zip(P0, ref)])
     assert np.linalg.norm(d_gpu - d_ref) <= 1e-3 * np.linalg.norm(d_ref)
+
+
+def test_step_with_timed_out_recurrence_leaves_parameters(monkeypatch):
+    """All-or-nothing state change (Section 4.2.3): when a bounded wait of
+    the step's recurrences runs out, the update writes no parameter and the
+    report says so after the backward.  The timeout is forced from the host
+    by setting the workspace's timeout word between the forward and the
+    backward call (every wait of the backward's persistent kernels then
+    returns at once, so they drain normally).  A clean step before and after
+    shows that the report covers the forward on its own too, and that the
+    next forward clears the word."""
+    import torch
+    from paper_1812_01329_amd import janus as J
+    from paper_1812_01329_amd.train_step import make_step
+    from tests.test_gpu_parity import _lstm
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    # bf16, H = 1024, B = 64: the persistent forward (asked for in two
+    # slices, so that it reports its unit groups) and backward kernels
+    monkeypatch.setenv("JANUS_FWD_SLICES", "2")
+    w = _lstm("mse", "bf16", L=2, I=64, H=1024, B=64, T=5, seed=52, P=16)
+    print(f"[sgd-hold] {w.name}", flush=True)
+    step = make_step(w, update=(0.5, 0.0))
+    fwd_reports = []
+    orig_bwd = J.janus_lstm_seq_bwd
+    force = {"on": False}
+
+    def bwd(*args, **kw):
+        fwd_reports.append(J.janus_lstm_device_report(step.desc, step.ws))   # the forward's report
+        if force["on"]:
+            off = step.fault - step.ws.data_ptr()
+            assert 0 <= off <= step.ws.numel() - 4
+            step.ws[off:off + 4].copy_(torch.tensor([1, 0, 0, 0], dtype=torch.uint8))
+        return orig_bwd(*args, **kw)
+
+    monkeypatch.setattr(J, "janus_lstm_seq_bwd", bwd)
+    # a clean step: the forward and the whole step report no timeout, and the update applies
+    P0 = [_host(p) for p in step.parameters()[0]]
+    step.run()
+    rep = J.janus_lstm_device_report(step.desc, step.ws)
+    assert fwd_reports[-1]["timed_out"] == 0 and fwd_reports[-1]["fwd_groups"] > 0
+    assert rep["timed_out"] == 0 and rep["bwd_groups"] > 0
+    P1 = [_host(p) for p in step.parameters()[0]]
+    assert any(not np.array_equal(a, b) for a, b in zip(P0, P1))
+    # the forced timeout: no parameter changes, the scale reads 0, the report raises
+    force["on"] = True
+    step.run()
+    with pytest.raises(J.JanusError) as e:
+        J.janus_lstm_device_report(step.desc, step.ws)
+    assert e.value.status == J.ERR_DEVICE
+    P2 = [_host(p) for p in step.parameters()[0]]
+    for a, b in zip(P1, P2):
+        assert np.array_equal(a, b)
+    assert _host(step.update.stats)[1] == 0.0
+    # the next step's forward clears the word: clean again, and it updates
+    force["on"] = False
+    step.run()
+    assert J.janus_lstm_device_report(step.desc, step.ws)["timed_out"] == 0
+    P3 = [_host(p) for p in step.parameters()[0]]
+    assert any(not np.array_equal(a, b) for a, b in zip(P2, P3))
+
+
+def test_held_update_writes_nothing():
+    """janus_sgd_clip_update with a non-zero hold word writes no parameter
+    and reports scale 0; with a zero word it matches the oracle."""
+    import torch
+    from paper_1812_01329_amd import janus as J
+    assert torch.cuda.is_available(), "GPU tests need a GPU"
+    params, grads = _inputs(71, [(33,), (5, 7)], "f32")
+    P = [_dev(p.ravel(), "f32") for p in params]
+    G = [_dev(g.ravel(), "f32") for g in grads]
+    d = J.SgdDesc(len(P), J.F32, 0.3, 0.0)
+    ws = torch.empty(J.sgd_workspace_bytes(d), dtype=torch.uint8, device="cuda")
+    stats = torch.full((2,), -1.0, dtype=torch.float32, device="cuda")
+    hold = torch.ones(1, dtype=torch.int32, device="cuda")
+    print("[sgd-held] hold=1 then hold=0", flush=True)
+    J.janus_sgd_clip_update(d, P, G, stats=stats, ws=ws, hold=hold.data_ptr())
+    torch.cuda.synchronize()
+    for p, ref in zip(P, params):
+        assert np.array_equal(_host(p), np.asarray(ref, np.float32).ravel())
+    assert _host(stats)[1] == 0.0
+    hold.zero_()
+    J.janus_sgd_clip_update(d, P, G, stats=stats, ws=ws, hold=hold.data_ptr())
+    torch.cuda.synchronize()
+    ref, norm, s, applied = osgd.sgd_clip_update(params, grads, 0.3, 0.0)
+    assert applied and _host(stats)[1] == 1.0
+    _check([_host(p) for p in P], ref, params, grads, "f32", 0.3, s)

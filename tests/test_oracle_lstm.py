@@ -246,3 +246,58 @@ def test_subset_rows_reproduce_full_batch_values():
     np.testing.assert_allclose(sub["y"][:, 0], full["y"][:, 2], atol=1e-15)
     np.testing.assert_allclose(sub["dx"][:, 0], full["dx"][:, 2], atol=1e-15)
     np.testing.assert_allclose(sub["dh0"][:, 0], full["dh0"][:, 2], atol=1e-15)
+
+
+@pytest.mark.parametrize("lengths", [None, [6, 1, 4, 6], [3, 0, 5, 2]])
+def test_mean_final_loss_against_torch_lstm(lengths):
+    """The variable-length workload's loss is the mean of the final h over
+    B * H entries: torch.nn.LSTM with packed lengths, hn[-1].mean(), and
+    autograd fix both its value and every gradient, so a wrong normalisation
+    (1/B instead of 1/(B H), say) shows up here even though finite
+    differences of the oracle would follow it."""
+    w = small_lstm("mean_final", L=1, I=5, H=6, B=4, T=6, lengths=lengths, seed=11, h0=True)
+    if lengths is not None and 0 in lengths:
+        # torch's packed sequences reject length 0: run torch on the other
+        # rows and rescale; a length-0 row keeps h0 (tested elsewhere)
+        keep = [b for b in range(w.B) if lengths[b] > 0]
+        sub = copy.deepcopy(w)
+        sub.B = len(keep)
+        sub.x = np.asarray(w.x)[:, keep]
+        sub.lengths = np.asarray(lengths, np.int32)[keep]
+        sub.h0 = np.asarray(w.h0)[:, keep]
+        sub.c0 = np.asarray(w.c0)[:, keep]
+        lstm_t, x, h0, c0, y, hn, cn = _torch_lstm(sub)
+        zero = [b for b in range(w.B) if lengths[b] == 0]
+        loss = (hn[-1].sum() + torch.tensor(np.asarray(w.h0)[-1, zero]).sum()) / (w.B * w.H)
+    else:
+        keep = list(range(w.B))
+        lstm_t, x, h0, c0, y, hn, cn = _torch_lstm(w)
+        loss = hn[-1].mean()
+    loss.backward()
+    ref = steps.lstm_step(w)
+    np.testing.assert_allclose(ref["loss"], loss.item(), rtol=1e-13)
+    np.testing.assert_allclose(ref["dx"][:, keep], x.grad.numpy(), atol=1e-13)
+    np.testing.assert_allclose(ref["dh0"][:, keep], h0.grad.numpy(), atol=1e-13)
+    np.testing.assert_allclose(ref["dc0"][:, keep], c0.grad.numpy(), atol=1e-13)
+    for l in range(w.L):
+        np.testing.assert_allclose(ref["dWx"][l], getattr(lstm_t, f"weight_ih_l{l}").grad.numpy(), atol=1e-13)
+        np.testing.assert_allclose(ref["dWh"][l], getattr(lstm_t, f"weight_hh_l{l}").grad.numpy(), atol=1e-13)
+        np.testing.assert_allclose(ref["db"][l], getattr(lstm_t, f"bias_ih_l{l}").grad.numpy(), atol=1e-13)
+
+
+@pytest.mark.parametrize("shape", [(1,), (7,), (3, 5), (2, 4, 6)])
+def test_mean_all_against_torch_mean(shape):
+    """heads.mean_all: value and gradient of torch.mean under autograd, and
+    the closed form mean(0..n-1) = (n-1)/2 with gradient 1/n everywhere."""
+    rng = np.random.default_rng(sum(shape))
+    h = rng.standard_normal(shape)
+    loss, dh = heads.mean_all(h)
+    ht = torch.tensor(h, requires_grad=True)
+    lt = ht.mean()
+    lt.backward()
+    assert abs(loss - lt.item()) < 1e-14
+    np.testing.assert_allclose(dh, ht.grad.numpy(), rtol=0, atol=0)
+    n = int(np.prod(shape))
+    loss, dh = heads.mean_all(np.arange(n, dtype=np.float64).reshape(shape))
+    assert loss == (n - 1) / 2
+    assert dh.shape == shape and np.all(dh == 1.0 / n)
