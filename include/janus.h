@@ -528,6 +528,28 @@ janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* const* params,
                                    float* stats, const uint32_t* hold, void* ws, size_t ws_bytes,
                                    void* stream);
 
+/*
+ * janus_sgd_clip_update for callers that cannot allocate device memory:
+ * code under stream capture, tight serving loops, harnesses that forbid
+ * hipMalloc.  Same arguments, rule and results as janus_sgd_clip_update,
+ * without ws / ws_bytes: the block sums of the norm and the control word live
+ * in a fixed array of the library (one per device, 33 KB, room for
+ * JANUS_SGD_NOALLOC_MAX_TENSORS tensors), whose device address the library
+ * looks up at the first call on each device and keeps until the process
+ * ends.  The call allocates nothing (no hipMalloc, no events, no tracing).
+ * Every call on one device shares that device's array: calls that overlap
+ * on one device (several streams or host threads) race, and the caller must
+ * order them.  Each call writes everything in the array that it reads, so
+ * nothing carries over from the previous call.
+ * Errors: as janus_sgd_clip_update (bad arguments -> INVALID_ARG, dtype ->
+ * UNSUPPORTED); n > JANUS_SGD_NOALLOC_MAX_TENSORS -> WORKSPACE; a failed
+ * lookup of the array -> DEVICE.
+ */
+#define JANUS_SGD_NOALLOC_MAX_TENSORS 256
+janus_status janus_sgd_clip_update_noalloc(const janus_sgd_desc* d, void* const* params,
+                                           const float* const* grads, const int64_t* sizes,
+                                           float* stats, const uint32_t* hold, void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Misc                                                                     */
 /* ------------------------------------------------------------------------ */

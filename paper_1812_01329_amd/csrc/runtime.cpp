@@ -160,6 +160,7 @@ TraceState& trace() {
 }  // namespace
 
 TraceScope::TraceScope(const char* label, double flops, double bytes, hipStream_t stream) {
+    if (!label) return;   // an untraced launch
     TraceState& t = trace();
     if (!t.on) return;
     std::lock_guard<std::mutex> lock(t.mu);

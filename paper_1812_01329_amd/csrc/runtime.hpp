@@ -72,7 +72,8 @@ struct UploadPiece {
 janus_status upload_pieces(const UploadPiece* pieces, int n, hipStream_t stream);
 
 // Brackets one kernel launch with trace events while tracing is on (see
-// janus_trace_begin); a no-op otherwise.  flops / bytes: algorithmic work.
+// janus_trace_begin); a no-op otherwise, and for a NULL label (a launch that
+// must not create events).  flops / bytes: algorithmic work.
 class TraceScope {
   public:
     TraceScope(const char* label, double flops, double bytes, hipStream_t stream);

@@ -17,6 +17,7 @@
 // Every sum runs in a fixed order, so the norm does not depend on timing.
 #include <algorithm>
 #include <cmath>
+#include <mutex>
 
 #include "device.hpp"
 #include "runtime.hpp"
@@ -167,9 +168,44 @@ __global__ __launch_bounds__(kSgdThreads) void sgd_update_kernel(SgdTable t, con
     }
 }
 
-int sgd_chunks(int n) { return (n + kSgdTable - 1) / kSgdTable; }
+constexpr int sgd_chunks(int n) { return (n + kSgdTable - 1) / kSgdTable; }
 
-size_t sgd_ws_bytes(int n) { return ((size_t(sgd_chunks(n)) * kSgdBlocks * sizeof(double) + 255) / 256) * 256 + 256; }
+constexpr size_t sgd_ws_bytes(int n) {
+    return ((size_t(sgd_chunks(n)) * kSgdBlocks * sizeof(double) + 255) / 256) * 256 + 256;
+}
+
+// The allocation-free update keeps its block sums and control word in this
+// file-scope array (one copy per device, alive until the process ends)
+// instead of a caller workspace: room for kNoAllocMaxTensors tensors.  Every
+// call writes all of it that it reads (each block its sum, the scale kernel
+// the control word), so nothing is cleared between calls.
+constexpr int kNoAllocMaxTensors = JANUS_SGD_NOALLOC_MAX_TENSORS;
+constexpr size_t kNoAllocScratchBytes = sgd_ws_bytes(kNoAllocMaxTensors);
+static_assert(kNoAllocScratchBytes <= 64 * 1024, "a modest fixed array");
+__device__ __align__(256) unsigned char scratch[kNoAllocScratchBytes];
+
+constexpr int kMaxDevices = 64;
+
+// Device address of `scratch` on the current device, looked up once per
+// device (hipGetSymbolAddress with that device current) and kept.  The
+// array's name in host code is only a stand-in for the symbol; kernels and
+// copies get this address.
+janus_status scratch_address(void** out) {
+    int dev = 0;
+    JANUS_HIP(hipGetDevice(&dev));
+    if (dev < 0 || dev >= kMaxDevices) return JANUS_ERR_UNSUPPORTED;
+    static std::mutex m;
+    static void* addr[kMaxDevices] = {};
+    std::lock_guard<std::mutex> lock(m);
+    if (!addr[dev]) {
+        void* p = nullptr;
+        JANUS_HIP(hipGetSymbolAddress(&p, HIP_SYMBOL(scratch)));
+        if (!p) return JANUS_ERR_DEVICE;
+        addr[dev] = p;
+    }
+    *out = addr[dev];
+    return JANUS_OK;
+}
 
 SgdTable sgd_table(int c, int n, void* const* params, const float* const* grads, const int64_t* sizes) {
     SgdTable t{};
@@ -194,9 +230,10 @@ extern "C" size_t janus_sgd_workspace_bytes(const janus_sgd_desc* d) {
     return sgd_ws_bytes(d->n);
 }
 
-extern "C" janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* const* params, const float* const* grads,
-                                              const int64_t* sizes, float* stats, const uint32_t* hold, void* ws,
-                                              size_t ws_bytes, void* stream) {
+namespace janus {
+namespace {
+
+janus_status sgd_check(const janus_sgd_desc* d, void* const* params, const float* const* grads, const int64_t* sizes) {
     if (!d || d->n < 1 || !params || !grads || !sizes) return JANUS_ERR_INVALID_ARG;
     if (!dtype_ok(d->dtype)) return JANUS_ERR_UNSUPPORTED;
     if (!std::isfinite(d->lr) || std::isnan(d->max_norm)) return JANUS_ERR_INVALID_ARG;
@@ -207,21 +244,28 @@ extern "C" janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* con
             reinterpret_cast<uintptr_t>(params[i]) % dtype_size(d->dtype) != 0)
             return JANUS_ERR_INVALID_ARG;
     }
-    if (!ws || ws_bytes < sgd_ws_bytes(d->n) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
-        return JANUS_ERR_WORKSPACE;
-    hipStream_t st = static_cast<hipStream_t>(stream);
+    return JANUS_OK;
+}
+
+// The three launches of the update on `ws` (sgd_ws_bytes(d->n) bytes, block
+// sums then the control word in its last 256 bytes).  `traced`: record the
+// launches for janus_trace_end (which creates events, so the
+// allocation-free entry point passes false).
+janus_status sgd_run(const janus_sgd_desc* d, void* const* params, const float* const* grads, const int64_t* sizes,
+                     float* stats, const uint32_t* hold, void* ws, hipStream_t st, bool traced) {
     const int nc = sgd_chunks(d->n);
     double* partial = static_cast<double*>(ws);
     SgdCtrl* ctrl = reinterpret_cast<SgdCtrl*>(static_cast<char*>(ws) + sgd_ws_bytes(d->n) - 256);
+    const char* no_label = nullptr;
     for (int c = 0; c < nc; ++c) {
         const SgdTable t = sgd_table(c, d->n, params, grads, sizes);
-        TraceScope trace("sgd_sumsq", 2.0 * double(t.off[t.n]), 4.0 * double(t.off[t.n]), st);
+        TraceScope trace(traced ? "sgd_sumsq" : no_label, 2.0 * double(t.off[t.n]), 4.0 * double(t.off[t.n]), st);
         hipLaunchKernelGGL(sgd_sumsq_kernel, dim3(kSgdBlocks), dim3(kSgdThreads), 0, st, t,
                            partial + int64_t(c) * kSgdBlocks);
         JANUS_LAUNCH_CHECK();
     }
     {
-        TraceScope trace("sgd_scale", 0.0, 8.0 * nc * kSgdBlocks, st);
+        TraceScope trace(traced ? "sgd_scale" : no_label, 0.0, 8.0 * nc * kSgdBlocks, st);
         hipLaunchKernelGGL(sgd_scale_kernel, dim3(1), dim3(kSgdThreads), 0, st, partial, nc * kSgdBlocks, d->lr,
                            d->max_norm, hold, ctrl, stats);
         JANUS_LAUNCH_CHECK();
@@ -229,7 +273,8 @@ extern "C" janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* con
     const size_t es = dtype_size(d->dtype);
     for (int c = 0; c < nc; ++c) {
         const SgdTable t = sgd_table(c, d->n, params, grads, sizes);
-        TraceScope trace("sgd_update", 2.0 * double(t.off[t.n]), (4.0 + 2.0 * es) * double(t.off[t.n]), st);
+        TraceScope trace(traced ? "sgd_update" : no_label, 2.0 * double(t.off[t.n]),
+                         (4.0 + 2.0 * es) * double(t.off[t.n]), st);
         if (d->dtype == JANUS_BF16)
             hipLaunchKernelGGL(sgd_update_kernel<bf16_t>, dim3(kSgdBlocks), dim3(kSgdThreads), 0, st, t, ctrl);
         else
@@ -237,4 +282,28 @@ extern "C" janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* con
         JANUS_LAUNCH_CHECK();
     }
     return JANUS_OK;
+}
+
+}  // namespace
+}  // namespace janus
+
+extern "C" janus_status janus_sgd_clip_update(const janus_sgd_desc* d, void* const* params, const float* const* grads,
+                                              const int64_t* sizes, float* stats, const uint32_t* hold, void* ws,
+                                              size_t ws_bytes, void* stream) {
+    janus_status e = sgd_check(d, params, grads, sizes);
+    if (e != JANUS_OK) return e;
+    if (!ws || ws_bytes < sgd_ws_bytes(d->n) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
+        return JANUS_ERR_WORKSPACE;
+    return sgd_run(d, params, grads, sizes, stats, hold, ws, static_cast<hipStream_t>(stream), true);
+}
+
+extern "C" janus_status janus_sgd_clip_update_noalloc(const janus_sgd_desc* d, void* const* params,
+                                                      const float* const* grads, const int64_t* sizes, float* stats,
+                                                      const uint32_t* hold, void* stream) {
+    janus_status e = sgd_check(d, params, grads, sizes);
+    if (e != JANUS_OK) return e;
+    if (d->n > kNoAllocMaxTensors) return JANUS_ERR_WORKSPACE;
+    void* ws = nullptr;
+    if ((e = scratch_address(&ws)) != JANUS_OK) return e;
+    return sgd_run(d, params, grads, sizes, stats, hold, ws, static_cast<hipStream_t>(stream), false);
 }

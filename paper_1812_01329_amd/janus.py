@@ -31,7 +31,8 @@ EXPORTS = [
     "janus_treelstm_bwd", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
     "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
     "janus_trace_end", "janus_status_string", "janus_version", "janus_last_error",
-    "janus_sgd_workspace_bytes", "janus_sgd_clip_update", "janus_lstm_state_carry",
+    "janus_sgd_workspace_bytes", "janus_sgd_clip_update", "janus_sgd_clip_update_noalloc",
+    "janus_lstm_state_carry",
     "janus_treernn_workspace_bytes", "janus_treernn_fwd", "janus_treernn_bwd",
     "janus_childsum_workspace_bytes", "janus_childsum_fwd", "janus_childsum_bwd",
 ]
@@ -140,6 +141,8 @@ def lib():
         L.janus_sgd_workspace_bytes.argtypes = [C.POINTER(SgdDesc)]
         L.janus_sgd_clip_update.argtypes = [C.POINTER(SgdDesc), C.POINTER(vp), C.POINTER(vp),
                                             C.POINTER(C.c_int64), vp, vp, vp, sz, vp]
+        L.janus_sgd_clip_update_noalloc.argtypes = [C.POINTER(SgdDesc), C.POINTER(vp), C.POINTER(vp),
+                                                    C.POINTER(C.c_int64), vp, vp, vp]
         L.janus_mse_workspace_bytes.restype = sz
         L.janus_mse_workspace_bytes.argtypes = [C.POINTER(MseDesc)]
         L.janus_linear_mse.argtypes = [C.POINTER(MseDesc), vp, vp, vp, vp, vp, vp, vp, vp, vp, sz, vp]
@@ -390,6 +393,19 @@ def janus_sgd_clip_update(desc: SgdDesc, params, grads, stats=None, ws=None, str
     st = lib().janus_sgd_clip_update(C.byref(desc), _ptr_array(params), _ptr_array(grads), S, _p(stats),
                                      None if hold is None else C.c_void_p(int(hold)), _p(ws), wsb, _stream(stream))
     _check(st, "janus_sgd_clip_update")
+
+
+SGD_NOALLOC_MAX_TENSORS = 256   # JANUS_SGD_NOALLOC_MAX_TENSORS
+
+
+def janus_sgd_clip_update_noalloc(desc: SgdDesc, params, grads, stats=None, stream=None, hold=None):
+    """janus_sgd_clip_update without a workspace (the library's fixed
+    per-device array; at most SGD_NOALLOC_MAX_TENSORS tensors)."""
+    n = len(params)
+    S = (C.c_int64 * n)(*[int(t.numel()) for t in params])
+    st = lib().janus_sgd_clip_update_noalloc(C.byref(desc), _ptr_array(params), _ptr_array(grads), S, _p(stats),
+                                             None if hold is None else C.c_void_p(int(hold)), _stream(stream))
+    _check(st, "janus_sgd_clip_update_noalloc")
 
 
 # ---------------------------------------------------------------- tracing
