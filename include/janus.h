@@ -309,8 +309,7 @@ janus_status janus_treernn_fwd(const janus_treernn_desc* d, const janus_tree_bat
  *  dh_root [num_trees, H] float32: gradient of h_root.
  *  demb [V, H], dW [H, 2H], db [H]: float32, overwritten (rows of demb for
  *          words not in the batch are 0; a leaf's gradient is its dh).
- * Errors: as the forward; UNSUPPORTED when the batch has more than 16384
- * leaves.
+ * Errors: as the forward.
  */
 janus_status janus_treernn_bwd(const janus_treernn_desc* d, const janus_tree_batch* t,
                                const void* W, void* ws, size_t ws_bytes,
@@ -369,8 +368,7 @@ janus_status janus_childsum_fwd(const janus_childsum_desc* d, const janus_nary_t
  *  dh_root [num_trees, H] float32: gradient of h_root (the roots' c gets 0).
  *  demb [V, E], dW [4H, E], dU [4H, H], db [4H]: float32, overwritten (rows
  *          of demb for words not in the batch are 0).
- * Errors: as the forward; UNSUPPORTED when the batch has more than 16384
- * nodes.
+ * Errors: as the forward.
  */
 janus_status janus_childsum_bwd(const janus_childsum_desc* d, const janus_nary_tree_batch* t,
                                 const void* emb, const void* W, const void* U,
@@ -406,7 +404,13 @@ size_t janus_xent_workspace_bytes(const janus_xent_desc* d, janus_xent_op op);
  *           -log softmax(h Wout^T + bout)[ids[r]]; out = dh [rows, H] dtype;
  *           dtable = dWout [V, H], dbias = dbout [V] float32.
  *  EMBED_BWD:  in = dx [rows, H] dtype; dtable = dE [V, H] float32
- *           (deterministic: each row of dE sums its rows in ascending r).
+ *           (deterministic: each row of dE sums its rows in ascending r;
+ *           rows of ids not present are 0).  The rows are grouped by id on
+ *           the host from ids_host (a stable counting sort, O(rows + V)) and
+ *           one workgroup sums each group; any number of rows.
+ *  ws:      XENT_FWD_BWD and EMBED_BWD take a workspace of
+ *           janus_xent_workspace_bytes(d, op) bytes (256-byte aligned; for
+ *           EMBED_BWD 12 bytes per row); EMBED_FWD takes none (NULL).
  * Errors: INVALID_ARG, TOKEN (an id outside [0, V)), WORKSPACE.
  */
 janus_status janus_embed_softmax_xent(const janus_xent_desc* d, janus_xent_op op,

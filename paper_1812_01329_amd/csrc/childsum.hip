@@ -136,6 +136,7 @@ struct CsWs {
     float* Wt = nullptr;         // [E x 4H]
     float* Ut = nullptr;         // [H x 4H]
     float* part = nullptr;
+    int32_t* seg = nullptr;      // the nodes grouped by word, for the embedding gradient
 };
 
 size_t carve_cs(const janus_treelstm_desc& d, int32_t N, void* base, CsWs& w) {
@@ -158,6 +159,7 @@ size_t carve_cs(const janus_treelstm_desc& d, int32_t N, void* base, CsWs& w) {
     w.Wt = c.take<float>(int64_t(E) * 4 * H);
     w.Ut = c.take<float>(int64_t(H) * 4 * H);
     w.part = c.take<float>(colsum_partial_floats(4 * H));
+    w.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)));
     return c.off + 256;
 }
 
@@ -310,7 +312,6 @@ extern "C" janus_status janus_childsum_bwd(const janus_childsum_desc* d, const j
     janus_status e = prepare_cs(d, t, ws, ws_bytes, s, w, st);
     if (e != JANUS_OK) return e;
     const int H = d->H, E = d->E, N = s.N;
-    if (N > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
     const int L = int(s.level_offsets.size()) - 1;
     // roots have no parent: their dG rows and dc stay 0
     if ((e = zero_fill(w.G, sizeof(float) * size_t(N) * 4 * H, st)) != JANUS_OK) return e;
@@ -341,5 +342,5 @@ extern "C" janus_status janus_childsum_bwd(const janus_childsum_desc* d, const j
     e = simt_gemm<false, kSimtStore>("childsum_dx_gemm", N, E, 4 * H, w.dXW, 4 * H, nullptr,
                                      static_cast<const float*>(W), E, nullptr, nullptr, w.dx, E, st);
     if (e != JANUS_OK) return e;
-    return embed_backward(JANUS_F32, w.dx, w.pword, N, E, demb, d->V, st);
+    return embed_backward(JANUS_F32, w.dx, s.pword.data(), N, E, demb, d->V, w.seg, st);
 }

@@ -6,6 +6,7 @@
 // shuffles in a fixed butterfly, then a fixed sequence of partials), so two
 // runs on the same inputs give identical bits.
 #include <algorithm>
+#include <vector>
 
 #include "device.hpp"
 #include "ops.hpp"
@@ -65,55 +66,31 @@ __global__ void embed_fwd_kernel(const T* E, const int32_t* ids, int V, int H, T
     }
 }
 
-// dE[v] = sum of dx[r] over rows with ids[r] == v, summed in ascending r by
-// the block that owns the first occurrence of v (no atomics).
+// dE[id] = sum of dx over the rows of one group of equal ids, in ascending
+// row order.  seg = [order (rows) | off (nseg + 1) | sid (nseg)]: group g
+// covers order[off[g] .. off[g + 1]) and has id sid[g].  One workgroup per
+// group, threads over the columns; the rows of a frequent id are loaded eight
+// at a time and added in order, so the loads overlap and the sum is fixed.
 template <typename T>
-__global__ void embed_bwd_kernel(const T* dx, const int32_t* ids, int rows, int V, int H, float* dE) {
-    extern __shared__ int32_t sid[];   // ids[r ..), then in place the rows that match
-    __shared__ int nmatch;
-    __shared__ int owner;
-    const int r = blockIdx.x;
-    const int tid = threadIdx.x, lane = tid & 63;
-    const int32_t id = min(max(ids[r], 0), V - 1);
-    if (tid == 0) owner = 1;
-    __syncthreads();
-    for (int q = tid; q < r; q += blockDim.x)
-        if (min(max(ids[q], 0), V - 1) == id) owner = 0;
-    __syncthreads();
-    if (!owner) return;
-    const int n_rest = rows - r;
-    for (int q = tid; q < n_rest; q += blockDim.x) sid[q] = min(max(ids[r + q], 0), V - 1);
-    __syncthreads();
-    if (tid < 64) {
-        // wave 0 compacts the matching rows in ascending order; a chunk is
-        // read before any of its slots is written, and the matches so far
-        // never outnumber the entries read
-        int n = 0;
-        for (int q0 = 0; q0 < n_rest; q0 += 64) {
-            const int q = q0 + lane;
-            const bool m = q < n_rest && sid[q] == id;
-            const unsigned long long bal = __ballot(m);
-            if (m) sid[n + __popcll(bal & ((1ull << lane) - 1ull))] = r + q;
-            n += __popcll(bal);
-        }
-        if (lane == 0) nmatch = n;
-    }
-    __syncthreads();
-    const int n = nmatch;
-    // the rows of a frequent id (tens of them) are loaded eight at a time and
-    // added in ascending order, so the loads overlap and the sum stays fixed
-    for (int j = tid; j < H; j += blockDim.x) {
+__global__ void embed_bwd_seg_kernel(const T* dx, const int32_t* seg, int rows, int nseg, int H, float* dE) {
+    const int g = blockIdx.x;
+    const int32_t* order = seg;
+    const int32_t* off = seg + rows;
+    const int32_t* sid = off + nseg + 1;
+    const int k0 = off[g], k1 = off[g + 1];
+    const int64_t id = sid[g];
+    for (int j = threadIdx.x; j < H; j += blockDim.x) {
         float s = 0.f;
-        int k = 0;
-        for (; k + 8 <= n; k += 8) {
+        int k = k0;
+        for (; k + 8 <= k1; k += 8) {
             float v[8];
 #pragma unroll
-            for (int e = 0; e < 8; ++e) v[e] = to_f(dx[int64_t(sid[k + e]) * H + j]);
+            for (int e = 0; e < 8; ++e) v[e] = to_f(dx[int64_t(order[k + e]) * H + j]);
 #pragma unroll
             for (int e = 0; e < 8; ++e) s += v[e];
         }
-        for (; k < n; ++k) s += to_f(dx[int64_t(sid[k]) * H + j]);
-        dE[int64_t(id) * H + j] = s;
+        for (; k < k1; ++k) s += to_f(dx[int64_t(order[k]) * H + j]);
+        dE[id * H + j] = s;
     }
 }
 
@@ -249,6 +226,7 @@ using HeadBF16 = TileCfg<bf16_t, 128, 128, 32, 2, 2>;
 using HeadF32 = TileCfg<float, 64, 64, 32, 2, 2>;
 
 struct XentWs {
+    int32_t* seg = nullptr;      // EMBED_BWD: the rows grouped by id
     float* logits = nullptr;
     void* dz = nullptr;
     float* loss_rows = nullptr;
@@ -283,6 +261,7 @@ size_t carve_xent(const janus_xent_desc& d, janus_xent_op op, void* base, XentWs
         w.gs_bytes = head_gemm_scratch(d.dtype, d.rows, d.H, d.V);
         w.gs = c.take<char>(int64_t(w.gs_bytes));
     }
+    if (op == JANUS_EMBED_BWD) w.seg = c.take<int32_t>(int64_t(embed_seg_ints(d.rows)));
     return c.off + 256;
 }
 
@@ -469,20 +448,46 @@ janus_status xent_impl(const janus_xent_desc& d, const int32_t* ids_dev, const v
 
 }  // namespace
 
-janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_dev, int rows, int H, float* dE, int V,
-                            hipStream_t st) {
-    if (rows > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
+size_t embed_seg_ints(int rows) { return rows > 0 ? size_t(3) * rows + 1 : 1; }
+
+janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_host, int rows, int H, float* dE, int V,
+                            int32_t* seg_dev, hipStream_t st) {
     janus_status e = zero_fill(dE, size_t(V) * H * sizeof(float), st);
     if (e != JANUS_OK) return e;
     if (rows <= 0) return JANUS_OK;
-    const size_t sm = size_t(rows) * sizeof(int32_t);
-    TraceScope trace("embed_bwd", 0.0, double(rows) * H * (4.0 + dtype_size(dt)), st);
+    // stable counting sort by id: count, exclusive scan, place rows in
+    // ascending order within each id
+    std::vector<int32_t> count(size_t(V) + 1, 0);
+    for (int r = 0; r < rows; ++r) ++count[size_t(ids_host[r]) + 1];
+    int nseg = 0;
+    for (int v = 0; v < V; ++v) {
+        nseg += count[size_t(v) + 1] != 0;
+        count[size_t(v) + 1] += count[size_t(v)];
+    }
+    std::vector<int32_t> seg(size_t(rows) + 2 * size_t(nseg) + 1);
+    int32_t* order = seg.data();
+    int32_t* off = order + rows;
+    int32_t* sid = off + nseg + 1;
+    {
+        std::vector<int32_t> next(count.begin(), count.end() - 1);
+        for (int r = 0; r < rows; ++r) order[next[size_t(ids_host[r])]++] = r;
+        int g = 0;
+        for (int v = 0; v < V; ++v)
+            if (count[size_t(v) + 1] != count[size_t(v)]) {
+                off[g] = count[size_t(v)];
+                sid[g] = v;
+                ++g;
+            }
+        off[nseg] = rows;
+    }
+    if ((e = upload(seg_dev, seg.data(), seg.size() * sizeof(int32_t), st)) != JANUS_OK) return e;
+    TraceScope trace("embed_bwd", 0.0, double(rows) * H * dtype_size(dt) + double(nseg) * H * 4.0, st);
     if (dt == JANUS_BF16)
-        hipLaunchKernelGGL(embed_bwd_kernel<bf16_t>, dim3(rows), dim3(256), sm, st, static_cast<const bf16_t*>(dx),
-                           ids_dev, rows, V, H, dE);
+        hipLaunchKernelGGL(embed_bwd_seg_kernel<bf16_t>, dim3(unsigned(nseg)), dim3(256), 0, st,
+                           static_cast<const bf16_t*>(dx), seg_dev, rows, nseg, H, dE);
     else
-        hipLaunchKernelGGL(embed_bwd_kernel<float>, dim3(rows), dim3(256), sm, st, static_cast<const float*>(dx),
-                           ids_dev, rows, V, H, dE);
+        hipLaunchKernelGGL(embed_bwd_seg_kernel<float>, dim3(unsigned(nseg)), dim3(256), 0, st,
+                           static_cast<const float*>(dx), seg_dev, rows, nseg, H, dE);
     JANUS_LAUNCH_CHECK();
     return JANUS_OK;
 }
@@ -508,12 +513,11 @@ extern "C" janus_status janus_embed_softmax_xent(const janus_xent_desc* d, janus
     if (op == JANUS_XENT_FWD_BWD && (!table || !bias || !in || !out || !dtable || !dbias || !loss))
         return JANUS_ERR_INVALID_ARG;
     if (op == JANUS_EMBED_BWD && (!in || !dtable)) return JANUS_ERR_INVALID_ARG;
-    if (op == JANUS_EMBED_BWD && d->rows > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
     for (int32_t r = 0; r < d->rows; ++r)
         if (ids_host[r] < 0 || ids_host[r] >= d->V) return JANUS_ERR_TOKEN;
     XentWs w;
     const size_t need = carve_xent(*d, op, nullptr, w);
-    if (op == JANUS_XENT_FWD_BWD) {
+    if (op != JANUS_EMBED_FWD) {
         if (!ws || ws_bytes < need || reinterpret_cast<uintptr_t>(ws) % 256 != 0) return JANUS_ERR_WORKSPACE;
         carve_xent(*d, op, ws, w);
     }
@@ -541,7 +545,7 @@ extern "C" janus_status janus_embed_softmax_xent(const janus_xent_desc* d, janus
         JANUS_LAUNCH_CHECK();
         return JANUS_OK;
     }
-    if (op == JANUS_EMBED_BWD) return embed_backward(d->dtype, in, ids_dev, d->rows, d->H, dtable, d->V, st);
+    if (op == JANUS_EMBED_BWD) return embed_backward(d->dtype, in, ids_host, d->rows, d->H, dtable, d->V, w.seg, st);
     if (d->dtype == JANUS_BF16)
         return xent_impl<bf16_t>(*d, ids_dev, table, bias, in, out, dtable, dbias, loss, w, st);
     return xent_impl<float>(*d, ids_dev, table, bias, in, out, dtable, dbias, loss, w, st);

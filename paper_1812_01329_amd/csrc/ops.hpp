@@ -75,10 +75,14 @@ janus_status colsum(janus_dtype dt, const void* in, int64_t R, int C, int64_t ld
 // clear `bytes` bytes of device memory (a kernel, so it may be captured)
 janus_status zero_fill(void* p, size_t bytes, hipStream_t stream);
 
-// dE [V, H] float32 = 0, then dE[ids[r]] = sum of dx[r] over rows with that
-// id, in ascending r (one owner per id, no atomics).  rows <= kMaxEmbedBwdRows.
-constexpr int kMaxEmbedBwdRows = 16384;
-janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_dev, int rows, int H, float* dE, int V,
-                            hipStream_t stream);
+// dE [V, H] float32 = 0, then dE[ids[r]] = sum of dx[r] over the rows with
+// that id, in ascending r (deterministic, no atomics).  The rows are grouped
+// by id on the host (a stable counting sort of ids_host, already range
+// checked) and the groups go to the device in `seg_dev`, a region of
+// embed_seg_ints(rows) int32 of device memory the caller provides (a
+// workspace piece); one workgroup then sums each group.
+size_t embed_seg_ints(int rows);
+janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_host, int rows, int H, float* dE, int V,
+                            int32_t* seg_dev, hipStream_t stream);
 
 }  // namespace janus

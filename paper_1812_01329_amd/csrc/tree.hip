@@ -49,6 +49,7 @@ struct TreeWs {
     float* Wt = nullptr;         // [E x 5H]  W transposed (forward)
     float* Ut = nullptr;         // [2H x 5H] U transposed (forward)
     float* part = nullptr;
+    int32_t* seg = nullptr;      // the leaves grouped by word, for the embedding gradient
     int64_t ld5 = 0;
 };
 
@@ -72,6 +73,7 @@ size_t carve(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base, Tre
     w.Wt = c.take<float>(int64_t(d.E) * 5 * H);
     w.Ut = c.take<float>(int64_t(2) * H * 5 * H);
     w.part = c.take<float>(colsum_partial_floats(5 * H));
+    w.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)));
     return c.off + 256;
 }
 
@@ -252,8 +254,12 @@ janus_status check(const janus_treelstm_desc* d) {
     return JANUS_OK;
 }
 
-janus_status upload_tree(const janus_tree_batch* t, const TreeSchedule& s, const TreeWs& w, hipStream_t st) {
-    TreeHost h;
+// `keep`: receives the host arrays (the backward groups the leaves by word
+// from them)
+janus_status upload_tree(const janus_tree_batch* t, const TreeSchedule& s, const TreeWs& w, hipStream_t st,
+                         TreeHost* keep = nullptr) {
+    TreeHost local;
+    TreeHost& h = keep ? *keep : local;
     build_host(t, s, h);
     const size_t nb = sizeof(int32_t) * s.N;
     // carved one after another (nothing else between them): one copy
@@ -312,6 +318,7 @@ size_t carve_rnn(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base,
     w.dh = c.take<float>(int64_t(N) * H);
     w.Wt = c.take<float>(int64_t(2) * H * H);
     w.part = c.take<float>(colsum_partial_floats(H));
+    w.s.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)));
     return c.off + 256;
 }
 
@@ -412,9 +419,9 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
     janus_status e = prepare(d, t, ws, ws_bytes, s, w);
     if (e != JANUS_OK) return e;
     const int M0 = s.level_offsets[1];
-    if (M0 > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if ((e = upload_tree(t, s, w, st)) != JANUS_OK) return e;
+    TreeHost host;
+    if ((e = upload_tree(t, s, w, st, &host)) != JANUS_OK) return e;
     const int H = d->H, E = d->E, N = s.N;
     const int64_t kh = int64_t(t->num_trees) * H;
     {
@@ -468,7 +475,7 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
     e = simt_gemm<false, kSimtStore>("tree_dx_gemm", M0, E, 5 * H, w.A, w.ld5, nullptr, static_cast<const float*>(W), E,
                                      nullptr, nullptr, w.dxl, E, st);
     if (e != JANUS_OK) return e;
-    return embed_backward(JANUS_F32, w.dxl, w.lword, M0, E, demb, d->V, st);
+    return embed_backward(JANUS_F32, w.dxl, host.lword.data(), M0, E, demb, d->V, w.seg, st);
 }
 
 extern "C" size_t janus_treernn_workspace_bytes(const janus_treernn_desc* d, int32_t max_nodes, int32_t max_trees) {
@@ -524,9 +531,9 @@ extern "C" janus_status janus_treernn_bwd(const janus_treernn_desc* d, const jan
     janus_status e = prepare_rnn(d, t, ws, ws_bytes, s, w);
     if (e != JANUS_OK) return e;
     const int M0 = s.level_offsets[1];
-    if (M0 > kMaxEmbedBwdRows) return JANUS_ERR_UNSUPPORTED;
     hipStream_t st = static_cast<hipStream_t>(stream);
-    if ((e = upload_tree(t, s, w.s, st)) != JANUS_OK) return e;
+    TreeHost host;
+    if ((e = upload_tree(t, s, w.s, st, &host)) != JANUS_OK) return e;
     const int H = d->H, N = s.N;
     const int64_t kh = int64_t(t->num_trees) * H;
     {
@@ -559,5 +566,5 @@ extern "C" janus_status janus_treernn_bwd(const janus_treernn_desc* d, const jan
         return e;
     }
     // the leaves' dh is the gradient of their word vectors
-    return embed_backward(JANUS_F32, w.dh, w.s.lword, M0, H, demb, d->V, st);
+    return embed_backward(JANUS_F32, w.dh, host.lword.data(), M0, H, demb, d->V, w.s.seg, st);
 }

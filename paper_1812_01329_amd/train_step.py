@@ -107,6 +107,8 @@ class LSTMStep:
             self.edesc = J.XentDesc(w.V, I, T * B, self.desc.dtype)
             xw = J.janus_xent_workspace_bytes(w.V, H, T * B, self.desc.dtype, J.XENT_FWD_BWD)
             self.xws = torch.empty(xw, dtype=torch.uint8, device=device)
+            ew = J.janus_xent_workspace_bytes(w.V, I, T * B, self.desc.dtype, J.EMBED_BWD)
+            self.ews = torch.empty(ew, dtype=torch.uint8, device=device)
         else:
             self.x = _dev(w.x, tdt, device)
             self.dx = None if self.skip_dx else zeros(T, B, I, dt=tdt)
@@ -180,7 +182,7 @@ class LSTMStep:
                              self.dx, self.dh0, self.dc0, self.dWx, self.dWh, self.db)
         if w.head == "xent":
             J.janus_embed_softmax_xent(self.edesc, J.EMBED_BWD, self.ids_host, self.ids, inp=self.dx,
-                                       dtable=self.dE)
+                                       dtable=self.dE, ws=self.ews)
         if self.update is not None:
             self.update.apply(hold=self.fault)
 

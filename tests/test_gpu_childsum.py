@@ -63,3 +63,11 @@ def test_childsum_wide_hidden():
     """H = 320: the level contraction's N = 4H = 1280 columns in 20 blocks,
     the dh contraction's K = 1280 in two LDS chunks."""
     _run_and_check(wl.sst_childsum(n_trees=5, E=40, H=320, V=64, seed=84))
+
+
+def test_childsum_many_nodes():
+    """More than 16384 nodes, each with a word (520 trees of 35-45 nodes):
+    the embedding gradient has no row limit."""
+    w = wl.sst_childsum(n_trees=520, E=8, H=8, V=300, min_nodes=35, max_nodes=45, seed=75)
+    assert w.trees.num_nodes > 16384
+    _run_and_check(w)

@@ -63,14 +63,44 @@ def test_embedding_gather_and_scatter(dtype, V, Hd, rows, kind):
     torch.cuda.synchronize()
     np.testing.assert_array_equal(_host(x), H_.embed_forward(E, ids))
     dE = torch.full((V, Hd), 7.0, dtype=torch.float32, device="cuda:0")   # overwritten, not accumulated
-    J.janus_embed_softmax_xent(desc, J.EMBED_BWD, ids, ids_dev, inp=_dev(dx, dtype), dtable=dE)
+    ews = torch.empty(J.janus_xent_workspace_bytes(V, Hd, rows, dt, J.EMBED_BWD), dtype=torch.uint8, device="cuda:0")
+    J.janus_embed_softmax_xent(desc, J.EMBED_BWD, ids, ids_dev, inp=_dev(dx, dtype), dtable=dE, ws=ews)
     torch.cuda.synchronize()
     first = dE.cpu().numpy().copy()
     ref = H_.embed_backward(V, dx, ids)
     check("dE", first, ref, TOL["f32"]["grad"])
     untouched = np.setdiff1d(np.arange(V), ids)
     assert np.all(first[untouched] == 0.0)
-    J.janus_embed_softmax_xent(desc, J.EMBED_BWD, ids, ids_dev, inp=_dev(dx, dtype), dtable=dE)
+    J.janus_embed_softmax_xent(desc, J.EMBED_BWD, ids, ids_dev, inp=_dev(dx, dtype), dtable=dE, ws=ews)
+    torch.cuda.synchronize()
+    np.testing.assert_array_equal(dE.cpu().numpy(), first)
+
+
+@pytest.mark.parametrize("dtype,V,Hd,rows", [("bf16", 10000, 650, 20000), ("f32", 20000, 300, 24000),
+                                             ("bf16", 10000, 64, 1)])
+def test_embedding_backward_many_zipf_rows(dtype, V, Hd, rows):
+    """EMBED_BWD past the old 16384-row limit, with Zipf(1.1) ids (the most
+    frequent id holds about 15 % of the rows): the sums in ascending row
+    order of each id, against the oracle, and identical bits on a repeat."""
+    import torch
+    from paper_1812_01329_amd import janus as J
+    from paper_1812_01329_amd import workloads as wl
+    rng = np.random.default_rng(rows + V)
+    ids = wl.zipf_truncated(rng, 1.1, V, rows).astype(np.int32)
+    print(f"[embed-zipf] {dtype} V={V} H={Hd} rows={rows} distinct={len(np.unique(ids))}", flush=True)
+    dx = _vals(rng, (rows, Hd), 1.0, dtype)
+    dt = J.BF16 if dtype == "bf16" else J.F32
+    desc = J.XentDesc(V, Hd, rows, dt)
+    ids_dev = torch.from_numpy(ids).to("cuda:0")
+    dE = torch.full((V, Hd), 7.0, dtype=torch.float32, device="cuda:0")
+    ews = torch.empty(J.janus_xent_workspace_bytes(V, Hd, rows, dt, J.EMBED_BWD), dtype=torch.uint8, device="cuda:0")
+    dxd = _dev(dx, dtype)
+    J.janus_embed_softmax_xent(desc, J.EMBED_BWD, ids, ids_dev, inp=dxd, dtable=dE, ws=ews)
+    torch.cuda.synchronize()
+    first = dE.cpu().numpy().copy()
+    check("dE", first, H_.embed_backward(V, dx, ids), TOL["f32"]["grad"])
+    assert np.all(first[np.setdiff1d(np.arange(V), ids)] == 0.0)
+    J.janus_embed_softmax_xent(desc, J.EMBED_BWD, ids, ids_dev, inp=dxd, dtable=dE, ws=ews)
     torch.cuda.synchronize()
     np.testing.assert_array_equal(dE.cpu().numpy(), first)
 

@@ -103,6 +103,20 @@ def test_treelstm_wide_hidden_fp32():
         check(k, g[k], r[k], t["grad"])
 
 
+def test_treelstm_many_leaves_fp32():
+    """More than 16384 leaves in one batch (700 trees of 25-31 leaves): the
+    embedding gradient groups the leaves by word on the host, with no row
+    limit."""
+    w = wl.sst_treelstm(n_trees=700, E=8, H=8, V=500, min_leaves=25, max_leaves=31, seed=14)
+    assert int((w.trees.left < 0).sum()) > 16384
+    _, g = _run(w)
+    r = oracle_steps.tree_step(w)
+    t = TOL["f32"]
+    check("h_root", g["h_root"], r["h_root"], t["out"])
+    for k in ("dW", "dU", "db", "demb"):
+        check(k, g[k], r[k], t["grad"])
+
+
 def test_lm2048_reduced_shape_bf16():
     """The regression workload's structure (2 layers, projection + MSE) at a
     shape the oracle runs in seconds, spanning several tiles with ragged tails."""

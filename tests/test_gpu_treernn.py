@@ -56,3 +56,12 @@ def test_treernn_only_leaves():
     w = wl.sst_treernn(n_trees=4, H=32, V=20, seed=73, sizes=[1, 1, 1, 1])
     g, _ = _run_and_check(w)
     assert not g["dW"].any() and not g["db"].any()
+
+
+def test_treernn_many_leaves():
+    """More than 16384 leaves in one batch (700 trees of 25-31 leaves): the
+    embedding gradient groups the leaves by word on the host, with no row
+    limit."""
+    w = wl.sst_treernn(n_trees=700, H=8, V=500, seed=74, min_leaves=25, max_leaves=31)
+    assert int((w.trees.left < 0).sum()) > 16384
+    _run_and_check(w)
