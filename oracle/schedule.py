@@ -114,3 +114,68 @@ def tree_schedule(left, right, word, root, V):
     offsets = [sum(1 for n in range(N) if level[n] < k) for k in range(num_levels + 1)]
     return (np.asarray(level, np.int32), np.asarray(offsets, np.int32),
             np.asarray(order, np.int32), num_levels)
+
+
+def nary_schedule(offsets, children, word, root, V):
+    """Trees of any arity given as child lists: node n's children are
+    children[offsets[n]:offsets[n + 1]].  Every node carries a word (the
+    Child-Sum TreeLSTM reads x at every node).
+
+        level(n) = 0 without children, else 1 + max over its children
+        order    = node ids sorted by (level, id)
+
+    Checks, in this order: offsets start at 0 and never decrease; every
+    child id is in range and has one parent; every word lies in [0, V);
+    roots are in range, parentless and distinct, and every node is reached
+    from exactly one root (no cycles, no strays).  Returns (level,
+    level_offsets, order, num_levels)."""
+    offsets = [int(v) for v in offsets]
+    N = len(offsets) - 1
+    if N <= 0 or len(root) == 0:
+        raise ScheduleError("tree", "empty batch")
+    if offsets[0] != 0:
+        raise ScheduleError("tree", "offsets do not start at 0")
+    for n in range(N):
+        if offsets[n + 1] < offsets[n]:
+            raise ScheduleError("tree", f"offsets decrease at node {n}")
+    kids = [int(children[e]) for e in range(offsets[N])]
+    has_parent = [False] * N
+    for c in kids:
+        if not (0 <= c < N) or has_parent[c]:
+            raise ScheduleError("tree", f"bad or shared child {c}")
+        has_parent[c] = True
+    for n in range(N):
+        if not (0 <= int(word[n]) < V):
+            raise ScheduleError("token", f"node {n}: word {word[n]} outside [0, {V})")
+    seen = set()
+    for k in root:
+        k = int(k)
+        if not (0 <= k < N) or has_parent[k] or k in seen:
+            raise ScheduleError("tree", f"bad root {k}")
+        seen.add(k)
+    reached = [False] * N
+    stack = [int(k) for k in root]
+    while stack:
+        n = stack.pop()
+        if reached[n]:
+            raise ScheduleError("tree", "node reached twice")
+        reached[n] = True
+        stack.extend(kids[offsets[n]:offsets[n + 1]])
+    if not all(reached):
+        raise ScheduleError("tree", "node not reachable from a root")
+    level = [None] * N
+    sys.setrecursionlimit(max(10000, 4 * N + 100))
+
+    def height(n):
+        if level[n] is None:
+            ch = kids[offsets[n]:offsets[n + 1]]
+            level[n] = 0 if not ch else 1 + max(height(c) for c in ch)
+        return level[n]
+
+    for k in root:
+        height(int(k))
+    num_levels = max(level) + 1
+    order = sorted(range(N), key=lambda n: (level[n], n))
+    level_offsets = [sum(1 for n in range(N) if level[n] < k) for k in range(num_levels + 1)]
+    return (np.asarray(level, np.int32), np.asarray(level_offsets, np.int32),
+            np.asarray(order, np.int32), num_levels)

@@ -35,89 +35,6 @@ namespace janus {
 
 namespace {
 
-// Host schedule: nodes ordered by (level, id); children lists by position.
-struct NarySchedule {
-    int32_t N = 0;
-    std::vector<int32_t> level_offsets;   // [num_levels + 1]
-    std::vector<int32_t> pword, pcoff, pkids, rootk, rootpos;
-};
-
-janus_status build_nary_schedule(const janus_nary_tree_batch* t, int32_t V, NarySchedule& s) {
-    if (!t || t->num_trees <= 0 || t->num_nodes <= 0 || !t->child_offsets || !t->word || !t->root)
-        return JANUS_ERR_INVALID_ARG;
-    const int32_t N = t->num_nodes, K = t->num_trees;
-    const int32_t* off = t->child_offsets;
-    if (off[0] != 0) return JANUS_ERR_TREE;
-    for (int32_t n = 0; n < N; ++n)
-        if (off[n + 1] < off[n]) return JANUS_ERR_TREE;
-    const int32_t E = off[N];
-    if (E > 0 && !t->children) return JANUS_ERR_INVALID_ARG;
-    std::vector<int32_t> parent(N, -1);
-    for (int32_t e = 0; e < E; ++e) {
-        const int32_t c = t->children[e];
-        if (c < 0 || c >= N || parent[c] >= 0) return JANUS_ERR_TREE;
-        parent[c] = 1;
-    }
-    for (int32_t n = 0; n < N; ++n)
-        if (t->word[n] < 0 || t->word[n] >= V) return JANUS_ERR_TOKEN;
-    // levels by an explicit post-order walk from every root; a node seen twice
-    // or never is malformed (a cycle, a shared child, an unreachable node)
-    std::vector<int32_t> level(N, -1), state(N, 0), rootk(N, -1);
-    std::vector<std::pair<int32_t, int32_t>> stack;
-    int32_t seen = 0;
-    for (int32_t k = 0; k < K; ++k) {
-        const int32_t r = t->root[k];
-        if (r < 0 || r >= N || parent[r] >= 0 || state[r] != 0) return JANUS_ERR_TREE;
-        rootk[r] = k;
-        stack.push_back({r, off[r]});
-        state[r] = 1;
-        while (!stack.empty()) {
-            auto& [n, next] = stack.back();
-            if (next < off[n + 1]) {
-                const int32_t c = t->children[next++];
-                if (state[c] != 0) return JANUS_ERR_TREE;
-                state[c] = 1;
-                stack.push_back({c, off[c]});
-            } else {
-                int32_t lv = 0;
-                for (int32_t e = off[n]; e < off[n + 1]; ++e) lv = std::max(lv, level[t->children[e]] + 1);
-                level[n] = lv;
-                state[n] = 2;
-                ++seen;
-                stack.pop_back();
-            }
-        }
-    }
-    if (seen != N) return JANUS_ERR_TREE;
-    int32_t L = 0;
-    for (int32_t n = 0; n < N; ++n) L = std::max(L, level[n] + 1);
-    s.N = N;
-    s.level_offsets.assign(L + 1, 0);
-    for (int32_t n = 0; n < N; ++n) ++s.level_offsets[level[n] + 1];
-    for (int32_t k = 0; k < L; ++k) s.level_offsets[k + 1] += s.level_offsets[k];
-    std::vector<int32_t> pos(N), fill(s.level_offsets.begin(), s.level_offsets.end() - 1);
-    for (int32_t n = 0; n < N; ++n) pos[n] = fill[level[n]]++;   // ascending id within a level
-    s.pword.assign(N, 0);
-    s.rootk.assign(N, -1);
-    s.rootpos.assign(K, 0);
-    s.pcoff.assign(N + 1, 0);
-    std::vector<int32_t> node_at(N);
-    for (int32_t n = 0; n < N; ++n) node_at[pos[n]] = n;
-    for (int32_t p = 0; p < N; ++p) {
-        const int32_t n = node_at[p];
-        s.pword[p] = t->word[n];
-        s.rootk[p] = rootk[n];
-        s.pcoff[p + 1] = s.pcoff[p] + (off[n + 1] - off[n]);
-    }
-    s.pkids.assign(std::max(E, 1), 0);
-    for (int32_t p = 0; p < N; ++p) {
-        const int32_t n = node_at[p];
-        for (int32_t e = off[n], q = s.pcoff[p]; e < off[n + 1]; ++e, ++q) s.pkids[q] = pos[t->children[e]];
-    }
-    for (int32_t k = 0; k < K; ++k) s.rootpos[k] = pos[t->root[k]];
-    return JANUS_OK;
-}
-
 struct CsWs {
     int32_t* pword = nullptr;    // [N] word of the node at each position
     int32_t* pcoff = nullptr;    // [N + 1] children of position p: pkids[pcoff[p] .. pcoff[p + 1])

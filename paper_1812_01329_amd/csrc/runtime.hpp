@@ -31,9 +31,22 @@ struct TreeSchedule {
     std::vector<int32_t> pos;            // [N] level-ordered position of each node
 };
 
+// Trees of any arity (child lists): nodes ordered by (level, id), a node's
+// level one more than its highest child's; children lists by position.
+struct NarySchedule {
+    int32_t N = 0;
+    std::vector<int32_t> level_offsets;   // [num_levels + 1]
+    std::vector<int32_t> pword;           // [N] word of the node at each position
+    std::vector<int32_t> pcoff;           // [N + 1] children of position p: pkids[pcoff[p] .. pcoff[p + 1])
+    std::vector<int32_t> pkids;           // [max(E, 1)] child positions
+    std::vector<int32_t> rootk;           // [N] tree index of a root position, -1 otherwise
+    std::vector<int32_t> rootpos;         // [K] position of root k
+};
+
 janus_status build_seq_schedule(int32_t B, int32_t T, const int32_t* lengths, SeqSchedule& s);
 janus_status validate_tree_batch(const janus_tree_batch* t, int32_t V);
 janus_status build_tree_schedule(const janus_tree_batch* t, int32_t V, TreeSchedule& s);
+janus_status build_nary_schedule(const janus_nary_tree_batch* t, int32_t V, NarySchedule& s);
 
 // ---------------------------------------------------------------- workspace
 // Bump allocator used both to size a workspace (base == nullptr) and to

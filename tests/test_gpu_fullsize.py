@@ -2,10 +2,15 @@
 batch 256, length 256, projection 2048 + MSE, bf16 storage with float32
 accumulation), in the launch configuration the benchmark times.
 
-Two independent checks:
+Three independent checks:
   * sampled elements of every output and gradient against values the
     float64 oracle wrote for the whole batch (tests/golden/lm2048_golden.json,
     written by tests/golden/make_lm2048_golden.py);
+  * whole rows (one per gate block) and whole columns of the weight
+    gradients dWx[l], dWh[l], and all of db[l], element by element, against
+    the same oracle run (tests/golden/lm2048_slices.npz, same script): an
+    error confined to a few rows or columns after 256 accumulated steps
+    would slip past the samples;
   * whole rows of the per-sequence outputs (y, hT, cT, dh0, dc0) for a few
     sequences against the oracle run on just those sequences, which gives
     the same values because every per-sequence output depends only on its
@@ -25,6 +30,7 @@ from tests.parity import TOL, check
 pytestmark = pytest.mark.gpu
 
 GOLDEN = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "lm2048_golden.json")
+SLICES = os.path.join(os.path.dirname(os.path.abspath(__file__)), "golden", "lm2048_slices.npz")
 
 
 @pytest.fixture(scope="module")
@@ -70,6 +76,25 @@ def test_sampled_against_full_batch_oracle(full_step):
         # the tensor's own scale agrees with the oracle's
         amax = float(np.abs(arr).max())
         assert abs(amax - rec["absmax"]) <= tol * rec["absmax"] + 1e-30, (key, amax, rec["absmax"])
+
+
+def test_weight_gradient_rows_and_columns(full_step):
+    w, g = full_step
+    gold = np.load(SLICES, allow_pickle=False)
+    t = TOL["bf16"]["grad"]
+    for k in ("dWx", "dWh"):
+        for l in range(w.L):
+            got = g[k][l]
+            scale = float(gold[f"{k}{l}_absmax"])
+            rows, cols = gold[f"{k}{l}_rows"], gold[f"{k}{l}_cols"]
+            for name, a, ref in ((f"{k}[{l}] rows {rows.tolist()}", got[rows], gold[f"{k}{l}_rowvals"]),
+                                 (f"{k}[{l}] cols {cols.tolist()}", got[:, cols], gold[f"{k}{l}_colvals"])):
+                assert a.shape == ref.shape, name
+                err = np.abs(a - ref.astype(np.float64)).max() / max(scale, 1e-30)
+                print(f"[fullsize] {name}: relative error {err:.3e}", flush=True)
+                assert err <= t, f"{name}: relative error {err:.3e} > {t:.1e}"
+    for l in range(w.L):
+        check(f"db[{l}] (all)", g["db"][l], gold[f"db{l}"].astype(np.float64), t)
 
 
 def test_whole_sequences_against_oracle(full_step):
