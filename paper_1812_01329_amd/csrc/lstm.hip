@@ -77,7 +77,6 @@ struct LstmWs {
 // ------------------------------------------------------- persistent path
 struct DeviceInfo {
     int cus = 0;
-    int coop = 0;
     size_t lds = 0;
     int xccs = 0;
 };
@@ -95,7 +94,6 @@ DeviceInfo device_info() {
         DeviceInfo d;
         int v = 0;
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) d.cus = v;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeCooperativeLaunch, dev) == hipSuccess) d.coop = v;
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess) d.lds = size_t(v);
         if (hipDeviceGetAttribute(&v, hipDeviceAttributeNumberOfXccs, dev) == hipSuccess) d.xccs = v;
         // a failed query must not surface as the error of a later launch check
@@ -295,7 +293,7 @@ bool use_persistent(const janus_lstm_desc& d) {
     const bool env = !(e && e[0] == '0');
     if (!env || d.dtype != JANUS_BF16 || d.H % 8 != 0 || d.B > persist::kMaxB) return false;
     const DeviceInfo info = device_info();
-    if (!info.coop || info.cus <= 0) return false;
+    if (info.cus <= 0) return false;
     return persist_fwd_slices(d) > 0 && persist_bwd_slices(d) > 0;
 }
 
@@ -896,12 +894,29 @@ bool weight_aligned(const janus_lstm_desc& d) {
     return (int64_t(d.H) * int64_t(dtype_size(d.dtype))) % 16 == 0;
 }
 
-template <class K>
-janus_status coop_launch(K kernel, int blocks, size_t smem, void* arg, hipStream_t st, size_t& attr_smem) {
+// Launch of a persistent kernel: an ordinary dispatch on the caller's stream.
+// The grid barrier needs every workgroup resident at once.  The fit checks
+// allow at most one workgroup per CU and no more workgroups than CUs, and the
+// occupancy query below confirms that the registers and LDS of one workgroup
+// fit a CU, so on a device that runs nothing else every workgroup is placed
+// at launch.  Should some not be (another process holding CUs), the waits are
+// bounded: they set the error flag, the grid drains, and the device report
+// returns JANUS_ERR_DEVICE.
+//
+// A cooperative launch would make the runtime check residency itself, but it
+// dispatches through a second hardware queue, ordered against the caller's
+// stream with extra barrier packets around every launch; under a profiler
+// that queue's teardown ended the process with a segmentation fault at exit.
+template <class K, class A>
+janus_status persistent_launch(K kernel, int blocks, size_t smem, const A& args, hipStream_t st, size_t& attr_smem) {
     if (janus_status e = raise_lds_limit(kernel, smem, attr_smem); e != JANUS_OK) return e;
-    void* args[] = {arg};
-    JANUS_HIP(hipLaunchCooperativeKernel(reinterpret_cast<const void*>(kernel), dim3(blocks), dim3(persist::kThreads),
-                                         args, unsigned(smem), st));
+    const DeviceInfo info = device_info();
+    int per_cu = 0;
+    JANUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kernel),
+                                                           persist::kThreads, smem));
+    if (per_cu < 1 || int64_t(per_cu) * info.cus < blocks) return JANUS_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(kernel, dim3(blocks), dim3(persist::kThreads), smem, st, args);
+    JANUS_LAUNCH_CHECK();
     return JANUS_OK;
 }
 
@@ -914,10 +929,10 @@ janus_status launch_fwd_persistent(const janus_lstm_desc& d, int ns, persist::Fw
     TraceScope trace("lstm_fwd_persistent", flops, 0.0, st);
 #define JANUS_FWD_CASES(NS, I)                                                                               \
     switch (kw) {                                                                                            \
-        case 1: return coop_launch(persist::lstm_fwd_persistent<1, NS>, blocks, smem, &a, st, attr[I][0]); \
-        case 2: return coop_launch(persist::lstm_fwd_persistent<2, NS>, blocks, smem, &a, st, attr[I][1]); \
-        case 4: return coop_launch(persist::lstm_fwd_persistent<4, NS>, blocks, smem, &a, st, attr[I][2]); \
-        default: return coop_launch(persist::lstm_fwd_persistent<8, NS>, blocks, smem, &a, st, attr[I][3]); \
+        case 1: return persistent_launch(persist::lstm_fwd_persistent<1, NS>, blocks, smem, a, st, attr[I][0]); \
+        case 2: return persistent_launch(persist::lstm_fwd_persistent<2, NS>, blocks, smem, a, st, attr[I][1]); \
+        case 4: return persistent_launch(persist::lstm_fwd_persistent<4, NS>, blocks, smem, a, st, attr[I][2]); \
+        default: return persistent_launch(persist::lstm_fwd_persistent<8, NS>, blocks, smem, a, st, attr[I][3]); \
     }
     if (ns == 4) JANUS_FWD_CASES(4, 2)
     if (ns == 2) JANUS_FWD_CASES(2, 1)
@@ -934,17 +949,17 @@ janus_status launch_bwd_persistent(const janus_lstm_desc& d, int ns, persist::Bw
     TraceScope trace("lstm_bwd_persistent", flops, 0.0, st);
     if (ns == 8) {
         switch (kw) {
-            case 1: return coop_launch(persist::lstm_bwd_persistent<1, 8>, blocks, smem, &a, st, attr[4]);
-            case 2: return coop_launch(persist::lstm_bwd_persistent<2, 8>, blocks, smem, &a, st, attr[5]);
-            case 4: return coop_launch(persist::lstm_bwd_persistent<4, 8>, blocks, smem, &a, st, attr[6]);
-            default: return coop_launch(persist::lstm_bwd_persistent<8, 8>, blocks, smem, &a, st, attr[7]);
+            case 1: return persistent_launch(persist::lstm_bwd_persistent<1, 8>, blocks, smem, a, st, attr[4]);
+            case 2: return persistent_launch(persist::lstm_bwd_persistent<2, 8>, blocks, smem, a, st, attr[5]);
+            case 4: return persistent_launch(persist::lstm_bwd_persistent<4, 8>, blocks, smem, a, st, attr[6]);
+            default: return persistent_launch(persist::lstm_bwd_persistent<8, 8>, blocks, smem, a, st, attr[7]);
         }
     }
     switch (kw) {
-        case 1: return coop_launch(persist::lstm_bwd_persistent<1, 4>, blocks, smem, &a, st, attr[0]);
-        case 2: return coop_launch(persist::lstm_bwd_persistent<2, 4>, blocks, smem, &a, st, attr[1]);
-        case 4: return coop_launch(persist::lstm_bwd_persistent<4, 4>, blocks, smem, &a, st, attr[2]);
-        default: return coop_launch(persist::lstm_bwd_persistent<8, 4>, blocks, smem, &a, st, attr[3]);
+        case 1: return persistent_launch(persist::lstm_bwd_persistent<1, 4>, blocks, smem, a, st, attr[0]);
+        case 2: return persistent_launch(persist::lstm_bwd_persistent<2, 4>, blocks, smem, a, st, attr[1]);
+        case 4: return persistent_launch(persist::lstm_bwd_persistent<4, 4>, blocks, smem, a, st, attr[2]);
+        default: return persistent_launch(persist::lstm_bwd_persistent<8, 4>, blocks, smem, a, st, attr[3]);
     }
 }
 

@@ -1,5 +1,5 @@
 // Persistent recurrence kernels: the whole time loop of one layer in one
-// cooperative launch, with each workgroup's slice of the recurrent weight
+// launch of co-resident workgroups, with each workgroup's slice of the recurrent weight
 // resident in LDS for all steps and steps separated by a device-wide barrier.
 //
 // Gate-interleaved layout: activations are stored with column 4u + g for
