@@ -264,17 +264,35 @@ janus_status janus_treelstm_fwd(const janus_treelstm_desc* d, const janus_tree_b
                                 void* ws, size_t ws_bytes, void* stream);
 
 /*
- * Backward of the call above (same d, t, emb, W, U and workspace).
+ * Backward of the call above (same d, t, emb, W, U and workspace; the
+ * workspace must be left unchanged between the two calls: it holds the
+ * forward's gates, cells and uploaded schedule).
  *  dh_root [num_trees, H] dtype: gradient of h_root (gradient of the roots'
  *          c is zero).
  *  demb [V, E], dW [5H, E], dU [5H, 2H], db [5H]: float32, overwritten
  *          (rows of demb for words not in the batch are 0).
+ * Where the weight slices fit one CU's LDS each direction is one launch of
+ * co-resident workgroups that runs every level with a device-wide barrier
+ * between levels (the waits are bounded; see janus_treelstm_device_report).
  */
 janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const janus_tree_batch* t,
                                 const void* emb, const void* W, const void* U,
                                 void* ws, size_t ws_bytes, const void* dh_root,
                                 float* demb, float* dW, float* dU, float* db,
                                 void* stream);
+
+/*
+ * Device-side status of the TreeLSTM calls made with this workspace since
+ * the last forward (same d and t).  Synchronises `stream`, then sets
+ * *timed_out = 1 if a level barrier of the forward or backward ran out of
+ * its bounded wait (their results are then undefined) and returns
+ * JANUS_ERR_DEVICE; else *timed_out = 0 and JANUS_OK.  The flag is cleared
+ * by the next forward.  Errors: as janus_treelstm_fwd's validation, or
+ * INVALID_ARG for a NULL timed_out.
+ */
+janus_status janus_treelstm_device_report(const janus_treelstm_desc* d, const janus_tree_batch* t,
+                                          const void* ws, size_t ws_bytes, int32_t* timed_out,
+                                          void* stream);
 
 /* ------------------------------------------------------------------------ */
 /* Binary TreeRNN over a batch of trees                                     */

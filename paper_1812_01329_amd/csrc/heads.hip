@@ -6,6 +6,8 @@
 // shuffles in a fixed butterfly, then a fixed sequence of partials), so two
 // runs on the same inputs give identical bits.
 #include <algorithm>
+#include <mutex>
+#include <cstdlib>
 #include <vector>
 
 #include "device.hpp"
@@ -450,11 +452,7 @@ janus_status xent_impl(const janus_xent_desc& d, const int32_t* ids_dev, const v
 
 size_t embed_seg_ints(int rows) { return rows > 0 ? size_t(3) * rows + 1 : 1; }
 
-janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_host, int rows, int H, float* dE, int V,
-                            int32_t* seg_dev, hipStream_t st) {
-    janus_status e = zero_fill(dE, size_t(V) * H * sizeof(float), st);
-    if (e != JANUS_OK) return e;
-    if (rows <= 0) return JANUS_OK;
+int embed_segments(const int32_t* ids_host, int rows, int V, std::vector<int32_t>& seg) {
     // stable counting sort by id: count, exclusive scan, place rows in
     // ascending order within each id
     std::vector<int32_t> count(size_t(V) + 1, 0);
@@ -464,22 +462,30 @@ janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_h
         nseg += count[size_t(v) + 1] != 0;
         count[size_t(v) + 1] += count[size_t(v)];
     }
-    std::vector<int32_t> seg(size_t(rows) + 2 * size_t(nseg) + 1);
+    seg.assign(size_t(rows) + 2 * size_t(nseg) + 1, 0);
     int32_t* order = seg.data();
     int32_t* off = order + rows;
     int32_t* sid = off + nseg + 1;
-    {
-        std::vector<int32_t> next(count.begin(), count.end() - 1);
-        for (int r = 0; r < rows; ++r) order[next[size_t(ids_host[r])]++] = r;
-        int g = 0;
-        for (int v = 0; v < V; ++v)
-            if (count[size_t(v) + 1] != count[size_t(v)]) {
-                off[g] = count[size_t(v)];
-                sid[g] = v;
-                ++g;
-            }
-        off[nseg] = rows;
-    }
+    std::vector<int32_t> next(count.begin(), count.end() - 1);
+    for (int r = 0; r < rows; ++r) order[next[size_t(ids_host[r])]++] = r;
+    int g = 0;
+    for (int v = 0; v < V; ++v)
+        if (count[size_t(v) + 1] != count[size_t(v)]) {
+            off[g] = count[size_t(v)];
+            sid[g] = v;
+            ++g;
+        }
+    off[nseg] = rows;
+    return nseg;
+}
+
+janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_host, int rows, int H, float* dE, int V,
+                            int32_t* seg_dev, hipStream_t st) {
+    janus_status e = zero_fill(dE, size_t(V) * H * sizeof(float), st);
+    if (e != JANUS_OK) return e;
+    if (rows <= 0) return JANUS_OK;
+    std::vector<int32_t> seg;
+    const int nseg = embed_segments(ids_host, rows, V, seg);
     if ((e = upload(seg_dev, seg.data(), seg.size() * sizeof(int32_t), st)) != JANUS_OK) return e;
     TraceScope trace("embed_bwd", 0.0, double(rows) * H * dtype_size(dt) + double(nseg) * H * 4.0, st);
     if (dt == JANUS_BF16)
@@ -488,6 +494,106 @@ janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_h
     else
         hipLaunchKernelGGL(embed_bwd_seg_kernel<float>, dim3(unsigned(nseg)), dim3(256), 0, st,
                            static_cast<const float*>(dx), seg_dev, rows, nseg, H, dE);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+// ------------------------------------------------------- small softmax head
+// The whole softmax cross-entropy head of a small problem (a few hundred
+// rows, at most 64 classes, e.g. the 5-class sentiment head at the tree
+// roots) in one workgroup: h and Wout in LDS, the logits, per-row
+// log-sum-exp, loss, dz = (softmax - onehot) / rows, dh = dz Wout,
+// dWout = dz^T h and dbout = column sums of dz, each summed in a fixed
+// order.  One launch instead of three contractions, two reductions and
+// the column sums.
+constexpr int kXentSmallV = 64;
+constexpr size_t kXentSmallLds = 64 * 1024;
+
+size_t xent_small_lds(const janus_xent_desc& d) {
+    return sizeof(float) * (size_t(d.rows) * d.H + size_t(d.V) * d.H + size_t(d.rows) * d.V + size_t(d.rows));
+}
+bool xent_small_fits(const janus_xent_desc& d) {
+    const char* e = getenv("JANUS_XENT_SMALL");
+    if (e && e[0] == '0') return false;
+    return d.V <= kXentSmallV && xent_small_lds(d) <= kXentSmallLds;
+}
+
+template <typename T>
+__global__ __launch_bounds__(256) void xent_small_kernel(const T* h, const T* W, const T* b, const int32_t* tgt,
+                                                         int rows, int V, int H, T* dh, float* dW, float* db,
+                                                         float* loss) {
+    extern __shared__ float xs[];
+    float* hs = xs;                    // [rows][H]
+    float* wsm = hs + rows * H;        // [V][H]
+    float* zs = wsm + V * H;           // [rows][V]: logits, then dz
+    float* ls = zs + rows * V;         // [rows] loss of each row
+    const int tid = threadIdx.x;
+    for (int i = tid; i < rows * H; i += blockDim.x) hs[i] = to_f(h[i]);
+    for (int i = tid; i < V * H; i += blockDim.x) wsm[i] = to_f(W[i]);
+    __syncthreads();
+    for (int i = tid; i < rows * V; i += blockDim.x) {
+        const int r = i / V, v = i - r * V;
+        float s = to_f(b[v]);
+        for (int k = 0; k < H; ++k) s += hs[r * H + k] * wsm[v * H + k];
+        zs[i] = s;
+    }
+    __syncthreads();
+    const float inv = 1.f / float(rows);
+    for (int r = tid; r < rows; r += blockDim.x) {
+        float* z = zs + r * V;
+        float m = -INFINITY;
+        for (int v = 0; v < V; ++v) m = fmaxf(m, z[v]);
+        float se = 0.f;
+        for (int v = 0; v < V; ++v) se += __expf(z[v] - m);
+        const int t = min(max(tgt[r], 0), V - 1);
+        ls[r] = m + __logf(se) - z[t];
+        const float rs = 1.f / se;
+        for (int v = 0; v < V; ++v) z[v] = (__expf(z[v] - m) * rs - (v == t ? 1.f : 0.f)) * inv;
+    }
+    __syncthreads();
+    if (tid == 0) {
+        float s = 0.f;
+        for (int r = 0; r < rows; ++r) s += ls[r];
+        *loss = s * inv;
+    }
+    for (int i = tid; i < rows * H; i += blockDim.x) {
+        const int r = i / H, k = i - r * H;
+        float s = 0.f;
+        for (int v = 0; v < V; ++v) s += zs[r * V + v] * wsm[v * H + k];
+        dh[i] = from_f<T>(s);
+    }
+    for (int i = tid; i < V * H; i += blockDim.x) {
+        const int v = i / H, k = i - v * H;
+        float s = 0.f;
+        for (int r = 0; r < rows; ++r) s += zs[r * V + v] * hs[r * H + k];
+        dW[i] = s;
+    }
+    for (int v = tid; v < V; v += blockDim.x) {
+        float s = 0.f;
+        for (int r = 0; r < rows; ++r) s += zs[r * V + v];
+        db[v] = s;
+    }
+}
+
+template <typename T>
+janus_status xent_small(const janus_xent_desc& d, const int32_t* ids_dev, const void* Wout, const void* bout,
+                        const void* h, void* dh, float* dWout, float* dbout, float* loss, hipStream_t st) {
+    static std::mutex m;
+    static size_t attr = 0;
+    const size_t smem = xent_small_lds(d);
+    {
+        std::lock_guard<std::mutex> lock(m);
+        if (smem > attr) {
+            JANUS_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(xent_small_kernel<T>),
+                                          hipFuncAttributeMaxDynamicSharedMemorySize, int(smem)));
+            attr = smem;
+        }
+    }
+    TraceScope trace("xent_small", 2.0 * 3.0 * d.rows * double(d.V) * d.H,
+                     double(dtype_size(d.dtype)) * (2.0 * d.rows * d.H + double(d.V) * d.H), st);
+    hipLaunchKernelGGL(xent_small_kernel<T>, dim3(1), dim3(256), smem, st, static_cast<const T*>(h),
+                       static_cast<const T*>(Wout), static_cast<const T*>(bout), ids_dev, d.rows, d.V, d.H,
+                       static_cast<T*>(dh), dWout, dbout, loss);
     JANUS_LAUNCH_CHECK();
     return JANUS_OK;
 }
@@ -546,6 +652,11 @@ extern "C" janus_status janus_embed_softmax_xent(const janus_xent_desc* d, janus
         return JANUS_OK;
     }
     if (op == JANUS_EMBED_BWD) return embed_backward(d->dtype, in, ids_host, d->rows, d->H, dtable, d->V, w.seg, st);
+    if (xent_small_fits(*d)) {
+        if (d->dtype == JANUS_BF16)
+            return xent_small<bf16_t>(*d, ids_dev, table, bias, in, out, dtable, dbias, loss, st);
+        return xent_small<float>(*d, ids_dev, table, bias, in, out, dtable, dbias, loss, st);
+    }
     if (d->dtype == JANUS_BF16)
         return xent_impl<bf16_t>(*d, ids_dev, table, bias, in, out, dtable, dbias, loss, w, st);
     return xent_impl<float>(*d, ids_dev, table, bias, in, out, dtable, dbias, loss, w, st);

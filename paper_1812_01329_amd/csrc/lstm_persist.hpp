@@ -68,16 +68,21 @@ __device__ __forceinline__ unsigned xcc_id() {
 }
 
 // Per-workgroup barrier bookkeeping, meaningful in thread 0 only (xcount:
-// in the first 16 lanes of wave 0).
-struct Barrier {
-    Sync* s;
+// in the first 16 lanes of wave 0).  S is the counter block: Sync here, or
+// any struct with the same count / xcd / census / error members.
+template <class S>
+struct BarrierT {
+    S* s;
     unsigned x, xsize, nx, nb, phase;
     unsigned xidx;                     // arrival order of this workgroup among those on its XCD
     unsigned xfirst;                   // workgroups on the XCDs numbered below this one
     unsigned xcount;                   // lane q < 16 of wave 0: workgroups on XCD q
 };
 
-__device__ __forceinline__ bool spin_until(Sync* s, const unsigned* p, unsigned target) {
+using Barrier = BarrierT<Sync>;
+
+template <class S>
+__device__ __forceinline__ bool spin_until(S* s, const unsigned* p, unsigned target) {
     int spins = 0;
     while (__hip_atomic_load(p, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) < target) {
         if (__hip_atomic_load(&s->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u) return false;
@@ -93,7 +98,8 @@ __device__ __forceinline__ bool spin_until(Sync* s, const unsigned* p, unsigned 
 // Ordering the workgroups by (XCD, arrival order on it) gives each a rank
 // xfirst + xidx in [0, gridDim.x) under which consecutive ranks share an XCD
 // wherever possible, whatever order the hardware placed them in.
-__device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
+template <class S>
+__device__ __forceinline__ void barrier_init(BarrierT<S>& b, S* s) {
     b.s = s;
     b.nb = gridDim.x;
     b.phase = 0;
@@ -149,7 +155,8 @@ __device__ __forceinline__ void barrier_init(Barrier& b, Sync* s) {
 //
 // After a timeout every later wait returns at once, so all waves still reach
 // the end of the kernel (results are then garbage and `error` is set).
-__device__ __forceinline__ void barrier_arrive(Barrier& b) {
+template <class S>
+__device__ __forceinline__ void barrier_arrive(BarrierT<S>& b) {
     ++b.phase;
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     __builtin_amdgcn_s_waitcnt(0);
@@ -157,7 +164,8 @@ __device__ __forceinline__ void barrier_arrive(Barrier& b) {
     __atomic_signal_fence(__ATOMIC_SEQ_CST);
     if (threadIdx.x == 0) __hip_atomic_fetch_add(&b.s->xcd[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
 }
-__device__ __forceinline__ void barrier_wait(Barrier& b) {
+template <class S>
+__device__ __forceinline__ void barrier_wait(BarrierT<S>& b) {
     if (threadIdx.x < 64) {
         const unsigned q = threadIdx.x & 15u;
         const unsigned target = b.phase * b.xcount;   // 0 past lane 15 and for empty XCDs

@@ -1,6 +1,8 @@
 // Internal launchers shared between the library's translation units.
 #pragma once
 
+#include <vector>
+
 #include "runtime.hpp"
 
 namespace janus {
@@ -82,6 +84,9 @@ janus_status zero_fill(void* p, size_t bytes, hipStream_t stream);
 // embed_seg_ints(rows) int32 of device memory the caller provides (a
 // workspace piece); one workgroup then sums each group.
 size_t embed_seg_ints(int rows);
+// The host part: rows grouped by id into seg = order[rows], off[nseg + 1],
+// sid[nseg] (ids ascending, rows ascending within an id); returns nseg.
+int embed_segments(const int32_t* ids_host, int rows, int V, std::vector<int32_t>& seg);
 janus_status embed_backward(janus_dtype dt, const void* dx, const int32_t* ids_host, int rows, int H, float* dE, int V,
                             int32_t* seg_dev, hipStream_t stream);
 

@@ -21,15 +21,21 @@
 // [dh_L; dh_R] to the two children (each node has one parent, so these are
 // plain stores).  After the loop: dU = da_int^T HLR, dW = da_leaf^T X_leaf,
 // db = column sums of da, dx_leaf = da_leaf W, then the embedding gradient.
+#include <algorithm>
+#include <cstdlib>
+#include <mutex>
 #include <vector>
 
 #include "device.hpp"
 #include "ops.hpp"
 #include "simt.hpp"
+#include "tree_persist.hpp"
 
 namespace janus {
 
 namespace {
+
+constexpr int kMaxTreeGrid = 4096;   // workgroups of a persistent tree launch (seg's tail is sized for it)
 
 struct TreeWs {
     // level-ordered device schedule
@@ -51,6 +57,19 @@ struct TreeWs {
     float* part = nullptr;
     int32_t* seg = nullptr;      // the leaves grouped by word, for the embedding gradient
     int64_t ld5 = 0;
+    // persistent path: level offsets and the barrier's counters (carved right
+    // after the schedule arrays and before `seg`, so that each direction's
+    // upload is one copy), and node rows padded to whole 128-byte lines
+    int32_t* loff = nullptr;     // [N + 1]
+    tpersist::TreeSync* tsync = nullptr;
+    float* Gp = nullptr;         // [N x ldg] gates
+    float* Cp = nullptr;         // [N x ldc]
+    float* HLRp = nullptr;       // [N x ldl]
+    float* dhp = nullptr;        // [N x ldc]
+    float* dcp = nullptr;        // [N x ldc]
+    float* dAp = nullptr;        // [N x lda]
+    float* dxp = nullptr;        // [N x ldx]
+    int64_t ldg = 0, ldc = 0, ldl = 0, lda = 0, ldx = 0;
 };
 
 size_t carve(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base, TreeWs& w) {
@@ -63,6 +82,12 @@ size_t carve(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base, Tre
     w.parent = c.take<int32_t>(N);
     w.rootk = c.take<int32_t>(N);
     w.rootpos = c.take<int32_t>(K);
+    w.loff = c.take<int32_t>(int64_t(N) + 1);
+    w.tsync = c.take<tpersist::TreeSync>(1);
+    // the leaves grouped by word, and (persistent backward) each workgroup's
+    // first group of the embedding rows: one entry per workgroup, at most one
+    // per CU of the devices the library plans for
+    w.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)) + kMaxTreeGrid);
     w.A = c.take<float>(int64_t(N) * w.ld5);
     w.G = c.take<float>(int64_t(N) * w.ld5);
     w.C = c.take<float>(int64_t(N) * H);
@@ -73,7 +98,17 @@ size_t carve(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base, Tre
     w.Wt = c.take<float>(int64_t(d.E) * 5 * H);
     w.Ut = c.take<float>(int64_t(2) * H * 5 * H);
     w.part = c.take<float>(colsum_partial_floats(5 * H));
-    w.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)));
+    w.ldg = w.lda = round_up(int64_t(5) * H, 32);
+    w.ldc = round_up(H, 32);
+    w.ldl = round_up(int64_t(2) * H, 32);
+    w.ldx = round_up(d.E, 32);
+    w.Gp = c.take<float>(int64_t(N) * w.ldg);
+    w.Cp = c.take<float>(int64_t(N) * w.ldc);
+    w.HLRp = c.take<float>(int64_t(N) * w.ldl);
+    w.dhp = c.take<float>(int64_t(N) * w.ldc);
+    w.dcp = c.take<float>(int64_t(N) * w.ldc);
+    w.dAp = c.take<float>(int64_t(N) * w.lda);
+    w.dxp = c.take<float>(int64_t(N) * w.ldx);
     return c.off + 256;
 }
 
@@ -282,6 +317,209 @@ janus_status prepare(const janus_treelstm_desc* d, const janus_tree_batch* t, vo
 }
 
 
+// ------------------------------------------------------- persistent path
+struct TreeDev {
+    int cus = 0;
+    size_t lds = 0;
+};
+// Properties of the current device, queried once per device under a lock.
+TreeDev tree_dev() {
+    static std::mutex m;
+    static TreeDev cache[64];
+    static bool have[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return TreeDev{};
+    std::lock_guard<std::mutex> lock(m);
+    if (!have[dev]) {
+        TreeDev t;
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) t.cus = v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess) t.lds = size_t(v);
+        (void)hipGetLastError();
+        cache[dev] = t;
+        have[dev] = true;
+    }
+    return cache[dev];
+}
+
+// Grid and LDS of the persistent TreeLSTM kernels: one workgroup per CU at
+// most, the grid a multiple of the unit groups (forward) and of the column
+// tiles (backward) so every workgroup holds one weight slice.  Off with
+// JANUS_TREE_PERSIST=0, where a slice does not fit the LDS (about H > 170
+// for the backward's U columns) or for inputs wider than 512; the
+// level-by-level kernels run then.
+struct TreePlan {
+    bool on = false;
+    int ngroups = 0, fwd_grid = 0, ncol = 0, bwd_grid = 0;
+    size_t fwd_lds = 0, bwd_lds = 0;
+};
+TreePlan tree_plan(const janus_treelstm_desc& d) {
+    TreePlan p;
+    const char* e = getenv("JANUS_TREE_PERSIST");
+    if (e && e[0] == '0') return p;
+    const TreeDev dev = tree_dev();
+    if (dev.cus <= 0 || dev.lds == 0) return p;
+    if (d.E > tpersist::kMaxE) return p;
+    p.ngroups = (d.H + tpersist::kUG - 1) / tpersist::kUG;
+    p.ncol = (2 * d.H + 31) / 32;
+    if (p.ngroups > dev.cus || p.ncol > dev.cus) return p;
+    const int cus = dev.cus < kMaxTreeGrid ? dev.cus : kMaxTreeGrid;
+    p.fwd_grid = p.ngroups * (cus / p.ngroups);
+    p.bwd_grid = p.ncol * (cus / p.ncol);
+    p.fwd_lds = size_t(tpersist::fwd_lds_floats(d.E, d.H)) * sizeof(float);
+    p.bwd_lds = size_t(tpersist::bwd_lds_floats(d.H)) * sizeof(float);
+    p.on = p.fwd_lds <= dev.lds && p.bwd_lds <= dev.lds;
+    return p;
+}
+
+// An ordinary launch of a grid whose workgroups must all be resident (the
+// plan allows one per CU and no more than the CUs; the occupancy query
+// confirms one fits a CU).  The barrier's waits are bounded.
+template <class K, class A>
+janus_status tree_persistent_launch(K kernel, int blocks, size_t smem, const A& args, hipStream_t st,
+                                    size_t& attr_smem) {
+    static std::mutex m;
+    {
+        std::lock_guard<std::mutex> lock(m);
+        if (smem > attr_smem) {
+            JANUS_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                          hipFuncAttributeMaxDynamicSharedMemorySize, int(smem)));
+            attr_smem = smem;
+        }
+    }
+    int per_cu = 0;
+    JANUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kernel),
+                                                           tpersist::kThreads, smem));
+    if (per_cu < 1 || int64_t(per_cu) * tree_dev().cus < blocks) return JANUS_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(kernel, dim3(blocks), dim3(tpersist::kThreads), smem, st, args);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+// Forward on the persistent path: the schedule, the level offsets and the
+// barrier's counters (with its error flag) go over in one copy, then one
+// launch runs every level.
+janus_status treelstm_fwd_persistent_call(const janus_treelstm_desc& d, const janus_tree_batch* t,
+                                          const TreeSchedule& s, const TreeWs& w, const TreePlan& plan,
+                                          const void* emb, const void* W, const void* U, const void* b, void* h_root,
+                                          hipStream_t st) {
+    TreeHost h;
+    build_host(t, s, h);
+    const size_t nb = sizeof(int32_t) * s.N;
+    const std::vector<char> zero_sync(sizeof(tpersist::TreeSync), 0);
+    const UploadPiece pieces[] = {{w.lword, h.lword.data(), nb},
+                                  {w.lchild, h.lchild.data(), nb},
+                                  {w.rchild, h.rchild.data(), nb},
+                                  {w.parent, h.parent.data(), nb},
+                                  {w.rootk, h.rootk.data(), nb},
+                                  {w.rootpos, h.rootpos.data(), sizeof(int32_t) * t->num_trees},
+                                  {w.loff, s.level_offsets.data(), sizeof(int32_t) * s.level_offsets.size()},
+                                  {w.tsync, zero_sync.data(), zero_sync.size()}};
+    janus_status e = upload_pieces(pieces, 8, st);
+    if (e != JANUS_OK) return e;
+    tpersist::FwdArgs a;
+    a.E = d.E;
+    a.H = d.H;
+    a.N = s.N;
+    a.M0 = s.level_offsets[1];
+    a.nlev = s.num_levels;
+    a.ngroups = plan.ngroups;
+    a.loff = w.loff;
+    a.lword = w.lword;
+    a.lchild = w.lchild;
+    a.rchild = w.rchild;
+    a.parent = w.parent;
+    a.rootk = w.rootk;
+    a.emb = static_cast<const float*>(emb);
+    a.W = static_cast<const float*>(W);
+    a.U = static_cast<const float*>(U);
+    a.b = static_cast<const float*>(b);
+    a.G = w.Gp;
+    a.ldg = w.ldg;
+    a.C = w.Cp;
+    a.ldc = w.ldc;
+    a.HLR = w.HLRp;
+    a.ldl = w.ldl;
+    a.h_root = static_cast<float*>(h_root);
+    a.sync = w.tsync;
+    static size_t attr = 0;
+    const double flops = 2.0 * 5.0 * d.H * (double(a.M0) * d.E + double(s.N - a.M0) * 2.0 * d.H);
+    TraceScope trace("treelstm_fwd_persistent", flops, 0.0, st);
+    return tree_persistent_launch(tpersist::treelstm_fwd_persistent, plan.fwd_grid, plan.fwd_lds, a, st, attr);
+}
+
+// Backward on the persistent path: the schedule is the forward's (the
+// workspace is unchanged between the two calls); the leaves grouped by word
+// and the barrier's counters (not its error flag) go over in one copy, then
+// one launch runs the levels, the weight and input gradients and the
+// embedding gradient.
+janus_status treelstm_bwd_persistent_call(const janus_treelstm_desc& d, const janus_tree_batch* t,
+                                          const TreeSchedule& s, const TreeWs& w, const TreePlan& plan,
+                                          const void* emb, const void* W, const void* U, const void* dh_root,
+                                          float* demb, float* dW, float* dU, float* db, hipStream_t st) {
+    TreeHost h;
+    build_host(t, s, h);
+    const int M0 = s.level_offsets[1];
+    std::vector<int32_t> seg;
+    const int nseg = embed_segments(h.lword.data(), M0, d.V, seg);
+    // first group of each workgroup's rows [V w / grid, V (w + 1) / grid)
+    const int32_t* sid = seg.data() + M0 + nseg + 1;
+    for (int g = 0; g < plan.bwd_grid; ++g) {
+        const int64_t v0 = int64_t(d.V) * g / plan.bwd_grid;
+        seg.push_back(int32_t(std::lower_bound(sid, sid + nseg, v0) - sid));
+        sid = seg.data() + M0 + nseg + 1;   // push_back may move the array
+    }
+    const size_t counters = sizeof(tpersist::TreeSync) - tpersist::kTreeSyncCounters;
+    const std::vector<char> zero_counters(counters, 0);
+    const UploadPiece pieces[] = {
+        {reinterpret_cast<char*>(w.tsync) + tpersist::kTreeSyncCounters, zero_counters.data(), counters},
+        {w.seg, seg.data(), seg.size() * sizeof(int32_t)}};
+    janus_status e = upload_pieces(pieces, 2, st);
+    if (e != JANUS_OK) return e;
+    tpersist::BwdArgs a;
+    a.E = d.E;
+    a.H = d.H;
+    a.N = s.N;
+    a.M0 = M0;
+    a.nlev = s.num_levels;
+    a.ncol = plan.ncol;
+    a.nseg = nseg;
+    a.V = d.V;
+    a.loff = w.loff;
+    a.lword = w.lword;
+    a.lchild = w.lchild;
+    a.rchild = w.rchild;
+    a.rootk = w.rootk;
+    a.seg = w.seg;
+    a.emb = static_cast<const float*>(emb);
+    a.W = static_cast<const float*>(W);
+    a.U = static_cast<const float*>(U);
+    a.G = w.Gp;
+    a.ldg = w.ldg;
+    a.C = w.Cp;
+    a.ldc = w.ldc;
+    a.HLR = w.HLRp;
+    a.ldl = w.ldl;
+    a.dh_root = static_cast<const float*>(dh_root);
+    a.dh = w.dhp;
+    a.dc = w.dcp;
+    a.dA = w.dAp;
+    a.lda = w.lda;
+    a.dxl = w.dxp;
+    a.ldx = w.ldx;
+    a.demb = demb;
+    a.dW = dW;
+    a.dU = dU;
+    a.db = db;
+    a.sync = w.tsync;
+    static size_t attr = 0;
+    // [dh_L; dh_R] = dA U on internal nodes, dU, dW and dx_leaf
+    const double Nint = double(s.N - M0);
+    const double flops = 2.0 * 5.0 * d.H * (Nint * 2.0 * d.H * 2.0 + double(M0) * d.E * 2.0);
+    TraceScope trace("treelstm_bwd_persistent", flops, 0.0, st);
+    return tree_persistent_launch(tpersist::treelstm_bwd_persistent, plan.bwd_grid, plan.bwd_lds, a, st, attr);
+}
+
 // ------------------------------------------------------------------ TreeRNN
 // Binary TreeRNN on the same frontier schedule: a leaf's h is its word
 // vector (embedding width = H), an internal node h = tanh(W [h_L; h_R] + b).
@@ -380,6 +618,8 @@ extern "C" janus_status janus_treelstm_fwd(const janus_treelstm_desc* d, const j
     janus_status e = prepare(d, t, ws, ws_bytes, s, w);
     if (e != JANUS_OK) return e;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    const TreePlan plan = tree_plan(*d);
+    if (plan.on) return treelstm_fwd_persistent_call(*d, t, s, w, plan, emb, W, U, b, h_root, st);
     if ((e = upload_tree(t, s, w, st)) != JANUS_OK) return e;
     const int H = d->H, E = d->E;
     const int M0 = s.level_offsets[1];
@@ -420,6 +660,9 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
     if (e != JANUS_OK) return e;
     const int M0 = s.level_offsets[1];
     hipStream_t st = static_cast<hipStream_t>(stream);
+    const TreePlan plan = tree_plan(*d);
+    if (plan.on)
+        return treelstm_bwd_persistent_call(*d, t, s, w, plan, emb, W, U, dh_root, demb, dW, dU, db, st);
     TreeHost host;
     if ((e = upload_tree(t, s, w, st, &host)) != JANUS_OK) return e;
     const int H = d->H, E = d->E, N = s.N;
@@ -476,6 +719,21 @@ extern "C" janus_status janus_treelstm_bwd(const janus_treelstm_desc* d, const j
                                      nullptr, nullptr, w.dxl, E, st);
     if (e != JANUS_OK) return e;
     return embed_backward(JANUS_F32, w.dxl, host.lword.data(), M0, E, demb, d->V, w.seg, st);
+}
+
+extern "C" janus_status janus_treelstm_device_report(const janus_treelstm_desc* d, const janus_tree_batch* t,
+                                                     const void* ws, size_t ws_bytes, int32_t* timed_out,
+                                                     void* stream) {
+    if (!timed_out) return JANUS_ERR_INVALID_ARG;
+    TreeSchedule s;
+    TreeWs w;
+    janus_status e = prepare(d, t, const_cast<void*>(ws), ws_bytes, s, w);
+    if (e != JANUS_OK) return e;
+    unsigned flag = 0;
+    JANUS_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+    JANUS_HIP(hipMemcpy(&flag, &w.tsync->error, sizeof(flag), hipMemcpyDeviceToHost));
+    *timed_out = flag != 0u ? 1 : 0;
+    return flag != 0u ? JANUS_ERR_DEVICE : JANUS_OK;
 }
 
 extern "C" size_t janus_treernn_workspace_bytes(const janus_treernn_desc* d, int32_t max_nodes, int32_t max_trees) {

@@ -1,0 +1,763 @@
+// Persistent level programs of the binary TreeLSTM: the whole forward pass
+// of a tree batch in one launch, and the whole backward pass (levels, weight
+// gradients, input gradients and the embedding gradient) in another.
+//
+// The recursion over a tree (Section 4.2.1: recursive calls become graph
+// invocations; Section 6.1: the TreeNN models) visits a node after both of
+// its subtrees.  Nodes of equal height are independent, so a level is one
+// batched step over all trees of the batch (the parallel execution of
+// independent nodes, "+PARL" in Section 6.3.1).  Here the levels run inside
+// one kernel, separated by a device-wide barrier, instead of one or two
+// launches per level: the per-level cost drops from launch and drain to one
+// barrier, and each workgroup's weight slice stays in LDS for all levels.
+//
+// Node rows are level-ordered positions p (a level is a contiguous range,
+// leaves first, M0 of them).  Gate blocks are (i, f_L, f_R, o, u); the gate
+// q of unit j sits at column q * H + j of G and dA.
+//
+// Forward.  The 5H gate columns are split in groups of 6 units (30 of the
+// 32 columns of an MFMA tile); workgroup w keeps the W and U columns of
+// group w mod G in LDS and takes the 32-node row tiles r = w / G, r + R, ...
+// of every level.  A tile's operand rows (the leaves' embedding rows, the
+// internal nodes' [h_L; h_R]) are staged in LDS, contracted with fp32 MFMA
+// (K split over the four waves, partial tiles summed in LDS), and the cell
+// update runs in the same workgroup: c goes to its row, h to the parent's
+// [h_L; h_R] row (or to h_root), the gates to G for the backward.
+//
+// Backward, levels from the top down.  Workgroup w keeps the 32 columns
+// w mod NC of U (the columns of [dh_L; dh_R]) in LDS and takes row tiles of
+// each internal level; per tile it recomputes the cell backward of its rows
+// for all units, in chunks of 32 units, into LDS, and contracts the chunk
+// with its U columns: [dh_L; dh_R] = dA U, sent to the two children (each
+// node has one parent, so the rows are plain stores).  The workgroup of
+// column tile c also stores dA and the children's dc of the unit chunks
+// c, c + NC, ... (spread so no column tile carries all the stores).  Level
+// 0 (the leaves) only stores dA.  After a barrier the workgroups share the contractions over
+// nodes: dU = dA_int^T [h_L; h_R], dW = dA_leaf^T x_leaf, db = column sums
+// of dA, dx_leaf = dA_leaf W; after another the embedding gradient, row by
+// row of the table (the leaves grouped by word on the host; rows no leaf
+// uses are zero), so each row is written once.
+//
+// Memory between workgroups follows the rule of the persistent recurrence
+// kernels: a value another workgroup reads in the same launch is stored
+// write-through and read only after a barrier that follows the store, at an
+// address no workgroup read earlier in the launch.  Rows that cross
+// workgroups are padded to whole 128-byte lines, so a line never mixes a row
+// that is already read with one that is not yet written.
+#pragma once
+
+#include "device.hpp"
+#include "lstm_persist.hpp"
+
+namespace janus {
+namespace tpersist {
+
+constexpr int kThreads = 256;          // 4 waves
+constexpr int kWaves = kThreads / 64;
+constexpr int kUG = 6;                 // units per forward group: 5 x 6 = 30 of 32 tile columns
+constexpr int kUC = 32;                // units per chunk of the backward's cell recompute
+constexpr int kKC = 128;               // k per staged chunk of the contractions over nodes
+constexpr int kRed = 33;               // row pitch of the per-wave partial tiles
+constexpr int kMaxE = 2 * kThreads;    // input width the embedding-gradient phase handles
+
+__host__ __device__ constexpr int pad16(int x) { return (x + 15) & ~15; }
+__host__ __device__ constexpr int padto(int x, int m) { return (x + m - 1) / m * m; }
+
+// Counter block of the grid barrier.  `error` comes first: the backward's
+// upload zeroes the counters that follow it and leaves a flag the forward
+// set.
+struct TreeSync {
+    unsigned error;
+    unsigned pad_e[63];
+    unsigned count;
+    unsigned pad0[63];
+    unsigned xcd[16][64];
+    unsigned census[16][64];
+};
+constexpr size_t kTreeSyncCounters = offsetof(TreeSync, count);   // byte offset of the counters
+
+using TreeBarrier = persist::BarrierT<TreeSync>;
+
+// A store other workgroups read later in the launch: device-scope, so it is
+// written through the L2 of this XCD to memory (the L2s of the XCDs are not
+// coherent with each other), and counted like any store by the wait at the
+// barrier's arrival.
+__device__ __forceinline__ void store_through(float* base, int64_t idx, float v) {
+    __hip_atomic_store(base + idx, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void zero_acc(f32x16_t& acc) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+}
+
+// Sum the four waves' 32 x 32 tiles: every wave writes its accumulator to
+// red[wave][row][col]; after the barrier red holds the parts, summed by the
+// reader in wave order.
+__device__ __forceinline__ void spill_acc(const f32x16_t& acc, float* red, int wave, int lane) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) red[(wave * 32 + acc_row(v, lane)) * kRed + acc_col(lane)] = acc[v];
+}
+__device__ __forceinline__ float red_sum(const float* red, int m, int c) {
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += red[(w * 32 + m) * kRed + c];
+    return s;
+}
+
+// Copy n elements into LDS: element i is ld(i) (which returns 0 outside its
+// operand) and goes where st(i, v) puts it.  Each thread issues NB loads
+// before it writes any, so it pays one memory round trip per NB elements
+// rather than one per element.
+template <int NB, class Ld, class St>
+__device__ __forceinline__ void stage(int n, Ld ld, St st) {
+    for (int base = int(threadIdx.x); base < n; base += kThreads * NB) {
+        float v[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int idx = base + i * kThreads;
+            v[i] = idx < n ? ld(idx) : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int idx = base + i * kThreads;
+            if (idx < n) st(idx, v[i]);
+        }
+    }
+}
+// The same with 16-byte pieces (ld4 returns a float4).
+template <int NB, class Ld, class St>
+__device__ __forceinline__ void stage4(int n, Ld ld, St st) {
+    for (int base = int(threadIdx.x); base < n; base += kThreads * NB) {
+        float4 v[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int idx = base + i * kThreads;
+            v[i] = idx < n ? ld(idx) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int idx = base + i * kThreads;
+            if (idx < n) st(idx, v[i]);
+        }
+    }
+}
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+
+
+// ---------------------------------------------------------------- forward
+struct FwdArgs {
+    int E, H, N, M0, nlev, ngroups;
+    const int32_t* loff;       // [nlev + 1] level offsets
+    const int32_t* lword;      // [N] word of a leaf
+    const int32_t* lchild;     // [N] position of the left child, -1 for leaves
+    const int32_t* rchild;
+    const int32_t* parent;     // [N] 2 * parent position + side, -1 for roots
+    const int32_t* rootk;      // [N] tree index of a root, -1 otherwise
+    const float* emb;          // [V x E]
+    const float* W;            // [5H x E]
+    const float* U;            // [5H x 2H]
+    const float* b;            // [5H]
+    float* G;                  // [N x ldg] gates after activation
+    int64_t ldg;
+    float* C;                  // [N x ldc]
+    int64_t ldc;
+    float* HLR;                // [(N - M0) x ldl]: row p - M0 holds [h_L ; h_R] of node p
+    int64_t ldl;
+    float* h_root;             // [trees x H]
+    TreeSync* sync;
+};
+
+__host__ __device__ inline int fwd_lds_floats(int E, int H) {
+    const int sE = pad16(E) + 4, sU = pad16(2 * H) + 4, sA = (sE > sU ? sE : sU);
+    return 32 * (sE + sU + sA) + kWaves * 32 * kRed + 64;   // + the row offsets of a tile (int64)
+}
+
+// Stage a [32 x K] weight slice (row c = tile column c: gate c / 6 of unit
+// 6 g + c % 6) into LDS rows of pitch ld, zero past K and for absent units.
+__device__ __forceinline__ void stage_fwd_slice(float* dst, int ld, const float* src, int K, int KP, int H, int g) {
+    auto row_of = [&](int c) -> int64_t {
+        const int q = c / kUG, j = kUG * g + c % kUG;
+        return (q < 5 && j < H) ? int64_t(q) * H + j : -1;
+    };
+    if (K % 4 == 0) {
+        const int KP4 = KP / 4;
+        stage4<8>(32 * KP4,
+                  [&](int idx) {
+                      const int c = idx / KP4, k = 4 * (idx - c * KP4);
+                      const int64_t r = row_of(c);
+                      return (r >= 0 && k < K) ? ld4(src + r * K + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+                  },
+                  [&](int idx, float4 v) {
+                      const int c = idx / KP4, k = 4 * (idx - c * KP4);
+                      *reinterpret_cast<float4*>(dst + c * ld + k) = v;
+                  });
+    } else {
+        stage<16>(32 * KP,
+                  [&](int idx) {
+                      const int c = idx / KP, k = idx - c * KP;
+                      const int64_t r = row_of(c);
+                      return (r >= 0 && k < K) ? src[r * K + k] : 0.f;
+                  },
+                  [&](int idx, float v) {
+                      const int c = idx / KP, k = idx - c * KP;
+                      dst[c * ld + k] = v;
+                  });
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void treelstm_fwd_persistent(FwdArgs a) {
+    extern __shared__ __align__(16) float sm[];
+    const int E = a.E, H = a.H;
+    const int KE = pad16(E), KU = pad16(2 * H), KA = KE > KU ? KE : KU;
+    const int sE = KE + 4, sU = KU + 4, sA = KA + 4;
+    float* Wl = sm;                 // [32 tile columns][sE]
+    float* Ul = Wl + 32 * sE;       // [32][sU]
+    float* At = Ul + 32 * sU;       // [32 node rows][sA]
+    float* red = At + 32 * sA;      // [waves][32][kRed]
+    int64_t* rowsrc = reinterpret_cast<int64_t*>(red + kWaves * 32 * kRed);   // [32] source row offset, -1 = none
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    TreeBarrier bar;
+    persist::barrier_init(bar, a.sync);
+    const int g = int(blockIdx.x) % a.ngroups, r0 = int(blockIdx.x) / a.ngroups;
+    const int R = int(gridDim.x) / a.ngroups;
+
+    stage_fwd_slice(Wl, sE, a.W, E, KE, H, g);
+    stage_fwd_slice(Ul, sU, a.U, 2 * H, KU, H, g);
+    // threads below 32 * 6 update one cell each: row cm of the tile, unit cj
+    const int cm = tid / kUG, cu = tid % kUG, cj = kUG * g + cu;
+    const bool cell_thread = tid < 32 * kUG && cj < H;
+    float bias[5];
+#pragma unroll
+    for (int q = 0; q < 5; ++q) bias[q] = cell_thread ? a.b[q * H + cj] : 0.f;
+
+    for (int L = 0; L < a.nlev; ++L) {
+        const int p0 = a.loff[L], p1 = a.loff[L + 1];
+        const int ntile = (p1 - p0 + 31) / 32;
+        const bool leaf = L == 0;
+        const int K = leaf ? E : 2 * H, KP = leaf ? KE : KU, sW = leaf ? sE : sU;
+        const float* Wsrc = leaf ? Wl : Ul;
+        const float* src = leaf ? a.emb : a.HLR;
+        for (int t = r0; t < ntile; t += R) {
+            const int pt = p0 + 32 * t, rows = min(32, p1 - pt);
+            const int p = pt + cm;
+            const bool cell = cell_thread && cm < rows;
+            // the cell's links, loaded while the tile is staged
+            int lc = -1, rc = -1, par = -1, rk = -1;
+            if (cell) {
+                lc = a.lchild[p];
+                rc = a.rchild[p];
+                par = a.parent[p];
+                rk = a.rootk[p];
+            }
+            __syncthreads();   // the previous tile's reads of At, red and rowsrc are done
+            if (tid < 32) {
+                const int q = pt + tid;
+                rowsrc[tid] = tid < rows ? (leaf ? int64_t(a.lword[q]) * E : int64_t(q - a.M0) * a.ldl) : -1;
+            }
+            __syncthreads();
+            if (K % 4 == 0) {
+                const int KP4 = KP / 4;
+                stage4<4>(32 * KP4,
+                          [&](int idx) {
+                              const int m = idx / KP4, k = 4 * (idx - m * KP4);
+                              const int64_t r = rowsrc[m];
+                              return (r >= 0 && k < K) ? ld4(src + r + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+                          },
+                          [&](int idx, float4 v) {
+                              const int m = idx / KP4, k = 4 * (idx - m * KP4);
+                              *reinterpret_cast<float4*>(At + m * sA + k) = v;
+                          });
+            } else {
+                stage<16>(32 * KP,
+                          [&](int idx) {
+                              const int m = idx / KP, k = idx - m * KP;
+                              const int64_t r = rowsrc[m];
+                              return (r >= 0 && k < K) ? src[r + k] : 0.f;
+                          },
+                          [&](int idx, float v) {
+                              const int m = idx / KP, k = idx - m * KP;
+                              At[m * sA + k] = v;
+                          });
+            }
+            // the children's c, loaded while the tile is contracted
+            const float cl = lc >= 0 ? a.C[int64_t(lc) * a.ldc + cj] : 0.f;
+            const float cr = rc >= 0 ? a.C[int64_t(rc) * a.ldc + cj] : 0.f;
+            __syncthreads();
+            // D[node m][tile column c] = sum_k rows[m][k] * Wslice[c][k], the
+            // k-steps of 16 dealt to the waves in turn
+            f32x16_t acc;
+            zero_acc(acc);
+            for (int ks = wave; ks < KP / 16; ks += kWaves) {
+                Frag<float> fa, fb;
+                fa.load(At + (lane & 31) * sA + ks * 16 + 8 * (lane >> 5));
+                fb.load(Wsrc + (lane & 31) * sW + ks * 16 + 8 * (lane >> 5));
+                mfma(acc, fa, fb);
+            }
+            spill_acc(acc, red, wave, lane);
+            __syncthreads();
+            if (cell) {
+                float z[5];
+#pragma unroll
+                for (int q = 0; q < 5; ++q) z[q] = bias[q] + red_sum(red, cm, q * kUG + cu);
+                const float gi = sigmoidf_(z[0]), gl = sigmoidf_(z[1]), gr = sigmoidf_(z[2]), go = sigmoidf_(z[3]);
+                const float gu = tanhf_(z[4]);
+                const float c = gi * gu + gl * cl + gr * cr;
+                const float h = go * tanhf_(c);
+                store_through(a.C, int64_t(p) * a.ldc + cj, c);
+                float* gp = a.G + int64_t(p) * a.ldg + cj;
+                gp[0] = gi;
+                gp[H] = gl;
+                gp[2 * H] = gr;
+                gp[3 * H] = go;
+                gp[4 * H] = gu;
+                if (par >= 0) store_through(a.HLR, int64_t((par >> 1) - a.M0) * a.ldl + (par & 1) * H + cj, h);
+                else a.h_root[int64_t(rk) * H + cj] = h;
+            }
+        }
+        if (L + 1 < a.nlev) {
+            persist::barrier_arrive(bar);
+            persist::barrier_wait(bar);
+        }
+    }
+}
+
+// --------------------------------------------------------------- backward
+struct BwdArgs {
+    int E, H, N, M0, nlev, ncol, nseg, V;
+    const int32_t* loff;
+    const int32_t* lword;
+    const int32_t* lchild;
+    const int32_t* rchild;
+    const int32_t* rootk;
+    const int32_t* seg;        // order[M0], off[nseg + 1], sid[nseg], first[grid]: the leaves grouped by word
+                               // (ids ascending), and each workgroup's first group of the embedding rows
+    const float* emb;          // [V x E]
+    const float* W;            // [5H x E]
+    const float* U;            // [5H x 2H]
+    const float* G;            // the forward's gates, cells and [h_L ; h_R] rows
+    int64_t ldg;
+    const float* C;
+    int64_t ldc;
+    const float* HLR;
+    int64_t ldl;
+    const float* dh_root;      // [trees x H]
+    float* dh;                 // [N x ldc] gradient of h from the parent's level
+    float* dc;                 // [N x ldc]
+    float* dA;                 // [N x lda] gradient of the gate pre-activations
+    int64_t lda;
+    float* dxl;                // [M0 x ldx] gradient of the leaves' inputs
+    int64_t ldx;
+    float* demb;               // [V x E], every row written
+    float* dW;                 // [5H x E]
+    float* dU;                 // [5H x 2H]
+    float* db;                 // [5H]
+    TreeSync* sync;
+};
+
+__host__ __device__ inline int bwd_hp(int H) { return padto(H, kUC); }
+__host__ __device__ inline int bwd_lds_floats(int H) {
+    const int sUs = 5 * bwd_hp(H) + 4, sC = 5 * kUC + 4;
+    const int level = 32 * sUs + 32 * sC;
+    const int tail = 2 * 32 * (kKC + 4);   // the contractions over nodes reuse the front
+    return (level > tail ? level : tail) + kWaves * 32 * kRed;
+}
+
+// The four rows a thread owns in a 32-row tile (rows tid / 32 + 8 i) and
+// their links; with the unit lane tid % 32 of a 32-unit chunk this is the
+// thread's share of the tile's cells.
+constexpr int kRowsPerThread = 32 * kUC / kThreads;   // 4
+struct RowLinks {
+    int p[kRowsPerThread], lc[kRowsPerThread], rc[kRowsPerThread], rk[kRowsPerThread];
+};
+// Inputs of the cell backward of one chunk (unit j of the thread's rows).
+struct CellIn {
+    float g[kRowsPerThread][5], c[kRowsPerThread], cl[kRowsPerThread], cr[kRowsPerThread];
+    float dh[kRowsPerThread], dc[kRowsPerThread];
+};
+
+__device__ __forceinline__ RowLinks row_links(const BwdArgs& a, int pt, int rows) {
+    RowLinks r;
+#pragma unroll
+    for (int i = 0; i < kRowsPerThread; ++i) {
+        const int m = int(threadIdx.x) / 32 + 8 * i;
+        r.p[i] = m < rows ? pt + m : -1;
+        r.lc[i] = r.p[i] >= 0 ? a.lchild[r.p[i]] : -1;
+        r.rc[i] = r.p[i] >= 0 ? a.rchild[r.p[i]] : -1;
+        r.rk[i] = r.p[i] >= 0 ? a.rootk[r.p[i]] : -1;
+    }
+    return r;
+}
+// All loads of a chunk are issued together (one round trip per chunk).
+__device__ __forceinline__ CellIn cell_inputs(const BwdArgs& a, const RowLinks& r, int j) {
+    CellIn x;
+    const int H = a.H;
+#pragma unroll
+    for (int i = 0; i < kRowsPerThread; ++i) {
+        const bool ok = r.p[i] >= 0 && j < H;
+        const int64_t p = ok ? r.p[i] : 0;
+#pragma unroll
+        for (int q = 0; q < 5; ++q) x.g[i][q] = ok ? a.G[p * a.ldg + q * H + j] : 0.f;
+        x.c[i] = ok ? a.C[p * a.ldc + j] : 0.f;
+        x.cl[i] = (ok && r.lc[i] >= 0) ? a.C[int64_t(r.lc[i]) * a.ldc + j] : 0.f;
+        x.cr[i] = (ok && r.rc[i] >= 0) ? a.C[int64_t(r.rc[i]) * a.ldc + j] : 0.f;
+        x.dh[i] = !ok ? 0.f : r.rk[i] >= 0 ? a.dh_root[int64_t(r.rk[i]) * H + j] : a.dh[p * a.ldc + j];
+        x.dc[i] = (!ok || r.rk[i] >= 0) ? 0.f : a.dc[p * a.ldc + j];
+    }
+    return x;
+}
+// Cell backward of row i: dA of the five gates (0 for an absent cell), and
+// the children's dc.
+__device__ __forceinline__ void cell_grad(const CellIn& x, int i, float (&da)[5], float& dcl, float& dcr) {
+    const float gi = x.g[i][0], gl = x.g[i][1], gr = x.g[i][2], go = x.g[i][3], gu = x.g[i][4];
+    const float tau = tanhf_(x.c[i]);
+    const float d_o = x.dh[i] * tau;
+    const float dct = x.dc[i] + x.dh[i] * go * (1.f - tau * tau);
+    da[0] = dct * gu * gi * (1.f - gi);
+    da[1] = dct * x.cl[i] * gl * (1.f - gl);
+    da[2] = dct * x.cr[i] * gr * (1.f - gr);
+    da[3] = d_o * go * (1.f - go);
+    da[4] = dct * gi * (1.f - gu * gu);
+    dcl = dct * gl;
+    dcr = dct * gr;
+}
+
+// acc += sum over k in [0, K) of Aop(row, k) Bop(col, k) for a 32 x 32 tile,
+// staged kKC k at a time through LDS (A and B chunks [32][kKC + 4]); the
+// waves take its k-steps of 16 in turn, and the next chunk is loaded into
+// registers while the current one is contracted.  fa(r, k) / fb(c, k)
+// return the operand value (0 outside).  AK: A is contiguous in k in memory
+// (consecutive threads then take consecutive k), else in r (consecutive
+// threads take consecutive rows of one k); B is always contiguous in c.
+template <bool AK, class FA, class FB>
+__device__ __forceinline__ void node_contraction(f32x16_t& acc, float* Ac, float* Bc, int K, FA fa, FB fb) {
+    constexpr int sK = kKC + 4, PER = 32 * kKC / kThreads;   // 8 elements of each operand per thread
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float va[PER], vb[PER];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * kThreads;
+            const int kk = idx / 32, r = idx % 32;
+            vb[i] = k0 + kk < K ? fb(r, k0 + kk) : 0.f;
+            if constexpr (AK) {
+                const int ra = idx / kKC, ka = idx % kKC;
+                va[i] = k0 + ka < K ? fa(ra, k0 + ka) : 0.f;
+            } else {
+                va[i] = k0 + kk < K ? fa(r, k0 + kk) : 0.f;
+            }
+        }
+    };
+    if (K > 0) fetch(0);
+    for (int k0 = 0; k0 < K; k0 += kKC) {
+        __syncthreads();   // the previous chunk's reads are done
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * kThreads;
+            const int kk = idx / 32, r = idx % 32;
+            Bc[r * sK + kk] = vb[i];
+            if constexpr (AK) Ac[(idx / kKC) * sK + idx % kKC] = va[i];
+            else Ac[r * sK + kk] = va[i];
+        }
+        if (k0 + kKC < K) fetch(k0 + kKC);
+        __syncthreads();
+        for (int ks = wave; ks < kKC / 16; ks += kWaves) {
+            Frag<float> xa, xb;
+            xa.load(Ac + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
+            xb.load(Bc + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
+            mfma(acc, xa, xb);
+        }
+    }
+}
+
+__global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
+    extern __shared__ __align__(16) float sm[];
+    const int E = a.E, H = a.H, H2 = 2 * a.H, G5 = 5 * a.H;
+    const int Hp = bwd_hp(H);
+    const int sUs = 5 * Hp + 4, sC = 5 * kUC + 4;
+    float* Us = sm;                         // [32 columns of [dh_L; dh_R]][5 Hp]: U[q H + j][col] at q Hp + j
+    float* dAc = Us + 32 * sUs;             // [32 node rows][5 kUC]: gate q of chunk unit u at q kUC + u
+    const int front = bwd_lds_floats(H) - kWaves * 32 * kRed;
+    float* red = sm + front;                // [waves][32][kRed]
+    const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
+    TreeBarrier bar;
+    persist::barrier_init(bar, a.sync);
+    const int col = int(blockIdx.x) % a.ncol, r0 = int(blockIdx.x) / a.ncol;
+    const int R = int(gridDim.x) / a.ncol;
+    // U[q H + j][32 col + c] -> Us[c][q Hp + j]: 32 consecutive columns of a
+    // row of U are one 128-byte piece
+    if (H2 % 4 == 0) {
+        stage4<8>(8 * 5 * Hp,
+                  [&](int idx) {
+                      const int row = idx / 8, c4 = 4 * (idx % 8), q = row / Hp, j = row - q * Hp, n = 32 * col + c4;
+                      return (j < H && n < H2) ? ld4(a.U + (int64_t(q) * H + j) * H2 + n) : make_float4(0.f, 0.f, 0.f, 0.f);
+                  },
+                  [&](int idx, float4 v) {
+                      const int row = idx / 8, c4 = 4 * (idx % 8);
+                      Us[(c4 + 0) * sUs + row] = v.x;
+                      Us[(c4 + 1) * sUs + row] = v.y;
+                      Us[(c4 + 2) * sUs + row] = v.z;
+                      Us[(c4 + 3) * sUs + row] = v.w;
+                  });
+    } else {
+        stage<16>(32 * 5 * Hp,
+                  [&](int idx) {
+                      const int row = idx / 32, c = idx % 32, q = row / Hp, j = row - q * Hp, n = 32 * col + c;
+                      return (j < H && n < H2) ? a.U[(int64_t(q) * H + j) * H2 + n] : 0.f;
+                  },
+                  [&](int idx, float v) { Us[(idx % 32) * sUs + idx / 32] = v; });
+    }
+    const int u = tid % 32;   // this thread's unit lane within a chunk
+
+    for (int L = a.nlev - 1; L >= 1; --L) {
+        const int p0 = a.loff[L], p1 = a.loff[L + 1];
+        const int ntile = (p1 - p0 + 31) / 32;
+        for (int t = r0; t < ntile; t += R) {
+            const int pt = p0 + 32 * t, rows = min(32, p1 - pt);
+            const RowLinks lk = row_links(a, pt, rows);
+            // inputs of chunks j0 and j0 + kUC in flight (two chunks ahead)
+            CellIn x = cell_inputs(a, lk, u);
+            CellIn xn = cell_inputs(a, lk, kUC + u);
+            f32x16_t acc;
+            zero_acc(acc);
+            for (int j0 = 0; j0 < H; j0 += kUC) {
+                const int j = j0 + u;
+                __syncthreads();   // the previous chunk's reads of dAc are done
+#pragma unroll
+                for (int i = 0; i < kRowsPerThread; ++i) {
+                    const int m = tid / 32 + 8 * i;
+                    float da[5], dcl, dcr;
+                    cell_grad(x, i, da, dcl, dcr);
+                    if (lk.p[i] < 0 || j >= H) {
+#pragma unroll
+                        for (int q = 0; q < 5; ++q) da[q] = 0.f;
+                    } else if ((j0 / kUC) % a.ncol == col) {
+#pragma unroll
+                        for (int q = 0; q < 5; ++q) store_through(a.dA, int64_t(lk.p[i]) * a.lda + q * H + j, da[q]);
+                        store_through(a.dc, int64_t(lk.lc[i]) * a.ldc + j, dcl);
+                        store_through(a.dc, int64_t(lk.rc[i]) * a.ldc + j, dcr);
+                    }
+#pragma unroll
+                    for (int q = 0; q < 5; ++q) dAc[m * sC + q * kUC + u] = da[q];
+                }
+                // the chunk after next, loaded while this one is contracted
+                x = xn;
+                if (j0 + 2 * kUC < H) xn = cell_inputs(a, lk, j + 2 * kUC);
+                __syncthreads();
+                // D[node m][column c] += sum over the chunk's gate columns
+                for (int ks = wave; ks < 5 * (kUC / 16); ks += kWaves) {
+                    const int q = ks / (kUC / 16), s = ks - q * (kUC / 16);
+                    Frag<float> fa, fb;
+                    fa.load(dAc + (lane & 31) * sC + q * kUC + s * 16 + 8 * (lane >> 5));
+                    fb.load(Us + (lane & 31) * sUs + q * Hp + j0 + s * 16 + 8 * (lane >> 5));
+                    mfma(acc, fa, fb);
+                }
+            }
+            spill_acc(acc, red, wave, lane);
+            __syncthreads();
+            // [dh_L; dh_R] of the tile's rows to the two children
+            for (int idx = tid; idx < 32 * 32; idx += kThreads) {
+                const int m = idx / 32, c = idx % 32, n = 32 * col + c;
+                if (m < rows && n < H2) {
+                    const int p = pt + m;
+                    const float v = red_sum(red, m, c);
+                    if (n < H) store_through(a.dh, int64_t(a.lchild[p]) * a.ldc + n, v);
+                    else store_through(a.dh, int64_t(a.rchild[p]) * a.ldc + (n - H), v);
+                }
+            }
+            __syncthreads();   // red is read before the next tile overwrites it
+        }
+        persist::barrier_arrive(bar);
+        persist::barrier_wait(bar);
+    }
+    // the leaves: dA only (no children), tiles dealt to all workgroups
+    {
+        const int ntile = (a.M0 + 31) / 32;
+        for (int t = int(blockIdx.x); t < ntile; t += int(gridDim.x)) {
+            const int rows = min(32, a.M0 - 32 * t);
+            const RowLinks lk = row_links(a, 32 * t, rows);
+            for (int j0 = 0; j0 < H; j0 += kUC) {
+                const CellIn x = cell_inputs(a, lk, j0 + u);
+#pragma unroll
+                for (int i = 0; i < kRowsPerThread; ++i) {
+                    if (lk.p[i] < 0 || j0 + u >= H) continue;
+                    float da[5], dcl, dcr;
+                    cell_grad(x, i, da, dcl, dcr);
+#pragma unroll
+                    for (int q = 0; q < 5; ++q) store_through(a.dA, int64_t(lk.p[i]) * a.lda + q * H + j0 + u, da[q]);
+                }
+            }
+        }
+    }
+    persist::barrier_arrive(bar);
+    persist::barrier_wait(bar);
+
+    // contractions over nodes, dealt to the workgroups in turn
+    {
+        float* Ac = sm;
+        float* Bc = sm + 32 * (kKC + 4);
+        const int ng = (G5 + 31) / 32, nh2 = (H2 + 31) / 32, ne = (E + 31) / 32, nl = (a.M0 + 31) / 32;
+        const int n_dU = ng * nh2, n_dW = ng * ne, n_dx = nl * ne, n_db = ng;
+        const int total = n_dU + n_dW + n_dx + n_db;
+        const int Nint = a.N - a.M0;
+        for (int it = int(blockIdx.x); it < total; it += int(gridDim.x)) {
+            if (it >= n_dU + n_dW + n_dx) {
+                // db over all nodes for 32 columns: 32 row groups of 16-byte
+                // pieces (8 per row), 16 loads in flight per thread, then the
+                // groups in order
+                const int i = it - (n_dU + n_dW + n_dx);
+                const int c4 = 4 * (tid % 8), rg = tid / 8, n = 32 * i + c4;
+                constexpr int RG = kThreads / 8;
+                float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
+                const bool vec = a.lda % 4 == 0;
+                for (int p0 = rg; p0 < a.N; p0 += RG * 16) {
+                    float4 v[16];
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) {
+                        const int p = p0 + q * RG;
+                        v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
+                        if (p < a.N) {
+                            const float* row = a.dA + int64_t(p) * a.lda + n;
+                            if (vec && n + 3 < G5) v[q] = ld4(row);
+                            else {
+                                v[q].x = n < G5 ? row[0] : 0.f;
+                                v[q].y = n + 1 < G5 ? row[1] : 0.f;
+                                v[q].z = n + 2 < G5 ? row[2] : 0.f;
+                                v[q].w = n + 3 < G5 ? row[3] : 0.f;
+                            }
+                        }
+                    }
+#pragma unroll
+                    for (int q = 0; q < 16; ++q) {
+                        s4.x += v[q].x; s4.y += v[q].y; s4.z += v[q].z; s4.w += v[q].w;
+                    }
+                }
+                __syncthreads();
+                red[rg * 32 + c4 + 0] = s4.x;
+                red[rg * 32 + c4 + 1] = s4.y;
+                red[rg * 32 + c4 + 2] = s4.z;
+                red[rg * 32 + c4 + 3] = s4.w;
+                __syncthreads();
+                if (tid < 32 && 32 * i + tid < G5) {
+                    float t2 = 0.f;
+                    for (int q = 0; q < RG; ++q) t2 += red[q * 32 + tid];
+                    a.db[32 * i + tid] = t2;
+                }
+                continue;
+            }
+            f32x16_t acc;
+            zero_acc(acc);
+            int kind, ti, tj;
+            if (it < n_dU) { kind = 0; ti = it / nh2; tj = it % nh2; }
+            else if (it < n_dU + n_dW) { kind = 1; ti = (it - n_dU) / ne; tj = (it - n_dU) % ne; }
+            else { kind = 2; ti = (it - n_dU - n_dW) / ne; tj = (it - n_dU - n_dW) % ne; }
+            if (kind == 0) {
+                // dU[32 ti + r][32 tj + c] = sum over internal nodes of dA[p][.] [h_L; h_R][p][.]
+                node_contraction<false>(acc, Ac, Bc, Nint,
+                    [&](int r, int k) {
+                        const int n = 32 * ti + r;
+                        return n < G5 ? a.dA[int64_t(a.M0 + k) * a.lda + n] : 0.f;
+                    },
+                    [&](int c, int k) {
+                        const int n = 32 * tj + c;
+                        return n < H2 ? a.HLR[int64_t(k) * a.ldl + n] : 0.f;
+                    });
+            } else if (kind == 1) {
+                // dW = sum over leaves of dA[p][.] x_p[.]
+                node_contraction<false>(acc, Ac, Bc, a.M0,
+                    [&](int r, int k) {
+                        const int n = 32 * ti + r;
+                        return n < G5 ? a.dA[int64_t(k) * a.lda + n] : 0.f;
+                    },
+                    [&](int c, int k) {
+                        const int n = 32 * tj + c;
+                        return n < E ? a.emb[int64_t(a.lword[k]) * E + n] : 0.f;
+                    });
+            } else {
+                // dx_leaf[p][.] = sum over gate columns of dA[p][k] W[k][.]
+                node_contraction<true>(acc, Ac, Bc, G5,
+                    [&](int r, int k) {
+                        const int p = 32 * ti + r;
+                        return p < a.M0 ? a.dA[int64_t(p) * a.lda + k] : 0.f;
+                    },
+                    [&](int c, int k) {
+                        const int n = 32 * tj + c;
+                        return n < E ? a.W[int64_t(k) * E + n] : 0.f;
+                    });
+            }
+            spill_acc(acc, red, wave, lane);
+            __syncthreads();
+            for (int idx = tid; idx < 32 * 32; idx += kThreads) {
+                const int r = idx / 32, c = idx % 32;
+                const float v = red_sum(red, r, c);
+                if (kind == 0) {
+                    const int m = 32 * ti + r, n = 32 * tj + c;
+                    if (m < G5 && n < H2) a.dU[int64_t(m) * H2 + n] = v;
+                } else if (kind == 1) {
+                    const int m = 32 * ti + r, n = 32 * tj + c;
+                    if (m < G5 && n < E) a.dW[int64_t(m) * E + n] = v;
+                } else {
+                    const int p = 32 * ti + r, n = 32 * tj + c;
+                    if (p < a.M0 && n < E) store_through(a.dxl, int64_t(p) * a.ldx + n, v);
+                }
+            }
+            __syncthreads();   // red is read before the next item overwrites it
+        }
+    }
+    persist::barrier_arrive(bar);
+    persist::barrier_wait(bar);
+
+    // the embedding gradient.  Rows without leaves are zero: each workgroup
+    // zeroes those of an equal share of the table (first[w] is the first group
+    // whose id is at least its first row).  Rows with leaves are the sum of
+    // their dx rows in ascending leaf order, one group per workgroup in turn,
+    // so a frequent word's many leaves do not all fall to one workgroup.
+    {
+        const int32_t* order = a.seg;
+        const int32_t* off = order + a.M0;
+        const int32_t* sid = off + a.nseg + 1;
+        const int32_t* first = sid + a.nseg;
+        const int64_t v0 = int64_t(a.V) * blockIdx.x / gridDim.x, v1 = int64_t(a.V) * (blockIdx.x + 1) / gridDim.x;
+        int gi = first[blockIdx.x];
+        int64_t next_id = gi < a.nseg ? sid[gi] : a.V;
+        for (int64_t v = v0; v < v1; ++v) {
+            if (v == next_id) {
+                ++gi;
+                next_id = gi < a.nseg ? sid[gi] : a.V;
+                continue;
+            }
+            for (int e = tid; e < E; e += kThreads) a.demb[v * E + e] = 0.f;
+        }
+        int* lorder = reinterpret_cast<int*>(sm);   // the leaves of the current row, kThreads at a time
+        for (int g = int(blockIdx.x); g < a.nseg; g += int(gridDim.x)) {
+            const int64_t v = sid[g];
+            const int k0 = off[g], k1 = off[g + 1];
+            float s[2] = {0.f, 0.f};   // columns tid and tid + kThreads (E <= kMaxE)
+            for (int kb = k0; kb < k1; kb += kThreads) {
+                const int nk = min(kThreads, k1 - kb);
+                __syncthreads();   // the previous batch of leaves is read
+                if (tid < nk) lorder[tid] = order[kb + tid];
+                __syncthreads();
+                for (int k = 0; k < nk; k += 8) {
+                    float x0[8], x1[8];
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        const int64_t r = k + q < nk ? int64_t(lorder[k + q]) * a.ldx : -1;
+                        x0[q] = (r >= 0 && tid < E) ? a.dxl[r + tid] : 0.f;
+                        x1[q] = (r >= 0 && tid + kThreads < E) ? a.dxl[r + tid + kThreads] : 0.f;
+                    }
+#pragma unroll
+                    for (int q = 0; q < 8; ++q) {
+                        s[0] += x0[q];
+                        s[1] += x1[q];
+                    }
+                }
+            }
+            if (tid < E) a.demb[v * E + tid] = s[0];
+            if (tid + kThreads < E) a.demb[v * E + tid + kThreads] = s[1];
+        }
+    }
+}
+
+}  // namespace tpersist
+}  // namespace janus

@@ -28,7 +28,7 @@ EXPORTS = [
     "janus_lstm_workspace_bytes", "janus_lstm_seq_fwd", "janus_lstm_seq_bwd", "janus_lstm_device_report",
     "janus_lstm_fault_flag", "janus_lstm_schedule",
     "janus_treelstm_workspace_bytes", "janus_tree_schedule_build", "janus_treelstm_fwd",
-    "janus_treelstm_bwd", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
+    "janus_treelstm_bwd", "janus_treelstm_device_report", "janus_xent_workspace_bytes", "janus_embed_softmax_xent",
     "janus_mse_workspace_bytes", "janus_linear_mse", "janus_loss_reduce", "janus_trace_begin",
     "janus_trace_end", "janus_status_string", "janus_version", "janus_last_error",
     "janus_sgd_workspace_bytes", "janus_sgd_clip_update", "janus_sgd_clip_update_noalloc",
@@ -123,6 +123,8 @@ def lib():
         L.janus_treelstm_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, vp, vp, vp, vp, sz, vp]
         L.janus_treelstm_bwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, vp, vp, sz, vp, vp, vp,
                                          vp, vp, vp]
+        L.janus_treelstm_device_report.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, sz,
+                                                   C.POINTER(i32), vp]
         L.janus_treernn_workspace_bytes.restype = sz
         L.janus_treernn_workspace_bytes.argtypes = [C.POINTER(TreeDesc), i32, i32]
         L.janus_treernn_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, vp, vp, vp, sz, vp]
@@ -295,6 +297,18 @@ def janus_treelstm_bwd(desc: TreeDesc, trees, emb, W, U, ws, dh_root, demb, dW, 
                                   ws.numel() * ws.element_size(), _p(dh_root), _p(demb), _p(dW), _p(dU), _p(db),
                                   _stream(stream))
     _check(st, "janus_treelstm_bwd")
+
+
+def janus_treelstm_device_report(desc: TreeDesc, trees, ws, stream=None) -> int:
+    """Synchronises the stream and returns 1 if a level barrier of the last
+    TreeLSTM forward or backward on this workspace ran out of its wait (the
+    call then raises JanusError(DEVICE)), else 0."""
+    tb, keep = _tree_c(trees.left, trees.right, trees.word, trees.root)
+    out = C.c_int32(0)
+    st = lib().janus_treelstm_device_report(C.byref(desc), C.byref(tb), _p(ws), ws.numel() * ws.element_size(),
+                                            C.byref(out), _stream(stream))
+    _check(st, "janus_treelstm_device_report")
+    return int(out.value)
 
 
 def janus_treernn_workspace_bytes(H, V, max_nodes, max_trees) -> int:

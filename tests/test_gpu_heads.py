@@ -105,16 +105,21 @@ def test_embedding_backward_many_zipf_rows(dtype, V, Hd, rows):
     np.testing.assert_array_equal(dE.cpu().numpy(), first)
 
 
-@pytest.mark.parametrize("dtype,V,Hd,rows", [("f32", 5, 150, 25), ("f32", 1001, 36, 77), ("bf16", 1001, 64, 300),
-                                             ("bf16", 5, 64, 33), ("f32", 13001, 36, 9)])
+@pytest.mark.parametrize("dtype,V,Hd,rows,small", [("f32", 5, 150, 25, "1"), ("f32", 5, 150, 25, "0"),
+                                                   ("f32", 1001, 36, 77, "1"), ("bf16", 1001, 64, 300, "1"),
+                                                   ("bf16", 5, 64, 33, "1"), ("bf16", 5, 64, 33, "0"),
+                                                   ("f32", 64, 96, 40, "1"), ("f32", 13001, 36, 9, "1")])
 @pytest.mark.parametrize("kind", ["same", "ends", "random"])
-def test_softmax_cross_entropy(dtype, V, Hd, rows, kind):
+def test_softmax_cross_entropy(dtype, V, Hd, rows, small, kind, monkeypatch):
     """XENT_FWD_BWD: mean loss, dh, dWout and dbout of one call, with the
-    targets all on one class, on the two end classes, or random.  A row of
-    up to 12288 logits stays in LDS across the softmax passes; the 13001
-    class case takes the path that reads the row again."""
+    targets all on one class, on the two end classes, or random.  Heads of
+    at most 64 classes whose operands fit 64 KB of LDS run in one workgroup
+    (JANUS_XENT_SMALL=0 takes the contractions instead, as for the larger
+    heads); a row of up to 12288 logits stays in LDS across the softmax
+    passes; the 13001 class case takes the path that reads the row again."""
     import torch
     from paper_1812_01329_amd import janus as J
+    monkeypatch.setenv("JANUS_XENT_SMALL", small)
     rng = np.random.default_rng(3 * V + rows)
     tgt = _ids(kind, rng, V, rows)
     print(f"[xent] {dtype} V={V} H={Hd} rows={rows} targets={kind}", flush=True)
@@ -129,9 +134,12 @@ def test_softmax_cross_entropy(dtype, V, Hd, rows, kind):
     dW = torch.empty((V, Hd), dtype=torch.float32, device="cuda:0")
     db = torch.empty((V,), dtype=torch.float32, device="cuda:0")
     loss = torch.empty((1,), dtype=torch.float32, device="cuda:0")
+    J.janus_trace_begin()
     J.janus_embed_softmax_xent(desc, J.XENT_FWD_BWD, tgt, torch.from_numpy(tgt).to("cuda:0"), table=_dev(W, dtype),
                                bias=_dev(b, dtype), inp=_dev(h, dtype), out=dh, dtable=dW, dbias=db, loss=loss,
                                ws=ws)
+    labels = {r["label"] for r in J.janus_trace_end()}
+    assert ("xent_small" in labels) == (small == "1" and V <= 64), labels
     torch.cuda.synchronize()
     rl, rdh, rdW, rdb, _ = H_.softmax_xent(h, W, b, tgt)
     t = TOL[dtype]

@@ -117,6 +117,87 @@ def test_treelstm_many_leaves_fp32():
         check(k, g[k], r[k], t["grad"])
 
 
+def _chain_and_leaf_batch():
+    """A one-leaf tree, a left chain of 12 leaves and a balanced 16-leaf tree."""
+    left, right, word, roots = [], [], [], []
+    rng = np.random.default_rng(1)
+    roots.append(wl.random_bracketing(rng, 1, np.array([3]), left, right, word))
+    prev = None
+    for k in range(12):
+        left.append(-1); right.append(-1); word.append(int(rng.integers(0, 40)))
+        leaf = len(left) - 1
+        if prev is None:
+            prev = leaf
+        else:
+            left.append(prev); right.append(leaf); word.append(-1)
+            prev = len(left) - 1
+    roots.append(prev)
+    roots.append(wl.random_bracketing(rng, 16, rng.integers(0, 40, 16), left, right, word))
+    trees = wl.TreeBatch(np.asarray(left, np.int32), np.asarray(right, np.int32), np.asarray(word, np.int32),
+                         np.asarray(roots, np.int32))
+    base = wl.sst_treelstm(n_trees=2, E=24, H=20, V=40, seed=9)
+    base.trees = trees
+    base.labels = rng.integers(0, base.C, trees.num_trees).astype(np.int32)
+    return base
+
+
+def _leaves_only_batch():
+    """Seven trees of one leaf each: a single level, no internal node."""
+    base = wl.sst_treelstm(n_trees=2, E=24, H=20, V=40, seed=10)
+    n = 7
+    base.trees = wl.TreeBatch(np.full(n, -1, np.int32), np.full(n, -1, np.int32),
+                              np.arange(3, 3 + n, dtype=np.int32) * 5 % 40, np.arange(n, dtype=np.int32))
+    base.labels = np.random.default_rng(10).integers(0, base.C, n).astype(np.int32)
+    return base
+
+
+@pytest.mark.parametrize("persist", ["1", "0"])
+@pytest.mark.parametrize("case", ["sst", "chains", "leaves", "odd"])
+def test_treelstm_persistent_levels(persist, case, monkeypatch):
+    """The TreeLSTM step with each direction as one persistent launch (a
+    grid barrier between levels, fp32 MFMA contractions) and with the
+    level-by-level kernels (JANUS_TREE_PERSIST=0), each against the oracle:
+    the SST-sized batch, a one-leaf tree with a 12-leaf chain and a balanced
+    tree, a batch of one-leaf trees only, and odd sizes (E = 37, H = 29:
+    partial unit groups and column tiles)."""
+    from paper_1812_01329_amd import janus as J
+    monkeypatch.setenv("JANUS_TREE_PERSIST", persist)
+    if case == "sst":
+        w = wl.sst_treelstm()
+    elif case == "chains":
+        w = _chain_and_leaf_batch()
+    elif case == "leaves":
+        w = _leaves_only_batch()
+    else:
+        w = wl.sst_treelstm(n_trees=9, E=37, H=29, V=77, seed=15)
+    print(f"[tree-persist] case={case} persist={persist} N={w.trees.num_nodes}", flush=True)
+    J.janus_trace_begin()
+    step, g = _run(w)
+    labels = {r["label"] for r in J.janus_trace_end()}
+    if persist == "1":
+        assert {"treelstm_fwd_persistent", "treelstm_bwd_persistent"} <= labels, labels
+        assert not labels & {"tree_level_gemm", "tree_fwd_point", "tree_bwd_level"}, labels
+    else:
+        assert "treelstm_fwd_persistent" not in labels, labels
+    assert J.janus_treelstm_device_report(step.desc, w.trees, step.ws) == 0
+    r = oracle_steps.tree_step(w)
+    t = TOL["f32"]
+    check("loss", np.array([g["loss"]]), np.array([r["loss"]]), t["out"])
+    check("h_root", g["h_root"], r["h_root"], t["out"])
+    for k in ("dh_root", "dWs", "dbs", "dW", "dU", "db", "demb"):
+        check(k, g[k], r[k], t["grad"])
+    H = w.H
+    assert np.all(g["dW"][H:3 * H] == 0.0)   # forget rows of W see no gradient
+    used = np.zeros(w.V, bool)
+    used[w.trees.word[w.trees.word >= 0]] = True
+    assert np.all(g["demb"][~used] == 0.0)   # rows of words not in the batch are zero
+    # a second step on the same workspace gives the same bits
+    step.run()
+    g2 = step.results()
+    for k in ("h_root", "dW", "dU", "db", "demb"):
+        assert np.array_equal(g[k], g2[k]), k
+
+
 def test_lm2048_reduced_shape_bf16():
     """The regression workload's structure (2 layers, projection + MSE) at a
     shape the oracle runs in seconds, spanning several tiles with ragged tails."""
