@@ -285,13 +285,14 @@ int persist_bwd_slices(const janus_lstm_desc& d) {
     return 0;
 }
 
-// The persistent path needs bf16, H a multiple of 8, at most 256 rows, one
-// co-resident workgroup per slice and the weight slice in LDS.  It can be
+// The persistent path needs bf16, H a multiple of 8, one co-resident
+// workgroup per slice and the weight slice in LDS; a batch of more than 256
+// rows runs in parts of 256 sorted rows, one launch each.  It can be
 // switched off with JANUS_PERSIST=0 (the per-step kernels then run).
 bool use_persistent(const janus_lstm_desc& d) {
     const char* e = getenv("JANUS_PERSIST");
     const bool env = !(e && e[0] == '0');
-    if (!env || d.dtype != JANUS_BF16 || d.H % 8 != 0 || d.B > persist::kMaxB) return false;
+    if (!env || d.dtype != JANUS_BF16 || d.H % 8 != 0) return false;
     const DeviceInfo info = device_info();
     if (info.cus <= 0) return false;
     return persist_fwd_slices(d) > 0 && persist_bwd_slices(d) > 0;
@@ -971,6 +972,13 @@ double recurrent_rows(const SeqSchedule& s) {
     return r;
 }
 
+// Recurrent rows of the batch part starting at sorted row rb (at most kMaxB rows).
+double part_rows(const SeqSchedule& s, int rb) {
+    double rows = 0;
+    for (int t = 0; t < s.t_eff; ++t) rows += std::min(std::max(s.active[t] - rb, 0), persist::kMaxB);
+    return rows;
+}
+
 // With equal lengths the persistent forward also writes h transposed (HT,
 // h0 in the first B columns): HT is then h_{t-1} transposed for every
 // packed row (the dWh operand) and HT + B is the layer output transposed
@@ -1057,7 +1065,15 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     if (l == d.L - 1 && a.HT) a.Hs = nullptr;
     a.ldht = w.ldht;
     a.sync = w.sync;
-    return launch_fwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * recurrent_rows(s), st);
+    // batches past kMaxB rows run in parts of kMaxB sorted rows, one launch
+    // each (rows are independent sequences; the counters restart per launch)
+    for (int rb = 0; rb < B; rb += persist::kMaxB) {
+        if (rb > 0 && (e = zero_fill(w.sync, persist::kSyncCounterBytes, st)) != JANUS_OK) return e;
+        a.rbase = rb;
+        e = launch_fwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * part_rows(s, rb), st);
+        if (e != JANUS_OK) return e;
+    }
+    return JANUS_OK;
 }
 
 template <typename T, class Cfg>
@@ -1244,9 +1260,15 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
             a.ldh = w.ldh;
             a.ldg = w.ldg;
             a.sync = w.sync;
-            double rows = 0;
-            for (int t = 0; t < s.t_eff; ++t) rows += s.active[t];
-            if ((e = launch_bwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * rows, st)) != JANUS_OK) return e;
+            // parts of kMaxB sorted rows, as in the forward; the bias
+            // gradient of a later part is added to the earlier parts' sum
+            for (int rb = 0; rb < B; rb += persist::kMaxB) {
+                if (rb > 0 && (e = zero_fill(w.sync, persist::kSyncCounterBytes, st)) != JANUS_OK) return e;
+                a.rbase = rb;
+                a.db_add = rb > 0 ? 1 : 0;
+                e = launch_bwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * part_rows(s, rb), st);
+                if (e != JANUS_OK) return e;
+            }
         } else {
         {
         TraceScope trace("lstm_bwd_init", 0.0, double(bh) * 16.0, st);

@@ -253,6 +253,7 @@ __device__ __forceinline__ GroupPlace group_place(const Barrier& bar, Sync* sync
 // ---------------------------------------------------------------- forward
 struct FwdArgs {
     int H, B, t_eff, fixed;
+    int rbase;                         // first (sorted) batch row of this launch: rows rbase + [0, kMaxB)
     int Kp;                            // H rounded up to 64
     int nkg;                           // k-groups of 16 columns of h (Kp / 16)
     int ksp;                           // columns of the widest K slice (multiple of 16)
@@ -550,9 +551,10 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
     const int sg0 = s * a.nkg / NS, sgn = (s + 1) * a.nkg / NS - sg0;   // k-groups of slice s
     const int kg0 = kw * sgn / KW, kg1 = (kw + 1) * sgn / KW;
     const bf16_t* wrow = Ws + (lane & 31) * wld + 8 * (lane >> 5) + kg0 * 16;
-    const uint32_t hoff = (uint32_t(bt * a.nkg + sg0 + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
+    const int tb = a.rbase / 32 + bt;        // this wave's batch tile of the whole batch
+    const uint32_t hoff = (uint32_t(tb * a.nkg + sg0 + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
     const int H = a.H;
-    const int row = bt * 32 + (lane & 31);   // this lane's batch row (sorted order)
+    const int row = tb * 32 + (lane & 31);   // this lane's batch row (sorted order)
     const int ub = u0 + 4 * (lane >> 5);      // its four consecutive units
     // lanes of the kw == 0 waves own cells; with NS > 1 the last group may
     // extend past H, and its units there have none
@@ -606,7 +608,7 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
         for (int m = 0; m < MT; ++m)
 #pragma unroll
             for (int e = 0; e < 16; ++e) accs[m][e] = 0.f;
-        if (bt * 32 < act) {
+        if (tb * 32 < act) {
             // h_{t-1} is slot t of the fragment-layout copy
             const auto rs = make_rsrc(a.Hf + int64_t(t) * a.hf_slot, uint32_t(a.hf_slot) * 2u);
             contract_frag_mt<MT == 1 ? kDepthFrag : kDepthFrag2, MT>(accs, wrow, 32 * wld, rs, hoff, kg1 - kg0);
@@ -621,8 +623,8 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
             // tile m of a wave holds the pre-activations of member m's units for
             // its 32 batch rows; lane l's 16 values are stored as four 16-byte
             // pieces q, so each store of a wave is 1 KB in one piece
-            const uint32_t po = uint32_t((bt * 4) * 64 + lane) * 16u;
-            if (kw == 0 && bt * 32 < act) {
+            const uint32_t po = uint32_t((tb * 4) * 64 + lane) * 16u;
+            if (kw == 0 && tb * 32 < act) {
 #pragma unroll
                 for (int m = 0; m < MT; ++m) {
                     if (m == s) continue;
@@ -738,6 +740,8 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
 // ---------------------------------------------------------------- backward
 struct BwdArgs {
     int H, B, t_eff, fixed;
+    int rbase;                         // first (sorted) batch row of this launch: rows rbase + [0, kMaxB)
+    int db_add;                        // 1: add this launch's bias gradient to db (a later batch part)
     int nkg;                           // k-groups of 16 interleaved gate columns (4H / 16)
     int ksp;                           // columns of the widest K slice (multiple of 16)
     const int32_t* active;
@@ -876,12 +880,13 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
         __atomic_signal_fence(__ATOMIC_SEQ_CST);
     };
     const bf16_t* wrow = Ws + (lane & 31) * wld + 8 * (lane >> 5) + kg0 * 16;
-    const uint32_t goff = (uint32_t(bt * a.nkg + sg0 + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
-    const int crow = bt * 32 + (lane & 31);   // batch row of this lane's accumulator column
+    const int tb = a.rbase / 32 + bt;        // this wave's batch tile of the whole batch
+    const uint32_t goff = (uint32_t(tb * a.nkg + sg0 + kg0) * 512u + uint32_t(lane) * 8u) * 2u;
+    const int crow = tb * 32 + (lane & 31);   // batch row of this lane's accumulator column
 
     // pointwise ownership: row r, units [ub, ub + 4) (member s of the group
     // takes units [v0 + 8 s, v0 + 8 s + 8))
-    const int r = tid >> 1;
+    const int r = a.rbase + (tid >> 1);
     const int ub = v0 + 8 * s + 4 * (tid & 1);
     const bool mine = r < a.B && ub < H;
     const int b = mine ? (a.perm ? a.perm[r] : r) : 0;
@@ -951,7 +956,7 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             for (int m = 0; m < MT; ++m)
 #pragma unroll
                 for (int e = 0; e < 16; ++e) acc[m][e] = 0.f;
-            if (bt * 32 < act_next) {
+            if (tb * 32 < act_next) {
                 const auto rs = make_rsrc(a.Gf + int64_t(t + 1) * a.gf_slot, uint32_t(a.gf_slot) * 2u);
                 contract_frag_mt<MT == 1 ? kDepthFrag : kDepthFrag2, MT>(acc, wrow, 32 * wld, rs, goff, kg1 - kg0);
             }
@@ -1115,7 +1120,7 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
             float sum = 0.f;
             for (int w = 0; w < kWaves; ++w) sum += wsum[(w * 2 + half) * 16 + e];
             const int u = v0 + 8 * s + 4 * half + (e >> 2), g = e & 3;
-            if (u < H) a.db[int64_t(g) * H + u] = sum;
+            if (u < H) a.db[int64_t(g) * H + u] = a.db_add ? a.db[int64_t(g) * H + u] + sum : sum;
         }
     }
 }

@@ -252,17 +252,33 @@ def test_zero_steps(dtype):
             assert not t.any()
 
 
-def test_large_batch_bf16():
-    """B = 300 rows exceed one 256-row pass of the persistent kernels, so
-    the bf16 recurrence takes the per-step kernels."""
+@pytest.mark.parametrize("B,H,ragged,persist", [(300, 64, True, "1"), (300, 64, True, "0"), (512, 128, False, "1"),
+                                                 (544, 128, True, "1")])
+def test_large_batch_bf16(B, H, ragged, persist, monkeypatch):
+    """Batches of more than 256 rows: the persistent kernels run the sorted
+    rows in parts of 256, one launch each (rows are independent sequences),
+    the backward adding each part's bias gradient to the earlier parts'.
+    B = 300 and 544 with ragged lengths (the last part partial, rows of
+    length 0), B = 512 fixed length; B = 300 also through the per-step
+    kernels (JANUS_PERSIST=0).  Each against the oracle."""
     from paper_1812_01329_amd import janus as J
-    rng = np.random.default_rng(8)
-    w = _lstm("mean_final", "bf16", L=2, I=40, H=64, B=300, T=6, lengths=rng.integers(0, 7, 300), seed=8,
-              h0=True)
+    monkeypatch.setenv("JANUS_PERSIST", persist)
+    rng = np.random.default_rng(B + H)
+    lens = rng.integers(0, 7, B) if ragged else None
+    w = _lstm("mean_final" if ragged else "mse", "bf16", L=2, I=40, H=H, B=B, T=6, lengths=lens, seed=8, h0=True,
+              P=24)
+    print(f"[large-batch] B={B} H={H} ragged={ragged} persist={persist}", flush=True)
     J.janus_trace_begin()
-    _, g = _run(w)
-    labels = {r["label"] for r in J.janus_trace_end()}
-    assert "lstm_fwd_persistent" not in labels, labels
+    step, g = _run(w)
+    stats = J.janus_trace_end()
+    labels = {r["label"]: r["launches"] for r in stats}
+    if persist == "1":
+        parts = (B + 255) // 256
+        assert labels.get("lstm_fwd_persistent") == 2 * parts, labels   # two layers
+        assert labels.get("lstm_bwd_persistent") == 2 * parts, labels
+        assert J.janus_lstm_device_report(step.desc, step.ws)["timed_out"] == 0
+    else:
+        assert "lstm_fwd_persistent" not in labels, labels
     compare_lstm(g, oracle_steps.lstm_step(w), "bf16")
 
 
