@@ -219,6 +219,8 @@ def main():
                     "launches_per_step": top["launches"] // args.steps,
                     "avg_launch_us": round(avg_s * 1e6, 3),
                     "work_per_launch": per_launch,
+                    # algorithmic bytes of the same kernel (each value read or written once) per second
+                    "algorithmic_gbs": round(top["bytes"] / top["launches"] / avg_s / 1e9, 1) if top["bytes"] else None,
                     "traced_ms_per_step": round(total, 3)}
         print(f"[bench] traced pass: {total:.3f} ms of kernel time per step; top kernel {top['label']}",
               file=sys.stderr, flush=True)

@@ -922,12 +922,12 @@ janus_status persistent_launch(K kernel, int blocks, size_t smem, const A& args,
 }
 
 janus_status launch_fwd_persistent(const janus_lstm_desc& d, int ns, persist::FwdArgs& a, double flops,
-                                   hipStream_t st) {
+                                   double bytes, hipStream_t st) {
     static size_t attr[3][4] = {};
     const int kw = persist_kw(d.B);
     const size_t smem = persist_fwd_lds(d, ns);
     const int blocks = persist_fwd_blocks(d, ns);
-    TraceScope trace("lstm_fwd_persistent", flops, 0.0, st);
+    TraceScope trace("lstm_fwd_persistent", flops, bytes, st);
 #define JANUS_FWD_CASES(NS, I)                                                                               \
     switch (kw) {                                                                                            \
         case 1: return persistent_launch(persist::lstm_fwd_persistent<1, NS>, blocks, smem, a, st, attr[I][0]); \
@@ -942,12 +942,12 @@ janus_status launch_fwd_persistent(const janus_lstm_desc& d, int ns, persist::Fw
 }
 
 janus_status launch_bwd_persistent(const janus_lstm_desc& d, int ns, persist::BwdArgs& a, double flops,
-                                   hipStream_t st) {
+                                   double bytes, hipStream_t st) {
     static size_t attr[8] = {};
     const int kw = persist_kw(d.B);
     const size_t smem = persist_bwd_lds(d, ns);
     const int blocks = persist_bwd_blocks(d, ns);
-    TraceScope trace("lstm_bwd_persistent", flops, 0.0, st);
+    TraceScope trace("lstm_bwd_persistent", flops, bytes, st);
     if (ns == 8) {
         switch (kw) {
             case 1: return persistent_launch(persist::lstm_bwd_persistent<1, 8>, blocks, smem, a, st, attr[4]);
@@ -977,6 +977,29 @@ double part_rows(const SeqSchedule& s, int rb) {
     double rows = 0;
     for (int t = 0; t < s.t_eff; ++t) rows += std::min(std::max(s.active[t] - rb, 0), persist::kMaxB);
     return rows;
+}
+
+// Algorithmic bytes of one persistent launch over `rows` active rows: every
+// value the recurrence must read or write, counted once, plus the recurrent
+// weight (4H x H bf16) read once.
+//   forward, per row:  XG (4H bf16), h_{t-1} (H bf16), c_t (H fp32), the
+//                      gates (4H bf16), h_t for the next step (H bf16), and
+//                      the optional copies (h row-major, h transposed, y)
+//   backward, per row: the saved gates (4H bf16), c_{t-1} (H fp32), dy
+//                      (H bf16), dG_{t+1} (4H bf16), dG_t for the next step
+//                      (4H bf16), and the optional dG copies (transposed,
+//                      row-major)
+double fwd_persistent_bytes(const persist::FwdArgs& a, double rows) {
+    const double H = a.H;
+    const double per_row = (8.0 + 2.0 + 4.0 + 8.0 + 2.0) * H + (a.Hs ? 2.0 * H : 0.0) + (a.HT ? 2.0 * H : 0.0) +
+                           (a.y ? 2.0 * H : 0.0);
+    return rows * per_row + 8.0 * H * H;
+}
+double bwd_persistent_bytes(const persist::BwdArgs& a, double rows) {
+    const double H = a.H;
+    const double per_row = (8.0 + 4.0 + 8.0 + 8.0) * H + (a.dy ? 2.0 * H : 0.0) + (a.GT ? 8.0 * H : 0.0) +
+                           (a.G ? 8.0 * H : 0.0);
+    return rows * per_row + 8.0 * H * H;
 }
 
 // With equal lengths the persistent forward also writes h transposed (HT,
@@ -1070,7 +1093,8 @@ janus_status fwd_layer_persistent(const janus_lstm_desc& d, const SeqSchedule& s
     for (int rb = 0; rb < B; rb += persist::kMaxB) {
         if (rb > 0 && (e = zero_fill(w.sync, persist::kSyncCounterBytes, st)) != JANUS_OK) return e;
         a.rbase = rb;
-        e = launch_fwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * part_rows(s, rb), st);
+        const double rows = part_rows(s, rb);
+        e = launch_fwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * rows, fwd_persistent_bytes(a, rows), st);
         if (e != JANUS_OK) return e;
     }
     return JANUS_OK;
@@ -1266,7 +1290,8 @@ janus_status lstm_bwd_impl(const janus_lstm_desc& d, const SeqSchedule& s, const
                 if (rb > 0 && (e = zero_fill(w.sync, persist::kSyncCounterBytes, st)) != JANUS_OK) return e;
                 a.rbase = rb;
                 a.db_add = rb > 0 ? 1 : 0;
-                e = launch_bwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * part_rows(s, rb), st);
+                const double rows = part_rows(s, rb);
+                e = launch_bwd_persistent(d, ns, a, 2.0 * 4.0 * H * double(H) * rows, bwd_persistent_bytes(a, rows), st);
                 if (e != JANUS_OK) return e;
             }
         } else {
