@@ -334,6 +334,21 @@ janus_status janus_treernn_bwd(const janus_treernn_desc* d, const janus_tree_bat
                                const void* dh_root, float* demb, float* dW, float* db,
                                void* stream);
 
+/*
+ * Device-side status of the TreeRNN calls made with this workspace since the
+ * last forward (same d and t), as janus_treelstm_device_report: where the
+ * weight slices fit one CU's LDS (H up to about 312) each direction is one
+ * launch of co-resident workgroups with a device-wide barrier between levels
+ * (Section 4.2.1 recursion, run level by level); a barrier that ran out of
+ * its bounded wait sets *timed_out = 1 and the call returns
+ * JANUS_ERR_DEVICE (the results are then undefined).  The flag is cleared by
+ * the next forward.  Errors: as janus_treernn_fwd's validation, or
+ * INVALID_ARG for a NULL timed_out.
+ */
+janus_status janus_treernn_device_report(const janus_treernn_desc* d, const janus_tree_batch* t,
+                                         const void* ws, size_t ws_bytes, int32_t* timed_out,
+                                         void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Child-Sum TreeLSTM over trees of any arity                               */
 /* ------------------------------------------------------------------------ */

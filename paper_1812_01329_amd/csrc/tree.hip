@@ -30,6 +30,7 @@
 #include "ops.hpp"
 #include "simt.hpp"
 #include "tree_persist.hpp"
+#include "treernn_persist.hpp"
 
 namespace janus {
 
@@ -532,13 +533,19 @@ janus_status treelstm_bwd_persistent_call(const janus_treelstm_desc& d, const ja
 // db = column sums of da over the internal nodes, and the leaves' dh is the
 // gradient of their word vectors.
 struct TreeRnnWs {
-    TreeWs s;                    // schedule arrays (lword .. rootpos) only
+    TreeWs s;                    // schedule arrays (lword .. rootpos, loff, tsync, seg) only
     float* A = nullptr;          // [N x H] pre-activations (forward), da (backward)
     float* Hn = nullptr;         // [N x H] h of every node
     float* HLR = nullptr;        // [N - M0 x 2H] children's h of internal nodes
     float* dh = nullptr;         // [N x H]
     float* Wt = nullptr;         // [2H x H] W transposed
     float* part = nullptr;
+    // persistent path: node rows padded to whole 128-byte lines
+    float* Hnp = nullptr;        // [N x ldh]
+    float* HLRp = nullptr;       // [N x ldl]
+    float* dhp = nullptr;        // [N x ldh]
+    float* dAp = nullptr;        // [N x ldh]
+    int64_t ldh = 0, ldl = 0;
 };
 
 size_t carve_rnn(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base, TreeRnnWs& w) {
@@ -550,13 +557,23 @@ size_t carve_rnn(const janus_treelstm_desc& d, int32_t N, int32_t K, void* base,
     w.s.parent = c.take<int32_t>(N);
     w.s.rootk = c.take<int32_t>(N);
     w.s.rootpos = c.take<int32_t>(K);
+    // the persistent path's level offsets, barrier counters and leaf groups
+    // follow the schedule arrays, so each direction's upload is one copy
+    w.s.loff = c.take<int32_t>(int64_t(N) + 1);
+    w.s.tsync = c.take<tpersist::TreeSync>(1);
+    w.s.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)) + kMaxTreeGrid);
     w.A = c.take<float>(int64_t(N) * H);
     w.Hn = c.take<float>(int64_t(N) * H);
     w.HLR = c.take<float>(int64_t(N) * 2 * H);
     w.dh = c.take<float>(int64_t(N) * H);
     w.Wt = c.take<float>(int64_t(2) * H * H);
     w.part = c.take<float>(colsum_partial_floats(H));
-    w.s.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)));
+    w.ldh = round_up(H, 32);
+    w.ldl = round_up(int64_t(2) * H, 32);
+    w.Hnp = c.take<float>(int64_t(N) * w.ldh);
+    w.HLRp = c.take<float>(int64_t(N) * w.ldl);
+    w.dhp = c.take<float>(int64_t(N) * w.ldh);
+    w.dAp = c.take<float>(int64_t(N) * w.ldh);
     return c.off + 256;
 }
 
@@ -736,6 +753,154 @@ extern "C" janus_status janus_treelstm_device_report(const janus_treelstm_desc* 
     return flag != 0u ? JANUS_ERR_DEVICE : JANUS_OK;
 }
 
+namespace janus {
+namespace {
+
+// Grid and LDS of the persistent TreeRNN kernels: one workgroup per CU at
+// most, the grid a multiple of the column tiles of W (forward: H / 32 output
+// units; backward: 2H / 32 columns of [dh_L; dh_R]).  Off with
+// JANUS_TREE_PERSIST=0, for H above 512 (the embedding gradient's two
+// columns per thread), or where the forward's operand slabs do not fit the
+// LDS (about H > 312); the level-by-level kernels run then.
+struct RnnPlan {
+    bool on = false;
+    int ncol = 0, fwd_grid = 0, ncol2 = 0, bwd_grid = 0;
+    size_t fwd_lds = 0, bwd_lds = 0;
+};
+RnnPlan rnn_plan(const janus_treelstm_desc& d) {
+    RnnPlan p;
+    const char* e = getenv("JANUS_TREE_PERSIST");
+    if (e && e[0] == '0') return p;
+    const TreeDev dev = tree_dev();
+    if (dev.cus <= 0 || dev.lds == 0 || d.H > tpersist::kMaxE) return p;
+    p.ncol = (d.H + 31) / 32;
+    p.ncol2 = (2 * d.H + 31) / 32;
+    if (p.ncol2 > dev.cus) return p;
+    const int cus = dev.cus < kMaxTreeGrid ? dev.cus : kMaxTreeGrid;
+    p.fwd_grid = p.ncol * (cus / p.ncol);
+    p.bwd_grid = p.ncol2 * (cus / p.ncol2);
+    p.fwd_lds = size_t(tpersist::rnn_fwd_lds_floats(d.H)) * sizeof(float);
+    p.bwd_lds = size_t(tpersist::rnn_bwd_lds_floats(d.H)) * sizeof(float);
+    p.on = p.fwd_lds <= dev.lds && p.bwd_lds <= dev.lds;
+    return p;
+}
+// The backward addresses dA through one buffer descriptor (byte offsets
+// below 2^31); larger batches run the level-by-level kernels.
+bool rnn_persist_fits(const RnnPlan& p, const janus_treelstm_desc& d, int32_t N) {
+    return p.on && int64_t(N) * round_up(d.H, 32) * 4 < (int64_t(1) << 31);
+}
+
+// Forward: schedule, level offsets and the zeroed barrier block (error flag
+// included) in one copy, then one launch for every level.
+janus_status treernn_fwd_persistent_call(const janus_treelstm_desc& d, const janus_tree_batch* t,
+                                         const TreeSchedule& s, const TreeRnnWs& w, const RnnPlan& plan,
+                                         const void* emb, const void* W, const void* b, void* h_root,
+                                         hipStream_t st) {
+    TreeHost h;
+    build_host(t, s, h);
+    const size_t nb = sizeof(int32_t) * s.N;
+    const std::vector<char> zero_sync(sizeof(tpersist::TreeSync), 0);
+    const UploadPiece pieces[] = {{w.s.lword, h.lword.data(), nb},
+                                  {w.s.lchild, h.lchild.data(), nb},
+                                  {w.s.rchild, h.rchild.data(), nb},
+                                  {w.s.parent, h.parent.data(), nb},
+                                  {w.s.rootk, h.rootk.data(), nb},
+                                  {w.s.rootpos, h.rootpos.data(), sizeof(int32_t) * t->num_trees},
+                                  {w.s.loff, s.level_offsets.data(), sizeof(int32_t) * s.level_offsets.size()},
+                                  {w.s.tsync, zero_sync.data(), zero_sync.size()}};
+    janus_status e = upload_pieces(pieces, 8, st);
+    if (e != JANUS_OK) return e;
+    tpersist::RnnFwdArgs a;
+    a.H = d.H;
+    a.N = s.N;
+    a.M0 = s.level_offsets[1];
+    a.nlev = s.num_levels;
+    a.ncol = plan.ncol;
+    a.loff = w.s.loff;
+    a.lword = w.s.lword;
+    a.parent = w.s.parent;
+    a.rootk = w.s.rootk;
+    a.emb = static_cast<const float*>(emb);
+    a.W = static_cast<const float*>(W);
+    a.b = static_cast<const float*>(b);
+    a.Hn = w.Hnp;
+    a.ldh = w.ldh;
+    a.HLR = w.HLRp;
+    a.ldl = w.ldl;
+    a.h_root = static_cast<float*>(h_root);
+    a.sync = w.s.tsync;
+    static size_t attr = 0;
+    const double flops = 2.0 * d.H * 2.0 * d.H * double(s.N - a.M0);
+    TraceScope trace("treernn_fwd_persistent", flops, 0.0, st);
+    return tree_persistent_launch(tpersist::treernn_fwd_persistent, plan.fwd_grid, plan.fwd_lds, a, st, attr);
+}
+
+// Backward: the forward's schedule (the workspace is unchanged between the
+// calls); the leaves grouped by word and the barrier's counters (not its
+// error flag) in one copy, then one launch for the levels, dW, db and the
+// embedding gradient.
+janus_status treernn_bwd_persistent_call(const janus_treelstm_desc& d, const janus_tree_batch* t,
+                                         const TreeSchedule& s, const TreeRnnWs& w, const RnnPlan& plan,
+                                         const void* W, const void* dh_root, float* demb, float* dW, float* db,
+                                         hipStream_t st) {
+    TreeHost h;
+    build_host(t, s, h);
+    const int M0 = s.level_offsets[1];
+    std::vector<int32_t> seg;
+    const int nseg = embed_segments(h.lword.data(), M0, d.V, seg);
+    // first group of each workgroup's rows [V w / grid, V (w + 1) / grid)
+    for (int g = 0; g < plan.bwd_grid; ++g) {
+        const int32_t* sid = seg.data() + M0 + nseg + 1;
+        const int64_t v0 = int64_t(d.V) * g / plan.bwd_grid;
+        const int32_t first = int32_t(std::lower_bound(sid, sid + nseg, v0) - sid);
+        seg.push_back(first);
+    }
+    const size_t counters = sizeof(tpersist::TreeSync) - tpersist::kTreeSyncCounters;
+    const std::vector<char> zero_counters(counters, 0);
+    const UploadPiece pieces[] = {
+        {reinterpret_cast<char*>(w.s.tsync) + tpersist::kTreeSyncCounters, zero_counters.data(), counters},
+        {w.s.seg, seg.data(), seg.size() * sizeof(int32_t)}};
+    janus_status e = upload_pieces(pieces, 2, st);
+    if (e != JANUS_OK) return e;
+    tpersist::RnnBwdArgs a;
+    a.H = d.H;
+    a.N = s.N;
+    a.M0 = M0;
+    a.nlev = s.num_levels;
+    a.ncol = plan.ncol2;
+    a.nseg = nseg;
+    a.V = d.V;
+    a.ntrees = t->num_trees;
+    a.loff = w.s.loff;
+    a.lword = w.s.lword;
+    a.lchild = w.s.lchild;
+    a.rchild = w.s.rchild;
+    a.rootk = w.s.rootk;
+    a.rootpos = w.s.rootpos;
+    a.seg = w.s.seg;
+    a.W = static_cast<const float*>(W);
+    a.Hn = w.Hnp;
+    a.ldh = w.ldh;
+    a.HLR = w.HLRp;
+    a.ldl = w.ldl;
+    a.dh_root = static_cast<const float*>(dh_root);
+    a.dh = w.dhp;
+    a.dA = w.dAp;
+    a.lda = w.ldh;
+    a.demb = demb;
+    a.dW = dW;
+    a.db = db;
+    a.sync = w.s.tsync;
+    static size_t attr = 0;
+    // [dh_L; dh_R] = da W and dW, both 2 H 2H per internal node
+    const double flops = 2.0 * 2.0 * d.H * 2.0 * d.H * double(s.N - M0);
+    TraceScope trace("treernn_bwd_persistent", flops, 0.0, st);
+    return tree_persistent_launch(tpersist::treernn_bwd_persistent, plan.bwd_grid, plan.bwd_lds, a, st, attr);
+}
+
+}  // namespace
+}  // namespace janus
+
 extern "C" size_t janus_treernn_workspace_bytes(const janus_treernn_desc* d, int32_t max_nodes, int32_t max_trees) {
     if (check_rnn(d) != JANUS_OK || max_nodes <= 0 || max_trees <= 0) return 0;
     TreeRnnWs w;
@@ -751,6 +916,8 @@ extern "C" janus_status janus_treernn_fwd(const janus_treernn_desc* d, const jan
     janus_status e = prepare_rnn(d, t, ws, ws_bytes, s, w);
     if (e != JANUS_OK) return e;
     hipStream_t st = static_cast<hipStream_t>(stream);
+    const RnnPlan plan = rnn_plan(*d);
+    if (rnn_persist_fits(plan, *d, s.N)) return treernn_fwd_persistent_call(*d, t, s, w, plan, emb, W, b, h_root, st);
     if ((e = upload_tree(t, s, w.s, st)) != JANUS_OK) return e;
     const int H = d->H;
     const int M0 = s.level_offsets[1];
@@ -790,6 +957,9 @@ extern "C" janus_status janus_treernn_bwd(const janus_treernn_desc* d, const jan
     if (e != JANUS_OK) return e;
     const int M0 = s.level_offsets[1];
     hipStream_t st = static_cast<hipStream_t>(stream);
+    const RnnPlan plan = rnn_plan(*d);
+    if (rnn_persist_fits(plan, *d, s.N))
+        return treernn_bwd_persistent_call(*d, t, s, w, plan, W, dh_root, demb, dW, db, st);
     TreeHost host;
     if ((e = upload_tree(t, s, w.s, st, &host)) != JANUS_OK) return e;
     const int H = d->H, N = s.N;
@@ -825,4 +995,19 @@ extern "C" janus_status janus_treernn_bwd(const janus_treernn_desc* d, const jan
     }
     // the leaves' dh is the gradient of their word vectors
     return embed_backward(JANUS_F32, w.dh, host.lword.data(), M0, H, demb, d->V, w.s.seg, st);
+}
+
+extern "C" janus_status janus_treernn_device_report(const janus_treernn_desc* d, const janus_tree_batch* t,
+                                                    const void* ws, size_t ws_bytes, int32_t* timed_out,
+                                                    void* stream) {
+    if (!timed_out) return JANUS_ERR_INVALID_ARG;
+    TreeSchedule s;
+    TreeRnnWs w;
+    janus_status e = prepare_rnn(d, t, const_cast<void*>(ws), ws_bytes, s, w);
+    if (e != JANUS_OK) return e;
+    unsigned flag = 0;
+    JANUS_HIP(hipStreamSynchronize(static_cast<hipStream_t>(stream)));
+    JANUS_HIP(hipMemcpy(&flag, &w.s.tsync->error, sizeof(flag), hipMemcpyDeviceToHost));
+    *timed_out = flag != 0u ? 1 : 0;
+    return flag != 0u ? JANUS_ERR_DEVICE : JANUS_OK;
 }

@@ -144,6 +144,35 @@ __device__ __forceinline__ void stage4(int n, Ld ld, St st) {
 }
 __device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 
+// Copy an nrow x KQ grid of 16-byte pieces into LDS: piece (m, q) is
+// ld(m, q) (0 outside its operand) and goes where st(m, q, v) puts it.
+// Thread t takes pieces t, t + kThreads, ... in row-major order, stepping
+// (m, q) without a division, and issues NB loads before it writes any.
+template <int NB, class Ld, class St>
+__device__ __forceinline__ void stage4_2d(int nrow, int KQ, Ld ld, St st) {
+    const int dm = kThreads / KQ, dq = kThreads - dm * KQ;
+    int m = int(threadIdx.x) / KQ, q = int(threadIdx.x) - m * KQ;
+    while (m < nrow) {
+        float4 v[NB];
+        int mm[NB], qq[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            mm[i] = m;
+            qq[i] = q;
+            v[i] = m < nrow ? ld(m, q) : make_float4(0.f, 0.f, 0.f, 0.f);
+            q += dq;
+            m += dm;
+            if (q >= KQ) {
+                q -= KQ;
+                ++m;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+            if (mm[i] < nrow) st(mm[i], qq[i], v[i]);
+    }
+}
+
 
 // ---------------------------------------------------------------- forward
 struct FwdArgs {
@@ -738,16 +767,17 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
                 __syncthreads();   // the previous batch of leaves is read
                 if (tid < nk) lorder[tid] = order[kb + tid];
                 __syncthreads();
-                for (int k = 0; k < nk; k += 8) {
-                    float x0[8], x1[8];
+                constexpr int LB = 32;   // leaves per round trip
+                for (int k = 0; k < nk; k += LB) {
+                    float x0[LB], x1[LB];
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) {
+                    for (int q = 0; q < LB; ++q) {
                         const int64_t r = k + q < nk ? int64_t(lorder[k + q]) * a.ldx : -1;
                         x0[q] = (r >= 0 && tid < E) ? a.dxl[r + tid] : 0.f;
                         x1[q] = (r >= 0 && tid + kThreads < E) ? a.dxl[r + tid + kThreads] : 0.f;
                     }
 #pragma unroll
-                    for (int q = 0; q < 8; ++q) {
+                    for (int q = 0; q < LB; ++q) {
                         s[0] += x0[q];
                         s[1] += x1[q];
                     }

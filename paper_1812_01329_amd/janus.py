@@ -33,7 +33,7 @@ EXPORTS = [
     "janus_trace_end", "janus_status_string", "janus_version", "janus_last_error",
     "janus_sgd_workspace_bytes", "janus_sgd_clip_update", "janus_sgd_clip_update_noalloc",
     "janus_lstm_state_carry",
-    "janus_treernn_workspace_bytes", "janus_treernn_fwd", "janus_treernn_bwd",
+    "janus_treernn_workspace_bytes", "janus_treernn_fwd", "janus_treernn_bwd", "janus_treernn_device_report",
     "janus_childsum_workspace_bytes", "janus_childsum_fwd", "janus_childsum_bwd",
 ]
 
@@ -129,6 +129,8 @@ def lib():
         L.janus_treernn_workspace_bytes.argtypes = [C.POINTER(TreeDesc), i32, i32]
         L.janus_treernn_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, vp, vp, vp, sz, vp]
         L.janus_treernn_bwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, vp, sz, vp, vp, vp, vp, vp]
+        L.janus_treernn_device_report.argtypes = [C.POINTER(TreeDesc), C.POINTER(TreeBatchC), vp, sz,
+                                                  C.POINTER(i32), vp]
         L.janus_childsum_workspace_bytes.restype = sz
         L.janus_childsum_workspace_bytes.argtypes = [C.POINTER(TreeDesc), i32]
         L.janus_childsum_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(NaryBatchC), vp, vp, vp, vp, vp, vp, sz, vp]
@@ -308,6 +310,18 @@ def janus_treelstm_device_report(desc: TreeDesc, trees, ws, stream=None) -> int:
     st = lib().janus_treelstm_device_report(C.byref(desc), C.byref(tb), _p(ws), ws.numel() * ws.element_size(),
                                             C.byref(out), _stream(stream))
     _check(st, "janus_treelstm_device_report")
+    return int(out.value)
+
+
+def janus_treernn_device_report(desc: TreeDesc, trees, ws, stream=None) -> int:
+    """Synchronises the stream and returns 1 if a level barrier of the last
+    TreeRNN forward or backward on this workspace ran out of its wait (the
+    call then raises JanusError(DEVICE)), else 0."""
+    tb, keep = _tree_c(trees.left, trees.right, trees.word, trees.root)
+    out = C.c_int32(0)
+    st = lib().janus_treernn_device_report(C.byref(desc), C.byref(tb), _p(ws), ws.numel() * ws.element_size(),
+                                           C.byref(out), _stream(stream))
+    _check(st, "janus_treernn_device_report")
     return int(out.value)
 
 
