@@ -516,7 +516,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
     // U[q H + j][32 col + c] -> Us[c][q Hp + j]: 32 consecutive columns of a
     // row of U are one 128-byte piece
     if (H2 % 4 == 0) {
-        stage4<8>(8 * 5 * Hp,
+        stage4<16>(8 * 5 * Hp,
                   [&](int idx) {
                       const int row = idx / 8, c4 = 4 * (idx % 8), q = row / Hp, j = row - q * Hp, n = 32 * col + c4;
                       return (j < H && n < H2) ? ld4(a.U + (int64_t(q) * H + j) * H2 + n) : make_float4(0.f, 0.f, 0.f, 0.f);
