@@ -408,6 +408,21 @@ janus_status janus_childsum_bwd(const janus_childsum_desc* d, const janus_nary_t
                                 void* ws, size_t ws_bytes, const void* dh_root,
                                 float* demb, float* dW, float* dU, float* db, void* stream);
 
+/*
+ * Device-side status of the Child-Sum calls made with this workspace since
+ * the last forward (same d and t), as janus_treelstm_device_report: where
+ * the weight slices fit one CU's LDS (H up to about 156, E up to 512) each
+ * direction is one launch of co-resident workgroups with device-wide
+ * barriers between levels (Section 4.2.1 recursion, run level by level); a
+ * barrier that ran out of its bounded wait sets *timed_out = 1 and the call
+ * returns JANUS_ERR_DEVICE (the results are then undefined).  The flag is
+ * cleared by the next forward.  Errors: as janus_childsum_fwd's validation,
+ * or INVALID_ARG for a NULL timed_out.
+ */
+janus_status janus_childsum_device_report(const janus_childsum_desc* d, const janus_nary_tree_batch* t,
+                                          const void* ws, size_t ws_bytes, int32_t* timed_out,
+                                          void* stream);
+
 /* ------------------------------------------------------------------------ */
 /* Embedding and softmax cross-entropy                                      */
 /* ------------------------------------------------------------------------ */

@@ -27,6 +27,7 @@
 #include <algorithm>
 #include <vector>
 
+#include "childsum_persist.hpp"
 #include "device.hpp"
 #include "ops.hpp"
 #include "simt.hpp"
@@ -54,6 +55,23 @@ struct CsWs {
     float* Ut = nullptr;         // [H x 4H]
     float* part = nullptr;
     int32_t* seg = nullptr;      // the nodes grouped by word, for the embedding gradient
+    // persistent path: level offsets and the barrier's counters (carved right
+    // after the schedule arrays and before `seg`, so that each direction's
+    // upload is one copy), and node rows padded to whole 128-byte lines
+    int32_t* loff = nullptr;     // [N + 1]
+    tpersist::TreeSync* tsync = nullptr;
+    float* XWp = nullptr;        // [N x ld4]
+    float* Gp = nullptr;         // [N x ld4] h U^T (forward)
+    float* dGp = nullptr;        // [N x ld4]
+    float* dXWp = nullptr;       // [N x ld4]
+    float* Gtp = nullptr;        // [N x ld3]
+    float* Fp = nullptr;         // [N x ldh]
+    float* Cp = nullptr;         // [N x ldh]
+    float* Hnp = nullptr;        // [N x ldh]
+    float* dcp = nullptr;        // [N x ldh]
+    float* dhp = nullptr;        // [N x ldh]
+    float* dxp = nullptr;        // [N x ldx]
+    int64_t ld4 = 0, ld3 = 0, ldh = 0, ldx = 0;
 };
 
 size_t carve_cs(const janus_treelstm_desc& d, int32_t N, void* base, CsWs& w) {
@@ -63,6 +81,11 @@ size_t carve_cs(const janus_treelstm_desc& d, int32_t N, void* base, CsWs& w) {
     w.pcoff = c.take<int32_t>(int64_t(N) + 1);
     w.pkids = c.take<int32_t>(N);
     w.rootk = c.take<int32_t>(N);
+    w.loff = c.take<int32_t>(int64_t(N) + 1);
+    w.tsync = c.take<tpersist::TreeSync>(1);
+    // the nodes grouped by word, and (persistent backward) each workgroup's
+    // first group of the embedding rows
+    w.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)) + tpersist::kMaxTreeGrid);
     w.XW = c.take<float>(int64_t(N) * 4 * H);
     w.G = c.take<float>(int64_t(N) * 4 * H);
     w.Gt = c.take<float>(int64_t(N) * 3 * H);
@@ -76,7 +99,21 @@ size_t carve_cs(const janus_treelstm_desc& d, int32_t N, void* base, CsWs& w) {
     w.Wt = c.take<float>(int64_t(E) * 4 * H);
     w.Ut = c.take<float>(int64_t(H) * 4 * H);
     w.part = c.take<float>(colsum_partial_floats(4 * H));
-    w.seg = c.take<int32_t>(int64_t(embed_seg_ints(N)));
+    w.ld4 = round_up(int64_t(4) * H, 32);
+    w.ld3 = round_up(int64_t(3) * H, 32);
+    w.ldh = round_up(H, 32);
+    w.ldx = round_up(E, 32);
+    w.XWp = c.take<float>(int64_t(N) * w.ld4);
+    w.Gp = c.take<float>(int64_t(N) * w.ld4);
+    w.dGp = c.take<float>(int64_t(N) * w.ld4);
+    w.dXWp = c.take<float>(int64_t(N) * w.ld4);
+    w.Gtp = c.take<float>(int64_t(N) * w.ld3);
+    w.Fp = c.take<float>(int64_t(N) * w.ldh);
+    w.Cp = c.take<float>(int64_t(N) * w.ldh);
+    w.Hnp = c.take<float>(int64_t(N) * w.ldh);
+    w.dcp = c.take<float>(int64_t(N) * w.ldh);
+    w.dhp = c.take<float>(int64_t(N) * w.ldh);
+    w.dxp = c.take<float>(int64_t(N) * w.ldx);
     return c.off + 256;
 }
 
@@ -153,21 +190,173 @@ janus_status check_cs(const janus_treelstm_desc* d) {
     return JANUS_OK;
 }
 
+// Validates the call and carves the workspace; `upload` also copies the
+// schedule arrays (carved one after another: one copy) for the level-by-level
+// kernels.
 janus_status prepare_cs(const janus_treelstm_desc* d, const janus_nary_tree_batch* t, void* ws, size_t ws_bytes,
-                        NarySchedule& s, CsWs& w, hipStream_t st) {
+                        NarySchedule& s, CsWs& w, hipStream_t st, bool upload = true) {
     janus_status e = check_cs(d);
     if (e != JANUS_OK) return e;
     if ((e = build_nary_schedule(t, d->V, s)) != JANUS_OK) return e;
     if (!ws || ws_bytes < carve_cs(*d, s.N, nullptr, w) || reinterpret_cast<uintptr_t>(ws) % 256 != 0)
         return JANUS_ERR_WORKSPACE;
     carve_cs(*d, s.N, ws, w);
+    if (!upload) return JANUS_OK;
     const size_t nb = sizeof(int32_t) * s.N;
-    // carved one after another (nothing else between them): one copy
+    // the barrier block is zeroed too, so the device report of a call on
+    // this path reads no stale flag
+    const std::vector<char> zero_sync(sizeof(tpersist::TreeSync), 0);
     const UploadPiece pieces[] = {{w.pword, s.pword.data(), nb},
                                   {w.pcoff, s.pcoff.data(), nb + sizeof(int32_t)},
                                   {w.pkids, s.pkids.data(), sizeof(int32_t) * s.pkids.size()},
-                                  {w.rootk, s.rootk.data(), nb}};
-    return upload_pieces(pieces, 4, st);
+                                  {w.rootk, s.rootk.data(), nb},
+                                  {w.tsync, zero_sync.data(), zero_sync.size()}};
+    return upload_pieces(pieces, 5, st);
+}
+
+// ------------------------------------------------------- persistent path
+// Grid and LDS of the persistent Child-Sum kernels: one workgroup per CU at
+// most, the grid a multiple of the column tiles (forward: 4H / 32 gate
+// columns; backward: H / 32 columns of dh).  Off with JANUS_TREE_PERSIST=0,
+// for inputs wider than 512 (the embedding gradient's two columns per
+// thread), or where the backward's U columns and dG tile (two 32 x 4H slabs)
+// do not fit the LDS (about H > 156); the level-by-level kernels run then.
+struct CsPlan {
+    bool on = false;
+    int ncolf = 0, fwd_grid = 0, ncolb = 0, bwd_grid = 0;
+    size_t fwd_lds = 0, bwd_lds = 0;
+};
+CsPlan cs_plan(const janus_treelstm_desc& d) {
+    CsPlan p;
+    const char* e = getenv("JANUS_TREE_PERSIST");
+    if (e && e[0] == '0') return p;
+    const tpersist::TreeDev dev = tpersist::tree_dev();
+    if (dev.cus <= 0 || dev.lds == 0 || d.E > tpersist::kMaxE) return p;
+    p.ncolf = (4 * d.H + 31) / 32;
+    p.ncolb = (d.H + 31) / 32;
+    if (p.ncolf > dev.cus) return p;
+    const int cus = dev.cus < tpersist::kMaxTreeGrid ? dev.cus : tpersist::kMaxTreeGrid;
+    p.fwd_grid = p.ncolf * (cus / p.ncolf);
+    p.bwd_grid = p.ncolb * (cus / p.ncolb);
+    p.fwd_lds = size_t(tpersist::cs_fwd_lds_floats(d.E, d.H)) * sizeof(float);
+    p.bwd_lds = size_t(tpersist::cs_bwd_lds_floats(d.H)) * sizeof(float);
+    p.on = p.fwd_lds <= dev.lds && p.bwd_lds <= dev.lds;
+    return p;
+}
+
+// Forward: schedule, level offsets and the zeroed barrier block (error flag
+// included) in one copy, then one launch for every level.
+janus_status cs_fwd_persistent_call(const janus_treelstm_desc& d, const NarySchedule& s, const CsWs& w,
+                                    const CsPlan& plan, const void* emb, const void* W, const void* U, const void* b,
+                                    void* h_root, hipStream_t st) {
+    const size_t nb = sizeof(int32_t) * s.N;
+    const std::vector<char> zero_sync(sizeof(tpersist::TreeSync), 0);
+    const UploadPiece pieces[] = {{w.pword, s.pword.data(), nb},
+                                  {w.pcoff, s.pcoff.data(), nb + sizeof(int32_t)},
+                                  {w.pkids, s.pkids.data(), sizeof(int32_t) * s.pkids.size()},
+                                  {w.rootk, s.rootk.data(), nb},
+                                  {w.loff, s.level_offsets.data(), sizeof(int32_t) * s.level_offsets.size()},
+                                  {w.tsync, zero_sync.data(), zero_sync.size()}};
+    janus_status e = upload_pieces(pieces, 6, st);
+    if (e != JANUS_OK) return e;
+    tpersist::CsFwdArgs a;
+    a.E = d.E;
+    a.H = d.H;
+    a.N = s.N;
+    a.nlev = int(s.level_offsets.size()) - 1;
+    a.ncol = plan.ncolf;
+    a.loff = w.loff;
+    a.pword = w.pword;
+    a.pcoff = w.pcoff;
+    a.pkids = w.pkids;
+    a.rootk = w.rootk;
+    a.emb = static_cast<const float*>(emb);
+    a.W = static_cast<const float*>(W);
+    a.U = static_cast<const float*>(U);
+    a.b = static_cast<const float*>(b);
+    a.XW = w.XWp;
+    a.G = w.Gp;
+    a.ld4 = w.ld4;
+    a.Gt = w.Gtp;
+    a.ld3 = w.ld3;
+    a.F = w.Fp;
+    a.C = w.Cp;
+    a.Hn = w.Hnp;
+    a.ldh = w.ldh;
+    a.h_root = static_cast<float*>(h_root);
+    a.sync = w.tsync;
+    static size_t attr = 0;
+    const double flops = 2.0 * s.N * 4.0 * d.H * (double(d.E) + double(d.H));
+    TraceScope trace("childsum_fwd_persistent", flops, 0.0, st);
+    return tpersist::tree_persistent_launch(tpersist::childsum_fwd_persistent, plan.fwd_grid, plan.fwd_lds, a, st,
+                                            attr);
+}
+
+// Backward: the forward's schedule (the workspace is unchanged between the
+// calls); the nodes grouped by word and the barrier's counters (not its
+// error flag) in one copy, then one launch.
+janus_status cs_bwd_persistent_call(const janus_treelstm_desc& d, const NarySchedule& s, const CsWs& w,
+                                    const CsPlan& plan, const void* emb, const void* W, const void* U,
+                                    const void* dh_root, float* demb, float* dW, float* dU, float* db,
+                                    hipStream_t st) {
+    std::vector<int32_t> seg;
+    const int nseg = embed_segments(s.pword.data(), s.N, d.V, seg);
+    // first group of each workgroup's rows [V w / grid, V (w + 1) / grid)
+    for (int g = 0; g < plan.bwd_grid; ++g) {
+        const int32_t* sid = seg.data() + s.N + nseg + 1;
+        const int64_t v0 = int64_t(d.V) * g / plan.bwd_grid;
+        const int32_t first = int32_t(std::lower_bound(sid, sid + nseg, v0) - sid);
+        seg.push_back(first);
+    }
+    const size_t counters = sizeof(tpersist::TreeSync) - tpersist::kTreeSyncCounters;
+    const std::vector<char> zero_counters(counters, 0);
+    const UploadPiece pieces[] = {
+        {reinterpret_cast<char*>(w.tsync) + tpersist::kTreeSyncCounters, zero_counters.data(), counters},
+        {w.seg, seg.data(), seg.size() * sizeof(int32_t)}};
+    janus_status e = upload_pieces(pieces, 2, st);
+    if (e != JANUS_OK) return e;
+    tpersist::CsBwdArgs a;
+    a.E = d.E;
+    a.H = d.H;
+    a.N = s.N;
+    a.nlev = int(s.level_offsets.size()) - 1;
+    a.ncol = plan.ncolb;
+    a.nseg = nseg;
+    a.V = d.V;
+    a.loff = w.loff;
+    a.pword = w.pword;
+    a.pcoff = w.pcoff;
+    a.pkids = w.pkids;
+    a.rootk = w.rootk;
+    a.seg = w.seg;
+    a.emb = static_cast<const float*>(emb);
+    a.W = static_cast<const float*>(W);
+    a.U = static_cast<const float*>(U);
+    a.Gt = w.Gtp;
+    a.ld3 = w.ld3;
+    a.F = w.Fp;
+    a.C = w.Cp;
+    a.Hn = w.Hnp;
+    a.ldh = w.ldh;
+    a.dh_root = static_cast<const float*>(dh_root);
+    a.dG = w.dGp;
+    a.dXW = w.dXWp;
+    a.ld4 = w.ld4;
+    a.dc = w.dcp;
+    a.dh = w.dhp;
+    a.dx = w.dxp;
+    a.ldx = w.ldx;
+    a.demb = demb;
+    a.dW = dW;
+    a.dU = dU;
+    a.db = db;
+    a.sync = w.tsync;
+    static size_t attr = 0;
+    // dh = dG U, dW, dU and dx over every node
+    const double flops = 2.0 * s.N * 4.0 * d.H * (2.0 * d.H + 2.0 * d.E);
+    TraceScope trace("childsum_bwd_persistent", flops, 0.0, st);
+    return tpersist::tree_persistent_launch(tpersist::childsum_bwd_persistent, plan.bwd_grid, plan.bwd_lds, a, st,
+                                            attr);
 }
 
 }  // namespace
@@ -189,8 +378,10 @@ extern "C" janus_status janus_childsum_fwd(const janus_childsum_desc* d, const j
     hipStream_t st = static_cast<hipStream_t>(stream);
     NarySchedule s;
     CsWs w;
-    janus_status e = prepare_cs(d, t, ws, ws_bytes, s, w, st);
+    const CsPlan plan = cs_plan(*d);
+    janus_status e = prepare_cs(d, t, ws, ws_bytes, s, w, st, !plan.on);
     if (e != JANUS_OK) return e;
+    if (plan.on) return cs_fwd_persistent_call(*d, s, w, plan, emb, W, U, b, h_root, st);
     const int H = d->H, E = d->E, N = s.N;
     const int L = int(s.level_offsets.size()) - 1;
     if ((e = transpose_f32(static_cast<const float*>(W), 4 * H, E, w.Wt, st)) != JANUS_OK) return e;
@@ -226,8 +417,10 @@ extern "C" janus_status janus_childsum_bwd(const janus_childsum_desc* d, const j
     hipStream_t st = static_cast<hipStream_t>(stream);
     NarySchedule s;
     CsWs w;
-    janus_status e = prepare_cs(d, t, ws, ws_bytes, s, w, st);
+    const CsPlan plan = cs_plan(*d);
+    janus_status e = prepare_cs(d, t, ws, ws_bytes, s, w, st, !plan.on);
     if (e != JANUS_OK) return e;
+    if (plan.on) return cs_bwd_persistent_call(*d, s, w, plan, emb, W, U, dh_root, demb, dW, dU, db, st);
     const int H = d->H, E = d->E, N = s.N;
     const int L = int(s.level_offsets.size()) - 1;
     // roots have no parent: their dG rows and dc stay 0
@@ -260,4 +453,20 @@ extern "C" janus_status janus_childsum_bwd(const janus_childsum_desc* d, const j
                                      static_cast<const float*>(W), E, nullptr, nullptr, w.dx, E, st);
     if (e != JANUS_OK) return e;
     return embed_backward(JANUS_F32, w.dx, s.pword.data(), N, E, demb, d->V, w.seg, st);
+}
+
+extern "C" janus_status janus_childsum_device_report(const janus_childsum_desc* d, const janus_nary_tree_batch* t,
+                                                     const void* ws, size_t ws_bytes, int32_t* timed_out,
+                                                     void* stream) {
+    if (!timed_out) return JANUS_ERR_INVALID_ARG;
+    hipStream_t st = static_cast<hipStream_t>(stream);
+    NarySchedule s;
+    CsWs w;
+    janus_status e = prepare_cs(d, t, const_cast<void*>(ws), ws_bytes, s, w, st, false);
+    if (e != JANUS_OK) return e;
+    unsigned flag = 0;
+    JANUS_HIP(hipStreamSynchronize(st));
+    JANUS_HIP(hipMemcpy(&flag, &w.tsync->error, sizeof(flag), hipMemcpyDeviceToHost));
+    *timed_out = flag != 0u ? 1 : 0;
+    return flag != 0u ? JANUS_ERR_DEVICE : JANUS_OK;
 }

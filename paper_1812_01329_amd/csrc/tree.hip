@@ -36,7 +36,10 @@ namespace janus {
 
 namespace {
 
-constexpr int kMaxTreeGrid = 4096;   // workgroups of a persistent tree launch (seg's tail is sized for it)
+using tpersist::kMaxTreeGrid;
+using tpersist::TreeDev;
+using tpersist::tree_dev;
+using tpersist::tree_persistent_launch;
 
 struct TreeWs {
     // level-ordered device schedule
@@ -298,12 +301,16 @@ janus_status upload_tree(const janus_tree_batch* t, const TreeSchedule& s, const
     TreeHost& h = keep ? *keep : local;
     build_host(t, s, h);
     const size_t nb = sizeof(int32_t) * s.N;
-    // carved one after another (nothing else between them): one copy
+    // carved one after another (only the level offsets between them): one
+    // copy.  The barrier block is zeroed too, so the device report of a call
+    // on this path reads no stale flag.
+    const std::vector<char> zero_sync(sizeof(tpersist::TreeSync), 0);
     const UploadPiece pieces[] = {{w.lword, h.lword.data(), nb},   {w.lchild, h.lchild.data(), nb},
                                   {w.rchild, h.rchild.data(), nb}, {w.parent, h.parent.data(), nb},
                                   {w.rootk, h.rootk.data(), nb},
-                                  {w.rootpos, h.rootpos.data(), sizeof(int32_t) * t->num_trees}};
-    return upload_pieces(pieces, 6, st);
+                                  {w.rootpos, h.rootpos.data(), sizeof(int32_t) * t->num_trees},
+                                  {w.tsync, zero_sync.data(), zero_sync.size()}};
+    return upload_pieces(pieces, 7, st);
 }
 
 janus_status prepare(const janus_treelstm_desc* d, const janus_tree_batch* t, void* ws, size_t ws_bytes,
@@ -319,29 +326,6 @@ janus_status prepare(const janus_treelstm_desc* d, const janus_tree_batch* t, vo
 
 
 // ------------------------------------------------------- persistent path
-struct TreeDev {
-    int cus = 0;
-    size_t lds = 0;
-};
-// Properties of the current device, queried once per device under a lock.
-TreeDev tree_dev() {
-    static std::mutex m;
-    static TreeDev cache[64];
-    static bool have[64] = {};
-    int dev = 0;
-    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return TreeDev{};
-    std::lock_guard<std::mutex> lock(m);
-    if (!have[dev]) {
-        TreeDev t;
-        int v = 0;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) t.cus = v;
-        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess) t.lds = size_t(v);
-        (void)hipGetLastError();
-        cache[dev] = t;
-        have[dev] = true;
-    }
-    return cache[dev];
-}
 
 // Grid and LDS of the persistent TreeLSTM kernels: one workgroup per CU at
 // most, the grid a multiple of the unit groups (forward) and of the column
@@ -373,29 +357,6 @@ TreePlan tree_plan(const janus_treelstm_desc& d) {
     return p;
 }
 
-// An ordinary launch of a grid whose workgroups must all be resident (the
-// plan allows one per CU and no more than the CUs; the occupancy query
-// confirms one fits a CU).  The barrier's waits are bounded.
-template <class K, class A>
-janus_status tree_persistent_launch(K kernel, int blocks, size_t smem, const A& args, hipStream_t st,
-                                    size_t& attr_smem) {
-    static std::mutex m;
-    {
-        std::lock_guard<std::mutex> lock(m);
-        if (smem > attr_smem) {
-            JANUS_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
-                                          hipFuncAttributeMaxDynamicSharedMemorySize, int(smem)));
-            attr_smem = smem;
-        }
-    }
-    int per_cu = 0;
-    JANUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kernel),
-                                                           tpersist::kThreads, smem));
-    if (per_cu < 1 || int64_t(per_cu) * tree_dev().cus < blocks) return JANUS_ERR_UNSUPPORTED;
-    hipLaunchKernelGGL(kernel, dim3(blocks), dim3(tpersist::kThreads), smem, st, args);
-    JANUS_LAUNCH_CHECK();
-    return JANUS_OK;
-}
 
 // Forward on the persistent path: the schedule, the level offsets and the
 // barrier's counters (with its error flag) go over in one copy, then one

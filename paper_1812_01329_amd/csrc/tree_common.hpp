@@ -1,0 +1,314 @@
+// Shared pieces of the persistent tree level programs (binary TreeLSTM,
+// TreeRNN, Child-Sum TreeLSTM): the workgroup shape, the counter block of the
+// device-wide barrier, staging helpers that keep many loads in flight, the
+// 32 x 32 fp32 MFMA contraction over nodes, and the host-side launch of a
+// grid whose workgroups must all be resident.
+#pragma once
+
+#include <mutex>
+
+#include "device.hpp"
+#include "lstm_persist.hpp"
+#include "runtime.hpp"
+
+namespace janus {
+namespace tpersist {
+
+constexpr int kThreads = 256;          // 4 waves
+constexpr int kWaves = kThreads / 64;
+constexpr int kUG = 6;                 // units per forward group: 5 x 6 = 30 of 32 tile columns
+constexpr int kUC = 32;                // units per chunk of the backward's cell recompute
+constexpr int kKC = 128;               // k per staged chunk of the contractions over nodes
+constexpr int kRed = 33;               // row pitch of the per-wave partial tiles
+constexpr int kMaxE = 2 * kThreads;    // input width the embedding-gradient phase handles
+
+__host__ __device__ constexpr int pad16(int x) { return (x + 15) & ~15; }
+__host__ __device__ constexpr int padto(int x, int m) { return (x + m - 1) / m * m; }
+
+// Counter block of the grid barrier.  `error` comes first: the backward's
+// upload zeroes the counters that follow it and leaves a flag the forward
+// set.
+struct TreeSync {
+    unsigned error;
+    unsigned pad_e[63];
+    unsigned count;
+    unsigned pad0[63];
+    unsigned xcd[16][64];
+    unsigned census[16][64];
+};
+constexpr size_t kTreeSyncCounters = offsetof(TreeSync, count);   // byte offset of the counters
+
+using TreeBarrier = persist::BarrierT<TreeSync>;
+
+// A store other workgroups read later in the launch: device-scope, so it is
+// written through the L2 of this XCD to memory (the L2s of the XCDs are not
+// coherent with each other), and counted like any store by the wait at the
+// barrier's arrival.
+__device__ __forceinline__ void store_through(float* base, int64_t idx, float v) {
+    __hip_atomic_store(base + idx, v, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+}
+
+__device__ __forceinline__ void zero_acc(f32x16_t& acc) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) acc[v] = 0.f;
+}
+
+// Sum the four waves' 32 x 32 tiles: every wave writes its accumulator to
+// red[wave][row][col]; after the barrier red holds the parts, summed by the
+// reader in wave order.
+__device__ __forceinline__ void spill_acc(const f32x16_t& acc, float* red, int wave, int lane) {
+#pragma unroll
+    for (int v = 0; v < 16; ++v) red[(wave * 32 + acc_row(v, lane)) * kRed + acc_col(lane)] = acc[v];
+}
+__device__ __forceinline__ float red_sum(const float* red, int m, int c) {
+    float s = 0.f;
+#pragma unroll
+    for (int w = 0; w < kWaves; ++w) s += red[(w * 32 + m) * kRed + c];
+    return s;
+}
+
+// Copy n elements into LDS: element i is ld(i) (which returns 0 outside its
+// operand) and goes where st(i, v) puts it.  Each thread issues NB loads
+// before it writes any, so it pays one memory round trip per NB elements
+// rather than one per element.
+template <int NB, class Ld, class St>
+__device__ __forceinline__ void stage(int n, Ld ld, St st) {
+    for (int base = int(threadIdx.x); base < n; base += kThreads * NB) {
+        float v[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int idx = base + i * kThreads;
+            v[i] = idx < n ? ld(idx) : 0.f;
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int idx = base + i * kThreads;
+            if (idx < n) st(idx, v[i]);
+        }
+    }
+}
+// The same with 16-byte pieces (ld4 returns a float4).
+template <int NB, class Ld, class St>
+__device__ __forceinline__ void stage4(int n, Ld ld, St st) {
+    for (int base = int(threadIdx.x); base < n; base += kThreads * NB) {
+        float4 v[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int idx = base + i * kThreads;
+            v[i] = idx < n ? ld(idx) : make_float4(0.f, 0.f, 0.f, 0.f);
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            const int idx = base + i * kThreads;
+            if (idx < n) st(idx, v[i]);
+        }
+    }
+}
+__device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+
+// Copy an nrow x KQ grid of 16-byte pieces into LDS: piece (m, q) is
+// ld(m, q) (0 outside its operand) and goes where st(m, q, v) puts it.
+// Thread t takes pieces t, t + kThreads, ... in row-major order, stepping
+// (m, q) without a division, and issues NB loads before it writes any.
+template <int NB, class Ld, class St>
+__device__ __forceinline__ void stage4_2d(int nrow, int KQ, Ld ld, St st) {
+    const int dm = kThreads / KQ, dq = kThreads - dm * KQ;
+    int m = int(threadIdx.x) / KQ, q = int(threadIdx.x) - m * KQ;
+    while (m < nrow) {
+        float4 v[NB];
+        int mm[NB], qq[NB];
+#pragma unroll
+        for (int i = 0; i < NB; ++i) {
+            mm[i] = m;
+            qq[i] = q;
+            v[i] = m < nrow ? ld(m, q) : make_float4(0.f, 0.f, 0.f, 0.f);
+            q += dq;
+            m += dm;
+            if (q >= KQ) {
+                q -= KQ;
+                ++m;
+            }
+        }
+#pragma unroll
+        for (int i = 0; i < NB; ++i)
+            if (mm[i] < nrow) st(mm[i], qq[i], v[i]);
+    }
+}
+
+
+// acc += sum over k in [0, K) of Aop(row, k) Bop(col, k) for a 32 x 32 tile,
+// staged kKC k at a time through LDS (A and B chunks [32][kKC + 4]); the
+// waves take its k-steps of 16 in turn, and the next chunk is loaded into
+// registers while the current one is contracted.  fa(r, k) / fb(c, k)
+// return the operand value (0 outside).  AK: A is contiguous in k in memory
+// (consecutive threads then take consecutive k), else in r (consecutive
+// threads take consecutive rows of one k); B is always contiguous in c.
+template <bool AK, class FA, class FB>
+__device__ __forceinline__ void node_contraction(f32x16_t& acc, float* Ac, float* Bc, int K, FA fa, FB fb) {
+    constexpr int sK = kKC + 4, PER = 32 * kKC / kThreads;   // 8 elements of each operand per thread
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float va[PER], vb[PER];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * kThreads;
+            const int kk = idx / 32, r = idx % 32;
+            vb[i] = k0 + kk < K ? fb(r, k0 + kk) : 0.f;
+            if constexpr (AK) {
+                const int ra = idx / kKC, ka = idx % kKC;
+                va[i] = k0 + ka < K ? fa(ra, k0 + ka) : 0.f;
+            } else {
+                va[i] = k0 + kk < K ? fa(r, k0 + kk) : 0.f;
+            }
+        }
+    };
+    if (K > 0) fetch(0);
+    for (int k0 = 0; k0 < K; k0 += kKC) {
+        __syncthreads();   // the previous chunk's reads are done
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * kThreads;
+            const int kk = idx / 32, r = idx % 32;
+            Bc[r * sK + kk] = vb[i];
+            if constexpr (AK) Ac[(idx / kKC) * sK + idx % kKC] = va[i];
+            else Ac[r * sK + kk] = va[i];
+        }
+        if (k0 + kKC < K) fetch(k0 + kKC);
+        __syncthreads();
+        for (int ks = wave; ks < kKC / 16; ks += kWaves) {
+            Frag<float> xa, xb;
+            xa.load(Ac + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
+            xb.load(Bc + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
+            mfma(acc, xa, xb);
+        }
+    }
+}
+
+
+// Stage 32 weight rows 32 col + c (c < 32) of a [rows x K] matrix into LDS
+// rows of pitch ld, zero past K and past the last row.
+__device__ __forceinline__ void stage_weight_rows(float* dst, int ld, const float* src, int nrows, int K, int col) {
+    const int KP = pad16(K);
+    if (K % 4 == 0) {
+        stage4_2d<10>(32, KP / 4,
+                      [&](int c, int q) {
+                          const int n = 32 * col + c, k = 4 * q;
+                          return (n < nrows && k < K) ? ld4(src + int64_t(n) * K + k) : make_float4(0.f, 0.f, 0.f, 0.f);
+                      },
+                      [&](int c, int q, float4 v) { *reinterpret_cast<float4*>(dst + c * ld + 4 * q) = v; });
+    } else {
+        stage<16>(32 * KP,
+                  [&](int idx) {
+                      const int c = idx / KP, k = idx - c * KP, n = 32 * col + c;
+                      return (n < nrows && k < K) ? src[int64_t(n) * K + k] : 0.f;
+                  },
+                  [&](int idx, float v) { dst[(idx / KP) * ld + idx % KP] = v; });
+    }
+}
+
+// Stage the rows rowsrc[m] (element offsets into src, -1 = zero row) of K
+// columns into At (pitch ld), zero up to pad16(K).  K % 4 == 0 (16-byte
+// aligned rows): thread t owns the 16-byte column q = t mod KQ of the rows
+// t / KQ, t / KQ + RP, ... (RP = kThreads / KQ rows per pass), reads those
+// rows' offsets, then issues all its loads before it writes any.
+__device__ __forceinline__ void stage_tile_rows(float* At, int ld, const float* src, const int64_t* rowsrc, int K) {
+    const int KP = pad16(K);
+    if (K % 4 == 0 && KP / 4 <= kThreads) {
+        constexpr int NB = 16;
+        const int KQ = KP / 4, RP = kThreads / KQ;
+        const int q = int(threadIdx.x) % KQ, m0 = int(threadIdx.x) / KQ;
+        if (m0 >= RP) return;
+        const bool colok = 4 * q < K;
+        for (int mb = m0; mb < 32; mb += RP * NB) {
+            int64_t r[NB];
+#pragma unroll
+            for (int i = 0; i < NB; ++i) {
+                const int m = mb + i * RP;
+                r[i] = (m < 32 && colok) ? rowsrc[m] : -1;
+            }
+            float4 v[NB];
+#pragma unroll
+            for (int i = 0; i < NB; ++i) v[i] = r[i] >= 0 ? ld4(src + r[i] + 4 * q) : make_float4(0.f, 0.f, 0.f, 0.f);
+#pragma unroll
+            for (int i = 0; i < NB; ++i) {
+                const int m = mb + i * RP;
+                if (m < 32) *reinterpret_cast<float4*>(At + m * ld + 4 * q) = v[i];
+            }
+        }
+    } else {
+        stage<16>(32 * KP,
+                  [&](int idx) {
+                      const int m = idx / KP, k = idx - m * KP;
+                      const int64_t r = rowsrc[m];
+                      return (r >= 0 && k < K) ? src[r + k] : 0.f;
+                  },
+                  [&](int idx, float v) { At[(idx / KP) * ld + idx % KP] = v; });
+    }
+}
+
+// acc = the tile's rows At [32 x KP] times the weight slice Wl [32 x KP]
+// (transposed), k-steps of 16 dealt to the waves in turn.
+__device__ __forceinline__ void tile_mfma(f32x16_t& acc, const float* At, int lda, const float* Wl, int ldw, int KP,
+                                          int wave, int lane) {
+    zero_acc(acc);
+    for (int ks = wave; ks < KP / 16; ks += kWaves) {
+        Frag<float> fa, fb;
+        fa.load(At + (lane & 31) * lda + ks * 16 + 8 * (lane >> 5));
+        fb.load(Wl + (lane & 31) * ldw + ks * 16 + 8 * (lane >> 5));
+        mfma(acc, fa, fb);
+    }
+}
+
+// ------------------------------------------------------------ host side
+constexpr int kMaxTreeGrid = 4096;   // workgroups of a persistent tree launch (the leaf groups' tail is sized for it)
+
+struct TreeDev {
+    int cus = 0;
+    size_t lds = 0;
+};
+// Properties of the current device, queried once per device under a lock.
+inline TreeDev tree_dev() {
+    static std::mutex m;
+    static TreeDev cache[64];
+    static bool have[64] = {};
+    int dev = 0;
+    if (hipGetDevice(&dev) != hipSuccess || dev < 0 || dev >= 64) return TreeDev{};
+    std::lock_guard<std::mutex> lock(m);
+    if (!have[dev]) {
+        TreeDev t;
+        int v = 0;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMultiprocessorCount, dev) == hipSuccess) t.cus = v;
+        if (hipDeviceGetAttribute(&v, hipDeviceAttributeMaxSharedMemoryPerBlock, dev) == hipSuccess) t.lds = size_t(v);
+        (void)hipGetLastError();
+        cache[dev] = t;
+        have[dev] = true;
+    }
+    return cache[dev];
+}
+
+// An ordinary launch of a grid whose workgroups must all be resident (the
+// plan allows one per CU and no more than the CUs; the occupancy query
+// confirms one fits a CU).  The barrier's waits are bounded.
+template <class K, class A>
+inline janus_status tree_persistent_launch(K kernel, int blocks, size_t smem, const A& args, hipStream_t st,
+                                    size_t& attr_smem) {
+    static std::mutex m;
+    {
+        std::lock_guard<std::mutex> lock(m);
+        if (smem > attr_smem) {
+            JANUS_HIP(hipFuncSetAttribute(reinterpret_cast<const void*>(kernel),
+                                          hipFuncAttributeMaxDynamicSharedMemorySize, int(smem)));
+            attr_smem = smem;
+        }
+    }
+    int per_cu = 0;
+    JANUS_HIP(hipOccupancyMaxActiveBlocksPerMultiprocessor(&per_cu, reinterpret_cast<const void*>(kernel),
+                                                           kThreads, smem));
+    if (per_cu < 1 || int64_t(per_cu) * tree_dev().cus < blocks) return JANUS_ERR_UNSUPPORTED;
+    hipLaunchKernelGGL(kernel, dim3(blocks), dim3(kThreads), smem, st, args);
+    JANUS_LAUNCH_CHECK();
+    return JANUS_OK;
+}
+
+}  // namespace tpersist
+}  // namespace janus

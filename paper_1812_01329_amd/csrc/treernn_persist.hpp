@@ -36,7 +36,7 @@
 // padded to whole 128-byte lines.
 #pragma once
 
-#include "tree_persist.hpp"
+#include "tree_common.hpp"
 
 namespace janus {
 namespace tpersist {
@@ -155,23 +155,7 @@ __global__ __launch_bounds__(kThreads) void treernn_fwd_persistent(RnnFwdArgs a)
             }
             if (tid < 32) rowsrc[tid] = tid < rows ? int64_t(pt + tid - a.M0) * a.ldl : -1;
             __syncthreads();
-            if (K % 4 == 0) {
-                stage4_2d<20>(32, KP / 4,
-                              [&](int m, int q) {
-                                  const int64_t r = rowsrc[m];
-                                  const int k = 4 * q;
-                                  return (r >= 0 && k < K) ? ld4(a.HLR + r + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-                              },
-                              [&](int m, int q, float4 v) { *reinterpret_cast<float4*>(At + m * sK + 4 * q) = v; });
-            } else {
-                stage<16>(32 * KP,
-                          [&](int idx) {
-                              const int m = idx / KP, k = idx - m * KP;
-                              const int64_t r = rowsrc[m];
-                              return (r >= 0 && k < K) ? a.HLR[r + k] : 0.f;
-                          },
-                          [&](int idx, float v) { At[(idx / KP) * sK + idx % KP] = v; });
-            }
+            stage_tile_rows(At, sK, a.HLR, rowsrc, K);
             if (tid < rows)
                 rowdst[tid] = par >= 0 ? int64_t((par >> 1) - a.M0) * a.ldl + (par & 1) * H : -1 - int64_t(rk) * H;
             __syncthreads();

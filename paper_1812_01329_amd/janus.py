@@ -34,7 +34,7 @@ EXPORTS = [
     "janus_sgd_workspace_bytes", "janus_sgd_clip_update", "janus_sgd_clip_update_noalloc",
     "janus_lstm_state_carry",
     "janus_treernn_workspace_bytes", "janus_treernn_fwd", "janus_treernn_bwd", "janus_treernn_device_report",
-    "janus_childsum_workspace_bytes", "janus_childsum_fwd", "janus_childsum_bwd",
+    "janus_childsum_workspace_bytes", "janus_childsum_fwd", "janus_childsum_bwd", "janus_childsum_device_report",
 ]
 
 
@@ -136,6 +136,8 @@ def lib():
         L.janus_childsum_fwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(NaryBatchC), vp, vp, vp, vp, vp, vp, sz, vp]
         L.janus_childsum_bwd.argtypes = [C.POINTER(TreeDesc), C.POINTER(NaryBatchC), vp, vp, vp, vp, sz, vp, vp, vp,
                                          vp, vp, vp]
+        L.janus_childsum_device_report.argtypes = [C.POINTER(TreeDesc), C.POINTER(NaryBatchC), vp, sz,
+                                                   C.POINTER(i32), vp]
         L.janus_xent_workspace_bytes.restype = sz
         L.janus_xent_workspace_bytes.argtypes = [C.POINTER(XentDesc), C.c_int]
         L.janus_embed_softmax_xent.argtypes = [C.POINTER(XentDesc), C.c_int, pi32, vp, vp, vp, vp, vp, vp, vp, vp,
@@ -367,6 +369,18 @@ def janus_childsum_bwd(desc: TreeDesc, trees, emb, W, U, ws, dh_root, demb, dW, 
                                   ws.numel() * ws.element_size(), _p(dh_root), _p(demb), _p(dW), _p(dU), _p(db),
                                   _stream(stream))
     _check(st, "janus_childsum_bwd")
+
+
+def janus_childsum_device_report(desc: TreeDesc, trees, ws, stream=None) -> int:
+    """Synchronises the stream and returns 1 if a level barrier of the last
+    Child-Sum forward or backward on this workspace ran out of its wait (the
+    call then raises JanusError(DEVICE)), else 0."""
+    tb, keep = _nary_c(trees)
+    out = C.c_int32(0)
+    st = lib().janus_childsum_device_report(C.byref(desc), C.byref(tb), _p(ws), ws.numel() * ws.element_size(),
+                                            C.byref(out), _stream(stream))
+    _check(st, "janus_childsum_device_report")
+    return int(out.value)
 
 
 # ---------------------------------------------------------------- heads

@@ -11,21 +11,35 @@ from tests.parity import TOL, check
 pytestmark = pytest.mark.gpu
 
 
-def _run_and_check(w):
+def _run_and_check(w, labels=None):
     import torch
+    from paper_1812_01329_amd import janus as J
     from paper_1812_01329_amd.train_step import make_step
     assert torch.cuda.is_available(), "GPU tests need a GPU"
     t = w.trees
     print(f"[childsum] trees={t.num_trees} nodes={t.num_nodes} E={w.E_dim} H={w.H}", flush=True)
     step = make_step(w)
+    J.janus_trace_begin()
     step.run()
     g = step.results()
+    traced = J.janus_trace_end()
+    if labels is not None:
+        labels.update(r["label"] for r in traced)
+    assert J.janus_childsum_device_report(step.desc, t, step.ws) == 0
     r = oracle_steps.childsum_step(w)
     tol = TOL["f32"]
     check("loss", np.array([g["loss"]]), np.array([r["loss"]]), tol["out"])
     check("h_root", g["h_root"], r["h_root"], tol["out"])
     for k in ("dh_root", "dWs", "dbs", "dW", "dU", "db", "demb"):
         check(k, g[k], r[k], tol["grad"])
+    used = np.zeros(w.V, bool)
+    used[np.asarray(t.word)] = True
+    assert np.all(g["demb"][~used] == 0.0)   # rows of words not in the batch are zero
+    # a second step on the same workspace gives the same bits
+    step.run()
+    g2 = step.results()
+    for k in ("h_root", "dW", "dU", "db", "demb"):
+        assert np.array_equal(g[k], g2[k]), k
     return g, r
 
 
@@ -71,3 +85,51 @@ def test_childsum_many_nodes():
     w = wl.sst_childsum(n_trees=520, E=8, H=8, V=300, min_nodes=35, max_nodes=45, seed=75)
     assert w.trees.num_nodes > 16384
     _run_and_check(w)
+
+
+def _cs_batch(case):
+    if case == "sst":
+        return wl.sst_childsum()
+    if case == "chains":   # a 40-node chain and a 3-node chain: one level per node
+        return wl.sst_childsum(n_trees=2, E=24, H=32, V=50, seed=81, sizes=[40, 3], chain=True)
+    if case == "singles":  # one-node trees only: a single level, no child
+        return wl.sst_childsum(n_trees=5, E=24, H=32, V=50, seed=83, sizes=[1, 1, 1, 1, 1])
+    if case == "odd":      # E = 37, H = 29: partial column tiles, scalar staging
+        return wl.sst_childsum(n_trees=7, E=37, H=29, V=61, seed=85)
+    # H = 156: the widest the persistent backward takes (two 32 x 4H slabs in LDS)
+    return wl.sst_childsum(n_trees=9, E=300, H=156, V=300, seed=86)
+
+
+@pytest.mark.parametrize("persist", ["1", "0"])
+@pytest.mark.parametrize("case", ["sst", "chains", "singles", "odd", "wide"])
+def test_childsum_persistent_levels(persist, case, monkeypatch):
+    """The Child-Sum step with each direction as one persistent launch (device
+    barriers between the levels' cells and contractions, fp32 MFMA tiles) and
+    with the level-by-level kernels (JANUS_TREE_PERSIST=0), each against the
+    oracle: the SST-sized batch, chains, one-node trees, odd sizes, and the
+    widest H the persistent backward takes."""
+    monkeypatch.setenv("JANUS_TREE_PERSIST", persist)
+    w = _cs_batch(case)
+    print(f"[childsum-persist] case={case} persist={persist} N={w.trees.num_nodes}", flush=True)
+    labels = set()
+    _run_and_check(w, labels)
+    if persist == "1":
+        assert {"childsum_fwd_persistent", "childsum_bwd_persistent"} <= labels, labels
+        assert not labels & {"childsum_fwd_cell", "childsum_bwd_cell", "childsum_level_gemm"}, labels
+    else:
+        assert not labels & {"childsum_fwd_persistent", "childsum_bwd_persistent"}, labels
+
+
+def test_childsum_wide_hidden_runs_levels():
+    """H = 320 does not fit the persistent backward's LDS slabs: both
+    directions run the level-by-level kernels (checked against the oracle by
+    test_childsum_wide_hidden)."""
+    from paper_1812_01329_amd import janus as J
+    from paper_1812_01329_amd.train_step import make_step
+    w = wl.sst_childsum(n_trees=2, E=40, H=320, V=64, seed=87)
+    step = make_step(w)
+    J.janus_trace_begin()
+    step.run()
+    labels = {r["label"] for r in J.janus_trace_end()}
+    assert "childsum_fwd_persistent" not in labels and "childsum_fwd_cell" in labels, labels
+
