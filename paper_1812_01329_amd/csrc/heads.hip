@@ -528,8 +528,27 @@ __global__ __launch_bounds__(256) void xent_small_kernel(const T* h, const T* W,
     float* zs = wsm + V * H;           // [rows][V]: logits, then dz
     float* ls = zs + rows * V;         // [rows] loss of each row
     const int tid = threadIdx.x;
-    for (int i = tid; i < rows * H; i += blockDim.x) hs[i] = to_f(h[i]);
-    for (int i = tid; i < V * H; i += blockDim.x) wsm[i] = to_f(W[i]);
+    // h and W into LDS, NB elements in flight per thread: the raw values are
+    // loaded first and converted only after the last load of the batch is
+    // issued, so a batch costs one memory round trip, not one per element
+    auto stage = [&](float* dst, const T* src, int n) {
+        constexpr int NB = 32;
+        for (int base = tid; base < n; base += 256 * NB) {
+            T v[NB];
+#pragma unroll
+            for (int i = 0; i < NB; ++i) {
+                const int idx = base + i * 256;
+                v[i] = idx < n ? src[idx] : T(0);
+            }
+#pragma unroll
+            for (int i = 0; i < NB; ++i) {
+                const int idx = base + i * 256;
+                if (idx < n) dst[idx] = to_f(v[i]);
+            }
+        }
+    };
+    stage(hs, h, rows * H);
+    stage(wsm, W, V * H);
     __syncthreads();
     for (int i = tid; i < rows * V; i += blockDim.x) {
         const int r = i / V, v = i - r * V;
