@@ -394,7 +394,23 @@ __global__ __launch_bounds__(kThreads) void childsum_bwd_persistent(CsBwdArgs a)
             if (it < n_dW) { kind = 0; ti = it / ne; tj = it % ne; }
             else if (it < n_dW + n_dU) { kind = 1; ti = (it - n_dW) / nh; tj = (it - n_dW) % nh; }
             else { kind = 2; ti = (it - n_dW - n_dU) / ne; tj = (it - n_dW - n_dU) % ne; }
-            if (kind == 0) {
+            // rows of dXW, dG and h are padded to 32 floats: 16-byte pieces
+            // always; rows of emb and W when E % 4 == 0 and both are 16-byte aligned
+            const bool vec = E % 4 == 0 && aligned16(a.emb) && aligned16(a.W);
+            if (kind == 0 && vec) {
+                node_contraction4<false>(acc, Ac, Bc, a.N, min(32, G4 - 32 * ti), min(32, E - 32 * tj),
+                    [&](int r4, int k) { return ld4(a.dXW + int64_t(k) * a.ld4 + 32 * ti + r4); },
+                    [&](int c4, int k) { return ld4(a.emb + int64_t(a.pword[k]) * E + 32 * tj + c4); });
+            } else if (kind == 1) {
+                // dU = sum over nodes of dG[p][.] h_p[.]
+                node_contraction4<false>(acc, Ac, Bc, a.N, min(32, G4 - 32 * ti), min(32, H - 32 * tj),
+                    [&](int r4, int k) { return ld4(a.dG + int64_t(k) * a.ld4 + 32 * ti + r4); },
+                    [&](int c4, int k) { return ld4(a.Hn + int64_t(k) * a.ldh + 32 * tj + c4); });
+            } else if (kind == 2 && vec) {
+                node_contraction4<true>(acc, Ac, Bc, G4, min(32, a.N - 32 * ti), min(32, E - 32 * tj),
+                    [&](int r, int k4) { return ld4(a.dXW + int64_t(32 * ti + r) * a.ld4 + k4); },
+                    [&](int c4, int k) { return ld4(a.W + int64_t(k) * E + 32 * tj + c4); });
+            } else if (kind == 0) {
                 // dW[32 ti + r][32 tj + c] = sum over nodes of dXW[p][.] x_p[.]
                 node_contraction<false>(acc, Ac, Bc, a.N,
                     [&](int r, int k) {
@@ -404,17 +420,6 @@ __global__ __launch_bounds__(kThreads) void childsum_bwd_persistent(CsBwdArgs a)
                     [&](int c, int k) {
                         const int n = 32 * tj + c;
                         return n < E ? a.emb[int64_t(a.pword[k]) * E + n] : 0.f;
-                    });
-            } else if (kind == 1) {
-                // dU = sum over nodes of dG[p][.] h_p[.]
-                node_contraction<false>(acc, Ac, Bc, a.N,
-                    [&](int r, int k) {
-                        const int n = 32 * ti + r;
-                        return n < G4 ? a.dG[int64_t(k) * a.ld4 + n] : 0.f;
-                    },
-                    [&](int c, int k) {
-                        const int n = 32 * tj + c;
-                        return n < H ? a.Hn[int64_t(k) * a.ldh + n] : 0.f;
                     });
             } else {
                 // dx[p][.] = sum over gate columns of dXW[p][k] W[k][.]

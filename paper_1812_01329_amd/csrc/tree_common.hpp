@@ -105,6 +105,7 @@ __device__ __forceinline__ void stage4(int n, Ld ld, St st) {
     }
 }
 __device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
+__device__ __forceinline__ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 
 // Copy an nrow x KQ grid of 16-byte pieces into LDS: piece (m, q) is
 // ld(m, q) (0 outside its operand) and goes where st(m, q, v) puts it.
@@ -172,6 +173,74 @@ __device__ __forceinline__ void node_contraction(f32x16_t& acc, float* Ac, float
             Bc[r * sK + kk] = vb[i];
             if constexpr (AK) Ac[(idx / kKC) * sK + idx % kKC] = va[i];
             else Ac[r * sK + kk] = va[i];
+        }
+        if (k0 + kKC < K) fetch(k0 + kKC);
+        __syncthreads();
+        for (int ks = wave; ks < kKC / 16; ks += kWaves) {
+            Frag<float> xa, xb;
+            xa.load(Ac + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
+            xb.load(Bc + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
+            mfma(acc, xa, xb);
+        }
+    }
+}
+
+// The same with 16-byte pieces, for operands whose rows are 16-byte aligned
+// and padded so that four elements read from a valid start never leave the
+// row: fa4(i, k) returns A[i][k .. k + 3] (AK) or A[i .. i + 3][k], and
+// fb4(j, k) returns B[j .. j + 3][k], as loaded.  nA and nB count the valid
+// rows of A and columns of B in this tile; the elements past them (and past
+// K) are zeroed when the chunk is written to LDS, after the chunk's loads
+// are all issued.  A thread then issues 8 loads per chunk instead of 32.
+template <bool AK, class FA, class FB>
+__device__ __forceinline__ void node_contraction4(f32x16_t& acc, float* Ac, float* Bc, int K, int nA, int nB,
+                                                  FA fa4, FB fb4) {
+    constexpr int sK = kKC + 4, PER = 32 * kKC / 4 / kThreads;   // 4 pieces of each operand per thread
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float4 va[PER], vb[PER];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * kThreads;
+            const int kk = idx >> 3, c4 = 4 * (idx & 7);
+            vb[i] = (k0 + kk < K && c4 < nB) ? fb4(c4, k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
+            if constexpr (AK) {
+                const int r = idx >> 5, k4 = 4 * (idx & 31);
+                va[i] = (k0 + k4 < K && r < nA) ? fa4(r, k0 + k4) : make_float4(0.f, 0.f, 0.f, 0.f);
+            } else {
+                va[i] = (k0 + kk < K && c4 < nA) ? fa4(c4, k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+    };
+    // keep the first n elements of a piece
+    auto keep = [](float4 v, int n) {
+        if (n < 4) v.w = 0.f;
+        if (n < 3) v.z = 0.f;
+        if (n < 2) v.y = 0.f;
+        return v;
+    };
+    if (K > 0) fetch(0);
+    for (int k0 = 0; k0 < K; k0 += kKC) {
+        __syncthreads();   // the previous chunk's reads are done
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * kThreads;
+            const int kk = idx >> 3, c4 = 4 * (idx & 7);
+            const float4 b = keep(vb[i], nB - c4);
+            Bc[(c4 + 0) * sK + kk] = b.x;
+            Bc[(c4 + 1) * sK + kk] = b.y;
+            Bc[(c4 + 2) * sK + kk] = b.z;
+            Bc[(c4 + 3) * sK + kk] = b.w;
+            if constexpr (AK) {
+                const int r = idx >> 5, k4 = 4 * (idx & 31);
+                *reinterpret_cast<float4*>(Ac + r * sK + k4) = keep(va[i], K - (k0 + k4));
+            } else {
+                const float4 v = keep(va[i], nA - c4);
+                Ac[(c4 + 0) * sK + kk] = v.x;
+                Ac[(c4 + 1) * sK + kk] = v.y;
+                Ac[(c4 + 2) * sK + kk] = v.z;
+                Ac[(c4 + 3) * sK + kk] = v.w;
+            }
         }
         if (k0 + kKC < K) fetch(k0 + kKC);
         __syncthreads();

@@ -509,17 +509,22 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
             if (it < n_dU) { kind = 0; ti = it / nh2; tj = it % nh2; }
             else if (it < n_dU + n_dW) { kind = 1; ti = (it - n_dU) / ne; tj = (it - n_dU) % ne; }
             else { kind = 2; ti = (it - n_dU - n_dW) / ne; tj = (it - n_dU - n_dW) % ne; }
+            // rows of dA and [h_L; h_R] are padded to 32 floats: 16-byte
+            // pieces always; rows of emb and W when E % 4 == 0 and both are 16-byte aligned
+            const bool vec = E % 4 == 0 && aligned16(a.emb) && aligned16(a.W);
             if (kind == 0) {
                 // dU[32 ti + r][32 tj + c] = sum over internal nodes of dA[p][.] [h_L; h_R][p][.]
-                node_contraction<false>(acc, Ac, Bc, Nint,
-                    [&](int r, int k) {
-                        const int n = 32 * ti + r;
-                        return n < G5 ? a.dA[int64_t(a.M0 + k) * a.lda + n] : 0.f;
-                    },
-                    [&](int c, int k) {
-                        const int n = 32 * tj + c;
-                        return n < H2 ? a.HLR[int64_t(k) * a.ldl + n] : 0.f;
-                    });
+                node_contraction4<false>(acc, Ac, Bc, Nint, min(32, G5 - 32 * ti), min(32, H2 - 32 * tj),
+                    [&](int r4, int k) { return ld4(a.dA + int64_t(a.M0 + k) * a.lda + 32 * ti + r4); },
+                    [&](int c4, int k) { return ld4(a.HLR + int64_t(k) * a.ldl + 32 * tj + c4); });
+            } else if (kind == 1 && vec) {
+                node_contraction4<false>(acc, Ac, Bc, a.M0, min(32, G5 - 32 * ti), min(32, E - 32 * tj),
+                    [&](int r4, int k) { return ld4(a.dA + int64_t(k) * a.lda + 32 * ti + r4); },
+                    [&](int c4, int k) { return ld4(a.emb + int64_t(a.lword[k]) * E + 32 * tj + c4); });
+            } else if (kind == 2 && vec) {
+                node_contraction4<true>(acc, Ac, Bc, G5, min(32, a.M0 - 32 * ti), min(32, E - 32 * tj),
+                    [&](int r, int k4) { return ld4(a.dA + int64_t(32 * ti + r) * a.lda + k4); },
+                    [&](int c4, int k) { return ld4(a.W + int64_t(k) * E + 32 * tj + c4); });
             } else if (kind == 1) {
                 // dW = sum over leaves of dA[p][.] x_p[.]
                 node_contraction<false>(acc, Ac, Bc, a.M0,

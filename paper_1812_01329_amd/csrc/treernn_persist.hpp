@@ -421,15 +421,9 @@ __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a)
             f32x16_t acc;
             zero_acc(acc);
             // dW[32 ti + r][32 tj + c] = sum over internal nodes of da[p][.] [h_L; h_R][p][.]
-            node_contraction<false>(acc, Ac, Bc, Nint,
-                [&](int r, int k) {
-                    const int n = 32 * ti + r;
-                    return n < H ? a.dA[int64_t(a.M0 + k) * a.lda + n] : 0.f;
-                },
-                [&](int c, int k) {
-                    const int n = 32 * tj + c;
-                    return n < H2 ? a.HLR[int64_t(k) * a.ldl + n] : 0.f;
-                });
+            node_contraction4<false>(acc, Ac, Bc, Nint, min(32, H - 32 * ti), min(32, H2 - 32 * tj),
+                [&](int r4, int k) { return ld4(a.dA + int64_t(a.M0 + k) * a.lda + 32 * ti + r4); },
+                [&](int c4, int k) { return ld4(a.HLR + int64_t(k) * a.ldl + 32 * tj + c4); });
             spill_acc(acc, red, wave, lane);
             __syncthreads();
             for (int idx = tid; idx < 32 * 32; idx += kThreads) {
