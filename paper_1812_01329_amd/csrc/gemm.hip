@@ -13,6 +13,8 @@ namespace janus {
 
 namespace {
 
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
+
 // Epilogue: C = alpha * acc + bias, optional row scatter.  Specialised on the
 // output type and the scatter so that every accumulator index is a
 // compile-time constant (the 256-register accumulator stays in registers).
@@ -144,6 +146,12 @@ struct NtArgs {
 
 enum NtEpilogue { kEpiStore = 0, kEpiPartial = 1, kEpiMse = 2 };
 
+// Element v (0..15) of a 32 x 32 block held as four 16x16x32 MFMA products:
+// sub-block v / 4 = (a, b) covers rows 16 a + [0, 16), columns 16 b + [0, 16),
+// and its element v % 4 of lane l sits at row 4 (l / 16) + v % 4, column l % 16.
+__device__ __forceinline__ int nt_row(int v, int lane) { return 16 * (v >> 3) + 4 * (lane >> 4) + (v & 3); }
+__device__ __forceinline__ int nt_col(int v, int lane) { return 16 * ((v >> 2) & 1) + (lane & 15); }
+
 constexpr uint32_t kNtOutOfRange = 0x80000000u;
 
 typedef __attribute__((address_space(3))) void* lds_ptr_t;
@@ -238,28 +246,45 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
     };
 
     const int wr0 = C_::wave_row0(wave), wc0 = C_::wave_col0(wave);
-    f32x16_t acc[C_::FM][C_::FN];
+    // A wave's 128 x 64 block is 8 x 4 products of 16 x 16 (16x16x32 MFMA:
+    // the same operand bytes per flop as 32x32x16, measured 5-7 % faster on
+    // the step's shapes).  acc[i][j][s] holds sub-block (s / 2, s % 2) of the
+    // 32 x 32 block (i, j); element v of a 32 x 32 block is acc[i][j][v / 4][v % 4],
+    // at row nt_row(v, lane), column nt_col(v, lane).
+    f32x4_t acc[C_::FM][C_::FN][4];
     // fragment rows; the row swizzle is row % 8 = lane % 8 for every fragment
-    const int sw = lane & 7, kh = lane >> 5;
-    int arow[C_::FM], brow[C_::FN];
+    const int sw = lane & 7, kq = lane >> 4;
+    int arow[2 * C_::FM], brow[2 * C_::FN];
 #pragma unroll
-    for (int i = 0; i < C_::FM; ++i) arow[i] = (wr0 + i * 32 + (lane & 31)) * C_::BK;
+    for (int i = 0; i < 2 * C_::FM; ++i) arow[i] = (wr0 + i * 16 + (lane & 15)) * C_::BK;
 #pragma unroll
-    for (int j = 0; j < C_::FN; ++j) brow[j] = C_::BM * C_::BK + (wc0 + j * 32 + (lane & 31)) * C_::BK;
+    for (int j = 0; j < 2 * C_::FN; ++j) brow[j] = C_::BM * C_::BK + (wc0 + j * 16 + (lane & 15)) * C_::BK;
 
     auto compute = [&](const bf16_t* cur) {
 #pragma unroll
-        for (int ks = 0; ks < C_::BK / 16; ++ks) {
-            const int q = 2 * ks + kh;
-            Frag<bf16_t> fa[C_::FM], fb[C_::FN];
+        for (int ks = 0; ks < C_::BK / 32; ++ks) {
+            const int q = 4 * ks + kq;
+            // the B fragments, then the A fragments in two halves (fewer live
+            // registers: the persistent variant holds the next tile's loads too)
+            uint4 fb[2 * C_::FN];
 #pragma unroll
-            for (int i = 0; i < C_::FM; ++i) fa[i].load(cur + arow[i] + ((q ^ sw) << 3));
+            for (int j = 0; j < 2 * C_::FN; ++j) fb[j] = *reinterpret_cast<const uint4*>(cur + brow[j] + ((q ^ sw) << 3));
 #pragma unroll
-            for (int j = 0; j < C_::FN; ++j) fb[j].load(cur + brow[j] + ((q ^ sw) << 3));
+            for (int h = 0; h < 2; ++h) {
+                uint4 fa[C_::FM];
 #pragma unroll
-            for (int i = 0; i < C_::FM; ++i)
+                for (int i = 0; i < C_::FM; ++i)
+                    fa[i] = *reinterpret_cast<const uint4*>(cur + arow[h * C_::FM + i] + ((q ^ sw) << 3));
 #pragma unroll
-                for (int j = 0; j < C_::FN; ++j) mfma(acc[i][j], fa[i], fb[j]);
+                for (int i = 0; i < C_::FM; ++i)
+#pragma unroll
+                    for (int j = 0; j < 2 * C_::FN; ++j) {
+                        const int ii = h * C_::FM + i;
+                        f32x4_t& a = acc[ii / 2][j / 2][2 * (ii % 2) + j % 2];
+                        a = __builtin_amdgcn_mfma_f32_16x16x32_bf16(__builtin_bit_cast(bf16x8_t, fa[i]),
+                                                                    __builtin_bit_cast(bf16x8_t, fb[j]), a, 0, 0, 0);
+                    }
+            }
         }
     };
 
@@ -282,7 +307,7 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
 #pragma unroll
         for (int j = 0; j < C_::FN; ++j)
 #pragma unroll
-            for (int v = 0; v < 16; ++v) acc[i][j][v] = 0.f;
+            for (int s4 = 0; s4 < 4; ++s4) acc[i][j][s4] = f32x4_t{0.f, 0.f, 0.f, 0.f};
     int it = 0;
     for (; it + 1 < nk; it += 2) {
         sync();
@@ -345,8 +370,8 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
                 for (int j = 0; j < C_::FN; ++j)
 #pragma unroll
                     for (int v = 0; v < 16; ++v) {
-                        const int r = ii * 32 + acc_row(v, lane), c = j * 32 + acc_col(lane);
-                        tile[r * 64 + (c ^ ((r & 7) << 3))] = acc[2 * half + ii][j][v];
+                        const int r = ii * 32 + nt_row(v, lane), c = j * 32 + nt_col(v, lane);
+                        tile[r * 64 + (c ^ ((r & 7) << 3))] = acc[2 * half + ii][j][v >> 2][v & 3];
                     }
 #pragma unroll
             for (int q = 0; q < 8; ++q) {
@@ -404,17 +429,14 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
     } else if constexpr (EPI == kEpiPartial) {
         float* P = p.partial + int64_t(split) * p.M * p.N;
 #pragma unroll
-        for (int j = 0; j < C_::FN; ++j) {
-            const int col = n0 + wc0 + j * 32 + acc_col(lane);
-            if (col >= p.N) continue;
+        for (int j = 0; j < C_::FN; ++j)
 #pragma unroll
             for (int i = 0; i < C_::FM; ++i)
 #pragma unroll
                 for (int v = 0; v < 16; ++v) {
-                    const int row = m0 + wr0 + i * 32 + acc_row(v, lane);
-                    if (row < p.M) P[int64_t(row) * p.N + col] = acc[i][j][v];
+                    const int row = m0 + wr0 + i * 32 + nt_row(v, lane), col = n0 + wc0 + j * 32 + nt_col(v, lane);
+                    if (row < p.M && col < p.N) P[int64_t(row) * p.N + col] = acc[i][j][v >> 2][v & 3];
                 }
-        }
     } else {
         if (p.vec_store) {
             // Stage each wave's accumulators through LDS as in the MSE epilogue
@@ -450,8 +472,8 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
                     for (int j = 0; j < C_::FN; ++j)
 #pragma unroll
                         for (int v = 0; v < 16; ++v) {
-                            const int r = ii * 32 + acc_row(v, lane), c = j * 32 + acc_col(lane);
-                            tile[r * 64 + (c ^ ((r & 7) << 3))] = acc[pass * (RP / 32) + ii][j][v];
+                            const int r = ii * 32 + nt_row(v, lane), c = j * 32 + nt_col(v, lane);
+                            tile[r * 64 + (c ^ ((r & 7) << 3))] = acc[pass * (RP / 32) + ii][j][v >> 2][v & 3];
                         }
 #pragma unroll
                 for (int q = 0; q < RP / 8; ++q) {
@@ -480,7 +502,32 @@ void gemm_nt_fast_kernel(NtArgs p, GemmDesc g) {
                 }
             }
         } else {
-            store_tile_impl<bf16_t, NtCfg, OutT, SCATTER>(g, acc, m0, n0, tid);
+            // C = alpha acc + bias element by element (any N, ldc, alignment)
+            const bf16_t* bias = static_cast<const bf16_t*>(g.bias);
+            OutT* C = static_cast<OutT*>(g.C);
+            // a lane's columns: 16 b + l % 16 of each 32-column block j
+            float bv[C_::FN][2];
+#pragma unroll
+            for (int j = 0; j < C_::FN; ++j)
+#pragma unroll
+                for (int b = 0; b < 2; ++b) {
+                    const int col = n0 + wc0 + j * 32 + 16 * b + (lane & 15);
+                    bv[j][b] = (bias && col < p.N) ? bf2f(bias[col]) : 0.f;
+                }
+#pragma unroll
+            for (int i = 0; i < C_::FM; ++i)
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int row = m0 + wr0 + i * 32 + nt_row(v, lane);
+                    if (row >= p.M) continue;
+                    const int64_t crow = SCATTER ? int64_t(g.c_idx[row]) : int64_t(row);
+#pragma unroll
+                    for (int j = 0; j < C_::FN; ++j) {
+                        const int col = n0 + wc0 + j * 32 + nt_col(v, lane);
+                        if (col < p.N)
+                            C[crow * g.ldc + col] = from_f<OutT>(g.alpha * acc[i][j][v >> 2][v & 3] + bv[j][(v >> 2) & 1]);
+                    }
+                }
         }
     }
     if (!more) break;
@@ -704,10 +751,10 @@ const char* nt_label(bool f32out, bool scatter, bool partial) {
     return scatter ? "gemm_nt_bf16out_scatter" : "gemm_nt_bf16out";
 }
 
-// JANUS_GEMM_PERSIST=0 switches the persistent tile loop off
-bool getenv_off(const char* name) {
+// JANUS_GEMM_PERSIST=1 switches the persistent tile loop on
+bool getenv_on(const char* name) {
     const char* e = getenv(name);
-    return e && e[0] == '0';
+    return e && e[0] == '1';
 }
 
 // compute units of the current device (0 if the query fails)
@@ -730,11 +777,13 @@ janus_status launch_nt(const NtArgs& args, const GemmDesc& g, hipStream_t s) {
                       : 0;
     const int ntot = a.mt * a.nt * a.splits;
     // persistent tiles where every workgroup gets two or more: one per CU
-    // (a multiple of 8, so each XCD holds the same number)
+    // (a multiple of 8, so each XCD holds the same number).  Off unless asked
+    // for: with the 16x16x32 products that variant spills registers around
+    // its tile loop and runs slower than one workgroup per tile.
     int grid = 0;
     if constexpr (EPI == kEpiStore) {
         const int cus = device_cus() / 8 * 8;
-        if (a.vec_store && cus >= 8 && ntot % 8 == 0 && ntot >= 2 * cus && !getenv_off("JANUS_GEMM_PERSIST")) grid = cus;
+        if (a.vec_store && cus >= 8 && ntot % 8 == 0 && ntot >= 2 * cus && getenv_on("JANUS_GEMM_PERSIST")) grid = cus;
     }
     const double out_bytes = EPI == kEpiPartial ? 4.0 * a.splits : EPI == kEpiMse ? 4.0 : (sizeof(OutT) == 4 ? 4.0 : 2.0);
     TraceScope trace(EPI == kEpiMse ? "gemm_nt_mse" : nt_label(sizeof(OutT) == 4, SCATTER, EPI == kEpiPartial),

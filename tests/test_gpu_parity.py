@@ -356,13 +356,13 @@ def test_deterministic_repeat_persistent(H, B, ragged):
 
 @pytest.mark.parametrize("ragged", [False, True])
 def test_persistent_contraction_tiles(ragged, monkeypatch):
-    """Contractions of 512 tiles and more run as a persistent grid (one
+    """Contractions of 512 tiles and more can run as a persistent grid (one
     workgroup per CU walking the tiles, the next tile's first K block loaded
-    during the current tile's epilogue).  The input projection here has
-    8192 x 4096 outputs (512 tiles of 256 x 256), or, with ragged lengths,
-    about 8300 packed rows (528 tiles, the last M tile partial): with the
-    persistent grid and without (JANUS_GEMM_PERSIST=0) the step gives
-    identical bits, and matches the oracle."""
+    during the current tile's epilogue; JANUS_GEMM_PERSIST=1).  The input
+    projection here has 8192 x 4096 outputs (512 tiles of 256 x 256), or,
+    with ragged lengths, about 8300 packed rows (528 tiles, the last M tile
+    partial): with the persistent grid and without (JANUS_GEMM_PERSIST=0,
+    the default) the step gives identical bits, and matches the oracle."""
     T, lens = 32, None
     if ragged:
         T = 64
