@@ -344,7 +344,7 @@ TreePlan tree_plan(const janus_treelstm_desc& d) {
     if (e && e[0] == '0') return p;
     const TreeDev dev = tree_dev();
     if (dev.cus <= 0 || dev.lds == 0) return p;
-    if (d.E > tpersist::kMaxE) return p;
+    if (d.E > tpersist::kMaxE || d.H > tpersist::kUC * tpersist::kMaxCh) return p;
     p.ngroups = (d.H + tpersist::kUG - 1) / tpersist::kUG;
     p.ncol = (2 * d.H + 31) / 32;
     if (p.ngroups > dev.cus || p.ncol > dev.cus) return p;

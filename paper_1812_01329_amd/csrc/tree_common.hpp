@@ -104,6 +104,7 @@ __device__ __forceinline__ void stage4(int n, Ld ld, St st) {
         }
     }
 }
+typedef float f32x4_t __attribute__((ext_vector_type(4)));
 __device__ __forceinline__ float4 ld4(const float* p) { return *reinterpret_cast<const float4*>(p); }
 __device__ __forceinline__ bool aligned16(const void* p) { return (reinterpret_cast<uintptr_t>(p) & 15) == 0; }
 

@@ -137,9 +137,23 @@ __global__ __launch_bounds__(kThreads) void treelstm_fwd_persistent(FwdArgs a) {
 #pragma unroll
     for (int q = 0; q < 5; ++q) bias[q] = cell_thread ? a.b[q * H + cj] : 0.f;
 
+    // the cell's links (children, parent, root slot) of row cm of tile t at
+    // level L; those of a workgroup's first tile of a level are loaded
+    // before the barrier that precedes the level
+    int lc = -1, rc = -1, par = -1, rk = -1;
+    auto links = [&](int L, int t) {
+        const int pt = a.loff[L] + 32 * t, p = pt + cm;
+        const bool cell = cell_thread && p < a.loff[L + 1];
+        lc = cell ? a.lchild[p] : -1;
+        rc = cell ? a.rchild[p] : -1;
+        par = cell ? a.parent[p] : -1;
+        rk = cell ? a.rootk[p] : -1;
+    };
+    auto level_tiles = [&](int L) { return (a.loff[L + 1] - a.loff[L] + 31) / 32; };
+    if (r0 < level_tiles(0)) links(0, r0);
     for (int L = 0; L < a.nlev; ++L) {
         const int p0 = a.loff[L], p1 = a.loff[L + 1];
-        const int ntile = (p1 - p0 + 31) / 32;
+        const int ntile = level_tiles(L);
         const bool leaf = L == 0;
         const int K = leaf ? E : 2 * H, KP = leaf ? KE : KU, sW = leaf ? sE : sU;
         const float* Wsrc = leaf ? Wl : Ul;
@@ -148,32 +162,19 @@ __global__ __launch_bounds__(kThreads) void treelstm_fwd_persistent(FwdArgs a) {
             const int pt = p0 + 32 * t, rows = min(32, p1 - pt);
             const int p = pt + cm;
             const bool cell = cell_thread && cm < rows;
-            // the cell's links, loaded while the tile is staged
-            int lc = -1, rc = -1, par = -1, rk = -1;
-            if (cell) {
-                lc = a.lchild[p];
-                rc = a.rchild[p];
-                par = a.parent[p];
-                rk = a.rootk[p];
-            }
+            if (t != r0) links(L, t);
             __syncthreads();   // the previous tile's reads of At, red and rowsrc are done
             if (tid < 32) {
                 const int q = pt + tid;
                 rowsrc[tid] = tid < rows ? (leaf ? int64_t(a.lword[q]) * E : int64_t(q - a.M0) * a.ldl) : -1;
             }
             __syncthreads();
-            if (K % 4 == 0) {
-                const int KP4 = KP / 4;
-                stage4<4>(32 * KP4,
-                          [&](int idx) {
-                              const int m = idx / KP4, k = 4 * (idx - m * KP4);
-                              const int64_t r = rowsrc[m];
-                              return (r >= 0 && k < K) ? ld4(src + r + k) : make_float4(0.f, 0.f, 0.f, 0.f);
-                          },
-                          [&](int idx, float4 v) {
-                              const int m = idx / KP4, k = 4 * (idx - m * KP4);
-                              *reinterpret_cast<float4*>(At + m * sA + k) = v;
-                          });
+            // the children's c, in flight with the tile's rows
+            const float cl = a.C[int64_t(lc >= 0 ? lc : 0) * a.ldc + (cell ? cj : 0)];
+            const float cr = a.C[int64_t(rc >= 0 ? rc : 0) * a.ldc + (cell ? cj : 0)];
+            if (!leaf || aligned16(a.emb)) {
+                // every row in one round trip (16-byte pieces where K % 4 == 0)
+                stage_tile_rows(At, sA, src, rowsrc, K);
             } else {
                 stage<16>(32 * KP,
                           [&](int idx) {
@@ -186,9 +187,6 @@ __global__ __launch_bounds__(kThreads) void treelstm_fwd_persistent(FwdArgs a) {
                               At[m * sA + k] = v;
                           });
             }
-            // the children's c, loaded while the tile is contracted
-            const float cl = lc >= 0 ? a.C[int64_t(lc) * a.ldc + cj] : 0.f;
-            const float cr = rc >= 0 ? a.C[int64_t(rc) * a.ldc + cj] : 0.f;
             __syncthreads();
             // D[node m][tile column c] = sum_k rows[m][k] * Wslice[c][k], the
             // k-steps of 16 dealt to the waves in turn
@@ -208,7 +206,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_fwd_persistent(FwdArgs a) {
                 for (int q = 0; q < 5; ++q) z[q] = bias[q] + red_sum(red, cm, q * kUG + cu);
                 const float gi = sigmoidf_(z[0]), gl = sigmoidf_(z[1]), gr = sigmoidf_(z[2]), go = sigmoidf_(z[3]);
                 const float gu = tanhf_(z[4]);
-                const float c = gi * gu + gl * cl + gr * cr;
+                const float c = gi * gu + gl * (lc >= 0 ? cl : 0.f) + gr * (rc >= 0 ? cr : 0.f);
                 const float h = go * tanhf_(c);
                 store_through(a.C, int64_t(p) * a.ldc + cj, c);
                 float* gp = a.G + int64_t(p) * a.ldg + cj;
@@ -222,6 +220,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_fwd_persistent(FwdArgs a) {
             }
         }
         if (L + 1 < a.nlev) {
+            if (r0 < level_tiles(L + 1)) links(L + 1, r0);
             persist::barrier_arrive(bar);
             persist::barrier_wait(bar);
         }
@@ -328,6 +327,57 @@ __device__ __forceinline__ void cell_grad(const CellIn& x, int i, float (&da)[5]
     dcr = dct * gr;
 }
 
+// The internal levels run in 16-row tiles: thread rows tid / 32 + 8 i
+// (i < 2), unit lane tid % 32 of each 32-unit chunk.  A thread holds the
+// inputs of all its cells at once (H at most 32 kMaxCh), so a tile costs
+// one memory round trip for its inputs.
+constexpr int kLR = 16;
+constexpr int kLRows = kLR * kUC / kThreads;   // 2
+constexpr int kMaxCh = 6;
+struct LevLinks {
+    int p[kLRows], lc[kLRows], rc[kLRows], rk[kLRows];
+};
+struct LevIn {
+    float g[kLRows][kMaxCh][5], c[kLRows][kMaxCh], cl[kLRows][kMaxCh], cr[kLRows][kMaxCh];
+    float dh[kLRows][kMaxCh], dc[kLRows][kMaxCh];
+};
+__device__ __forceinline__ LevLinks lev_links(const BwdArgs& a, int pt, int rows) {
+    LevLinks r;
+#pragma unroll
+    for (int i = 0; i < kLRows; ++i) {
+        const int m = int(threadIdx.x) / 32 + 8 * i;
+        r.p[i] = m < rows ? pt + m : -1;
+        const int q = m < rows ? pt + m : pt;
+        r.lc[i] = a.lchild[q];
+        r.rc[i] = a.rchild[q];
+        r.rk[i] = a.rootk[q];
+    }
+    return r;
+}
+// Every load is issued before any value is used (indices clamped to valid
+// rows and units, absent cells masked afterwards by the caller).
+__device__ __forceinline__ void lev_inputs(const BwdArgs& a, const LevLinks& r, int nch, LevIn& x) {
+    const int H = a.H, u = int(threadIdx.x) % 32;
+#pragma unroll
+    for (int ch = 0; ch < kMaxCh; ++ch) {
+        if (ch >= nch) break;
+        const int j = min(32 * ch + u, H - 1);
+#pragma unroll
+        for (int i = 0; i < kLRows; ++i) {
+            const int64_t p = r.p[i] >= 0 ? r.p[i] : 0;
+            const int64_t pl = r.lc[i] >= 0 ? r.lc[i] : p, pr = r.rc[i] >= 0 ? r.rc[i] : p;
+            const float* gp = a.G + p * a.ldg + j;
+#pragma unroll
+            for (int q = 0; q < 5; ++q) x.g[i][ch][q] = gp[q * H];
+            x.c[i][ch] = a.C[p * a.ldc + j];
+            x.cl[i][ch] = a.C[pl * a.ldc + j];
+            x.cr[i][ch] = a.C[pr * a.ldc + j];
+            x.dh[i][ch] = r.rk[i] >= 0 ? a.dh_root[int64_t(r.rk[i]) * H + j] : a.dh[p * a.ldc + j];
+            x.dc[i][ch] = a.dc[p * a.ldc + j];
+        }
+    }
+}
+
 __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
     extern __shared__ __align__(16) float sm[];
     const int E = a.E, H = a.H, H2 = 2 * a.H, G5 = 5 * a.H;
@@ -367,54 +417,92 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
     }
     const int u = tid % 32;   // this thread's unit lane within a chunk
 
+    const int nch = (H + kUC - 1) / kUC;
+    auto level_tiles = [&](int L) { return (a.loff[L + 1] - a.loff[L] + kLR - 1) / kLR; };
+    // the links of this workgroup's first tile of a level are loaded before
+    // the barrier that precedes the level
+    LevLinks lk{};
+    if (a.nlev > 1 && r0 < level_tiles(a.nlev - 1)) {
+        const int pt = a.loff[a.nlev - 1] + kLR * r0;
+        lk = lev_links(a, pt, min(kLR, a.loff[a.nlev] - pt));
+    }
     for (int L = a.nlev - 1; L >= 1; --L) {
         const int p0 = a.loff[L], p1 = a.loff[L + 1];
-        const int ntile = (p1 - p0 + 31) / 32;
+        const int ntile = level_tiles(L);
         for (int t = r0; t < ntile; t += R) {
-            const int pt = p0 + 32 * t, rows = min(32, p1 - pt);
-            const RowLinks lk = row_links(a, pt, rows);
-            // inputs of chunks j0 and j0 + kUC in flight (two chunks ahead)
-            CellIn x = cell_inputs(a, lk, u);
-            CellIn xn = cell_inputs(a, lk, kUC + u);
-            f32x16_t acc;
-            zero_acc(acc);
-            for (int j0 = 0; j0 < H; j0 += kUC) {
-                const int j = j0 + u;
-                __syncthreads();   // the previous chunk's reads of dAc are done
+            const int pt = p0 + kLR * t, rows = min(kLR, p1 - pt);
+            if (t != r0) lk = lev_links(a, pt, rows);
+            LevIn x;
+            lev_inputs(a, lk, nch, x);
+            // D[node m][column 16 b + c] over the gate columns as 16x16x4
+            // products: k step jj of lane l takes gate column 8 (l / 16) + jj
+            // of a 32-column group in both operands, so eight steps cover the
+            // group once
+            f32x4_t acc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
 #pragma unroll
-                for (int i = 0; i < kRowsPerThread; ++i) {
+            for (int ch = 0; ch < kMaxCh; ++ch) {
+                if (ch >= nch) break;
+                const int j0 = ch * kUC, j = j0 + u;
+                float* dAb = dAc + (ch & 1) * kLR * sC;
+#pragma unroll
+                for (int i = 0; i < kLRows; ++i) {
                     const int m = tid / 32 + 8 * i;
-                    float da[5], dcl, dcr;
-                    cell_grad(x, i, da, dcl, dcr);
+                    const float gi = x.g[i][ch][0], gl = x.g[i][ch][1], gr = x.g[i][ch][2], go = x.g[i][ch][3];
+                    const float gu = x.g[i][ch][4];
+                    const float tau = tanhf_(x.c[i][ch]);
+                    const float dh = x.dh[i][ch], dc = lk.rk[i] >= 0 ? 0.f : x.dc[i][ch];
+                    const float d_o = dh * tau;
+                    const float dct = dc + dh * go * (1.f - tau * tau);
+                    float da[5];
+                    da[0] = dct * gu * gi * (1.f - gi);
+                    da[1] = dct * x.cl[i][ch] * gl * (1.f - gl);
+                    da[2] = dct * x.cr[i][ch] * gr * (1.f - gr);
+                    da[3] = d_o * go * (1.f - go);
+                    da[4] = dct * gi * (1.f - gu * gu);
                     if (lk.p[i] < 0 || j >= H) {
 #pragma unroll
                         for (int q = 0; q < 5; ++q) da[q] = 0.f;
-                    } else if ((j0 / kUC) % a.ncol == col) {
+                    } else if (ch % a.ncol == col) {
 #pragma unroll
                         for (int q = 0; q < 5; ++q) store_through(a.dA, int64_t(lk.p[i]) * a.lda + q * H + j, da[q]);
-                        store_through(a.dc, int64_t(lk.lc[i]) * a.ldc + j, dcl);
-                        store_through(a.dc, int64_t(lk.rc[i]) * a.ldc + j, dcr);
+                        store_through(a.dc, int64_t(lk.lc[i]) * a.ldc + j, dct * gl);
+                        store_through(a.dc, int64_t(lk.rc[i]) * a.ldc + j, dct * gr);
                     }
 #pragma unroll
-                    for (int q = 0; q < 5; ++q) dAc[m * sC + q * kUC + u] = da[q];
+                    for (int q = 0; q < 5; ++q) dAb[m * sC + q * kUC + u] = da[q];
                 }
-                // the chunk after next, loaded while this one is contracted
-                x = xn;
-                if (j0 + 2 * kUC < H) xn = cell_inputs(a, lk, j + 2 * kUC);
+                // the chunk's dA rows are complete; two buffers in turn, so the
+                // next chunk's cells may run while this one is contracted
                 __syncthreads();
-                // D[node m][column c] += sum over the chunk's gate columns
-                for (int ks = wave; ks < 5 * (kUC / 16); ks += kWaves) {
-                    const int q = ks / (kUC / 16), s = ks - q * (kUC / 16);
-                    Frag<float> fa, fb;
-                    fa.load(dAc + (lane & 31) * sC + q * kUC + s * 16 + 8 * (lane >> 5));
-                    fb.load(Us + (lane & 31) * sUs + q * Hp + j0 + s * 16 + 8 * (lane >> 5));
-                    mfma(acc, fa, fb);
+                // the chunk's (gate, column half) pairs, dealt to the waves in turn
+#pragma unroll
+                for (int pi = 0; pi < 10; ++pi) {
+                    if ((ch * 10 + pi) % kWaves != wave) continue;
+                    const int q = pi / 2, b = pi % 2;
+                    const float* ap = dAb + (lane & 15) * sC + q * kUC + 8 * (lane >> 4);
+                    const float* bp = Us + (16 * b + (lane & 15)) * sUs + q * Hp + j0 + 8 * (lane >> 4);
+                    const float4 a0 = *reinterpret_cast<const float4*>(ap), a1 = *reinterpret_cast<const float4*>(ap + 4);
+                    const float4 b0 = *reinterpret_cast<const float4*>(bp), b1 = *reinterpret_cast<const float4*>(bp + 4);
+                    f32x4_t& c4 = acc[b];
+                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, b0.x, c4, 0, 0, 0);
+                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, b0.y, c4, 0, 0, 0);
+                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.z, b0.z, c4, 0, 0, 0);
+                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, b0.w, c4, 0, 0, 0);
+                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, b1.x, c4, 0, 0, 0);
+                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.y, b1.y, c4, 0, 0, 0);
+                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, b1.z, c4, 0, 0, 0);
+                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, b1.w, c4, 0, 0, 0);
                 }
             }
-            spill_acc(acc, red, wave, lane);
+            // element v of acc[b] of lane l: row 4 (l / 16) + v, column 16 b + l % 16
+#pragma unroll
+            for (int b = 0; b < 2; ++b)
+#pragma unroll
+                for (int v = 0; v < 4; ++v)
+                    red[(wave * 32 + 4 * (lane >> 4) + v) * kRed + 16 * b + (lane & 15)] = acc[b][v];
             __syncthreads();
             // [dh_L; dh_R] of the tile's rows to the two children
-            for (int idx = tid; idx < 32 * 32; idx += kThreads) {
+            for (int idx = tid; idx < kLR * 32; idx += kThreads) {
                 const int m = idx / 32, c = idx % 32, n = 32 * col + c;
                 if (m < rows && n < H2) {
                     const int p = pt + m;
@@ -423,7 +511,11 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
                     else store_through(a.dh, int64_t(a.rchild[p]) * a.ldc + (n - H), v);
                 }
             }
-            __syncthreads();   // red is read before the next tile overwrites it
+            __syncthreads();   // red and the dA buffers are read before the next tile overwrites them
+        }
+        if (L > 1 && r0 < level_tiles(L - 1)) {
+            const int pt = a.loff[L - 1] + kLR * r0;
+            lk = lev_links(a, pt, min(kLR, a.loff[L] - pt));
         }
         persist::barrier_arrive(bar);
         persist::barrier_wait(bar);

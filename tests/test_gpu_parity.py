@@ -152,14 +152,17 @@ def _leaves_only_batch():
 
 
 @pytest.mark.parametrize("persist", ["1", "0"])
-@pytest.mark.parametrize("case", ["sst", "chains", "leaves", "odd"])
+@pytest.mark.parametrize("case", ["sst", "chains", "leaves", "odd", "wide"])
 def test_treelstm_persistent_levels(persist, case, monkeypatch):
     """The TreeLSTM step with each direction as one persistent launch (a
     grid barrier between levels, fp32 MFMA contractions) and with the
     level-by-level kernels (JANUS_TREE_PERSIST=0), each against the oracle:
     the SST-sized batch, a one-leaf tree with a 12-leaf chain and a balanced
-    tree, a batch of one-leaf trees only, and odd sizes (E = 37, H = 29:
-    partial unit groups and column tiles)."""
+    tree, a batch of one-leaf trees only, odd sizes (E = 37, H = 29:
+    partial unit groups and column tiles), and H = 184 over 120 trees (six
+    32-unit chunks per row, the last partial, the backward's widest LDS
+    layout, and levels of more 16-row tiles than a column tile has
+    workgroups)."""
     from paper_1812_01329_amd import janus as J
     monkeypatch.setenv("JANUS_TREE_PERSIST", persist)
     if case == "sst":
@@ -168,8 +171,10 @@ def test_treelstm_persistent_levels(persist, case, monkeypatch):
         w = _chain_and_leaf_batch()
     elif case == "leaves":
         w = _leaves_only_batch()
-    else:
+    elif case == "odd":
         w = wl.sst_treelstm(n_trees=9, E=37, H=29, V=77, seed=15)
+    else:
+        w = wl.sst_treelstm(n_trees=120, E=32, H=184, V=90, seed=16)
     print(f"[tree-persist] case={case} persist={persist} N={w.trees.num_nodes}", flush=True)
     J.janus_trace_begin()
     step, g = _run(w)
