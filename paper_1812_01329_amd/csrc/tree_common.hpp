@@ -193,10 +193,13 @@ __device__ __forceinline__ void node_contraction(f32x16_t& acc, float* Ac, float
 // rows of A and columns of B in this tile; the elements past them (and past
 // K) are zeroed when the chunk is written to LDS, after the chunk's loads
 // are all issued.  A thread then issues 8 loads per chunk instead of 32.
-template <bool AK, class FA, class FB>
+// KC is the chunk depth (Ac and Bc hold 32 rows of pitch KC + 4).
+template <bool AK, int KC = kKC, class FA, class FB>
 __device__ __forceinline__ void node_contraction4(f32x16_t& acc, float* Ac, float* Bc, int K, int nA, int nB,
                                                   FA fa4, FB fb4) {
-    constexpr int sK = kKC + 4, PER = 32 * kKC / 4 / kThreads;   // 4 pieces of each operand per thread
+    constexpr int sK = KC + 4, PER = 32 * KC / 4 / kThreads;   // pieces of each operand per thread
+    constexpr int CQ = KC / 4;                                  // 16-byte pieces per row of a chunk
+    static_assert(PER * kThreads * 4 == 32 * KC, "a chunk is whole passes of the workgroup");
     const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
     float4 va[PER], vb[PER];
     auto fetch = [&](int k0) {
@@ -206,7 +209,7 @@ __device__ __forceinline__ void node_contraction4(f32x16_t& acc, float* Ac, floa
             const int kk = idx >> 3, c4 = 4 * (idx & 7);
             vb[i] = (k0 + kk < K && c4 < nB) ? fb4(c4, k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
             if constexpr (AK) {
-                const int r = idx >> 5, k4 = 4 * (idx & 31);
+                const int r = idx / CQ, k4 = 4 * (idx % CQ);
                 va[i] = (k0 + k4 < K && r < nA) ? fa4(r, k0 + k4) : make_float4(0.f, 0.f, 0.f, 0.f);
             } else {
                 va[i] = (k0 + kk < K && c4 < nA) ? fa4(c4, k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
@@ -221,7 +224,7 @@ __device__ __forceinline__ void node_contraction4(f32x16_t& acc, float* Ac, floa
         return v;
     };
     if (K > 0) fetch(0);
-    for (int k0 = 0; k0 < K; k0 += kKC) {
+    for (int k0 = 0; k0 < K; k0 += KC) {
         __syncthreads();   // the previous chunk's reads are done
 #pragma unroll
         for (int i = 0; i < PER; ++i) {
@@ -233,7 +236,7 @@ __device__ __forceinline__ void node_contraction4(f32x16_t& acc, float* Ac, floa
             Bc[(c4 + 2) * sK + kk] = b.z;
             Bc[(c4 + 3) * sK + kk] = b.w;
             if constexpr (AK) {
-                const int r = idx >> 5, k4 = 4 * (idx & 31);
+                const int r = idx / CQ, k4 = 4 * (idx % CQ);
                 *reinterpret_cast<float4*>(Ac + r * sK + k4) = keep(va[i], K - (k0 + k4));
             } else {
                 const float4 v = keep(va[i], nA - c4);
@@ -243,9 +246,9 @@ __device__ __forceinline__ void node_contraction4(f32x16_t& acc, float* Ac, floa
                 Ac[(c4 + 3) * sK + kk] = v.w;
             }
         }
-        if (k0 + kKC < K) fetch(k0 + kKC);
+        if (k0 + KC < K) fetch(k0 + KC);
         __syncthreads();
-        for (int ks = wave; ks < kKC / 16; ks += kWaves) {
+        for (int ks = wave; ks < KC / 16; ks += kWaves) {
             Frag<float> xa, xb;
             xa.load(Ac + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
             xb.load(Bc + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));

@@ -261,70 +261,13 @@ struct BwdArgs {
 };
 
 __host__ __device__ inline int bwd_hp(int H) { return padto(H, kUC); }
+// chunk depth of the backward's 16-byte contractions over nodes
+constexpr int kKCB = kKC;
 __host__ __device__ inline int bwd_lds_floats(int H) {
     const int sUs = 5 * bwd_hp(H) + 4, sC = 5 * kUC + 4;
     const int level = 32 * sUs + 32 * sC;
-    const int tail = 2 * 32 * (kKC + 4);   // the contractions over nodes reuse the front
+    const int tail = 2 * 32 * (kKCB + 4);   // the contractions over nodes reuse the front
     return (level > tail ? level : tail) + kWaves * 32 * kRed;
-}
-
-// The four rows a thread owns in a 32-row tile (rows tid / 32 + 8 i) and
-// their links; with the unit lane tid % 32 of a 32-unit chunk this is the
-// thread's share of the tile's cells.
-constexpr int kRowsPerThread = 32 * kUC / kThreads;   // 4
-struct RowLinks {
-    int p[kRowsPerThread], lc[kRowsPerThread], rc[kRowsPerThread], rk[kRowsPerThread];
-};
-// Inputs of the cell backward of one chunk (unit j of the thread's rows).
-struct CellIn {
-    float g[kRowsPerThread][5], c[kRowsPerThread], cl[kRowsPerThread], cr[kRowsPerThread];
-    float dh[kRowsPerThread], dc[kRowsPerThread];
-};
-
-__device__ __forceinline__ RowLinks row_links(const BwdArgs& a, int pt, int rows) {
-    RowLinks r;
-#pragma unroll
-    for (int i = 0; i < kRowsPerThread; ++i) {
-        const int m = int(threadIdx.x) / 32 + 8 * i;
-        r.p[i] = m < rows ? pt + m : -1;
-        r.lc[i] = r.p[i] >= 0 ? a.lchild[r.p[i]] : -1;
-        r.rc[i] = r.p[i] >= 0 ? a.rchild[r.p[i]] : -1;
-        r.rk[i] = r.p[i] >= 0 ? a.rootk[r.p[i]] : -1;
-    }
-    return r;
-}
-// All loads of a chunk are issued together (one round trip per chunk).
-__device__ __forceinline__ CellIn cell_inputs(const BwdArgs& a, const RowLinks& r, int j) {
-    CellIn x;
-    const int H = a.H;
-#pragma unroll
-    for (int i = 0; i < kRowsPerThread; ++i) {
-        const bool ok = r.p[i] >= 0 && j < H;
-        const int64_t p = ok ? r.p[i] : 0;
-#pragma unroll
-        for (int q = 0; q < 5; ++q) x.g[i][q] = ok ? a.G[p * a.ldg + q * H + j] : 0.f;
-        x.c[i] = ok ? a.C[p * a.ldc + j] : 0.f;
-        x.cl[i] = (ok && r.lc[i] >= 0) ? a.C[int64_t(r.lc[i]) * a.ldc + j] : 0.f;
-        x.cr[i] = (ok && r.rc[i] >= 0) ? a.C[int64_t(r.rc[i]) * a.ldc + j] : 0.f;
-        x.dh[i] = !ok ? 0.f : r.rk[i] >= 0 ? a.dh_root[int64_t(r.rk[i]) * H + j] : a.dh[p * a.ldc + j];
-        x.dc[i] = (!ok || r.rk[i] >= 0) ? 0.f : a.dc[p * a.ldc + j];
-    }
-    return x;
-}
-// Cell backward of row i: dA of the five gates (0 for an absent cell), and
-// the children's dc.
-__device__ __forceinline__ void cell_grad(const CellIn& x, int i, float (&da)[5], float& dcl, float& dcr) {
-    const float gi = x.g[i][0], gl = x.g[i][1], gr = x.g[i][2], go = x.g[i][3], gu = x.g[i][4];
-    const float tau = tanhf_(x.c[i]);
-    const float d_o = x.dh[i] * tau;
-    const float dct = x.dc[i] + x.dh[i] * go * (1.f - tau * tau);
-    da[0] = dct * gu * gi * (1.f - gi);
-    da[1] = dct * x.cl[i] * gl * (1.f - gl);
-    da[2] = dct * x.cr[i] * gr * (1.f - gr);
-    da[3] = d_o * go * (1.f - go);
-    da[4] = dct * gi * (1.f - gu * gu);
-    dcl = dct * gl;
-    dcr = dct * gr;
 }
 
 // The internal levels run in 16-row tiles: thread rows tid / 32 + 8 i
@@ -439,10 +382,11 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
             // of a 32-column group in both operands, so eight steps cover the
             // group once
             f32x4_t acc[2] = {f32x4_t{0.f, 0.f, 0.f, 0.f}, f32x4_t{0.f, 0.f, 0.f, 0.f}};
-#pragma unroll
-            for (int ch = 0; ch < kMaxCh; ++ch) {
-                if (ch >= nch) break;
-                const int j0 = ch * kUC, j = j0 + u;
+            // the cells of chunk ch into dA buffer ch % 2 (zero past H and
+            // for absent rows); the chunk's column tile also stores dA and
+            // the children's dc
+            auto cells = [&](int ch) {
+                const int j = ch * kUC + u;
                 float* dAb = dAc + (ch & 1) * kLR * sC;
 #pragma unroll
                 for (int i = 0; i < kLRows; ++i) {
@@ -471,28 +415,42 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
 #pragma unroll
                     for (int q = 0; q < 5; ++q) dAb[m * sC + q * kUC + u] = da[q];
                 }
-                // the chunk's dA rows are complete; two buffers in turn, so the
-                // next chunk's cells may run while this one is contracted
-                __syncthreads();
-                // the chunk's (gate, column half) pairs, dealt to the waves in turn
+            };
+            // the chunk's gates dealt to the waves in turn; per gate both
+            // 16-column blocks, two independent accumulator chains
+            auto contract = [&](int ch) {
+                const int j0 = ch * kUC;
+                const float* dAb = dAc + (ch & 1) * kLR * sC;
 #pragma unroll
-                for (int pi = 0; pi < 10; ++pi) {
-                    if ((ch * 10 + pi) % kWaves != wave) continue;
-                    const int q = pi / 2, b = pi % 2;
+                for (int q = 0; q < 5; ++q) {
+                    if ((ch * 5 + q) % kWaves != wave) continue;
                     const float* ap = dAb + (lane & 15) * sC + q * kUC + 8 * (lane >> 4);
-                    const float* bp = Us + (16 * b + (lane & 15)) * sUs + q * Hp + j0 + 8 * (lane >> 4);
+                    const float* bp = Us + (lane & 15) * sUs + q * Hp + j0 + 8 * (lane >> 4);
                     const float4 a0 = *reinterpret_cast<const float4*>(ap), a1 = *reinterpret_cast<const float4*>(ap + 4);
                     const float4 b0 = *reinterpret_cast<const float4*>(bp), b1 = *reinterpret_cast<const float4*>(bp + 4);
-                    f32x4_t& c4 = acc[b];
-                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.x, b0.x, c4, 0, 0, 0);
-                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.y, b0.y, c4, 0, 0, 0);
-                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.z, b0.z, c4, 0, 0, 0);
-                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a0.w, b0.w, c4, 0, 0, 0);
-                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.x, b1.x, c4, 0, 0, 0);
-                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.y, b1.y, c4, 0, 0, 0);
-                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.z, b1.z, c4, 0, 0, 0);
-                    c4 = __builtin_amdgcn_mfma_f32_16x16x4f32(a1.w, b1.w, c4, 0, 0, 0);
+                    const float4 c0 = *reinterpret_cast<const float4*>(bp + 16 * sUs);
+                    const float4 c1 = *reinterpret_cast<const float4*>(bp + 16 * sUs + 4);
+                    const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
+                    const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
+                    const float cv[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
+#pragma unroll
+                    for (int jj = 0; jj < 8; ++jj) {
+                        acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[jj], bv[jj], acc[0], 0, 0, 0);
+                        acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[jj], cv[jj], acc[1], 0, 0, 0);
+                    }
                 }
+            };
+            // software pipeline over the chunks: the cells of chunk ch + 1 go
+            // to the other buffer while chunk ch is contracted; one barrier
+            // per chunk orders both buffers
+            cells(0);
+            __syncthreads();
+#pragma unroll
+            for (int ch = 0; ch < kMaxCh; ++ch) {
+                if (ch >= nch) break;
+                contract(ch);
+                if (ch + 1 < kMaxCh && ch + 1 < nch) cells(ch + 1);
+                __syncthreads();
             }
             // element v of acc[b] of lane l: row 4 (l / 16) + v, column 16 b + l % 16
 #pragma unroll
@@ -520,21 +478,33 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
         persist::barrier_arrive(bar);
         persist::barrier_wait(bar);
     }
-    // the leaves: dA only (no children), tiles dealt to all workgroups
+    // the leaves: dA only (no children, so the forget gates' entries are
+    // 0); 16-row tiles dealt to all workgroups, each tile's inputs in one
+    // round trip after its links
     {
-        const int ntile = (a.M0 + 31) / 32;
+        const int ntile = (a.M0 + kLR - 1) / kLR;
         for (int t = int(blockIdx.x); t < ntile; t += int(gridDim.x)) {
-            const int rows = min(32, a.M0 - 32 * t);
-            const RowLinks lk = row_links(a, 32 * t, rows);
-            for (int j0 = 0; j0 < H; j0 += kUC) {
-                const CellIn x = cell_inputs(a, lk, j0 + u);
+            const LevLinks ll = lev_links(a, kLR * t, min(kLR, a.M0 - kLR * t));
+            LevIn x;
+            lev_inputs(a, ll, nch, x);
 #pragma unroll
-                for (int i = 0; i < kRowsPerThread; ++i) {
-                    if (lk.p[i] < 0 || j0 + u >= H) continue;
-                    float da[5], dcl, dcr;
-                    cell_grad(x, i, da, dcl, dcr);
+            for (int ch = 0; ch < kMaxCh; ++ch) {
+                if (ch >= nch) break;
+                const int j = ch * kUC + u;
 #pragma unroll
-                    for (int q = 0; q < 5; ++q) store_through(a.dA, int64_t(lk.p[i]) * a.lda + q * H + j0 + u, da[q]);
+                for (int i = 0; i < kLRows; ++i) {
+                    if (ll.p[i] < 0 || j >= H) continue;
+                    const float gi = x.g[i][ch][0], go = x.g[i][ch][3], gu = x.g[i][ch][4];
+                    const float tau = tanhf_(x.c[i][ch]);
+                    const float dh = x.dh[i][ch], dc = ll.rk[i] >= 0 ? 0.f : x.dc[i][ch];
+                    const float d_o = dh * tau;
+                    const float dct = dc + dh * go * (1.f - tau * tau);
+                    float* row = a.dA + int64_t(ll.p[i]) * a.lda + j;
+                    store_through(row, 0, dct * gu * gi * (1.f - gi));
+                    store_through(row, H, 0.f);
+                    store_through(row, 2 * H, 0.f);
+                    store_through(row, 3 * H, d_o * go * (1.f - go));
+                    store_through(row, 4 * H, dct * gi * (1.f - gu * gu));
                 }
             }
         }
@@ -545,7 +515,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
     // contractions over nodes, dealt to the workgroups in turn
     {
         float* Ac = sm;
-        float* Bc = sm + 32 * (kKC + 4);
+        float* Bc = sm + 32 * (kKCB + 4);   // the scalar contraction's pitch kKC + 4 fits below
         const int ng = (G5 + 31) / 32, nh2 = (H2 + 31) / 32, ne = (E + 31) / 32, nl = (a.M0 + 31) / 32;
         const int n_dU = ng * nh2, n_dW = ng * ne, n_dx = nl * ne, n_db = ng;
         const int total = n_dU + n_dW + n_dx + n_db;
@@ -606,15 +576,15 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
             const bool vec = E % 4 == 0 && aligned16(a.emb) && aligned16(a.W);
             if (kind == 0) {
                 // dU[32 ti + r][32 tj + c] = sum over internal nodes of dA[p][.] [h_L; h_R][p][.]
-                node_contraction4<false>(acc, Ac, Bc, Nint, min(32, G5 - 32 * ti), min(32, H2 - 32 * tj),
+                node_contraction4<false, kKCB>(acc, Ac, Bc, Nint, min(32, G5 - 32 * ti), min(32, H2 - 32 * tj),
                     [&](int r4, int k) { return ld4(a.dA + int64_t(a.M0 + k) * a.lda + 32 * ti + r4); },
                     [&](int c4, int k) { return ld4(a.HLR + int64_t(k) * a.ldl + 32 * tj + c4); });
             } else if (kind == 1 && vec) {
-                node_contraction4<false>(acc, Ac, Bc, a.M0, min(32, G5 - 32 * ti), min(32, E - 32 * tj),
+                node_contraction4<false, kKCB>(acc, Ac, Bc, a.M0, min(32, G5 - 32 * ti), min(32, E - 32 * tj),
                     [&](int r4, int k) { return ld4(a.dA + int64_t(k) * a.lda + 32 * ti + r4); },
                     [&](int c4, int k) { return ld4(a.emb + int64_t(a.lword[k]) * E + 32 * tj + c4); });
             } else if (kind == 2 && vec) {
-                node_contraction4<true>(acc, Ac, Bc, G5, min(32, a.M0 - 32 * ti), min(32, E - 32 * tj),
+                node_contraction4<true, kKCB>(acc, Ac, Bc, G5, min(32, a.M0 - 32 * ti), min(32, E - 32 * tj),
                     [&](int r, int k4) { return ld4(a.dA + int64_t(32 * ti + r) * a.lda + k4); },
                     [&](int c4, int k) { return ld4(a.W + int64_t(k) * E + 32 * tj + c4); });
             } else if (kind == 1) {
