@@ -104,7 +104,10 @@ janus_status upload_pieces(const UploadPiece* pieces, int n, hipStream_t stream)
     bool ordered = true;
     for (int i = 0; i < n; ++i) {
         char* d = static_cast<char*>(pieces[i].dst);
-        if (d < base + span) ordered = false;   // overlaps or precedes the previous piece
+        // overlaps or precedes the previous piece, or leaves more than
+        // alignment padding between them (the image writes the gaps, with
+        // zeros, so they must hold nothing)
+        if (d < base + span || size_t(d - (base + span)) > kUploadMaxGap) ordered = false;
         if (ordered) span = size_t(d - base) + pieces[i].bytes;
     }
     if (!ordered || span > (size_t(16) << 20)) {

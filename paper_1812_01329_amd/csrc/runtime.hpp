@@ -75,8 +75,11 @@ janus_status upload(void* dst_dev, const void* src_host, size_t bytes, hipStream
 
 // Several host arrays for device buffers that lie one after another in one
 // region (carved in order, with padding between them): one copy of a host
-// image of the whole span instead of one copy per array.  Pieces out of
-// order, or a span past the staging capacity, are copied one by one.
+// image of the whole span instead of one copy per array; the padding is
+// written with zeros.  Pieces out of order, further apart than
+// kUploadMaxGap bytes, or spanning more than the staging capacity are
+// copied one by one.
+constexpr size_t kUploadMaxGap = size_t(64) << 10;
 struct UploadPiece {
     void* dst;
     const void* src;
