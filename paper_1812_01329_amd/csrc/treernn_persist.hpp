@@ -11,10 +11,10 @@
 // "+PARL" in Section 6.3.1).
 //
 // Forward.  Workgroup w keeps the 32 rows w mod NC of W (32 output units,
-// all 2H inputs) in LDS and takes the 32-node row tiles r = w / NC, r + R, ...
+// all 2H inputs) in LDS and takes the 16-node row tiles r = w / NC, r + R, ...
 // of each internal level: it stages the tile's [h_L; h_R] rows, contracts
-// them with fp32 MFMA (K split over the four waves, partial tiles summed in
-// LDS), and applies bias and tanh; h goes to its row (for the backward) and
+// them as fp32 16x16x4 products (K split over the four waves, partial tiles
+// summed in LDS), and applies bias and tanh; h goes to its row (for the backward) and
 // to the parent's [h_L; h_R] row or to h_root.  The leaves only copy their
 // word vectors to their parents' rows; those rows are dealt to all
 // workgroups before the first barrier.
@@ -59,8 +59,11 @@ struct RnnFwdArgs {
     TreeSync* sync;
 };
 
-// Row pitch of the staged operands (K = 2H, padded to the MFMA k-step).
-__host__ __device__ inline int rnn_fwd_pitch(int H) { return pad16(2 * H) + 4; }
+// Node rows per level tile: 16, contracted as 16x16x4 products.
+constexpr int kRT = 16;
+
+// Row pitch of the staged operands (K = 2H, padded to the products' 32-column k groups).
+__host__ __device__ inline int rnn_fwd_pitch(int H) { return padto(2 * H, 32) + 4; }
 __host__ __device__ inline int rnn_fwd_lds_floats(int H) {
     const int slab = 32 * rnn_fwd_pitch(H);
     const int red = kWaves * 32 * kRed;   // the partial tiles reuse the operand slab
@@ -69,9 +72,9 @@ __host__ __device__ inline int rnn_fwd_lds_floats(int H) {
 
 __global__ __launch_bounds__(kThreads) void treernn_fwd_persistent(RnnFwdArgs a) {
     extern __shared__ __align__(16) float sm[];
-    const int H = a.H, K = 2 * a.H, KP = pad16(K), sK = rnn_fwd_pitch(H);
+    const int H = a.H, K = 2 * a.H, KP = padto(K, 32), sK = rnn_fwd_pitch(H);
     float* Wl = sm;                       // [32 units][sK]: row c = W row 32 col + c
-    float* At = Wl + 32 * sK;             // [32 node rows][sK], then the partial tiles
+    float* At = Wl + 32 * sK;             // [32 node rows][sK] (16 used), then the partial tiles
     float* red = At;
     // [32] source row offset of each tile row (-1: none), and where its h
     // goes: >= 0 an offset into HLR, else -1 - (offset into h_root)
@@ -143,9 +146,9 @@ __global__ __launch_bounds__(kThreads) void treernn_fwd_persistent(RnnFwdArgs a)
 
     for (int L = 1; L < a.nlev; ++L) {
         const int p0 = a.loff[L], p1 = a.loff[L + 1];
-        const int ntile = (p1 - p0 + 31) / 32;
+        const int ntile = (p1 - p0 + kRT - 1) / kRT;
         for (int t = r0; t < ntile; t += R) {
-            const int pt = p0 + 32 * t, rows = min(32, p1 - pt);
+            const int pt = p0 + kRT * t, rows = min(kRT, p1 - pt);
             __syncthreads();   // the previous tile's reads of At (the partial tiles), rowsrc and rowdst are done
             // the destinations of the tile's h, loaded while the rows are staged
             int par = -1, rk = -1;
@@ -155,24 +158,17 @@ __global__ __launch_bounds__(kThreads) void treernn_fwd_persistent(RnnFwdArgs a)
             }
             if (tid < 32) rowsrc[tid] = tid < rows ? int64_t(pt + tid - a.M0) * a.ldl : -1;
             __syncthreads();
-            stage_tile_rows(At, sK, a.HLR, rowsrc, K);
+            stage_tile_rows(At, sK, a.HLR, rowsrc, K, KP);
             if (tid < rows)
                 rowdst[tid] = par >= 0 ? int64_t((par >> 1) - a.M0) * a.ldl + (par & 1) * H : -1 - int64_t(rk) * H;
             __syncthreads();
-            // D[node m][unit c] = sum_k rows[m][k] W[32 col + c][k], k-steps of
-            // 16 dealt to the waves in turn
-            f32x16_t acc;
-            zero_acc(acc);
-            for (int ks = wave; ks < KP / 16; ks += kWaves) {
-                Frag<float> fa, fb;
-                fa.load(At + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
-                fb.load(Wl + (lane & 31) * sK + ks * 16 + 8 * (lane >> 5));
-                mfma(acc, fa, fb);
-            }
+            // D[node m][unit c] = sum_k rows[m][k] W[32 col + c][k]
+            f32x4_t acc[2];
+            tile_mfma16(acc, At, sK, Wl, sK, KP, wave, lane);
             __syncthreads();   // every wave is done reading At before the partial tiles overwrite it
-            spill_acc(acc, red, wave, lane);
+            spill_acc16(acc, red, wave, lane);
             __syncthreads();
-            for (int idx = tid; idx < 32 * 32; idx += kThreads) {
+            for (int idx = tid; idx < kRT * 32; idx += kThreads) {
                 const int m = idx / 32, c = idx % 32, n = 32 * col + c;
                 if (m >= rows || n >= H) continue;
                 const int p = pt + m;
@@ -215,7 +211,7 @@ struct RnnBwdArgs {
     TreeSync* sync;
 };
 
-__host__ __device__ inline int rnn_bwd_pitch(int H) { return pad16(H) + 4; }
+__host__ __device__ inline int rnn_bwd_pitch(int H) { return padto(H, 32) + 4; }
 __host__ __device__ inline int rnn_bwd_front(int H) {
     const int level = 2 * 32 * rnn_bwd_pitch(H);
     const int tail = 2 * 32 * (kKC + 4);   // the contractions over nodes reuse the front
@@ -227,9 +223,9 @@ __host__ __device__ inline int rnn_bwd_lds_floats(int H) {
 
 __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a) {
     extern __shared__ __align__(16) float sm[];
-    const int H = a.H, H2 = 2 * a.H, KP = pad16(a.H), sH = rnn_bwd_pitch(a.H);
+    const int H = a.H, H2 = 2 * a.H, KP = padto(a.H, 32), sH = rnn_bwd_pitch(a.H);
     float* Ws = sm;                  // [32 columns of [dh_L; dh_R]][sH]: Ws[c][k] = W[k][32 col + c]
-    float* dAt = Ws + 32 * sH;       // [32 node rows][sH]: da of the tile
+    float* dAt = Ws + 32 * sH;       // [32 node rows][sH] (16 used): da of the tile
     float* red = sm + rnn_bwd_front(H);
     int* links = reinterpret_cast<int*>(red + kWaves * 32 * kRed);   // [32] left, [32] right child of the tile rows
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
@@ -282,9 +278,9 @@ __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a)
 
     for (int L = a.nlev - 1; L >= 1; --L) {
         const int p0 = a.loff[L], p1 = a.loff[L + 1];
-        const int ntile = (p1 - p0 + 31) / 32;
+        const int ntile = (p1 - p0 + kRT - 1) / kRT;
         for (int t = r0; t < ntile; t += R) {
-            const int pt = p0 + 32 * t, rows = min(32, p1 - pt);
+            const int pt = p0 + kRT * t, rows = min(kRT, p1 - pt);
             __syncthreads();   // the previous tile's reads of dAt and red are done
             // da = dh (1 - h^2) of the tile's rows in 16-byte pieces (rows are
             // padded to 32 floats, so a piece never crosses a row), NB pieces
@@ -300,7 +296,7 @@ __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a)
             {
                 constexpr int NB = 10;
                 int m = m_first, q = q_first;
-                while (m < 32) {
+                while (m < kRT) {
                     float4 dv[NB], hv[NB];
                     int mm[NB], qq[NB];
 #pragma unroll
@@ -324,7 +320,7 @@ __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a)
                     // is in flight before the first wait)
 #pragma unroll
                     for (int i = 0; i < NB; ++i) {
-                        if (mm[i] >= 32) continue;
+                        if (mm[i] >= kRT) continue;
                         const int k = 4 * qq[i];
                         // columns past H (the row's padding, never written) count as 0
                         if (k + 1 >= H) dv[i].y = hv[i].y = 0.f;
@@ -351,18 +347,12 @@ __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a)
             }
             __syncthreads();
             // D[node m][column c] = sum_k da[m][k] W[k][32 col + c]
-            f32x16_t acc;
-            zero_acc(acc);
-            for (int ks = wave; ks < KP / 16; ks += kWaves) {
-                Frag<float> fa, fb;
-                fa.load(dAt + (lane & 31) * sH + ks * 16 + 8 * (lane >> 5));
-                fb.load(Ws + (lane & 31) * sH + ks * 16 + 8 * (lane >> 5));
-                mfma(acc, fa, fb);
-            }
-            spill_acc(acc, red, wave, lane);
+            f32x4_t acc[2];
+            tile_mfma16(acc, dAt, sH, Ws, sH, KP, wave, lane);
+            spill_acc16(acc, red, wave, lane);
             __syncthreads();
             // [dh_L; dh_R] of the tile's rows to the two children
-            for (int idx = tid; idx < 32 * 32; idx += kThreads) {
+            for (int idx = tid; idx < kRT * 32; idx += kThreads) {
                 const int m = idx / 32, c = idx % 32, n = 32 * col + c;
                 if (m < rows && n < H2) {
                     const float v = red_sum(red, m, c);
