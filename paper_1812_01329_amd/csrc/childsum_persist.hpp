@@ -215,6 +215,8 @@ struct CsBwdArgs {
     TreeSync* sync;
 };
 
+// the backward's level tiles: 16 node rows, contracted as 16x16x4 products
+constexpr int kCsRT = 16;
 __host__ __device__ inline int cs_bwd_pitch(int H) { return pad16(4 * H) + 4; }
 __host__ __device__ inline int cs_bwd_front(int H) {
     const int slab = 32 * cs_bwd_pitch(H), red = kWaves * 32 * kRed;
@@ -229,7 +231,7 @@ __global__ __launch_bounds__(kThreads) void childsum_bwd_persistent(CsBwdArgs a)
     const int E = a.E, H = a.H, G4 = 4 * a.H;
     const int K4 = pad16(G4), sK = cs_bwd_pitch(H);
     float* Us = sm;                  // [32 columns of H][sK]: Us[c][k] = U[k][32 col + c]
-    float* At = Us + 32 * sK;        // [32 node rows][sK] dG tile, then the partial tiles
+    float* At = Us + 32 * sK;        // [32 node rows][sK] dG tile (16 used), then the partial tiles
     int64_t* rowsrc = reinterpret_cast<int64_t*>(sm + cs_bwd_front(H));
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     TreeBarrier bar;
@@ -273,20 +275,20 @@ __global__ __launch_bounds__(kThreads) void childsum_bwd_persistent(CsBwdArgs a)
     for (int L = a.nlev - 1; L >= 0; --L) {
         const int p0 = a.loff[L], p1 = a.loff[L + 1];
         // dh = dG U of the level's rows
-        const int ntile = (p1 - p0 + 31) / 32;
+        const int ntile = (p1 - p0 + kCsRT - 1) / kCsRT;
         for (int t = r0; t < ntile; t += R) {
-            const int pt = p0 + 32 * t, rows = min(32, p1 - pt);
+            const int pt = p0 + kCsRT * t, rows = min(kCsRT, p1 - pt);
             __syncthreads();   // the previous tile's reads of At (the partial tiles) and rowsrc are done
             if (tid < 32) rowsrc[tid] = tid < rows ? int64_t(pt + tid) * a.ld4 : -1;
             __syncthreads();
             stage_tile_rows(At, sK, a.dG, rowsrc, G4);
             __syncthreads();
-            f32x16_t acc;
-            tile_mfma(acc, At, sK, Us, sK, K4, wave, lane);
+            f32x4_t acc[2];
+            tile_mfma16(acc, At, sK, Us, sK, K4, wave, lane);
             __syncthreads();   // every wave is done reading At before the partial tiles overwrite it
-            spill_acc(acc, At, wave, lane);
+            spill_acc16(acc, At, wave, lane);
             __syncthreads();
-            for (int idx = tid; idx < 32 * 32; idx += kThreads) {
+            for (int idx = tid; idx < kCsRT * 32; idx += kThreads) {
                 const int m = idx / 32, c = idx % 32, n = 32 * col + c;
                 if (m < rows && n < H) store_through(a.dh, int64_t(pt + m) * a.ldh + n, red_sum(At, m, c));
             }

@@ -284,9 +284,8 @@ __device__ __forceinline__ void stage_weight_rows(float* dst, int ld, const floa
 // aligned rows): thread t owns the 16-byte column q = t mod KQ of the rows
 // t / KQ, t / KQ + RP, ... (RP = kThreads / KQ rows per pass), reads those
 // rows' offsets, then issues all its loads before it writes any.
-__device__ __forceinline__ void stage_tile_rows(float* At, int ld, const float* src, const int64_t* rowsrc, int K,
-                                                int KPz = 0) {
-    const int KP = KPz > 0 ? KPz : pad16(K);   // columns [K, KP) are written as zero
+__device__ __forceinline__ void stage_tile_rows(float* At, int ld, const float* src, const int64_t* rowsrc, int K) {
+    const int KP = pad16(K);
     if (K % 4 == 0 && KP / 4 <= kThreads) {
         constexpr int NB = 16;
         const int KQ = KP / 4, RP = kThreads / KQ;
@@ -334,20 +333,27 @@ __device__ __forceinline__ void tile_mfma(f32x16_t& acc, const float* At, int ld
 }
 
 // The same for a 16-row tile, as 16x16x4 products: D[16 x 32] (two 16 x 16
-// blocks, columns 16 b + .) = A[16 x KP] B[32 x KP]^T, KP a multiple of 32.
+// blocks, columns 16 b + .) = A[16 x KP] B[32 x KP]^T, KP a multiple of 16.
 // The 32-column k groups are dealt to the waves in turn; step jj of lane l
 // takes column 32 g + 8 (l / 16) + jj of both operands, so eight steps cover
-// the group once and each lane reads 8 consecutive floats per operand.
+// the group once and each lane reads 8 consecutive floats per operand.  When
+// KP is 16 past a multiple of 32, the last group's upper two lane quarters
+// take zeros (their columns lie past the rows' end).
 __device__ __forceinline__ void tile_mfma16(f32x4_t (&acc)[2], const float* A, int lda, const float* B, int ldb,
                                             int KP, int wave, int lane) {
     acc[0] = acc[1] = f32x4_t{0.f, 0.f, 0.f, 0.f};
-    for (int g = wave; g < KP / 32; g += kWaves) {
-        const float* ap = A + (lane & 15) * lda + 32 * g + 8 * (lane >> 4);
-        const float* bp = B + (lane & 15) * ldb + 32 * g + 8 * (lane >> 4);
-        const float4 a0 = *reinterpret_cast<const float4*>(ap), a1 = *reinterpret_cast<const float4*>(ap + 4);
-        const float4 b0 = *reinterpret_cast<const float4*>(bp), b1 = *reinterpret_cast<const float4*>(bp + 4);
-        const float4 c0 = *reinterpret_cast<const float4*>(bp + 16 * ldb);
-        const float4 c1 = *reinterpret_cast<const float4*>(bp + 16 * ldb + 4);
+    auto group = [&](int g, bool tail) {
+        const int k = 32 * g + 8 * (lane >> 4);
+        const bool ok = !tail || k < KP;
+        const float4 z = make_float4(0.f, 0.f, 0.f, 0.f);
+        const float* ap = A + (lane & 15) * lda + k;
+        const float* bp = B + (lane & 15) * ldb + k;
+        const float4 a0 = ok ? *reinterpret_cast<const float4*>(ap) : z;
+        const float4 a1 = ok ? *reinterpret_cast<const float4*>(ap + 4) : z;
+        const float4 b0 = ok ? *reinterpret_cast<const float4*>(bp) : z;
+        const float4 b1 = ok ? *reinterpret_cast<const float4*>(bp + 4) : z;
+        const float4 c0 = ok ? *reinterpret_cast<const float4*>(bp + 16 * ldb) : z;
+        const float4 c1 = ok ? *reinterpret_cast<const float4*>(bp + 16 * ldb + 4) : z;
         const float av[8] = {a0.x, a0.y, a0.z, a0.w, a1.x, a1.y, a1.z, a1.w};
         const float bv[8] = {b0.x, b0.y, b0.z, b0.w, b1.x, b1.y, b1.z, b1.w};
         const float cv[8] = {c0.x, c0.y, c0.z, c0.w, c1.x, c1.y, c1.z, c1.w};
@@ -356,7 +362,10 @@ __device__ __forceinline__ void tile_mfma16(f32x4_t (&acc)[2], const float* A, i
             acc[0] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[jj], bv[jj], acc[0], 0, 0, 0);
             acc[1] = __builtin_amdgcn_mfma_f32_16x16x4f32(av[jj], cv[jj], acc[1], 0, 0, 0);
         }
-    }
+    };
+    const int nfull = KP / 32;
+    for (int g = wave; g < nfull; g += kWaves) group(g, false);
+    if (KP % 32 != 0 && nfull % kWaves == wave) group(nfull, true);
 }
 // element v of acc[b] of lane l sits at row 4 (l / 16) + v, column 16 b + l % 16
 __device__ __forceinline__ void spill_acc16(const f32x4_t (&acc)[2], float* red, int wave, int lane) {

@@ -62,8 +62,8 @@ struct RnnFwdArgs {
 // Node rows per level tile: 16, contracted as 16x16x4 products.
 constexpr int kRT = 16;
 
-// Row pitch of the staged operands (K = 2H, padded to the products' 32-column k groups).
-__host__ __device__ inline int rnn_fwd_pitch(int H) { return padto(2 * H, 32) + 4; }
+// Row pitch of the staged operands (K = 2H, padded to the MFMA k-step).
+__host__ __device__ inline int rnn_fwd_pitch(int H) { return pad16(2 * H) + 4; }
 __host__ __device__ inline int rnn_fwd_lds_floats(int H) {
     const int slab = 32 * rnn_fwd_pitch(H);
     const int red = kWaves * 32 * kRed;   // the partial tiles reuse the operand slab
@@ -72,7 +72,7 @@ __host__ __device__ inline int rnn_fwd_lds_floats(int H) {
 
 __global__ __launch_bounds__(kThreads) void treernn_fwd_persistent(RnnFwdArgs a) {
     extern __shared__ __align__(16) float sm[];
-    const int H = a.H, K = 2 * a.H, KP = padto(K, 32), sK = rnn_fwd_pitch(H);
+    const int H = a.H, K = 2 * a.H, KP = pad16(K), sK = rnn_fwd_pitch(H);
     float* Wl = sm;                       // [32 units][sK]: row c = W row 32 col + c
     float* At = Wl + 32 * sK;             // [32 node rows][sK] (16 used), then the partial tiles
     float* red = At;
@@ -158,7 +158,7 @@ __global__ __launch_bounds__(kThreads) void treernn_fwd_persistent(RnnFwdArgs a)
             }
             if (tid < 32) rowsrc[tid] = tid < rows ? int64_t(pt + tid - a.M0) * a.ldl : -1;
             __syncthreads();
-            stage_tile_rows(At, sK, a.HLR, rowsrc, K, KP);
+            stage_tile_rows(At, sK, a.HLR, rowsrc, K);
             if (tid < rows)
                 rowdst[tid] = par >= 0 ? int64_t((par >> 1) - a.M0) * a.ldl + (par & 1) * H : -1 - int64_t(rk) * H;
             __syncthreads();
@@ -211,7 +211,7 @@ struct RnnBwdArgs {
     TreeSync* sync;
 };
 
-__host__ __device__ inline int rnn_bwd_pitch(int H) { return padto(H, 32) + 4; }
+__host__ __device__ inline int rnn_bwd_pitch(int H) { return pad16(H) + 4; }
 __host__ __device__ inline int rnn_bwd_front(int H) {
     const int level = 2 * 32 * rnn_bwd_pitch(H);
     const int tail = 2 * 32 * (kKC + 4);   // the contractions over nodes reuse the front
@@ -223,7 +223,7 @@ __host__ __device__ inline int rnn_bwd_lds_floats(int H) {
 
 __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a) {
     extern __shared__ __align__(16) float sm[];
-    const int H = a.H, H2 = 2 * a.H, KP = padto(a.H, 32), sH = rnn_bwd_pitch(a.H);
+    const int H = a.H, H2 = 2 * a.H, KP = pad16(a.H), sH = rnn_bwd_pitch(a.H);
     float* Ws = sm;                  // [32 columns of [dh_L; dh_R]][sH]: Ws[c][k] = W[k][32 col + c]
     float* dAt = Ws + 32 * sH;       // [32 node rows][sH] (16 used): da of the tile
     float* red = sm + rnn_bwd_front(H);
