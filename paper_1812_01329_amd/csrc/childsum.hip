@@ -343,7 +343,6 @@ janus_status cs_bwd_persistent_call(const janus_treelstm_desc& d, const NarySche
     a.dXW = w.dXWp;
     a.ld4 = w.ld4;
     a.dc = w.dcp;
-    a.dh = w.dhp;
     a.dx = w.dxp;
     a.ldx = w.ldx;
     a.demb = demb;

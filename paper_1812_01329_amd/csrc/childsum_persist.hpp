@@ -19,12 +19,13 @@
 // their parents; a barrier.
 //
 // Backward, levels from the top down.  The roots' dG and dc rows are zeroed
-// first.  Per level: dh = dG U of the level's rows as tiles (workgroup w
-// keeps the 32 columns w mod NC of U, K = 4H, in LDS; a row's dG is complete
-// once all its parents' levels are done, and a root's is zero); a barrier;
-// the cell backward, one (node, unit) pair per thread, which writes into the
-// row of each child k dG(k) = [da_iou; da_f(k)] and its dc, and into its own
-// row dXW = [da_iou; sum_k da_f]; a barrier.  Then dW = dXW^T X,
+// first.  Per level, one barrier: dh = dG U of the level's rows as 16-node
+// tiles (workgroup w keeps the 32 columns w mod NC of U, K = 4H, in LDS; a
+// row's dG is complete once all its parents' levels are done, and a root's
+// is zero), and in the same workgroup the cell backward of the tile's
+// (node, unit) pairs, dh taken from LDS, which writes into the row of each
+// child k dG(k) = [da_iou; da_f(k)] and its dc, and into its own row
+// dXW = [da_iou; sum_k da_f].  Then dW = dXW^T X,
 // dU = dG^T H, db (column sums of dXW) and dX = dXW W shared by the
 // workgroups; a barrier; the embedding gradient, word by word.
 //
@@ -205,7 +206,6 @@ struct CsBwdArgs {
     float* dXW;                // [N x ld4]
     int64_t ld4;
     float* dc;                 // [N x ldh]
-    float* dh;                 // [N x ldh]
     float* dx;                 // [N x ldx] gradient of the nodes' inputs
     int64_t ldx;
     float* demb;               // [V x E], every row written
@@ -274,10 +274,31 @@ __global__ __launch_bounds__(kThreads) void childsum_bwd_persistent(CsBwdArgs a)
 
     for (int L = a.nlev - 1; L >= 0; --L) {
         const int p0 = a.loff[L], p1 = a.loff[L + 1];
-        // dh = dG U of the level's rows
+        // Per 16-node tile: dh = dG U for the workgroup's 32 units, then the
+        // cell backward of those (node, unit) pairs in the same workgroup
+        // (dh stays in LDS): thread rows tid / 32 + 8 i, unit 32 col + tid % 32.
         const int ntile = (p1 - p0 + kCsRT - 1) / kCsRT;
         for (int t = r0; t < ntile; t += R) {
             const int pt = p0 + kCsRT * t, rows = min(kCsRT, p1 - pt);
+            const int c = tid % 32, j = 32 * col + c;
+            // the cells' own inputs, in flight while the tile is staged and
+            // contracted (indices clamped to a valid node and unit)
+            int rk[2], c0[2], c1[2];
+            float gi[2], go[2], gu[2], cp[2], dcp[2];
+#pragma unroll
+            for (int i = 0; i < 2; ++i) {
+                const int m = tid / 32 + 8 * i;
+                const int p = pt + min(m, rows - 1), jj = min(j, H - 1);
+                rk[i] = a.rootk[p];
+                c0[i] = a.pcoff[p];
+                c1[i] = a.pcoff[p + 1];
+                const float* gt = a.Gt + int64_t(p) * a.ld3 + jj;
+                gi[i] = gt[0];
+                go[i] = gt[H];
+                gu[i] = gt[2 * H];
+                cp[i] = a.C[int64_t(p) * a.ldh + jj];
+                dcp[i] = a.dc[int64_t(p) * a.ldh + jj];
+            }
             __syncthreads();   // the previous tile's reads of At (the partial tiles) and rowsrc are done
             if (tid < 32) rowsrc[tid] = tid < rows ? int64_t(pt + tid) * a.ld4 : -1;
             __syncthreads();
@@ -288,61 +309,49 @@ __global__ __launch_bounds__(kThreads) void childsum_bwd_persistent(CsBwdArgs a)
             __syncthreads();   // every wave is done reading At before the partial tiles overwrite it
             spill_acc16(acc, At, wave, lane);
             __syncthreads();
-            for (int idx = tid; idx < kCsRT * 32; idx += kThreads) {
-                const int m = idx / 32, c = idx % 32, n = 32 * col + c;
-                if (m < rows && n < H) store_through(a.dh, int64_t(pt + m) * a.ldh + n, red_sum(At, m, c));
-            }
-        }
-        persist::barrier_arrive(bar);
-        persist::barrier_wait(bar);
-        // the cell backward: (node, unit) pairs over the whole grid
-        const int64_t total = int64_t(p1 - p0) * H;
-        for (int64_t g = int64_t(blockIdx.x) * kThreads + tid; g < total; g += stride) {
-            const int m = int(g / H), j = int(g - int64_t(m) * H), p = p0 + m;
-            const int rk = a.rootk[p], c0 = a.pcoff[p], c1 = a.pcoff[p + 1];
-            const float dhp = a.dh[int64_t(p) * a.ldh + j];
-            const float dhr = rk >= 0 ? a.dh_root[int64_t(rk) * H + j] : 0.f;
-            const float* gt = a.Gt + int64_t(p) * a.ld3 + j;
-            const float gi = gt[0], go = gt[H], gu = gt[2 * H];
-            const float cp = a.C[int64_t(p) * a.ldh + j], dcp = a.dc[int64_t(p) * a.ldh + j];
-            const float dhv = dhp + dhr;
-            const float tau = tanhf_(cp);
-            const float dct = dcp + dhv * go * (1.f - tau * tau);
-            const float dai = dct * gu * gi * (1.f - gi);
-            const float dao = dhv * tau * go * (1.f - go);
-            const float dau = dct * gi * (1.f - gu * gu);
-            float dafs = 0.f;
-            for (int e0 = c0; e0 < c1; e0 += 4) {
-                int kid[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) kid[i] = e0 + i < c1 ? a.pkids[e0 + i] : -1;
-                float fk[4], ck[4];
+            for (int i = 0; i < 2; ++i) {
+                const int m = tid / 32 + 8 * i, p = pt + m;
+                if (m >= rows || j >= H) continue;
+                const float dhp = red_sum(At, m, c);
+                const float dhr = rk[i] >= 0 ? a.dh_root[int64_t(rk[i]) * H + j] : 0.f;
+                const float dhv = dhp + dhr;
+                const float tau = tanhf_(cp[i]);
+                const float dct = dcp[i] + dhv * go[i] * (1.f - tau * tau);
+                const float dai = dct * gu[i] * gi[i] * (1.f - gi[i]);
+                const float dao = dhv * tau * go[i] * (1.f - go[i]);
+                const float dau = dct * gi[i] * (1.f - gu[i] * gu[i]);
+                float dafs = 0.f;
+                for (int e0 = c0[i]; e0 < c1[i]; e0 += 4) {
+                    int kid[4];
 #pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    fk[i] = ck[i] = 0.f;
-                    if (kid[i] >= 0) {
-                        fk[i] = a.F[int64_t(kid[i]) * a.ldh + j];
-                        ck[i] = a.C[int64_t(kid[i]) * a.ldh + j];
+                    for (int q = 0; q < 4; ++q) kid[q] = e0 + q < c1[i] ? a.pkids[e0 + q] : -1;
+                    float fk[4], ck[4];
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        const int64_t o = int64_t(kid[q] >= 0 ? kid[q] : p) * a.ldh + j;
+                        fk[q] = a.F[o];
+                        ck[q] = a.C[o];
+                    }
+#pragma unroll
+                    for (int q = 0; q < 4; ++q) {
+                        if (kid[q] < 0) continue;
+                        const float daf = dct * ck[q] * fk[q] * (1.f - fk[q]);
+                        dafs += daf;
+                        const int64_t o = int64_t(kid[q]) * a.ld4 + j;
+                        store_through(a.dG, o, dai);
+                        store_through(a.dG, o + H, dao);
+                        store_through(a.dG, o + 2 * H, dau);
+                        store_through(a.dG, o + 3 * H, daf);
+                        store_through(a.dc, int64_t(kid[q]) * a.ldh + j, dct * fk[q]);
                     }
                 }
-#pragma unroll
-                for (int i = 0; i < 4; ++i) {
-                    if (kid[i] < 0) continue;
-                    const float daf = dct * ck[i] * fk[i] * (1.f - fk[i]);
-                    dafs += daf;
-                    const int64_t o = int64_t(kid[i]) * a.ld4 + j;
-                    store_through(a.dG, o, dai);
-                    store_through(a.dG, o + H, dao);
-                    store_through(a.dG, o + 2 * H, dau);
-                    store_through(a.dG, o + 3 * H, daf);
-                    store_through(a.dc, int64_t(kid[i]) * a.ldh + j, dct * fk[i]);
-                }
+                const int64_t o = int64_t(p) * a.ld4 + j;
+                store_through(a.dXW, o, dai);
+                store_through(a.dXW, o + H, dao);
+                store_through(a.dXW, o + 2 * H, dau);
+                store_through(a.dXW, o + 3 * H, dafs);
             }
-            const int64_t o = int64_t(p) * a.ld4 + j;
-            store_through(a.dXW, o, dai);
-            store_through(a.dXW, o + H, dao);
-            store_through(a.dXW, o + 2 * H, dau);
-            store_through(a.dXW, o + 3 * H, dafs);
         }
         persist::barrier_arrive(bar);
         persist::barrier_wait(bar);
