@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void childsum_fwd_persistent(CsFwdArgs a)
     int64_t* rowsrc = reinterpret_cast<int64_t*>(sm + cs_fwd_lds_floats(E, H) - 64);
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     TreeBarrier bar;
-    persist::barrier_init(bar, a.sync);
+    tree_census_arrive(bar, a.sync);
     const int col = int(blockIdx.x) % a.ncol, r0 = int(blockIdx.x) / a.ncol;
     const int R = int(gridDim.x) / a.ncol;
     stage_weight_rows(Wl, sE, a.W, G4, E, col);
@@ -118,6 +118,7 @@ __global__ __launch_bounds__(kThreads) void childsum_fwd_persistent(CsFwdArgs a)
         const int ntile = (a.N + 31) / 32;
         for (int t = r0; t < ntile; t += R) tile(32 * t, min(32, a.N - 32 * t), a.emb, E, Wl, sE, a.b, a.XW);
     }
+    tree_census_wait(bar);
     persist::barrier_arrive(bar);
     persist::barrier_wait(bar);
 
@@ -235,7 +236,7 @@ __global__ __launch_bounds__(kThreads) void childsum_bwd_persistent(CsBwdArgs a)
     int64_t* rowsrc = reinterpret_cast<int64_t*>(sm + cs_bwd_front(H));
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     TreeBarrier bar;
-    persist::barrier_init(bar, a.sync);
+    tree_census_arrive(bar, a.sync);
     const int col = int(blockIdx.x) % a.ncol, r0 = int(blockIdx.x) / a.ncol;
     const int R = int(gridDim.x) / a.ncol;
     const int64_t stride = int64_t(gridDim.x) * kThreads;
@@ -269,6 +270,7 @@ __global__ __launch_bounds__(kThreads) void childsum_bwd_persistent(CsBwdArgs a)
         for (int q = 0; q < 4; ++q) store_through(a.dG, int64_t(p) * a.ld4 + q * H + j, 0.f);
         store_through(a.dc, int64_t(p) * a.ldh + j, 0.f);
     }
+    tree_census_wait(bar);
     persist::barrier_arrive(bar);
     persist::barrier_wait(bar);
 

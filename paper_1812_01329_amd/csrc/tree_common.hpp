@@ -40,6 +40,40 @@ constexpr size_t kTreeSyncCounters = offsetof(TreeSync, count);   // byte offset
 
 using TreeBarrier = persist::BarrierT<TreeSync>;
 
+// The census of the workgroups on each XCD (which the grid barrier's waits
+// need), in two halves so that a kernel stages its weight slices while the
+// other workgroups arrive: tree_census_arrive counts this workgroup on its
+// XCD and in the total (thread 0, without waiting for the replies);
+// tree_census_wait waits until every workgroup has counted itself, then
+// lane q < 16 of wave 0 reads XCD q's count, all in one round trip.  The
+// fields the level barrier uses (x in thread 0, xcount in lanes 0-15) are
+// then set as the one-call census sets them.
+__device__ __forceinline__ void tree_census_arrive(TreeBarrier& b, TreeSync* s) {
+    b.s = s;
+    b.nb = gridDim.x;
+    b.phase = 0;
+    b.x = 0;
+    b.xsize = 1;
+    b.nx = 1;
+    b.xidx = 0;
+    b.xfirst = 0;
+    b.xcount = 0;
+    if (threadIdx.x == 0) {
+        b.x = persist::xcc_id();
+        __hip_atomic_fetch_add(&s->census[b.x][0], 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+        __hip_atomic_fetch_add(&s->count, 1u, __ATOMIC_RELEASE, __HIP_MEMORY_SCOPE_AGENT);
+    }
+}
+__device__ __forceinline__ void tree_census_wait(TreeBarrier& b) {
+    if (threadIdx.x < 64) {
+        if (threadIdx.x == 0) persist::spin_until(b.s, &b.s->count, b.nb);
+        __builtin_amdgcn_fence(__ATOMIC_ACQUIRE, "agent");
+        if (threadIdx.x < 16)
+            b.xcount = __hip_atomic_load(&b.s->census[threadIdx.x][0], __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+    }
+    __syncthreads();
+}
+
 // A store other workgroups read later in the launch: device-scope, so it is
 // written through the L2 of this XCD to memory (the L2s of the XCDs are not
 // coherent with each other), and counted like any store by the wait at the

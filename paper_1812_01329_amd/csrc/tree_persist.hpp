@@ -124,12 +124,13 @@ __global__ __launch_bounds__(kThreads) void treelstm_fwd_persistent(FwdArgs a) {
     int64_t* rowsrc = reinterpret_cast<int64_t*>(red + kWaves * 32 * kRed);   // [32] source row offset, -1 = none
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     TreeBarrier bar;
-    persist::barrier_init(bar, a.sync);
+    tree_census_arrive(bar, a.sync);
     const int g = int(blockIdx.x) % a.ngroups, r0 = int(blockIdx.x) / a.ngroups;
     const int R = int(gridDim.x) / a.ngroups;
 
     stage_fwd_slice(Wl, sE, a.W, E, KE, H, g);
     stage_fwd_slice(Ul, sU, a.U, 2 * H, KU, H, g);
+    tree_census_wait(bar);
     // threads below 32 * 6 update one cell each: row cm of the tile, unit cj
     const int cm = tid / kUG, cu = tid % kUG, cj = kUG * g + cu;
     const bool cell_thread = tid < 32 * kUG && cj < H;
@@ -332,7 +333,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
     float* red = sm + front;                // [waves][32][kRed]
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     TreeBarrier bar;
-    persist::barrier_init(bar, a.sync);
+    tree_census_arrive(bar, a.sync);
     const int col = int(blockIdx.x) % a.ncol, r0 = int(blockIdx.x) / a.ncol;
     const int R = int(gridDim.x) / a.ncol;
     // U[q H + j][32 col + c] -> Us[c][q Hp + j]: 32 consecutive columns of a
@@ -358,6 +359,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
                   },
                   [&](int idx, float v) { Us[(idx % 32) * sUs + idx / 32] = v; });
     }
+    tree_census_wait(bar);
     const int u = tid % 32;   // this thread's unit lane within a chunk
 
     const int nch = (H + kUC - 1) / kUC;

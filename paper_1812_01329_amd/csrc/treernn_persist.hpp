@@ -82,7 +82,7 @@ __global__ __launch_bounds__(kThreads) void treernn_fwd_persistent(RnnFwdArgs a)
     int64_t* rowdst = rowsrc + 32;
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     TreeBarrier bar;
-    persist::barrier_init(bar, a.sync);
+    tree_census_arrive(bar, a.sync);
     const int col = int(blockIdx.x) % a.ncol, r0 = int(blockIdx.x) / a.ncol;
     const int R = int(gridDim.x) / a.ncol;
 
@@ -139,6 +139,7 @@ __global__ __launch_bounds__(kThreads) void treernn_fwd_persistent(RnnFwdArgs a)
                   },
                   [&](int idx, float v) { Wl[(idx / KP) * sK + idx % KP] = v; });
     }
+    tree_census_wait(bar);
     if (a.nlev > 1) {
         persist::barrier_arrive(bar);
         persist::barrier_wait(bar);
@@ -230,7 +231,7 @@ __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a)
     int* links = reinterpret_cast<int*>(red + kWaves * 32 * kRed);   // [32] left, [32] right child of the tile rows
     const int tid = threadIdx.x, lane = tid & 63, wave = __builtin_amdgcn_readfirstlane(tid >> 6);
     TreeBarrier bar;
-    persist::barrier_init(bar, a.sync);
+    tree_census_arrive(bar, a.sync);
     const int col = int(blockIdx.x) % a.ncol, r0 = int(blockIdx.x) / a.ncol;
     const int R = int(gridDim.x) / a.ncol;
     // W[k][32 col + c] -> Ws[c][k]: 32 consecutive columns of a row of W are
@@ -266,6 +267,7 @@ __global__ __launch_bounds__(kThreads) void treernn_bwd_persistent(RnnBwdArgs a)
             store_through(a.dh, int64_t(a.rootpos[k]) * a.ldh + j, a.dh_root[q]);
         }
     }
+    tree_census_wait(bar);
     persist::barrier_arrive(bar);
     persist::barrier_wait(bar);
 
