@@ -87,6 +87,22 @@ def test_childsum_many_nodes():
     _run_and_check(w)
 
 
+def _with_star(w, k):
+    """The batch of w with a tree of one root over k leaves put first."""
+    t = w.trees
+    n = k + 1
+    off = np.asarray([0, k] + [k] * k, np.int32)          # node 0 is the root, nodes 1..k its leaves
+    rng = np.random.default_rng(k)
+    off2 = np.concatenate([off, t.child_offsets[1:] + k]).astype(np.int32)
+    kids = np.concatenate([np.arange(1, n, dtype=np.int32), t.children + n]).astype(np.int32)
+    word = np.concatenate([rng.integers(0, w.V, n), t.word]).astype(np.int32)
+    root = np.concatenate([[0], t.root + n]).astype(np.int32)
+    trees = wl.NaryTreeBatch(off2, kids, word, root)
+    labels = np.arange(trees.num_trees, dtype=np.int32) % w.C
+    return wl.ChildSumWorkload(w.name + "-star", w.E_dim, w.H, w.V, w.C, trees, labels, w.emb, w.W, w.U, w.b,
+                               w.Ws, w.bs)
+
+
 def _cs_batch(case):
     if case == "sst":
         return wl.sst_childsum()
@@ -96,18 +112,21 @@ def _cs_batch(case):
         return wl.sst_childsum(n_trees=5, E=24, H=32, V=50, seed=83, sizes=[1, 1, 1, 1, 1])
     if case == "odd":      # E = 37, H = 29: partial column tiles, scalar staging
         return wl.sst_childsum(n_trees=7, E=37, H=29, V=61, seed=85)
+    if case == "bigstar":  # a root over 600 leaves beside ordinary trees: a node with 600 children
+        return _with_star(wl.sst_childsum(n_trees=6, E=24, H=32, V=50, seed=87), 600)
     # H = 156: the widest the persistent backward takes (two 32 x 4H slabs in LDS)
     return wl.sst_childsum(n_trees=9, E=300, H=156, V=300, seed=86)
 
 
 @pytest.mark.parametrize("persist", ["1", "0"])
-@pytest.mark.parametrize("case", ["sst", "chains", "singles", "odd", "wide"])
+@pytest.mark.parametrize("case", ["sst", "chains", "singles", "odd", "bigstar", "wide"])
 def test_childsum_persistent_levels(persist, case, monkeypatch):
     """The Child-Sum step with each direction as one persistent launch (device
     barriers between the levels' cells and contractions, fp32 MFMA tiles) and
     with the level-by-level kernels (JANUS_TREE_PERSIST=0), each against the
-    oracle: the SST-sized batch, chains, one-node trees, odd sizes, and the
-    widest H the persistent backward takes."""
+    oracle: the SST-sized batch, chains, one-node trees, odd sizes, a root
+    over 600 leaves beside ordinary trees (one level holds a node with 600
+    children), and the widest H the persistent backward takes."""
     monkeypatch.setenv("JANUS_TREE_PERSIST", persist)
     w = _cs_batch(case)
     print(f"[childsum-persist] case={case} persist={persist} N={w.trees.num_nodes}", flush=True)
