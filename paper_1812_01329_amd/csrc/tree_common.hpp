@@ -292,6 +292,80 @@ __device__ __forceinline__ void node_contraction4(f32x16_t& acc, float* Ac, floa
 }
 
 
+// A 64 x 64 tile of the same sum, for operands in 16-byte pieces (the
+// conventions of node_contraction4; nA and nB count the valid rows of A and
+// columns of B, up to 64).  Chunks of KC k pass through LDS (A and B chunks
+// [64][KC + 4]) with the next chunk loaded into registers meanwhile.  Wave w
+// contracts the whole chunk for the 32 x 32 quadrant at rows 32 (w / 2) and
+// columns 32 (w % 2) of the tile, so acc needs no sum over the waves, and a
+// chunk's MFMA work (about as long as a load round trip) hides the next
+// chunk's loads.  Against four 32 x 32 tiles, the operands are read from
+// memory half as often.
+template <bool AK, int KC, class FA, class FB>
+__device__ __forceinline__ void node_contraction64(f32x16_t& acc, float* Ac, float* Bc, int K, int nA, int nB,
+                                                   FA fa4, FB fb4) {
+    constexpr int sK = KC + 4, PER = 64 * KC / 4 / kThreads;   // pieces of each operand per thread and chunk
+    constexpr int CQ = KC / 4;                                  // 16-byte pieces per row of a chunk
+    static_assert(PER * kThreads * 4 == 64 * KC, "a chunk is whole passes of the workgroup");
+    const int tid = threadIdx.x, lane = tid & 63, wave = tid >> 6;
+    float4 va[PER], vb[PER];
+    auto fetch = [&](int k0) {
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * kThreads;
+            const int kk = idx >> 4, c4 = 4 * (idx & 15);
+            vb[i] = (k0 + kk < K && c4 < nB) ? fb4(c4, k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
+            if constexpr (AK) {
+                const int r = idx / CQ, k4 = 4 * (idx % CQ);
+                va[i] = (k0 + k4 < K && r < nA) ? fa4(r, k0 + k4) : make_float4(0.f, 0.f, 0.f, 0.f);
+            } else {
+                va[i] = (k0 + kk < K && c4 < nA) ? fa4(c4, k0 + kk) : make_float4(0.f, 0.f, 0.f, 0.f);
+            }
+        }
+    };
+    auto keep = [](float4 v, int n) {
+        if (n < 4) v.w = 0.f;
+        if (n < 3) v.z = 0.f;
+        if (n < 2) v.y = 0.f;
+        return v;
+    };
+    const float* ar = Ac + (32 * (wave >> 1) + (lane & 31)) * sK + 8 * (lane >> 5);
+    const float* br = Bc + (32 * (wave & 1) + (lane & 31)) * sK + 8 * (lane >> 5);
+    if (K > 0) fetch(0);
+    for (int k0 = 0; k0 < K; k0 += KC) {
+        __syncthreads();   // the previous chunk's reads are done
+#pragma unroll
+        for (int i = 0; i < PER; ++i) {
+            const int idx = tid + i * kThreads;
+            const int kk = idx >> 4, c4 = 4 * (idx & 15);
+            const float4 b = keep(vb[i], nB - c4);
+            Bc[(c4 + 0) * sK + kk] = b.x;
+            Bc[(c4 + 1) * sK + kk] = b.y;
+            Bc[(c4 + 2) * sK + kk] = b.z;
+            Bc[(c4 + 3) * sK + kk] = b.w;
+            if constexpr (AK) {
+                const int r = idx / CQ, k4 = 4 * (idx % CQ);
+                *reinterpret_cast<float4*>(Ac + r * sK + k4) = keep(va[i], K - (k0 + k4));
+            } else {
+                const float4 v = keep(va[i], nA - c4);
+                Ac[(c4 + 0) * sK + kk] = v.x;
+                Ac[(c4 + 1) * sK + kk] = v.y;
+                Ac[(c4 + 2) * sK + kk] = v.z;
+                Ac[(c4 + 3) * sK + kk] = v.w;
+            }
+        }
+        if (k0 + KC < K) fetch(k0 + KC);
+        __syncthreads();
+        const int nks = (K - k0 < KC ? K - k0 + 15 : KC) / 16;   // k-steps of 16 holding data
+        for (int ks = 0; ks < nks; ++ks) {
+            Frag<float> xa, xb;
+            xa.load(ar + ks * 16);
+            xb.load(br + ks * 16);
+            mfma(acc, xa, xb);
+        }
+    }
+}
+
 // Stage 32 weight rows 32 col + c (c < 32) of a [rows x K] matrix into LDS
 // rows of pitch ld, zero past K and past the last row.
 __device__ __forceinline__ void stage_weight_rows(float* dst, int ld, const float* src, int nrows, int K, int col) {

@@ -267,7 +267,7 @@ constexpr int kKCB = kKC;
 __host__ __device__ inline int bwd_lds_floats(int H) {
     const int sUs = 5 * bwd_hp(H) + 4, sC = 5 * kUC + 4;
     const int level = 32 * sUs + 32 * sC;
-    const int tail = 2 * 32 * (kKCB + 4);   // the contractions over nodes reuse the front
+    const int tail = 2 * 64 * (kKCB + 4);   // the contractions over nodes (64 x 64 tiles) reuse the front
     return (level > tail ? level : tail) + kWaves * 32 * kRed;
 }
 
@@ -514,12 +514,17 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
     persist::barrier_arrive(bar);
     persist::barrier_wait(bar);
 
-    // contractions over nodes, dealt to the workgroups in turn
+    // contractions over nodes, dealt to the workgroups in turn: 64 x 64
+    // tiles where every operand can be read in 16-byte pieces (always for dU,
+    // whose rows are padded to 32 floats), else 32 x 32
     {
+        const bool vec = E % 4 == 0 && aligned16(a.emb) && aligned16(a.W);
+        const int T = vec ? 64 : 32;      // tile edge of the dW and dx items
         float* Ac = sm;
-        float* Bc = sm + 32 * (kKCB + 4);   // the scalar contraction's pitch kKC + 4 fits below
-        const int ng = (G5 + 31) / 32, nh2 = (H2 + 31) / 32, ne = (E + 31) / 32, nl = (a.M0 + 31) / 32;
-        const int n_dU = ng * nh2, n_dW = ng * ne, n_dx = nl * ne, n_db = ng;
+        float* Bc = sm + 64 * (kKCB + 4);   // the scalar contraction's pitch kKC + 4 fits below
+        const int ne = (E + T - 1) / T, nl = (a.M0 + T - 1) / T;
+        const int n_dU = ((G5 + 63) / 64) * ((H2 + 63) / 64), n_dW = ((G5 + T - 1) / T) * ne, n_dx = nl * ne;
+        const int n_db = (G5 + 31) / 32, nh2 = (H2 + 63) / 64;
         const int total = n_dU + n_dW + n_dx + n_db;
         const int Nint = a.N - a.M0;
         for (int it = int(blockIdx.x); it < total; it += int(gridDim.x)) {
@@ -531,7 +536,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
                 const int c4 = 4 * (tid % 8), rg = tid / 8, n = 32 * i + c4;
                 constexpr int RG = kThreads / 8;
                 float4 s4 = make_float4(0.f, 0.f, 0.f, 0.f);
-                const bool vec = a.lda % 4 == 0;
+                const bool vecb = a.lda % 4 == 0;
                 for (int p0 = rg; p0 < a.N; p0 += RG * 16) {
                     float4 v[16];
 #pragma unroll
@@ -540,7 +545,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
                         v[q] = make_float4(0.f, 0.f, 0.f, 0.f);
                         if (p < a.N) {
                             const float* row = a.dA + int64_t(p) * a.lda + n;
-                            if (vec && n + 3 < G5) v[q] = ld4(row);
+                            if (vecb && n + 3 < G5) v[q] = ld4(row);
                             else {
                                 v[q].x = n < G5 ? row[0] : 0.f;
                                 v[q].y = n + 1 < G5 ? row[1] : 0.f;
@@ -573,23 +578,42 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
             if (it < n_dU) { kind = 0; ti = it / nh2; tj = it % nh2; }
             else if (it < n_dU + n_dW) { kind = 1; ti = (it - n_dU) / ne; tj = (it - n_dU) % ne; }
             else { kind = 2; ti = (it - n_dU - n_dW) / ne; tj = (it - n_dU - n_dW) % ne; }
-            // rows of dA and [h_L; h_R] are padded to 32 floats: 16-byte
-            // pieces always; rows of emb and W when E % 4 == 0 and both are 16-byte aligned
-            const bool vec = E % 4 == 0 && aligned16(a.emb) && aligned16(a.W);
-            if (kind == 0) {
-                // dU[32 ti + r][32 tj + c] = sum over internal nodes of dA[p][.] [h_L; h_R][p][.]
-                node_contraction4<false, kKCB>(acc, Ac, Bc, Nint, min(32, G5 - 32 * ti), min(32, H2 - 32 * tj),
-                    [&](int r4, int k) { return ld4(a.dA + int64_t(a.M0 + k) * a.lda + 32 * ti + r4); },
-                    [&](int c4, int k) { return ld4(a.HLR + int64_t(k) * a.ldl + 32 * tj + c4); });
-            } else if (kind == 1 && vec) {
-                node_contraction4<false, kKCB>(acc, Ac, Bc, a.M0, min(32, G5 - 32 * ti), min(32, E - 32 * tj),
-                    [&](int r4, int k) { return ld4(a.dA + int64_t(k) * a.lda + 32 * ti + r4); },
-                    [&](int c4, int k) { return ld4(a.emb + int64_t(a.lword[k]) * E + 32 * tj + c4); });
-            } else if (kind == 2 && vec) {
-                node_contraction4<true, kKCB>(acc, Ac, Bc, G5, min(32, a.M0 - 32 * ti), min(32, E - 32 * tj),
-                    [&](int r, int k4) { return ld4(a.dA + int64_t(32 * ti + r) * a.lda + k4); },
-                    [&](int c4, int k) { return ld4(a.W + int64_t(k) * E + 32 * tj + c4); });
-            } else if (kind == 1) {
+            if (vec || kind == 0) {
+                // rows of dA and [h_L; h_R] are padded to 32 floats, and rows of
+                // emb and W are 16-byte aligned where vec holds: 16-byte pieces
+                const int m0 = 64 * ti, n0 = 64 * tj;
+                if (kind == 0) {
+                    // dU[m][n] = sum over internal nodes of dA[p][m] [h_L; h_R][p][n]
+                    node_contraction64<false, kKCB>(acc, Ac, Bc, Nint, min(64, G5 - m0), min(64, H2 - n0),
+                        [&](int r4, int k) { return ld4(a.dA + int64_t(a.M0 + k) * a.lda + m0 + r4); },
+                        [&](int c4, int k) { return ld4(a.HLR + int64_t(k) * a.ldl + n0 + c4); });
+                } else if (kind == 1) {
+                    // dW = sum over leaves of dA[p][.] x_p[.]
+                    node_contraction64<false, kKCB>(acc, Ac, Bc, a.M0, min(64, G5 - m0), min(64, E - n0),
+                        [&](int r4, int k) { return ld4(a.dA + int64_t(k) * a.lda + m0 + r4); },
+                        [&](int c4, int k) { return ld4(a.emb + int64_t(a.lword[k]) * E + n0 + c4); });
+                } else {
+                    // dx_leaf[p][.] = sum over gate columns of dA[p][k] W[k][.]
+                    node_contraction64<true, kKCB>(acc, Ac, Bc, G5, min(64, a.M0 - m0), min(64, E - n0),
+                        [&](int r, int k4) { return ld4(a.dA + int64_t(m0 + r) * a.lda + k4); },
+                        [&](int c4, int k) { return ld4(a.W + int64_t(k) * E + n0 + c4); });
+                }
+                // each wave holds the quadrant at rows 32 (wave / 2), columns 32 (wave % 2)
+                const int qm = m0 + 32 * (wave >> 1), qn = n0 + 32 * (wave & 1) + acc_col(lane);
+#pragma unroll
+                for (int v = 0; v < 16; ++v) {
+                    const int m = qm + acc_row(v, lane);
+                    if (kind == 0) {
+                        if (m < G5 && qn < H2) a.dU[int64_t(m) * H2 + qn] = acc[v];
+                    } else if (kind == 1) {
+                        if (m < G5 && qn < E) a.dW[int64_t(m) * E + qn] = acc[v];
+                    } else {
+                        if (m < a.M0 && qn < E) store_through(a.dxl, int64_t(m) * a.ldx + qn, acc[v]);
+                    }
+                }
+                continue;
+            }
+            if (kind == 1) {
                 // dW = sum over leaves of dA[p][.] x_p[.]
                 node_contraction<false>(acc, Ac, Bc, a.M0,
                     [&](int r, int k) {
@@ -617,10 +641,7 @@ __global__ __launch_bounds__(kThreads) void treelstm_bwd_persistent(BwdArgs a) {
             for (int idx = tid; idx < 32 * 32; idx += kThreads) {
                 const int r = idx / 32, c = idx % 32;
                 const float v = red_sum(red, r, c);
-                if (kind == 0) {
-                    const int m = 32 * ti + r, n = 32 * tj + c;
-                    if (m < G5 && n < H2) a.dU[int64_t(m) * H2 + n] = v;
-                } else if (kind == 1) {
+                if (kind == 1) {
                     const int m = 32 * ti + r, n = 32 * tj + c;
                     if (m < G5 && n < E) a.dW[int64_t(m) * E + n] = v;
                 } else {
