@@ -214,6 +214,45 @@ __device__ __forceinline__ void group_barrier(Sync* s, unsigned* cnt, unsigned& 
     __syncthreads();
 }
 
+// The same barrier for a group whose members all run on one XCD, whose
+// partial sums therefore go through that XCD's L2: each member publishes the
+// phase it reached in a flag word of its own (word 8 m + 4 of the group's
+// 64-word line, member m) with an ordinary store once its partial sums are
+// acknowledged, and lane q < members of wave 0 polls member q's flag with
+// loads that skip the L1, as the partial sums are read.  A barrier is then an
+// L2 round trip, not an atomic performed in memory and polls of it.  The
+// flags start at zero with the counters of every launch.
+__device__ __forceinline__ void group_barrier_l2(Sync* s, unsigned* line, unsigned& phase, unsigned members,
+                                                 int me) {
+    ++phase;
+    __atomic_signal_fence(__ATOMIC_SEQ_CST);
+    __builtin_amdgcn_s_waitcnt(0);
+    __syncthreads();
+    if (threadIdx.x < 64) {
+        const __amdgpu_buffer_rsrc_t rs = __builtin_amdgcn_make_buffer_rsrc(line, (short)0, int(64 * sizeof(unsigned)),
+                                                                            0x00020000);
+        const unsigned q = threadIdx.x;
+        if (q == 0) {
+            __builtin_amdgcn_s_waitcnt(0);
+            __builtin_amdgcn_raw_buffer_store_b32(phase, rs, int(4 * (8 * me + 4)), 0, 0);   // written back
+        }
+        bool done = q >= members;
+        int spins = 0;
+        while (true) {
+            if (!done) done = __builtin_amdgcn_raw_buffer_load_b32(rs, int(4 * (8 * q + 4)), 0, 16) >= phase;
+            if (__all(done)) break;
+            if ((++spins & 63) == 0 &&
+                __hip_atomic_load(&s->error, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT) != 0u)
+                break;
+            if (spins > kSpinLimit) {
+                if (q == 0) __hip_atomic_store(&s->error, 1u, __ATOMIC_RELAXED, __HIP_MEMORY_SCOPE_AGENT);
+                break;
+            }
+        }
+    }
+    __syncthreads();
+}
+
 // Place of a workgroup in the unit groups of NS members, from its census
 // rank p = xfirst + xidx: member s = p mod NS of group v = p / NS.  The
 // members hold consecutive ranks, so they run on one XCD (`local`) unless
@@ -639,7 +678,8 @@ __global__ __launch_bounds__(kThreads) void lstm_fwd_persistent(FwdArgs a) {
                     }
                 }
             }
-            group_barrier(a.sync, gcnt, gphase, unsigned(NS));
+            if (plocal) group_barrier_l2(a.sync, gcnt, gphase, unsigned(NS), s);
+            else group_barrier(a.sync, gcnt, gphase, unsigned(NS));
             // this workgroup's own tile, then the members' sums in member order
             f32x16_t own = accs[0];
 #pragma unroll
@@ -985,7 +1025,8 @@ __global__ __launch_bounds__(kThreads) void lstm_bwd_persistent(BwdArgs a) {
                         else store16<kStoreThrough>(rp, o, pv);
                     }
             }
-            group_barrier(a.sync, gcnt, gphase, unsigned(NS));
+            if (plocal) group_barrier_l2(a.sync, gcnt, gphase, unsigned(NS), s);
+            else group_barrier(a.sync, gcnt, gphase, unsigned(NS));
         }
 
         uint32_t dgl[8] = {0u, 0u, 0u, 0u, 0u, 0u, 0u, 0u};   // this step's dG, zero without a cell
